@@ -1,0 +1,220 @@
+/*
+ * bsp.h -- per-use backward-state checks of emulated FP8 rounding on MI355X (gfx950).
+ *
+ * A "use" is a gradient computation that reads a rounded tensor; the backward-state
+ * policy chooses, per use, whether it reads the original (U), the rounding the forward
+ * used (R) or a new rounding from the same law (N) (paper Sec. 1; Sec. 3.1; App. B).
+ * The reference gradient is the gradient of the forward as it actually ran, with
+ * gradients passed through every rounding unchanged (Sec. 1; App. B.2, Eq. app-ref).
+ * Each call below runs an operator's backward for every requested policy over K Monte
+ * Carlo roundings with the forward held fixed, and returns the reference gradient and
+ * each policy's mean gradient, its bias against the reference and its standard error
+ * over trials (App. C.4; App. D.4).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every pointer is DEVICE memory owned by the caller, row-major and contiguous,
+ *    unless its comment says "host". The library keeps no pointer after a call
+ *    returns and allocates no device memory: scratch comes from the caller's workspace
+ *    `ws` of `ws_bytes` bytes (256-byte aligned), sized by the matching
+ *    *_workspace_size() query with the same shape arguments.
+ *  - Every call enqueues its kernels on `stream` (a hipStream_t; NULL = the null
+ *    stream) and returns without waiting. Results are valid after the stream syncs.
+ *  - The return code reports only what the host can check: argument, shape, dtype,
+ *    workspace and launch errors. On a non-OK return nothing has been enqueued.
+ *    Conditions found on the device go to the caller's `bs_diag` (device memory),
+ *    which every call that takes one overwrites completely.
+ *  - Results are deterministic: the same inputs and seed give the same bits.
+ *  - The random word of element e of a rounding is Philox4x32-10 (Salmon et al.,
+ *    SC'11) keyed by the 64-bit seed, counter (e >> 2 as 64 bits, trial, use),
+ *    output word e & 3. The forward's own rounding of store `store_id` uses trial 0
+ *    and use id store_id*256; new roundings use trials 1..K and use ids
+ *    store_id*256 + j, j >= 1, as each call states.
+ *  - FP8 store: amax = max|x| over the whole tensor; s = fl32(amax / FMAX) (s = 1 when
+ *    amax = 0); y = fl32(x / s); |y| > FMAX is clamped and counted; then round to
+ *    nearest even, or stochastic rounding with P(up) = floor(frac * 2^32) / 2^32 where
+ *    frac is y's position between its two neighbouring FP8 values (Sec. 2.1, App. D.2).
+ *    Codes are OCP E4M3 (FMAX 448) or E5M2 (FMAX 57344); -0 is code 0x80.
+ *  - Policy estimates are written to bs_est arrays laid out [n_pol][numel] in the
+ *    order the policies are given. Any of mean/bias/se may be NULL (not written).
+ */
+#ifndef BSP_H
+#define BSP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BS_OK = 0,
+  BS_EINVAL = 1,        /* a NULL required pointer, negative size, bad enum or option */
+  BS_ESHAPE = 2,        /* sizes the kernels do not support (stated per call) */
+  BS_EDTYPE = 3,        /* dtype not supported by this call */
+  BS_EUNSUPPORTED = 4,  /* a valid request this build does not implement */
+  BS_EWORKSPACE = 5,    /* ws is NULL, misaligned or smaller than *_workspace_size() */
+  BS_EHIP = 6           /* a HIP runtime error while enqueueing */
+} bs_status;
+
+typedef enum { BS_F32 = 0, BS_BF16 = 1 } bs_dtype;
+typedef enum { BS_E4M3 = 0, BS_E5M2 = 1 } bs_fp8;
+typedef enum { BS_RNE = 0, BS_SR = 1 } bs_round;
+typedef enum { BS_READ_U = 0, BS_READ_R = 1, BS_READ_N = 2 } bs_read;
+
+/* Device-side diagnostics of one store. nonfinite != 0: the tensor held a NaN or an
+ * infinity and no codes were produced (outputs are then unspecified). n_saturated:
+ * entries with |x/s| > FMAX, clamped to +-FMAX (App. D.2 counts such entries). */
+typedef struct {
+  uint32_t nonfinite;
+  uint32_t n_saturated;
+  float amax;
+  float scale;
+} bs_diag;
+
+/* Per-policy estimate arrays, each [n_pol][numel] fp32, NULL = not wanted.
+ * mean = (1/K) sum_k g_k; bias = mean - g_ref; se = sample standard deviation of g_k
+ * over the K trials divided by sqrt(K) (App. C.4), 0 for a policy that draws nothing. */
+typedef struct {
+  float* mean;
+  float* bias;
+  float* se;
+} bs_est;
+
+const char* bs_status_string(bs_status s);
+/* Library version (major*10000 + minor*100 + patch). */
+int bs_version(void);
+
+/* ------------------------------------------------------------------------------------
+ * bs_qround -- the FP8 store of one tensor (Sec. 2.1; App. D.2, "at the TE output scale").
+ *   x        [n] fp32 or bf16 (xt).
+ *   fmt/mode format and rounding rule; seed/trial/use key the Philox words (SR only).
+ *   scale_in NULL: s = amax/FMAX from x; else s = *scale_in (device fp32, > 0).
+ *   codes    [n] uint8 out.  scale_out [1] fp32 out (the s used).
+ *   diag     [1] out.
+ * n may be 0 (diag then reports amax 0, scale 1). No workspace.
+ * ---------------------------------------------------------------------------------- */
+bs_status bs_qround(const void* x, bs_dtype xt, int64_t n, bs_fp8 fmt, bs_round mode,
+                    uint64_t seed, uint32_t trial, uint32_t use, const float* scale_in,
+                    uint8_t* codes, float* scale_out, bs_diag* diag, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * bs_rmsnorm_linear_fwd_bwd -- RMSNorm feeding a Linear through an FP8 store of the
+ * normalized output, and the two uses of that store (Sec. 3.1, Eq. norm-uses; App. D.4,
+ * Table "Store policies"; App. E.4 for the norm-input reading R).
+ *
+ * Forward: z = x * r_t with r_t = 1/sqrt(mean_j x_tj^2 + eps); u = gain * z, computed in
+ * fp32 in a fixed order (sum of squares in 64 lane-strided partials, partial l taking
+ * j = l, l+64, ... ascending, combined pairwise with offsets 32, 16, ..., 1; every step
+ * rounded to fp32, no fused multiply-add); (C_u, s) = FP8 store of u (trial 0, use
+ * store_id*256); Y = deq(C_u) W.
+ * Backward: du = dY W^T; reference dW = deq(C_u)^T dY, dgain = sum_t z du, dX = the
+ * RMSNorm backward with the unrounded z. Per policy: the gain use reads z (U),
+ * deq(C_u)/gain (R) or deq(C_f)/gain (N); the weight use reads u (U), deq(C_u) (R) or
+ * deq(C_f') (N); the norm-input use reads z (U) or deq(C_u)/gain (R). A new rounding is
+ * stochastic rounding of y = fl32(u/s) at the forward's scale; its use id is
+ * store_id*256+1 at the gain use and store_id*256+2 at the weight use, or +1 for both
+ * when fresh_shared != 0.
+ *
+ *   X [T,d] dt; gain [d] fp32; W [d,n] dt; dY [T,n] dt (dt fp32 or bf16).
+ *   T >= 0; d and n multiples of 8 with 8 <= d <= 8192, 8 <= n; K in [1, 4096].
+ *   pol (host) [n_pol], n_pol in [1, 16].
+ *   Y [T,n] fp32 (nullable); u_codes [T,d] uint8; u_scale [1] fp32;
+ *   dgain_ref [d], dW_ref [d,n], dX_ref [T,d] fp32; estimates dgain [n_pol][d],
+ *   dW [n_pol][d*n], dX [n_pol][T*d]. dW.se must be NULL when a policy reads N at the
+ *   weight use and K > 1 (per-trial contractions are not built: BS_EUNSUPPORTED).
+ * ---------------------------------------------------------------------------------- */
+typedef struct {
+  bs_read gain_use;
+  bs_read weight_use;
+  bs_read norm_input_use;  /* U (default of the paper) or R */
+  int fresh_shared;        /* 1: both N uses read one new rounding */
+} bs_norm_policy;
+
+size_t bs_rmsnorm_linear_workspace_size(int64_t T, int64_t d, int64_t n, int n_pol, int K);
+bs_status bs_rmsnorm_linear_fwd_bwd(const void* X, const float* gain, const void* W, const void* dY,
+                                    bs_dtype dt, int64_t T, int64_t d, int64_t n, float eps,
+                                    bs_fp8 fmt, bs_round fwd_mode, const bs_norm_policy* pol, int n_pol,
+                                    int K, uint64_t seed, uint32_t store_id, float* Y, uint8_t* u_codes,
+                                    float* u_scale, float* dgain_ref, float* dW_ref, float* dX_ref,
+                                    bs_est dgain, bs_est dW, bs_est dX, bs_diag* diag, void* ws,
+                                    size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * bs_attn_bwd_policy -- attention backward whose correction term D reads a stored
+ * copy of the output (Sec. 2.1, Eq. dterm; App. D.2).
+ *
+ * Scores S = c Q K^T (c = softmax_scale; causal: key j <= query i), P = softmax(S),
+ * O = P V. The store is the FP8 store of the fp32 O (mode fwd_mode, trial 0, use
+ * store_id*256). Backward: dV = P^T dO, dP = dO V^T, dS = P * (dP - D), dQ = c dS K,
+ * dK = c dS^T Q. The reference takes D = rowsum(dO * O) with the original O. Policy U
+ * reads O, R the forward's rounding deq(C_O), N a new stochastic rounding at the same
+ * scale (trials 1..K, use store_id*256+1). dV does not depend on the policy.
+ *
+ *   Q, Kt, V, dO [B,H,S,dh] bf16.  dh == 64; S >= 1; B, H >= 1.
+ *   O [B,H,S,dh] fp32: the original output to store; NULL = computed by the library's
+ *   forward (written to O_out if O_out != NULL).
+ *   d_pol (host) [n_pol] in {U, R, N}, n_pol in [1, 8]; K in [1, 4096].
+ *   O_codes [B,H,S,dh] uint8; O_scale [1]; dQ_ref, dK_ref, dV [B,H,S,dh] fp32;
+ *   D_ref [B,H,S] fp32 (nullable); estimates dQ, dK [n_pol][B*H*S*dh]
+ *   (dK.se must be NULL: BS_EUNSUPPORTED otherwise).
+ * ---------------------------------------------------------------------------------- */
+size_t bs_attn_workspace_size(int B, int H, int S, int dh, int n_pol, int K);
+bs_status bs_attn_bwd_policy(const void* Q, const void* Kt, const void* V, const void* dO, int B, int H,
+                             int S, int dh, int causal, float softmax_scale, const float* O, bs_fp8 fmt,
+                             bs_round fwd_mode, const bs_read* d_pol, int n_pol, int K, uint64_t seed,
+                             uint32_t store_id, float* O_out, uint8_t* O_codes, float* O_scale,
+                             float* dQ_ref, float* dK_ref, float* dV, float* D_ref, bs_est dQ, bs_est dK,
+                             bs_diag* diag, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * bs_linear_bwd_policy -- Linear backward whose incoming gradient is stochastically
+ * rounded to FP8 (E5M2 in the HYBRID recipe, App. D.1), read by two uses.
+ *
+ * y = X W. The reference uses the unrounded dY: dX_ref = dY W^T, dW_ref = X^T dY. In
+ * trial k the rounding C_k of dY (per-tensor scale s = amax(dY)/FMAX) is read by
+ * dX_k = deq(C_k) W^T and dW_k = X^T deq(C'_k): shared (sharing 0) means C' = C (use id
+ * store_id*256+1); per use (sharing 1) draws C' separately (use id store_id*256+2).
+ * Coupling: kappa = mean_k <dX_k - dX_ref, A> <dW_k - dW_ref, B> for fixed probes A, B
+ * (the coupling part of the error split of App. C.1; App. C.2's two-stage example).
+ *
+ *   X [M,k] dt, W [k,n] dt, dY [M,n] dt; dt bf16; k and n multiples of 8; M >= 0.
+ *   sharing (host) [n_pol] in {0, 1}, n_pol in [1, 4]; K in [1, 4096].
+ *   dX_ref [M,k], dW_ref [k,n] fp32; estimates dX [n_pol][M*k], dW [n_pol][k*n]
+ *   (se must be NULL: BS_EUNSUPPORTED otherwise).
+ *   probeA [M,k], probeB [k,n] fp32 and coupling [n_pol] fp64: all NULL or all set.
+ *   dY_scale [1] fp32 out.
+ * ---------------------------------------------------------------------------------- */
+size_t bs_linear_bwd_workspace_size(int64_t M, int64_t k, int64_t n, int n_pol, int K);
+bs_status bs_linear_bwd_policy(const void* X, const void* W, const void* dY, bs_dtype dt, int64_t M,
+                               int64_t k, int64_t n, bs_fp8 fmt, const int* sharing, int n_pol, int K,
+                               uint64_t seed, uint32_t store_id, float* dX_ref, float* dW_ref, bs_est dX,
+                               bs_est dW, const float* probeA, const float* probeB, double* coupling,
+                               float* dY_scale, bs_diag* diag, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * bs_policy_bias_estimate -- trial statistics of any use (App. C.4; App. D.4).
+ *   delta [K][m] fp32: per-trial gradient minus the reference, trials in order.
+ *   g_ref [m] (nullable, only for its norm). mean_err [m] out; se [m] out (nullable).
+ *   summary [3] fp64 out: ||mean_err||_2, ||g_ref||_2 (0 if g_ref NULL), and
+ *   R = ||mean_err||^2 / sum_j se_j^2 (NaN when the sum is 0).
+ *   K >= 1, m >= 0. Sums run in a fixed order (deterministic).
+ * ---------------------------------------------------------------------------------- */
+size_t bs_policy_bias_workspace_size(int K, int64_t m);
+bs_status bs_policy_bias_estimate(const float* delta, int K, int64_t m, const float* g_ref, float* mean_err,
+                                  float* se, double* summary, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * bs_gemm_bf16_nt -- the contraction the backward uses for dW/dX/du (building block).
+ *   C[M,N] = alpha * A[M,K] B[N,K]^T (+ C if accumulate), A and B bf16 with K contiguous
+ *   (leading dimensions lda, ldb in elements), C fp32 with leading dimension ldc.
+ *   K, lda, ldb multiples of 8; M, N, K >= 0.
+ * ---------------------------------------------------------------------------------- */
+bs_status bs_gemm_bf16_nt(const void* A, int64_t lda, const void* B, int64_t ldb, float* C, int64_t ldc,
+                          int64_t M, int64_t N, int64_t K, float alpha, int accumulate, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BSP_H */

@@ -1,0 +1,268 @@
+"""Python binding of libbsp.so (the C-ABI in include/bsp.h).
+
+Argument marshalling only: every step of every call runs in the library's HIP kernels.
+Tensors must be CUDA (HIP) tensors; outputs are allocated with torch and the work is
+enqueued on torch's current stream. There is no CPU fallback: if the library is not
+built, importing this module raises.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbsp.so")
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_39813_amd.build`")
+_lib = ctypes.CDLL(LIB_PATH)
+
+F32, BF16 = 0, 1
+E4M3, E5M2 = 0, 1
+RNE, SR = 0, 1
+READ = {"U": 0, "R": 1, "N": 2}
+_FMT = {"e4m3": E4M3, "e5m2": E5M2, E4M3: E4M3, E5M2: E5M2}
+_MODE = {"rne": RNE, "sr": SR, RNE: RNE, SR: SR}
+
+_vp, _i64, _u64, _u32, _int, _f32, _sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_uint32,
+                                         ctypes.c_int, ctypes.c_float, ctypes.c_size_t)
+
+
+class Diag(ctypes.Structure):
+    _fields_ = [("nonfinite", ctypes.c_uint32), ("n_saturated", ctypes.c_uint32), ("amax", ctypes.c_float),
+                ("scale", ctypes.c_float)]
+
+
+class Est(ctypes.Structure):
+    _fields_ = [("mean", _vp), ("bias", _vp), ("se", _vp)]
+
+
+class NormPolicy(ctypes.Structure):
+    _fields_ = [("gain_use", _int), ("weight_use", _int), ("norm_input_use", _int), ("fresh_shared", _int)]
+
+
+def _sig(name, res, args):
+    f = getattr(_lib, name)
+    f.restype = res
+    f.argtypes = args
+    return f
+
+
+_status_string = _sig("bs_status_string", ctypes.c_char_p, [_int])
+bs_version = _sig("bs_version", _int, [])
+_qround = _sig("bs_qround", _int, [_vp, _int, _i64, _int, _int, _u64, _u32, _u32, _vp, _vp, _vp, _vp, _vp])
+_gemm = _sig("bs_gemm_bf16_nt", _int, [_vp, _i64, _vp, _i64, _vp, _i64, _i64, _i64, _i64, _f32, _int, _vp])
+_pb_ws = _sig("bs_policy_bias_workspace_size", _sz, [_int, _i64])
+_pb = _sig("bs_policy_bias_estimate", _int, [_vp, _int, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp])
+_norm_ws = _sig("bs_rmsnorm_linear_workspace_size", _sz, [_i64, _i64, _i64, _int, _int])
+_norm = _sig("bs_rmsnorm_linear_fwd_bwd", _int,
+             [_vp, _vp, _vp, _vp, _int, _i64, _i64, _i64, _f32, _int, _int, ctypes.POINTER(NormPolicy), _int, _int,
+              _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, Est, _vp, _vp, _sz, _vp])
+_attn_ws = _sig("bs_attn_workspace_size", _sz, [_int, _int, _int, _int, _int, _int])
+_attn = _sig("bs_attn_bwd_policy", _int,
+             [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _vp, _int, _int, ctypes.POINTER(_int), _int,
+              _int, _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, _vp, _vp, _sz, _vp])
+_lin_ws = _sig("bs_linear_bwd_workspace_size", _sz, [_i64, _i64, _i64, _int, _int])
+_lin = _sig("bs_linear_bwd_policy", _int,
+            [_vp, _vp, _vp, _int, _i64, _i64, _i64, _int, ctypes.POINTER(_int), _int, _int, _u64, _u32, _vp, _vp,
+             Est, Est, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp])
+
+EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
+            "bs_policy_bias_estimate", "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
+            "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy"]
+
+
+class BspError(RuntimeError):
+    def __init__(self, code, call):
+        super().__init__(f"{call}: {_status_string(code).decode()} (status {code})")
+        self.code = code
+
+
+def _check(code, call):
+    if code != 0:
+        raise BspError(code, call)
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev_check(*ts):
+    for t in ts:
+        if t is not None:
+            if not t.is_cuda:
+                raise ValueError("libbsp works on device tensors only")
+            if not t.is_contiguous():
+                raise ValueError("tensors must be contiguous")
+
+
+def _dt(t):
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"dtype {t.dtype} not supported")
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _workspace(nbytes, device):
+    # 256-byte aligned by torch's caching allocator
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def diag_dict(d):
+    """Decode a device bs_diag (a 16-byte uint8 tensor) after a stream sync."""
+    raw = d.cpu().numpy().tobytes()
+    v = Diag.from_buffer_copy(raw)
+    return {"nonfinite": v.nonfinite, "n_saturated": v.n_saturated, "amax": v.amax, "scale": v.scale}
+
+
+def new_diag(device):
+    return torch.zeros(16, dtype=torch.uint8, device=device)
+
+
+# ----------------------------------------------------------------------------------
+def qround(x, fmt="e4m3", mode="rne", seed=0, trial=0, use=0, scale=None):
+    """FP8 store of x: returns (codes uint8, scale [1] fp32, diag tensor)."""
+    _dev_check(x, scale)
+    codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    s = torch.empty(1, dtype=torch.float32, device=x.device)
+    dg = new_diag(x.device)
+    _check(_qround(_p(x), _dt(x), x.numel(), _FMT[fmt], _MODE[mode], seed, trial, use, _p(scale), _p(codes), _p(s),
+                   _p(dg), _stream()), "bs_qround")
+    return codes, s, dg
+
+
+def gemm_bf16_nt(A, B, alpha=1.0, out=None, accumulate=False):
+    """C = alpha * A B^T for bf16 A [M, K], B [N, K] (K-contiguous), C fp32."""
+    _dev_check(A, B)
+    M, K = A.shape
+    N = B.shape[0]
+    C = out if out is not None else torch.empty(M, N, dtype=torch.float32, device=A.device)
+    _check(_gemm(_p(A), K, _p(B), K, _p(C), N, M, N, K, alpha, int(accumulate), _stream()), "bs_gemm_bf16_nt")
+    return C
+
+
+def policy_bias_estimate(delta, g_ref=None):
+    """Trial statistics of per-trial errors delta [K, m]: (mean_err, se, summary[3])."""
+    _dev_check(delta, g_ref)
+    K, m = delta.shape
+    mean = torch.empty(m, dtype=torch.float32, device=delta.device)
+    se = torch.empty(m, dtype=torch.float32, device=delta.device)
+    summ = torch.empty(3, dtype=torch.float64, device=delta.device)
+    ws = _workspace(_pb_ws(K, m), delta.device)
+    _check(_pb(_p(delta), K, m, _p(g_ref), _p(mean), _p(se), _p(summ), _p(ws), ws.numel(), _stream()),
+           "bs_policy_bias_estimate")
+    return mean, se, summ
+
+
+def _est(n_pol, numel, device, want_se):
+    mean = torch.empty(n_pol, numel, dtype=torch.float32, device=device)
+    bias = torch.empty(n_pol, numel, dtype=torch.float32, device=device)
+    se = torch.empty(n_pol, numel, dtype=torch.float32, device=device) if want_se else None
+    return {"mean": mean, "bias": bias, "se": se}, Est(_p(mean), _p(bias), _p(se))
+
+
+def parse_norm_policy(code):
+    """'G/W' letters, optional suffixes ':R' (norm-input reads R) and ':shared'."""
+    parts = code.split(":")
+    g, w = parts[0].split("/")
+    return NormPolicy(READ[g], READ[w], READ["R"] if "R" in parts[1:] else READ["U"], 1 if "shared" in parts[1:] else 0)
+
+
+def rmsnorm_linear(X, gain, W, dY, *, eps=1e-5, fmt="e4m3", fwd_mode="rne", policies=("U/U", "R/R", "N/N"), K=16,
+                   seed=0, store_id=0, want_y=True, want_se=True, ws=None):
+    """RMSNorm -> FP8 store -> Linear and the per-use policy estimates (bs_rmsnorm_linear_fwd_bwd)."""
+    _dev_check(X, gain, W, dY)
+    T, d = X.shape
+    n = W.shape[1]
+    dev = X.device
+    pol = (NormPolicy * len(policies))(*[parse_norm_policy(p) for p in policies])
+    out = {"u_codes": torch.empty(T, d, dtype=torch.uint8, device=dev),
+           "u_scale": torch.empty(1, dtype=torch.float32, device=dev),
+           "dgain_ref": torch.empty(d, dtype=torch.float32, device=dev),
+           "dW_ref": torch.empty(d, n, dtype=torch.float32, device=dev),
+           "dX_ref": torch.empty(T, d, dtype=torch.float32, device=dev),
+           "Y": torch.empty(T, n, dtype=torch.float32, device=dev) if want_y else None,
+           "diag": new_diag(dev)}
+    weight_n = any(p.split(":")[0].split("/")[1] == "N" for p in policies)
+    eg, cg = _est(len(policies), d, dev, want_se)
+    ew, cw = _est(len(policies), d * n, dev, want_se and not (weight_n and K > 1))
+    ex, cx = _est(len(policies), T * d, dev, want_se)
+    if ws is None:
+        ws = _workspace(_norm_ws(T, d, n, len(policies), K), dev)
+    _check(_norm(_p(X), _p(gain), _p(W), _p(dY), _dt(X), T, d, n, eps, _FMT[fmt], _MODE[fwd_mode], pol, len(policies), K,
+                 seed, store_id, _p(out["Y"]), _p(out["u_codes"]), _p(out["u_scale"]), _p(out["dgain_ref"]),
+                 _p(out["dW_ref"]), _p(out["dX_ref"]), cg, cw, cx, _p(out["diag"]), _p(ws), ws.numel(), _stream()),
+           "bs_rmsnorm_linear_fwd_bwd")
+    out["dgain"], out["dW"], out["dX"] = eg, ew, ex
+    out["policies"] = list(policies)
+    return out
+
+
+def rmsnorm_linear_workspace(T, d, n, n_pol, K, device):
+    return _workspace(_norm_ws(T, d, n, n_pol, K), device)
+
+
+def attn_bwd_policy(Q, Kt, V, dO, *, causal=True, scale=None, O=None, fmt="e4m3", fwd_mode="sr",
+                    policies=("U", "R", "N"), K=32, seed=0, store_id=0, want_o=True, want_se=True, ws=None):
+    """Attention backward with D read from each policy's copy of O (bs_attn_bwd_policy)."""
+    _dev_check(Q, Kt, V, dO, O)
+    B, H, S, dh = Q.shape
+    dev = Q.device
+    c = 1.0 / dh ** 0.5 if scale is None else scale
+    pol = (_int * len(policies))(*[READ[p] for p in policies])
+    shp = (B, H, S, dh)
+    out = {"O": torch.empty(shp, dtype=torch.float32, device=dev) if want_o else None,
+           "O_codes": torch.empty(shp, dtype=torch.uint8, device=dev),
+           "O_scale": torch.empty(1, dtype=torch.float32, device=dev),
+           "dQ_ref": torch.empty(shp, dtype=torch.float32, device=dev),
+           "dK_ref": torch.empty(shp, dtype=torch.float32, device=dev),
+           "dV": torch.empty(shp, dtype=torch.float32, device=dev),
+           "D_ref": torch.empty(B, H, S, dtype=torch.float32, device=dev),
+           "diag": new_diag(dev)}
+    numel = B * H * S * dh
+    eq, cq = _est(len(policies), numel, dev, want_se)
+    ek, ck = _est(len(policies), numel, dev, False)
+    if ws is None:
+        ws = _workspace(_attn_ws(B, H, S, dh, len(policies), K), dev)
+    _check(_attn(_p(Q), _p(Kt), _p(V), _p(dO), B, H, S, dh, int(causal), c, _p(O), _FMT[fmt], _MODE[fwd_mode], pol,
+                 len(policies), K, seed, store_id, _p(out["O"]), _p(out["O_codes"]), _p(out["O_scale"]),
+                 _p(out["dQ_ref"]), _p(out["dK_ref"]), _p(out["dV"]), _p(out["D_ref"]), cq, ck, _p(out["diag"]),
+                 _p(ws), ws.numel(), _stream()), "bs_attn_bwd_policy")
+    out["dQ"], out["dK"] = eq, ek
+    return out
+
+
+def attn_workspace(B, H, S, dh, n_pol, K, device):
+    return _workspace(_attn_ws(B, H, S, dh, n_pol, K), device)
+
+
+def linear_bwd_policy(X, W, dY, *, fmt="e5m2", sharings=("shared", "per_use"), K=16, seed=0, store_id=0,
+                      probeA=None, probeB=None, ws=None):
+    """Linear backward with an FP8-rounded incoming gradient (bs_linear_bwd_policy)."""
+    _dev_check(X, W, dY, probeA, probeB)
+    M, k = X.shape
+    n = W.shape[1]
+    dev = X.device
+    sh = (_int * len(sharings))(*[0 if s == "shared" else 1 for s in sharings])
+    out = {"dX_ref": torch.empty(M, k, dtype=torch.float32, device=dev),
+           "dW_ref": torch.empty(k, n, dtype=torch.float32, device=dev),
+           "dY_scale": torch.empty(1, dtype=torch.float32, device=dev),
+           "coupling": torch.empty(len(sharings), dtype=torch.float64, device=dev) if probeA is not None else None,
+           "diag": new_diag(dev)}
+    ex, cx = _est(len(sharings), M * k, dev, False)
+    ew, cw = _est(len(sharings), k * n, dev, False)
+    if ws is None:
+        ws = _workspace(_lin_ws(M, k, n, len(sharings), K), dev)
+    _check(_lin(_p(X), _p(W), _p(dY), _dt(X), M, k, n, _FMT[fmt], sh, len(sharings), K, seed, store_id,
+                _p(out["dX_ref"]), _p(out["dW_ref"]), cx, cw, _p(probeA), _p(probeB), _p(out["coupling"]),
+                _p(out["dY_scale"]), _p(out["diag"]), _p(ws), ws.numel(), _stream()), "bs_linear_bwd_policy")
+    out["dX"], out["dW"] = ex, ew
+    return out
+
+
+def linear_bwd_workspace(M, k, n, n_pol, K, device):
+    return _workspace(_lin_ws(M, k, n, n_pol, K), device)

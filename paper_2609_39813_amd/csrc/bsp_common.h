@@ -1,0 +1,203 @@
+// Device helpers shared by the gfx950 kernels: Philox4x32-10, the FP8 codec, bf16
+// splitting, wave reductions and the workspace carver. Everything here is written for
+// CDNA4 (64-wide wavefronts); nothing is shared with the CPU oracle.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "../../include/bsp.h"
+
+#define BS_WAVE 64
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16;
+
+namespace bsp {
+
+// ---------------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 32x32->64
+// multiplies and xors, key bumped by the Weyl constants between rounds. The counter is
+// (element >> 2 lo, element >> 2 hi, trial, use); the key is the 64-bit seed.
+// ---------------------------------------------------------------------------------
+struct Philox4 {
+  uint32_t w0, w1, w2, w3;
+};
+
+__device__ __forceinline__ Philox4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                                 uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    c1 = (uint32_t)p1;
+    c3 = (uint32_t)p0;
+    c0 = n0;
+    c2 = n2;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return {c0, c1, c2, c3};
+}
+
+// Words for the 4 consecutive elements of group g = element >> 2.
+__device__ __forceinline__ Philox4 philox_group(uint64_t seed, uint64_t g, uint32_t trial, uint32_t use) {
+  return philox4x32_10((uint32_t)g, (uint32_t)(g >> 32), trial, use, (uint32_t)seed, (uint32_t)(seed >> 32));
+}
+
+__device__ __forceinline__ uint32_t philox_word(const Philox4& p, int q) {
+  return q == 0 ? p.w0 : (q == 1 ? p.w1 : (q == 2 ? p.w2 : p.w3));
+}
+
+// ---------------------------------------------------------------------------------
+// FP8 codec. For a magnitude a <= FMAX the bracketing grid values are lo = mi * step
+// and hi = lo + step, with v = a / step exact (step is a power of two), mi = floor(v)
+// and frac = v - mi exact. The code of magnitude m*step is base + m, where base is
+// (e + bias - 1) << mbits in the normal range (e = exponent of a) and 0 below it; a
+// carry of m into the next binade lands on the right code by construction.
+// ---------------------------------------------------------------------------------
+struct F8 {
+  int mbits;
+  int bias;
+  float fmax;
+};
+
+__host__ __device__ __forceinline__ F8 f8_format(int fmt) {
+  return fmt == BS_E5M2 ? F8{2, 15, 57344.0f} : F8{3, 7, 448.0f};
+}
+
+struct Bracket {
+  uint32_t base;  // code of 0 * step in a's binade
+  uint32_t mi;    // floor(a / step)
+  float frac;     // a / step - mi, in [0, 1)
+  int sh;         // a / step = a * 2^sh
+};
+
+__device__ __forceinline__ Bracket f8_bracket(float a, F8 f) {
+  Bracket b;
+  const float min_normal = ldexpf(1.0f, 1 - f.bias);
+  if (a >= min_normal) {
+    const int e = ilogbf(a);
+    b.sh = f.mbits - e;
+    b.base = (uint32_t)(e + f.bias - 1) << f.mbits;
+  } else {
+    b.sh = f.bias + f.mbits - 1;
+    b.base = 0;
+  }
+  const float v = ldexpf(a, b.sh);
+  const float fl = floorf(v);
+  b.mi = (uint32_t)fl;
+  b.frac = v - fl;
+  return b;
+}
+
+// floor(frac * 2^32): exact when frac has at most 32 fraction bits, truncated below.
+__device__ __forceinline__ uint32_t sr_threshold(float frac) { return (uint32_t)(frac * 4294967296.0f); }
+
+// Round up iff R + F >= 2^32 (so P(up) = F / 2^32).
+__device__ __forceinline__ uint32_t sr_up(uint32_t F, uint32_t R) { return (F != 0u) & (R >= (0u - F)); }
+
+__device__ __forceinline__ uint32_t rne_up(const Bracket& b) {
+  return (b.frac > 0.5f) | ((b.frac == 0.5f) & (b.mi & 1u));
+}
+
+// Step (hi - lo) of a bracket, as a float power of two.
+__device__ __forceinline__ float f8_step(const Bracket& b) { return ldexpf(1.0f, -b.sh); }
+
+// Real value of a finite FP8 code.
+__device__ __forceinline__ float f8_value(uint32_t code, F8 f) {
+  const uint32_t mag = code & 0x7Fu;
+  const int ef = (int)(mag >> f.mbits);
+  const int mf = (int)(mag & ((1u << f.mbits) - 1u));
+  const float v = ef ? ldexpf((float)((1 << f.mbits) + mf), ef - f.bias - f.mbits)
+                     : ldexpf((float)mf, 1 - f.bias - f.mbits);
+  return (code & 0x80u) ? -v : v;
+}
+
+// ---------------------------------------------------------------------------------
+// bf16: exact conversions of values with at most 8 significant bits, and the split of
+// an fp32 value into up to three bf16 terms whose sum is the value (each term rounds the
+// remainder to nearest; three terms carry all 24 bits).
+// ---------------------------------------------------------------------------------
+__device__ __forceinline__ u16 bf16_bits(float x) {
+  __bf16 h = (__bf16)x;
+  return __builtin_bit_cast(u16, h);
+}
+__device__ __forceinline__ float bf16_to_f32(u16 b) { return __uint_as_float((uint32_t)b << 16); }
+
+__device__ __forceinline__ void split3(float x, u16& h0, u16& h1, u16& h2) {
+  h0 = bf16_bits(x);
+  const float r1 = x - bf16_to_f32(h0);
+  h1 = bf16_bits(r1);
+  const float r2 = r1 - bf16_to_f32(h1);
+  h2 = bf16_bits(r2);
+}
+
+template <typename T>
+__device__ __forceinline__ float load_f32(const T* p, int64_t i);
+template <>
+__device__ __forceinline__ float load_f32<float>(const float* p, int64_t i) {
+  return p[i];
+}
+template <>
+__device__ __forceinline__ float load_f32<u16>(const u16* p, int64_t i) {
+  return bf16_to_f32(p[i]);
+}
+
+// ---------------------------------------------------------------------------------
+// Wave and block reductions (wave64).
+// ---------------------------------------------------------------------------------
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_down(v, off, BS_WAVE);
+  return v;  // valid in lane 0
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t o = __shfl_down(v, off, BS_WAVE);
+    v = v > o ? v : o;
+  }
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_down(v, off, BS_WAVE);
+  return v;
+}
+
+}  // namespace bsp
+
+// ---------------------------------------------------------------------------------
+// Host side: workspace carving and launch checking.
+// ---------------------------------------------------------------------------------
+namespace bsp {
+
+struct Carver {
+  char* base;
+  size_t off = 0;
+  size_t cap;
+  explicit Carver(void* p = nullptr, size_t c = 0) : base((char*)p), cap(c) {}
+  template <typename T>
+  T* take(size_t count) {
+    off = (off + 255) & ~(size_t)255;
+    T* p = base ? (T*)(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+  size_t used() const { return (off + 255) & ~(size_t)255; }
+};
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+}  // namespace bsp
+
+#define BS_CHECK_LAUNCH()                                   \
+  do {                                                      \
+    if (hipGetLastError() != hipSuccess) return BS_EHIP;    \
+  } while (0)

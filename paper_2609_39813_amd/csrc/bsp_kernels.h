@@ -1,0 +1,56 @@
+// Internal launchers of the gfx950 kernels (host-callable, enqueue on a stream).
+#pragma once
+#include "bsp_common.h"
+
+namespace bsp {
+
+constexpr int GEMM_MAX_SEG = 8;
+struct GemmArgs {
+  const u16* A[GEMM_MAX_SEG];
+  const u16* B[GEMM_MAX_SEG];
+  int nseg;
+  int M, N, K;
+  int64_t lda, ldb, ldc;
+  float alpha;
+  const float* alpha_dev;  // nullable: alpha is multiplied by *alpha_dev
+  int accumulate;
+  float* C;
+};
+
+// Append the products A_i B_j (i + j <= 2) of nA and nB bf16 terms to g's segments.
+inline bool gemm_add_products(GemmArgs& g, const u16* const* A, int nA, const u16* const* B, int nB) {
+  for (int s = 0; s <= 2; ++s)
+    for (int i = 0; i < nA; ++i) {
+      const int j = s - i;
+      if (j < 0 || j >= nB) continue;
+      if (g.nseg >= GEMM_MAX_SEG) return false;
+      g.A[g.nseg] = A[i];
+      g.B[g.nseg] = B[j];
+      ++g.nseg;
+    }
+  return true;
+}
+
+bs_status launch_gemm(const GemmArgs& g, hipStream_t st);
+
+bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode, uint64_t seed, uint32_t trial,
+                       uint32_t use, const float* scale_in, uint8_t* codes, float* scale_out, bs_diag* diag,
+                       hipStream_t st, bool amax_done);
+bs_status launch_fresh_count(const float* u, int64_t T, int64_t d, int fmt, const float* scale, uint64_t seed,
+                             uint32_t use, int K, u16* counts, const float* w, double* partial, hipStream_t st);
+
+bs_status launch_fill2d(float* p, int64_t rows, int64_t cols, int64_t ld, float v, hipStream_t st);
+bs_status launch_fill_f64(double* p, int64_t n, double v, hipStream_t st);
+bs_status launch_init_diag(bs_diag* diag, hipStream_t st);
+
+// bf16 operand planes. Row-major: out_p[r*ldo + c], c < C (ldo >= C). Transposed:
+// out_p[c*ldo + r], r < R, zero for R <= r < ldo. p = 0..nterms-1 (terms of the
+// split of each fp32 value; bf16 inputs with nterms == 1 are copied).
+bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64_t ldi, bool transpose,
+                        u16* const* out, int nterms, int64_t ldo, float scale, hipStream_t st);
+
+// Trial statistics over per-trial rows (App. C.4, App. D.4).
+bs_status launch_policy_bias(const float* delta, int K, int64_t m, const float* g_ref, float* mean_err, float* se,
+                             double* summary, double* ws, hipStream_t st);
+
+}  // namespace bsp

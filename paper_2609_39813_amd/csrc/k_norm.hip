@@ -1,0 +1,333 @@
+// Normalization store (RMSNorm -> FP8 store -> Linear) kernels: forward in the fixed
+// fp32 order, operand planes for the contractions, the gain use's column reductions,
+// the gain use's per-trial standard error, and the normalization input gradient.
+#include "bsp_kernels.h"
+#include "k_norm.h"
+
+namespace bsp {
+
+// One wave64 per row. Lane l accumulates x_j^2 for j = l, l + 64, ... in ascending j,
+// the 64 partials are combined pairwise with offsets 32, 16, ..., 1, then
+// ms = ss / d, r = 1 / sqrt(ms + eps), z = x r, u = gain z; every operation rounded to
+// fp32 with no contraction. max |u| goes to amax_bits (see amax_kernel).
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(const T* __restrict__ X, const float* __restrict__ gain,
+                                                          int64_t Tn, int64_t d, float eps, float* __restrict__ u,
+                                                          float* __restrict__ rstd, uint32_t* __restrict__ amax_bits) {
+#pragma clang fp contract(off)
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t t = (int64_t)blockIdx.x * 4 + w;
+  uint32_t m = 0;
+  if (t < Tn) {
+    const T* xr = X + t * d;
+    float p = 0.0f;
+    for (int64_t j = lane; j < d; j += 64) {
+      const float x = load_f32(xr, j);
+      const float sq = x * x;
+      p = p + sq;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const float o = __shfl_down(p, off, 64);
+      if (lane < off) p = p + o;
+    }
+    const float ss = __shfl(p, 0, 64);
+    const float ms = __fdiv_rn(ss, (float)d);
+    const float r = 1.0f / sqrtf(ms + eps);  // both correctly rounded (built with -fhip-fp32-correctly-rounded-divide-sqrt)
+    float* ur = u + t * d;
+    for (int64_t j = lane; j < d; j += 64) {
+      const float z = load_f32(xr, j) * r;
+      const float uv = gain[j] * z;
+      ur[j] = uv;
+      const uint32_t b = __float_as_uint(fabsf(uv));
+      m = m > b ? m : b;
+    }
+    if (lane == 0) rstd[t] = r;
+  }
+  m = wave_max_u32(m);
+  __shared__ uint32_t red[4];
+  if (lane == 0) red[w] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t b = red[0];
+    for (int i = 1; i < 4; ++i) b = b > red[i] ? b : red[i];
+    if (b) atomicMax(amax_bits, b);
+  }
+}
+
+// Transposed planes [d][ldo] of per-element operands of the weight-use contractions.
+//   NP_VAL : val(C_u)                                      (1 term, exact)
+//   NP_RESU: u - s * val(C_u)  (= minus the forward's rounding error; 3 terms)
+//   NP_RESN: sign * (n_up - K * [C_u rounded up]) * step   (1 term if K <= 256, else 2)
+template <int MODE>
+__global__ __launch_bounds__(256) void norm_planes_t_kernel(NormPlaneArgs a) {
+  __shared__ u16 tile[3][64][66];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  const float s = *a.scale;
+#pragma unroll 2
+  for (int i = 0; i < 16; ++i) {
+    const int rr = ty + 4 * i;
+    const int64_t t = r0 + rr, j = c0 + tx;
+    u16 o[3] = {0, 0, 0};
+    if (t < a.T && j < a.d) {
+      const int64_t e = t * a.d + j;
+      const uint32_t code = a.codes[e];
+      if (MODE == NP_VAL) {
+        o[0] = bf16_bits(f8_value(code, a.f));
+      } else if (MODE == NP_RESU) {
+        split3(fmaf(-s, f8_value(code, a.f), a.u[e]), o[0], o[1], o[2]);
+      } else {
+        const float y = __fdiv_rn(a.u[e], s);
+        const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
+        const int h = (code & 0x7Fu) != b.base + b.mi;
+        const float v = (float)((int)a.counts[e] - a.K * h) * f8_step(b);
+        split3(signbit(y) ? -v : v, o[0], o[1], o[2]);
+      }
+    }
+    for (int p = 0; p < a.nterms; ++p) tile[p][rr][tx] = o[p];
+  }
+  __syncthreads();
+#pragma unroll 2
+  for (int i = 0; i < 16; ++i) {
+    const int cc = ty + 4 * i;
+    const int64_t j = c0 + cc, t = r0 + tx;
+    if (j < a.d && t < a.ldo)
+      for (int p = 0; p < a.nterms; ++p) a.out[p][j * a.ldo + t] = tile[p][tx][cc];
+  }
+}
+
+// Row-major plane of val(C) (exact bf16), the A operand of the Linear forward.
+__global__ __launch_bounds__(256) void val_rows_kernel(const uint8_t* __restrict__ codes, int64_t n, F8 f,
+                                                       u16* __restrict__ out) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = bf16_bits(f8_value(codes[i], f));
+}
+
+// Gain use, partial column sums over a tile of 64 rows (fp64):
+//   q0: z du                      (reference)
+//   q1: (s val(C_u) - gain z) / gain * du          (R: reads deq(C_u) / gain)
+//   q2: (s mean_k val(C_k) - gain z) / gain * du   (N: reads a new rounding; mean over
+//       the K trials = sign (lo + n_up step / K))
+// z = fl32(x r) is recomputed exactly as in the forward.
+template <typename T>
+__global__ __launch_bounds__(256) void gain_partials_kernel(GainArgs<T> a) {
+#pragma clang fp contract(off)
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t rt = blockIdx.y;
+  if (j >= a.d) return;
+  const double s = *a.scale;
+  const float sf = *a.scale;
+  const double g = a.gain[j];
+  double q0 = 0.0, q1 = 0.0, q2 = 0.0;
+  const int64_t tend = (rt + 1) * 64 < a.T ? (rt + 1) * 64 : a.T;
+  for (int64_t t = rt * 64; t < tend; ++t) {
+    const int64_t e = t * a.d + j;
+    const float z = load_f32(a.X, e) * a.rstd[t];
+    const double du = a.du[e];
+    const double gz = g * (double)z;
+    q0 += (double)z * du;
+    if (a.want_r) q1 += (s * (double)f8_value(a.codes[e], a.f) - gz) / g * du;
+    if (a.counts) {
+      const float y = __fdiv_rn(a.u[e], sf);
+      const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
+      const double step = f8_step(b);
+      double mv = (double)b.mi * step + (double)a.counts[e] * step / a.K;
+      if (signbit(y)) mv = -mv;
+      q2 += (s * mv - gz) / g * du;
+    }
+  }
+  const int64_t nrt = gridDim.y;
+  a.part[(0 * nrt + rt) * a.d + j] = q0;
+  a.part[(1 * nrt + rt) * a.d + j] = q1;
+  a.part[(2 * nrt + rt) * a.d + j] = q2;
+}
+
+__global__ __launch_bounds__(256) void gain_final_kernel(const double* __restrict__ part, int64_t nrt, int64_t d,
+                                                         float* __restrict__ ref, float* __restrict__ bias_r,
+                                                         float* __restrict__ bias_n) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j >= d) return;
+  double q[3] = {0.0, 0.0, 0.0};
+  for (int i = 0; i < 3; ++i)
+    for (int64_t rt = 0; rt < nrt; ++rt) q[i] += part[(i * nrt + rt) * d + j];
+  ref[j] = (float)q[0];
+  if (bias_r) bias_r[j] = (float)q[1];
+  if (bias_n) bias_n[j] = (float)q[2];
+}
+
+// se of the gain use under N: the per-trial gradient is const + (s / gain) S_k with
+// S_k = sum over row tiles of the fresh counter's partials; Welford over k in order.
+__global__ __launch_bounds__(256) void gain_se_kernel(const double* __restrict__ part, int K, int64_t nrt, int64_t d,
+                                                      const float* __restrict__ scale, const float* __restrict__ gain,
+                                                      float* __restrict__ se) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j >= d) return;
+  double mean = 0.0, m2 = 0.0;
+  for (int k = 0; k < K; ++k) {
+    double S = 0.0;
+    for (int64_t rt = 0; rt < nrt; ++rt) S += part[((int64_t)k * nrt + rt) * d + j];
+    const double dlt = S - mean;
+    mean += dlt / (k + 1);
+    m2 += dlt * (S - mean);
+  }
+  const double f = fabs((double)*scale / (double)gain[j]);
+  se[j] = K > 1 ? (float)(f * sqrt(m2 / (K - 1) / K)) : 0.0f;
+}
+
+// Normalization input gradient, one wave64 per row:
+//   dz = gain du; dx = r (dz - zhat (sum_j dz zhat) / d), zhat = z (U) or s val(C_u) / gain (R).
+template <typename T>
+__global__ __launch_bounds__(256) void norm_dx_kernel(DxArgs<T> a) {
+#pragma clang fp contract(off)
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t t = (int64_t)blockIdx.x * 4 + w;
+  if (t >= a.T) return;
+  const float r = a.rstd[t];
+  const double s = a.scale ? (double)*a.scale : 1.0;
+  double dot_u = 0.0, dot_r = 0.0;
+  for (int64_t j = lane; j < a.d; j += 64) {
+    const int64_t e = t * a.d + j;
+    const double z = (double)(load_f32(a.X, e) * r);
+    const double g = a.gain[j];
+    const double dz = g * (double)a.du[e];
+    dot_u += dz * z;
+    if (a.dx_r) dot_r += dz * (s * (double)f8_value(a.codes[e], a.f) / g);
+  }
+  dot_u = wave_sum_f64(dot_u);
+  dot_r = wave_sum_f64(dot_r);
+  dot_u = __shfl(dot_u, 0, 64) / (double)a.d;
+  dot_r = __shfl(dot_r, 0, 64) / (double)a.d;
+  for (int64_t j = lane; j < a.d; j += 64) {
+    const int64_t e = t * a.d + j;
+    const double z = (double)(load_f32(a.X, e) * r);
+    const double g = a.gain[j];
+    const double dz = g * (double)a.du[e];
+    a.dx_ref[e] = (float)((double)r * (dz - z * dot_u));
+    if (a.dx_r) {
+      const double zr = s * (double)f8_value(a.codes[e], a.f) / g;
+      a.dx_r[e] = (float)((double)r * (dz - zr * dot_r));
+    }
+  }
+}
+
+// mean = ref + bias, bias, se (each output nullable; bias / se inputs nullable = 0).
+__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ ref, const float* __restrict__ bias,
+                                                      const float* __restrict__ se, int64_t n, float* __restrict__ mean_out,
+                                                      float* __restrict__ bias_out, float* __restrict__ se_out) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const float b = bias ? bias[i] : 0.0f;
+    if (mean_out) mean_out[i] = bias ? ref[i] + b : ref[i];
+    if (bias_out) bias_out[i] = b;
+    if (se_out) se_out[i] = se ? se[i] : 0.0f;
+  }
+}
+
+// mean = alt, bias = alt - ref (a use whose reading is computed in full).
+__global__ __launch_bounds__(256) void combine_alt_kernel(const float* __restrict__ ref, const float* __restrict__ alt,
+                                                          int64_t n, float* __restrict__ mean_out,
+                                                          float* __restrict__ bias_out, float* __restrict__ se_out) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    if (mean_out) mean_out[i] = alt[i];
+    if (bias_out) bias_out[i] = alt[i] - ref[i];
+    if (se_out) se_out[i] = 0.0f;
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// launchers
+// ------------------------------------------------------------------------------------
+static unsigned grid1d(int64_t n, int64_t cap = 8192) {
+  const int64_t want = (n + 255) / 256;
+  return (unsigned)(want < 1 ? 1 : (want < cap ? want : cap));
+}
+
+bs_status launch_rmsnorm_fwd(const void* X, bs_dtype dt, const float* gain, int64_t T, int64_t d, float eps, float* u,
+                             float* rstd, bs_diag* diag, hipStream_t st) {
+  if (T > 0) {
+    const unsigned blocks = (unsigned)((T + 3) / 4);
+    if (dt == BS_F32)
+      rmsnorm_fwd_kernel<float><<<blocks, 256, 0, st>>>((const float*)X, gain, T, d, eps, u, rstd,
+                                                        (uint32_t*)&diag->amax);
+    else
+      rmsnorm_fwd_kernel<u16><<<blocks, 256, 0, st>>>((const u16*)X, gain, T, d, eps, u, rstd,
+                                                      (uint32_t*)&diag->amax);
+  }
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+bs_status launch_norm_planes(int mode, const NormPlaneArgs& a, hipStream_t st) {
+  if (a.d <= 0 || a.ldo <= 0) return BS_OK;
+  dim3 grid((unsigned)((a.d + 63) / 64), (unsigned)((a.ldo + 63) / 64));
+  if (mode == NP_VAL)
+    norm_planes_t_kernel<NP_VAL><<<grid, 256, 0, st>>>(a);
+  else if (mode == NP_RESU)
+    norm_planes_t_kernel<NP_RESU><<<grid, 256, 0, st>>>(a);
+  else
+    norm_planes_t_kernel<NP_RESN><<<grid, 256, 0, st>>>(a);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+bs_status launch_val_rows(const uint8_t* codes, int64_t n, int fmt, u16* out, hipStream_t st) {
+  if (n > 0) val_rows_kernel<<<grid1d(n), 256, 0, st>>>(codes, n, f8_format(fmt), out);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+template <typename T>
+bs_status launch_gain_t(const GainArgs<T>& a, float* ref, float* bias_r, float* bias_n, hipStream_t st) {
+  if (a.d <= 0) return BS_OK;
+  const int64_t nrt = (a.T + 63) / 64;
+  if (nrt == 0) {
+    if (ref) launch_fill2d(ref, 1, a.d, a.d, 0.0f, st);
+    if (bias_r) launch_fill2d(bias_r, 1, a.d, a.d, 0.0f, st);
+    if (bias_n) launch_fill2d(bias_n, 1, a.d, a.d, 0.0f, st);
+    BS_CHECK_LAUNCH();
+    return BS_OK;
+  }
+  dim3 grid((unsigned)((a.d + 255) / 256), (unsigned)nrt);
+  gain_partials_kernel<T><<<grid, 256, 0, st>>>(a);
+  gain_final_kernel<<<(unsigned)((a.d + 255) / 256), 256, 0, st>>>(a.part, nrt, a.d, ref, bias_r, bias_n);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+template bs_status launch_gain_t<float>(const GainArgs<float>&, float*, float*, float*, hipStream_t);
+template bs_status launch_gain_t<u16>(const GainArgs<u16>&, float*, float*, float*, hipStream_t);
+
+bs_status launch_gain_se(const double* part, int K, int64_t T, int64_t d, const float* scale, const float* gain,
+                         float* se, hipStream_t st) {
+  if (d <= 0) return BS_OK;
+  const int64_t nrt = (T + 31) / 32;
+  gain_se_kernel<<<(unsigned)((d + 255) / 256), 256, 0, st>>>(part, K, nrt, d, scale, gain, se);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+template <typename T>
+bs_status launch_dx_t(const DxArgs<T>& a, hipStream_t st) {
+  if (a.T > 0) norm_dx_kernel<T><<<(unsigned)((a.T + 3) / 4), 256, 0, st>>>(a);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+template bs_status launch_dx_t<float>(const DxArgs<float>&, hipStream_t);
+template bs_status launch_dx_t<u16>(const DxArgs<u16>&, hipStream_t);
+
+bs_status launch_combine(const float* ref, const float* bias, const float* se, int64_t n, float* mean_out,
+                         float* bias_out, float* se_out, hipStream_t st) {
+  if (n <= 0 || (!mean_out && !bias_out && !se_out)) return BS_OK;
+  combine_kernel<<<grid1d(n), 256, 0, st>>>(ref, bias, se, n, mean_out, bias_out, se_out);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+bs_status launch_combine_alt(const float* ref, const float* alt, int64_t n, float* mean_out, float* bias_out,
+                             float* se_out, hipStream_t st) {
+  if (n <= 0 || (!mean_out && !bias_out && !se_out)) return BS_OK;
+  combine_alt_kernel<<<grid1d(n), 256, 0, st>>>(ref, alt, n, mean_out, bias_out, se_out);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+}  // namespace bsp

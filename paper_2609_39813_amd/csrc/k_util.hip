@@ -1,0 +1,187 @@
+// Utility kernels: fills, bf16 operand planes (copy / split / transpose), and the trial
+// statistics reducer.
+#include "bsp_kernels.h"
+
+namespace bsp {
+
+__global__ void init_diag_only(bs_diag* diag) {
+  if (threadIdx.x == 0) {
+    diag->nonfinite = 0;
+    diag->n_saturated = 0;
+    diag->amax = 0.0f;
+    diag->scale = 1.0f;
+  }
+}
+
+bs_status launch_init_diag(bs_diag* diag, hipStream_t st) {
+  init_diag_only<<<1, 64, 0, st>>>(diag);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+__global__ void fill2d_kernel(float* p, int64_t rows, int64_t cols, int64_t ld, float v) {
+  const int64_t n = rows * cols;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[(i / cols) * ld + (i % cols)] = v;
+}
+__global__ void fill_f64_kernel(double* p, int64_t n, double v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = v;
+}
+
+bs_status launch_fill2d(float* p, int64_t rows, int64_t cols, int64_t ld, float v, hipStream_t st) {
+  const int64_t n = rows * cols;
+  if (n <= 0) return BS_OK;
+  const int64_t want = (n + 255) / 256;
+  fill2d_kernel<<<(unsigned)(want < 4096 ? want : 4096), 256, 0, st>>>(p, rows, cols, ld, v);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_fill_f64(double* p, int64_t n, double v, hipStream_t st) {
+  if (n <= 0) return BS_OK;
+  const int64_t want = (n + 255) / 256;
+  fill_f64_kernel<<<(unsigned)(want < 4096 ? want : 4096), 256, 0, st>>>(p, n, v);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+// ------------------------------------------------------------------------------------
+// bf16 planes of a [R, C] matrix: value * scale split into nterms bf16 terms.
+// ------------------------------------------------------------------------------------
+struct PlaneOut {
+  u16* p[3];
+};
+
+__device__ __forceinline__ void split_to(float v, int nterms, u16 (&o)[3]) {
+  if (nterms == 1) {
+    o[0] = bf16_bits(v);
+    o[1] = o[2] = 0;
+  } else {
+    split3(v, o[0], o[1], o[2]);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void planes_rows_kernel(const T* __restrict__ in, int64_t R, int64_t C, int64_t ldi,
+                                                          PlaneOut out, int nterms, int64_t ldo, float scale) {
+  const int64_t n = R * ldo;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / ldo, c = i - r * ldo;
+    const float v = c < C ? load_f32(in, r * ldi + c) * scale : 0.0f;
+    u16 o[3];
+    split_to(v, nterms, o);
+    for (int p = 0; p < nterms; ++p) out.p[p][i] = o[p];
+  }
+}
+
+// Transposed: out_p[c * ldo + r] for r < ldo (zero for r >= R). Tile 64 x 64 through LDS.
+template <typename T>
+__global__ __launch_bounds__(256) void planes_t_kernel(const T* __restrict__ in, int64_t R, int64_t C, int64_t ldi,
+                                                       PlaneOut out, int nterms, int64_t ldo, float scale) {
+  __shared__ u16 tile[3][64][66];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int rr = ty + 4 * i;
+    const int64_t r = r0 + rr, c = c0 + tx;
+    const float v = (r < R && c < C) ? load_f32(in, r * ldi + c) * scale : 0.0f;
+    u16 o[3];
+    split_to(v, nterms, o);
+    for (int p = 0; p < nterms; ++p) tile[p][rr][tx] = o[p];
+  }
+  __syncthreads();
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int cc = ty + 4 * i;
+    const int64_t c = c0 + cc, r = r0 + tx;
+    if (c < C && r < ldo)
+      for (int p = 0; p < nterms; ++p) out.p[p][c * ldo + r] = tile[p][tx][cc];
+  }
+}
+
+bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64_t ldi, bool transpose,
+                        u16* const* outp, int nterms, int64_t ldo, float scale, hipStream_t st) {
+  if (nterms < 1 || nterms > 3) return BS_EINVAL;
+  PlaneOut out{{outp[0], nterms > 1 ? outp[1] : nullptr, nterms > 2 ? outp[2] : nullptr}};
+  if (transpose) {
+    if (C <= 0 || ldo <= 0) return BS_OK;
+    dim3 grid((unsigned)((C + 63) / 64), (unsigned)((ldo + 63) / 64));
+    if (dt == BS_F32)
+      planes_t_kernel<float><<<grid, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
+    else
+      planes_t_kernel<u16><<<grid, 256, 0, st>>>((const u16*)in, R, C, ldi, out, nterms, ldo, scale);
+  } else {
+    const int64_t n = R * ldo;
+    if (n <= 0) return BS_OK;
+    const int64_t want = (n + 255) / 256;
+    const unsigned blocks = (unsigned)(want < 8192 ? want : 8192);
+    if (dt == BS_F32)
+      planes_rows_kernel<float><<<blocks, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
+    else
+      planes_rows_kernel<u16><<<blocks, 256, 0, st>>>((const u16*)in, R, C, ldi, out, nterms, ldo, scale);
+  }
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+// ------------------------------------------------------------------------------------
+// Trial statistics: per column j of delta [K][m], mean over trials (fp64, trials in
+// order), sample variance by a second pass, se = sd / sqrt(K); block partial sums of
+// mean^2, ref^2 and se^2 (fp64), combined in block order by one more kernel.
+// ------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void trial_stats_kernel(const float* __restrict__ delta, int K, int64_t m,
+                                                          const float* __restrict__ g_ref, float* __restrict__ mean_err,
+                                                          float* __restrict__ se, double* __restrict__ part) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  double mean = 0.0, var = 0.0, ref = 0.0;
+  if (j < m) {
+    // mean = d_1 + (1/K) sum_k (d_k - d_1): exactly d_1 when every trial agrees
+    const double d1 = delta[j];
+    double s = 0.0;
+    for (int k = 1; k < K; ++k) s += (double)delta[(int64_t)k * m + j] - d1;
+    mean = d1 + s / K;
+    double q = 0.0;
+    for (int k = 0; k < K; ++k) {
+      const double e = (double)delta[(int64_t)k * m + j] - mean;
+      q += e * e;
+    }
+    var = K > 1 ? q / (K - 1) / K : 0.0;
+    mean_err[j] = (float)mean;
+    if (se) se[j] = (float)sqrt(var);
+    if (g_ref) ref = g_ref[j];
+  }
+  __shared__ double red[3][4];
+  double v[3] = {mean * mean, ref * ref, var};
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int i = 0; i < 3; ++i) {
+    const double s = wave_sum_f64(v[i]);
+    if (lane == 0) red[i][w] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x < 3) {
+    const int i = threadIdx.x;
+    part[(int64_t)blockIdx.x * 3 + i] = ((red[i][0] + red[i][1]) + red[i][2]) + red[i][3];
+  }
+}
+
+__global__ void trial_summary_kernel(const double* __restrict__ part, int64_t nblk, double* __restrict__ summary) {
+  if (threadIdx.x != 0) return;
+  double s[3] = {0.0, 0.0, 0.0};
+  for (int64_t b = 0; b < nblk; ++b)
+    for (int i = 0; i < 3; ++i) s[i] += part[b * 3 + i];
+  summary[0] = sqrt(s[0]);
+  summary[1] = sqrt(s[1]);
+  summary[2] = s[2] > 0.0 ? s[0] / s[2] : __builtin_nan("");
+}
+
+bs_status launch_policy_bias(const float* delta, int K, int64_t m, const float* g_ref, float* mean_err, float* se,
+                             double* summary, double* ws, hipStream_t st) {
+  const int64_t nblk = (m + 255) / 256;
+  if (nblk > 0)
+    trial_stats_kernel<<<(unsigned)nblk, 256, 0, st>>>(delta, K, m, g_ref, mean_err, se, ws);
+  if (summary) trial_summary_kernel<<<1, 64, 0, st>>>(ws, nblk, summary);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+}  // namespace bsp

@@ -1,0 +1,72 @@
+"""Seeded synthetic inputs shaped like the paper's operators (no method arithmetic here).
+
+The paper's workloads are FineWeb-Edu windows through a 390M Llama-3-style model (App. D.1,
+Table "Training recipes"); neither the data nor trained weights are available, so these
+generators stand in for them with the operator shapes of that model: width 1024, MLP width
+4096, 16 heads of 64, sequences of 1024 or 2048 tokens. Every tensor is drawn from torch's
+CPU generator seeded with 1000 * config + i for the i-th tensor of the config, drawn as
+fp32 normals and rounded to nearest into the stated dtype. N(0, v) means variance v.
+
+The same tensors feed the oracle (as fp32 values) and the library (as device tensors).
+"""
+import torch
+
+CONFIGS = {
+    1: dict(name="rmsnorm_linear_fp32", T=256, d=64, n=64, dtype=torch.float32, K=64, fwd_mode="rne",
+            policies=("U/U", "R/R", "N/N"), seed=0xB5F1),
+    2: dict(name="rmsnorm_linear_390m_mlp_up", T=8192, d=1024, n=4096, dtype=torch.bfloat16, K=256, fwd_mode="rne",
+            policies=("U/U", "R/R", "N/N"), seed=0xB5F2),
+    3: dict(name="attention_bwd_b4_h16_s1024_d64", B=4, H=16, S=1024, dh=64, dtype=torch.bfloat16, K=32,
+            fwd_mode="sr", policies=("U", "R", "N"), seed=0xB5F3),
+    4: dict(name="linear_bwd_e5m2_16384x2048x8192", M=16384, k=2048, n=8192, dtype=torch.bfloat16, K=64,
+            sharings=("shared", "per_use"), seed=0xB5F4),
+}
+
+
+def _gen(config, i):
+    g = torch.Generator()
+    g.manual_seed(1000 * config + i)
+    return g
+
+
+def normal(shape, std, dtype, config, i):
+    return (torch.randn(*shape, generator=_gen(config, i), dtype=torch.float32) * std).to(dtype)
+
+
+def rmsnorm_linear_inputs(T, d, n, dtype, config=2):
+    """X ~ N(0,1) [T,d]; gain = 1 + 0.1 N(0,1) [d] fp32; W ~ N(0, 1/d) [d,n]; dY ~ N(0,1) [T,n]."""
+    X = normal((T, d), 1.0, dtype, config, 0)
+    gain = 1.0 + 0.1 * torch.randn(d, generator=_gen(config, 1), dtype=torch.float32)
+    W = normal((d, n), d ** -0.5, dtype, config, 2)
+    dY = normal((T, n), 1.0, dtype, config, 3)
+    return X, gain, W, dY
+
+
+def attention_inputs(B, H, S, dh, dtype=torch.bfloat16, config=3):
+    """Q, K, V, dO ~ N(0, 1) [B, H, S, dh]."""
+    return tuple(normal((B, H, S, dh), 1.0, dtype, config, i) for i in range(4))
+
+
+def linear_bwd_inputs(M, k, n, dtype=torch.bfloat16, config=4, tail_frac=0.01, tail_mult=100.0):
+    """X ~ N(0,1) [M,k]; W ~ N(0, 1/k) [k,n]; dY ~ N(0, 1e-2) [M,n] with a seeded 1% of entries
+    multiplied by 100 (the heavy tail); probes A [M,k], B [k,n] ~ N(0,1) fp32."""
+    X = normal((M, k), 1.0, dtype, config, 0)
+    W = normal((k, n), k ** -0.5, dtype, config, 1)
+    dy = torch.randn(M, n, generator=_gen(config, 2), dtype=torch.float32) * 0.1
+    tail = torch.rand(M, n, generator=_gen(config, 3)) < tail_frac
+    dy = torch.where(tail, dy * tail_mult, dy).to(dtype)
+    A = torch.randn(M, k, generator=_gen(config, 4), dtype=torch.float32)
+    Bp = torch.randn(k, n, generator=_gen(config, 5), dtype=torch.float32)
+    return X, W, dy, A, Bp
+
+
+def config_inputs(c, **override):
+    cfg = dict(CONFIGS[c])
+    cfg.update(override)
+    if c in (1, 2):
+        return cfg, rmsnorm_linear_inputs(cfg["T"], cfg["d"], cfg["n"], cfg["dtype"], c)
+    if c == 3:
+        return cfg, attention_inputs(cfg["B"], cfg["H"], cfg["S"], cfg["dh"], cfg["dtype"], c)
+    if c == 4:
+        return cfg, linear_bwd_inputs(cfg["M"], cfg["k"], cfg["n"], cfg["dtype"], c)
+    raise KeyError(c)

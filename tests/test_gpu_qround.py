@@ -1,0 +1,82 @@
+"""GPU parity: bs_qround against the oracle's FP8 store, bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import fp8, philox, qround as oq
+
+pytestmark = pytest.mark.gpu
+FMT = {"e4m3": fp8.E4M3, "e5m2": fp8.E5M2}
+
+
+def run(lib, x, fmt, mode, seed=0, trial=0, use=0, scale=None):
+    print(f"[qround] n={x.numel()} dtype={x.dtype} fmt={fmt} mode={mode} seed={seed}", flush=True)
+    codes, s, dg = lib.qround(x.cuda(), fmt, mode, seed, trial, use, None if scale is None else scale.cuda())
+    torch.cuda.synchronize()
+    return codes.cpu().numpy(), float(s.cpu()[0]), lib.diag_dict(dg)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+@pytest.mark.parametrize("mode", ["rne", "sr"])
+@pytest.mark.parametrize("n", [1, 3, 4, 4097, 100003])
+def test_codes_bit_exact(lib, dtype, fmt, mode, n):
+    g = torch.Generator().manual_seed(n)
+    x = (torch.randn(n, generator=g) * 3).to(dtype)
+    codes, s, dg = run(lib, x, fmt, mode, seed=0xB5F0 + n, trial=3, use=257)
+    ref = oq.qround(x.float().numpy(), FMT[fmt], oq.RNE if mode == "rne" else oq.SR, 0xB5F0 + n, 3, 257)
+    assert s == float(ref.scale) and dg["scale"] == float(ref.scale)
+    assert dg["amax"] == float(ref.amax) and dg["nonfinite"] == 0
+    assert dg["n_saturated"] == ref.n_saturated
+    assert np.array_equal(codes, ref.codes)
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+@pytest.mark.parametrize("mode", ["rne", "sr"])
+def test_codec_edge_values_unit_scale(lib, fmt, mode):
+    f = FMT[fmt]
+    grid = np.unique(np.abs(fp8.decode(np.arange(256, dtype=np.uint8), f)))
+    grid = grid[grid <= f.fmax]               # drop the NaN pattern of E4M3 / infinities of E5M2
+    mids = (grid[1:] + grid[:-1]) / 2
+    vals = np.concatenate([grid, -grid, mids, -mids, np.nextafter(mids.astype(np.float32), np.float32(0)),
+                           np.nextafter(mids.astype(np.float32), np.float32(1e9)), [0.0, -0.0, f.min_sub / 2,
+                           -f.min_sub / 3, 1e-30, -1e-38, f.fmax * 1.5, -f.fmax * 7, 2.0 ** -20, 2.0 ** -27]])
+    x = torch.tensor(vals.astype(np.float32))
+    one = torch.ones(1)
+    codes, s, dg = run(lib, x, fmt, mode, seed=77, trial=1, use=2, scale=one)
+    ref = oq.round_scaled(x.numpy(), f, oq.RNE if mode == "rne" else oq.SR, 77, 1, 2)
+    assert s == 1.0
+    assert ref[1] == 2
+    assert dg["n_saturated"] == ref[1]
+    assert np.array_equal(codes, ref[0])
+
+
+def test_zero_tensor_and_empty(lib):
+    codes, s, dg = run(lib, torch.zeros(1000), "e4m3", "sr", seed=5)
+    assert s == 1.0 and np.all(codes == 0) and dg["amax"] == 0.0
+    codes, s, dg = run(lib, torch.zeros(0), "e5m2", "rne")
+    assert s == 1.0 and codes.size == 0 and dg["nonfinite"] == 0
+
+
+@pytest.mark.parametrize("bad", [float("nan"), float("inf"), float("-inf")])
+def test_nonfinite_flagged(lib, bad):
+    x = torch.randn(5000)
+    x[1234] = bad
+    _, _, dg = run(lib, x, "e4m3", "rne")
+    assert dg["nonfinite"] == 1
+
+
+def test_large_tensor_sampled_sr(lib):
+    # the size of the E5M2 gradient store of the 16384 x 8192 Linear backward
+    n = 16384 * 8192
+    g = torch.Generator().manual_seed(11)
+    x = (torch.randn(n, generator=g) * 0.1).to(torch.bfloat16)
+    codes, s, dg = run(lib, x, "e5m2", "sr", seed=0xB5F4, trial=9, use=1025)
+    xf = x.float().numpy()
+    amax = np.float32(np.abs(xf).max())
+    assert dg["amax"] == float(amax)
+    sc = oq.scale_of(amax, fp8.E5M2)
+    assert s == float(sc)
+    idx = np.unique(np.concatenate([np.arange(4096), np.random.default_rng(0).integers(0, n, 200000), [n - 1]]))
+    ref, _ = oq.round_scaled(oq.scaled(xf[idx], sc), fp8.E5M2, oq.SR, 0xB5F4, 9, 1025, elements=idx.astype(np.uint64))
+    assert np.array_equal(codes[idx], ref)
