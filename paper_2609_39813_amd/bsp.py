@@ -66,6 +66,22 @@ _lin = _sig("bs_linear_bwd_policy", _int,
             [_vp, _vp, _vp, _int, _i64, _i64, _i64, _int, ctypes.POINTER(_int), _int, _int, _u64, _u32, _vp, _vp,
              Est, Est, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp])
 
+_prof_enable = _sig("bs_profile_enable", _int, [_int])
+_prof_read = _sig("bs_profile_read", _int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_int)])
+
+
+def profile_enable(on=True):
+    _check(_prof_enable(int(on)), "bs_profile_enable")
+
+
+def profile_read(kernel=None):
+    """(total ms, launches) of the instrumented kernel since profile_enable."""
+    ms, n = ctypes.c_double(), _int()
+    _check(_prof_read(None if kernel is None else kernel.encode(), ctypes.byref(ms), ctypes.byref(n)),
+           "bs_profile_read")
+    return ms.value, n.value
+
+
 EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
             "bs_policy_bias_estimate", "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
             "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy"]

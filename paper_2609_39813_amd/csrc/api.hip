@@ -87,7 +87,7 @@ struct NormWs {
   float *u, *rstd, *du, *bias_rg, *bias_ng, *se_g, *bias_u, *bias_n[2], *dx_r;
   u16 *dyT[3], *uvalT, *resU[3], *resN[2], *uval_rows, *wT[3], *dy_rows[3], *w_rows[3];
   u16 *counts_g, *counts_w;
-  double *partial, *gain_part;
+  double *partial, *gain_part, *trial_sums;
 };
 
 NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype dt, const NormPlan& p, bool want_y) {
@@ -123,7 +123,10 @@ NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype dt
   }
   if (p.gain_n || p.weight_n[0]) w.counts_g = c.take<u16>(T * d);
   if (p.weight_n[1]) w.counts_w = c.take<u16>(T * d);
-  if (p.gain_se) w.partial = c.take<double>((int64_t)K * ((T + 31) / 32) * d + 1);
+  if (p.gain_se) {
+    w.partial = c.take<double>((int64_t)K * ((T + 31) / 32) * d + 1);
+    w.trial_sums = c.take<double>((int64_t)K * d);
+  }
   if (p.want_dxr) w.dx_r = c.take<float>(T * d);
   return w;
 }
@@ -282,7 +285,7 @@ bs_status bs_rmsnorm_linear_fwd_bwd(const void* X, const float* gain, const void
                      p.gain_r ? 1 : 0, f, T, d, w.gain_part};
     BS_TRY(launch_gain_t(ga, dgain_ref, w.bias_rg, w.bias_ng, st));
   }
-  if (p.gain_se) BS_TRY(launch_gain_se(w.partial, K, T, d, u_scale, gain, w.se_g, st));
+  if (p.gain_se) BS_TRY(launch_gain_se(w.partial, K, T, d, u_scale, gain, w.trial_sums, w.se_g, st));
 
   // weight use: U bias = (u - s val)^T dY; N bias = (s / K) (sum of up counts residual)^T dY
   if (p.weight_u) {

@@ -33,6 +33,18 @@ inline bool gemm_add_products(GemmArgs& g, const u16* const* A, int nA, const u1
 
 bs_status launch_gemm(const GemmArgs& g, hipStream_t st);
 
+// Records HIP events around a kernel launch while profiling is enabled (bs_profile_enable).
+class ProfScope {
+ public:
+  ProfScope(const char* name, hipStream_t st);
+  ~ProfScope();
+
+ private:
+  const char* name_;
+  hipStream_t st_;
+  hipEvent_t a_, b_;
+};
+
 bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode, uint64_t seed, uint32_t trial,
                        uint32_t use, const float* scale_in, uint8_t* codes, float* scale_out, bs_diag* diag,
                        hipStream_t st, bool amax_done);

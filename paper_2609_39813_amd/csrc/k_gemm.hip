@@ -116,6 +116,7 @@ bs_status launch_gemm(const GemmArgs& g, hipStream_t st) {
   const int64_t tiles = (int64_t)((g.M + GBM - 1) / GBM) * ((g.N + GBN - 1) / GBN);
   if (tiles > 0x7FFFFFFF) return BS_ESHAPE;
   if (g.K == 0) return g.accumulate ? BS_OK : launch_fill2d(g.C, g.M, g.N, g.ldc, 0.0f, st);
+  ProfScope prof("gemm", st);
   gemm_nt_kernel<<<(unsigned)tiles, 256, 0, st>>>(g);
   BS_CHECK_LAUNCH();
   return BS_OK;

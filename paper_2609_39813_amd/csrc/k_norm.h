@@ -57,7 +57,7 @@ bs_status launch_val_rows(const uint8_t* codes, int64_t n, int fmt, u16* out, hi
 template <typename T>
 bs_status launch_gain_t(const GainArgs<T>& a, float* ref, float* bias_r, float* bias_n, hipStream_t st);
 bs_status launch_gain_se(const double* part, int K, int64_t T, int64_t d, const float* scale, const float* gain,
-                         float* se, hipStream_t st);
+                         double* S, float* se, hipStream_t st);
 template <typename T>
 bs_status launch_dx_t(const DxArgs<T>& a, hipStream_t st);
 bs_status launch_combine(const float* ref, const float* bias, const float* se, int64_t n, float* mean_out,

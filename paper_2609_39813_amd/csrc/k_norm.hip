@@ -143,33 +143,56 @@ __global__ __launch_bounds__(256) void gain_partials_kernel(GainArgs<T> a) {
   a.part[(2 * nrt + rt) * a.d + j] = q2;
 }
 
+// Sums the row-tile partials of each column: 4 segments of row tiles per column, each
+// summed in order, then the segments in order (fixed order, deterministic).
 __global__ __launch_bounds__(256) void gain_final_kernel(const double* __restrict__ part, int64_t nrt, int64_t d,
                                                          float* __restrict__ ref, float* __restrict__ bias_r,
                                                          float* __restrict__ bias_n) {
-  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (j >= d) return;
+  __shared__ double red[3][4][64];
+  const int c = threadIdx.x & 63, sgi = threadIdx.x >> 6;
+  const int64_t j = (int64_t)blockIdx.x * 64 + c;
+  const int64_t per = (nrt + 3) / 4;
+  const int64_t r0 = sgi * per, r1 = (r0 + per) < nrt ? (r0 + per) : nrt;
   double q[3] = {0.0, 0.0, 0.0};
-  for (int i = 0; i < 3; ++i)
-    for (int64_t rt = 0; rt < nrt; ++rt) q[i] += part[(i * nrt + rt) * d + j];
-  ref[j] = (float)q[0];
-  if (bias_r) bias_r[j] = (float)q[1];
-  if (bias_n) bias_n[j] = (float)q[2];
+  if (j < d)
+    for (int i = 0; i < 3; ++i)
+      for (int64_t rt = r0; rt < r1; ++rt) q[i] += part[(i * nrt + rt) * d + j];
+  for (int i = 0; i < 3; ++i) red[i][sgi][c] = q[i];
+  __syncthreads();
+  if (sgi == 0 && j < d) {
+    double t[3];
+    for (int i = 0; i < 3; ++i) t[i] = ((red[i][0][c] + red[i][1][c]) + red[i][2][c]) + red[i][3][c];
+    ref[j] = (float)t[0];
+    if (bias_r) bias_r[j] = (float)t[1];
+    if (bias_n) bias_n[j] = (float)t[2];
+  }
 }
 
 // se of the gain use under N: the per-trial gradient is const + (s / gain) S_k with
-// S_k = sum over row tiles of the fresh counter's partials; Welford over k in order.
-__global__ __launch_bounds__(256) void gain_se_kernel(const double* __restrict__ part, int K, int64_t nrt, int64_t d,
+// S_k = sum over row tiles of the new-rounding counter's partials. First S_k[j] for every
+// (trial, column) (row tiles summed in order), then Welford over k in order per column.
+__global__ __launch_bounds__(256) void gain_trial_sum_kernel(const double* __restrict__ part, int64_t nrt, int64_t d,
+                                                             double* __restrict__ S) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t k = blockIdx.y;
+  if (j >= d) return;
+  const double* p = part + k * nrt * d + j;
+  double acc = 0.0;
+  for (int64_t rt = 0; rt < nrt; ++rt) acc += p[rt * d];
+  S[k * d + j] = acc;
+}
+
+__global__ __launch_bounds__(256) void gain_se_kernel(const double* __restrict__ S, int K, int64_t d,
                                                       const float* __restrict__ scale, const float* __restrict__ gain,
                                                       float* __restrict__ se) {
   const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (j >= d) return;
   double mean = 0.0, m2 = 0.0;
   for (int k = 0; k < K; ++k) {
-    double S = 0.0;
-    for (int64_t rt = 0; rt < nrt; ++rt) S += part[((int64_t)k * nrt + rt) * d + j];
-    const double dlt = S - mean;
+    const double v = S[(int64_t)k * d + j];
+    const double dlt = v - mean;
     mean += dlt / (k + 1);
-    m2 += dlt * (S - mean);
+    m2 += dlt * (v - mean);
   }
   const double f = fabs((double)*scale / (double)gain[j]);
   se[j] = K > 1 ? (float)(f * sqrt(m2 / (K - 1) / K)) : 0.0f;
@@ -246,6 +269,7 @@ bs_status launch_rmsnorm_fwd(const void* X, bs_dtype dt, const float* gain, int6
                              float* rstd, bs_diag* diag, hipStream_t st) {
   if (T > 0) {
     const unsigned blocks = (unsigned)((T + 3) / 4);
+    ProfScope prof("rmsnorm_fwd", st);
     if (dt == BS_F32)
       rmsnorm_fwd_kernel<float><<<blocks, 256, 0, st>>>((const float*)X, gain, T, d, eps, u, rstd,
                                                         (uint32_t*)&diag->amax);
@@ -289,7 +313,7 @@ bs_status launch_gain_t(const GainArgs<T>& a, float* ref, float* bias_r, float* 
   }
   dim3 grid((unsigned)((a.d + 255) / 256), (unsigned)nrt);
   gain_partials_kernel<T><<<grid, 256, 0, st>>>(a);
-  gain_final_kernel<<<(unsigned)((a.d + 255) / 256), 256, 0, st>>>(a.part, nrt, a.d, ref, bias_r, bias_n);
+  gain_final_kernel<<<(unsigned)((a.d + 63) / 64), 256, 0, st>>>(a.part, nrt, a.d, ref, bias_r, bias_n);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
@@ -297,10 +321,11 @@ template bs_status launch_gain_t<float>(const GainArgs<float>&, float*, float*, 
 template bs_status launch_gain_t<u16>(const GainArgs<u16>&, float*, float*, float*, hipStream_t);
 
 bs_status launch_gain_se(const double* part, int K, int64_t T, int64_t d, const float* scale, const float* gain,
-                         float* se, hipStream_t st) {
+                         double* S, float* se, hipStream_t st) {
   if (d <= 0) return BS_OK;
   const int64_t nrt = (T + 31) / 32;
-  gain_se_kernel<<<(unsigned)((d + 255) / 256), 256, 0, st>>>(part, K, nrt, d, scale, gain, se);
+  gain_trial_sum_kernel<<<dim3((unsigned)((d + 255) / 256), (unsigned)K), 256, 0, st>>>(part, nrt, d, S);
+  gain_se_kernel<<<(unsigned)((d + 255) / 256), 256, 0, st>>>(S, K, d, scale, gain, se);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

@@ -198,6 +198,7 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
   if (n > 0) {
     const int64_t groups = (n + 3) / 4;
     const unsigned blocks = (unsigned)((groups + 255) / 256);
+    ProfScope prof("quantize", st);
 #define QK(T, M) quantize_kernel<T, M><<<blocks, 256, 0, st>>>((const T*)x, n, f, diag, codes, seed, trial, use)
     if (xt == BS_F32) {
       if (mode == BS_SR) QK(float, BS_SR); else QK(float, BS_RNE);
@@ -215,6 +216,7 @@ bs_status launch_fresh_count(const float* u, int64_t T, int64_t d, int fmt, cons
   if (T == 0) return BS_OK;
   const F8 f = f8_format(fmt);
   dim3 grid((unsigned)((d + 255) / 256), (unsigned)((T + 31) / 32));
+  ProfScope prof(partial ? "fresh_count_se" : "fresh_count", st);
   if (partial)
     fresh_count_kernel<true><<<grid, 256, 0, st>>>(u, T, d, f, scale, seed, use, K, counts, w, partial);
   else

@@ -1,0 +1,82 @@
+// Kernel timing instrumentation: when enabled, a pair of HIP events is recorded on the
+// launch stream around each instrumented kernel launch; bs_profile_read() waits for the
+// events and sums the elapsed time per kernel name. Off by default (no events recorded).
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "bsp_kernels.h"
+
+namespace bsp {
+
+namespace {
+struct Rec {
+  std::string name;
+  hipEvent_t a, b;
+};
+std::mutex g_mu;
+bool g_on = false;
+std::vector<hipEvent_t> g_pool;
+size_t g_next = 0;
+std::vector<Rec> g_recs;
+constexpr size_t kPool = 16384;
+
+void release_all() {
+  for (auto e : g_pool) hipEventDestroy(e);
+  g_pool.clear();
+  g_recs.clear();
+  g_next = 0;
+}
+}  // namespace
+
+ProfScope::ProfScope(const char* name, hipStream_t st) : name_(name), st_(st), a_(nullptr), b_(nullptr) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_on || g_next + 2 > g_pool.size()) return;
+  a_ = g_pool[g_next++];
+  b_ = g_pool[g_next++];
+  hipEventRecord(a_, st_);
+}
+
+ProfScope::~ProfScope() {
+  if (!a_) return;
+  hipEventRecord(b_, st_);
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_recs.push_back({name_, a_, b_});
+}
+
+}  // namespace bsp
+
+extern "C" {
+
+int bs_profile_enable(int on) {
+  using namespace bsp;
+  std::lock_guard<std::mutex> lk(g_mu);
+  release_all();
+  g_on = on != 0;
+  if (g_on) {
+    g_pool.resize(kPool);
+    for (auto& e : g_pool)
+      if (hipEventCreate(&e) != hipSuccess) return BS_EHIP;
+  }
+  return BS_OK;
+}
+
+int bs_profile_read(const char* kernel, double* total_ms, int* launches) {
+  using namespace bsp;
+  std::lock_guard<std::mutex> lk(g_mu);
+  double tot = 0.0;
+  int n = 0;
+  for (auto& r : g_recs) {
+    if (kernel && r.name != kernel) continue;
+    if (hipEventSynchronize(r.b) != hipSuccess) return BS_EHIP;
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return BS_EHIP;
+    tot += ms;
+    ++n;
+  }
+  if (total_ms) *total_ms = tot;
+  if (launches) *launches = n;
+  return BS_OK;
+}
+
+}  // extern "C"
