@@ -4,16 +4,6 @@
 
 extern "C" {
 
-size_t bs_attn_workspace_size(int B, int H, int S, int dh, int n_pol, int K) {
-  (void)B; (void)H; (void)S; (void)dh; (void)n_pol; (void)K;
-  return 0;
-}
-bs_status bs_attn_bwd_policy(const void*, const void*, const void*, const void*, int, int, int, int, int, float,
-                             const float*, bs_fp8, bs_round, const bs_read*, int, int, uint64_t, uint32_t, float*,
-                             uint8_t*, float*, float*, float*, float*, float*, bs_est, bs_est, bs_diag*, void*, size_t,
-                             void*) {
-  return BS_EUNSUPPORTED;
-}
 size_t bs_linear_bwd_workspace_size(int64_t M, int64_t k, int64_t n, int n_pol, int K) {
   (void)M; (void)k; (void)n; (void)n_pol; (void)K;
   return 0;

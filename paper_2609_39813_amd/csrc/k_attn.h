@@ -1,0 +1,50 @@
+// Argument blocks and launchers of the attention kernels (dh = 64).
+#pragma once
+#include "bsp_kernels.h"
+
+namespace bsp {
+
+constexpr int ATTN_MAX_POL = 8;
+
+struct AttnArgs {
+  const u16 *Q, *K, *V;  // [B*H][S][64] bf16
+  int S, causal;
+  float scale;
+  float* m;      // [B*H][S] row max of c S
+  float* l;      // [B*H][S] row sum of exp(c S - m)
+  float* O_out;  // nullable [B*H][S][64] fp32
+};
+
+struct AttnDArgs {
+  const float* O;         // original output, fp32
+  const u16* dO;          // bf16
+  const uint8_t* codes;   // forward's store of O
+  const float* scale;     // device s
+  int64_t rows;           // B*H*S
+  F8 f;
+  uint64_t seed;
+  uint32_t use;           // new roundings' use id
+  int K, want_n;
+  float *D_ref, *dD_R, *dD_N, *sd_N;  // [rows]
+};
+
+struct AttnBwdArgs {
+  const u16 *Q, *K, *V, *dO;
+  const float *m, *l, *D_ref, *dD_R, *dD_N, *sd_N;  // dD_R / dD_N / sd_N nullable
+  int S, causal, ntrial;  // ntrial: K, the number of new roundings
+  float scale;
+  float *dQ_ref, *dK_ref, *dV;
+  int n_pol;
+  int pol[ATTN_MAX_POL];
+  float* mean[ATTN_MAX_POL];   // dQ estimates, already offset per policy
+  float* bias[ATTN_MAX_POL];
+  float* se[ATTN_MAX_POL];
+  float* kmean[ATTN_MAX_POL];  // dK estimates
+  float* kbias[ATTN_MAX_POL];
+};
+
+bs_status launch_attn_fwd(const AttnArgs& a, int B, int H, hipStream_t st);
+bs_status launch_attn_d(const AttnDArgs& a, hipStream_t st);
+bs_status launch_attn_bwd(const AttnBwdArgs& a, int B, int H, hipStream_t st);
+
+}  // namespace bsp

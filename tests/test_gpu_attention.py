@@ -1,0 +1,127 @@
+"""GPU parity: bs_attn_bwd_policy against the oracle (oracle/attention.py).
+
+The oracle's fp32 output O is handed to both sides, so the FP8 store is compared bit for bit;
+the library's own forward is compared separately (O within 1e-5, and codes bit for bit wherever
+the two fp32 outputs agree). The exact FP8 attention example of App. C.6 must reproduce its
+eight cells exactly.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention, fp8, qround as oq
+from paper_2609_39813_amd import synth
+from tests import attn_example
+from tests.parity import assert_rel, assert_zero_where_oracle_zero, to_np
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-5
+
+
+def inputs(B, H, S, seed):
+    return [t.to(torch.bfloat16) for t in synth.attention_inputs(B, H, S, 64, torch.float32, config=100 + seed)]
+
+
+def run(lib, Q, K, V, dO, O=None, causal=True, pols=("U", "R", "N"), Kt=8, seed=3, fwd_mode="sr"):
+    print(f"[attn] shape={tuple(Q.shape)} causal={causal} pols={pols} K={Kt} O={'given' if O is not None else 'computed'}",
+          flush=True)
+    out = lib.attn_bwd_policy(Q.cuda(), K.cuda(), V.cuda(), dO.cuda(), causal=causal, O=None if O is None else
+                              torch.from_numpy(np.ascontiguousarray(O)).cuda(), fwd_mode=fwd_mode, policies=pols, K=Kt,
+                              seed=seed, store_id=1)
+    torch.cuda.synchronize()
+    return out
+
+
+def compare(out, ref, pols, heads=None):
+    B, H = out["dQ_ref"].shape[:2]
+    idx = [b * H + h for b, h in (ref["heads"] if heads is None else heads)]
+    sel = lambda t: to_np(t).reshape(B * H, *t.shape[2:])[idx]
+    assert_rel(sel(out["dV"]), ref["dV_ref"], TOL, "dV")
+    assert_rel(sel(out["dQ_ref"]), ref["dQ_ref"], TOL, "dQ_ref")
+    assert_rel(sel(out["dK_ref"]), ref["dK_ref"], TOL, "dK_ref")
+    assert_rel(sel(out["D_ref"]), ref["D_ref"], TOL, "D_ref")
+    n = out["dQ_ref"].numel()
+    shp = out["dQ_ref"].shape
+    for i, p in enumerate(pols):
+        for name in ("dQ", "dK"):
+            est = out[name]
+            m = sel(est["mean"][i].reshape(shp))
+            b = sel(est["bias"][i].reshape(shp))
+            om, ob, ose = ref[p][name]
+            assert_rel(m, om, TOL, f"{p} {name} mean")
+            if not assert_zero_where_oracle_zero(b, ob, f"{p} {name} bias"):
+                assert_rel(b, ob, TOL, f"{p} {name} bias")
+            if est["se"] is not None:
+                s = sel(est["se"][i].reshape(shp))
+                if not assert_zero_where_oracle_zero(s, ose, f"{p} {name} se"):
+                    assert_rel(s, ose, TOL, f"{p} {name} se")
+    assert n == np.prod(shp)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("S", [150, 64, 1])
+def test_ragged_given_output(lib, causal, S):
+    Q, K, V, dO = inputs(1, 2, S, seed=S)
+    ref = attention.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.float().numpy(), causal=causal,
+                          fmt=fp8.E4M3, fwd_mode=oq.SR, policies=("U", "R", "N"), K=8, seed=3, store_id=1)
+    out = run(lib, Q, K, V, dO, O=ref["O32"], causal=causal)
+    assert np.array_equal(out["O_codes"].cpu().numpy(), ref["codes"])
+    assert float(out["O_scale"].cpu()[0]) == float(ref["scale"])
+    compare(out, ref, ("U", "R", "N"))
+
+
+def test_rne_store_and_policy_order(lib):
+    Q, K, V, dO = inputs(2, 1, 96, seed=7)
+    pols = ("N", "U", "R", "N")
+    ref = attention.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.float().numpy(), causal=True,
+                          fmt=fp8.E4M3, fwd_mode=oq.RNE, policies=("N", "U", "R"), K=5, seed=9, store_id=1)
+    ref["N"] = ref["N"]
+    out = run(lib, Q, K, V, dO, O=ref["O32"], pols=pols, Kt=5, seed=9, fwd_mode="rne")
+    assert np.array_equal(out["O_codes"].cpu().numpy(), ref["codes"])
+    compare(out, ref, pols)
+
+
+def test_library_forward(lib):
+    Q, K, V, dO = inputs(1, 3, 200, seed=11)
+    ref = attention.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.float().numpy(), causal=True,
+                          fmt=fp8.E4M3, fwd_mode=oq.SR, policies=("U", "R", "N"), K=6, seed=4, store_id=1)
+    out = run(lib, Q, K, V, dO, O=None, Kt=6, seed=4)
+    O = to_np(out["O"])
+    assert_rel(O, ref["O"], TOL, "forward O")
+    same = out["O"].cpu().numpy() == ref["O32"]
+    # where the two fp32 outputs agree bit for bit and share the scale, so must the codes
+    if float(out["O_scale"].cpu()[0]) == float(ref["scale"]):
+        assert np.array_equal(out["O_codes"].cpu().numpy()[same], ref["codes"][same])
+    compare(out, ref, ("U",))
+
+
+def test_fp8_attention_example_cells_exact(lib):
+    ex = attn_example.load()
+    Qn, Kn, Vn = attn_example.inputs(ex)
+    O, _, _, _ = attention.forward(Qn, Kn, Vn, True, ex["c"])
+    a, c = ex["a"], ex["c"]
+    Q, K, V = (torch.from_numpy(t).to(torch.bfloat16) for t in (Qn, Kn, Vn))
+    for cell in ex["cells"]:
+        for key, h in (("T_h_shared_deviation", cell["sigma"] * a), ("T_h_fixed", a)):
+            dq = {}
+            for which, sign in (("shared", cell["sigma"]), ("indep", cell["tau"])):
+                Os, dOn = attn_example.saved_and_grad(ex, O, sign, h)
+                out = lib.attn_bwd_policy(Q.cuda(), K.cuda(), V.cuda(), torch.from_numpy(dOn).to(torch.bfloat16).cuda(),
+                                          causal=True, scale=c, O=torch.from_numpy(Os).cuda(), policies=("U",), K=1)
+                torch.cuda.synchronize()
+                dq[which] = float(out["dQ_ref"][0, 0, -1, 0].cpu())
+            T = (dq["indep"] - dq["shared"]) / c
+            assert T == cell[key], (cell, key, T)
+
+
+@pytest.mark.slow
+def test_config3_full_size_sampled_heads(lib):
+    cfg = synth.CONFIGS[3]
+    Q, K, V, dO = synth.attention_inputs(cfg["B"], cfg["H"], cfg["S"], cfg["dh"], cfg["dtype"], 3)
+    heads = [(0, 0), (3, 15)]
+    ref = attention.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.float().numpy(), causal=True,
+                          fmt=fp8.E4M3, fwd_mode=oq.SR, policies=cfg["policies"], K=cfg["K"], seed=cfg["seed"],
+                          store_id=1, heads=heads)
+    out = run(lib, Q, K, V, dO, O=ref["O32"], pols=cfg["policies"], Kt=cfg["K"], seed=cfg["seed"])
+    assert np.array_equal(out["O_codes"].cpu().numpy(), ref["codes"])
+    compare(out, ref, cfg["policies"], heads=heads)
