@@ -48,8 +48,30 @@ class ProfScope {
 bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode, uint64_t seed, uint32_t trial,
                        uint32_t use, const float* scale_in, uint8_t* codes, float* scale_out, bs_diag* diag,
                        hipStream_t st, bool amax_done);
+enum { FC_COUNT = 0, FC_COLSUM = 1, FC_BLOCKSUM = 2 };
+template <typename X>
+struct FreshArgs {
+  const X* x;          // [T][d] values to round (fp32 or bf16), scaled by 1/s
+  int64_t T, d;
+  F8 f;
+  const float* scale;  // device s
+  uint64_t seed;
+  uint32_t use;
+  int K;
+  u16* counts;         // [T][d] up counts (nullable)
+  const float* w1;     // [T][d] weights (FC_COLSUM, FC_BLOCKSUM)
+  const float* w2;     // [T][d] second weight (FC_BLOCKSUM, nullable)
+  double* partial;     // FC_COLSUM: [K][ceil(T/32)][d]; FC_BLOCKSUM: [K][2][nblocks]
+};
+template <typename X>
+bs_status launch_fresh_count_t(const FreshArgs<X>& a, int mode, hipStream_t st);
+inline int64_t fresh_count_blocks(int64_t T, int64_t d) { return ((d + 255) / 256) * ((T + 31) / 32); }
+
 bs_status launch_fresh_count(const float* u, int64_t T, int64_t d, int fmt, const float* scale, uint64_t seed,
                              uint32_t use, int K, u16* counts, const float* w, double* partial, hipStream_t st);
+
+bs_status launch_combine(const float* ref, const float* bias, const float* se, int64_t n, float* mean_out,
+                         float* bias_out, float* se_out, hipStream_t st);
 
 bs_status launch_fill2d(float* p, int64_t rows, int64_t cols, int64_t ld, float v, hipStream_t st);
 bs_status launch_fill_f64(double* p, int64_t n, double v, hipStream_t st);

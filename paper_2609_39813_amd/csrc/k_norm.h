@@ -60,8 +60,6 @@ bs_status launch_gain_se(const double* part, int K, int64_t T, int64_t d, const 
                          double* S, float* se, hipStream_t st);
 template <typename T>
 bs_status launch_dx_t(const DxArgs<T>& a, hipStream_t st);
-bs_status launch_combine(const float* ref, const float* bias, const float* se, int64_t n, float* mean_out,
-                         float* bias_out, float* se_out, hipStream_t st);
 
 bs_status launch_combine_alt(const float* ref, const float* alt, int64_t n, float* mean_out, float* bias_out,
                              float* se_out, hipStream_t st);

@@ -93,85 +93,130 @@ __global__ __launch_bounds__(256) void quantize_kernel(const T* __restrict__ x, 
   if ((threadIdx.x & 63) == 0 && nsat) atomicAdd(&diag->n_saturated, nsat);
 }
 
-// K-trial counter of new roundings of a [T, d] store y = fl32(u / s) (d % 4 == 0).
+// K-trial counter of new roundings of a [T, d] store y = fl32(x / s) (d % 4 == 0).
 // counts[t, j] = number of trials k in 1..K whose rounding of element t*d + j goes up.
-// With PARTIALS, also the per-trial column sums
-//   partial[k-1][rt][j] = sum over the block's rows t of up_k(t, j) * sign(y) * step(t, j) * w(t, j)
-// (fp64) for a weight w (the gain use's du), one row tile rt = 32 rows per block.
-// Block: 256 threads = 64 column groups (4 columns each) x 4 row lanes; 8 rows per thread.
-template <bool PARTIALS>
-__global__ __launch_bounds__(256) void fresh_count_kernel(const float* __restrict__ u, int64_t T, int64_t d, F8 f,
-                                                          const float* __restrict__ scale, uint64_t seed,
-                                                          uint32_t use, int K, u16* __restrict__ counts,
-                                                          const float* __restrict__ w,
-                                                          double* __restrict__ partial) {
-  constexpr int RT = 32, RPT = 8;
+// Block: 256 threads = 64 column groups (4 columns each) x 4 row lanes, 8 rows per thread,
+// so one block covers 32 rows x 256 columns. With c = sign(y) step (t, j) w(t, j):
+//   FC_COLSUM: partial[k-1][rt][j] = sum over the block's 32 rows of up_k c      (w = w1)
+//   FC_BLOCKSUM: partial[k-1][i][b] = sum over the block's elements of up_k c_i (w1, w2)
+// all in fp64, trials reduced through LDS four at a time.
+template <typename X, int MODE>
+__global__ __launch_bounds__(256) void fresh_count_kernel(FreshArgs<X> a) {
+  constexpr int RT = 32, RPT = 8, TB = 4;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   const int64_t j0 = (int64_t)blockIdx.x * 256 + 4 * tx;
   const int64_t t0 = (int64_t)blockIdx.y * RT;
-  const bool colok = j0 < d;
-  const float s = *scale;
-  uint32_t F[RPT][4];
-  float c[RPT][4];
-  uint32_t cnt[RPT][4];
+  const bool colok = j0 < a.d;
+  const float s = *a.scale;
+  uint32_t F[RPT][4], cnt[RPT][4];
+  float c1[RPT][4], c2[RPT][4];
 #pragma unroll
   for (int r = 0; r < RPT; ++r) {
     const int64_t t = t0 + ty + 4 * r;
-    const bool ok = colok && t < T;
-    float4 uv = ok ? *(const float4*)(u + t * d + j0) : make_float4(0.f, 0.f, 0.f, 0.f);
-    float4 wv = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (PARTIALS && ok) wv = *(const float4*)(w + t * d + j0);
-    const float uu[4] = {uv.x, uv.y, uv.z, uv.w};
-    const float ww[4] = {wv.x, wv.y, wv.z, wv.w};
+    const bool ok = colok && t < a.T;
+    float xv[4] = {0.f, 0.f, 0.f, 0.f}, w1v[4] = {0.f, 0.f, 0.f, 0.f}, w2v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (ok) {
+      const int64_t e = t * a.d + j0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) xv[q] = load_f32(a.x, e + q);
+      if (MODE != FC_COUNT) {
+        const float4 v = *(const float4*)(a.w1 + e);
+        w1v[0] = v.x; w1v[1] = v.y; w1v[2] = v.z; w1v[3] = v.w;
+      }
+      if (MODE == FC_BLOCKSUM && a.w2) {
+        const float4 v = *(const float4*)(a.w2 + e);
+        w2v[0] = v.x; w2v[1] = v.y; w2v[2] = v.z; w2v[3] = v.w;
+      }
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float y = __fdiv_rn(uu[q], s);
-      const float a = fminf(fabsf(y), f.fmax);
-      const Bracket b = f8_bracket(a, f);
+      const float y = __fdiv_rn(xv[q], s);
+      const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
       F[r][q] = ok ? sr_threshold(b.frac) : 0u;
-      c[r][q] = PARTIALS ? (signbit(y) ? -1.0f : 1.0f) * f8_step(b) * ww[q] : 0.0f;
+      const float sc = (signbit(y) ? -1.0f : 1.0f) * f8_step(b);
+      c1[r][q] = sc * w1v[q];
+      c2[r][q] = sc * w2v[q];
       cnt[r][q] = 0;
     }
   }
-  __shared__ double red[PARTIALS ? 4 : 1][PARTIALS ? 256 : 1];
-  const int64_t nrt = (T + RT - 1) / RT;
-  for (int k = 1; k <= K; ++k) {
-    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  constexpr int NR = MODE == FC_COLSUM ? 4 * 256 : (MODE == FC_BLOCKSUM ? 2 * 4 : 1);
+  __shared__ double red[MODE == FC_COUNT ? 1 : TB][NR];
+  const int64_t nrt = gridDim.y;
+  const int64_t nblk = (int64_t)gridDim.x * gridDim.y, bid = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+  for (int k0 = 1; k0 <= a.K; k0 += TB) {
+    double acc[TB][4];
 #pragma unroll
-    for (int r = 0; r < RPT; ++r) {
-      const int64_t t = t0 + ty + 4 * r;
-      const uint64_t g = (uint64_t)((t * d + j0) >> 2);
-      const Philox4 p = philox_group(seed, g, (uint32_t)k, use);
-      const uint32_t R[4] = {p.w0, p.w1, p.w2, p.w3};
+    for (int i = 0; i < TB; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t up = sr_up(F[r][q], R[q]);
-        cnt[r][q] += up;
-        if (PARTIALS) acc[q] += up ? (double)c[r][q] : 0.0;
-      }
-    }
-    if (PARTIALS) {
+      for (int q = 0; q < 4; ++q) acc[i][q] = 0.0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) red[ty][4 * tx + q] = acc[q];
-      __syncthreads();
-      if (ty == 0) {
+    for (int i = 0; i < TB; ++i) {
+      const int k = k0 + i;
+      if (k > a.K) break;
+#pragma unroll
+      for (int r = 0; r < RPT; ++r) {
+        const int64_t t = t0 + ty + 4 * r;
+        const uint64_t g = (uint64_t)((t * a.d + j0) >> 2);
+        const Philox4 p = philox_group(a.seed, g, (uint32_t)k, a.use);
+        const uint32_t R[4] = {p.w0, p.w1, p.w2, p.w3};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int col = 4 * tx + q;
-          const double v = ((red[0][col] + red[1][col]) + red[2][col]) + red[3][col];
-          if (colok) partial[((int64_t)(k - 1) * nrt + blockIdx.y) * d + j0 + q] = v;
+          const uint32_t up = sr_up(F[r][q], R[q]);
+          cnt[r][q] += up;
+          if (MODE == FC_COLSUM) acc[i][q] += up ? (double)c1[r][q] : 0.0;
+          if (MODE == FC_BLOCKSUM) {
+            acc[i][0] += up ? (double)c1[r][q] : 0.0;
+            acc[i][1] += up ? (double)c2[r][q] : 0.0;
+          }
         }
+      }
+    }
+    if (MODE == FC_COLSUM) {
+#pragma unroll
+      for (int i = 0; i < TB; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) red[i][ty * 256 + 4 * tx + q] = acc[i][q];
+      __syncthreads();
+      // thread -> (trial i, column); each sums its column's 4 row lanes in order
+      for (int o = threadIdx.x; o < TB * 256; o += 256) {
+        const int i = o >> 8, col = o & 255;
+        const int k = k0 + i;
+        const double v = ((red[i][col] + red[i][256 + col]) + red[i][512 + col]) + red[i][768 + col];
+        const int64_t j = (int64_t)blockIdx.x * 256 + col;
+        if (k <= a.K && j < a.d) a.partial[((int64_t)(k - 1) * nrt + blockIdx.y) * a.d + j] = v;
+      }
+      __syncthreads();
+    }
+    if (MODE == FC_BLOCKSUM) {
+      const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+      for (int i = 0; i < TB; ++i) {
+        const double v1 = wave_sum_f64(acc[i][0]);
+        const double v2 = wave_sum_f64(acc[i][1]);
+        if (lane == 0) {
+          red[i][2 * wv] = v1;
+          red[i][2 * wv + 1] = v2;
+        }
+      }
+      __syncthreads();
+      if (threadIdx.x < 2 * TB) {
+        const int i = threadIdx.x >> 1, u = threadIdx.x & 1;
+        const int k = k0 + i;
+        const double v = ((red[i][u] + red[i][2 + u]) + red[i][4 + u]) + red[i][6 + u];
+        if (k <= a.K) a.partial[((int64_t)(k - 1) * 2 + u) * nblk + bid] = v;
       }
       __syncthreads();
     }
   }
+  if (a.counts) {
 #pragma unroll
-  for (int r = 0; r < RPT; ++r) {
-    const int64_t t = t0 + ty + 4 * r;
-    if (colok && t < T) {
-      const uint32_t lo = cnt[r][0] | (cnt[r][1] << 16);
-      const uint32_t hi = cnt[r][2] | (cnt[r][3] << 16);
-      *(uint2*)(counts + t * d + j0) = make_uint2(lo, hi);
+    for (int r = 0; r < RPT; ++r) {
+      const int64_t t = t0 + ty + 4 * r;
+      if (colok && t < a.T) {
+        const uint32_t lo = cnt[r][0] | (cnt[r][1] << 16);
+        const uint32_t hi = cnt[r][2] | (cnt[r][3] << 16);
+        *(uint2*)(a.counts + t * a.d + j0) = make_uint2(lo, hi);
+      }
     }
   }
 }
@@ -195,7 +240,7 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
     }
   }
   finalize_scale_kernel<<<1, 64, 0, st>>>(diag, scale_in, scale_out, f.fmax);
-  if (n > 0) {
+  if (n > 0 && codes) {  // codes == nullptr: the scale only
     const int64_t groups = (n + 3) / 4;
     const unsigned blocks = (unsigned)((groups + 255) / 256);
     ProfScope prof("quantize", st);
@@ -211,18 +256,27 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
   return BS_OK;
 }
 
-bs_status launch_fresh_count(const float* u, int64_t T, int64_t d, int fmt, const float* scale, uint64_t seed,
-                             uint32_t use, int K, u16* counts, const float* w, double* partial, hipStream_t st) {
-  if (T == 0) return BS_OK;
-  const F8 f = f8_format(fmt);
-  dim3 grid((unsigned)((d + 255) / 256), (unsigned)((T + 31) / 32));
-  ProfScope prof(partial ? "fresh_count_se" : "fresh_count", st);
-  if (partial)
-    fresh_count_kernel<true><<<grid, 256, 0, st>>>(u, T, d, f, scale, seed, use, K, counts, w, partial);
+template <typename X>
+bs_status launch_fresh_count_t(const FreshArgs<X>& a, int mode, hipStream_t st) {
+  if (a.T == 0) return BS_OK;
+  dim3 grid((unsigned)((a.d + 255) / 256), (unsigned)((a.T + 31) / 32));
+  ProfScope prof(mode == FC_COUNT ? "fresh_count" : (mode == FC_COLSUM ? "fresh_count_se" : "fresh_count_kappa"), st);
+  if (mode == FC_COUNT)
+    fresh_count_kernel<X, FC_COUNT><<<grid, 256, 0, st>>>(a);
+  else if (mode == FC_COLSUM)
+    fresh_count_kernel<X, FC_COLSUM><<<grid, 256, 0, st>>>(a);
   else
-    fresh_count_kernel<false><<<grid, 256, 0, st>>>(u, T, d, f, scale, seed, use, K, counts, nullptr, nullptr);
+    fresh_count_kernel<X, FC_BLOCKSUM><<<grid, 256, 0, st>>>(a);
   BS_CHECK_LAUNCH();
   return BS_OK;
+}
+template bs_status launch_fresh_count_t<float>(const FreshArgs<float>&, int, hipStream_t);
+template bs_status launch_fresh_count_t<u16>(const FreshArgs<u16>&, int, hipStream_t);
+
+bs_status launch_fresh_count(const float* u, int64_t T, int64_t d, int fmt, const float* scale, uint64_t seed,
+                             uint32_t use, int K, u16* counts, const float* w, double* partial, hipStream_t st) {
+  FreshArgs<float> a{u, T, d, f8_format(fmt), scale, seed, use, K, counts, w, nullptr, partial};
+  return launch_fresh_count_t(a, partial ? FC_COLSUM : FC_COUNT, st);
 }
 
 }  // namespace bsp
