@@ -75,6 +75,60 @@ def cpu_baseline(cfg, X, g, W, dY, rows):
                        f"{t2:.1f} s; linear extrapolation to all {cfg['d']} rows = {full:.0f} s per step")}
 
 
+def side_measurements(bsp, synth, torch, dev, reps=5):
+    """The metric's other two figures, timed live with HIP events: the FP8 store's HBM rate
+    on the 16384 x 8192 bf16 gradient (E5M2, SR) and the attention backward's MFMA rate at
+    B4 H16 S1024 d64 (causal, three D policies, K = 32)."""
+    out = {}
+    cfg4 = synth.CONFIGS[4]
+    _, _, dy, _, _ = synth.linear_bwd_inputs(cfg4["M"], cfg4["k"], cfg4["n"], torch.bfloat16, 4)
+    dy = dy.to(dev)
+    n = dy.numel()
+    bsp.qround(dy, "e5m2", "sr", seed=cfg4["seed"], trial=1, use=1)
+    torch.cuda.synchronize()
+    bsp.profile_enable(True)
+    for _ in range(reps):
+        bsp.qround(dy, "e5m2", "sr", seed=cfg4["seed"], trial=1, use=1)
+    torch.cuda.synchronize()
+    am_ms, am_n = bsp.profile_read("amax")
+    q_ms, q_n = bsp.profile_read("quantize")
+    bsp.profile_enable(False)
+    am_s, q_s = am_ms / am_n / 1e3, q_ms / q_n / 1e3
+    out["qround_e5m2_16384x8192"] = {
+        "amax_GBps": round(2 * n / am_s / 1e9, 1), "amax_hbm_frac": round(2 * n / am_s / 1e9 / HBM_PEAK_GBPS, 4),
+        "quantize_GBps": round(3 * n / q_s / 1e9, 1), "quantize_hbm_frac": round(3 * n / q_s / 1e9 / HBM_PEAK_GBPS, 4),
+        "bytes": "amax reads 2 B/elem; quantize reads 2 B and writes 1 B per element", "elements": n}
+    del dy
+    cfg3 = synth.CONFIGS[3]
+    Q, K, V, dO = (t.to(dev) for t in synth.attention_inputs(cfg3["B"], cfg3["H"], cfg3["S"], cfg3["dh"],
+                                                             cfg3["dtype"], 3))
+    ws = bsp.attn_workspace(cfg3["B"], cfg3["H"], cfg3["S"], cfg3["dh"], 3, cfg3["K"], dev)
+    run = lambda: bsp.attn_bwd_policy(Q, K, V, dO, causal=True, policies=cfg3["policies"], K=cfg3["K"],
+                                      seed=cfg3["seed"], fwd_mode=cfg3["fwd_mode"], ws=ws)
+    run()
+    torch.cuda.synchronize()
+    bsp.profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        run()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / reps
+    b_ms, b_n = bsp.profile_read("attn_bwd")
+    f_ms, f_n = bsp.profile_read("attn_fwd")
+    bsp.profile_enable(False)
+    heads, S, dh = cfg3["B"] * cfg3["H"], cfg3["S"], cfg3["dh"]
+    # causal matmul of S x S x dh: S^2 dh flops; reference backward (S, dP, dV, dQ, dK) + 3 bias
+    # contractions (G = P K and the two dK bias terms)
+    flops = 8 * heads * S * S * dh
+    b_s = b_ms / b_n / 1e3
+    out["attn_bwd_b4_h16_s1024_d64"] = {
+        "TFLOPs": round(flops / b_s / 1e12, 1), "mfma_frac": round(flops / b_s / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+        "bwd_ms": round(b_s * 1e3, 4), "fwd_ms": round(f_ms / f_n, 4), "call_ms": round(wall * 1e3, 4),
+        "policy_trials_per_s": round(len(cfg3["policies"]) * cfg3["K"] / wall, 1),
+        "flops": "8 causal S x S x dh matmuls per head (5 of the reference backward + 3 bias contractions)"}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -133,6 +187,8 @@ def main():
              "kernel_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in prof.items()},
              "fresh_count_se_Getps": round(et_per_launch / (se_ms / max(se_n, 1) / 1e3) / 1e9, 1) if se_n else None,
              "path": "collapsed (per-element up-counts; se at the gain use from per-trial sums)"}
+
+    extra.update(side_measurements(bsp, synth, torch, dev))
 
     line = {"metric": "policy-trials/sec", "value": round(value, 1), "unit": "policy-trials/s", "n_gpus": 1,
             "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),

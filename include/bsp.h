@@ -218,8 +218,8 @@ bs_status bs_gemm_bf16_nt(const void* A, int64_t lda, const void* B, int64_t ldb
  * Kernel timing instrumentation (host calls; for benchmarks and profiling).
  *   bs_profile_enable(1) clears earlier records and starts recording a pair of HIP
  *   events on the launch stream around each launch of the instrumented kernels
- *   ("fresh_count", "fresh_count_se", "quantize", "gemm", "rmsnorm_fwd", "attn_fwd",
- *   "attn_bwd");
+ *   ("fresh_count", "fresh_count_se", "fresh_count_kappa", "amax", "quantize", "gemm",
+ *   "rmsnorm_fwd", "attn_fwd", "attn_bwd");
  *   bs_profile_enable(0) stops and frees them. bs_profile_read waits for the recorded
  *   events of `kernel` (NULL: all) and returns their summed elapsed time and count.
  *   Return values are bs_status codes.

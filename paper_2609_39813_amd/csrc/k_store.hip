@@ -15,16 +15,44 @@ __global__ void init_diag_kernel(bs_diag* diag) {
 
 // max |x| as the bit pattern of a non-negative float: the integer order of such
 // patterns is the float order, and NaN/Inf patterns (>= 0x7F800000) sort above every
-// finite value, so one atomicMax also detects non-finite input.
+// finite value, so one atomicMax also detects non-finite input. Each thread streams
+// 16-byte vectors (8 bf16 or 4 fp32) in a grid-stride loop; the scalar tail is done once.
+template <typename T>
+__device__ __forceinline__ uint32_t vec_absmax(uint4 v);
+template <>
+__device__ __forceinline__ uint32_t vec_absmax<float>(uint4 v) {
+  const uint32_t a = v.x & 0x7FFFFFFFu, b = v.y & 0x7FFFFFFFu, c = v.z & 0x7FFFFFFFu, d = v.w & 0x7FFFFFFFu;
+  return max(max(a, b), max(c, d));
+}
+template <>
+__device__ __forceinline__ uint32_t vec_absmax<u16>(uint4 v) {
+  // bf16 -> fp32 bit patterns are the bf16 bits shifted by 16, order preserved
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  uint32_t m = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t lo = (w[i] << 16) & 0x7FFFFFFFu, hi = w[i] & 0x7FFF0000u;
+    m = max(m, max(lo, hi));
+  }
+  return m;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void amax_kernel(const T* __restrict__ x, int64_t n,
                                                    uint32_t* __restrict__ amax_bits) {
+  constexpr int PER = 16 / sizeof(T);
   uint32_t m = 0;
+  const int64_t nvec = ((uintptr_t)x & 15) ? 0 : n / PER;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-    const uint32_t b = __float_as_uint(fabsf(load_f32(x, i)));
-    m = m > b ? m : b;
+  const uint4* xv = (const uint4*)x;
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (; i + 3 * stride < nvec; i += 4 * stride) {
+    const uint4 a = xv[i], b = xv[i + stride], c = xv[i + 2 * stride], d = xv[i + 3 * stride];
+    m = max(m, max(max(vec_absmax<T>(a), vec_absmax<T>(b)), max(vec_absmax<T>(c), vec_absmax<T>(d))));
   }
+  for (; i < nvec; i += stride) m = max(m, vec_absmax<T>(xv[i]));
+  for (int64_t j = nvec * PER + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += stride)
+    m = max(m, __float_as_uint(fabsf(load_f32(x, j))));
   m = wave_max_u32(m);
   __shared__ uint32_t red[4];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -32,7 +60,7 @@ __global__ __launch_bounds__(256) void amax_kernel(const T* __restrict__ x, int6
   __syncthreads();
   if (threadIdx.x == 0) {
     uint32_t b = red[0];
-    for (int i = 1; i < (int)(blockDim.x >> 6); ++i) b = b > red[i] ? b : red[i];
+    for (int k = 1; k < (int)(blockDim.x >> 6); ++k) b = b > red[k] ? b : red[k];
     if (b) atomicMax(amax_bits, b);
   }
 }
@@ -53,40 +81,73 @@ __global__ void finalize_scale_kernel(bs_diag* diag, const float* scale_in, floa
   if (scale_out) *scale_out = s;
 }
 
-// One thread per group of 4 consecutive elements (one Philox call).
+// Eight consecutive elements per thread (two Philox groups): 16- or 32-byte loads, an
+// 8-byte store of the codes.
+template <typename T, int MODE>
+__device__ __forceinline__ uint32_t code_of(float xv, float s, F8 f, uint32_t R, uint32_t& nsat) {
+  const float y = __fdiv_rn(xv, s);
+  float a = fabsf(y);
+  if (a > f.fmax) {
+    a = f.fmax;
+    ++nsat;
+  }
+  const Bracket b = f8_bracket(a, f);
+  const uint32_t up = MODE == BS_SR ? sr_up(sr_threshold(b.frac), R) : rne_up(b);
+  return (b.base + b.mi + up) | (signbit(y) ? 0x80u : 0u);
+}
+
 template <typename T, int MODE>
 __global__ __launch_bounds__(256) void quantize_kernel(const T* __restrict__ x, int64_t n, F8 f,
                                                        bs_diag* __restrict__ diag, uint8_t* __restrict__ codes,
                                                        uint64_t seed, uint32_t trial, uint32_t use) {
   if (diag->nonfinite) return;
   const float s = diag->scale;
-  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t e0 = g * 4;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t e0 = t * 8;
   uint32_t nsat = 0;
   if (e0 < n) {
-    Philox4 p{0, 0, 0, 0};
-    if (MODE == BS_SR) p = philox_group(seed, (uint64_t)g, trial, use);
-    uint32_t packed = 0;
-    const int cnt = (int)((n - e0) < 4 ? (n - e0) : 4);
+    float xv[8];
+    const int cnt = (int)((n - e0) < 8 ? (n - e0) : 8);
+    const bool vec = cnt == 8 && (((uintptr_t)(x + e0)) & 15) == 0 && (((uintptr_t)(codes + e0)) & 7) == 0;
+    if (vec) {
+      if (sizeof(T) == 2) {
+        const uint4 v = *(const uint4*)(x + e0);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (q < cnt) {
-        const float y = __fdiv_rn(load_f32(x, e0 + q), s);
-        float a = fabsf(y);
-        if (a > f.fmax) {
-          a = f.fmax;
-          ++nsat;
+        for (int i = 0; i < 4; ++i) {
+          xv[2 * i] = __uint_as_float(w[i] << 16);
+          xv[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
         }
-        const Bracket b = f8_bracket(a, f);
-        const uint32_t up = MODE == BS_SR ? sr_up(sr_threshold(b.frac), philox_word(p, q)) : rne_up(b);
-        const uint32_t code = (b.base + b.mi + up) | (signbit(y) ? 0x80u : 0u);
-        packed |= code << (8 * q);
+      } else {
+        const float4 a = *(const float4*)(x + e0), b = *(const float4*)(x + e0 + 4);
+        xv[0] = a.x; xv[1] = a.y; xv[2] = a.z; xv[3] = a.w;
+        xv[4] = b.x; xv[5] = b.y; xv[6] = b.z; xv[7] = b.w;
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) xv[q] = q < cnt ? load_f32(x, e0 + q) : 0.0f;
+    }
+    Philox4 p0{0, 0, 0, 0}, p1{0, 0, 0, 0};
+    if (MODE == BS_SR) {
+      p0 = philox_group(seed, (uint64_t)(2 * t), trial, use);
+      p1 = philox_group(seed, (uint64_t)(2 * t + 1), trial, use);
+    }
+    const uint32_t R[8] = {p0.w0, p0.w1, p0.w2, p0.w3, p1.w0, p1.w1, p1.w2, p1.w3};
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      uint32_t sat = 0;
+      const uint32_t code = code_of<T, MODE>(xv[q], s, f, R[q], sat);
+      if (q < cnt) {
+        nsat += sat;
+        if (q < 4) lo |= code << (8 * q);
+        else hi |= code << (8 * (q - 4));
       }
     }
-    if (cnt == 4 && ((uintptr_t)(codes + e0) & 3) == 0) {
-      *(uint32_t*)(codes + e0) = packed;
+    if (vec) {
+      *(uint2*)(codes + e0) = make_uint2(lo, hi);
     } else {
-      for (int q = 0; q < cnt; ++q) codes[e0 + q] = (uint8_t)(packed >> (8 * q));
+      for (int q = 0; q < cnt; ++q) codes[e0 + q] = (uint8_t)((q < 4 ? lo >> (8 * q) : hi >> (8 * (q - 4))));
     }
   }
   nsat = wave_sum_u32(nsat);
@@ -231,8 +292,9 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
   if (!amax_done) {
     init_diag_kernel<<<1, 64, 0, st>>>(diag);
     if (n > 0 && !scale_in) {
-      const int64_t want = (n + 255) / 256;
-      const int blocks = (int)(want < 2048 ? want : 2048);
+      const int64_t want = (n / (16 / (xt == BS_F32 ? 4 : 2)) + 255) / 256 + 1;
+      const int blocks = (int)(want < 4096 ? want : 4096);
+      ProfScope prof("amax", st);
       if (xt == BS_F32)
         amax_kernel<float><<<blocks, 256, 0, st>>>((const float*)x, n, (uint32_t*)&diag->amax);
       else
@@ -241,8 +303,8 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
   }
   finalize_scale_kernel<<<1, 64, 0, st>>>(diag, scale_in, scale_out, f.fmax);
   if (n > 0 && codes) {  // codes == nullptr: the scale only
-    const int64_t groups = (n + 3) / 4;
-    const unsigned blocks = (unsigned)((groups + 255) / 256);
+    const int64_t threads = (n + 7) / 8;
+    const unsigned blocks = (unsigned)((threads + 255) / 256);
     ProfScope prof("quantize", st);
 #define QK(T, M) quantize_kernel<T, M><<<blocks, 256, 0, st>>>((const T*)x, n, f, diag, codes, seed, trial, use)
     if (xt == BS_F32) {
