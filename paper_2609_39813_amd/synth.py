@@ -18,6 +18,8 @@ CONFIGS = {
             policies=("U/U", "R/R", "N/N"), seed=0xB5F2),
     3: dict(name="attention_bwd_b4_h16_s1024_d64", B=4, H=16, S=1024, dh=64, dtype=torch.bfloat16, K=32,
             fwd_mode="sr", policies=("U", "R", "N"), seed=0xB5F3),
+    5: dict(name="decoder_layer_b8_s2048_d1024_h16_f4096", B=8, S=2048, d=1024, H=16, F=4096, K=16, fwd_mode="rne",
+            seed=0xB5F5),
     4: dict(name="linear_bwd_e5m2_16384x2048x8192", M=16384, k=2048, n=8192, dtype=torch.bfloat16, K=64,
             sharings=("shared", "per_use"), seed=0xB5F4),
 }
@@ -58,6 +60,29 @@ def linear_bwd_inputs(M, k, n, dtype=torch.bfloat16, config=4, tail_frac=0.01, t
     A = torch.randn(M, k, generator=_gen(config, 4), dtype=torch.float32)
     Bp = torch.randn(k, n, generator=_gen(config, 5), dtype=torch.float32)
     return X, W, dy, A, Bp
+
+
+def decoder_inputs(B, S, d, H, F, vocab=131072, config=5):
+    """One decoder layer: x = embedding rows (N(0,1)) of random tokens in [0, vocab), bf16
+    [B*S, d]; weights N(0, 0.02^2) in bf16 (Wqkv [d, 3d], Wo [d, d], Wg, Wu [d, F], Wd [F, d]);
+    gains 1 (fp32); dOut ~ N(0, 1) bf16 [B*S, d]. Returns (x, params, dOut), (B, S, H)."""
+    g = _gen(config, 0)
+    tok = torch.randint(0, vocab, (B * S,), generator=g)
+    # embedding row of token v: a normal vector seeded by (config, v), drawn on demand
+    rows = []
+    for v in tok.tolist():
+        gv = torch.Generator()
+        gv.manual_seed(1000 * config + 17 + v)
+        rows.append(torch.randn(d, generator=gv))
+    x = torch.stack(rows).to(torch.bfloat16)
+    p = {"gain1": torch.ones(d), "gain2": torch.ones(d),
+         "Wqkv": normal((d, 3 * d), 0.02, torch.bfloat16, config, 1),
+         "Wo": normal((d, d), 0.02, torch.bfloat16, config, 2),
+         "Wg": normal((d, F), 0.02, torch.bfloat16, config, 3),
+         "Wu": normal((d, F), 0.02, torch.bfloat16, config, 4),
+         "Wd": normal((F, d), 0.02, torch.bfloat16, config, 5)}
+    dOut = normal((B * S, d), 1.0, torch.bfloat16, config, 6)
+    return (x, p, dOut), (B, S, H)
 
 
 def config_inputs(c, **override):
