@@ -119,6 +119,7 @@ bs_status bs_qround(const void* x, bs_dtype xt, int64_t n, bs_fp8 fmt, bs_round 
  *
  *   X [T,d] dt; gain [d] fp32; W [d,n] dt; dY [T,n] dt (dt fp32 or bf16).
  *   T >= 0; d and n multiples of 8 with 8 <= d <= 8192, 8 <= n; K in [1, 4096].
+ *   dY NULL: forward only (u_codes, u_scale, Y, diag); the backward outputs are not written.
  *   pol (host) [n_pol], n_pol in [1, 16].
  *   Y [T,n] fp32 (nullable); u_codes [T,d] uint8; u_scale [1] fp32;
  *   dgain_ref [d], dW_ref [d,n], dX_ref [T,d] fp32; estimates dgain [n_pol][d],
@@ -152,7 +153,9 @@ bs_status bs_rmsnorm_linear_fwd_bwd(const void* X, const float* gain, const void
  * reads O, R the forward's rounding deq(C_O), N a new stochastic rounding at the same
  * scale (trials 1..K, use store_id*256+1). dV does not depend on the policy.
  *
- *   Q, Kt, V, dO [B,H,S,dh] bf16.  dh == 64; S >= 1; B, H >= 1.
+ *   Q, Kt, V [B,H,S,dh] bf16; dO [B,H,S,dh] bf16 or fp32 (dO_type; fp32 enters the
+ *   contractions as three exact bf16 terms). dO NULL: forward and store only (O_out,
+ *   O_codes, O_scale, diag). dh == 64; S >= 1; B, H >= 1.
  *   O [B,H,S,dh] fp32: the original output to store; NULL = computed by the library's
  *   forward (written to O_out if O_out != NULL).
  *   d_pol (host) [n_pol] in {U, R, N}, n_pol in [1, 8]; K in [1, 4096].
@@ -161,8 +164,8 @@ bs_status bs_rmsnorm_linear_fwd_bwd(const void* X, const float* gain, const void
  *   (dK.se must be NULL: BS_EUNSUPPORTED otherwise).
  * ---------------------------------------------------------------------------------- */
 size_t bs_attn_workspace_size(int B, int H, int S, int dh, int n_pol, int K);
-bs_status bs_attn_bwd_policy(const void* Q, const void* Kt, const void* V, const void* dO, int B, int H,
-                             int S, int dh, int causal, float softmax_scale, const float* O, bs_fp8 fmt,
+bs_status bs_attn_bwd_policy(const void* Q, const void* Kt, const void* V, const void* dO, bs_dtype dO_type,
+                             int B, int H, int S, int dh, int causal, float softmax_scale, const float* O, bs_fp8 fmt,
                              bs_round fwd_mode, const bs_read* d_pol, int n_pol, int K, uint64_t seed,
                              uint32_t store_id, float* O_out, uint8_t* O_codes, float* O_scale,
                              float* dQ_ref, float* dK_ref, float* dV, float* D_ref, bs_est dQ, bs_est dK,

@@ -59,7 +59,7 @@ _norm = _sig("bs_rmsnorm_linear_fwd_bwd", _int,
               _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, Est, _vp, _vp, _sz, _vp])
 _attn_ws = _sig("bs_attn_workspace_size", _sz, [_int, _int, _int, _int, _int, _int])
 _attn = _sig("bs_attn_bwd_policy", _int,
-             [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _vp, _int, _int, ctypes.POINTER(_int), _int,
+             [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _int, _f32, _vp, _int, _int, ctypes.POINTER(_int), _int,
               _int, _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, _vp, _vp, _sz, _vp])
 _lin_ws = _sig("bs_linear_bwd_workspace_size", _sz, [_i64, _i64, _i64, _int, _int])
 _lin = _sig("bs_linear_bwd_policy", _int,
@@ -244,7 +244,8 @@ def attn_bwd_policy(Q, Kt, V, dO, *, causal=True, scale=None, O=None, fmt="e4m3"
     ek, ck = _est(len(policies), numel, dev, False)
     if ws is None:
         ws = _workspace(_attn_ws(B, H, S, dh, len(policies), K), dev)
-    _check(_attn(_p(Q), _p(Kt), _p(V), _p(dO), B, H, S, dh, int(causal), c, _p(O), _FMT[fmt], _MODE[fwd_mode], pol,
+    _check(_attn(_p(Q), _p(Kt), _p(V), _p(dO), F32 if dO is not None and dO.dtype == torch.float32 else BF16,
+                 B, H, S, dh, int(causal), c, _p(O), _FMT[fmt], _MODE[fwd_mode], pol,
                  len(policies), K, seed, store_id, _p(out["O"]), _p(out["O_codes"]), _p(out["O_scale"]),
                  _p(out["dQ_ref"]), _p(out["dK_ref"]), _p(out["dV"]), _p(out["D_ref"]), cq, ck, _p(out["diag"]),
                  _p(ws), ws.numel(), _stream()), "bs_attn_bwd_policy")

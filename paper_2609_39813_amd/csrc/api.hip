@@ -2,6 +2,7 @@
 // each call. Every step of the computation runs in the kernels of this library.
 #include "bsp_kernels.h"
 #include "k_norm.h"
+#include "norm_run.h"
 
 using namespace bsp;
 
@@ -73,88 +74,11 @@ bs_status bs_policy_bias_estimate(const float* delta, int K, int64_t m, const fl
 }
 
 // ------------------------------------------------------------------------------------
-// RMSNorm -> FP8 store -> Linear
+// RMSNorm -> FP8 store -> Linear (the runner is in norm_run.hip)
 // ------------------------------------------------------------------------------------
-namespace {
-
-struct NormPlan {
-  bool gain_n = false, gain_r = false, weight_u = false, want_dxr = false;
-  bool weight_n[2] = {false, false};  // use +1 (shared), use +2 (per use)
-  bool gain_se = false;
-};
-
-struct NormWs {
-  float *u, *rstd, *du, *bias_rg, *bias_ng, *se_g, *bias_u, *bias_n[2], *dx_r;
-  u16 *dyT[3], *uvalT, *resU[3], *resN[2], *uval_rows, *wT[3], *dy_rows[3], *w_rows[3];
-  u16 *counts_g, *counts_w;
-  double *partial, *gain_part, *trial_sums;
-};
-
-NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype dt, const NormPlan& p, bool want_y) {
-  NormWs w{};
-  const int64_t Tp = round_up(T > 0 ? T : 1, 64);
-  const int nt = dt == BS_F32 ? 3 : 1;
-  w.u = c.take<float>(T * d);
-  w.rstd = c.take<float>(T > 0 ? T : 1);
-  w.du = c.take<float>(T * d);
-  for (int i = 0; i < nt; ++i) w.dyT[i] = c.take<u16>(n * Tp);
-  w.uvalT = c.take<u16>(d * Tp);
-  if (dt == BS_F32) {
-    for (int i = 0; i < 3; ++i) w.dy_rows[i] = c.take<u16>(T * n);
-    for (int i = 0; i < 3; ++i) w.w_rows[i] = c.take<u16>(d * n);
-  }
-  if (want_y) {
-    w.uval_rows = c.take<u16>(T * d);
-    for (int i = 0; i < nt; ++i) w.wT[i] = c.take<u16>(n * d);
-  }
-  w.bias_rg = c.take<float>(d);
-  w.bias_ng = c.take<float>(d);
-  w.se_g = c.take<float>(d);
-  w.gain_part = c.take<double>(3 * ((T + 63) / 64) * d + 1);
-  if (p.weight_u) {
-    for (int i = 0; i < 3; ++i) w.resU[i] = c.take<u16>(d * Tp);
-    w.bias_u = c.take<float>(d * n);
-  }
-  if (p.weight_n[0] || p.weight_n[1]) {
-    const int ntN = K > 256 ? 2 : 1;
-    for (int i = 0; i < ntN; ++i) w.resN[i] = c.take<u16>(d * Tp);
-    for (int i = 0; i < 2; ++i)
-      if (p.weight_n[i]) w.bias_n[i] = c.take<float>(d * n);
-  }
-  if (p.gain_n || p.weight_n[0]) w.counts_g = c.take<u16>(T * d);
-  if (p.weight_n[1]) w.counts_w = c.take<u16>(T * d);
-  if (p.gain_se) {
-    w.partial = c.take<double>((int64_t)K * ((T + 31) / 32) * d + 1);
-    w.trial_sums = c.take<double>((int64_t)K * d);
-  }
-  if (p.want_dxr) w.dx_r = c.take<float>(T * d);
-  return w;
-}
-
-NormPlan plan_norm(const bs_norm_policy* pol, int n_pol, bool want_gain_se) {
-  NormPlan p;
-  for (int i = 0; i < n_pol; ++i) {
-    if (pol[i].gain_use == BS_READ_N) p.gain_n = true;
-    if (pol[i].gain_use == BS_READ_R) p.gain_r = true;
-    if (pol[i].weight_use == BS_READ_U) p.weight_u = true;
-    if (pol[i].weight_use == BS_READ_N) p.weight_n[pol[i].fresh_shared ? 0 : 1] = true;
-    if (pol[i].norm_input_use == BS_READ_R) p.want_dxr = true;
-  }
-  p.gain_se = want_gain_se && p.gain_n;
-  return p;
-}
-
-}  // namespace
-
 size_t bs_rmsnorm_linear_workspace_size(int64_t T, int64_t d, int64_t n, int n_pol, int K) {
-  // sized for the most demanding policy set (every use read under every letter)
   (void)n_pol;
-  NormPlan p;
-  p.gain_n = p.gain_r = p.weight_u = p.want_dxr = p.gain_se = true;
-  p.weight_n[0] = p.weight_n[1] = true;
-  Carver c;
-  carve_norm(c, T, d, n, K, BS_F32, p, true);
-  return c.used();
+  return norm_ws_size(T, d, n, K);
 }
 
 bs_status bs_rmsnorm_linear_fwd_bwd(const void* X, const float* gain, const void* W, const void* dY, bs_dtype dt,
@@ -163,180 +87,9 @@ bs_status bs_rmsnorm_linear_fwd_bwd(const void* X, const float* gain, const void
                                     float* Y, uint8_t* u_codes, float* u_scale, float* dgain_ref, float* dW_ref,
                                     float* dX_ref, bs_est dgain, bs_est dW, bs_est dX, bs_diag* diag, void* ws,
                                     size_t ws_bytes, void* stream) {
-  hipStream_t st = (hipStream_t)stream;
-  if (!gain || !W || !u_scale || !dgain_ref || !dW_ref || !diag || !pol) return BS_EINVAL;
-  if (T < 0 || (T > 0 && (!X || !dY || !u_codes || !dX_ref))) return BS_EINVAL;
-  if (dt != BS_F32 && dt != BS_BF16) return BS_EDTYPE;
-  if ((fmt != BS_E4M3 && fmt != BS_E5M2) || (fwd_mode != BS_RNE && fwd_mode != BS_SR)) return BS_EINVAL;
-  if (n_pol < 1 || n_pol > 16 || K < 1 || K > 4096 || !(eps >= 0.0f)) return BS_EINVAL;
-  if (d < 8 || d > 8192 || (d & 7) || n < 8 || (n & 7) || T > 0x7FFFFFFF || n > 0x7FFFFFFF) return BS_ESHAPE;
-  for (int i = 0; i < n_pol; ++i) {
-    if (pol[i].gain_use < BS_READ_U || pol[i].gain_use > BS_READ_N || pol[i].weight_use < BS_READ_U ||
-        pol[i].weight_use > BS_READ_N)
-      return BS_EINVAL;
-    if (pol[i].norm_input_use != BS_READ_U && pol[i].norm_input_use != BS_READ_R) return BS_EINVAL;
-    if (pol[i].weight_use == BS_READ_N && dW.se && K > 1) return BS_EUNSUPPORTED;
-  }
-  const NormPlan p = plan_norm(pol, n_pol, dgain.se != nullptr);
-  Carver probe;
-  carve_norm(probe, T, d, n, K, dt, p, Y != nullptr);
-  if (!ws || ((uintptr_t)ws & 255) || ws_bytes < probe.used()) return BS_EWORKSPACE;
-  Carver c(ws, ws_bytes);
-  NormWs w = carve_norm(c, T, d, n, K, dt, p, Y != nullptr);
-
-  const int64_t Tp = round_up(T > 0 ? T : 1, 64);
-  const int nt = dt == BS_F32 ? 3 : 1;
-  const F8 f = f8_format(fmt);
-  const uint32_t base = store_id * 256u;
-  const uint32_t use_g = base + 1, use_w[2] = {base + 1, base + 2};
-
-  // forward: fixed-order RMSNorm with fused amax, then the store
-  BS_TRY(launch_init_diag(diag, st));
-  BS_TRY(launch_rmsnorm_fwd(X, dt, gain, T, d, eps, w.u, w.rstd, diag, st));
-  BS_TRY(launch_store(w.u, BS_F32, T * d, fmt, fwd_mode, seed, 0, base, nullptr, u_codes, u_scale, diag, st, true));
-
-  // du = dY W^T  (A = dY [T, n], B = W [d, n], both n-contiguous)
-  {
-    GemmArgs g{};
-    g.M = (int)T;
-    g.N = (int)d;
-    g.K = (int)n;
-    g.lda = n;
-    g.ldb = n;
-    g.ldc = d;
-    g.alpha = 1.0f;
-    g.C = w.du;
-    if (dt == BS_BF16) {
-      g.A[0] = (const u16*)dY;
-      g.B[0] = (const u16*)W;
-      g.nseg = 1;
-    } else {
-      BS_TRY(launch_planes(dY, dt, T, n, n, false, w.dy_rows, 3, n, 1.0f, st));
-      BS_TRY(launch_planes(W, dt, d, n, n, false, w.w_rows, 3, n, 1.0f, st));
-      gemm_add_products(g, w.dy_rows, 3, w.w_rows, 3);
-    }
-    BS_TRY(launch_gemm(g, st));
-  }
-
-  // weight-use operands in the contraction layout [*, Tp]
-  BS_TRY(launch_planes(dY, dt, T, n, n, true, w.dyT, nt, Tp, 1.0f, st));
-  NormPlaneArgs pa{};
-  pa.u = w.u;
-  pa.codes = u_codes;
-  pa.scale = u_scale;
-  pa.K = K;
-  pa.f = f;
-  pa.T = T;
-  pa.d = d;
-  pa.ldo = Tp;
-  pa.out[0] = w.uvalT;
-  pa.nterms = 1;
-  BS_TRY(launch_norm_planes(NP_VAL, pa, st));
-
-  auto weight_gemm = [&](u16* const* A, int nA, float* C, float alpha, const float* alpha_dev) -> bs_status {
-    GemmArgs g{};
-    g.M = (int)d;
-    g.N = (int)n;
-    g.K = (int)Tp;
-    g.lda = Tp;
-    g.ldb = Tp;
-    g.ldc = n;
-    g.alpha = alpha;
-    g.alpha_dev = alpha_dev;
-    g.C = C;
-    if (!gemm_add_products(g, A, nA, w.dyT, nt)) return BS_EINVAL;
-    return launch_gemm(g, st);
-  };
-  // reference: dW = s val(C_u)^T dY
-  BS_TRY(weight_gemm(&w.uvalT, 1, dW_ref, 1.0f, u_scale));
-
-  // Linear forward Y = s val(C_u) W  (A = val rows [T, d], B = W^T [n, d])
-  if (Y) {
-    BS_TRY(launch_val_rows(u_codes, T * d, fmt, w.uval_rows, st));
-    BS_TRY(launch_planes(W, dt, d, n, n, true, w.wT, nt, d, 1.0f, st));
-    GemmArgs g{};
-    g.M = (int)T;
-    g.N = (int)n;
-    g.K = (int)d;
-    g.lda = d;
-    g.ldb = d;
-    g.ldc = n;
-    g.alpha = 1.0f;
-    g.alpha_dev = u_scale;
-    g.C = Y;
-    gemm_add_products(g, &w.uval_rows, 1, w.wT, nt);
-    BS_TRY(launch_gemm(g, st));
-  }
-
-  // new roundings: up counts over K trials (gain use: use +1; weight use: +1 shared / +2)
-  if (p.gain_n || p.weight_n[0])
-    BS_TRY(launch_fresh_count(w.u, T, d, fmt, u_scale, seed, use_g, K, w.counts_g, w.du,
-                              p.gain_se ? w.partial : nullptr, st));
-  if (p.weight_n[1]) BS_TRY(launch_fresh_count(w.u, T, d, fmt, u_scale, seed, use_w[1], K, w.counts_w, nullptr,
-                                               nullptr, st));
-
-  // gain use: reference and the R / N biases (fp64 column sums)
-  if (dt == BS_F32) {
-    GainArgs<float> ga{(const float*)X, w.rstd, gain, w.u, w.du, u_codes, p.gain_n ? w.counts_g : nullptr, u_scale, K,
-                       p.gain_r ? 1 : 0, f, T, d, w.gain_part};
-    BS_TRY(launch_gain_t(ga, dgain_ref, w.bias_rg, w.bias_ng, st));
-  } else {
-    GainArgs<u16> ga{(const u16*)X, w.rstd, gain, w.u, w.du, u_codes, p.gain_n ? w.counts_g : nullptr, u_scale, K,
-                     p.gain_r ? 1 : 0, f, T, d, w.gain_part};
-    BS_TRY(launch_gain_t(ga, dgain_ref, w.bias_rg, w.bias_ng, st));
-  }
-  if (p.gain_se) BS_TRY(launch_gain_se(w.partial, K, T, d, u_scale, gain, w.trial_sums, w.se_g, st));
-
-  // weight use: U bias = (u - s val)^T dY; N bias = (s / K) (sum of up counts residual)^T dY
-  if (p.weight_u) {
-    pa.out[0] = w.resU[0];
-    pa.out[1] = w.resU[1];
-    pa.out[2] = w.resU[2];
-    pa.nterms = 3;
-    BS_TRY(launch_norm_planes(NP_RESU, pa, st));
-    BS_TRY(weight_gemm(w.resU, 3, w.bias_u, 1.0f, nullptr));
-  }
-  for (int i = 0; i < 2; ++i) {
-    if (!p.weight_n[i]) continue;
-    pa.counts = i == 0 ? w.counts_g : w.counts_w;
-    pa.out[0] = w.resN[0];
-    pa.out[1] = w.resN[1];
-    pa.out[2] = nullptr;
-    pa.nterms = K > 256 ? 2 : 1;
-    BS_TRY(launch_norm_planes(NP_RESN, pa, st));
-    BS_TRY(weight_gemm(w.resN, pa.nterms, w.bias_n[i], 1.0f / (float)K, u_scale));
-  }
-
-  // norm-input use
-  if (dt == BS_F32) {
-    DxArgs<float> da{(const float*)X, w.rstd, gain, w.du, u_codes, u_scale, f, T, d, dX_ref, w.dx_r};
-    BS_TRY(launch_dx_t(da, st));
-  } else {
-    DxArgs<u16> da{(const u16*)X, w.rstd, gain, w.du, u_codes, u_scale, f, T, d, dX_ref, w.dx_r};
-    BS_TRY(launch_dx_t(da, st));
-  }
-
-  // per-policy estimates
-  for (int i = 0; i < n_pol; ++i) {
-    const bs_norm_policy& q = pol[i];
-    const float* bg = q.gain_use == BS_READ_R ? w.bias_rg : (q.gain_use == BS_READ_N ? w.bias_ng : nullptr);
-    const float* sg = (q.gain_use == BS_READ_N && p.gain_se) ? w.se_g : nullptr;
-    BS_TRY(launch_combine(dgain_ref, bg, sg, d, dgain.mean ? dgain.mean + i * d : nullptr,
-                          dgain.bias ? dgain.bias + i * d : nullptr, dgain.se ? dgain.se + i * d : nullptr, st));
-    const float* bw = q.weight_use == BS_READ_U ? w.bias_u
-                      : (q.weight_use == BS_READ_N ? w.bias_n[q.fresh_shared ? 0 : 1] : nullptr);
-    const int64_t dn = d * n;
-    BS_TRY(launch_combine(dW_ref, bw, nullptr, dn, dW.mean ? dW.mean + i * dn : nullptr,
-                          dW.bias ? dW.bias + i * dn : nullptr, dW.se ? dW.se + i * dn : nullptr, st));
-    const int64_t td = T * d;
-    if (q.norm_input_use == BS_READ_R)
-      BS_TRY(launch_combine_alt(dX_ref, w.dx_r, td, dX.mean ? dX.mean + i * td : nullptr,
-                                dX.bias ? dX.bias + i * td : nullptr, dX.se ? dX.se + i * td : nullptr, st));
-    else
-      BS_TRY(launch_combine(dX_ref, nullptr, nullptr, td, dX.mean ? dX.mean + i * td : nullptr,
-                            dX.bias ? dX.bias + i * td : nullptr, dX.se ? dX.se + i * td : nullptr, st));
-  }
-  return BS_OK;
+  NormIO io{X, dt, gain, W, dt, dY, dt, T, d, n, eps, fmt, fwd_mode, pol, n_pol, K, seed, store_id,
+            Y, u_codes, u_scale, dgain_ref, dW_ref, dX_ref, dgain, dW, dX, diag};
+  return norm_run(io, ws, ws_bytes, (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -1,0 +1,122 @@
+// The attention runner: forward (row max / row sum, and O when not handed in), the FP8 store of
+// O, the D variants of every policy, and the two-pass multi-D backward.
+#include "attn_run.h"
+#include "k_attn.h"
+
+#define BS_TRY(x)               \
+  do {                          \
+    const bs_status _s = (x);   \
+    if (_s != BS_OK) return _s; \
+  } while (0)
+
+namespace bsp {
+
+namespace {
+struct AttnWs {
+  float *m, *l, *O, *D_ref, *dD_R, *dD_N, *sd_N;
+};
+AttnWs carve_attn(Carver& c, int64_t rows, int64_t numel, bool need_o, bool need_dref) {
+  AttnWs w{};
+  w.m = c.take<float>(rows);
+  w.l = c.take<float>(rows);
+  if (need_o) w.O = c.take<float>(numel);
+  if (need_dref) w.D_ref = c.take<float>(rows);
+  w.dD_R = c.take<float>(rows);
+  w.dD_N = c.take<float>(rows);
+  w.sd_N = c.take<float>(rows);
+  return w;
+}
+}  // namespace
+
+size_t attn_ws_size(int B, int H, int S, int dh) {
+  if (B < 0 || H < 0 || S < 0 || dh < 0) return 0;
+  Carver c;
+  const int64_t rows = (int64_t)B * H * S;
+  carve_attn(c, rows, rows * dh, true, true);
+  return c.used();
+}
+
+bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
+  const bool fwd_only = !io.dO && !io.dO32;
+  if (!io.Q || !io.Kt || !io.V || !io.O_codes || !io.O_scale || !io.diag) return BS_EINVAL;
+  if (!fwd_only && (!io.dQ_ref || !io.dK_ref || !io.dV || !io.pol)) return BS_EINVAL;
+  if (io.B < 1 || io.H < 1 || io.S < 1 || io.K < 1 || io.K > 4096) return BS_EINVAL;
+  if (!fwd_only && (io.n_pol < 1 || io.n_pol > ATTN_MAX_POL)) return BS_EINVAL;
+  if (!(io.scale > 0.0f) || (io.fmt != BS_E4M3 && io.fmt != BS_E5M2) ||
+      (io.fwd_mode != BS_RNE && io.fwd_mode != BS_SR))
+    return BS_EINVAL;
+  if (io.dh != 64) return BS_ESHAPE;
+  if ((int64_t)io.B * io.H > 65535) return BS_ESHAPE;
+  if (io.dK.se) return BS_EUNSUPPORTED;
+  bool want_r = false, want_n = false;
+  for (int i = 0; i < (fwd_only ? 0 : io.n_pol); ++i) {
+    if (io.pol[i] < BS_READ_U || io.pol[i] > BS_READ_N) return BS_EINVAL;
+    want_r |= io.pol[i] == BS_READ_R;
+    want_n |= io.pol[i] == BS_READ_N;
+  }
+  const int64_t rows = (int64_t)io.B * io.H * io.S, numel = rows * io.dh;
+  const bool need_o = !io.O && !io.O_out;
+  Carver probe;
+  carve_attn(probe, rows, numel, need_o, !io.D_ref);
+  if (!ws || ((uintptr_t)ws & 255) || ws_bytes < probe.used()) return BS_EWORKSPACE;
+  Carver c(ws, ws_bytes);
+  AttnWs w = carve_attn(c, rows, numel, need_o, !io.D_ref);
+  float* dref = io.D_ref ? io.D_ref : w.D_ref;
+
+  // forward: m, l (and O when the caller does not hand it in)
+  AttnArgs fa{(const u16*)io.Q, (const u16*)io.Kt, (const u16*)io.V, io.S, io.causal, io.scale, w.m, w.l, nullptr};
+  const float* Oorig = io.O;
+  if (!io.O) {
+    fa.O_out = io.O_out ? io.O_out : w.O;
+    Oorig = fa.O_out;
+  }
+  BS_TRY(launch_attn_fwd(fa, io.B, io.H, st));
+  if (io.O && io.O_out) {
+    if (hipMemcpyAsync(io.O_out, io.O, sizeof(float) * numel, hipMemcpyDeviceToDevice, st) != hipSuccess)
+      return BS_EHIP;
+  }
+
+  // the store of O (trial 0, use store_id*256)
+  const uint32_t base = io.store_id * 256u;
+  BS_TRY(launch_store(Oorig, BS_F32, numel, io.fmt, io.fwd_mode, io.seed, 0, base, nullptr, io.O_codes, io.O_scale,
+                      io.diag, st, false));
+  if (fwd_only) return BS_OK;
+
+  // D variants
+  AttnDArgs da{Oorig, (const u16*)io.dO, io.dO32, io.O_codes, io.O_scale, rows, f8_format(io.fmt), io.seed, base + 1,
+               io.K, want_n ? 1 : 0, dref, w.dD_R, w.dD_N, w.sd_N};
+  BS_TRY(launch_attn_d(da, st));
+
+  AttnBwdArgs ba{};
+  ba.Q = (const u16*)io.Q;
+  ba.K = (const u16*)io.Kt;
+  ba.V = (const u16*)io.V;
+  ba.dO = (const u16*)io.dO;
+  ba.dO32 = io.dO32;
+  ba.m = w.m;
+  ba.l = w.l;
+  ba.D_ref = dref;
+  ba.dD_R = want_r ? w.dD_R : nullptr;
+  ba.dD_N = want_n ? w.dD_N : nullptr;
+  ba.sd_N = want_n ? w.sd_N : nullptr;
+  ba.S = io.S;
+  ba.causal = io.causal;
+  ba.ntrial = io.K;
+  ba.scale = io.scale;
+  ba.dQ_ref = io.dQ_ref;
+  ba.dK_ref = io.dK_ref;
+  ba.dV = io.dV;
+  ba.n_pol = io.n_pol;
+  for (int i = 0; i < io.n_pol; ++i) {
+    ba.pol[i] = io.pol[i];
+    ba.mean[i] = io.dQ.mean ? io.dQ.mean + i * numel : nullptr;
+    ba.bias[i] = io.dQ.bias ? io.dQ.bias + i * numel : nullptr;
+    ba.se[i] = io.dQ.se ? io.dQ.se + i * numel : nullptr;
+    ba.kmean[i] = io.dK.mean ? io.dK.mean + i * numel : nullptr;
+    ba.kbias[i] = io.dK.bias ? io.dK.bias + i * numel : nullptr;
+  }
+  BS_TRY(launch_attn_bwd(ba, io.B, io.H, st));
+  return BS_OK;
+}
+
+}  // namespace bsp

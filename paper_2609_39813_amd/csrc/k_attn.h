@@ -17,7 +17,8 @@ struct AttnArgs {
 
 struct AttnDArgs {
   const float* O;         // original output, fp32
-  const u16* dO;          // bf16
+  const u16* dO;          // bf16 (used when dO32 is null)
+  const float* dO32;      // nullable: fp32 incoming gradient
   const uint8_t* codes;   // forward's store of O
   const float* scale;     // device s
   int64_t rows;           // B*H*S
@@ -30,6 +31,7 @@ struct AttnDArgs {
 
 struct AttnBwdArgs {
   const u16 *Q, *K, *V, *dO;
+  const float* dO32;  // nullable: fp32 incoming gradient (enters as three exact bf16 terms)
   const float *m, *l, *D_ref, *dD_R, *dD_N, *sd_N;  // dD_R / dD_N / sd_N nullable
   int S, causal, ntrial;  // ntrial: K, the number of new roundings
   float scale;

@@ -49,6 +49,50 @@ __device__ __forceinline__ void load_tile_t(u16* T, const u16* __restrict__ g, i
   }
 }
 
+// rows [r0, r0 + 64) of a [S, 64] fp32 matrix as three exact bf16 terms (row-major tiles)
+__device__ __forceinline__ void load_tile3(u16* const* T, const float* __restrict__ g, int r0, int S) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (tid >> 3) + 32 * i, c = (tid & 7) * 8;
+    float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (r0 + r < S) {
+      const float4 a = *(const float4*)(g + (int64_t)(r0 + r) * AT + c);
+      const float4 b = *(const float4*)(g + (int64_t)(r0 + r) * AT + c + 4);
+      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    }
+    u16 o[3][8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) split3(v[q], o[0][q], o[1][q], o[2][q]);
+#pragma unroll
+    for (int p = 0; p < 3; ++p) *(uint4*)(T[p] + sw(r, c)) = *(const uint4*)o[p];
+  }
+}
+
+// the same rows transposed: T_p[c][r]
+__device__ __forceinline__ void load_tile3_t(u16* const* T, const float* __restrict__ g, int r0, int S) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (tid >> 3) + 32 * i, c = (tid & 7) * 8;
+    float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (r0 + r < S) {
+      const float4 a = *(const float4*)(g + (int64_t)(r0 + r) * AT + c);
+      const float4 b = *(const float4*)(g + (int64_t)(r0 + r) * AT + c + 4);
+      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      u16 o0, o1, o2;
+      split3(v[q], o0, o1, o2);
+      const int idx = sw(c + q, r);
+      T[0][idx] = o0;
+      T[1][idx] = o1;
+      T[2][idx] = o2;
+    }
+  }
+}
+
 __device__ __forceinline__ void put3(u16* T0, u16* T1, u16* T2, int row, int col, float v) {
   u16 a, b, c;
   split3(v, a, b, c);
@@ -174,11 +218,19 @@ __global__ __launch_bounds__(256) void attn_d_kernel(AttnDArgs a) {
   double w[4] = {0.0, 0.0, 0.0, 0.0};
   if (ok) {
     const float4 o4 = *(const float4*)(a.O + e0);
-    const uint2 d2 = *(const uint2*)(a.dO + e0);
     const uint32_t c4 = *(const uint32_t*)(a.codes + e0);
     const float ov[4] = {o4.x, o4.y, o4.z, o4.w};
-    const float dv[4] = {bf16_to_f32((u16)(d2.x & 0xFFFF)), bf16_to_f32((u16)(d2.x >> 16)),
-                         bf16_to_f32((u16)(d2.y & 0xFFFF)), bf16_to_f32((u16)(d2.y >> 16))};
+    float dv[4];
+    if (a.dO32) {
+      const float4 g4 = *(const float4*)(a.dO32 + e0);
+      dv[0] = g4.x; dv[1] = g4.y; dv[2] = g4.z; dv[3] = g4.w;
+    } else {
+      const uint2 d2 = *(const uint2*)(a.dO + e0);
+      dv[0] = bf16_to_f32((u16)(d2.x & 0xFFFF));
+      dv[1] = bf16_to_f32((u16)(d2.x >> 16));
+      dv[2] = bf16_to_f32((u16)(d2.y & 0xFFFF));
+      dv[3] = bf16_to_f32((u16)(d2.y >> 16));
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const double o = ov[q], g = dv[q];
@@ -231,15 +283,21 @@ __global__ __launch_bounds__(256) void attn_d_kernel(AttnDArgs a) {
 // backward, query-block-major: dQ = c dS K and G = P K; per-policy dQ estimates
 //   bias_v = -c dD_v G (row-scaled), se_N = c |G| sd_N / sqrt(K).
 // ------------------------------------------------------------------------------------
+template <int NDO>
 __global__ __launch_bounds__(256) void attn_bwd_q_kernel(AttnBwdArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 sQ[AT * AT], sdO[AT * AT], sK[AT * AT], sV[AT * AT], sKt[AT * AT],
+  __shared__ __attribute__((aligned(16))) u16 sQ[AT * AT], sdO[NDO][AT * AT], sK[AT * AT], sV[AT * AT], sKt[AT * AT],
       sP[3][AT * AT], sdS[3][AT * AT];
   const int qb = blockIdx.x, bh = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int q0 = qb * AT;
   const int64_t hb = (int64_t)bh * a.S * AT, rb = (int64_t)bh * a.S;
   load_tile(sQ, a.Q + hb, q0, a.S);
-  load_tile(sdO, a.dO + hb, q0, a.S);
+  if (NDO == 1) {
+    load_tile(sdO[0], a.dO + hb, q0, a.S);
+  } else {
+    u16* const t3[3] = {sdO[0], sdO[NDO > 1 ? 1 : 0], sdO[NDO > 2 ? 2 : 0]};
+    load_tile3(t3, a.dO32 + hb, q0, a.S);
+  }
   float mr[4], il[4], dr[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
@@ -264,11 +322,13 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(AttnBwdArgs a) {
     for (int t = 0; t < 4; ++t) s[t] = dp[t] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < AT; kk += 32) {
-      const bf16x8 fq = frag(sQ, 16 * w, kk, lane), fo = frag(sdO, 16 * w, kk, lane);
+      const bf16x8 fq = frag(sQ, 16 * w, kk, lane);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
+        const bf16x8 fv = frag(sV, 16 * t, kk, lane);
         s[t] = mfma(fq, frag(sK, 16 * t, kk, lane), s[t]);
-        dp[t] = mfma(fo, frag(sV, 16 * t, kk, lane), dp[t]);
+#pragma unroll
+        for (int i = 0; i < NDO; ++i) dp[t] = mfma(frag(sdO[i], 16 * w, kk, lane), fv, dp[t]);
       }
     }
 #pragma unroll
@@ -329,9 +389,10 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(AttnBwdArgs a) {
 // dK_v = -c P^T (dD_v * Q) for v in {R, N}, from S^T = K Q^T so that each wave reads only
 // its own key rows of the P^T / dS^T tiles.
 // ------------------------------------------------------------------------------------
+template <int NDO>
 __global__ __launch_bounds__(256) void attn_bwd_k_kernel(AttnBwdArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 sK[AT * AT], sV[AT * AT], sQ[AT * AT], sQt[AT * AT], sdO[AT * AT],
-      sdOt[AT * AT], sPt[3][AT * AT], sdSt[3][AT * AT];
+  __shared__ __attribute__((aligned(16))) u16 sK[AT * AT], sV[AT * AT], sQ[AT * AT], sQt[AT * AT], sdO[NDO][AT * AT],
+      sdOt[NDO][AT * AT], sPt[3][AT * AT], sdSt[3][AT * AT];
   __shared__ float rowm[AT], rowil[AT], rowd[AT], rowdr[AT], rowdn[AT];
   const int kb = blockIdx.x, bh = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -348,8 +409,15 @@ __global__ __launch_bounds__(256) void attn_bwd_k_kernel(AttnBwdArgs a) {
     __syncthreads();
     load_tile(sQ, a.Q + hb, q0, a.S);
     load_tile_t(sQt, a.Q + hb, q0, a.S);
-    load_tile(sdO, a.dO + hb, q0, a.S);
-    load_tile_t(sdOt, a.dO + hb, q0, a.S);
+    if (NDO == 1) {
+      load_tile(sdO[0], a.dO + hb, q0, a.S);
+      load_tile_t(sdOt[0], a.dO + hb, q0, a.S);
+    } else {
+      u16* const t3[3] = {sdO[0], sdO[NDO > 1 ? 1 : 0], sdO[NDO > 2 ? 2 : 0]};
+      u16* const t3t[3] = {sdOt[0], sdOt[NDO > 1 ? 1 : 0], sdOt[NDO > 2 ? 2 : 0]};
+      load_tile3(t3, a.dO32 + hb, q0, a.S);
+      load_tile3_t(t3t, a.dO32 + hb, q0, a.S);
+    }
     if (threadIdx.x < AT) {
       const int q = q0 + threadIdx.x;
       const bool ok = q < a.S;
@@ -370,7 +438,8 @@ __global__ __launch_bounds__(256) void attn_bwd_k_kernel(AttnBwdArgs a) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         s[t] = mfma(fk, frag(sQ, 16 * t, kk, lane), s[t]);
-        dp[t] = mfma(fv, frag(sdO, 16 * t, kk, lane), dp[t]);
+#pragma unroll
+        for (int i = 0; i < NDO; ++i) dp[t] = mfma(fv, frag(sdO[i], 16 * t, kk, lane), dp[t]);
       }
     }
     float pv[4][4];
@@ -395,7 +464,9 @@ __global__ __launch_bounds__(256) void attn_bwd_k_kernel(AttnBwdArgs a) {
         const bf16x8 fp = frag(sPt[tm], 16 * w, kk, lane), fs = frag(sdSt[tm], 16 * w, kk, lane);
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          av[t] = mfma(fp, frag(sdOt, 16 * t, kk, lane), av[t]);
+#pragma unroll
+          for (int i = 0; i < NDO; ++i)
+            if (tm + i <= 2) av[t] = mfma(fp, frag(sdOt[i], 16 * t, kk, lane), av[t]);
           ak[t] = mfma(fs, frag(sQt, 16 * t, kk, lane), ak[t]);
         }
       }
@@ -474,8 +545,13 @@ bs_status launch_attn_d(const AttnDArgs& a, hipStream_t st) {
 bs_status launch_attn_bwd(const AttnBwdArgs& a, int B, int H, hipStream_t st) {
   dim3 grid((unsigned)((a.S + AT - 1) / AT), (unsigned)(B * H));
   ProfScope prof("attn_bwd", st);
-  attn_bwd_k_kernel<<<grid, 256, 0, st>>>(a);
-  attn_bwd_q_kernel<<<grid, 256, 0, st>>>(a);
+  if (a.dO32) {
+    attn_bwd_k_kernel<3><<<grid, 256, 0, st>>>(a);
+    attn_bwd_q_kernel<3><<<grid, 256, 0, st>>>(a);
+  } else {
+    attn_bwd_k_kernel<1><<<grid, 256, 0, st>>>(a);
+    attn_bwd_q_kernel<1><<<grid, 256, 0, st>>>(a);
+  }
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

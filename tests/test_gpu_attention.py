@@ -70,6 +70,16 @@ def test_ragged_given_output(lib, causal, S):
     compare(out, ref, ("U", "R", "N"))
 
 
+def test_fp32_incoming_gradient(lib):
+    Q, K, V, _ = inputs(1, 2, 130, seed=21)
+    dO = synth.normal((1, 2, 130, 64), 1.0, torch.float32, 121, 7)      # fp32, not bf16-exact
+    ref = attention.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.numpy(), causal=True,
+                          fmt=fp8.E4M3, fwd_mode=oq.SR, policies=("U", "R", "N"), K=6, seed=8, store_id=1)
+    out = run(lib, Q, K, V, dO, O=ref["O32"], Kt=6, seed=8)
+    assert np.array_equal(out["O_codes"].cpu().numpy(), ref["codes"])
+    compare(out, ref, ("U", "R", "N"))
+
+
 def test_rne_store_and_policy_order(lib):
     Q, K, V, dO = inputs(2, 1, 96, seed=7)
     pols = ("N", "U", "R", "N")
