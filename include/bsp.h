@@ -218,6 +218,74 @@ bs_status bs_gemm_bf16_nt(const void* A, int64_t lda, const void* B, int64_t ldb
                           int64_t M, int64_t N, int64_t K, float alpha, int accumulate, void* stream);
 
 /* ------------------------------------------------------------------------------------
+ * bs_decoder_layer_policy -- one pre-norm decoder layer (RMSNorm, causal multi-head attention
+ * with dh = 64, SwiGLU MLP, no biases; the block of App. D.1) with four FP8 stores, and the
+ * per-use check of every store (Sec. 4.1): each use is evaluated at its own operator with the
+ * incoming gradient the straight-through reference backward delivers there.
+ *
+ *   u1 = gain1*RMSNorm(x)  [store 0]  QKV = deq(C_u1) Wqkv;  Q, K, V = bf16(QKV) per head
+ *   O = softmax(c Q K^T) V [store 1]  h = x + deq(C_O) Wo
+ *   u2 = gain2*RMSNorm(h)  [store 2]  [g | hh] = deq(C_u2) [Wg | Wu];  a = silu(g) * hh
+ *   a                      [store 3]  out = h + deq(C_a) Wd
+ *
+ * Every store rounds with fwd_mode at trial 0, use store*256. Uses and their new roundings:
+ *   store 0 and 2 (normalization stores): gain use (+1), weight use (+2), normalization-input
+ *   use (U or R only), as bs_rmsnorm_linear_fwd_bwd; store 1: D use (+1, head-major element
+ *   order) as bs_attn_bwd_policy with the fp32 incoming gradient, weight use of Wo (+2,
+ *   token-major order); store 3: weight use of Wd (+2).
+ *
+ *   x [T, d] bf16 with T = B*S (row t = b*S + s); dOut [T, d] bf16; d = 64*H, d and F
+ *   multiples of 8; weights bf16 row-major Wqkv [d, 3d], Wo [d, d], Wg [d, F], Wu [d, F],
+ *   Wd [F, d]; gains fp32 [d]. K in [1, 4096].
+ *   fixed (nullable): the realized forward to hold fixed instead of computing it (all of
+ *   its pointers set): Q, K, V bf16 [B, H, S, 64], O fp32 [B, H, S, 64], h fp32 [T, d],
+ *   gh = [g | hh] fp32 [T, 2F], a fp32 [T, F].
+ *   grads: reference gradients (each nullable): dx [T,d], dgain1 [d], dWqkv [d,3d], dWo [d,d],
+ *   dgain2 [d], dWg [d,F], dWu [d,F], dWd [F,d].
+ *   stores (each nullable): codes of u1 [T,d], O [B,H,S,64], u2 [T,d], a [T,F]; scales [4].
+ *   table [BS_LAYER_ROWS][3 letters U,R,N][3] fp64: sum of squared bias, sum of squared
+ *   reference, sum of squared se of the row's gradient under the letter; NaN where the build
+ *   has no estimate (N at a normalization-input use, se of a weight use or of dK under N).
+ *   Rows: 0 u1 gain, 1 u1 weight (dWqkv), 2 u1 norm-input (dX), 3 O D (dQ), 4 O D (dK),
+ *   5 O weight (dWo), 6 u2 gain, 7 u2 weight ([dWg | dWu]), 8 u2 norm-input, 9 a weight (dWd).
+ *   diags [4] (nullable; one per store). Every pointer is device memory (the structs themselves
+ *   are host memory); outputs are owned by the caller.
+ *   ws: device workspace, 256-byte aligned, of bs_decoder_layer_workspace_size(B,S,d,H,F,K) bytes
+ *   (0 for shapes the call rejects).
+ *   Returns BS_EINVAL for a null required pointer, K outside [1, 4096], eps < 0, an unknown
+ *   format or mode, or a partly set `fixed`; BS_ESHAPE unless d = 64*H <= 8192, F a multiple of
+ *   8 and B*H <= 65535; BS_EWORKSPACE for a short or misaligned workspace; BS_EHIP on a failed
+ *   launch. Work is enqueued on `stream` (nullable: the null stream) and is asynchronous.
+ * ---------------------------------------------------------------------------------- */
+#define BS_LAYER_ROWS 10
+typedef struct {
+  const float* gain1;
+  const void* Wqkv;
+  const void* Wo;
+  const float* gain2;
+  const void* Wg;
+  const void* Wu;
+  const void* Wd;
+} bs_layer_weights;
+typedef struct {
+  const void *Q, *K, *V;
+  const float *O, *h, *gh, *a;
+} bs_layer_forward;
+typedef struct {
+  float *dx, *dgain1, *dWqkv, *dWo, *dgain2, *dWg, *dWu, *dWd;
+} bs_layer_grads;
+typedef struct {
+  uint8_t *u1, *O, *u2, *a;
+  float* scales;
+} bs_layer_stores;
+
+size_t bs_decoder_layer_workspace_size(int B, int S, int d, int H, int F, int K);
+bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* w, const void* dOut, int B, int S, int d,
+                                  int H, int F, float eps, bs_fp8 fmt, bs_round fwd_mode, int K, uint64_t seed,
+                                  const bs_layer_forward* fixed, bs_layer_grads grads, bs_layer_stores stores,
+                                  double* table, bs_diag* diags, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
  * Kernel timing instrumentation (host calls; for benchmarks and profiling).
  *   bs_profile_enable(1) clears earlier records and starts recording a pair of HIP
  *   events on the launch stream around each launch of the instrumented kernels

@@ -66,6 +66,28 @@ _lin = _sig("bs_linear_bwd_policy", _int,
             [_vp, _vp, _vp, _int, _i64, _i64, _i64, _int, ctypes.POINTER(_int), _int, _int, _u64, _u32, _vp, _vp,
              Est, Est, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp])
 
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(k, _vp) for k in ("gain1", "Wqkv", "Wo", "gain2", "Wg", "Wu", "Wd")]
+
+
+class LayerForward(ctypes.Structure):
+    _fields_ = [(k, _vp) for k in ("Q", "K", "V", "O", "h", "gh", "a")]
+
+
+class LayerGrads(ctypes.Structure):
+    _fields_ = [(k, _vp) for k in ("dx", "dgain1", "dWqkv", "dWo", "dgain2", "dWg", "dWu", "dWd")]
+
+
+class LayerStores(ctypes.Structure):
+    _fields_ = [(k, _vp) for k in ("u1", "O", "u2", "a", "scales")]
+
+
+_layer_ws = _sig("bs_decoder_layer_workspace_size", _sz, [_int] * 6)
+_layer = _sig("bs_decoder_layer_policy", _int,
+              [_vp, ctypes.POINTER(LayerWeights), _vp, _int, _int, _int, _int, _int, _f32, _int, _int, _int, _u64,
+               ctypes.POINTER(LayerForward), LayerGrads, LayerStores, _vp, _vp, _vp, _sz, _vp])
+
 _prof_enable = _sig("bs_profile_enable", _int, [_int])
 _prof_read = _sig("bs_profile_read", _int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_int)])
 
@@ -84,7 +106,8 @@ def profile_read(kernel=None):
 
 EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
             "bs_policy_bias_estimate", "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
-            "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy"]
+            "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
+            "bs_decoder_layer_workspace_size", "bs_decoder_layer_policy", "bs_profile_enable", "bs_profile_read"]
 
 
 class BspError(RuntimeError):
@@ -283,3 +306,59 @@ def linear_bwd_policy(X, W, dY, *, fmt="e5m2", sharings=("shared", "per_use"), K
 
 def linear_bwd_workspace(M, k, n, n_pol, K, device):
     return _workspace(_lin_ws(M, k, n, n_pol, K), device)
+
+
+LAYER_ROWS = (("u1", "gain", "dgain"), ("u1", "weight", "dW"), ("u1", "norm_input", "dX"), ("O", "D", "dQ"),
+              ("O", "D", "dK"), ("O", "weight", "dW"), ("u2", "gain", "dgain"), ("u2", "weight", "dW"),
+              ("u2", "norm_input", "dX"), ("a", "weight", "dW"))
+
+
+def decoder_layer_workspace(B, S, d, H, F, K, device):
+    n = _layer_ws(B, S, d, H, F, K)
+    if n == 0:
+        raise BspError(3, "bs_decoder_layer_workspace_size")
+    return _workspace(n, device)
+
+
+def decoder_layer_policy(x, p, dOut, *, B, S, H, eps=1e-5, fmt="e4m3", fwd_mode="rne", K=16, seed=0, fixed=None,
+                         ws=None):
+    """One decoder layer with four FP8 stores and the per-use check of every store
+    (bs_decoder_layer_policy). p: gain1, gain2 fp32 [d]; Wqkv, Wo, Wg, Wu, Wd bf16. fixed:
+    None, or the realized forward {Q, K, V (bf16 [B,H,S,64]), O ([B,H,S,64]), h, gh ([T,2F]),
+    a ([T,F]) fp32}. Returns the table as {(store, use, grad, letter): (bias^2, ref^2, se^2)}
+    plus reference gradients, store codes and scales."""
+    T, d = x.shape
+    F = p["Wg"].shape[1]
+    dev = x.device
+    ts = [x, dOut] + [p[k] for k in ("gain1", "Wqkv", "Wo", "gain2", "Wg", "Wu", "Wd")]
+    if fixed is not None:
+        ts += [fixed[k] for k in ("Q", "K", "V", "O", "h", "gh", "a")]
+    _dev_check(*ts)
+    wts = LayerWeights(*[p[k].data_ptr() for k in ("gain1", "Wqkv", "Wo", "gain2", "Wg", "Wu", "Wd")])
+    fx = None
+    if fixed is not None:
+        fx = ctypes.byref(LayerForward(*[fixed[k].data_ptr() for k in ("Q", "K", "V", "O", "h", "gh", "a")]))
+    e = lambda *shape: torch.empty(*shape, dtype=torch.float32, device=dev)
+    out = {"dx": e(T, d), "dgain1": e(d), "dWqkv": e(d, 3 * d), "dWo": e(d, d), "dgain2": e(d), "dWg": e(d, F),
+           "dWu": e(d, F), "dWd": e(F, d),
+           "codes_u1": torch.empty(T, d, dtype=torch.uint8, device=dev),
+           "codes_O": torch.empty(B, H, S, d // H, dtype=torch.uint8, device=dev),
+           "codes_u2": torch.empty(T, d, dtype=torch.uint8, device=dev),
+           "codes_a": torch.empty(T, F, dtype=torch.uint8, device=dev),
+           "scales": e(4), "diags": torch.zeros(4, 16, dtype=torch.uint8, device=dev),
+           "table_raw": torch.empty(len(LAYER_ROWS), 3, 3, dtype=torch.float64, device=dev)}
+    grads = LayerGrads(*[out[k].data_ptr() for k in ("dx", "dgain1", "dWqkv", "dWo", "dgain2", "dWg", "dWu", "dWd")])
+    stores = LayerStores(*[out[k].data_ptr() for k in ("codes_u1", "codes_O", "codes_u2", "codes_a", "scales")])
+    if ws is None:
+        ws = decoder_layer_workspace(B, S, d, H, F, K, dev)
+    _check(_layer(_p(x), ctypes.byref(wts), _p(dOut), B, S, d, H, F, eps, _FMT[fmt], _MODE[fwd_mode], K, seed, fx,
+                  grads, stores, _p(out["table_raw"]), _p(out["diags"]), _p(ws), ws.numel(), _stream()),
+           "bs_decoder_layer_policy")
+    return out
+
+
+def layer_table(raw):
+    """{(store, use, grad, letter): (bias^2, ref^2, se^2)} from the [rows][3][3] table (host)."""
+    raw = raw.cpu().numpy() if hasattr(raw, "cpu") else raw
+    return {LAYER_ROWS[r] + (l,): tuple(float(v) for v in raw[r, i]) for r in range(len(LAYER_ROWS))
+            for i, l in enumerate("URN")}

@@ -1,0 +1,23 @@
+// Launchers of the decoder layer's elementwise kernels.
+#pragma once
+#include "bsp_kernels.h"
+
+namespace bsp {
+
+bs_status launch_qkv_heads(const float* qkv, int B, int S, int H, int dh, u16* Q, u16* K, u16* V, hipStream_t st);
+bs_status launch_heads_tokens_f32(const float* in, float* out, int B, int S, int H, int dh, bool to_tokens,
+                                  hipStream_t st);
+bs_status launch_heads_tokens_u8(const uint8_t* in, uint8_t* out, int B, int S, int H, int dh, hipStream_t st);
+bs_status launch_dqkv_tokens(const float* dQ, const float* dK, const float* dV, float* out, int B, int S, int H,
+                             int dh, hipStream_t st);
+bs_status launch_bf16_to_f32(const u16* in, float* out, int64_t n, hipStream_t st);
+bs_status launch_concat_cols(const u16* A, const u16* B, u16* out, int64_t rows, int64_t c1, int64_t c2,
+                             hipStream_t st);
+bs_status launch_split_cols(const float* in, float* A, float* B, int64_t rows, int64_t c, hipStream_t st);
+bs_status launch_swiglu_fwd(const float* gh, float* a, int64_t T, int64_t F, hipStream_t st);
+bs_status launch_swiglu_bwd(const float* da, const float* gh, float* dgh, int64_t T, int64_t F, hipStream_t st);
+bs_status launch_add(const void* a, bs_dtype at, const float* b, float* out, int64_t n, hipStream_t st);
+bs_status launch_sumsq(const float* x, int64_t n, double* part, double* out, hipStream_t st);
+bs_status launch_set_f64(double* p, double v, hipStream_t st);
+
+}  // namespace bsp

@@ -1,0 +1,219 @@
+// Elementwise kernels of the decoder layer: head / token permutations, SwiGLU forward and
+// backward, residual adds, bf16 concatenation, and fixed-order sums of squares.
+#include "k_layer.h"
+
+namespace bsp {
+
+static unsigned blocks_for(int64_t n, int64_t cap = 16384) {
+  const int64_t want = (n + 255) / 256;
+  return (unsigned)(want < 1 ? 1 : (want < cap ? want : cap));
+}
+#define GRID_LOOP(i, n) \
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < (n); i += (int64_t)gridDim.x * blockDim.x)
+
+// QKV [T][3d] fp32 -> Q, K, V [B,H,S,dh] bf16 (round to nearest even)
+__global__ void qkv_heads_kernel(const float* __restrict__ qkv, int B, int S, int H, int dh, u16* __restrict__ Q,
+                                 u16* __restrict__ K, u16* __restrict__ V) {
+  const int d = H * dh;
+  const int64_t n = (int64_t)B * S * 3 * d;
+  GRID_LOOP(i, n) {
+    const int64_t t = i / (3 * d);
+    const int col = (int)(i - t * 3 * d);
+    const int which = col / d, hc = col - which * d, h = hc / dh, c = hc - h * dh;
+    const int b = (int)(t / S), s = (int)(t - (int64_t)b * S);
+    const int64_t o = (((int64_t)b * H + h) * S + s) * dh + c;
+    (which == 0 ? Q : (which == 1 ? K : V))[o] = bf16_bits(qkv[i]);
+  }
+}
+
+// [B,H,S,dh] <-> [T][H*dh] (row t = b*S + s); element size 4 (fp32) or 1 (codes)
+template <typename E>
+__global__ void heads_tokens_kernel(const E* __restrict__ in, E* __restrict__ out, int B, int S, int H, int dh,
+                                    int to_tokens) {
+  const int64_t n = (int64_t)B * H * S * dh;
+  GRID_LOOP(i, n) {
+    const int c = (int)(i % dh);
+    const int64_t r = i / dh;
+    const int s = (int)(r % S);
+    const int64_t bh = r / S;
+    const int h = (int)(bh % H), b = (int)(bh / H);
+    const int64_t tok = ((int64_t)b * S + s) * (H * dh) + h * dh + c;
+    if (to_tokens)
+      out[tok] = in[i];
+    else
+      out[i] = in[tok];
+  }
+}
+
+// dQ, dK, dV [B,H,S,dh] -> dQKV [T][3d]
+__global__ void dqkv_tokens_kernel(const float* __restrict__ dQ, const float* __restrict__ dK,
+                                   const float* __restrict__ dV, float* __restrict__ out, int B, int S, int H, int dh) {
+  const int d = H * dh;
+  const int64_t n = (int64_t)B * S * 3 * d;
+  GRID_LOOP(i, n) {
+    const int64_t t = i / (3 * d);
+    const int col = (int)(i - t * 3 * d);
+    const int which = col / d, hc = col - which * d, h = hc / dh, c = hc - h * dh;
+    const int b = (int)(t / S), s = (int)(t - (int64_t)b * S);
+    const int64_t o = (((int64_t)b * H + h) * S + s) * dh + c;
+    out[i] = (which == 0 ? dQ : (which == 1 ? dK : dV))[o];
+  }
+}
+
+__global__ void bf16_to_f32_kernel(const u16* __restrict__ in, float* __restrict__ out, int64_t n) {
+  GRID_LOOP(i, n) out[i] = bf16_to_f32(in[i]);
+}
+
+// out[r][0:c1] = A[r][:], out[r][c1:c1+c2] = B[r][:]
+__global__ void concat_cols_kernel(const u16* __restrict__ A, const u16* __restrict__ Bm, u16* __restrict__ out,
+                                   int64_t rows, int64_t c1, int64_t c2) {
+  const int64_t w = c1 + c2, n = rows * w;
+  GRID_LOOP(i, n) {
+    const int64_t r = i / w, c = i - r * w;
+    out[i] = c < c1 ? A[r * c1 + c] : Bm[r * c2 + (c - c1)];
+  }
+}
+
+// A[r][:] = in[r][0:c], B[r][:] = in[r][c:2c] (either output nullable)
+__global__ void split_cols_kernel(const float* __restrict__ in, float* __restrict__ A, float* __restrict__ Bm,
+                                  int64_t rows, int64_t c) {
+  const int64_t n = rows * 2 * c;
+  GRID_LOOP(i, n) {
+    const int64_t r = i / (2 * c), j = i - r * 2 * c;
+    if (j < c) {
+      if (A) A[r * c + j] = in[i];
+    } else if (Bm) {
+      Bm[r * c + j - c] = in[i];
+    }
+  }
+}
+
+// a = silu(g) * hh with gh = [g | hh] [T][2F]
+__global__ void swiglu_fwd_kernel(const float* __restrict__ gh, float* __restrict__ a, int64_t T, int64_t F) {
+  const int64_t n = T * F;
+  GRID_LOOP(i, n) {
+    const int64_t t = i / F, j = i - t * F;
+    const float g = gh[t * 2 * F + j], hh = gh[t * 2 * F + F + j];
+    a[i] = g / (1.0f + expf(-g)) * hh;
+  }
+}
+
+// dg = da hh silu'(g), dhh = da silu(g), into [T][2F] (fp64 arithmetic, fp32 result)
+__global__ void swiglu_bwd_kernel(const float* __restrict__ da, const float* __restrict__ gh, float* __restrict__ dgh,
+                                  int64_t T, int64_t F) {
+  const int64_t n = T * F;
+  GRID_LOOP(i, n) {
+    const int64_t t = i / F, j = i - t * F;
+    const double g = gh[t * 2 * F + j], hh = gh[t * 2 * F + F + j], d = da[i];
+    const double sg = 1.0 / (1.0 + exp(-g));
+    dgh[t * 2 * F + j] = (float)(d * hh * sg * (1.0 + g * (1.0 - sg)));
+    dgh[t * 2 * F + F + j] = (float)(d * g * sg);
+  }
+}
+
+// out = a (bf16 or fp32) + b (fp32)
+template <typename TA>
+__global__ void add_kernel(const TA* __restrict__ a, const float* __restrict__ b, float* __restrict__ out, int64_t n) {
+  GRID_LOOP(i, n) out[i] = load_f32(a, i) + b[i];
+}
+
+// fixed-order sum of squares (fp64): block partials, then one thread in block order
+__global__ __launch_bounds__(256) void sumsq_kernel(const float* __restrict__ x, int64_t n, double* __restrict__ part) {
+  double s = 0.0;
+  GRID_LOOP(i, n) {
+    const double v = x[i];
+    s += v * v;
+  }
+  __shared__ double red[4];
+  s = wave_sum_f64(s);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) part[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+__global__ void sumsq_final_kernel(const double* __restrict__ part, int nblk, double* __restrict__ out) {
+  if (threadIdx.x != 0) return;
+  double s = 0.0;
+  for (int b = 0; b < nblk; ++b) s += part[b];
+  *out = s;
+}
+__global__ void set_f64_kernel(double* p, double v) {
+  if (threadIdx.x == 0) *p = v;
+}
+
+// ------------------------------------------------------------------------------------
+bs_status launch_qkv_heads(const float* qkv, int B, int S, int H, int dh, u16* Q, u16* K, u16* V, hipStream_t st) {
+  qkv_heads_kernel<<<blocks_for((int64_t)B * S * 3 * H * dh), 256, 0, st>>>(qkv, B, S, H, dh, Q, K, V);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_heads_tokens_f32(const float* in, float* out, int B, int S, int H, int dh, bool to_tokens,
+                                  hipStream_t st) {
+  heads_tokens_kernel<float><<<blocks_for((int64_t)B * S * H * dh), 256, 0, st>>>(in, out, B, S, H, dh, to_tokens);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_heads_tokens_u8(const uint8_t* in, uint8_t* out, int B, int S, int H, int dh, hipStream_t st) {
+  heads_tokens_kernel<uint8_t><<<blocks_for((int64_t)B * S * H * dh), 256, 0, st>>>(in, out, B, S, H, dh, 1);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_dqkv_tokens(const float* dQ, const float* dK, const float* dV, float* out, int B, int S, int H,
+                             int dh, hipStream_t st) {
+  dqkv_tokens_kernel<<<blocks_for((int64_t)B * S * 3 * H * dh), 256, 0, st>>>(dQ, dK, dV, out, B, S, H, dh);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_bf16_to_f32(const u16* in, float* out, int64_t n, hipStream_t st) {
+  if (n > 0) bf16_to_f32_kernel<<<blocks_for(n), 256, 0, st>>>(in, out, n);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_concat_cols(const u16* A, const u16* B, u16* out, int64_t rows, int64_t c1, int64_t c2,
+                             hipStream_t st) {
+  concat_cols_kernel<<<blocks_for(rows * (c1 + c2)), 256, 0, st>>>(A, B, out, rows, c1, c2);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_split_cols(const float* in, float* A, float* B, int64_t rows, int64_t c, hipStream_t st) {
+  if (rows <= 0 || c <= 0 || (!A && !B)) return BS_OK;
+  split_cols_kernel<<<blocks_for(rows * 2 * c), 256, 0, st>>>(in, A, B, rows, c);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_swiglu_fwd(const float* gh, float* a, int64_t T, int64_t F, hipStream_t st) {
+  if (T > 0) swiglu_fwd_kernel<<<blocks_for(T * F), 256, 0, st>>>(gh, a, T, F);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_swiglu_bwd(const float* da, const float* gh, float* dgh, int64_t T, int64_t F, hipStream_t st) {
+  if (T > 0) swiglu_bwd_kernel<<<blocks_for(T * F), 256, 0, st>>>(da, gh, dgh, T, F);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_add(const void* a, bs_dtype at, const float* b, float* out, int64_t n, hipStream_t st) {
+  if (n <= 0) return BS_OK;
+  if (at == BS_F32)
+    add_kernel<float><<<blocks_for(n), 256, 0, st>>>((const float*)a, b, out, n);
+  else
+    add_kernel<u16><<<blocks_for(n), 256, 0, st>>>((const u16*)a, b, out, n);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_sumsq(const float* x, int64_t n, double* part, double* out, hipStream_t st) {
+  if (!x) {
+    set_f64_kernel<<<1, 64, 0, st>>>(out, __builtin_nan(""));
+  } else {
+    const int nblk = 1024;
+    sumsq_kernel<<<nblk, 256, 0, st>>>(x, n, part);
+    sumsq_final_kernel<<<1, 64, 0, st>>>(part, nblk, out);
+  }
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_set_f64(double* p, double v, hipStream_t st) {
+  set_f64_kernel<<<1, 64, 0, st>>>(p, v);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+}  // namespace bsp
