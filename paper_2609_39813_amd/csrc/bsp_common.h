@@ -100,8 +100,10 @@ __device__ __forceinline__ Bracket f8_bracket(float a, F8 f) {
 // floor(frac * 2^32): exact when frac has at most 32 fraction bits, truncated below.
 __device__ __forceinline__ uint32_t sr_threshold(float frac) { return (uint32_t)(frac * 4294967296.0f); }
 
-// Round up iff R + F >= 2^32 (so P(up) = F / 2^32).
-__device__ __forceinline__ uint32_t sr_up(uint32_t F, uint32_t R) { return (F != 0u) & (R >= (0u - F)); }
+// Round up iff R + F >= 2^32 (so P(up) = F / 2^32): the carry out of the 32-bit add.
+__device__ __forceinline__ uint32_t sr_up(uint32_t F, uint32_t R) {
+  return (uint32_t)(((uint64_t)R + (uint64_t)F) >> 32);
+}
 
 __device__ __forceinline__ uint32_t rne_up(const Bracket& b) {
   return (b.frac > 0.5f) | ((b.frac == 0.5f) & (b.mi & 1u));

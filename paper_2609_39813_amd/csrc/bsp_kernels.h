@@ -61,14 +61,15 @@ struct FreshArgs {
   u16* counts;         // [T][d] up counts (nullable)
   const float* w1;     // [T][d] weights (FC_COLSUM, FC_BLOCKSUM)
   const float* w2;     // [T][d] second weight (FC_BLOCKSUM, nullable)
-  double* partial;     // FC_COLSUM: [K][ceil(T/32)][d]; FC_BLOCKSUM: [K][2][nblocks]
+  double* partial;     // FC_BLOCKSUM: [K][2][nblocks]
+  float* colsum = nullptr;  // FC_COLSUM: [K][ceil(T/32)][d]
 };
 template <typename X>
 bs_status launch_fresh_count_t(const FreshArgs<X>& a, int mode, hipStream_t st);
 inline int64_t fresh_count_blocks(int64_t T, int64_t d) { return ((d + 255) / 256) * ((T + 31) / 32); }
 
 bs_status launch_fresh_count(const float* u, int64_t T, int64_t d, int fmt, const float* scale, uint64_t seed,
-                             uint32_t use, int K, u16* counts, const float* w, double* partial, hipStream_t st);
+                             uint32_t use, int K, u16* counts, const float* w, float* colsum, hipStream_t st);
 
 bs_status launch_combine(const float* ref, const float* bias, const float* se, int64_t n, float* mean_out,
                          float* bias_out, float* se_out, hipStream_t st);

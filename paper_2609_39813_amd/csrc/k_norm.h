@@ -56,7 +56,7 @@ bs_status launch_norm_planes(int mode, const NormPlaneArgs& a, hipStream_t st);
 bs_status launch_val_rows(const uint8_t* codes, int64_t n, int fmt, u16* out, hipStream_t st);
 template <typename T>
 bs_status launch_gain_t(const GainArgs<T>& a, float* ref, float* bias_r, float* bias_n, hipStream_t st);
-bs_status launch_gain_se(const double* part, int K, int64_t T, int64_t d, const float* scale, const float* gain,
+bs_status launch_gain_se(const float* part, int K, int64_t T, int64_t d, const float* scale, const float* gain,
                          double* S, float* se, hipStream_t st);
 template <typename T>
 bs_status launch_dx_t(const DxArgs<T>& a, hipStream_t st);

@@ -171,12 +171,12 @@ __global__ __launch_bounds__(256) void gain_final_kernel(const double* __restric
 // se of the gain use under N: the per-trial gradient is const + (s / gain) S_k with
 // S_k = sum over row tiles of the new-rounding counter's partials. First S_k[j] for every
 // (trial, column) (row tiles summed in order), then Welford over k in order per column.
-__global__ __launch_bounds__(256) void gain_trial_sum_kernel(const double* __restrict__ part, int64_t nrt, int64_t d,
+__global__ __launch_bounds__(256) void gain_trial_sum_kernel(const float* __restrict__ part, int64_t nrt, int64_t d,
                                                              double* __restrict__ S) {
   const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t k = blockIdx.y;
   if (j >= d) return;
-  const double* p = part + k * nrt * d + j;
+  const float* p = part + k * nrt * d + j;
   double acc = 0.0;
   for (int64_t rt = 0; rt < nrt; ++rt) acc += p[rt * d];
   S[k * d + j] = acc;
@@ -320,7 +320,7 @@ bs_status launch_gain_t(const GainArgs<T>& a, float* ref, float* bias_r, float* 
 template bs_status launch_gain_t<float>(const GainArgs<float>&, float*, float*, float*, hipStream_t);
 template bs_status launch_gain_t<u16>(const GainArgs<u16>&, float*, float*, float*, hipStream_t);
 
-bs_status launch_gain_se(const double* part, int K, int64_t T, int64_t d, const float* scale, const float* gain,
+bs_status launch_gain_se(const float* part, int K, int64_t T, int64_t d, const float* scale, const float* gain,
                          double* S, float* se, hipStream_t st) {
   if (d <= 0) return BS_OK;
   const int64_t nrt = (T + 31) / 32;

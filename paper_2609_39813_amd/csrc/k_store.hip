@@ -1,5 +1,7 @@
 // FP8 store kernels: amax, scale, quantize (RNE / stochastic), and the K-trial
 // stochastic-rounding counter of a store's new roundings.
+#include <type_traits>
+
 #include "bsp_kernels.h"
 
 namespace bsp {
@@ -157,14 +159,22 @@ __global__ __launch_bounds__(256) void quantize_kernel(const T* __restrict__ x, 
 // K-trial counter of new roundings of a [T, d] store y = fl32(x / s) (d % 4 == 0).
 // counts[t, j] = number of trials k in 1..K whose rounding of element t*d + j goes up.
 // Block: 256 threads = 64 column groups (4 columns each) x 4 row lanes, 8 rows per thread,
-// so one block covers 32 rows x 256 columns. With c = sign(y) step (t, j) w(t, j):
-//   FC_COLSUM: partial[k-1][rt][j] = sum over the block's 32 rows of up_k c      (w = w1)
-//   FC_BLOCKSUM: partial[k-1][i][b] = sum over the block's elements of up_k c_i (w1, w2)
-// all in fp64, trials reduced through LDS four at a time.
+// so one block covers 32 rows x 256 columns. The row lane is the wave, except for FC_COLSUM,
+// where a wave holds 16 column groups x 4 row lanes so that the column sums reduce inside the
+// wave (cross-lane adds in a fixed order, no barrier). With c = sign(y) step (t, j) w(t, j):
+//   FC_COLSUM: colsum[k-1][rt][j] = sum over the block's 32 rows of up_k c (w = w1), fp32
+//   FC_BLOCKSUM: partial[k-1][i][b] = sum over the block's elements of up_k c_i (w1, w2), fp64
+// FC_BLOCKSUM reduces through LDS four trials at a time, in a fixed order. The column sums feed only a
+// sample variance over trials: they hold no trial-independent term (an element whose
+// rounding never goes up adds nothing), so fp32 rounding of a 32-row sum perturbs each trial
+// by a few ulps of values of the size of the trial-to-trial spread, far below the 1e-5 of the
+// statistic, and the sums over row blocks are taken in fp64.
 template <typename X, int MODE>
-__global__ __launch_bounds__(256) void fresh_count_kernel(FreshArgs<X> a) {
-  constexpr int RT = 32, RPT = 8, TB = 4;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+__device__ __forceinline__ void fresh_count_body(const FreshArgs<X>& a) {
+  constexpr int RT = 32, RPT = 8, TB = MODE == FC_COLSUM ? 1 : 4;
+  const int lane = threadIdx.x & 63;
+  const int tx = MODE == FC_COLSUM ? (threadIdx.x >> 6) * 16 + (lane & 15) : lane;
+  const int ty = MODE == FC_COLSUM ? lane >> 4 : threadIdx.x >> 6;
   const int64_t j0 = (int64_t)blockIdx.x * 256 + 4 * tx;
   const int64_t t0 = (int64_t)blockIdx.y * RT;
   const bool colok = j0 < a.d;
@@ -193,23 +203,25 @@ __global__ __launch_bounds__(256) void fresh_count_kernel(FreshArgs<X> a) {
     for (int q = 0; q < 4; ++q) {
       const float y = __fdiv_rn(xv[q], s);
       const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
-      F[r][q] = ok ? sr_threshold(b.frac) : 0u;
+      F[r][q] = sr_threshold(ok ? b.frac : 0.0f);
       const float sc = (signbit(y) ? -1.0f : 1.0f) * f8_step(b);
       c1[r][q] = sc * w1v[q];
       c2[r][q] = sc * w2v[q];
       cnt[r][q] = 0;
+      // opaque from here on: keeps the row-validity test out of the trial loop
+      asm volatile("" : "+v"(F[r][q]), "+v"(c1[r][q]));
     }
   }
-  constexpr int NR = MODE == FC_COLSUM ? 4 * 256 : (MODE == FC_BLOCKSUM ? 2 * 4 : 1);
-  __shared__ double red[MODE == FC_COUNT ? 1 : TB][NR];
+  using Acc = typename std::conditional<MODE == FC_COLSUM, float, double>::type;
+  __shared__ double red[MODE == FC_BLOCKSUM ? TB : 1][2 * 4];
   const int64_t nrt = gridDim.y;
   const int64_t nblk = (int64_t)gridDim.x * gridDim.y, bid = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
   for (int k0 = 1; k0 <= a.K; k0 += TB) {
-    double acc[TB][4];
+    Acc acc[TB][4];
 #pragma unroll
     for (int i = 0; i < TB; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc[i][q] = 0.0;
+      for (int q = 0; q < 4; ++q) acc[i][q] = 0;
 #pragma unroll
     for (int i = 0; i < TB; ++i) {
       const int k = k0 + i;
@@ -224,32 +236,34 @@ __global__ __launch_bounds__(256) void fresh_count_kernel(FreshArgs<X> a) {
         for (int q = 0; q < 4; ++q) {
           const uint32_t up = sr_up(F[r][q], R[q]);
           cnt[r][q] += up;
-          if (MODE == FC_COLSUM) acc[i][q] += up ? (double)c1[r][q] : 0.0;
+          if (MODE == FC_COLSUM) acc[i][q] += up ? c1[r][q] : 0.0f;
           if (MODE == FC_BLOCKSUM) {
             acc[i][0] += up ? (double)c1[r][q] : 0.0;
             acc[i][1] += up ? (double)c2[r][q] : 0.0;
           }
         }
+        // column sums: at most four Philox groups in flight (register budget of three waves)
+        if (MODE == FC_COLSUM && (r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
       }
     }
     if (MODE == FC_COLSUM) {
+      // sum over the 4 row lanes (lane bits 4 and 5): (l + l^16) + (l^32 + l^48)
 #pragma unroll
-      for (int i = 0; i < TB; ++i)
+      for (int i = 0; i < TB; ++i) {
+        float v[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) red[i][ty * 256 + 4 * tx + q] = acc[i][q];
-      __syncthreads();
-      // thread -> (trial i, column); each sums its column's 4 row lanes in order
-      for (int o = threadIdx.x; o < TB * 256; o += 256) {
-        const int i = o >> 8, col = o & 255;
+        for (int q = 0; q < 4; ++q) {
+          v[q] = (float)acc[i][q];
+          v[q] += __shfl_xor(v[q], 16, 64);
+          v[q] += __shfl_xor(v[q], 32, 64);
+        }
         const int k = k0 + i;
-        const double v = ((red[i][col] + red[i][256 + col]) + red[i][512 + col]) + red[i][768 + col];
-        const int64_t j = (int64_t)blockIdx.x * 256 + col;
-        if (k <= a.K && j < a.d) a.partial[((int64_t)(k - 1) * nrt + blockIdx.y) * a.d + j] = v;
+        if (ty == 0 && colok && k <= a.K)
+          *(float4*)(a.colsum + ((int64_t)(k - 1) * nrt + blockIdx.y) * a.d + j0) = make_float4(v[0], v[1], v[2], v[3]);
       }
-      __syncthreads();
     }
     if (MODE == FC_BLOCKSUM) {
-      const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+      const int wv = threadIdx.x >> 6;
 #pragma unroll
       for (int i = 0; i < TB; ++i) {
         const double v1 = wave_sum_f64(acc[i][0]);
@@ -280,6 +294,17 @@ __global__ __launch_bounds__(256) void fresh_count_kernel(FreshArgs<X> a) {
       }
     }
   }
+}
+
+// The column-sum variant holds the per-element weights too; it is held to 168 registers so that
+// three waves share each SIMD (the Philox latency needs them).
+template <typename X, int MODE>
+__global__ __launch_bounds__(256) void fresh_count_kernel(FreshArgs<X> a) {
+  fresh_count_body<X, MODE>(a);
+}
+template <typename X>
+__global__ __launch_bounds__(256) void fresh_colsum_kernel(FreshArgs<X> a) {
+  fresh_count_body<X, FC_COLSUM>(a);
 }
 
 // ------------------------------------------------------------------------------------
@@ -326,7 +351,7 @@ bs_status launch_fresh_count_t(const FreshArgs<X>& a, int mode, hipStream_t st) 
   if (mode == FC_COUNT)
     fresh_count_kernel<X, FC_COUNT><<<grid, 256, 0, st>>>(a);
   else if (mode == FC_COLSUM)
-    fresh_count_kernel<X, FC_COLSUM><<<grid, 256, 0, st>>>(a);
+    fresh_colsum_kernel<X><<<grid, 256, 0, st>>>(a);
   else
     fresh_count_kernel<X, FC_BLOCKSUM><<<grid, 256, 0, st>>>(a);
   BS_CHECK_LAUNCH();
@@ -336,9 +361,9 @@ template bs_status launch_fresh_count_t<float>(const FreshArgs<float>&, int, hip
 template bs_status launch_fresh_count_t<u16>(const FreshArgs<u16>&, int, hipStream_t);
 
 bs_status launch_fresh_count(const float* u, int64_t T, int64_t d, int fmt, const float* scale, uint64_t seed,
-                             uint32_t use, int K, u16* counts, const float* w, double* partial, hipStream_t st) {
-  FreshArgs<float> a{u, T, d, f8_format(fmt), scale, seed, use, K, counts, w, nullptr, partial};
-  return launch_fresh_count_t(a, partial ? FC_COLSUM : FC_COUNT, st);
+                             uint32_t use, int K, u16* counts, const float* w, float* colsum, hipStream_t st) {
+  FreshArgs<float> a{u, T, d, f8_format(fmt), scale, seed, use, K, counts, w, nullptr, nullptr, colsum};
+  return launch_fresh_count_t(a, colsum ? FC_COLSUM : FC_COUNT, st);
 }
 
 }  // namespace bsp

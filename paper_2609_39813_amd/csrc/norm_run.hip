@@ -23,7 +23,8 @@ struct NormWs {
   float *u, *rstd, *du, *bias_rg, *bias_ng, *se_g, *bias_u, *bias_n[2], *dx_r;
   u16 *dyT[3], *uvalT, *resU[3], *resN[2], *uval_rows, *wT[3], *dy_rows[3], *w_rows[3];
   u16 *counts_g, *counts_w;
-  double *partial, *gain_part, *trial_sums;
+  float* partial;
+  double *gain_part, *trial_sums;
 };
 
 NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype wt, bs_dtype gt, const NormPlan& p,
@@ -61,7 +62,7 @@ NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype wt
   if (p.gain_n || p.weight_n[0]) w.counts_g = c.take<u16>(T * d);
   if (p.weight_n[1]) w.counts_w = c.take<u16>(T * d);
   if (p.gain_se) {
-    w.partial = c.take<double>((int64_t)K * ((T + 31) / 32) * d + 1);
+    w.partial = c.take<float>((int64_t)K * ((T + 31) / 32) * d + 1);
     w.trial_sums = c.take<double>((int64_t)K * d);
   }
   if (p.want_dxr) w.dx_r = c.take<float>(T * d);
