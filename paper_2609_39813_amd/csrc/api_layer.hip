@@ -39,7 +39,8 @@ struct WeightUseIO {
 
 struct WeightUseWs {
   u16 *dyT[3], *valT, *res[3], *counts;
-  float *bias_u, *bias_n;
+  float *bias_u, *bias_n, *gpart;
+  int64_t gpart_cap;
 };
 
 WeightUseWs carve_wu(Carver& c, int64_t T, int64_t k, int64_t n) {
@@ -51,6 +52,8 @@ WeightUseWs carve_wu(Carver& c, int64_t T, int64_t k, int64_t n) {
   w.counts = c.take<u16>(T * k);
   w.bias_u = c.take<float>(k * n);
   w.bias_n = c.take<float>(k * n);
+  w.gpart_cap = 16 * k * n;  // split-K partials: the long-T contraction has few output tiles
+  w.gpart = c.take<float>(w.gpart_cap);
   return w;
 }
 
@@ -83,6 +86,8 @@ bs_status weight_use_run(const WeightUseIO& io, void* ws, size_t ws_bytes, hipSt
     g.alpha = alpha;
     g.alpha_dev = alpha_dev;
     g.C = C;
+    g.part = w.gpart;
+    g.part_cap = w.gpart_cap;
     if (!gemm_add_products(g, A, nA, w.dyT, nt)) return BS_EINVAL;
     return launch_gemm(g, st);
   };

@@ -15,6 +15,8 @@ struct GemmArgs {
   const float* alpha_dev;  // nullable: alpha is multiplied by *alpha_dev
   int accumulate;
   float* C;
+  float* part = nullptr;    // nullable: split-K partials, part_cap floats (device workspace)
+  int64_t part_cap = 0;
 };
 
 // Append the products A_i B_j (i + j <= 2) of nA and nB bf16 terms to g's segments.

@@ -1,5 +1,7 @@
 // The normalization-store runner: RMSNorm -> FP8 store -> Linear and the per-use estimates
 // of the store's gain, weight and normalization-input uses.
+#include <algorithm>
+
 #include "bsp_kernels.h"
 #include "k_norm.h"
 #include "norm_run.h"
@@ -25,6 +27,8 @@ struct NormWs {
   u16 *counts_g, *counts_w;
   float* partial;
   double *gain_part, *trial_sums;
+  float* gpart;  // split-K partials of the contractions
+  int64_t gpart_cap;
 };
 
 NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype wt, bs_dtype gt, const NormPlan& p,
@@ -66,6 +70,9 @@ NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype wt
     w.trial_sums = c.take<double>((int64_t)K * d);
   }
   if (p.want_dxr) w.dx_r = c.take<float>(T * d);
+  // split-K partials for the contractions with few output tiles (du: T x d; weight use: d x n)
+  w.gpart_cap = 4 * d * std::max<int64_t>(std::max<int64_t>(T, n), 64);
+  w.gpart = c.take<float>(w.gpart_cap);
   return w;
 }
 
@@ -173,6 +180,8 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     g.ldc = d;
     g.alpha = 1.0f;
     g.C = w.du;
+    g.part = w.gpart;
+    g.part_cap = w.gpart_cap;
     u16* A0 = (u16*)dY;
     u16* B0 = (u16*)W;
     u16* const* Aops = &A0;
@@ -215,6 +224,8 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     g.alpha = alpha;
     g.alpha_dev = alpha_dev;
     g.C = C;
+    g.part = w.gpart;
+    g.part_cap = w.gpart_cap;
     if (!gemm_add_products(g, A, nA, w.dyT, nt)) return BS_EINVAL;
     return launch_gemm(g, st);
   };
