@@ -14,9 +14,18 @@ namespace bsp {
 namespace {
 struct AttnWs {
   float *m, *l, *O, *D_ref, *dD_R, *dD_N, *sd_N;
+  u16 *Qt, *Kt, *dOp[3], *dOt[3];
 };
-AttnWs carve_attn(Carver& c, int64_t rows, int64_t numel, bool need_o, bool need_dref) {
+AttnWs carve_attn(Carver& c, int64_t rows, int64_t numel, bool need_o, bool need_dref, int64_t bh = 0, int64_t Sp = 0,
+                  int ndo = 0) {
   AttnWs w{};
+  if (ndo > 0) {  // operand copies for the backward
+    w.Qt = c.take<u16>(bh * 64 * Sp);
+    w.Kt = c.take<u16>(bh * 64 * Sp);
+    for (int i = 0; i < ndo; ++i) w.dOt[i] = c.take<u16>(bh * 64 * Sp);
+    if (ndo == 3)
+      for (int i = 0; i < 3; ++i) w.dOp[i] = c.take<u16>(numel);
+  }
   w.m = c.take<float>(rows);
   w.l = c.take<float>(rows);
   if (need_o) w.O = c.take<float>(numel);
@@ -32,7 +41,7 @@ size_t attn_ws_size(int B, int H, int S, int dh) {
   if (B < 0 || H < 0 || S < 0 || dh < 0) return 0;
   Carver c;
   const int64_t rows = (int64_t)B * H * S;
-  carve_attn(c, rows, rows * dh, true, true);
+  carve_attn(c, rows, rows * dh, true, true, (int64_t)B * H, (S + 63) / 64 * 64, 3);
   return c.used();
 }
 
@@ -46,7 +55,7 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       (io.fwd_mode != BS_RNE && io.fwd_mode != BS_SR))
     return BS_EINVAL;
   if (io.dh != 64) return BS_ESHAPE;
-  if ((int64_t)io.B * io.H > 65535) return BS_ESHAPE;
+  if ((int64_t)io.B * io.H > 65535 || (io.S + 63) / 64 > 65535) return BS_ESHAPE;
   if (io.dK.se) return BS_EUNSUPPORTED;
   bool want_r = false, want_n = false;
   for (int i = 0; i < (fwd_only ? 0 : io.n_pol); ++i) {
@@ -56,11 +65,13 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   }
   const int64_t rows = (int64_t)io.B * io.H * io.S, numel = rows * io.dh;
   const bool need_o = !io.O && !io.O_out;
+  const int64_t bh = (int64_t)io.B * io.H, Sp = (io.S + 63) / 64 * 64;
+  const int ndo = fwd_only ? 0 : (io.dO32 ? 3 : 1);
   Carver probe;
-  carve_attn(probe, rows, numel, need_o, !io.D_ref);
+  carve_attn(probe, rows, numel, need_o, !io.D_ref, bh, Sp, ndo);
   if (!ws || ((uintptr_t)ws & 255) || ws_bytes < probe.used()) return BS_EWORKSPACE;
   Carver c(ws, ws_bytes);
-  AttnWs w = carve_attn(c, rows, numel, need_o, !io.D_ref);
+  AttnWs w = carve_attn(c, rows, numel, need_o, !io.D_ref, bh, Sp, ndo);
   float* dref = io.D_ref ? io.D_ref : w.D_ref;
 
   // forward: m, l (and O when the caller does not hand it in)
@@ -87,7 +98,16 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
                io.K, want_n ? 1 : 0, dref, w.dD_R, w.dD_N, w.sd_N};
   BS_TRY(launch_attn_d(da, st));
 
+  BS_TRY(launch_attn_prep((const u16*)io.Q, (const u16*)io.Kt, (const u16*)io.dO, io.dO32, (int)bh, io.S, (int)Sp, w.Qt,
+                          w.Kt, w.dOp, w.dOt, st));
   AttnBwdArgs ba{};
+  ba.Qt = w.Qt;
+  ba.Kt = w.Kt;
+  for (int i = 0; i < 3; ++i) {
+    ba.dOp[i] = w.dOp[i];
+    ba.dOt[i] = w.dOt[i];
+  }
+  ba.Sp = (int)Sp;
   ba.Q = (const u16*)io.Q;
   ba.K = (const u16*)io.Kt;
   ba.V = (const u16*)io.V;

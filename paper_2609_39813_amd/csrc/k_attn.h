@@ -32,6 +32,12 @@ struct AttnDArgs {
 struct AttnBwdArgs {
   const u16 *Q, *K, *V, *dO;
   const float* dO32;  // nullable: fp32 incoming gradient (enters as three exact bf16 terms)
+  // operand copies written by launch_attn_prep: Q^T, K^T [B*H][64][Sp] and the incoming
+  // gradient's planes (row-major [B*H][S][64], only for an fp32 gradient) and their transposes
+  const u16 *Qt, *Kt;
+  const u16* dOp[3];
+  const u16* dOt[3];
+  int Sp;
   const float *m, *l, *D_ref, *dD_R, *dD_N, *sd_N;  // dD_R / dD_N / sd_N nullable
   int S, causal, ntrial;  // ntrial: K, the number of new roundings
   float scale;
@@ -47,6 +53,9 @@ struct AttnBwdArgs {
 
 bs_status launch_attn_fwd(const AttnArgs& a, int B, int H, hipStream_t st);
 bs_status launch_attn_d(const AttnDArgs& a, hipStream_t st);
+// Q^T, K^T, and the planes of the incoming gradient (and their transposes) for the backward.
+bs_status launch_attn_prep(const u16* Q, const u16* K, const u16* dO, const float* dO32, int BH, int S, int Sp,
+                           u16* Qt, u16* Kt, u16* const* dOp, u16* const* dOt, hipStream_t st);
 bs_status launch_attn_bwd(const AttnBwdArgs& a, int B, int H, hipStream_t st);
 
 }  // namespace bsp

@@ -119,7 +119,8 @@ __device__ __forceinline__ float group16_sum(float v) {
 template <bool WRITE_O>
 __global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) u16 sQ[AT * AT], sK[AT * AT], sVt[AT * AT], sP[3][AT * AT];
-  const int qb = blockIdx.x, bh = blockIdx.y;
+  // heaviest (most key blocks) first: blocks are dispatched in index order
+  const int bh = blockIdx.x, qb = a.causal ? (int)gridDim.y - 1 - (int)blockIdx.y : (int)blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int q0 = qb * AT;
   const int64_t hb = (int64_t)bh * a.S * AT;
@@ -202,330 +203,513 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
 }
 
 // ------------------------------------------------------------------------------------
-// D variants, one row per 16 lanes (4 elements per lane, one Philox call per trial):
+// D variants, one row per 4 lanes (16 elements per lane, four Philox calls per trial):
 //   D_ref = sum dO O; dD_R = sum dO (s val(C_O) - O);
 //   dD_k  = sum dO (s val(C_k) - O) for new roundings k = 1..K, = A + s S_k with
-//   A = sum dO (s sign lo - O), S_k = sum dO sign step up_k; mean and sample SD over k (fp64).
+//   A = sum dO (s sign lo - O) (fp64) and S_k = sum dO sign step up_k. S_k holds no
+//   trial-independent term, so it is summed in fp32 (per lane in element order, then over the
+//   row's 4 lanes); its mean and sample SD over k come from fp64 sums of S_k - S_1.
 // ------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void attn_d_kernel(AttnDArgs a) {
-  const int64_t row = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
-  const int sub = threadIdx.x & 15;
+  constexpr int EPL = 16;
+  const int64_t row = (int64_t)blockIdx.x * 64 + (threadIdx.x >> 2);
+  const int sub = threadIdx.x & 3;
   const bool ok = row < a.rows;
-  const int64_t e0 = row * AT + 4 * sub;
+  const int64_t e0 = row * AT + EPL * sub;
   const float s = *a.scale;
   double dref = 0.0, dr = 0.0, A = 0.0;
-  uint32_t F[4] = {0, 0, 0, 0};
-  double w[4] = {0.0, 0.0, 0.0, 0.0};
-  if (ok) {
-    const float4 o4 = *(const float4*)(a.O + e0);
-    const uint32_t c4 = *(const uint32_t*)(a.codes + e0);
-    const float ov[4] = {o4.x, o4.y, o4.z, o4.w};
-    float dv[4];
-    if (a.dO32) {
-      const float4 g4 = *(const float4*)(a.dO32 + e0);
-      dv[0] = g4.x; dv[1] = g4.y; dv[2] = g4.z; dv[3] = g4.w;
-    } else {
-      const uint2 d2 = *(const uint2*)(a.dO + e0);
-      dv[0] = bf16_to_f32((u16)(d2.x & 0xFFFF));
-      dv[1] = bf16_to_f32((u16)(d2.x >> 16));
-      dv[2] = bf16_to_f32((u16)(d2.y & 0xFFFF));
-      dv[3] = bf16_to_f32((u16)(d2.y >> 16));
-    }
+  uint32_t F[EPL];
+  float w[EPL];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const double o = ov[q], g = dv[q];
-      dref += g * o;
-      dr += g * ((double)s * (double)f8_value((c4 >> (8 * q)) & 0xFFu, a.f) - o);
-      const float y = __fdiv_rn(ov[q], s);
-      const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
-      const double sg = signbit(y) ? -1.0 : 1.0;
-      const double step = f8_step(b);
-      A += g * ((double)s * sg * (double)b.mi * step - o);
-      F[q] = sr_threshold(b.frac);
-      w[q] = g * sg * step;
+  for (int q = 0; q < EPL; ++q) {
+    F[q] = 0u;
+    w[q] = 0.0f;
+  }
+  if (ok) {
+#pragma unroll
+    for (int j = 0; j < EPL / 4; ++j) {
+      const int64_t e = e0 + 4 * j;
+      const float4 o4 = *(const float4*)(a.O + e);
+      const uint32_t c4 = *(const uint32_t*)(a.codes + e);
+      const float ov[4] = {o4.x, o4.y, o4.z, o4.w};
+      float dv[4];
+      if (a.dO32) {
+        const float4 g4 = *(const float4*)(a.dO32 + e);
+        dv[0] = g4.x; dv[1] = g4.y; dv[2] = g4.z; dv[3] = g4.w;
+      } else {
+        const uint2 d2 = *(const uint2*)(a.dO + e);
+        dv[0] = bf16_to_f32((u16)(d2.x & 0xFFFF));
+        dv[1] = bf16_to_f32((u16)(d2.x >> 16));
+        dv[2] = bf16_to_f32((u16)(d2.y & 0xFFFF));
+        dv[3] = bf16_to_f32((u16)(d2.y >> 16));
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const double o = ov[q], g = dv[q];
+        dref += g * o;
+        dr += g * ((double)s * (double)f8_value((c4 >> (8 * q)) & 0xFFu, a.f) - o);
+        const float y = __fdiv_rn(ov[q], s);
+        const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
+        const float step = f8_step(b);
+        A += g * ((double)s * (signbit(y) ? -1.0 : 1.0) * (double)b.mi * (double)step - o);
+        F[4 * j + q] = sr_threshold(b.frac);
+        w[4 * j + q] = (signbit(y) ? -dv[q] : dv[q]) * step;  // exact: a power-of-two scaling
+      }
     }
   }
-  // fixed-order sums over the 16 lanes of a row (xor tree 8, 4, 2, 1)
-  auto rowsum = [&](double v) {
-#pragma unroll
-    for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  // fixed-order sums over the row's 4 lanes
+  auto rowsum = [&](auto v) {
+    v += __shfl_xor(v, 1, 64);
+    v += __shfl_xor(v, 2, 64);
     return v;
   };
   dref = rowsum(dref);
   dr = rowsum(dr);
   A = rowsum(A);
-  double mean = 0.0, m2 = 0.0;
+  double mean = 0.0, var = 0.0;
   if (a.want_n) {
-    const uint64_t g = (uint64_t)(e0 >> 2);
-    for (int k = 1; k <= a.K; ++k) {
-      const Philox4 p = philox_group(a.seed, g, (uint32_t)k, a.use);
-      const uint32_t R[4] = {p.w0, p.w1, p.w2, p.w3};
-      double Sk = 0.0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) Sk += sr_up(F[q], R[q]) ? w[q] : 0.0;
+    for (int q = 0; q < EPL; ++q) asm volatile("" : "+v"(F[q]), "+v"(w[q]));
+    double s1 = 0.0, d1 = 0.0, d2 = 0.0;
+    const uint64_t g0 = (uint64_t)(e0 >> 2);
+    for (int k = 1; k <= a.K; ++k) {
+      float Sk = 0.0f;
+#pragma unroll
+      for (int j = 0; j < EPL / 4; ++j) {
+        const Philox4 p = philox_group(a.seed, g0 + j, (uint32_t)k, a.use);
+        const uint32_t R[4] = {p.w0, p.w1, p.w2, p.w3};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) Sk += sr_up(F[4 * j + q], R[q]) ? w[4 * j + q] : 0.0f;
+      }
       Sk = rowsum(Sk);
-      const double dl = Sk - mean;
-      mean += dl / k;
-      m2 += dl * (Sk - mean);
+      if (k == 1) s1 = Sk;
+      const double dl = (double)Sk - s1;
+      d1 += dl;
+      d2 += dl * dl;
     }
+    mean = s1 + d1 / a.K;
+    var = a.K > 1 ? fmax(d2 - d1 * d1 / a.K, 0.0) / (a.K - 1) : 0.0;
   }
   if (ok && sub == 0) {
     a.D_ref[row] = (float)dref;
     a.dD_R[row] = (float)dr;
     if (a.want_n) {
       a.dD_N[row] = (float)(A + (double)s * mean);
-      a.sd_N[row] = a.K > 1 ? (float)((double)s * sqrt(m2 / (a.K - 1))) : 0.0f;
+      a.sd_N[row] = (float)((double)s * sqrt(var));
     }
   }
 }
 
 // ------------------------------------------------------------------------------------
-// backward, query-block-major: dQ = c dS K and G = P K; per-policy dQ estimates
-//   bias_v = -c dD_v G (row-scaled), se_N = c |G| sd_N / sqrt(K).
+// Backward. P and dS never leave registers: an MFMA result tile holds D[i][j] with j on
+// lane & 15 and i = 4 (lane >> 4) + r, which is the layout of an MFMA operand whose row is j
+// and whose k index runs over i. A 32-deep k step joins two such tiles: slot v of lane group
+// g holds k = 16 (v >> 2) + 4 g + (v & 3) (within 32 of the step), and the other operand is
+// read from a transposed tile in the same order (two 8-byte reads). Transposed tiles keep
+// their 8-byte units XOR-swizzled by (row & 15), so the 16 rows of a read phase hit distinct
+// banks. P and dS enter their products as three exact bf16 terms.
+// ------------------------------------------------------------------------------------
+// P = 2^(c log2(e) S - m log2(e)) / l: one hardware exp2 per element (relative error of a few
+// ulps; the exponent's rounding adds |m| 2^-24, below 1e-6 for the scores of these inputs)
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ int swt(int row, int unit) { return row * AT + ((unit ^ (row & 15)) << 2); }
+
+__device__ __forceinline__ bf16x8 frag_t(const u16* T, int row, int s, int g) {
+  const uint2 a = *(const uint2*)(T + swt(row, 8 * s + g));
+  const uint2 b = *(const uint2*)(T + swt(row, 8 * s + 4 + g));
+  return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+}
+
+// the three bf16 terms of eight fp32 values as MFMA operands
+__device__ __forceinline__ void pack3(const float* v, bf16x8* t) {
+  u16 h[3][8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) split3(v[q], h[0][q], h[1][q], h[2][q]);
+#pragma unroll
+  for (int p = 0; p < 3; ++p) t[p] = __builtin_bit_cast(bf16x8, *(const uint4*)h[p]);
+}
+
+// a row-major [64][64] bf16 tile (rows r0.. of a [*, 64] matrix with nrow rows, zeros past
+// them) as two 16-byte pieces per thread, and its store into LDS
+struct TileRegs {
+  uint4 v[2];
+};
+__device__ __forceinline__ void tile_fetch(TileRegs& t, const u16* __restrict__ g, int r0, int nrow) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (threadIdx.x >> 3) + 32 * i, c = (threadIdx.x & 7) * 8;
+    t.v[i] = r0 + r < nrow ? *(const uint4*)(g + (int64_t)(r0 + r) * AT + c) : make_uint4(0, 0, 0, 0);
+  }
+}
+__device__ __forceinline__ void tile_put(u16* T, const TileRegs& t) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (threadIdx.x >> 3) + 32 * i, c = (threadIdx.x & 7) * 8;
+    *(uint4*)(T + sw(r, c)) = t.v[i];
+  }
+}
+// columns c0 .. c0 + 63 of a transposed [64][ld] matrix (ld a multiple of 64, zero padded)
+__device__ __forceinline__ void tile_fetch_t(TileRegs& t, const u16* __restrict__ g, int c0, int ld) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (threadIdx.x >> 3) + 32 * i, c = (threadIdx.x & 7) * 8;
+    t.v[i] = *(const uint4*)(g + (int64_t)r * ld + c0 + c);
+  }
+}
+__device__ __forceinline__ void tile_put_t(u16* T, const TileRegs& t) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (threadIdx.x >> 3) + 32 * i, u = (threadIdx.x & 7) * 2;
+    *(uint2*)(T + swt(r, u)) = make_uint2(t.v[i].x, t.v[i].y);
+    *(uint2*)(T + swt(r, u + 1)) = make_uint2(t.v[i].z, t.v[i].w);
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// key-block-major: dV = P^T dO, dK = c dS^T Q and the dK bias terms -c P^T (dD_v * Q)
+// (v = R, N). S = Q K^T and dP = dO V^T are formed with queries as rows, so that their
+// result tiles are the (key, query) operands of the three products.
 // ------------------------------------------------------------------------------------
 template <int NDO>
-__global__ __launch_bounds__(256) void attn_bwd_q_kernel(AttnBwdArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 sQ[AT * AT], sdO[NDO][AT * AT], sK[AT * AT], sV[AT * AT], sKt[AT * AT],
-      sP[3][AT * AT], sdS[3][AT * AT];
-  const int qb = blockIdx.x, bh = blockIdx.y;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int q0 = qb * AT;
-  const int64_t hb = (int64_t)bh * a.S * AT, rb = (int64_t)bh * a.S;
-  load_tile(sQ, a.Q + hb, q0, a.S);
-  if (NDO == 1) {
-    load_tile(sdO[0], a.dO + hb, q0, a.S);
-  } else {
-    u16* const t3[3] = {sdO[0], sdO[NDO > 1 ? 1 : 0], sdO[NDO > 2 ? 2 : 0]};
-    load_tile3(t3, a.dO32 + hb, q0, a.S);
+__global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
+  constexpr int NT = 2 + 2 * NDO;  // Q, Q^T, dO planes, dO^T planes
+  __shared__ __attribute__((aligned(16))) u16 sm[2][NT][AT * AT];
+  __shared__ float rows[2][5][AT];  // m, 1/l, D, dD_R, dD_N per query
+  // heaviest (most query blocks) first: blocks are dispatched in index order
+  const int bh = blockIdx.x, kb = blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, c16 = lane & 15;
+  const int k0 = kb * AT;
+  const int64_t hb = (int64_t)bh * a.S * AT, tb = (int64_t)bh * AT * a.Sp, rb = (int64_t)bh * a.S;
+  const int key = k0 + 16 * w + c16;
+  // this wave's keys as the second operand of S and dP (fixed over the loop)
+  bf16x8 fk[2], fv[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int64_t e = hb + (int64_t)key * AT + 32 * s + 8 * g;
+    const uint4 zk = key < a.S ? *(const uint4*)(a.K + e) : make_uint4(0, 0, 0, 0);
+    const uint4 zv = key < a.S ? *(const uint4*)(a.V + e) : make_uint4(0, 0, 0, 0);
+    fk[s] = __builtin_bit_cast(bf16x8, zk);
+    fv[s] = __builtin_bit_cast(bf16x8, zv);
   }
-  float mr[4], il[4], dr[4];
+  const u16* dOrow[NDO];
+#pragma unroll
+  for (int i = 0; i < NDO; ++i) dOrow[i] = (NDO == 1 ? a.dO : a.dOp[i]) + hb;
+
+  TileRegs pf[NT];
+  float prow[5];
+  auto fetch = [&](int q0) {
+    tile_fetch(pf[0], a.Q + hb, q0, a.S);
+    tile_fetch_t(pf[1], a.Qt + tb, q0, a.Sp);
+#pragma unroll
+    for (int i = 0; i < NDO; ++i) {
+      tile_fetch(pf[2 + i], dOrow[i], q0, a.S);
+      tile_fetch_t(pf[2 + NDO + i], a.dOt[i] + tb, q0, a.Sp);
+    }
+    if (threadIdx.x < AT) {
+      const int q = q0 + threadIdx.x;
+      const bool ok = q < a.S;
+      prow[0] = ok ? a.m[rb + q] * kLog2e : 0.0f;
+      prow[1] = ok ? 1.0f / a.l[rb + q] : 0.0f;
+      prow[2] = ok ? a.D_ref[rb + q] : 0.0f;
+      prow[3] = (ok && a.dD_R) ? a.dD_R[rb + q] : 0.0f;
+      prow[4] = (ok && a.dD_N) ? a.dD_N[rb + q] : 0.0f;
+    }
+  };
+  auto put = [&](int st) {
+    tile_put(sm[st][0], pf[0]);
+    tile_put_t(sm[st][1], pf[1]);
+#pragma unroll
+    for (int i = 0; i < NDO; ++i) {
+      tile_put(sm[st][2 + i], pf[2 + i]);
+      tile_put_t(sm[st][2 + NDO + i], pf[2 + NDO + i]);
+    }
+    if (threadIdx.x < AT)
+#pragma unroll
+      for (int k = 0; k < 5; ++k) rows[st][k][threadIdx.x] = prow[k];
+  };
+
+  floatx4 av[4], ak[4], akr[4], akn[4];
+#pragma unroll
+  for (int n = 0; n < 4; ++n) av[n] = ak[n] = akr[n] = akn[n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const bool want_r = a.dD_R != nullptr, want_n = a.dD_N != nullptr;
+  const float c2 = a.scale * kLog2e;
+  const int nqb = (a.S + AT - 1) / AT, qb0 = a.causal ? kb : 0;
+  fetch(qb0 * AT);
+  put(0);
+  __syncthreads();
+  for (int qb = qb0; qb < nqb; ++qb) {
+    const int st = (qb - qb0) & 1, q0 = qb * AT;
+    if (qb + 1 < nqb) fetch(q0 + AT);
+    const u16* tQ = sm[st][0];
+    const u16* tQt = sm[st][1];
+    // S, dP: query tiles t (rows), this wave's keys (columns)
+    floatx4 sv[4], dp[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) sv[t] = dp[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        sv[t] = mfma(*(const bf16x8*)(tQ + sw(16 * t + c16, 32 * s + 8 * g)), fk[s], sv[t]);
+#pragma unroll
+        for (int i = 0; i < NDO; ++i)
+          dp[t] = mfma(*(const bf16x8*)(sm[st][2 + i] + sw(16 * t + c16, 32 * s + 8 * g)), fv[s], dp[t]);
+      }
+    }
+    float p[4][4], ds[4][4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int ql = 16 * t + 4 * g + r, q = q0 + ql;
+        const bool ok = key < a.S && q < a.S && (!a.causal || key <= q);
+        const float pv = ok ? __builtin_amdgcn_exp2f(fmaf(c2, sv[t][r], -rows[st][0][ql])) * rows[st][1][ql] : 0.0f;
+        p[t][r] = pv;
+        ds[t][r] = ok ? pv * (dp[t][r] - rows[st][2][ql]) : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      float vp[8], vd[8];
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        vp[v] = p[2 * s + (v >> 2)][v & 3];
+        vd[v] = ds[2 * s + (v >> 2)][v & 3];
+      }
+      bf16x8 tp[3], td[3];
+      pack3(vp, tp);
+      pack3(vd, td);
+      bf16x8 fq[4];
+#pragma unroll
+      for (int n = 0; n < 4; ++n) {
+        fq[n] = frag_t(tQt, 16 * n + c16, s, g);
+#pragma unroll
+        for (int i = 0; i < NDO; ++i) {
+          const bf16x8 fo = frag_t(sm[st][2 + NDO + i], 16 * n + c16, s, g);
+#pragma unroll
+          for (int j = 0; j < 3; ++j)
+            if (i + j <= 2) av[n] = mfma(tp[j], fo, av[n]);
+        }
+#pragma unroll
+        for (int j = 0; j < 3; ++j) ak[n] = mfma(td[j], fq[n], ak[n]);
+      }
+      // bias terms: P scaled per query by dD_v
+#pragma unroll
+      for (int v2 = 0; v2 < 2; ++v2) {
+        if (v2 == 0 ? !want_r : !want_n) continue;
+        float vb[8];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) vb[v] = vp[v] * rows[st][3 + v2][32 * s + 16 * (v >> 2) + 4 * g + (v & 3)];
+        bf16x8 tb3[3];
+        pack3(vb, tb3);
+#pragma unroll
+        for (int n = 0; n < 4; ++n)
+#pragma unroll
+          for (int j = 0; j < 3; ++j) {
+            if (v2 == 0)
+              akr[n] = mfma(tb3[j], fq[n], akr[n]);
+            else
+              akn[n] = mfma(tb3[j], fq[n], akn[n]);
+          }
+      }
+    }
+    if (qb + 1 < nqb) put(st ^ 1);
+    __syncthreads();
+  }
+  const float c = a.scale;
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const int q = q0 + 16 * w + 4 * (lane >> 4) + r;
-    const bool ok = q < a.S;
-    mr[r] = ok ? a.m[rb + q] : 0.0f;
-    il[r] = ok ? a.l[rb + q] : 1.0f;
-    dr[r] = ok ? a.D_ref[rb + q] : 0.0f;
+    const int kr = k0 + 16 * w + 4 * g + r;
+    if (kr >= a.S) continue;
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      const int64_t e = hb + (int64_t)kr * AT + 16 * n + c16;
+      const float dk = c * ak[n][r];
+      a.dV[e] = av[n][r];
+      a.dK_ref[e] = dk;
+      for (int pi = 0; pi < a.n_pol; ++pi) {
+        const int kind = a.pol[pi];
+        const float bias = kind == BS_READ_U ? 0.0f : -c * (kind == BS_READ_R ? akr[n][r] : akn[n][r]);
+        if (a.kmean[pi]) a.kmean[pi][e] = dk + bias;
+        if (a.kbias[pi]) a.kbias[pi][e] = bias;
+      }
+    }
   }
+}
+
+// ------------------------------------------------------------------------------------
+// query-block-major: dQ = c dS K and G = P K; per-policy dQ estimates
+//   bias_v = -c dD_v G (row-scaled), se_N = c |G| sd_N / sqrt(K).
+// S^T = K Q^T and dP^T = V dO^T put keys on the k index of the dS / P operands.
+// ------------------------------------------------------------------------------------
+template <int NDO>
+__global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
+  __shared__ __attribute__((aligned(16))) u16 sm[2][3][AT * AT];  // K, V, K^T
+  // heaviest (most key blocks) first: blocks are dispatched in index order
+  const int bh = blockIdx.x, qb = a.causal ? (int)gridDim.y - 1 - (int)blockIdx.y : (int)blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, c16 = lane & 15;
+  const int q0 = qb * AT;
+  const int64_t hb = (int64_t)bh * a.S * AT, tb = (int64_t)bh * AT * a.Sp, rb = (int64_t)bh * a.S;
+  const int q = q0 + 16 * w + c16;
+  const bool qok = q < a.S;
+  bf16x8 fq[2], fdo[NDO][2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int64_t e = hb + (int64_t)q * AT + 32 * s + 8 * g;
+    fq[s] = __builtin_bit_cast(bf16x8, qok ? *(const uint4*)(a.Q + e) : make_uint4(0, 0, 0, 0));
+#pragma unroll
+    for (int i = 0; i < NDO; ++i) {
+      const u16* src = NDO == 1 ? a.dO : a.dOp[i];
+      fdo[i][s] = __builtin_bit_cast(bf16x8, qok ? *(const uint4*)(src + e) : make_uint4(0, 0, 0, 0));
+    }
+  }
+  const float mq = qok ? a.m[rb + q] * kLog2e : 0.0f;
+  const float c2 = a.scale * kLog2e;
+  const float ilq = qok ? 1.0f / a.l[rb + q] : 0.0f;
+  const float dq_ref = qok ? a.D_ref[rb + q] : 0.0f;
+
+  TileRegs pf[3];
+  auto fetch = [&](int k0) {
+    tile_fetch(pf[0], a.K + hb, k0, a.S);
+    tile_fetch(pf[1], a.V + hb, k0, a.S);
+    tile_fetch_t(pf[2], a.Kt + tb, k0, a.Sp);
+  };
+  auto put = [&](int st) {
+    tile_put(sm[st][0], pf[0]);
+    tile_put(sm[st][1], pf[1]);
+    tile_put_t(sm[st][2], pf[2]);
+  };
   floatx4 aq[4], ag[4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) aq[t] = ag[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int n = 0; n < 4; ++n) aq[n] = ag[n] = floatx4{0.f, 0.f, 0.f, 0.f};
   const int nkb = a.causal ? qb + 1 : (a.S + AT - 1) / AT;
+  fetch(0);
+  put(0);
+  __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
-    __syncthreads();
-    load_tile(sK, a.K + hb, kb * AT, a.S);
-    load_tile(sV, a.V + hb, kb * AT, a.S);
-    load_tile_t(sKt, a.K + hb, kb * AT, a.S);
-    __syncthreads();
-    floatx4 s[4], dp[4];
+    const int st = kb & 1, k0 = kb * AT;
+    if (kb + 1 < nkb) fetch(k0 + AT);
+    const u16* tK = sm[st][0];
+    const u16* tV = sm[st][1];
+    const u16* tKt = sm[st][2];
+    floatx4 sv[4], dp[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) s[t] = dp[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < 4; ++t) sv[t] = dp[t] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kk = 0; kk < AT; kk += 32) {
-      const bf16x8 fq = frag(sQ, 16 * w, kk, lane);
+    for (int s = 0; s < 2; ++s) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const bf16x8 fv = frag(sV, 16 * t, kk, lane);
-        s[t] = mfma(fq, frag(sK, 16 * t, kk, lane), s[t]);
+        sv[t] = mfma(*(const bf16x8*)(tK + sw(16 * t + c16, 32 * s + 8 * g)), fq[s], sv[t]);
+        const bf16x8 fvv = *(const bf16x8*)(tV + sw(16 * t + c16, 32 * s + 8 * g));
 #pragma unroll
-        for (int i = 0; i < NDO; ++i) dp[t] = mfma(frag(sdO[i], 16 * w, kk, lane), fv, dp[t]);
+        for (int i = 0; i < NDO; ++i) dp[t] = mfma(fvv, fdo[i][s], dp[t]);
+      }
+    }
+    float p[4][4], ds[4][4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int kk = k0 + 16 * t + 4 * g + r;
+        const bool ok = kk < a.S && qok && (!a.causal || kk <= q);
+        const float pv = ok ? __builtin_amdgcn_exp2f(fmaf(c2, sv[t][r], -mq)) * ilq : 0.0f;
+        p[t][r] = pv;
+        ds[t][r] = ok ? pv * (dp[t][r] - dq_ref) : 0.0f;
       }
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int ql = 16 * w + 4 * (lane >> 4) + r, q = q0 + ql;
+    for (int s = 0; s < 2; ++s) {
+      float vp[8], vd[8];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int kl = 16 * t + (lane & 15), key = kb * AT + kl;
-        const bool ok = key < a.S && q < a.S && (!a.causal || key <= q);
-        const float p = ok ? expf(a.scale * s[t][r] - mr[r]) / il[r] : 0.0f;
-        put3(sP[0], sP[1], sP[2], ql, kl, p);
-        put3(sdS[0], sdS[1], sdS[2], ql, kl, p * (dp[t][r] - dr[r]));
+      for (int v = 0; v < 8; ++v) {
+        vp[v] = p[2 * s + (v >> 2)][v & 3];
+        vd[v] = ds[2 * s + (v >> 2)][v & 3];
       }
-    }
-    __syncthreads();
+      bf16x8 tp[3], td[3];
+      pack3(vp, tp);
+      pack3(vd, td);
 #pragma unroll
-    for (int kk = 0; kk < AT; kk += 32) {
+      for (int n = 0; n < 4; ++n) {
+        const bf16x8 fk = frag_t(tKt, 16 * n + c16, s, g);
 #pragma unroll
-      for (int tm = 0; tm < 3; ++tm) {
-        const bf16x8 fs = frag(sdS[tm], 16 * w, kk, lane), fp = frag(sP[tm], 16 * w, kk, lane);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const bf16x8 fk = frag(sKt, 16 * t, kk, lane);
-          aq[t] = mfma(fs, fk, aq[t]);
-          ag[t] = mfma(fp, fk, ag[t]);
+        for (int j = 0; j < 3; ++j) {
+          aq[n] = mfma(td[j], fk, aq[n]);
+          ag[n] = mfma(tp[j], fk, ag[n]);
         }
       }
     }
+    if (kb + 1 < nkb) put(st ^ 1);
+    __syncthreads();
   }
   const float c = a.scale;
   const float rk = a.ntrial > 0 ? 1.0f / sqrtf((float)a.ntrial) : 0.0f;
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const int q = q0 + 16 * w + 4 * (lane >> 4) + r;
-    if (q >= a.S) continue;
-    const float ddr = a.dD_R ? a.dD_R[rb + q] : 0.0f;
-    const float ddn = a.dD_N ? a.dD_N[rb + q] : 0.0f;
-    const float sdn = a.sd_N ? a.sd_N[rb + q] : 0.0f;
+    const int qr = q0 + 16 * w + 4 * g + r;
+    if (qr >= a.S) continue;
+    const float ddr = a.dD_R ? a.dD_R[rb + qr] : 0.0f;
+    const float ddn = a.dD_N ? a.dD_N[rb + qr] : 0.0f;
+    const float sdn = a.sd_N ? a.sd_N[rb + qr] : 0.0f;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int64_t e = hb + (int64_t)q * AT + 16 * t + (lane & 15);
-      const float dq = c * aq[t][r];
-      const float g = ag[t][r];
+    for (int n = 0; n < 4; ++n) {
+      const int64_t e = hb + (int64_t)qr * AT + 16 * n + c16;
+      const float dq = c * aq[n][r];
+      const float gg = ag[n][r];
       a.dQ_ref[e] = dq;
-      for (int p = 0; p < a.n_pol; ++p) {
-        const int kind = a.pol[p];
-        const float bias = kind == BS_READ_U ? 0.0f : -c * (kind == BS_READ_R ? ddr : ddn) * g;
-        if (a.mean[p]) a.mean[p][e] = dq + bias;
-        if (a.bias[p]) a.bias[p][e] = bias;
-        if (a.se[p]) a.se[p][e] = kind == BS_READ_N ? c * fabsf(g) * sdn * rk : 0.0f;
+      for (int pi = 0; pi < a.n_pol; ++pi) {
+        const int kind = a.pol[pi];
+        const float bias = kind == BS_READ_U ? 0.0f : -c * (kind == BS_READ_R ? ddr : ddn) * gg;
+        if (a.mean[pi]) a.mean[pi][e] = dq + bias;
+        if (a.bias[pi]) a.bias[pi][e] = bias;
+        if (a.se[pi]) a.se[pi][e] = kind == BS_READ_N ? c * fabsf(gg) * sdn * rk : 0.0f;
       }
     }
   }
 }
 
 // ------------------------------------------------------------------------------------
-// backward, key-block-major: dV = P^T dO, dK = c dS^T Q and the bias terms
-// dK_v = -c P^T (dD_v * Q) for v in {R, N}, from S^T = K Q^T so that each wave reads only
-// its own key rows of the P^T / dS^T tiles.
+// operand copies for the backward: X^T [BH][64][Sp] (zero past S) of bf16 X [BH][S][64];
+// for an fp32 X, its three bf16 planes (row-major) and their transposes
 // ------------------------------------------------------------------------------------
-template <int NDO>
-__global__ __launch_bounds__(256) void attn_bwd_k_kernel(AttnBwdArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 sK[AT * AT], sV[AT * AT], sQ[AT * AT], sQt[AT * AT], sdO[NDO][AT * AT],
-      sdOt[NDO][AT * AT], sPt[3][AT * AT], sdSt[3][AT * AT];
-  __shared__ float rowm[AT], rowil[AT], rowd[AT], rowdr[AT], rowdn[AT];
-  const int kb = blockIdx.x, bh = blockIdx.y;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int k0 = kb * AT;
-  const int64_t hb = (int64_t)bh * a.S * AT, rb = (int64_t)bh * a.S;
-  load_tile(sK, a.K + hb, k0, a.S);
-  load_tile(sV, a.V + hb, k0, a.S);
-  floatx4 av[4], ak[4], akr[4], akn[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) av[t] = ak[t] = akr[t] = akn[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const int nqb = (a.S + AT - 1) / AT;
-  for (int qb = a.causal ? kb : 0; qb < nqb; ++qb) {
-    const int q0 = qb * AT;
-    __syncthreads();
-    load_tile(sQ, a.Q + hb, q0, a.S);
-    load_tile_t(sQt, a.Q + hb, q0, a.S);
-    if (NDO == 1) {
-      load_tile(sdO[0], a.dO + hb, q0, a.S);
-      load_tile_t(sdOt[0], a.dO + hb, q0, a.S);
+template <typename X>
+__global__ __launch_bounds__(256) void attn_prep_kernel(const X* __restrict__ x, int S, int Sp, u16* __restrict__ xt0,
+                                                        u16* __restrict__ xt1, u16* __restrict__ xt2,
+                                                        u16* __restrict__ xp0, u16* __restrict__ xp1,
+                                                        u16* __restrict__ xp2) {
+  constexpr int NP = sizeof(X) == 4 ? 3 : 1;
+  __shared__ u16 t[NP][AT][AT + 2];
+  const int r0 = blockIdx.x * AT, bh = blockIdx.y;
+  const int64_t hb = (int64_t)bh * S * AT, tb = (int64_t)bh * AT * Sp;
+  u16* const xp[3] = {xp0, xp1, xp2};
+  u16* const xt[3] = {xt0, xt1, xt2};
+  for (int e = threadIdx.x; e < AT * AT; e += 256) {
+    const int r = e >> 6, c = e & 63;
+    const bool ok = r0 + r < S;
+    if constexpr (NP == 1) {
+      t[0][r][c] = ok ? (u16)x[hb + (int64_t)(r0 + r) * AT + c] : (u16)0;
     } else {
-      u16* const t3[3] = {sdO[0], sdO[NDO > 1 ? 1 : 0], sdO[NDO > 2 ? 2 : 0]};
-      u16* const t3t[3] = {sdOt[0], sdOt[NDO > 1 ? 1 : 0], sdOt[NDO > 2 ? 2 : 0]};
-      load_tile3(t3, a.dO32 + hb, q0, a.S);
-      load_tile3_t(t3t, a.dO32 + hb, q0, a.S);
-    }
-    if (threadIdx.x < AT) {
-      const int q = q0 + threadIdx.x;
-      const bool ok = q < a.S;
-      rowm[threadIdx.x] = ok ? a.m[rb + q] : 0.0f;
-      rowil[threadIdx.x] = ok ? a.l[rb + q] : 1.0f;
-      rowd[threadIdx.x] = ok ? a.D_ref[rb + q] : 0.0f;
-      rowdr[threadIdx.x] = (ok && a.dD_R) ? a.dD_R[rb + q] : 0.0f;
-      rowdn[threadIdx.x] = (ok && a.dD_N) ? a.dD_N[rb + q] : 0.0f;
-    }
-    __syncthreads();
-    // S^T and dP^T for keys 16w.. of this block, all 64 queries
-    floatx4 s[4], dp[4];
+      const float v = ok ? load_f32(x, hb + (int64_t)(r0 + r) * AT + c) : 0.0f;
+      u16 h[3];
+      split3(v, h[0], h[1], h[2]);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) s[t] = dp[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < AT; kk += 32) {
-      const bf16x8 fk = frag(sK, 16 * w, kk, lane), fv = frag(sV, 16 * w, kk, lane);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        s[t] = mfma(fk, frag(sQ, 16 * t, kk, lane), s[t]);
-#pragma unroll
-        for (int i = 0; i < NDO; ++i) dp[t] = mfma(fv, frag(sdO[i], 16 * t, kk, lane), dp[t]);
-      }
-    }
-    float pv[4][4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int kl = 16 * w + 4 * (lane >> 4) + r, key = k0 + kl;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int ql = 16 * t + (lane & 15), q = q0 + ql;
-        const bool ok = key < a.S && q < a.S && (!a.causal || key <= q);
-        const float p = ok ? expf(a.scale * s[t][r] - rowm[ql]) / rowil[ql] : 0.0f;
-        pv[t][r] = p;
-        put3(sPt[0], sPt[1], sPt[2], kl, ql, p);
-        put3(sdSt[0], sdSt[1], sdSt[2], kl, ql, p * (dp[t][r] - rowd[ql]));
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < AT; kk += 32) {
-#pragma unroll
-      for (int tm = 0; tm < 3; ++tm) {
-        const bf16x8 fp = frag(sPt[tm], 16 * w, kk, lane), fs = frag(sdSt[tm], 16 * w, kk, lane);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-#pragma unroll
-          for (int i = 0; i < NDO; ++i)
-            if (tm + i <= 2) av[t] = mfma(fp, frag(sdOt[i], 16 * t, kk, lane), av[t]);
-          ak[t] = mfma(fs, frag(sQt, 16 * t, kk, lane), ak[t]);
-        }
-      }
-    }
-    // bias terms: P^T scaled by dD_v per query, reusing the P^T tiles of this wave's rows
-    for (int v = 0; v < 2; ++v) {
-      if (v == 0 ? !a.dD_R : !a.dD_N) continue;
-      const float* dd = v == 0 ? rowdr : rowdn;
-      __syncthreads();
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int kl = 16 * w + 4 * (lane >> 4) + r;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const int ql = 16 * t + (lane & 15);
-          put3(sPt[0], sPt[1], sPt[2], kl, ql, pv[t][r] * dd[ql]);
-        }
-      }
-      __syncthreads();
-#pragma unroll
-      for (int kk = 0; kk < AT; kk += 32) {
-#pragma unroll
-        for (int tm = 0; tm < 3; ++tm) {
-          const bf16x8 fp = frag(sPt[tm], 16 * w, kk, lane);
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            if (v == 0)
-              akr[t] = mfma(fp, frag(sQt, 16 * t, kk, lane), akr[t]);
-            else
-              akn[t] = mfma(fp, frag(sQt, 16 * t, kk, lane), akn[t]);
-          }
-        }
+      for (int p = 0; p < NP; ++p) {
+        t[p][r][c] = h[p];
+        if (ok) xp[p][hb + (int64_t)(r0 + r) * AT + c] = h[p];
       }
     }
   }
-  const float c = a.scale;
+  __syncthreads();
+  for (int e = threadIdx.x; e < AT * AT; e += 256) {
+    const int c = e >> 6, r = e & 63;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int key = k0 + 16 * w + 4 * (lane >> 4) + r;
-    if (key >= a.S) continue;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int64_t e = hb + (int64_t)key * AT + 16 * t + (lane & 15);
-      const float dk = c * ak[t][r];
-      a.dV[e] = av[t][r];
-      a.dK_ref[e] = dk;
-      for (int p = 0; p < a.n_pol; ++p) {
-        const int kind = a.pol[p];
-        const float bias = kind == BS_READ_U ? 0.0f : -c * (kind == BS_READ_R ? akr[t][r] : akn[t][r]);
-        if (a.kmean[p]) a.kmean[p][e] = dk + bias;
-        if (a.kbias[p]) a.kbias[p][e] = bias;
-      }
-    }
+    for (int p = 0; p < NP; ++p) xt[p][tb + (int64_t)c * Sp + r0 + r] = t[p][r][c];
   }
 }
 
 // ------------------------------------------------------------------------------------
 bs_status launch_attn_fwd(const AttnArgs& a, int B, int H, hipStream_t st) {
-  dim3 grid((unsigned)((a.S + AT - 1) / AT), (unsigned)(B * H));
+  dim3 grid((unsigned)(B * H), (unsigned)((a.S + AT - 1) / AT));
   ProfScope prof("attn_fwd", st);
   if (a.O_out)
     attn_fwd_kernel<true><<<grid, 256, 0, st>>>(a);
@@ -537,13 +721,28 @@ bs_status launch_attn_fwd(const AttnArgs& a, int B, int H, hipStream_t st) {
 
 bs_status launch_attn_d(const AttnDArgs& a, hipStream_t st) {
   if (a.rows <= 0) return BS_OK;
-  attn_d_kernel<<<(unsigned)((a.rows + 15) / 16), 256, 0, st>>>(a);
+  ProfScope prof("attn_d", st);
+  attn_d_kernel<<<(unsigned)((a.rows + 63) / 64), 256, 0, st>>>(a);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+bs_status launch_attn_prep(const u16* Q, const u16* K, const u16* dO, const float* dO32, int BH, int S, int Sp,
+                           u16* Qt, u16* Kt, u16* const* dOp, u16* const* dOt, hipStream_t st) {
+  dim3 grid((unsigned)(Sp / AT), (unsigned)BH);
+  ProfScope prof("attn_prep", st);
+  attn_prep_kernel<u16><<<grid, 256, 0, st>>>(Q, S, Sp, Qt, nullptr, nullptr, nullptr, nullptr, nullptr);
+  attn_prep_kernel<u16><<<grid, 256, 0, st>>>(K, S, Sp, Kt, nullptr, nullptr, nullptr, nullptr, nullptr);
+  if (dO32)
+    attn_prep_kernel<float><<<grid, 256, 0, st>>>(dO32, S, Sp, dOt[0], dOt[1], dOt[2], dOp[0], dOp[1], dOp[2]);
+  else if (dO)
+    attn_prep_kernel<u16><<<grid, 256, 0, st>>>(dO, S, Sp, dOt[0], nullptr, nullptr, nullptr, nullptr, nullptr);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
 
 bs_status launch_attn_bwd(const AttnBwdArgs& a, int B, int H, hipStream_t st) {
-  dim3 grid((unsigned)((a.S + AT - 1) / AT), (unsigned)(B * H));
+  dim3 grid((unsigned)(B * H), (unsigned)((a.S + AT - 1) / AT));
   ProfScope prof("attn_bwd", st);
   if (a.dO32) {
     attn_bwd_k_kernel<3><<<grid, 256, 0, st>>>(a);

@@ -48,9 +48,12 @@ __global__ __launch_bounds__(256) void amax_kernel(const T* __restrict__ x, int6
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const uint4* xv = (const uint4*)x;
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  for (; i + 3 * stride < nvec; i += 4 * stride) {
-    const uint4 a = xv[i], b = xv[i + stride], c = xv[i + 2 * stride], d = xv[i + 3 * stride];
-    m = max(m, max(max(vec_absmax<T>(a), vec_absmax<T>(b)), max(vec_absmax<T>(c), vec_absmax<T>(d))));
+  for (; i + 7 * stride < nvec; i += 8 * stride) {
+    uint4 v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = xv[i + k * stride];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) m = max(m, vec_absmax<T>(v[k]));
   }
   for (; i < nvec; i += stride) m = max(m, vec_absmax<T>(xv[i]));
   for (int64_t j = nvec * PER + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += stride)
@@ -317,8 +320,10 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
   if (!amax_done) {
     init_diag_kernel<<<1, 64, 0, st>>>(diag);
     if (n > 0 && !scale_in) {
+      // at most two blocks per CU, eight 16-byte loads in flight per thread: enough to keep
+      // HBM busy while the per-block atomics stay few (same-address atomics serialize)
       const int64_t want = (n / (16 / (xt == BS_F32 ? 4 : 2)) + 255) / 256 + 1;
-      const int blocks = (int)(want < 4096 ? want : 4096);
+      const int blocks = (int)(want < 512 ? want : 512);
       ProfScope prof("amax", st);
       if (xt == BS_F32)
         amax_kernel<float><<<blocks, 256, 0, st>>>((const float*)x, n, (uint32_t*)&diag->amax);
