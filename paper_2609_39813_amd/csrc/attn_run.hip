@@ -14,11 +14,12 @@ namespace bsp {
 namespace {
 struct AttnWs {
   float *m, *l, *O, *D_ref, *dD_R, *dD_N, *sd_N;
-  u16 *Qt, *Kt, *dOp[3], *dOt[3];
+  u16 *Vt, *Qt, *Kt, *dOp[3], *dOt[3];
 };
 AttnWs carve_attn(Carver& c, int64_t rows, int64_t numel, bool need_o, bool need_dref, int64_t bh = 0, int64_t Sp = 0,
                   int ndo = 0) {
   AttnWs w{};
+  w.Vt = c.take<u16>(bh * 64 * Sp);
   if (ndo > 0) {  // operand copies for the backward
     w.Qt = c.take<u16>(bh * 64 * Sp);
     w.Kt = c.take<u16>(bh * 64 * Sp);
@@ -55,6 +56,8 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       (io.fwd_mode != BS_RNE && io.fwd_mode != BS_SR))
     return BS_EINVAL;
   if (io.dh != 64) return BS_ESHAPE;
+  for (const void* p : {io.Q, io.Kt, io.V, io.dO, (const void*)io.dO32, (const void*)io.O})
+    if ((uintptr_t)p & 15) return BS_EINVAL;  // 16-byte vector loads
   if ((int64_t)io.B * io.H > 65535 || (io.S + 63) / 64 > 65535) return BS_ESHAPE;
   if (io.dK.se) return BS_EUNSUPPORTED;
   bool want_r = false, want_n = false;
@@ -75,7 +78,14 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   float* dref = io.D_ref ? io.D_ref : w.D_ref;
 
   // forward: m, l (and O when the caller does not hand it in)
-  AttnArgs fa{(const u16*)io.Q, (const u16*)io.Kt, (const u16*)io.V, io.S, io.causal, io.scale, w.m, w.l, nullptr};
+  {  // transposed operand copies: V^T for the forward; Q^T, K^T (and dO^T) for the backward
+    const u16* src[4] = {(const u16*)io.V, (const u16*)io.Q, (const u16*)io.Kt, (const u16*)io.dO};
+    u16* dst[4] = {w.Vt, w.Qt, w.Kt, w.dOt[0]};
+    const int n = fwd_only ? 1 : (io.dO32 ? 3 : 4);
+    BS_TRY(launch_attn_transpose(src, dst, n, (int)bh, io.S, (int)Sp, st));
+  }
+  AttnArgs fa{(const u16*)io.Q, (const u16*)io.Kt, (const u16*)io.V, io.S, io.causal, io.scale, w.m, w.l, nullptr,
+              w.Vt, (int)Sp};
   const float* Oorig = io.O;
   if (!io.O) {
     fa.O_out = io.O_out ? io.O_out : w.O;
@@ -98,8 +108,7 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
                io.K, want_n ? 1 : 0, dref, w.dD_R, w.dD_N, w.sd_N};
   BS_TRY(launch_attn_d(da, st));
 
-  BS_TRY(launch_attn_prep((const u16*)io.Q, (const u16*)io.Kt, (const u16*)io.dO, io.dO32, (int)bh, io.S, (int)Sp, w.Qt,
-                          w.Kt, w.dOp, w.dOt, st));
+  if (io.dO32) BS_TRY(launch_attn_split(io.dO32, (int)bh, io.S, (int)Sp, w.dOp, w.dOt, st));
   AttnBwdArgs ba{};
   ba.Qt = w.Qt;
   ba.Kt = w.Kt;

@@ -10,9 +10,11 @@ struct AttnArgs {
   const u16 *Q, *K, *V;  // [B*H][S][64] bf16
   int S, causal;
   float scale;
-  float* m;      // [B*H][S] row max of c S
-  float* l;      // [B*H][S] row sum of exp(c S - m)
+  float* m;      // [B*H][S] row max of c log2(e) S
+  float* l;      // [B*H][S] row sum of 2^(c log2(e) S - m)
   float* O_out;  // nullable [B*H][S][64] fp32
+  const u16* Vt; // V^T [B*H][64][Sp] (zero past S), from launch_attn_transpose
+  int Sp;
 };
 
 struct AttnDArgs {
@@ -53,9 +55,11 @@ struct AttnBwdArgs {
 
 bs_status launch_attn_fwd(const AttnArgs& a, int B, int H, hipStream_t st);
 bs_status launch_attn_d(const AttnDArgs& a, hipStream_t st);
-// Q^T, K^T, and the planes of the incoming gradient (and their transposes) for the backward.
-bs_status launch_attn_prep(const u16* Q, const u16* K, const u16* dO, const float* dO32, int BH, int S, int Sp,
-                           u16* Qt, u16* Kt, u16* const* dOp, u16* const* dOt, hipStream_t st);
+// X_i^T [BH][64][Sp] (zero past S) of n <= 4 bf16 X_i [BH][S][64] (16-byte aligned)
+bs_status launch_attn_transpose(const u16* const* X, u16* const* Xt, int n, int BH, int S, int Sp, hipStream_t st);
+// the three bf16 planes of an fp32 incoming gradient [BH][S][64] and their transposes
+bs_status launch_attn_split(const float* dO32, int BH, int S, int Sp, u16* const* dOp, u16* const* dOt,
+                            hipStream_t st);
 bs_status launch_attn_bwd(const AttnBwdArgs& a, int B, int H, hipStream_t st);
 
 }  // namespace bsp

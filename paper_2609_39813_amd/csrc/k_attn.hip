@@ -114,95 +114,6 @@ __device__ __forceinline__ float group16_sum(float v) {
 }
 
 // ------------------------------------------------------------------------------------
-// forward: row max m, row sum l (P = exp(c S - m) / l) and optionally O = P V
-// ------------------------------------------------------------------------------------
-template <bool WRITE_O>
-__global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 sQ[AT * AT], sK[AT * AT], sVt[AT * AT], sP[3][AT * AT];
-  // heaviest (most key blocks) first: blocks are dispatched in index order
-  const int bh = blockIdx.x, qb = a.causal ? (int)gridDim.y - 1 - (int)blockIdx.y : (int)blockIdx.y;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int q0 = qb * AT;
-  const int64_t hb = (int64_t)bh * a.S * AT;
-  load_tile(sQ, a.Q + hb, q0, a.S);
-  float mr[4], lr[4];
-  floatx4 acc[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    mr[r] = -INFINITY;
-    lr[r] = 0.0f;
-    acc[r] = floatx4{0.f, 0.f, 0.f, 0.f};
-  }
-  const int nkb = a.causal ? qb + 1 : (a.S + AT - 1) / AT;
-  for (int kb = 0; kb < nkb; ++kb) {
-    __syncthreads();
-    load_tile(sK, a.K + hb, kb * AT, a.S);
-    load_tile_t(sVt, a.V + hb, kb * AT, a.S);
-    __syncthreads();
-    floatx4 s[4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) s[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < AT; kk += 32) {
-      const bf16x8 fa = frag(sQ, 16 * w, kk, lane);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) s[t] = mfma(fa, frag(sK, 16 * t, kk, lane), s[t]);
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int ql = 16 * w + 4 * (lane >> 4) + r, q = q0 + ql;
-      float x[4];
-      float mx = -INFINITY;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int key = kb * AT + 16 * t + (lane & 15);
-        const bool ok = key < a.S && q < a.S && (!a.causal || key <= q);
-        x[t] = ok ? a.scale * s[t][r] : -INFINITY;
-        mx = fmaxf(mx, x[t]);
-      }
-      mx = group16_max(mx);
-      const float mn = fmaxf(mr[r], mx);
-      const float alpha = mn == -INFINITY ? 0.0f : (mr[r] == -INFINITY ? 0.0f : expf(mr[r] - mn));
-      float rs = 0.0f;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const float p = x[t] == -INFINITY ? 0.0f : expf(x[t] - mn);
-        rs += p;
-        put3(sP[0], sP[1], sP[2], ql, 16 * t + (lane & 15), p);
-      }
-      rs = group16_sum(rs);
-      lr[r] = lr[r] * alpha + rs;
-      mr[r] = mn;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) acc[t][r] *= alpha;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < AT; kk += 32) {
-#pragma unroll
-      for (int tm = 0; tm < 3; ++tm) {
-        const bf16x8 fa = frag(sP[tm], 16 * w, kk, lane);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) acc[t] = mfma(fa, frag(sVt, 16 * t, kk, lane), acc[t]);
-      }
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int q = q0 + 16 * w + 4 * (lane >> 4) + r;
-    if (q >= a.S) continue;
-    if ((lane & 15) == 0) {
-      a.m[(int64_t)bh * a.S + q] = mr[r];
-      a.l[(int64_t)bh * a.S + q] = lr[r];
-    }
-    if (WRITE_O) {
-#pragma unroll
-      for (int t = 0; t < 4; ++t) a.O_out[hb + (int64_t)q * AT + 16 * t + (lane & 15)] = acc[t][r] / lr[r];
-    }
-  }
-}
-
-// ------------------------------------------------------------------------------------
 // D variants, one row per 4 lanes (16 elements per lane, four Philox calls per trial):
 //   D_ref = sum dO O; dD_R = sum dO (s val(C_O) - O);
 //   dD_k  = sum dO (s val(C_k) - O) for new roundings k = 1..K, = A + s S_k with
@@ -309,8 +220,8 @@ __global__ __launch_bounds__(256) void attn_d_kernel(AttnDArgs a) {
 // their 8-byte units XOR-swizzled by (row & 15), so the 16 rows of a read phase hit distinct
 // banks. P and dS enter their products as three exact bf16 terms.
 // ------------------------------------------------------------------------------------
-// P = 2^(c log2(e) S - m log2(e)) / l: one hardware exp2 per element (relative error of a few
-// ulps; the exponent's rounding adds |m| 2^-24, below 1e-6 for the scores of these inputs)
+// P = 2^(c log2(e) S - m) / l with m the row max of c log2(e) S: one hardware exp2 per
+// element (a few ulps; the exponent's rounding adds |m| 2^-24, below 1e-6 for these scores)
 constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ int swt(int row, int unit) { return row * AT + ((unit ^ (row & 15)) << 2); }
@@ -321,13 +232,30 @@ __device__ __forceinline__ bf16x8 frag_t(const u16* T, int row, int s, int g) {
   return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
 }
 
-// the three bf16 terms of eight fp32 values as MFMA operands
+// the three bf16 terms (round to nearest, then the exact remainders) of eight fp32 values as
+// MFMA operands, converted two at a time into packed registers
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
+  const bf16x2 v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ float lo_f32(uint32_t p) { return __uint_as_float(p << 16); }
+__device__ __forceinline__ float hi_f32(uint32_t p) { return __uint_as_float(p & 0xFFFF0000u); }
 __device__ __forceinline__ void pack3(const float* v, bf16x8* t) {
-  u16 h[3][8];
+  uint32_t w[3][4];
 #pragma unroll
-  for (int q = 0; q < 8; ++q) split3(v[q], h[0][q], h[1][q], h[2][q]);
+  for (int i = 0; i < 4; ++i) {
+    const float a = v[2 * i], b = v[2 * i + 1];
+    const uint32_t p0 = pk_bf16(a, b);
+    const float ra = a - lo_f32(p0), rb = b - hi_f32(p0);
+    const uint32_t p1 = pk_bf16(ra, rb);
+    const float sa = ra - lo_f32(p1), sb = rb - hi_f32(p1);
+    w[0][i] = p0;
+    w[1][i] = p1;
+    w[2][i] = pk_bf16(sa, sb);
+  }
 #pragma unroll
-  for (int p = 0; p < 3; ++p) t[p] = __builtin_bit_cast(bf16x8, *(const uint4*)h[p]);
+  for (int p = 0; p < 3; ++p) t[p] = __builtin_bit_cast(bf16x8, make_uint4(w[p][0], w[p][1], w[p][2], w[p][3]));
 }
 
 // a row-major [64][64] bf16 tile (rows r0.. of a [*, 64] matrix with nrow rows, zeros past
@@ -363,6 +291,139 @@ __device__ __forceinline__ void tile_put_t(u16* T, const TileRegs& t) {
     const int r = (threadIdx.x >> 3) + 32 * i, u = (threadIdx.x & 7) * 2;
     *(uint2*)(T + swt(r, u)) = make_uint2(t.v[i].x, t.v[i].y);
     *(uint2*)(T + swt(r, u + 1)) = make_uint2(t.v[i].z, t.v[i].w);
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// forward: row max m, row sum l (P = exp(c S - m) / l) and optionally O = P V.
+// S^T = K Q^T puts keys on the k index of the P operand of P V (register resident, three
+// bf16 terms); wave w owns queries 16 w .. 16 w + 15, one per lane column.
+// ------------------------------------------------------------------------------------
+template <bool WRITE_O>
+__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) u16 sm[2][2][AT * AT];  // K, V^T
+  // heaviest (most key blocks) first: blocks are dispatched in index order
+  const int bh = blockIdx.x, qb = a.causal ? (int)gridDim.y - 1 - (int)blockIdx.y : (int)blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, c16 = lane & 15;
+  const int q0 = qb * AT;
+  const int64_t hb = (int64_t)bh * a.S * AT, tb = (int64_t)bh * AT * a.Sp;
+  const int q = q0 + 16 * w + c16;
+  const bool qok = q < a.S;
+  bf16x8 fq[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+    fq[s] = __builtin_bit_cast(bf16x8, qok ? *(const uint4*)(a.Q + hb + (int64_t)q * AT + 32 * s + 8 * g)
+                                           : make_uint4(0, 0, 0, 0));
+  const float c2 = a.scale * kLog2e;
+  float m2 = -INFINITY, l = 0.0f;  // running max of c log2(e) S and sum, for query q (this lane's column)
+  floatx4 acc[4];
+#pragma unroll
+  for (int n = 0; n < 4; ++n) acc[n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  TileRegs pf[2];
+  auto fetch = [&](int k0) {
+    tile_fetch(pf[0], a.K + hb, k0, a.S);
+    tile_fetch_t(pf[1], a.Vt + tb, k0, a.Sp);
+  };
+  auto put = [&](int st) {
+    tile_put(sm[st][0], pf[0]);
+    tile_put_t(sm[st][1], pf[1]);
+  };
+  const int nkb = a.causal ? qb + 1 : (a.S + AT - 1) / AT;
+  fetch(0);
+  put(0);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int st = kb & 1, k0 = kb * AT;
+    if (kb + 1 < nkb) fetch(k0 + AT);
+    const u16* tK = sm[st][0];
+    const u16* tVt = sm[st][1];
+    floatx4 sv[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) sv[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) sv[t] = mfma(*(const bf16x8*)(tK + sw(16 * t + c16, 32 * s + 8 * g)), fq[s], sv[t]);
+    // masks only where the block crosses S or the causal diagonal (a uniform test)
+    const bool full = k0 + AT <= a.S && q0 + AT <= a.S && (!a.causal || k0 + AT - 1 <= q0);
+    float x[4][4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) x[t][r] = c2 * sv[t][r];
+    if (!full) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = k0 + 16 * t + 4 * g + r;
+          x[t][r] = (key < a.S && qok && (!a.causal || key <= q)) ? x[t][r] : -INFINITY;
+        }
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) mx = fmaxf(mx, x[t][r]);
+    // over the four lane groups of this query column
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mn = fmaxf(m2, mx);
+    const float alpha = (mn == -INFINITY || m2 == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m2 - mn);
+    float p[4][4], rs = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        // a row with no key yet has mn = -inf; its masked entries must not give 2^NaN
+        p[t][r] = __builtin_amdgcn_exp2f(mn == -INFINITY ? -INFINITY : x[t][r] - mn);
+        rs += p[t][r];
+      }
+    rs += __shfl_xor(rs, 16, 64);
+    rs += __shfl_xor(rs, 32, 64);
+    l = l * alpha + rs;
+    m2 = mn;
+    if (WRITE_O) {
+      // the accumulator rows are queries 16 w + 4 g + r: their rescale factors live in the
+      // lanes whose column is that query
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float ar = __shfl(alpha, 4 * g + r, 64);
+#pragma unroll
+        for (int n = 0; n < 4; ++n) acc[n][r] *= ar;
+      }
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        float vp[8];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) vp[v] = p[2 * s + (v >> 2)][v & 3];
+        bf16x8 tp[3];
+        pack3(vp, tp);
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+          const bf16x8 fv = frag_t(tVt, 16 * n + c16, s, g);
+#pragma unroll
+          for (int j = 0; j < 3; ++j) acc[n] = mfma(tp[j], fv, acc[n]);
+        }
+      }
+    }
+    if (kb + 1 < nkb) put(st ^ 1);
+    __syncthreads();
+  }
+  const int64_t rb = (int64_t)bh * a.S;
+  if (qok && g == 0) {
+    a.m[rb + q] = m2;
+    a.l[rb + q] = l;
+  }
+  if (WRITE_O) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int qr = q0 + 16 * w + 4 * g + r;
+      const float lr = __shfl(l, 4 * g + r, 64);
+      if (qr >= a.S) continue;
+#pragma unroll
+      for (int n = 0; n < 4; ++n) a.O_out[hb + (int64_t)qr * AT + 16 * n + c16] = acc[n][r] / lr;
+    }
   }
 }
 
@@ -409,7 +470,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
     if (threadIdx.x < AT) {
       const int q = q0 + threadIdx.x;
       const bool ok = q < a.S;
-      prow[0] = ok ? a.m[rb + q] * kLog2e : 0.0f;
+      prow[0] = ok ? a.m[rb + q] : 0.0f;
       prow[1] = ok ? 1.0f / a.l[rb + q] : 0.0f;
       prow[2] = ok ? a.D_ref[rb + q] : 0.0f;
       prow[3] = (ok && a.dD_R) ? a.dD_R[rb + q] : 0.0f;
@@ -457,18 +518,30 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
           dp[t] = mfma(*(const bf16x8*)(sm[st][2 + i] + sw(16 * t + c16, 32 * s + 8 * g)), fv[s], dp[t]);
       }
     }
+    // masks only where the block crosses S or the causal diagonal (a uniform test)
+    const bool full = k0 + AT <= a.S && q0 + AT <= a.S && (!a.causal || k0 + AT - 1 <= q0);
     float p[4][4], ds[4][4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) p[t][r] = fmaf(c2, sv[t][r], -rows[st][0][16 * t + 4 * g + r]);
+    if (!full) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int q = q0 + 16 * t + 4 * g + r;
+          p[t][r] = (key < a.S && q < a.S && (!a.causal || key <= q)) ? p[t][r] : -INFINITY;  // 2^-inf = 0
+        }
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int ql = 16 * t + 4 * g + r, q = q0 + ql;
-        const bool ok = key < a.S && q < a.S && (!a.causal || key <= q);
-        const float pv = ok ? __builtin_amdgcn_exp2f(fmaf(c2, sv[t][r], -rows[st][0][ql])) * rows[st][1][ql] : 0.0f;
-        p[t][r] = pv;
-        ds[t][r] = ok ? pv * (dp[t][r] - rows[st][2][ql]) : 0.0f;
+        const int ql = 16 * t + 4 * g + r;
+        p[t][r] = __builtin_amdgcn_exp2f(p[t][r]) * rows[st][1][ql];
+        ds[t][r] = p[t][r] * (dp[t][r] - rows[st][2][ql]);
       }
-    }
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       float vp[8], vd[8];
@@ -564,7 +637,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
       fdo[i][s] = __builtin_bit_cast(bf16x8, qok ? *(const uint4*)(src + e) : make_uint4(0, 0, 0, 0));
     }
   }
-  const float mq = qok ? a.m[rb + q] * kLog2e : 0.0f;
+  const float mq = qok ? a.m[rb + q] : 0.0f;
   const float c2 = a.scale * kLog2e;
   const float ilq = qok ? 1.0f / a.l[rb + q] : 0.0f;
   const float dq_ref = qok ? a.D_ref[rb + q] : 0.0f;
@@ -606,18 +679,29 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
         for (int i = 0; i < NDO; ++i) dp[t] = mfma(fvv, fdo[i][s], dp[t]);
       }
     }
+    // masks only where the block crosses S or the causal diagonal (a uniform test)
+    const bool full = k0 + AT <= a.S && q0 + AT <= a.S && (!a.causal || k0 + AT - 1 <= q0);
     float p[4][4], ds[4][4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) p[t][r] = fmaf(c2, sv[t][r], -mq);
+    if (!full) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int kk = k0 + 16 * t + 4 * g + r;
+          p[t][r] = (kk < a.S && qok && (!a.causal || kk <= q)) ? p[t][r] : -INFINITY;  // 2^-inf = 0
+        }
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int kk = k0 + 16 * t + 4 * g + r;
-        const bool ok = kk < a.S && qok && (!a.causal || kk <= q);
-        const float pv = ok ? __builtin_amdgcn_exp2f(fmaf(c2, sv[t][r], -mq)) * ilq : 0.0f;
-        p[t][r] = pv;
-        ds[t][r] = ok ? pv * (dp[t][r] - dq_ref) : 0.0f;
+        p[t][r] = __builtin_amdgcn_exp2f(p[t][r]) * ilq;
+        ds[t][r] = p[t][r] * (dp[t][r] - dq_ref);
       }
-    }
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       float vp[8], vd[8];
@@ -727,16 +811,57 @@ bs_status launch_attn_d(const AttnDArgs& a, hipStream_t st) {
   return BS_OK;
 }
 
-bs_status launch_attn_prep(const u16* Q, const u16* K, const u16* dO, const float* dO32, int BH, int S, int Sp,
-                           u16* Qt, u16* Kt, u16* const* dOp, u16* const* dOt, hipStream_t st) {
+// X^T [BH][64][Sp] of up to four bf16 X [BH][S][64] (one per grid z): a 64 x 64 tile through
+// LDS with 16-byte accesses on both sides; chunk c of tile row r sits at c ^ ((r >> 3) & 7), so
+// the column reads of eight rows 8 apart fall on distinct banks
+struct TransposeJobs {
+  const u16* x[4];
+  u16* xt[4];
+};
+__global__ __launch_bounds__(256) void attn_transpose_kernel(TransposeJobs jobs, int S, int Sp) {
+  __shared__ __attribute__((aligned(16))) u16 t[AT * AT];
+  const int r0 = blockIdx.x * AT, bh = blockIdx.y;
+  const u16* __restrict__ x = jobs.x[blockIdx.z];
+  u16* __restrict__ xt = jobs.xt[blockIdx.z];
+  const int64_t hb = (int64_t)bh * S * AT, tb = (int64_t)bh * AT * Sp;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (threadIdx.x >> 3) + 32 * i, c = threadIdx.x & 7;
+    const uint4 v = r0 + r < S ? *(const uint4*)(x + hb + (int64_t)(r0 + r) * AT + 8 * c) : make_uint4(0, 0, 0, 0);
+    *(uint4*)(t + r * AT + 8 * (c ^ ((r >> 3) & 7))) = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int d = (threadIdx.x >> 3) + 32 * i, m = threadIdx.x & 7;  // output row d, rows 8 m .. 8 m + 7
+    u16 o[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      const int r = 8 * m + v;
+      o[v] = t[r * AT + 8 * ((d >> 3) ^ m) + (d & 7)];
+    }
+    *(uint4*)(xt + tb + (int64_t)d * Sp + r0 + 8 * m) = *(const uint4*)o;
+  }
+}
+
+bs_status launch_attn_transpose(const u16* const* X, u16* const* Xt, int n, int BH, int S, int Sp, hipStream_t st) {
+  if (n < 1 || n > 4) return BS_EINVAL;
+  TransposeJobs jobs{};
+  for (int i = 0; i < n; ++i) {
+    jobs.x[i] = X[i];
+    jobs.xt[i] = Xt[i];
+  }
+  ProfScope prof("attn_prep", st);
+  attn_transpose_kernel<<<dim3((unsigned)(Sp / AT), (unsigned)BH, (unsigned)n), 256, 0, st>>>(jobs, S, Sp);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+bs_status launch_attn_split(const float* dO32, int BH, int S, int Sp, u16* const* dOp, u16* const* dOt,
+                            hipStream_t st) {
   dim3 grid((unsigned)(Sp / AT), (unsigned)BH);
   ProfScope prof("attn_prep", st);
-  attn_prep_kernel<u16><<<grid, 256, 0, st>>>(Q, S, Sp, Qt, nullptr, nullptr, nullptr, nullptr, nullptr);
-  attn_prep_kernel<u16><<<grid, 256, 0, st>>>(K, S, Sp, Kt, nullptr, nullptr, nullptr, nullptr, nullptr);
-  if (dO32)
-    attn_prep_kernel<float><<<grid, 256, 0, st>>>(dO32, S, Sp, dOt[0], dOt[1], dOt[2], dOp[0], dOp[1], dOp[2]);
-  else if (dO)
-    attn_prep_kernel<u16><<<grid, 256, 0, st>>>(dO, S, Sp, dOt[0], nullptr, nullptr, nullptr, nullptr, nullptr);
+  attn_prep_kernel<float><<<grid, 256, 0, st>>>(dO32, S, Sp, dOt[0], dOt[1], dOt[2], dOp[0], dOp[1], dOp[2]);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
