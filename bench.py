@@ -23,16 +23,37 @@ sys.path.insert(0, ROOT)
 # Peak figures of one MI355X (AMD public specification).
 HBM_PEAK_GBPS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
-# One 32-bit VALU operation per lane per clock: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
-# (the non-packed half of the 157.3 TFLOP/s fp32 figure, counting an FMA as 2 flops).
-VALU_LANE_OPS = 256 * 64 * 2.4e9
-# Operations of one element-trial of stochastic rounding: a quarter of a Philox4x32-10
-# call (10 rounds x (2 multiplies 32x32->64 + 2 three-input xors) for 4 words; the key
-# schedule is uniform and runs on the scalar unit) plus the threshold test and the count
-# update: 5 + 5 + 2 = 12, each counted as one lane operation.
-OPS_PER_ELEMENT_TRIAL = 12
-# Ceiling on element-trials per second: 3.28e12.
+# VALU issue: one wave64 instruction per SIMD every 4 clocks (16 lanes), i.e. one 32-bit lane
+# operation per lane-slot per clock: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.32e12.
+VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
+# VALU instructions per element-trial of the K-trial counter as compiled for gfx950: one pass of
+# its trial loop (4 trials x 32 elements per lane) issues 544 v_mad_u64_u32 + 608 v_bitop3_b32
+# (Philox4x32-10; the key schedule and the uniform counter words run on the scalar unit) +
+# 128 v_add_co_u32 (round-up carry) + 128 v_addc_co_u32 (count) = 1408 / 128 = 11.0.
+# (Written out, Philox needs 10 multiplies and 10 xors per 4 words: 12 per element-trial.)
+OPS_PER_ELEMENT_TRIAL = 1408 / 128
+# Ceiling on element-trials per second: 3.57e12.
 ALU_PEAK_ETPS = VALU_LANE_OPS / OPS_PER_ELEMENT_TRIAL
+
+# HBM bytes per launch of the counter at the benchmark shape, from two rocprofv3 --pmc passes
+# (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) over this script, each scaled by what the
+# counter reads for the 256 MiB device copy at the end of this script: FETCH_SIZE read
+# 131084 KiB for 262144 KiB copied (x 2.000), WRITE_SIZE 262144 KiB (x 1.000). The counter
+# read 16558 KiB fetched and 16384 KiB written. Valid only for the kernel source it was
+# measured on (SHA-256 prefix of csrc/k_store.hip + bsp_common.h + bsp_kernels.h, in that
+# order); otherwise reported as null.
+TRAFFIC_BYTES = (16558 * 2.000 + 16384 * 1.000) * 1024
+TRAFFIC_SOURCES = ("k_store.hip", "bsp_common.h", "bsp_kernels.h")
+TRAFFIC_SHA256 = "e8988545a180bf9f"
+
+
+def traffic_if_current():
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_39813_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return TRAFFIC_BYTES if h.hexdigest()[:16] == TRAFFIC_SHA256 else None
 
 
 def parse():
@@ -75,36 +96,7 @@ def cpu_baseline(cfg, X, g, W, dY, rows):
                        f"{t2:.1f} s; linear extrapolation to all {cfg['d']} rows = {full:.0f} s per step")}
 
 
-def side_measurements(bsp, synth, torch, dev, reps=5):
-    """The metric's other two figures, timed live with HIP events: the FP8 store's HBM rate
-    on the 16384 x 8192 bf16 gradient (E5M2, SR) and the attention backward's MFMA rate at
-    B4 H16 S1024 d64 (causal, three D policies, K = 32)."""
-    out = {}
-    cfg4 = synth.CONFIGS[4]
-    _, _, dy, _, _ = synth.linear_bwd_inputs(cfg4["M"], cfg4["k"], cfg4["n"], torch.bfloat16, 4)
-    dy = dy.to(dev)
-    n = dy.numel()
-    bsp.qround(dy, "e5m2", "sr", seed=cfg4["seed"], trial=1, use=1)
-    torch.cuda.synchronize()
-    bsp.profile_enable(True)
-    for _ in range(reps):
-        bsp.qround(dy, "e5m2", "sr", seed=cfg4["seed"], trial=1, use=1)
-    torch.cuda.synchronize()
-    am_ms, am_n = bsp.profile_read("amax")
-    q_ms, q_n = bsp.profile_read("quantize")
-    bsp.profile_enable(False)
-    am_s, q_s = am_ms / am_n / 1e3, q_ms / q_n / 1e3
-    out["qround_e5m2_16384x8192"] = {
-        "amax_GBps": round(2 * n / am_s / 1e9, 1), "amax_hbm_frac": round(2 * n / am_s / 1e9 / HBM_PEAK_GBPS, 4),
-        "quantize_GBps": round(3 * n / q_s / 1e9, 1), "quantize_hbm_frac": round(3 * n / q_s / 1e9 / HBM_PEAK_GBPS, 4),
-        "bytes": "amax reads 2 B/elem; quantize reads 2 B and writes 1 B per element", "elements": n}
-    del dy
-    cfg3 = synth.CONFIGS[3]
-    Q, K, V, dO = (t.to(dev) for t in synth.attention_inputs(cfg3["B"], cfg3["H"], cfg3["S"], cfg3["dh"],
-                                                             cfg3["dtype"], 3))
-    ws = bsp.attn_workspace(cfg3["B"], cfg3["H"], cfg3["S"], cfg3["dh"], 3, cfg3["K"], dev)
-    run = lambda: bsp.attn_bwd_policy(Q, K, V, dO, causal=True, policies=cfg3["policies"], K=cfg3["K"],
-                                      seed=cfg3["seed"], fwd_mode=cfg3["fwd_mode"], ws=ws)
+def _timed(bsp, torch, run, names, reps):
     run()
     torch.cuda.synchronize()
     bsp.profile_enable(True)
@@ -113,20 +105,96 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
         run()
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / reps
-    b_ms, b_n = bsp.profile_read("attn_bwd")
-    f_ms, f_n = bsp.profile_read("attn_fwd")
+    prof = {k: bsp.profile_read(k) for k in names}
     bsp.profile_enable(False)
+    return wall, {k: v[0] / reps for k, v in prof.items()}  # ms per call
+
+
+def side_measurements(bsp, synth, torch, dev, reps=5):
+    """The metric's other figures and the other scope rows, timed live with HIP events: the FP8
+    store's HBM rate on the 16384 x 8192 bf16 gradient (E5M2, SR); the attention backward's MFMA
+    rate at B4 H16 S1024 d64 (causal, D read by U / R / N, K = 32); the E5M2 Linear backward at
+    16384 x 2048 x 8192 (shared and per-use new roundings, K = 64); one decoder layer at
+    B8 S2048 d1024 H16 F4096 (K = 16, all four stores, every use)."""
+    out = {}
+    cfg4 = synth.CONFIGS[4]
+    X4, W4, dy4, _, _ = synth.linear_bwd_inputs(cfg4["M"], cfg4["k"], cfg4["n"], torch.bfloat16, 4)
+    dy = dy4.to(dev)
+    n = dy.numel()
+    wall, t = _timed(bsp, torch, lambda: bsp.qround(dy, "e5m2", "sr", seed=cfg4["seed"], trial=1, use=1),
+                     ("amax", "quantize"), reps)
+    am_s, q_s = t["amax"] / 1e3, t["quantize"] / 1e3
+    out["qround_e5m2_16384x8192"] = {
+        "amax_GBps": round(2 * n / am_s / 1e9, 1), "amax_hbm_frac": round(2 * n / am_s / 1e9 / HBM_PEAK_GBPS, 4),
+        "quantize_GBps": round(3 * n / q_s / 1e9, 1), "quantize_hbm_frac": round(3 * n / q_s / 1e9 / HBM_PEAK_GBPS, 4),
+        "bytes": "amax reads 2 B/elem; quantize reads 2 B and writes 1 B per element", "elements": n}
+
+    # E5M2 Linear backward (dX = deq(C) W^T, dW = X^T deq(C), shared / per-use new roundings)
+    Xd, Wd = X4.to(dev), W4.to(dev)
+    del X4, W4, dy4
+    lws = bsp.linear_bwd_workspace(cfg4["M"], cfg4["k"], cfg4["n"], len(cfg4["sharings"]), cfg4["K"], dev)
+    wall, t = _timed(bsp, torch, lambda: bsp.linear_bwd_policy(Xd, Wd, dy, fmt="e5m2", sharings=cfg4["sharings"],
+                                                                K=cfg4["K"], seed=cfg4["seed"], ws=lws),
+                     ("gemm", "gemm_split_sum", "fresh_count", "amax", "quantize"), 3)
+    mnk2 = 2.0 * cfg4["M"] * cfg4["k"] * cfg4["n"]
+    segs = 11  # dX_ref, dW_ref, dX bias (3 residual terms), dW bias shared (3), dW bias per use (3)
+    g_s = (t["gemm"] + t["gemm_split_sum"]) / 1e3
+    out["linear_bwd_e5m2_16384x2048x8192"] = {
+        "policy_trials_per_s": round(len(cfg4["sharings"]) * cfg4["K"] / wall, 1), "call_ms": round(wall * 1e3, 3),
+        "gemm_TFLOPs": round(segs * mnk2 / g_s / 1e12, 1),
+        "gemm_mfma_frac": round(segs * mnk2 / g_s / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+        "kernel_ms": {k: round(v, 4) for k, v in t.items()},
+        "flops": "11 bf16 contractions of 2 M k n each (references and residual terms)"}
+    del Xd, Wd, dy, lws
+    torch.cuda.empty_cache()
+
+    cfg3 = synth.CONFIGS[3]
+    Q, K, V, dO = (t_.to(dev) for t_ in synth.attention_inputs(cfg3["B"], cfg3["H"], cfg3["S"], cfg3["dh"],
+                                                               cfg3["dtype"], 3))
+    ws = bsp.attn_workspace(cfg3["B"], cfg3["H"], cfg3["S"], cfg3["dh"], 3, cfg3["K"], dev)
+    wall, t = _timed(bsp, torch, lambda: bsp.attn_bwd_policy(Q, K, V, dO, causal=True, policies=cfg3["policies"],
+                                                              K=cfg3["K"], seed=cfg3["seed"], fwd_mode=cfg3["fwd_mode"],
+                                                              ws=ws),
+                     ("attn_bwd", "attn_fwd", "attn_d", "attn_prep"), reps)
     heads, S, dh = cfg3["B"] * cfg3["H"], cfg3["S"], cfg3["dh"]
     # causal matmul of S x S x dh: S^2 dh flops; reference backward (S, dP, dV, dQ, dK) + 3 bias
     # contractions (G = P K and the two dK bias terms)
     flops = 8 * heads * S * S * dh
-    b_s = b_ms / b_n / 1e3
+    b_s = t["attn_bwd"] / 1e3
     out["attn_bwd_b4_h16_s1024_d64"] = {
         "TFLOPs": round(flops / b_s / 1e12, 1), "mfma_frac": round(flops / b_s / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
-        "bwd_ms": round(b_s * 1e3, 4), "fwd_ms": round(f_ms / f_n, 4), "call_ms": round(wall * 1e3, 4),
+        "bwd_ms": round(b_s * 1e3, 4), "fwd_ms": round(t["attn_fwd"], 4), "d_ms": round(t["attn_d"], 4),
+        "call_ms": round(wall * 1e3, 4),
         "policy_trials_per_s": round(len(cfg3["policies"]) * cfg3["K"] / wall, 1),
         "flops": "8 causal S x S x dh matmuls per head (5 of the reference backward + 3 bias contractions)"}
+    del Q, K, V, dO, ws
+    torch.cuda.empty_cache()
+
+    # one decoder layer with four stores and the per-use check of each
+    cfg5 = synth.CONFIGS[5]
+    (x, p, dOut), (B, S5, H) = synth.decoder_inputs(cfg5["B"], cfg5["S"], cfg5["d"], cfg5["H"], cfg5["F"], config=5)
+    xd, pd, dOd = x.to(dev), {k: v.to(dev) for k, v in p.items()}, dOut.to(dev)
+    lws = bsp.decoder_layer_workspace(B, S5, cfg5["d"], H, cfg5["F"], cfg5["K"], dev)
+    wall, t = _timed(bsp, torch, lambda: bsp.decoder_layer_policy(xd, pd, dOd, B=B, S=S5, H=H, fmt="e4m3",
+                                                                   fwd_mode=cfg5["fwd_mode"], K=cfg5["K"],
+                                                                   seed=cfg5["seed"], ws=lws),
+                     ("gemm", "gemm_split_sum", "attn_bwd", "attn_fwd", "attn_d", "fresh_count", "fresh_count_se"), 3)
+    out["decoder_layer_b8_s2048_d1024_h16_f4096"] = {
+        "call_ms": round(wall * 1e3, 3), "policy_trials_per_s": round(3 * cfg5["K"] / wall, 1),
+        "kernel_ms": {k: round(v, 4) for k, v in t.items()},
+        "work": "forward, reference backward, and U/R/N at the 10 uses of the 4 stores, K = 16"}
+    del xd, pd, dOd, lws
+    torch.cuda.empty_cache()
     return out
+
+
+def calibration_copy(torch, dev):
+    """A plain 256 MiB device copy (read 256 MiB, write 256 MiB): the reference that scales the
+    HBM byte counters of the profiler passes over this script."""
+    src = torch.full((64 << 20,), 1.0, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
 
 
 def main():
@@ -157,7 +225,8 @@ def main():
         step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    prof = {k: bsp.profile_read(k) for k in ("fresh_count", "fresh_count_se", "gemm", "quantize", "rmsnorm_fwd")}
+    prof = {k: bsp.profile_read(k) for k in ("fresh_count", "fresh_count_se", "gemm", "gemm_split_sum", "quantize",
+                                             "rmsnorm_fwd")}
     bsp.profile_enable(False)
 
     ms_per_step = elapsed / args.steps * 1e3
@@ -168,9 +237,12 @@ def main():
     fc_avg_s = fc_ms / max(fc_n, 1) / 1e3
     et_per_launch = cfg["T"] * cfg["d"] * cfg["K"]
     achieved = et_per_launch / fc_avg_s / 1e9 if fc_n else 0.0
-    roofline = {"bound": "alu", "kernel": "fresh_count_kernel<false>", "achieved": round(achieved, 1),
+    traffic = traffic_if_current()
+    roofline = {"bound": "alu", "kernel": "fresh_count_kernel<float, FC_COUNT>", "achieved": round(achieved, 1),
                 "peak": round(ALU_PEAK_ETPS / 1e9, 1), "unit": "Gelement-trials/s",
-                "frac": round(achieved * 1e9 / ALU_PEAK_ETPS, 4), "traffic": None,
+                "frac": round(achieved * 1e9 / ALU_PEAK_ETPS, 4), "traffic": traffic,
+                "traffic_unit": "bytes per launch (HBM, profiler counters scaled by a known copy)",
+                "algorithmic_bytes": cfg["T"] * cfg["d"] * (4 + 2),
                 "avg_launch_ms": round(fc_avg_s * 1e3, 4), "launches": fc_n,
                 "work_per_launch": f"{et_per_launch} element-trials ({cfg['T']}x{cfg['d']} elements x K={cfg['K']})"}
     se_ms, se_n = prof["fresh_count_se"]
@@ -178,6 +250,7 @@ def main():
     q_ms, q_n = prof["quantize"]
     q_bytes = cfg["T"] * cfg["d"] * (4 + 1)           # read u fp32, write codes
     g_ms, g_n = prof["gemm"]
+    g_ms += prof["gemm_split_sum"][0]
     # contractions per step: du, dW_ref, Y, U-bias (3 bf16 terms), N-bias: 7 x 2 T d n
     g_flops = 7 * 2.0 * cfg["T"] * cfg["d"] * cfg["n"] * args.steps
     extra = {"quantize_GBps": round(q_bytes / (q_ms / max(q_n, 1) / 1e3) / 1e9, 1) if q_n else None,
@@ -189,6 +262,7 @@ def main():
              "path": "collapsed (per-element up-counts; se at the gain use from per-trial sums)"}
 
     extra.update(side_measurements(bsp, synth, torch, dev))
+    calibration_copy(torch, dev)
 
     line = {"metric": "policy-trials/sec", "value": round(value, 1), "unit": "policy-trials/s", "n_gpus": 1,
             "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
