@@ -206,7 +206,7 @@ LayerWs carve_layer(Carver& c, int B, int S, int d, int H, int F, int K) {
   w.k_bias = c.take<float>(3 * Td);
   w.wo_bias = c.take<float>(3 * (int64_t)d * d);
   w.wd_bias = c.take<float>(3 * (int64_t)F * d);
-  w.part = c.take<double>(1024);
+  w.part = c.take<double>(sumsq_part_size());
   w.diag = c.take<bs_diag>(4);
   w.sub_bytes = sub_ws_size(B, S, d, H, F, K);
   w.sub = c.take<char>(w.sub_bytes);
@@ -387,36 +387,41 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
   if (grads.dx) BS_TRY(launch_add(w.dh, BS_F32, w.dxn1, grads.dx, Td, st));
   if (grads.dWg || grads.dWu) BS_TRY(launch_split_cols(w.dWgu, grads.dWg, grads.dWu, d, F, st));
 
-  // ---------------- table: sums of squares (fp64, fixed order) ----------------
-  const double nan = __builtin_nan("");
+  // ---------------- table: sums of squares (fp64, fixed order), one batch ----------------
   // se argument: a device array, or kZero (the letter has no spread) / kNaN (no estimate here)
   const float* const kZero = (const float*)1;
   const float* const kNaN = (const float*)2;
-  auto row = [&](int r, int l, const float* bias, const float* ref, const float* se, int64_t n) -> bs_status {
+  SumsqBatch batch{};
+  auto put = [&](const float* x, int64_t n, double* out) { batch.job[batch.count++] = SumsqJob{x, n, out}; };
+  auto row = [&](int r, int l, const float* bias, const float* ref, const float* se, int64_t n) {
     double* out = table + ((int64_t)r * 3 + l) * 3;
     if (!bias) {
-      for (int q = 0; q < 3; ++q) BS_TRY(launch_set_f64(out + q, nan, st));
-      return BS_OK;
+      for (int q = 0; q < 3; ++q) put(nullptr, 0, out + q);
+      return;
     }
-    BS_TRY(launch_sumsq(bias, n, w.part, out + 0, st));
-    BS_TRY(launch_sumsq(ref, n, w.part, out + 1, st));
-    if (se == kZero) return launch_set_f64(out + 2, 0.0, st);
-    if (se == kNaN) return launch_set_f64(out + 2, nan, st);
-    return launch_sumsq(se, n, w.part, out + 2, st);
+    put(bias, n, out + 0);
+    put(ref, n, out + 1);
+    if (se == kZero)
+      put(nullptr, 1, out + 2);
+    else if (se == kNaN)
+      put(nullptr, 0, out + 2);
+    else
+      put(se, n, out + 2);
   };
   for (int l = 0; l < 3; ++l) {  // npol[l] reads letter l at the gain and weight uses
     const float* wse = l == 2 ? kNaN : kZero;
-    BS_TRY(row(0, l, w.e1.g_bias + l * d, dgain1, l == 2 ? w.e1.g_se + l * d : kZero, d));
-    BS_TRY(row(1, l, w.e1.w_bias + l * d3d, dWqkv, wse, d3d));
-    BS_TRY(row(2, l, l == 2 ? nullptr : w.e1.x_bias + (l == 0 ? 0 : 3) * Td, w.dxn1, kZero, Td));
-    BS_TRY(row(3, l, w.q_bias + l * Td, w.dQ, l == 2 ? w.q_se + l * Td : kZero, Td));
-    BS_TRY(row(4, l, w.k_bias + l * Td, w.dK, wse, Td));
-    BS_TRY(row(5, l, w.wo_bias + l * dd, dWo, wse, dd));
-    BS_TRY(row(6, l, w.e2.g_bias + l * d, dgain2, l == 2 ? w.e2.g_se + l * d : kZero, d));
-    BS_TRY(row(7, l, w.e2.w_bias + l * d2F, w.dWgu, wse, d2F));
-    BS_TRY(row(8, l, l == 2 ? nullptr : w.e2.x_bias + (l == 0 ? 0 : 3) * Td, w.dxn2, kZero, Td));
-    BS_TRY(row(9, l, w.wd_bias + l * Fd, dWd, wse, Fd));
+    row(0, l, w.e1.g_bias + l * d, dgain1, l == 2 ? w.e1.g_se + l * d : kZero, d);
+    row(1, l, w.e1.w_bias + l * d3d, dWqkv, wse, d3d);
+    row(2, l, l == 2 ? nullptr : w.e1.x_bias + (l == 0 ? 0 : 3) * Td, w.dxn1, kZero, Td);
+    row(3, l, w.q_bias + l * Td, w.dQ, l == 2 ? w.q_se + l * Td : kZero, Td);
+    row(4, l, w.k_bias + l * Td, w.dK, wse, Td);
+    row(5, l, w.wo_bias + l * dd, dWo, wse, dd);
+    row(6, l, w.e2.g_bias + l * d, dgain2, l == 2 ? w.e2.g_se + l * d : kZero, d);
+    row(7, l, w.e2.w_bias + l * d2F, w.dWgu, wse, d2F);
+    row(8, l, l == 2 ? nullptr : w.e2.x_bias + (l == 0 ? 0 : 3) * Td, w.dxn2, kZero, Td);
+    row(9, l, w.wd_bias + l * Fd, dWd, wse, Fd);
   }
+  BS_TRY(launch_sumsq_batch(batch, w.part, st));
   return BS_OK;
 }
 

@@ -132,7 +132,10 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs g) {
 // ------------------------------------------------------------------------------------
 // pipelined kernel
 // ------------------------------------------------------------------------------------
-constexpr int LBK = 32, LNST = 4;
+#ifndef BSP_GEMM_STAGES
+#define BSP_GEMM_STAGES 4
+#endif
+constexpr int LBK = 32, LNST = BSP_GEMM_STAGES;
 
 __device__ __forceinline__ int lds_swz(int r, int c) { return r * 64 + ((c ^ ((r >> 1) & 3)) << 4); }
 
@@ -229,25 +232,27 @@ __global__ __launch_bounds__(256) void gemm_lds_kernel(GemmArgs g, int cps) {
   };
   // wait until chunk c has landed (at most the loads of the chunks issued after it pending),
   // then a barrier without a memory fence (the fence would drain the prefetches too)
-  auto land = [&](int c) {
-    const int after = min(n - 1, c + 1) - c;  // chunks issued after c when c is awaited
-    if (after >= 1)
+  auto wait_chunks = [&](int after) {  // at most `after` chunks' loads still pending
+    static_assert(LNST >= 3 && LNST <= 5, "waits below cover up to three chunks in flight");
+    if (LNST >= 5 && after >= 3)
+      BS_WAIT_VM(3 * LPC);
+    else if (LNST >= 4 && after >= 2)
+      BS_WAIT_VM(2 * LPC);
+    else if (after >= 1)
       BS_WAIT_VM(LPC);
     else
       BS_WAIT_VM(0);
+  };
+  auto land = [&](int x) {
+    // chunks issued when x is awaited: up to min(n - 1, x + LNST - 3)
+    wait_chunks(min(n - 1, x + LNST - 3) - x);
     asm volatile("s_barrier" ::: "memory");
   };
 
 #pragma unroll
   for (int st = 0; st < LNST - 1; ++st)
     if (st < n) issue(st);
-  // chunk 0: at most chunks 1 and 2 pending
-  if (n >= 3)
-    BS_WAIT_VM(2 * LPC);
-  else if (n == 2)
-    BS_WAIT_VM(LPC);
-  else
-    BS_WAIT_VM(0);
+  wait_chunks(min(n - 1, LNST - 2));  // chunk 0 with chunks 1 .. LNST - 2 still in flight
   asm volatile("s_barrier" ::: "memory");
   read_frags(0, fa[0], fb[0]);
 

@@ -17,7 +17,19 @@ bs_status launch_split_cols(const float* in, float* A, float* B, int64_t rows, i
 bs_status launch_swiglu_fwd(const float* gh, float* a, int64_t T, int64_t F, hipStream_t st);
 bs_status launch_swiglu_bwd(const float* da, const float* gh, float* dgh, int64_t T, int64_t F, hipStream_t st);
 bs_status launch_add(const void* a, bs_dtype at, const float* b, float* out, int64_t n, hipStream_t st);
-bs_status launch_sumsq(const float* x, int64_t n, double* part, double* out, hipStream_t st);
-bs_status launch_set_f64(double* p, double v, hipStream_t st);
+// Batched sums of squares (fp64, fixed order): job i writes sum x^2 over n floats to out, or
+// NaN (x == nullptr, n == 0) or 0 (x == nullptr, n == 1). Two launches for the whole batch.
+constexpr int SUMSQ_MAX = 96, SUMSQ_BLOCKS = 256;
+struct SumsqJob {
+  const float* x;
+  int64_t n;
+  double* out;
+};
+struct SumsqBatch {
+  SumsqJob job[SUMSQ_MAX];
+  int count;
+};
+inline size_t sumsq_part_size() { return (size_t)SUMSQ_MAX * SUMSQ_BLOCKS; }  // doubles
+bs_status launch_sumsq_batch(const SumsqBatch& b, double* part, hipStream_t st);
 
 }  // namespace bsp

@@ -1,5 +1,5 @@
 // Elementwise kernels of the decoder layer: head / token permutations, SwiGLU forward and
-// backward, residual adds, bf16 concatenation, and fixed-order sums of squares.
+// backward, residual adds, bf16 concatenation, and batched fixed-order sums of squares.
 #include "k_layer.h"
 
 namespace bsp {
@@ -117,28 +117,35 @@ __global__ void add_kernel(const TA* __restrict__ a, const float* __restrict__ b
   GRID_LOOP(i, n) out[i] = load_f32(a, i) + b[i];
 }
 
-// fixed-order sum of squares (fp64): block partials, then one thread in block order
-__global__ __launch_bounds__(256) void sumsq_kernel(const float* __restrict__ x, int64_t n, double* __restrict__ part) {
+// batched: grid (SUMSQ_BLOCKS, count); block b of job j sums x[i]^2 for i = b*256 + t, stepping
+// by the grid, then the 4 waves in order; the final kernel folds the job's partials in a
+// fixed tree
+__global__ __launch_bounds__(256) void sumsq_batch_kernel(SumsqBatch b, double* __restrict__ part) {
+  const SumsqJob j = b.job[blockIdx.y];
   double s = 0.0;
-  GRID_LOOP(i, n) {
-    const double v = x[i];
-    s += v * v;
-  }
+  if (j.x)
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < j.n; i += (int64_t)SUMSQ_BLOCKS * 256) {
+      const double v = j.x[i];
+      s += v * v;
+    }
   __shared__ double red[4];
   s = wave_sum_f64(s);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
   __syncthreads();
-  if (threadIdx.x == 0) part[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+  if (threadIdx.x == 0) part[(int64_t)blockIdx.y * SUMSQ_BLOCKS + blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
 }
-__global__ void sumsq_final_kernel(const double* __restrict__ part, int nblk, double* __restrict__ out) {
-  if (threadIdx.x != 0) return;
-  double s = 0.0;
-  for (int b = 0; b < nblk; ++b) s += part[b];
-  *out = s;
+__global__ __launch_bounds__(256) void sumsq_batch_final(SumsqBatch b, const double* __restrict__ part) {
+  const SumsqJob j = b.job[blockIdx.x];
+  __shared__ double t[SUMSQ_BLOCKS];
+  t[threadIdx.x] = part[(int64_t)blockIdx.x * SUMSQ_BLOCKS + threadIdx.x];
+  __syncthreads();
+  for (int o = SUMSQ_BLOCKS / 2; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) t[threadIdx.x] += t[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *j.out = j.x ? t[0] : (j.n == 1 ? 0.0 : __builtin_nan(""));
 }
-__global__ void set_f64_kernel(double* p, double v) {
-  if (threadIdx.x == 0) *p = v;
-}
+
 
 // ------------------------------------------------------------------------------------
 bs_status launch_qkv_heads(const float* qkv, int B, int S, int H, int dh, u16* Q, u16* K, u16* V, hipStream_t st) {
@@ -199,19 +206,11 @@ bs_status launch_add(const void* a, bs_dtype at, const float* b, float* out, int
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
-bs_status launch_sumsq(const float* x, int64_t n, double* part, double* out, hipStream_t st) {
-  if (!x) {
-    set_f64_kernel<<<1, 64, 0, st>>>(out, __builtin_nan(""));
-  } else {
-    const int nblk = 1024;
-    sumsq_kernel<<<nblk, 256, 0, st>>>(x, n, part);
-    sumsq_final_kernel<<<1, 64, 0, st>>>(part, nblk, out);
-  }
-  BS_CHECK_LAUNCH();
-  return BS_OK;
-}
-bs_status launch_set_f64(double* p, double v, hipStream_t st) {
-  set_f64_kernel<<<1, 64, 0, st>>>(p, v);
+bs_status launch_sumsq_batch(const SumsqBatch& b, double* part, hipStream_t st) {
+  if (b.count <= 0) return BS_OK;
+  if (b.count > SUMSQ_MAX) return BS_EINVAL;
+  sumsq_batch_kernel<<<dim3(SUMSQ_BLOCKS, (unsigned)b.count), 256, 0, st>>>(b, part);
+  sumsq_batch_final<<<(unsigned)b.count, SUMSQ_BLOCKS, 0, st>>>(b, part);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

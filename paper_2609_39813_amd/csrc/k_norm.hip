@@ -178,24 +178,44 @@ __global__ __launch_bounds__(256) void gain_trial_sum_kernel(const float* __rest
   if (j >= d) return;
   const float* p = part + k * nrt * d + j;
   double acc = 0.0;
-  for (int64_t rt = 0; rt < nrt; ++rt) acc += p[rt * d];
+  int64_t rt = 0;
+  for (; rt + 8 <= nrt; rt += 8) {  // eight loads in flight, added in row-tile order
+    float v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = p[(rt + q) * d];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc += v[q];
+  }
+  for (; rt < nrt; ++rt) acc += p[rt * d];
   S[k * d + j] = acc;
 }
 
+// se of the gain use under N: 16 lanes per column, each over trials k = lane, lane + 16, ...
+// of the shifted values S_k - S_0 (sum and sum of squares, fp64), folded over the 16 lanes
+// in a fixed tree; sample variance over the K trials, se = |s / gain| sqrt(var / K).
 __global__ __launch_bounds__(256) void gain_se_kernel(const double* __restrict__ S, int K, int64_t d,
                                                       const float* __restrict__ scale, const float* __restrict__ gain,
                                                       float* __restrict__ se) {
-  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (j >= d) return;
-  double mean = 0.0, m2 = 0.0;
-  for (int k = 0; k < K; ++k) {
-    const double v = S[(int64_t)k * d + j];
-    const double dlt = v - mean;
-    mean += dlt / (k + 1);
-    m2 += dlt * (v - mean);
+  const int64_t j = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+  const int sub = threadIdx.x & 15;
+  const bool ok = j < d;
+  const double s0 = ok ? S[j] : 0.0;
+  double a1 = 0.0, a2 = 0.0;
+  if (ok)
+    for (int k = sub; k < K; k += 16) {
+      const double v = S[(int64_t)k * d + j] - s0;
+      a1 += v;
+      a2 += v * v;
+    }
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) {
+    a1 += __shfl_xor(a1, o, 64);
+    a2 += __shfl_xor(a2, o, 64);
   }
+  if (!ok || sub != 0) return;
+  const double var = K > 1 ? fmax(a2 - a1 * a1 / K, 0.0) / (K - 1) : 0.0;
   const double f = fabs((double)*scale / (double)gain[j]);
-  se[j] = K > 1 ? (float)(f * sqrt(m2 / (K - 1) / K)) : 0.0f;
+  se[j] = (float)(f * sqrt(var / K));
 }
 
 // Normalization input gradient, one wave64 per row:
@@ -238,7 +258,24 @@ __global__ __launch_bounds__(256) void norm_dx_kernel(DxArgs<T> a) {
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ ref, const float* __restrict__ bias,
                                                       const float* __restrict__ se, int64_t n, float* __restrict__ mean_out,
                                                       float* __restrict__ bias_out, float* __restrict__ se_out) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+  // 16-byte vectors when every pointer allows them, then the scalar tail
+  bool vec = true;
+  for (const void* p : {(const void*)ref, (const void*)bias, (const void*)se, (const void*)mean_out,
+                        (const void*)bias_out, (const void*)se_out})
+    vec = vec && ((uintptr_t)p & 15) == 0;
+  const int64_t n4 = vec ? n / 4 : 0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    const float4 b = bias ? ((const float4*)bias)[i] : z;
+    if (mean_out) {
+      const float4 r = ((const float4*)ref)[i];
+      ((float4*)mean_out)[i] = bias ? make_float4(r.x + b.x, r.y + b.y, r.z + b.z, r.w + b.w) : r;
+    }
+    if (bias_out) ((float4*)bias_out)[i] = b;
+    if (se_out) ((float4*)se_out)[i] = se ? ((const float4*)se)[i] : z;
+  }
+  for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
     const float b = bias ? bias[i] : 0.0f;
     if (mean_out) mean_out[i] = bias ? ref[i] + b : ref[i];
     if (bias_out) bias_out[i] = b;
@@ -325,7 +362,7 @@ bs_status launch_gain_se(const float* part, int K, int64_t T, int64_t d, const f
   if (d <= 0) return BS_OK;
   const int64_t nrt = (T + 31) / 32;
   gain_trial_sum_kernel<<<dim3((unsigned)((d + 255) / 256), (unsigned)K), 256, 0, st>>>(part, nrt, d, S);
-  gain_se_kernel<<<(unsigned)((d + 255) / 256), 256, 0, st>>>(S, K, d, scale, gain, se);
+  gain_se_kernel<<<(unsigned)((d + 15) / 16), 256, 0, st>>>(S, K, d, scale, gain, se);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
@@ -342,7 +379,7 @@ template bs_status launch_dx_t<u16>(const DxArgs<u16>&, hipStream_t);
 bs_status launch_combine(const float* ref, const float* bias, const float* se, int64_t n, float* mean_out,
                          float* bias_out, float* se_out, hipStream_t st) {
   if (n <= 0 || (!mean_out && !bias_out && !se_out)) return BS_OK;
-  combine_kernel<<<grid1d(n), 256, 0, st>>>(ref, bias, se, n, mean_out, bias_out, se_out);
+  combine_kernel<<<grid1d((n + 3) / 4, 4096), 256, 0, st>>>(ref, bias, se, n, mean_out, bias_out, se_out);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
