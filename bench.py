@@ -261,6 +261,17 @@ def main():
              "fresh_count_se_Getps": round(et_per_launch / (se_ms / max(se_n, 1) / 1e3) / 1e9, 1) if se_n else None,
              "path": "collapsed (per-element up-counts; se at the gain use from per-trial sums)"}
 
+    # the per-trial-contraction path (labelled apart): the same step with the se of dW under N,
+    # K = 256 contractions of the per-trial residual planes with dY
+    wall, t = _timed(bsp, torch, lambda: bsp.rmsnorm_linear(Xd, gd, Wd, dYd, fmt="e4m3", fwd_mode=cfg["fwd_mode"],
+                                                             policies=pols, K=cfg["K"], seed=cfg["seed"], want_y=True,
+                                                             want_se=True, want_dw_se=True, ws=ws),
+                     ("gemm", "gemm_split_sum", "trial_planes"), 2)
+    extra["per_trial_path"] = {
+        "policy_trials_per_s": round(len(pols) * cfg["K"] / wall, 1), "ms_per_step": round(wall * 1e3, 3),
+        "kernel_ms": {k: round(v, 4) for k, v in t.items()},
+        "work": "the collapsed step plus K = 256 per-trial contractions (2 d n T flop each) for the se of dW "
+                "under N"}
     extra.update(side_measurements(bsp, synth, torch, dev))
     calibration_copy(torch, dev)
 

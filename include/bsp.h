@@ -123,8 +123,9 @@ bs_status bs_qround(const void* x, bs_dtype xt, int64_t n, bs_fp8 fmt, bs_round 
  *   pol (host) [n_pol], n_pol in [1, 16].
  *   Y [T,n] fp32 (nullable); u_codes [T,d] uint8; u_scale [1] fp32;
  *   dgain_ref [d], dW_ref [d,n], dX_ref [T,d] fp32; estimates dgain [n_pol][d],
- *   dW [n_pol][d*n], dX [n_pol][T*d]. dW.se must be NULL when a policy reads N at the
- *   weight use and K > 1 (per-trial contractions are not built: BS_EUNSUPPORTED).
+ *   dW [n_pol][d*n], dX [n_pol][T*d]. The other estimates collapse the K trials by
+ *   linearity; a non-NULL dW.se with a policy that reads N at the weight use runs the K
+ *   per-trial contractions (App. C.4's sample SD over trials; K x 2 d n T flop more).
  * ---------------------------------------------------------------------------------- */
 typedef struct {
   bs_read gain_use;

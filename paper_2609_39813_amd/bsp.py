@@ -212,8 +212,10 @@ def parse_norm_policy(code):
 
 
 def rmsnorm_linear(X, gain, W, dY, *, eps=1e-5, fmt="e4m3", fwd_mode="rne", policies=("U/U", "R/R", "N/N"), K=16,
-                   seed=0, store_id=0, want_y=True, want_se=True, ws=None):
-    """RMSNorm -> FP8 store -> Linear and the per-use policy estimates (bs_rmsnorm_linear_fwd_bwd)."""
+                   seed=0, store_id=0, want_y=True, want_se=True, want_dw_se=False, ws=None):
+    """RMSNorm -> FP8 store -> Linear and the per-use policy estimates (bs_rmsnorm_linear_fwd_bwd).
+    want_dw_se: also the se of dW where the weight use reads a new rounding (K per-trial
+    contractions; the other estimates collapse the trials)."""
     _dev_check(X, gain, W, dY)
     T, d = X.shape
     n = W.shape[1]
@@ -228,7 +230,7 @@ def rmsnorm_linear(X, gain, W, dY, *, eps=1e-5, fmt="e4m3", fwd_mode="rne", poli
            "diag": new_diag(dev)}
     weight_n = any(p.split(":")[0].split("/")[1] == "N" for p in policies)
     eg, cg = _est(len(policies), d, dev, want_se)
-    ew, cw = _est(len(policies), d * n, dev, want_se and not (weight_n and K > 1))
+    ew, cw = _est(len(policies), d * n, dev, want_se and (want_dw_se or not weight_n))
     ex, cx = _est(len(policies), T * d, dev, want_se)
     if ws is None:
         ws = _workspace(_norm_ws(T, d, n, len(policies), K), dev)

@@ -61,6 +61,28 @@ bs_status launch_gain_se(const float* part, int K, int64_t T, int64_t d, const f
 template <typename T>
 bs_status launch_dx_t(const DxArgs<T>& a, hipStream_t st);
 
+// Per-trial weight-use residual planes: for trials k0 .. k0 + nb - 1 (new roundings of u at
+// the store's scale, use id `use`), plane b [d][ldo] holds sign * (up_k - [C_u rounded up]) * step
+// (one exact bf16 term; zero for t >= T).
+struct TrialPlaneArgs {
+  const float* u;
+  const uint8_t* codes;
+  const float* scale;
+  F8 f;
+  int64_t T, d, ldo;
+  uint64_t seed;
+  uint32_t use;
+  int k0, nb;
+  u16* out;  // [nb][d][ldo]
+};
+bs_status launch_trial_planes(const TrialPlaneArgs& a, hipStream_t st);
+// Shifted fp64 sums over trials of delta [nb][m] (trials k0 ..): trial 1 is stored as the shift
+// d1; S1 += delta - d1, S2 += (delta - d1)^2 for the others, in trial order.
+bs_status launch_trial_accum(const float* delta, int nb, int k0, int64_t m, float* d1, double* S1, double* S2,
+                             hipStream_t st);
+// se = sqrt(max(S2 - S1^2 / K, 0) / (K - 1) / K) (0 for K = 1)
+bs_status launch_trial_se(const double* S1, const double* S2, int K, int64_t m, float* se, hipStream_t st);
+
 bs_status launch_combine_alt(const float* ref, const float* alt, int64_t n, float* mean_out, float* bias_out,
                              float* se_out, hipStream_t st);
 

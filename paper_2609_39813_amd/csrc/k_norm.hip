@@ -97,6 +97,88 @@ __global__ __launch_bounds__(256) void norm_planes_t_kernel(NormPlaneArgs a) {
   }
 }
 
+// Per-trial residual planes of the weight use (the per-trial contraction path): a block covers
+// 64 rows t x 64 columns j; a thread holds 4 rows x 4 consecutive columns (one Philox call per
+// row and trial), the trial's values go through an LDS tile to rows of the plane [j][t].
+__global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
+  __shared__ u16 tile[64][66];
+  const int64_t t0 = (int64_t)blockIdx.y * 64, j0 = (int64_t)blockIdx.x * 64;
+  const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;  // column group, row group
+  const float s = *a.scale;
+  uint32_t F[4][4];
+  u16 sv[4][4];    // bf16 of sign * step
+  uint32_t h[4];   // bit q: the forward's code was rounded up
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int64_t t = t0 + rg + 16 * q;
+    h[q] = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int64_t j = j0 + 4 * cg + c;
+      F[q][c] = 0;
+      sv[q][c] = 0;
+      if (t < a.T && j < a.d) {
+        const int64_t e = t * a.d + j;
+        const float y = __fdiv_rn(a.u[e], s);
+        const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
+        F[q][c] = sr_threshold(b.frac);
+        sv[q][c] = bf16_bits(signbit(y) ? -f8_step(b) : f8_step(b));
+        h[q] |= (uint32_t)((a.codes[e] & 0x7Fu) != b.base + b.mi) << c;
+      }
+    }
+  }
+  for (int b = 0; b < a.nb; ++b) {
+    const uint32_t k = (uint32_t)(a.k0 + b);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t t = t0 + rg + 16 * q;
+      const int64_t jg = j0 + 4 * cg;
+      const Philox4 p = philox_group(a.seed, (uint64_t)((t * a.d + jg) >> 2), k, a.use);
+      const uint32_t R[4] = {p.w0, p.w1, p.w2, p.w3};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t up = sr_up(F[q][c], R[c]), hb = (h[q] >> c) & 1u;
+        tile[4 * cg + c][rg + 16 * q] = up == hb ? (u16)0 : (up ? sv[q][c] : (u16)(sv[q][c] ^ 0x8000u));
+      }
+    }
+    __syncthreads();
+    u16* out = a.out + (int64_t)b * a.d * a.ldo;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int cc = (threadIdx.x >> 6) + 4 * i;
+      const int tx = threadIdx.x & 63;
+      const int64_t j = j0 + cc, t = t0 + tx;
+      if (j < a.d && t < a.ldo) out[j * a.ldo + t] = tile[cc][tx];
+    }
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(256) void trial_accum_kernel(const float* __restrict__ delta, int nb, int k0, int64_t m,
+                                                          float* __restrict__ d1, double* __restrict__ S1,
+                                                          double* __restrict__ S2) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += (int64_t)gridDim.x * blockDim.x) {
+    float shift = k0 == 1 ? delta[i] : d1[i];
+    double a1 = k0 == 1 ? 0.0 : S1[i], a2 = k0 == 1 ? 0.0 : S2[i];
+    for (int b = (k0 == 1 ? 1 : 0); b < nb; ++b) {
+      const double x = (double)delta[(int64_t)b * m + i] - (double)shift;
+      a1 += x;
+      a2 += x * x;
+    }
+    if (k0 == 1) d1[i] = shift;
+    S1[i] = a1;
+    S2[i] = a2;
+  }
+}
+
+__global__ __launch_bounds__(256) void trial_se_kernel(const double* __restrict__ S1, const double* __restrict__ S2,
+                                                       int K, int64_t m, float* __restrict__ se) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += (int64_t)gridDim.x * blockDim.x) {
+    const double a1 = S1[i];
+    se[i] = K > 1 ? (float)sqrt(fmax(S2[i] - a1 * a1 / K, 0.0) / (K - 1) / K) : 0.0f;
+  }
+}
+
 // Row-major plane of val(C) (exact bf16), the A operand of the Linear forward.
 __global__ __launch_bounds__(256) void val_rows_kernel(const uint8_t* __restrict__ codes, int64_t n, F8 f,
                                                        u16* __restrict__ out) {
@@ -331,6 +413,27 @@ bs_status launch_norm_planes(int mode, const NormPlaneArgs& a, hipStream_t st) {
   return BS_OK;
 }
 
+bs_status launch_trial_planes(const TrialPlaneArgs& a, hipStream_t st) {
+  if (a.nb <= 0 || a.d <= 0) return BS_OK;
+  dim3 grid((unsigned)((a.d + 63) / 64), (unsigned)((a.ldo + 63) / 64));
+  ProfScope prof("trial_planes", st);
+  trial_planes_kernel<<<grid, 256, 0, st>>>(a);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_trial_accum(const float* delta, int nb, int k0, int64_t m, float* d1, double* S1, double* S2,
+                             hipStream_t st) {
+  if (m <= 0 || nb <= 0) return BS_OK;
+  trial_accum_kernel<<<grid1d(m), 256, 0, st>>>(delta, nb, k0, m, d1, S1, S2);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_trial_se(const double* S1, const double* S2, int K, int64_t m, float* se, hipStream_t st) {
+  if (m <= 0) return BS_OK;
+  trial_se_kernel<<<grid1d(m), 256, 0, st>>>(S1, S2, K, m, se);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
 bs_status launch_val_rows(const uint8_t* codes, int64_t n, int fmt, u16* out, hipStream_t st) {
   if (n > 0) val_rows_kernel<<<grid1d(n), 256, 0, st>>>(codes, n, f8_format(fmt), out);
   BS_CHECK_LAUNCH();

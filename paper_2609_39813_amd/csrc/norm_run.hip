@@ -15,9 +15,13 @@
 namespace bsp {
 namespace {
 
+// trials per per-trial contraction (stacked along the output rows)
+inline int trial_batch(int K) { return K < 8 ? K : 8; }
+
 struct NormPlan {
   bool gain_n = false, gain_r = false, weight_u = false, want_dxr = false;
   bool weight_n[2] = {false, false};  // use +1 (shared), use +2 (per use)
+  bool weight_se[2] = {false, false}; // se of the weight use under N: per-trial contractions
   bool gain_se = false;
 };
 
@@ -29,6 +33,9 @@ struct NormWs {
   double *gain_part, *trial_sums;
   float* gpart;  // split-K partials of the contractions
   int64_t gpart_cap;
+  u16* tplanes;   // per-trial residual planes [BT][d][Tp]
+  float *tdelta, *td1, *se_w[2];
+  double *tS1, *tS2;
 };
 
 NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype wt, bs_dtype gt, const NormPlan& p,
@@ -70,13 +77,23 @@ NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype wt
     w.trial_sums = c.take<double>((int64_t)K * d);
   }
   if (p.want_dxr) w.dx_r = c.take<float>(T * d);
+  if (p.weight_se[0] || p.weight_se[1]) {
+    const int bt = trial_batch(K);
+    w.tplanes = c.take<u16>((int64_t)bt * d * Tp);
+    w.tdelta = c.take<float>((int64_t)bt * d * n);
+    w.td1 = c.take<float>(d * n);
+    w.tS1 = c.take<double>(d * n);
+    w.tS2 = c.take<double>(d * n);
+    for (int i = 0; i < 2; ++i)
+      if (p.weight_se[i]) w.se_w[i] = c.take<float>(d * n);
+  }
   // split-K partials for the contractions with few output tiles (du: T x d; weight use: d x n)
   w.gpart_cap = 4 * d * std::max<int64_t>(std::max<int64_t>(T, n), 64);
   w.gpart = c.take<float>(w.gpart_cap);
   return w;
 }
 
-NormPlan plan_norm(const bs_norm_policy* pol, int n_pol, bool want_gain_se) {
+NormPlan plan_norm(const bs_norm_policy* pol, int n_pol, bool want_gain_se, bool want_weight_se) {
   NormPlan p;
   for (int i = 0; i < n_pol; ++i) {
     if (pol[i].gain_use == BS_READ_N) p.gain_n = true;
@@ -84,6 +101,7 @@ NormPlan plan_norm(const bs_norm_policy* pol, int n_pol, bool want_gain_se) {
     if (pol[i].weight_use == BS_READ_U) p.weight_u = true;
     if (pol[i].weight_use == BS_READ_N) p.weight_n[pol[i].fresh_shared ? 0 : 1] = true;
     if (pol[i].norm_input_use == BS_READ_R) p.want_dxr = true;
+    if (pol[i].weight_use == BS_READ_N && want_weight_se) p.weight_se[pol[i].fresh_shared ? 0 : 1] = true;
   }
   p.gain_se = want_gain_se && p.gain_n;
   return p;
@@ -97,6 +115,7 @@ size_t norm_ws_size(int64_t T, int64_t d, int64_t n, int K) {
   NormPlan p;
   p.gain_n = p.gain_r = p.weight_u = p.want_dxr = p.gain_se = true;
   p.weight_n[0] = p.weight_n[1] = true;
+  p.weight_se[0] = p.weight_se[1] = true;
   Carver c;
   carve_norm(c, T, d, n, K, BS_F32, BS_F32, p, true);
   return c.used();
@@ -129,9 +148,8 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         pol[i].weight_use > BS_READ_N)
       return BS_EINVAL;
     if (pol[i].norm_input_use != BS_READ_U && pol[i].norm_input_use != BS_READ_R) return BS_EINVAL;
-    if (pol[i].weight_use == BS_READ_N && dW.se && K > 1) return BS_EUNSUPPORTED;
   }
-  const NormPlan p = fwd_only ? NormPlan{} : plan_norm(pol, n_pol, dgain.se != nullptr);
+  const NormPlan p = fwd_only ? NormPlan{} : plan_norm(pol, n_pol, dgain.se != nullptr, dW.se != nullptr);
   Carver probe;
   carve_norm(probe, T, d, n, K, wt, gt, p, Y != nullptr);
   if (!ws || ((uintptr_t)ws & 255) || ws_bytes < probe.used()) return BS_EWORKSPACE;
@@ -271,6 +289,33 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     BS_TRY(weight_gemm(w.resN, pa.nterms, w.bias_n[i], 1.0f / (float)K, u_scale));
   }
 
+  // se of the weight use under N: per-trial contractions (trials stacked along the rows of
+  // the output), shifted fp64 sums over trials, sample SD / sqrt(K)
+  for (int i = 0; i < 2; ++i) {
+    if (!p.weight_se[i]) continue;
+    const int bt = trial_batch(K);
+    for (int k0 = 1; k0 <= K; k0 += bt) {
+      const int nb = K - k0 + 1 < bt ? K - k0 + 1 : bt;
+      const TrialPlaneArgs ta{w.u, u_codes, u_scale, f, T, d, Tp, seed, use_w[i], k0, nb, w.tplanes};
+      BS_TRY(launch_trial_planes(ta, st));
+      GemmArgs g{};
+      g.M = (int)(nb * d);
+      g.N = (int)n;
+      g.K = (int)Tp;
+      g.lda = Tp;
+      g.ldb = Tp;
+      g.ldc = n;
+      g.alpha = 1.0f;
+      g.alpha_dev = u_scale;
+      g.C = w.tdelta;
+      const u16* A0 = w.tplanes;
+      if (!gemm_add_products(g, &A0, 1, w.dyT, nt)) return BS_EINVAL;
+      BS_TRY(launch_gemm(g, st));
+      BS_TRY(launch_trial_accum(w.tdelta, nb, k0, d * n, w.td1, w.tS1, w.tS2, st));
+    }
+    BS_TRY(launch_trial_se(w.tS1, w.tS2, K, d * n, w.se_w[i], st));
+  }
+
   // norm-input use
   if (xt == BS_F32) {
     DxArgs<float> da{(const float*)X, w.rstd, gain, w.du, u_codes, u_scale, f, T, d, dX_ref, w.dx_r};
@@ -290,7 +335,9 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     const float* bw = q.weight_use == BS_READ_U ? w.bias_u
                       : (q.weight_use == BS_READ_N ? w.bias_n[q.fresh_shared ? 0 : 1] : nullptr);
     const int64_t dn = d * n;
-    BS_TRY(launch_combine(dW_ref, bw, nullptr, dn, dW.mean ? dW.mean + i * dn : nullptr,
+    const float* sw = (q.weight_use == BS_READ_N && p.weight_se[q.fresh_shared ? 0 : 1]) ? w.se_w[q.fresh_shared ? 0 : 1]
+                                                                                        : nullptr;
+    BS_TRY(launch_combine(dW_ref, bw, sw, dn, dW.mean ? dW.mean + i * dn : nullptr,
                           dW.bias ? dW.bias + i * dn : nullptr, dW.se ? dW.se + i * dn : nullptr, st));
     const int64_t td = T * d;
     if (q.norm_input_use == BS_READ_R)

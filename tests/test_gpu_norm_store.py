@@ -110,3 +110,20 @@ def test_config2_full_size_sampled(lib):
     out, ref = run_both(lib, T, d, n, cfg["dtype"], cfg["K"], cfg["policies"], seed=cfg["seed"],
                         oracle_kw=dict(dw_rows=rows, gain_cols=cols, dx_rows=xrows), config=2)
     compare(out, ref, cfg["policies"], rows=rows, cols=cols, xrows=xrows, d=d, n=n)
+
+
+def test_weight_use_se_per_trial(lib):
+    """se of dW where the weight use reads a new rounding: the K per-trial contractions (trial
+    batches of 8 and a ragged last batch) against the oracle's sample SD over its K passes."""
+    for (T, d, n, K, shared) in ((300, 192, 136, 12, False), (130, 64, 72, 9, True)):
+        X, g, W, dY = synth.rmsnorm_linear_inputs(T, d, n, torch.bfloat16, 2)
+        pols = ("N/N", "U/N", "R/R", "U/U")
+        codes = [p + (":shared" if shared else "") for p in pols]
+        print(f"[norm_store] dW se per trial T={T} d={d} n={n} K={K} shared={shared}", flush=True)
+        out = lib.rmsnorm_linear(X.cuda(), g.cuda(), W.cuda(), dY.cuda(), policies=codes, K=K, seed=31,
+                                 want_dw_se=True)
+        torch.cuda.synchronize()
+        ref = norm_store.check(X.float().numpy(), g.numpy(), W.float().numpy(), dY.float().numpy(), eps=1e-5,
+                               fmt=fp8.E4M3, fwd_mode=oq.RNE, policies=pols, K=K, seed=31, fresh_shared=shared)
+        assert out["dW"]["se"] is not None
+        compare(out, ref, pols, d=d, n=n)
