@@ -100,6 +100,14 @@ __device__ __forceinline__ Bracket f8_bracket(float a, F8 f) {
 // floor(frac * 2^32): exact when frac has at most 32 fraction bits, truncated below.
 __device__ __forceinline__ uint32_t sr_threshold(float frac) { return (uint32_t)(frac * 4294967296.0f); }
 
+// y = fl32(x / s) as the fp64 product x * fl64(1 / s) rounded once to fp32 (rs = 1.0 / (double)s,
+// computed once). Identical to the IEEE fp32 quotient: the product is within 2^-52 relative of
+// x / s, while the quotient of two floats is never a rounding midpoint and, when inexact, is at
+// least 2^-49 relative away from every midpoint (x - s m is a nonzero multiple of the smaller
+// operand grid; m needs 25 significant bits). Subnormal and overflowing quotients round the same
+// way from the fp64 value.
+__device__ __forceinline__ float div_scale(float x, double rs) { return (float)((double)x * rs); }
+
 // Round up iff R + F >= 2^32 (so P(up) = F / 2^32): the carry out of the 32-bit add.
 __device__ __forceinline__ uint32_t sr_up(uint32_t F, uint32_t R) {
   return (uint32_t)(((uint64_t)R + (uint64_t)F) >> 32);

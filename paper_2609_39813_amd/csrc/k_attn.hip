@@ -128,6 +128,7 @@ __global__ __launch_bounds__(256) void attn_d_kernel(AttnDArgs a) {
   const bool ok = row < a.rows;
   const int64_t e0 = row * AT + EPL * sub;
   const float s = *a.scale;
+  const double rs = 1.0 / (double)s;
   double dref = 0.0, dr = 0.0, A = 0.0;
   uint32_t F[EPL];
   float w[EPL];
@@ -159,7 +160,7 @@ __global__ __launch_bounds__(256) void attn_d_kernel(AttnDArgs a) {
         const double o = ov[q], g = dv[q];
         dref += g * o;
         dr += g * ((double)s * (double)f8_value((c4 >> (8 * q)) & 0xFFu, a.f) - o);
-        const float y = __fdiv_rn(ov[q], s);
+        const float y = div_scale(ov[q], rs);
         const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
         const float step = f8_step(b);
         A += g * ((double)s * (signbit(y) ? -1.0 : 1.0) * (double)b.mi * (double)step - o);

@@ -10,7 +10,7 @@ namespace bsp {
 // split into three exact bf16 terms.
 __device__ __forceinline__ float resid_value(const ResidArgs& a, int64_t e, float s) {
   const float g = bf16_to_f32(a.dY[e]);
-  const float y = __fdiv_rn(g, s);
+  const float y = div_scale(g, 1.0 / (double)s);
   const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
   const double num = ((double)b.mi * a.K + (double)a.counts[e]) * (double)f8_step(b);
   double mv = num / a.K;
@@ -61,10 +61,11 @@ __global__ __launch_bounds__(256) void kappa_fixed_kernel(const u16* __restrict_
                                                           F8 f, int64_t n_el, const float* __restrict__ AW,
                                                           const float* __restrict__ XB, double* __restrict__ part) {
   const float s = *scale;
+  const double rs = 1.0 / (double)s;
   double a0 = 0.0, b0 = 0.0;
   for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n_el; e += (int64_t)gridDim.x * 256) {
     const float g = bf16_to_f32(dY[e]);
-    const float y = __fdiv_rn(g, s);
+    const float y = div_scale(g, rs);
     const Bracket b = f8_bracket(fminf(fabsf(y), f.fmax), f);
     double lo = (double)b.mi * (double)f8_step(b);
     if (signbit(y)) lo = -lo;

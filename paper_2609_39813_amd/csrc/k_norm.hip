@@ -65,6 +65,7 @@ __global__ __launch_bounds__(256) void norm_planes_t_kernel(NormPlaneArgs a) {
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
   const float s = *a.scale;
+  const double rs = 1.0 / (double)s;
 #pragma unroll 2
   for (int i = 0; i < 16; ++i) {
     const int rr = ty + 4 * i;
@@ -78,7 +79,7 @@ __global__ __launch_bounds__(256) void norm_planes_t_kernel(NormPlaneArgs a) {
       } else if (MODE == NP_RESU) {
         split3(fmaf(-s, f8_value(code, a.f), a.u[e]), o[0], o[1], o[2]);
       } else {
-        const float y = __fdiv_rn(a.u[e], s);
+        const float y = div_scale(a.u[e], rs);
         const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
         const int h = (code & 0x7Fu) != b.base + b.mi;
         const float v = (float)((int)a.counts[e] - a.K * h) * f8_step(b);
@@ -104,7 +105,7 @@ __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
   __shared__ u16 tile[64][66];
   const int64_t t0 = (int64_t)blockIdx.y * 64, j0 = (int64_t)blockIdx.x * 64;
   const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;  // column group, row group
-  const float s = *a.scale;
+  const double rs = 1.0 / (double)*a.scale;
   uint32_t F[4][4];
   u16 sv[4][4];    // bf16 of sign * step
   uint32_t h[4];   // bit q: the forward's code was rounded up
@@ -119,7 +120,7 @@ __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
       sv[q][c] = 0;
       if (t < a.T && j < a.d) {
         const int64_t e = t * a.d + j;
-        const float y = __fdiv_rn(a.u[e], s);
+        const float y = div_scale(a.u[e], rs);
         const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
         F[q][c] = sr_threshold(b.frac);
         sv[q][c] = bf16_bits(signbit(y) ? -f8_step(b) : f8_step(b));
@@ -200,6 +201,7 @@ __global__ __launch_bounds__(256) void gain_partials_kernel(GainArgs<T> a) {
   if (j >= a.d) return;
   const double s = *a.scale;
   const float sf = *a.scale;
+  const double rsf = 1.0 / (double)sf;
   const double g = a.gain[j];
   double q0 = 0.0, q1 = 0.0, q2 = 0.0;
   const int64_t tend = (rt + 1) * 64 < a.T ? (rt + 1) * 64 : a.T;
@@ -211,7 +213,7 @@ __global__ __launch_bounds__(256) void gain_partials_kernel(GainArgs<T> a) {
     q0 += (double)z * du;
     if (a.want_r) q1 += (s * (double)f8_value(a.codes[e], a.f) - gz) / g * du;
     if (a.counts) {
-      const float y = __fdiv_rn(a.u[e], sf);
+      const float y = div_scale(a.u[e], rsf);
       const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
       const double step = f8_step(b);
       double mv = (double)b.mi * step + (double)a.counts[e] * step / a.K;

@@ -89,8 +89,8 @@ __global__ void finalize_scale_kernel(bs_diag* diag, const float* scale_in, floa
 // Eight consecutive elements per thread (two Philox groups): 16- or 32-byte loads, an
 // 8-byte store of the codes.
 template <typename T, int MODE>
-__device__ __forceinline__ uint32_t code_of(float xv, float s, F8 f, uint32_t R, uint32_t& nsat) {
-  const float y = __fdiv_rn(xv, s);
+__device__ __forceinline__ uint32_t code_of(float xv, double rs, F8 f, uint32_t R, uint32_t& nsat) {
+  const float y = div_scale(xv, rs);
   float a = fabsf(y);
   if (a > f.fmax) {
     a = f.fmax;
@@ -106,7 +106,7 @@ __global__ __launch_bounds__(256) void quantize_kernel(const T* __restrict__ x, 
                                                        bs_diag* __restrict__ diag, uint8_t* __restrict__ codes,
                                                        uint64_t seed, uint32_t trial, uint32_t use) {
   if (diag->nonfinite) return;
-  const float s = diag->scale;
+  const double rs = 1.0 / (double)diag->scale;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t e0 = t * 8;
   uint32_t nsat = 0;
@@ -142,7 +142,7 @@ __global__ __launch_bounds__(256) void quantize_kernel(const T* __restrict__ x, 
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       uint32_t sat = 0;
-      const uint32_t code = code_of<T, MODE>(xv[q], s, f, R[q], sat);
+      const uint32_t code = code_of<T, MODE>(xv[q], rs, f, R[q], sat);
       if (q < cnt) {
         nsat += sat;
         if (q < 4) lo |= code << (8 * q);
@@ -181,7 +181,7 @@ __device__ __forceinline__ void fresh_count_body(const FreshArgs<X>& a) {
   const int64_t j0 = (int64_t)blockIdx.x * 256 + 4 * tx;
   const int64_t t0 = (int64_t)blockIdx.y * RT;
   const bool colok = j0 < a.d;
-  const float s = *a.scale;
+  const double rs = 1.0 / (double)*a.scale;
   uint32_t F[RPT][4], cnt[RPT][4];
   float c1[RPT][4], c2[RPT][4];
 #pragma unroll
@@ -204,7 +204,7 @@ __device__ __forceinline__ void fresh_count_body(const FreshArgs<X>& a) {
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float y = __fdiv_rn(xv[q], s);
+      const float y = div_scale(xv[q], rs);
       const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
       F[r][q] = sr_threshold(ok ? b.frac : 0.0f);
       const float sc = (signbit(y) ? -1.0f : 1.0f) * f8_step(b);
