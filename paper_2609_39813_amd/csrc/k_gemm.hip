@@ -6,14 +6,19 @@
 // are summed in one pass: that is how fp32-valued operands enter as a sum of exact bf16
 // terms. Products of bf16 values are exact in the fp32 accumulator.
 //
-// Two kernels. The pipelined kernel (K a multiple of 32) moves operand tiles straight from
-// global memory into LDS (global_load_lds_dwordx4, no register staging) through a ring of
-// four 32-deep stages, three chunks ahead of the MFMAs; a 256 x 256 block tile is split over
-// 4 wave64s of 128 x 128 (8 x 8 MFMA 16x16x32 tiles, accumulators in AGPRs). Rows of a stage
-// are 64 B; the 16-byte chunk c of row r sits at chunk c ^ ((r >> 1) & 3), so the eight rows
-// a ds_read_b128 phase touches fall on distinct banks. Shapes with fewer tiles than CUs split
-// K over blocks into fp32 partials that one more kernel sums in a fixed order (the result
-// does not depend on timing). The register-staged kernel below serves the other shapes.
+// Two kernels. The pipelined kernel (K a multiple of 64) moves operand tiles straight from
+// global memory into LDS (buffer_load_dwordx4 ... lds, no register staging) in 64-deep
+// chunks, so that every operand row of a chunk is one full 128-byte line; two LDS stages
+// (128 KB for a 256 x 256 tile) hold the chunk being computed and the next one. A 256 x 256
+// block tile is split over 4 wave64s of 128 x 128 (8 x 8 MFMA 16x16x32 tiles, accumulators
+// in AGPRs). The 16-byte unit u of row r sits at unit u ^ (r & 7) of its LDS row, so the
+// rows one ds_read_b128 serves together fall on distinct banks. The operand loads go through
+// buffer resources that end with the tile's last valid row (rows past M or N read as zero).
+// The instruction order of the main loop is fixed in source (scheduling barriers): LDS reads
+// of the next k-step and the global loads of the chunk after next are spread between the
+// MFMAs, one barrier per chunk. Shapes with fewer tiles than CUs split K over blocks into
+// fp32 partials that one more kernel sums in a fixed order (the result does not depend on
+// timing). The register-staged kernel below serves the other shapes.
 //
 // Register-staged kernel: tile 128 x 128 x 64 or 256 x 256 x 64, 256 threads (4 wave64s in
 // 2 x 2), double-buffered LDS with a 16-byte row pad (row stride 144 B keeps the 16 rows read
@@ -132,21 +137,20 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs g) {
 // ------------------------------------------------------------------------------------
 // pipelined kernel
 // ------------------------------------------------------------------------------------
-#ifndef BSP_GEMM_STAGES
-#define BSP_GEMM_STAGES 4
+// A stage holds a 64-deep K chunk: every operand row is one 128-byte line. The 16-byte unit u
+// of row r sits at unit u ^ swz(r) of its LDS row, so that the rows one ds_read_b128 serves
+// together fall on distinct banks.
+constexpr int LBK = 64, LNST = 2;
+#ifndef BSP_GEMM_SWZ
+#define BSP_GEMM_SWZ(r) ((r) & 7)
 #endif
-constexpr int LBK = 32, LNST = BSP_GEMM_STAGES;
-
-__device__ __forceinline__ int lds_swz(int r, int c) { return r * 64 + ((c ^ ((r >> 1) & 3)) << 4); }
-
-// s_waitcnt with vmcnt = n and the other counters left at their maxima (gfx9 encoding)
-#define BS_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
+__device__ __forceinline__ int lds_swz(int r, int u) { return r * 128 + ((u ^ BSP_GEMM_SWZ(r)) << 4); }
 
 template <int BM, int BN>
 __global__ __launch_bounds__(256) void gemm_lds_kernel(GemmArgs g, int cps) {
   constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 16, FN = WN / 16;
-  constexpr int AI = BM / 64, BI = BN / 64, LPC = AI + BI;  // 1-KB loads per wave per stage
-  constexpr int STAGE = (BM + BN) * 64;
+  constexpr int AI = BM / 32, BI = BN / 32, LPC = AI + BI;  // 1-KB loads (8 rows) per wave per chunk
+  constexpr int STAGE = (BM + BN) * 128;
   __shared__ __attribute__((aligned(1024))) char smem[LNST * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -167,42 +171,44 @@ __global__ __launch_bounds__(256) void gemm_lds_kernel(GemmArgs g, int cps) {
   const int c0 = split * cps;
   const int n = min(total, c0 + cps) - c0;
 
-  // Load i of this wave fills rows (wave * AI + i) * 16 .. +15 of A (then B): lane l writes
-  // row l / 4, chunk position l % 4, which holds logical chunk (l % 4) ^ ((row >> 1) & 3).
-  // Rows past M (N) repeat the last row; their products are never stored.
-  int64_t offa[AI], offb[BI];
-#pragma unroll
-  for (int i = 0; i < AI; ++i) {
-    const int r = (wave * AI + i) * 16 + (lane >> 2);
-    offa[i] = (int64_t)min(bm + r, g.M - 1) * g.lda + (((lane & 3) ^ ((r >> 1) & 3)) << 3);
-  }
-#pragma unroll
-  for (int i = 0; i < BI; ++i) {
-    const int r = (wave * BI + i) * 16 + (lane >> 2);
-    offb[i] = (int64_t)min(bn + r, g.N - 1) * g.ldb + (((lane & 3) ^ ((r >> 1) & 3)) << 3);
-  }
-  // the next chunk to load: segment, k offset and the segment's operands (wave-uniform)
+  // Operand tiles are read through buffer resources whose range ends with the tile's last
+  // valid row: rows past M (N) read as zero (their products are never stored) and cost no
+  // memory traffic. Load i of this wave fills rows (wave * AI + i) * 8 .. +7 of A (then B):
+  // lane l writes row l / 8 at unit position l % 8, which holds logical unit (l % 8) ^ swz(row);
+  // swz(row) = swz(l / 8) because the row's other terms are multiples of 8. One per-lane byte
+  // offset per operand; the load index and the k position enter as scalar offsets.
+  const int rows_a = min(g.M - bm, BM), rows_b = min(g.N - bn, BN);
+  const uint32_t lane_a = (uint32_t)(((wave * AI * 8 + (lane >> 3)) * g.lda + (((lane & 7) ^ BSP_GEMM_SWZ(lane >> 3)) << 3)) * 2);
+  const uint32_t lane_b = (uint32_t)(((wave * BI * 8 + (lane >> 3)) * g.ldb + (((lane & 7) ^ BSP_GEMM_SWZ(lane >> 3)) << 3)) * 2);
+  const uint32_t step_a = (uint32_t)(8 * g.lda * 2), step_b = (uint32_t)(8 * g.ldb * 2);
+  auto rsrc = [](const u16* base, int64_t row0, int rows, int64_t ld) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(base + row0 * ld), (short)0, (int)(rows * ld * 2), 0x00020000);
+  };
+  // The next chunk to load: segment, k offset and the segment's resources (wave-uniform).
+  // Past the last chunk of the contraction the position wraps to the start of the last
+  // segment: the loop body is branch-free, and the surplus loads land in a stage that is
+  // never read again.
   int iss_seg = c0 / nch, iss_k = (c0 - iss_seg * nch) * LBK;
-  const u16* pa = g.A[iss_seg];
-  const u16* pb = g.B[iss_seg];
-  auto issue = [&](int st) {
+  __amdgpu_buffer_rsrc_t ra = rsrc(g.A[iss_seg], bm, rows_a, g.lda);
+  __amdgpu_buffer_rsrc_t rb = rsrc(g.B[iss_seg], bn, rows_b, g.ldb);
+  auto issue_one = [&](int st, int i) {
     char* base = smem + st * STAGE;
-#pragma unroll
-    for (int i = 0; i < AI; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(pa + offa[i] + iss_k),
-                                       (void __attribute__((address_space(3)))*)(base + (wave * AI + i) * 1024),
-                                       16, 0, 0);
-#pragma unroll
-    for (int i = 0; i < BI; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(pb + offb[i] + iss_k),
-                                       (void __attribute__((address_space(3)))*)(base + BM * 64 + (wave * BI + i) * 1024),
-                                       16, 0, 0);
+    if (i < AI)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (void __attribute__((address_space(3)))*)(base + (wave * AI + i) * 1024),
+                                               16, lane_a, (uint32_t)iss_k * 2 + i * step_a, 0, 0);
+    else
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rb, (void __attribute__((address_space(3)))*)(base + BM * 128 + (wave * BI + i - AI) * 1024), 16, lane_b,
+          (uint32_t)iss_k * 2 + (i - AI) * step_b, 0, 0);
+  };
+  // Kept out of the MFMA regions: the rare segment switch is a branch with scalar loads.
+  auto advance = [&]() {
     iss_k += LBK;
     if (iss_k == g.K) {
       iss_k = 0;
       if (++iss_seg < g.nseg) {
-        pa = g.A[iss_seg];
-        pb = g.B[iss_seg];
+        ra = rsrc(g.A[iss_seg], bm, rows_a, g.lda);
+        rb = rsrc(g.B[iss_seg], bn, rows_b, g.ldb);
       }
     }
   };
@@ -213,66 +219,92 @@ __global__ __launch_bounds__(256) void gemm_lds_kernel(GemmArgs g, int cps) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // Software pipeline: the fragments of chunk c + 1 are read from LDS while the MFMAs of
-  // chunk c run; chunk c + 3 is in flight from global memory.
   const int fr = lane & 15, fc = lane >> 4;
   bf16x8 fa[2][FM], fb[2][FN];
-  auto read_frags = [&](int c, bf16x8* a, bf16x8* b) {
-    const char* base = smem + (c % LNST) * STAGE;
-#pragma unroll
-    for (int i = 0; i < FM; ++i) a[i] = *(const bf16x8*)(base + lds_swz(wm * WM + i * 16 + fr, fc));
-#pragma unroll
-    for (int j = 0; j < FN; ++j) b[j] = *(const bf16x8*)(base + BM * 64 + lds_swz(wn * WN + j * 16 + fr, fc));
+  // MFMA t of a k-step, in row-major (i, j) order
+  auto mfma_t = [&](int buf, int t) {
+    const int i = t / FN, j = t % FN;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
   };
-  auto mfmas = [&](const bf16x8* a, const bf16x8* b) {
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-  };
-  // wait until chunk c has landed (at most the loads of the chunks issued after it pending),
-  // then a barrier without a memory fence (the fence would drain the prefetches too)
-  auto wait_chunks = [&](int after) {  // at most `after` chunks' loads still pending
-    static_assert(LNST >= 3 && LNST <= 5, "waits below cover up to three chunks in flight");
-    if (LNST >= 5 && after >= 3)
-      BS_WAIT_VM(3 * LPC);
-    else if (LNST >= 4 && after >= 2)
-      BS_WAIT_VM(2 * LPC);
-    else if (after >= 1)
-      BS_WAIT_VM(LPC);
+  // read q of a k-step's fragments: B first (the first MFMAs use every B fragment), then A
+  auto read_q = [&](int st, int s, int q, bf16x8* a, bf16x8* b) {
+    const char* base = smem + st * STAGE;
+    if (q < FN)
+      b[q] = *(const bf16x8*)(base + BM * 128 + lds_swz(wn * WN + q * 16 + fr, fc + 4 * s));
     else
-      BS_WAIT_VM(0);
+      a[q - FN] = *(const bf16x8*)(base + lds_swz(wm * WM + (q - FN) * 16 + fr, fc + 4 * s));
   };
-  auto land = [&](int x) {
-    // chunks issued when x is awaited: up to min(n - 1, x + LNST - 3)
-    wait_chunks(min(n - 1, x + LNST - 3) - x);
-    asm volatile("s_barrier" ::: "memory");
-  };
+  // wait until at most vm of this wave's loads are pending and its fragment reads are done,
+  // then a barrier without a memory fence (a fence would drain the prefetch too)
+#define BS_LAND(vm)                                                                             \
+  do {                                                                                          \
+    __builtin_amdgcn_s_waitcnt(((vm) & 15) | (((vm) >> 4) << 14) | (7 << 4)); /* lgkmcnt(0) */ \
+    asm volatile("s_barrier" ::: "memory");                                                     \
+  } while (0)
+  static_assert(LPC < 64, "vmcnt range");
 
+  // Prologue: chunks 0 and 1 in flight; chunk 0 landed; its first k-step in registers.
 #pragma unroll
-  for (int st = 0; st < LNST - 1; ++st)
-    if (st < n) issue(st);
-  wait_chunks(min(n - 1, LNST - 2));  // chunk 0 with chunks 1 .. LNST - 2 still in flight
-  asm volatile("s_barrier" ::: "memory");
-  read_frags(0, fa[0], fb[0]);
+  for (int st = 0; st < 2; ++st) {
+#pragma unroll
+    for (int i = 0; i < LPC; ++i) issue_one(st, i);
+    advance();
+  }
+  BS_LAND(LPC);
+#pragma unroll
+  for (int q = 0; q < FM + FN; ++q) read_q(0, 0, q, fa[0], fb[0]);
 
-  for (int c = 0; c + 1 < n; ++c) {
-    land(c + 1);
-    if (c + LNST - 1 < n) issue((c + LNST - 1) % LNST);
-    read_frags(c + 1, fa[1], fb[1]);
-    mfmas(fa[0], fb[0]);
-    // interleave: one fragment read after every few MFMAs
+  // Chunk c (stage c & 1), two k-steps of 32; the fragments alternate between two register
+  // sets (k-step 0 computes from set 0 and fills set 1, k-step 1 the reverse).
+  // k-step 0: its MFMAs, with the fragments of k-step 1 (same stage, landed) read in between.
+  // k-step 1: the MFMAs of the first PA fragment rows; then chunk c + 1 is awaited and every
+  //   wave has finished reading chunk c; the loads of chunk c + 2 go into chunk c's stage and
+  //   the first fragments of chunk c + 1 are read, both between the remaining MFMAs.
+  // The instruction order is fixed in source: a scheduling barrier closes every small group
+  // (loads, reads and the MFMAs between them), so reads are issued well before their use and
+  // the loads are spread over the MFMA stream. The last iteration reads a stage of surplus
+  // data that is never used.
+  constexpr int NM = FM * FN;                  // MFMAs per k-step
+  constexpr int RD = FM + FN;                  // fragment reads per k-step
+  constexpr int PA = FM >= 4 ? FM / 4 : 1;     // rows before the barrier
+  constexpr int NA = PA * FN, NB = NM - NA;    // MFMAs before / after the barrier
+  constexpr int M0 = NM / RD >= 2 ? 2 : 1;     // k-step 0: one read per M0 MFMAs
+  constexpr int GRP = LPC > RD ? LPC : RD;     // k-step 1: groups of (load, read, MFMAs)
+  constexpr int M1 = (2 * NB) / (3 * GRP) > 0 ? (2 * NB) / (3 * GRP) : 1;  // groups span 2/3 of NB
+  for (int c = 0; c < n; ++c) {
+    const int st = c & 1;
 #pragma unroll
-    for (int q = 0; q < FM + FN; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, (FM * FN) / (FM + FN), 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    for (int q = 0; q < RD; ++q) {
+      read_q(st, 1, q, fa[1], fb[1]);
+#pragma unroll
+      for (int t = q * M0; t < (q + 1) * M0; ++t) mfma_t(0, t);
+      __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
-    for (int i = 0; i < FM; ++i) fa[0][i] = fa[1][i];
+    for (int t = RD * M0; t < NM; ++t) mfma_t(0, t);
+    __builtin_amdgcn_sched_barrier(0);
+
 #pragma unroll
-    for (int j = 0; j < FN; ++j) fb[0][j] = fb[1][j];
+    for (int t = 0; t < NA; ++t) mfma_t(1, t);
+    __builtin_amdgcn_sched_barrier(0);
+    BS_LAND(0);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int q = 0; q < GRP; ++q) {
+      if (q < LPC) issue_one(st, q);
+      if (q < RD) read_q(st ^ 1, 0, q, fa[0], fb[0]);
+#pragma unroll
+      for (int t = NA + q * M1; t < NA + (q + 1) * M1 && t < NM; ++t) mfma_t(1, t);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int t = NA + GRP * M1; t < NM; ++t) mfma_t(1, t);
+    __builtin_amdgcn_sched_barrier(0);
+    advance();
   }
-  mfmas(fa[0], fb[0]);
+  // no load into LDS may outlive the block (the CU hands its LDS to the next block)
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+#undef BS_LAND
 
   // D[i][j] of a 16x16 tile sits in lane (j + 16 * (i / 4)), register i % 4.
   const int oc = lane & 15, orow = (lane >> 4) * 4;
@@ -317,11 +349,11 @@ static bs_status launch_gemm_lds(const GemmArgs& g0, hipStream_t st) {
   GemmArgs g = g0;
   const int64_t tiles = (int64_t)((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   const int total = (g.K / LBK) * g.nseg;
-  // split K while the tiles leave CUs idle, keeping at least 32 chunks (1024 of K) per block
+  // split K while the tiles leave CUs idle, keeping at least 16 chunks (1024 of K) per block
   int splits = 1;
   if (g.part && tiles < 256) {
     const int64_t want = (256 + tiles - 1) / tiles;
-    const int64_t by_k = total / 32;
+    const int64_t by_k = total / 16;
     const int64_t by_ws = g.part_cap / ((int64_t)g.M * g.N);
     splits = (int)std::max<int64_t>(1, std::min(want, std::min(by_k, by_ws)));
   }
@@ -362,8 +394,9 @@ bs_status launch_gemm(const GemmArgs& g, hipStream_t st) {
 #ifdef BSP_GEMM_CFG
   return BSP_GEMM_CFG(g, st);
 #else
-  // pipelined kernel for 32-aligned K and 16-byte aligned operands
-  bool lds_ok = (g.K % LBK) == 0 && g.M >= 1 && g.N >= 1;
+  // pipelined kernel for 64-aligned K and 16-byte aligned operands
+  // (buffer offsets of one 256-row tile fit in 31 bits)
+  bool lds_ok = (g.K % LBK) == 0 && g.M >= 1 && g.N >= 1 && g.lda < (1 << 21) && g.ldb < (1 << 21);
   for (int i = 0; i < g.nseg; ++i) lds_ok = lds_ok && ((uintptr_t)g.A[i] & 15) == 0 && ((uintptr_t)g.B[i] & 15) == 0;
   if (lds_ok) {
     if ((int64_t)g.M * g.N >= (int64_t)256 * 256 * 16) return launch_gemm_lds<256, 256>(g, st);
