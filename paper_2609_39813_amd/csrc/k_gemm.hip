@@ -10,8 +10,9 @@
 // global memory into LDS (buffer_load_dwordx4 ... lds, no register staging) in 64-deep
 // chunks, so that every operand row of a chunk is one full 128-byte line; two LDS stages
 // (128 KB for a 256 x 256 tile) hold the chunk being computed and the next one. A 256 x 256
-// block tile is split over 4 wave64s of 128 x 128 (8 x 8 MFMA 16x16x32 tiles, accumulators
-// in AGPRs). The 16-byte unit u of row r sits at unit u ^ (r & 7) of its LDS row, so the
+// block tile is split over 8 wave64s of 128 x 64 (8 x 4 MFMA 16x16x32 tiles, accumulators in
+// AGPRs): at 128 accumulator registers a wave fits twice per SIMD, so one wave's MFMAs run
+// while the other waits on a load issue or the barrier. The 16-byte unit u of row r sits at unit u ^ (r & 7) of its LDS row, so the
 // rows one ds_read_b128 serves together fall on distinct banks. The operand loads go through
 // buffer resources that end with the tile's last valid row (rows past M or N read as zero).
 // The instruction order of the main loop is fixed in source (scheduling barriers): LDS reads
@@ -146,16 +147,19 @@ constexpr int LBK = 64, LNST = 2;
 #endif
 __device__ __forceinline__ int lds_swz(int r, int u) { return r * 128 + ((u ^ BSP_GEMM_SWZ(r)) << 4); }
 
-template <int BM, int BN>
-__global__ __launch_bounds__(256) void gemm_lds_kernel(GemmArgs g, int cps) {
-  constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 16, FN = WN / 16;
-  constexpr int AI = BM / 32, BI = BN / 32, LPC = AI + BI;  // 1-KB loads (8 rows) per wave per chunk
+// Block tile BM x BN, WGM x WGN wave64s, each owning a (BM / WGM) x (BN / WGN) tile.
+template <int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, int cps) {
+  constexpr int NW = WGM * WGN;
+  constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 16, FN = WN / 16;
+  constexpr int AI = BM / (8 * NW), BI = BN / (8 * NW), LPC = AI + BI;  // 1-KB loads (8 rows) per wave per chunk
+  static_assert(AI * 8 * NW == BM && BI * 8 * NW == BN, "loads cover the tile");
   constexpr int STAGE = (BM + BN) * 128;
   __shared__ __attribute__((aligned(1024))) char smem[LNST * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN, ntile = tiles_m * tiles_n;
   const int nblk = gridDim.x;
   int bid = blockIdx.x;
@@ -344,7 +348,7 @@ __global__ __launch_bounds__(256) void gemm_split_sum_kernel(GemmArgs g, int spl
   }
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int WGM, int WGN>
 static bs_status launch_gemm_lds(const GemmArgs& g0, hipStream_t st) {
   GemmArgs g = g0;
   const int64_t tiles = (int64_t)((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
@@ -363,7 +367,7 @@ static bs_status launch_gemm_lds(const GemmArgs& g0, hipStream_t st) {
   if (tiles * splits > 0x7FFFFFFF) return BS_ESHAPE;
   {
     ProfScope prof("gemm", st);
-    gemm_lds_kernel<BM, BN><<<(unsigned)(tiles * splits), 256, 0, st>>>(g, cps);
+    gemm_lds_kernel<BM, BN, WGM, WGN><<<(unsigned)(tiles * splits), 64 * WGM * WGN, 0, st>>>(g, cps);
     BS_CHECK_LAUNCH();
   }
   if (splits > 1) {
@@ -399,8 +403,11 @@ bs_status launch_gemm(const GemmArgs& g, hipStream_t st) {
   bool lds_ok = (g.K % LBK) == 0 && g.M >= 1 && g.N >= 1 && g.lda < (1 << 21) && g.ldb < (1 << 21);
   for (int i = 0; i < g.nseg; ++i) lds_ok = lds_ok && ((uintptr_t)g.A[i] & 15) == 0 && ((uintptr_t)g.B[i] & 15) == 0;
   if (lds_ok) {
-    if ((int64_t)g.M * g.N >= (int64_t)256 * 256 * 16) return launch_gemm_lds<256, 256>(g, st);
-    return launch_gemm_lds<128, 128>(g, st);
+#ifndef BSP_GEMM_BIG
+#define BSP_GEMM_BIG 256, 256, 2, 4
+#endif
+    if ((int64_t)g.M * g.N >= (int64_t)256 * 256 * 16) return launch_gemm_lds<BSP_GEMM_BIG>(g, st);
+    return launch_gemm_lds<128, 128, 2, 2>(g, st);
   }
   // 256 x 256 tiles once they still give every CU a tile; 128 x 128 below that
   const int64_t big = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256);
