@@ -61,6 +61,11 @@ __device__ __forceinline__ uint32_t philox_word(const Philox4& p, int q) {
 // and frac = v - mi exact. The code of magnitude m*step is base + m, where base is
 // (e + bias - 1) << mbits in the normal range (e = exponent of a) and 0 below it; a
 // carry of m into the next binade lands on the right code by construction.
+// Everything is taken from the fp32 bit pattern with integer operations: with a = M 2^(e-23)
+// (M the 24-bit significand) and q = max(e, 1 - bias) the binade of the grid step
+// 2^(q - mbits), v = M / 2^w with w = 23 - mbits + q - e, so mi = M >> w and the fraction is
+// the low w bits of M; F = floor(frac 2^32) is those bits moved to the top of a 32-bit word
+// (exact for w <= 32, truncated beyond).
 // ---------------------------------------------------------------------------------
 struct F8 {
   int mbits;
@@ -75,30 +80,26 @@ __host__ __device__ __forceinline__ F8 f8_format(int fmt) {
 struct Bracket {
   uint32_t base;  // code of 0 * step in a's binade
   uint32_t mi;    // floor(a / step)
-  float frac;     // a / step - mi, in [0, 1)
+  uint32_t F;     // floor((a / step - mi) * 2^32)
   int sh;         // a / step = a * 2^sh
 };
 
+// 0 <= a <= fmax, finite
 __device__ __forceinline__ Bracket f8_bracket(float a, F8 f) {
+  const uint32_t bits = __float_as_uint(a);
+  const int E = (int)(bits >> 23);
+  const uint32_t M = (bits & 0x7FFFFFu) | (E ? 0x800000u : 0u);
+  const int e = E ? E - 127 : -126;
+  const int q = max(e, 1 - f.bias);
+  const int w = 23 - f.mbits + q - e;  // >= 20
   Bracket b;
-  const float min_normal = ldexpf(1.0f, 1 - f.bias);
-  if (a >= min_normal) {
-    const int e = ilogbf(a);
-    b.sh = f.mbits - e;
-    b.base = (uint32_t)(e + f.bias - 1) << f.mbits;
-  } else {
-    b.sh = f.bias + f.mbits - 1;
-    b.base = 0;
-  }
-  const float v = ldexpf(a, b.sh);
-  const float fl = floorf(v);
-  b.mi = (uint32_t)fl;
-  b.frac = v - fl;
+  b.sh = f.mbits - q;
+  b.base = (uint32_t)(q + f.bias - 1) << f.mbits;
+  b.mi = w < 32 ? M >> w : 0u;
+  const uint32_t D = w < 32 ? M & ((1u << w) - 1u) : M;
+  b.F = w <= 32 ? (w == 32 ? D : D << (32 - w)) : (w < 64 ? D >> (w - 32) : 0u);
   return b;
 }
-
-// floor(frac * 2^32): exact when frac has at most 32 fraction bits, truncated below.
-__device__ __forceinline__ uint32_t sr_threshold(float frac) { return (uint32_t)(frac * 4294967296.0f); }
 
 // y = fl32(x / s) as the fp64 product x * fl64(1 / s) rounded once to fp32 (rs = 1.0 / (double)s,
 // computed once). Identical to the IEEE fp32 quotient: the product is within 2^-52 relative of
@@ -114,11 +115,11 @@ __device__ __forceinline__ uint32_t sr_up(uint32_t F, uint32_t R) {
 }
 
 __device__ __forceinline__ uint32_t rne_up(const Bracket& b) {
-  return (b.frac > 0.5f) | ((b.frac == 0.5f) & (b.mi & 1u));
+  return (b.F > 0x80000000u) | ((b.F == 0x80000000u) & (b.mi & 1u));
 }
 
 // Step (hi - lo) of a bracket, as a float power of two.
-__device__ __forceinline__ float f8_step(const Bracket& b) { return ldexpf(1.0f, -b.sh); }
+__device__ __forceinline__ float f8_step(const Bracket& b) { return __uint_as_float((uint32_t)(127 - b.sh) << 23); }
 
 // Real value of a finite FP8 code.
 __device__ __forceinline__ float f8_value(uint32_t code, F8 f) {

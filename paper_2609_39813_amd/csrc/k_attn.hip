@@ -164,7 +164,7 @@ __global__ __launch_bounds__(256) void attn_d_kernel(AttnDArgs a) {
         const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
         const float step = f8_step(b);
         A += g * ((double)s * (signbit(y) ? -1.0 : 1.0) * (double)b.mi * (double)step - o);
-        F[4 * j + q] = sr_threshold(b.frac);
+        F[4 * j + q] = b.F;
         w[4 * j + q] = (signbit(y) ? -dv[q] : dv[q]) * step;  // exact: a power-of-two scaling
       }
     }

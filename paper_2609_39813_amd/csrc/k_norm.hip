@@ -122,7 +122,7 @@ __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
         const int64_t e = t * a.d + j;
         const float y = div_scale(a.u[e], rs);
         const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
-        F[q][c] = sr_threshold(b.frac);
+        F[q][c] = b.F;
         sv[q][c] = bf16_bits(signbit(y) ? -f8_step(b) : f8_step(b));
         h[q] |= (uint32_t)((a.codes[e] & 0x7Fu) != b.base + b.mi) << c;
       }

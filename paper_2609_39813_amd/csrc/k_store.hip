@@ -86,23 +86,45 @@ __global__ void finalize_scale_kernel(bs_diag* diag, const float* scale_in, floa
   if (scale_out) *scale_out = s;
 }
 
-// Eight consecutive elements per thread (two Philox groups): 16- or 32-byte loads, an
-// 8-byte store of the codes.
-template <typename T, int MODE>
-__device__ __forceinline__ uint32_t code_of(float xv, double rs, F8 f, uint32_t R, uint32_t& nsat) {
-  const float y = div_scale(xv, rs);
-  float a = fabsf(y);
-  if (a > f.fmax) {
-    a = f.fmax;
-    ++nsat;
-  }
-  const Bracket b = f8_bracket(a, f);
-  const uint32_t up = MODE == BS_SR ? sr_up(sr_threshold(b.frac), R) : rne_up(b);
-  return (b.base + b.mi + up) | (signbit(y) ? 0x80u : 0u);
+// gfx950's conversion instructions to the OCP formats ("fp8" = E4M3, "bf8" = E5M2): the packed
+// conversion rounds to nearest even, the stochastic one rounds up iff R + F >= 2^32 with its
+// 32-bit operand R and F = floor(frac 2^32) -- the codec above, bit for bit, for |y| <= FMAX
+// (negative values that round to zero keep the sign bit). Values are clamped to +-FMAX first.
+template <int FMT, bool HI>
+__device__ __forceinline__ uint32_t cvt_rne2(float a, float b, uint32_t old) {
+  return FMT == BS_E5M2 ? (uint32_t)__builtin_amdgcn_cvt_pk_bf8_f32(a, b, (int)old, HI)
+                        : (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)old, HI);
+}
+template <int FMT, int BYTE>
+__device__ __forceinline__ uint32_t cvt_sr1(float a, uint32_t R, uint32_t old) {
+  return FMT == BS_E5M2 ? (uint32_t)__builtin_amdgcn_cvt_sr_bf8_f32(a, (int)R, (int)old, BYTE)
+                        : (uint32_t)__builtin_amdgcn_cvt_sr_fp8_f32(a, (int)R, (int)old, BYTE);
 }
 
-template <typename T, int MODE>
-__global__ __launch_bounds__(256) void quantize_kernel(const T* __restrict__ x, int64_t n, F8 f,
+// y = fl32(x / s) clamped to [-FMAX, FMAX] (sign of zero kept); counts the wave's clamped
+// values (a ballot and a scalar popcount: the count is wave-uniform)
+__device__ __forceinline__ float scaled_clamped(float x, double rs, float fmax, uint32_t& nsat) {
+  const float y = div_scale(x, rs);
+  nsat += (uint32_t)__popcll(__ballot(fabsf(y) > fmax));
+  return __builtin_amdgcn_fmed3f(y, -fmax, fmax);
+}
+
+// Four codes packed into a word from four scaled values (R: the Philox words, SR only).
+template <int FMT, int MODE>
+__device__ __forceinline__ uint32_t codes4(const float* y, const uint32_t* R) {
+  if (MODE == BS_SR) {
+    uint32_t w = cvt_sr1<FMT, 0>(y[0], R[0], 0u);
+    w = cvt_sr1<FMT, 1>(y[1], R[1], w);
+    w = cvt_sr1<FMT, 2>(y[2], R[2], w);
+    return cvt_sr1<FMT, 3>(y[3], R[3], w);
+  }
+  return cvt_rne2<FMT, true>(y[2], y[3], cvt_rne2<FMT, false>(y[0], y[1], 0u));
+}
+
+// Eight consecutive elements per thread (two Philox groups): one 16- or 32-byte load, an 8-byte
+// store of the codes. The last thread of a ragged tensor takes the element-wise path.
+template <typename T, int FMT, int MODE>
+__global__ __launch_bounds__(256) void quantize_kernel(const T* __restrict__ x, int64_t n, float fmax,
                                                        bs_diag* __restrict__ diag, uint8_t* __restrict__ codes,
                                                        uint64_t seed, uint32_t trial, uint32_t use) {
   if (diag->nonfinite) return;
@@ -132,30 +154,24 @@ __global__ __launch_bounds__(256) void quantize_kernel(const T* __restrict__ x, 
 #pragma unroll
       for (int q = 0; q < 8; ++q) xv[q] = q < cnt ? load_f32(x, e0 + q) : 0.0f;
     }
-    Philox4 p0{0, 0, 0, 0}, p1{0, 0, 0, 0};
+    uint32_t R[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if (MODE == BS_SR) {
-      p0 = philox_group(seed, (uint64_t)(2 * t), trial, use);
-      p1 = philox_group(seed, (uint64_t)(2 * t + 1), trial, use);
+      const Philox4 p0 = philox_group(seed, (uint64_t)(2 * t), trial, use);
+      const Philox4 p1 = philox_group(seed, (uint64_t)(2 * t + 1), trial, use);
+      R[0] = p0.w0; R[1] = p0.w1; R[2] = p0.w2; R[3] = p0.w3;
+      R[4] = p1.w0; R[5] = p1.w1; R[6] = p1.w2; R[7] = p1.w3;
     }
-    const uint32_t R[8] = {p0.w0, p0.w1, p0.w2, p0.w3, p1.w0, p1.w1, p1.w2, p1.w3};
-    uint32_t lo = 0, hi = 0;
+    float y[8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      uint32_t sat = 0;
-      const uint32_t code = code_of<T, MODE>(xv[q], rs, f, R[q], sat);
-      if (q < cnt) {
-        nsat += sat;
-        if (q < 4) lo |= code << (8 * q);
-        else hi |= code << (8 * (q - 4));
-      }
-    }
+    for (int q = 0; q < 8; ++q) y[q] = scaled_clamped(xv[q], rs, fmax, nsat);  // padding zeros never clamp
+    const uint32_t lo = codes4<FMT, MODE>(y, R), hi = codes4<FMT, MODE>(y + 4, R + 4);
     if (vec) {
       *(uint2*)(codes + e0) = make_uint2(lo, hi);
     } else {
       for (int q = 0; q < cnt; ++q) codes[e0 + q] = (uint8_t)((q < 4 ? lo >> (8 * q) : hi >> (8 * (q - 4))));
     }
   }
-  nsat = wave_sum_u32(nsat);
+  // nsat is the wave's count here (threads past n contribute zeros to the ballots)
   if ((threadIdx.x & 63) == 0 && nsat) atomicAdd(&diag->n_saturated, nsat);
 }
 
@@ -206,7 +222,7 @@ __device__ __forceinline__ void fresh_count_body(const FreshArgs<X>& a) {
     for (int q = 0; q < 4; ++q) {
       const float y = div_scale(xv[q], rs);
       const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
-      F[r][q] = sr_threshold(ok ? b.frac : 0.0f);
+      F[r][q] = ok ? b.F : 0u;
       const float sc = (signbit(y) ? -1.0f : 1.0f) * f8_step(b);
       c1[r][q] = sc * w1v[q];
       c2[r][q] = sc * w2v[q];
@@ -323,7 +339,10 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
       // at most two blocks per CU, eight 16-byte loads in flight per thread: enough to keep
       // HBM busy while the per-block atomics stay few (same-address atomics serialize)
       const int64_t want = (n / (16 / (xt == BS_F32 ? 4 : 2)) + 255) / 256 + 1;
-      const int blocks = (int)(want < 512 ? want : 512);
+#ifndef BSP_AMAX_BLOCKS
+#define BSP_AMAX_BLOCKS 512
+#endif
+      const int blocks = (int)(want < BSP_AMAX_BLOCKS ? want : BSP_AMAX_BLOCKS);
       ProfScope prof("amax", st);
       if (xt == BS_F32)
         amax_kernel<float><<<blocks, 256, 0, st>>>((const float*)x, n, (uint32_t*)&diag->amax);
@@ -336,12 +355,20 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
     const int64_t threads = (n + 7) / 8;
     const unsigned blocks = (unsigned)((threads + 255) / 256);
     ProfScope prof("quantize", st);
-#define QK(T, M) quantize_kernel<T, M><<<blocks, 256, 0, st>>>((const T*)x, n, f, diag, codes, seed, trial, use)
+#define QK(T, FM, M) \
+  quantize_kernel<T, FM, M><<<blocks, 256, 0, st>>>((const T*)x, n, f.fmax, diag, codes, seed, trial, use)
+#define QKF(T)                                              \
+  if (fmt == BS_E5M2) {                                     \
+    if (mode == BS_SR) QK(T, BS_E5M2, BS_SR); else QK(T, BS_E5M2, BS_RNE); \
+  } else {                                                  \
+    if (mode == BS_SR) QK(T, BS_E4M3, BS_SR); else QK(T, BS_E4M3, BS_RNE); \
+  }
     if (xt == BS_F32) {
-      if (mode == BS_SR) QK(float, BS_SR); else QK(float, BS_RNE);
+      QKF(float);
     } else {
-      if (mode == BS_SR) QK(u16, BS_SR); else QK(u16, BS_RNE);
+      QKF(u16);
     }
+#undef QKF
 #undef QK
   }
   BS_CHECK_LAUNCH();
