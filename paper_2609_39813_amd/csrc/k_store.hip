@@ -48,12 +48,18 @@ __global__ __launch_bounds__(256) void amax_kernel(const T* __restrict__ x, int6
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const uint4* xv = (const uint4*)x;
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  for (; i + 7 * stride < nvec; i += 8 * stride) {
-    uint4 v[8];
+  // eight 16-byte non-temporal loads in flight per thread (streamed once, not kept in cache)
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  constexpr int U = 8;
+  for (; i + (U - 1) * stride < nvec; i += U * stride) {
+    uint4 v[U];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = xv[i + k * stride];
+    for (int k = 0; k < U; ++k) {
+      const u32x4 t = __builtin_nontemporal_load((const u32x4*)(xv + i + k * stride));
+      v[k] = make_uint4(t.x, t.y, t.z, t.w);
+    }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) m = max(m, vec_absmax<T>(v[k]));
+    for (int k = 0; k < U; ++k) m = max(m, vec_absmax<T>(v[k]));
   }
   for (; i < nvec; i += stride) m = max(m, vec_absmax<T>(xv[i]));
   for (int64_t j = nvec * PER + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += stride)
@@ -86,10 +92,12 @@ __global__ void finalize_scale_kernel(bs_diag* diag, const float* scale_in, floa
   if (scale_out) *scale_out = s;
 }
 
-// gfx950's conversion instructions to the OCP formats ("fp8" = E4M3, "bf8" = E5M2): the packed
-// conversion rounds to nearest even, the stochastic one rounds up iff R + F >= 2^32 with its
-// 32-bit operand R and F = floor(frac 2^32) -- the codec above, bit for bit, for |y| <= FMAX
-// (negative values that round to zero keep the sign bit). Values are clamped to +-FMAX first.
+// gfx950's conversion instructions to the OCP formats ("fp8" = E4M3, "bf8" = E5M2), on values
+// clamped to +-FMAX first. The packed conversion rounds to nearest even: the codec above, bit for
+// bit (negative values that round to zero keep the sign bit). The stochastic one rounds up iff
+// R + F >= 2^32 with its 32-bit operand R for every normal FP8 magnitude (there F has at most 21
+// significant bits); below the smallest normal magnitude it does not resolve F to all 32 bits
+// (at R + F = 2^32 exactly it stays down), so nonzero values there take the integer path.
 template <int FMT, bool HI>
 __device__ __forceinline__ uint32_t cvt_rne2(float a, float b, uint32_t old) {
   return FMT == BS_E5M2 ? (uint32_t)__builtin_amdgcn_cvt_pk_bf8_f32(a, b, (int)old, HI)
@@ -109,6 +117,12 @@ __device__ __forceinline__ float scaled_clamped(float x, double rs, float fmax, 
   return __builtin_amdgcn_fmed3f(y, -fmax, fmax);
 }
 
+// stochastic rounding of one clamped value by the integer codec
+__device__ __forceinline__ uint32_t sr_code(float y, uint32_t R, F8 f) {
+  const Bracket b = f8_bracket(fabsf(y), f);
+  return (b.base + b.mi + sr_up(b.F, R)) | (signbit(y) ? 0x80u : 0u);
+}
+
 // Four codes packed into a word from four scaled values (R: the Philox words, SR only).
 template <int FMT, int MODE>
 __device__ __forceinline__ uint32_t codes4(const float* y, const uint32_t* R) {
@@ -116,7 +130,19 @@ __device__ __forceinline__ uint32_t codes4(const float* y, const uint32_t* R) {
     uint32_t w = cvt_sr1<FMT, 0>(y[0], R[0], 0u);
     w = cvt_sr1<FMT, 1>(y[1], R[1], w);
     w = cvt_sr1<FMT, 2>(y[2], R[2], w);
-    return cvt_sr1<FMT, 3>(y[3], R[3], w);
+    w = cvt_sr1<FMT, 3>(y[3], R[3], w);
+    const F8 f = f8_format(FMT);
+    const float min_normal = __uint_as_float((uint32_t)(128 - f.bias) << 23);
+    bool sub = false;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sub |= fabsf(y[q]) < min_normal && y[q] != 0.0f;
+    if (sub) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (fabsf(y[q]) < min_normal && y[q] != 0.0f)
+          w = (w & ~(0xFFu << (8 * q))) | (sr_code(y[q], R[q], f) << (8 * q));
+    }
+    return w;
   }
   return cvt_rne2<FMT, true>(y[2], y[3], cvt_rne2<FMT, false>(y[0], y[1], 0u));
 }
@@ -336,13 +362,10 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
   if (!amax_done) {
     init_diag_kernel<<<1, 64, 0, st>>>(diag);
     if (n > 0 && !scale_in) {
-      // at most two blocks per CU, eight 16-byte loads in flight per thread: enough to keep
+      // at most eight blocks per CU, eight 16-byte loads in flight per thread: enough to keep
       // HBM busy while the per-block atomics stay few (same-address atomics serialize)
       const int64_t want = (n / (16 / (xt == BS_F32 ? 4 : 2)) + 255) / 256 + 1;
-#ifndef BSP_AMAX_BLOCKS
-#define BSP_AMAX_BLOCKS 512
-#endif
-      const int blocks = (int)(want < BSP_AMAX_BLOCKS ? want : BSP_AMAX_BLOCKS);
+      const int blocks = (int)(want < 2048 ? want : 2048);
       ProfScope prof("amax", st);
       if (xt == BS_F32)
         amax_kernel<float><<<blocks, 256, 0, st>>>((const float*)x, n, (uint32_t*)&diag->amax);

@@ -80,3 +80,56 @@ def test_large_tensor_sampled_sr(lib):
     idx = np.unique(np.concatenate([np.arange(4096), np.random.default_rng(0).integers(0, n, 200000), [n - 1]]))
     ref, _ = oq.round_scaled(oq.scaled(xf[idx], sc), fp8.E5M2, oq.SR, 0xB5F4, 9, 1025, elements=idx.astype(np.uint64))
     assert np.array_equal(codes[idx], ref)
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+def test_sr_decision_at_the_full_word_boundary(lib, fmt):
+    """Magnitudes just above zero whose rounding threshold F uses all 32 bits (the fraction of
+    the smallest step is the whole 24-bit significand), placed so that R + F lands exactly on
+    2^32 (rounds up) or one below it (stays down) for each element's own Philox word R."""
+    f = FMT[fmt]
+    seed, trial, use = 0xB5F9, 2, 3
+    n = 1 << 20
+    R = oq.philox.words(seed, trial, use, np.arange(n, dtype=np.uint64)).astype(np.int64)
+    T = (1 << 32) - R                              # F = T rounds up, F = T - 1 does not
+    cand = np.where((T > (1 << 23)) & (T < (1 << 24)))[0]
+    assert cand.size > 1000
+    # y = M 2^(e-23) with e chosen so that w = 32: F = M exactly (E4M3 e = -18, E5M2 e = -25)
+    e = -18 if fmt == "e4m3" else -25
+    M = T[cand] - (np.arange(cand.size) & 1)       # even positions: exactly on the boundary
+    g = torch.Generator().manual_seed(5)
+    x = (torch.randn(n, generator=g) * 0.3).numpy().astype(np.float32)
+    sign = np.where(np.arange(cand.size) % 4 < 2, 1.0, -1.0)
+    x[cand] = (sign * np.ldexp(M.astype(np.float64), e - 23)).astype(np.float32)
+    codes, s, dg = run(lib, torch.from_numpy(x), fmt, "sr", seed=seed, trial=trial, use=use, scale=torch.ones(1))
+    ref, nsat = oq.round_scaled(x, f, oq.SR, seed, trial, use)
+    bad = np.where(codes != ref)[0]
+    assert bad.size == 0, [(int(i), float(x[i]), int(R[i]), int(codes[i]), int(ref[i])) for i in bad[:8]]
+    assert dg["n_saturated"] == nsat
+    up = (codes[cand] & 0x7F) == 1
+    assert np.array_equal(up, (np.arange(cand.size) & 1) == 0)
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+def test_sr_decision_at_the_boundary_normal_range(lib, fmt):
+    """Normal magnitudes in [1, 2): F = D 2^(32 - w) with D the w discarded significand bits
+    (w = 20 for E4M3, 21 for E5M2). D = ceil((2^32 - R) / 2^(32 - w)) is the smallest fraction that
+    rounds up for the element's word R; D - 1 stays down."""
+    f = FMT[fmt]
+    seed, trial, use = 0xB5FA, 5, 7
+    n = 1 << 16
+    R = oq.philox.words(seed, trial, use, np.arange(n, dtype=np.uint64)).astype(np.int64)
+    w = 23 - f.mbits
+    D = -((R - (1 << 32)) // (1 << (32 - w)))        # ceil((2^32 - R) / 2^(32 - w))
+    keep = D < (1 << w)
+    D = np.where(np.arange(n) & 1, D - 1, D)
+    x = np.ldexp(((1 << w) * (1 << f.mbits) + D).astype(np.float64), -23).astype(np.float32)
+    x = np.where(np.arange(n) % 4 < 2, x, -x).astype(np.float32)
+    x[~keep] = 1.0
+    codes, s, dg = run(lib, torch.from_numpy(x), fmt, "sr", seed=seed, trial=trial, use=use, scale=torch.ones(1))
+    ref, _ = oq.round_scaled(x, f, oq.SR, seed, trial, use)
+    bad = np.where(codes != ref)[0]
+    assert bad.size == 0, [(int(i), float(x[i]), int(R[i]), int(codes[i]), int(ref[i])) for i in bad[:8]]
+    one = int(fp8.encode(np.array([1.0]), np.array([False]), f)[0])  # the down value of every element
+    up = (codes & 0x7F) != one
+    assert np.array_equal(up[keep], (np.arange(n)[keep] & 1) == 0)
