@@ -48,9 +48,25 @@ __global__ __launch_bounds__(256) void amax_kernel(const T* __restrict__ x, int6
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const uint4* xv = (const uint4*)x;
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  // eight 16-byte non-temporal loads in flight per thread (streamed once, not kept in cache)
+  // Each block streams its own contiguous range of vectors, eight 16-byte non-temporal loads in
+  // flight per thread (read once, not kept in cache); the remainder goes grid-strided.
   typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
   constexpr int U = 8;
+  {
+    const int64_t per = ((nvec / gridDim.x) / (U * blockDim.x)) * (U * blockDim.x);
+    const int64_t b0 = (int64_t)blockIdx.x * per;
+    for (int64_t j = 0; j < per; j += U * blockDim.x) {
+      uint4 v[U];
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        const u32x4 t = __builtin_nontemporal_load((const u32x4*)(xv + b0 + j + k * blockDim.x + threadIdx.x));
+        v[k] = make_uint4(t.x, t.y, t.z, t.w);
+      }
+#pragma unroll
+      for (int k = 0; k < U; ++k) m = max(m, vec_absmax<T>(v[k]));
+    }
+    i = per * gridDim.x + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  }
   for (; i + (U - 1) * stride < nvec; i += U * stride) {
     uint4 v[U];
 #pragma unroll
@@ -362,10 +378,10 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
   if (!amax_done) {
     init_diag_kernel<<<1, 64, 0, st>>>(diag);
     if (n > 0 && !scale_in) {
-      // at most eight blocks per CU, eight 16-byte loads in flight per thread: enough to keep
-      // HBM busy while the per-block atomics stay few (same-address atomics serialize)
+      // four blocks per CU, each streaming a contiguous range with eight 16-byte loads in flight
+      // per thread; the per-block atomics stay few (same-address atomics serialize)
       const int64_t want = (n / (16 / (xt == BS_F32 ? 4 : 2)) + 255) / 256 + 1;
-      const int blocks = (int)(want < 2048 ? want : 2048);
+      const int blocks = (int)(want < 1024 ? want : 1024);
       ProfScope prof("amax", st);
       if (xt == BS_F32)
         amax_kernel<float><<<blocks, 256, 0, st>>>((const float*)x, n, (uint32_t*)&diag->amax);
