@@ -173,6 +173,53 @@ bs_status bs_attn_bwd_policy(const void* Q, const void* Kt, const void* V, const
                              bs_diag* diag, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------
+ * bs_attn_pstore_policy -- attention whose probabilities P pass through an FP8 store, and
+ * the two uses of that store in the backward: the gradient of V and the softmax's backward
+ * (App. B.2, Eq. app-ref and Eq. app-errors; App. B.3; App. B.4; Table app-theory-errors).
+ *
+ * Forward: P = softmax(c Q K^T) (causal: key j <= query i), computed in fp32 with the row
+ * max m of x = fl32(c log2(e) S) and row sum l, p = fl32(2^(x - m)) / l rounded once more to
+ * fp32 (so the largest entry of a row is exactly fl32(1/l)). (C_P, s) = FP8 store of P
+ * (amax = max P, mode fwd_mode, trial 0, use store_id*256; element ((b H + h) S + i) S + j).
+ * O = deq(C_P) V (the forward as it ran: p_q = deq(C_P)).
+ * Backward with the forward held fixed and the incoming gradient dO: dp = dO V^T per row;
+ * reference dV_ref = p_q^T dO, ds = J(p) dp with J(x) = diag(x) - x x^T, dQ_ref = c ds K,
+ * dK_ref = c ds^T Q. A policy names the softmax's backward read first, then the dV read:
+ *   softmax  U J(p)   R J(p_q)   N J(a)   K K(a) = diag(a 1^T a) - a a^T
+ *            J2 (a+b)/2 diag - (a b^T + b a^T)/2 = J2(a, b)    Q2 J2(p_q, a)
+ *   dV       U p      R p_q      N a
+ * where a and b are new stochastic roundings of y = fl32(P/s) at the forward's scale, trial
+ * k = 1..K, use ids store_id*256+1 (a) and +2 (b); a policy that reads N at both uses reads
+ * the same a. The mean over the K trials is formed exactly from per-row and per-element sums
+ * of the up-decisions (every trial's rounding is drawn; no trial's gradient materializes).
+ *
+ *   Q, Kt (the keys), V, dO [B,H,S,dh] bf16, 16-byte aligned; dh == 64; S >= 4 a multiple of 4;
+ *   B*H <= 65535. pol (host) [n_pol], n_pol in [1, 8]; K in [1, 32].
+ *   O [B,H,S,dh] fp32 (nullable); P_out [B,H,S,S] fp32 (nullable): the realized P;
+ *   P_codes [B,H,S,S] uint8 (zero above the causal diagonal); P_scale [1] fp32 (nullable);
+ *   dQ_ref, dK_ref, dV_ref [B,H,S,dh] fp32; estimates dQ, dK, dV [n_pol][B*H*S*dh]
+ *   (se must be NULL: BS_EUNSUPPORTED otherwise). diag: the store's amax, scale, saturations;
+ *   nonfinite != 0 when a row sum is not a positive finite number (then nothing else is written).
+ *   ws: bs_attn_pstore_workspace_size(B, H, S, dh, K, causal) bytes (0 for shapes the call
+ *   rejects); about 8 causal-half S^2 fp32 fields per head plus 12 [B,H,S,dh] fp32 arrays.
+ * Returns BS_EINVAL for a null required pointer, a bad enum, K or n_pol out of range or a
+ * misaligned pointer; BS_ESHAPE for dh != 64 or S not a multiple of 4.
+ * ---------------------------------------------------------------------------------- */
+typedef enum { BS_SM_U = 0, BS_SM_R = 1, BS_SM_N = 2, BS_SM_K = 3, BS_SM_J2 = 4, BS_SM_Q2 = 5 } bs_softmax_read;
+typedef struct {
+  bs_softmax_read softmax_read;
+  bs_read v_read;
+} bs_pstore_policy;
+
+size_t bs_attn_pstore_workspace_size(int B, int H, int S, int dh, int K, int causal);
+bs_status bs_attn_pstore_policy(const void* Q, const void* Kt, const void* V, const void* dO, int B, int H, int S,
+                                int dh, int causal, float softmax_scale, bs_fp8 fmt, bs_round fwd_mode,
+                                const bs_pstore_policy* pol, int n_pol, int K, uint64_t seed, uint32_t store_id,
+                                float* O, float* P_out, uint8_t* P_codes, float* P_scale, float* dQ_ref,
+                                float* dK_ref, float* dV_ref, bs_est dQ, bs_est dK, bs_est dV, bs_diag* diag,
+                                void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
  * bs_linear_bwd_policy -- Linear backward whose incoming gradient is stochastically
  * rounded to FP8 (E5M2 in the HYBRID recipe, App. D.1), read by two uses.
  *
@@ -291,7 +338,7 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* w, cons
  *   bs_profile_enable(1) clears earlier records and starts recording a pair of HIP
  *   events on the launch stream around each launch of the instrumented kernels
  *   ("fresh_count", "fresh_count_se", "fresh_count_kappa", "amax", "quantize", "gemm",
- *   "rmsnorm_fwd", "attn_fwd", "attn_bwd");
+ *   "rmsnorm_fwd", "attn_fwd", "attn_bwd", "pstore_fwd", "pstore_rows", "pstore_dq", "pstore_dkv");
  *   bs_profile_enable(0) stops and frees them. bs_profile_read waits for the recorded
  *   events of `kernel` (NULL: all) and returns their summed elapsed time and count.
  *   Return values are bs_status codes.

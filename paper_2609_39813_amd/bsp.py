@@ -61,6 +61,17 @@ _attn_ws = _sig("bs_attn_workspace_size", _sz, [_int, _int, _int, _int, _int, _i
 _attn = _sig("bs_attn_bwd_policy", _int,
              [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _int, _f32, _vp, _int, _int, ctypes.POINTER(_int), _int,
               _int, _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, _vp, _vp, _sz, _vp])
+
+
+class PstorePolicy(ctypes.Structure):
+    _fields_ = [("softmax_read", _int), ("v_read", _int)]
+
+
+SOFTMAX_READ = {"U": 0, "R": 1, "N": 2, "K": 3, "J2": 4, "Q2": 5}
+_ps_ws = _sig("bs_attn_pstore_workspace_size", _sz, [_int] * 6)
+_ps = _sig("bs_attn_pstore_policy", _int,
+           [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _int, _int, ctypes.POINTER(PstorePolicy), _int,
+            _int, _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, Est, _vp, _vp, _sz, _vp])
 _lin_ws = _sig("bs_linear_bwd_workspace_size", _sz, [_i64, _i64, _i64, _int, _int])
 _lin = _sig("bs_linear_bwd_policy", _int,
             [_vp, _vp, _vp, _int, _i64, _i64, _i64, _int, ctypes.POINTER(_int), _int, _int, _u64, _u32, _vp, _vp,
@@ -106,7 +117,7 @@ def profile_read(kernel=None):
 
 EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
             "bs_policy_bias_estimate", "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
-            "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
+            "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_attn_pstore_workspace_size", "bs_attn_pstore_policy", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
             "bs_decoder_layer_workspace_size", "bs_decoder_layer_policy", "bs_profile_enable", "bs_profile_read"]
 
 
@@ -280,6 +291,51 @@ def attn_bwd_policy(Q, Kt, V, dO, *, causal=True, scale=None, O=None, fmt="e4m3"
 
 def attn_workspace(B, H, S, dh, n_pol, K, device):
     return _workspace(_attn_ws(B, H, S, dh, n_pol, K), device)
+
+
+def parse_pstore_policy(code):
+    """'J2/R' -> the softmax's backward read first, then the read at the gradient of V."""
+    sm, v = code.split("/")
+    return PstorePolicy(SOFTMAX_READ[sm], READ[v])
+
+
+def attn_pstore_workspace(B, H, S, dh, K, causal, device):
+    n = _ps_ws(B, H, S, dh, K, int(causal))
+    if n == 0:
+        raise BspError(2, "bs_attn_pstore_workspace_size")
+    return _workspace(n, device)
+
+
+def attn_pstore_policy(Q, Kt, V, dO, *, causal=True, scale=None, fmt="e4m3", fwd_mode="rne",
+                       policies=("U/R", "R/R", "U/U", "N/N", "R/U", "K/R", "J2/R", "Q2/R"), K=16, seed=0, store_id=0,
+                       want_p=False, ws=None):
+    """Attention with an FP8 store of P and the per-policy estimates of its two uses
+    (bs_attn_pstore_policy)."""
+    _dev_check(Q, Kt, V, dO)
+    B, H, S, dh = Q.shape
+    dev = Q.device
+    c = 1.0 / dh ** 0.5 if scale is None else scale
+    pol = (PstorePolicy * len(policies))(*[parse_pstore_policy(p) for p in policies])
+    shp = (B, H, S, dh)
+    out = {"O": torch.empty(shp, dtype=torch.float32, device=dev),
+           "P": torch.empty(B, H, S, S, dtype=torch.float32, device=dev) if want_p else None,
+           "P_codes": torch.empty(B, H, S, S, dtype=torch.uint8, device=dev),
+           "P_scale": torch.empty(1, dtype=torch.float32, device=dev),
+           "dQ_ref": torch.empty(shp, dtype=torch.float32, device=dev),
+           "dK_ref": torch.empty(shp, dtype=torch.float32, device=dev),
+           "dV_ref": torch.empty(shp, dtype=torch.float32, device=dev),
+           "diag": new_diag(dev)}
+    numel = B * H * S * dh
+    ests = [_est(len(policies), numel, dev, False) for _ in range(3)]
+    if ws is None:
+        ws = attn_pstore_workspace(B, H, S, dh, K, causal, dev)
+    _check(_ps(_p(Q), _p(Kt), _p(V), _p(dO), B, H, S, dh, int(causal), c, _FMT[fmt], _MODE[fwd_mode], pol,
+               len(policies), K, seed, store_id, _p(out["O"]), _p(out["P"]), _p(out["P_codes"]), _p(out["P_scale"]),
+               _p(out["dQ_ref"]), _p(out["dK_ref"]), _p(out["dV_ref"]), ests[0][1], ests[1][1], ests[2][1],
+               _p(out["diag"]), _p(ws), ws.numel(), _stream()), "bs_attn_pstore_policy")
+    out["dQ"], out["dK"], out["dV"] = (e[0] for e in ests)
+    out["policies"] = list(policies)
+    return out
 
 
 def linear_bwd_policy(X, W, dY, *, fmt="e5m2", sharings=("shared", "per_use"), K=16, seed=0, store_id=0,

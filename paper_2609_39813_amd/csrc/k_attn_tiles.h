@@ -1,0 +1,95 @@
+// Tile helpers of the attention kernels (dh = 64): LDS tile layouts, MFMA operand fragments,
+// exact three-term bf16 splits and the register-staged tile copies.
+//
+// All tiles are 64 x 64 bf16 in LDS with rows of 128 B whose 16-byte chunks are XOR-swizzled
+// by (row & 7); MFMA 16x16x32 bf16 operands are read as 16-byte fragments: lane l takes row
+// r0 + (l & 15), columns k0 + 8 (l >> 4) .. + 7. A 16x16 result tile holds D[4 (l >> 4) + r]
+// [l & 15] in register r of lane l.
+#pragma once
+#include "bsp_kernels.h"
+
+namespace bsp {
+
+constexpr int AT = 64;  // block rows / keys, and dh
+
+__device__ __forceinline__ int sw(int row, int col) { return row * AT + ((((col >> 3) ^ (row & 7)) << 3) | (col & 7)); }
+
+__device__ __forceinline__ floatx4 mfma(bf16x8 a, bf16x8 b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// P = 2^(c log2(e) S - m) / l with m the row max of c log2(e) S: one hardware exp2 per
+// element (a few ulps; the exponent's rounding adds |m| 2^-24, below 1e-6 for these scores)
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ int swt(int row, int unit) { return row * AT + ((unit ^ (row & 15)) << 2); }
+
+__device__ __forceinline__ bf16x8 frag_t(const u16* T, int row, int s, int g) {
+  const uint2 a = *(const uint2*)(T + swt(row, 8 * s + g));
+  const uint2 b = *(const uint2*)(T + swt(row, 8 * s + 4 + g));
+  return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+}
+
+// the three bf16 terms (round to nearest, then the exact remainders) of eight fp32 values as
+// MFMA operands, converted two at a time into packed registers
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
+  const bf16x2 v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ float lo_f32(uint32_t p) { return __uint_as_float(p << 16); }
+__device__ __forceinline__ float hi_f32(uint32_t p) { return __uint_as_float(p & 0xFFFF0000u); }
+__device__ __forceinline__ void pack3(const float* v, bf16x8* t) {
+  uint32_t w[3][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float a = v[2 * i], b = v[2 * i + 1];
+    const uint32_t p0 = pk_bf16(a, b);
+    const float ra = a - lo_f32(p0), rb = b - hi_f32(p0);
+    const uint32_t p1 = pk_bf16(ra, rb);
+    const float sa = ra - lo_f32(p1), sb = rb - hi_f32(p1);
+    w[0][i] = p0;
+    w[1][i] = p1;
+    w[2][i] = pk_bf16(sa, sb);
+  }
+#pragma unroll
+  for (int p = 0; p < 3; ++p) t[p] = __builtin_bit_cast(bf16x8, make_uint4(w[p][0], w[p][1], w[p][2], w[p][3]));
+}
+
+// a row-major [64][64] bf16 tile (rows r0.. of a [*, 64] matrix with nrow rows, zeros past
+// them) as two 16-byte pieces per thread, and its store into LDS
+struct TileRegs {
+  uint4 v[2];
+};
+__device__ __forceinline__ void tile_fetch(TileRegs& t, const u16* __restrict__ g, int r0, int nrow) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (threadIdx.x >> 3) + 32 * i, c = (threadIdx.x & 7) * 8;
+    t.v[i] = r0 + r < nrow ? *(const uint4*)(g + (int64_t)(r0 + r) * AT + c) : make_uint4(0, 0, 0, 0);
+  }
+}
+__device__ __forceinline__ void tile_put(u16* T, const TileRegs& t) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (threadIdx.x >> 3) + 32 * i, c = (threadIdx.x & 7) * 8;
+    *(uint4*)(T + sw(r, c)) = t.v[i];
+  }
+}
+// columns c0 .. c0 + 63 of a transposed [64][ld] matrix (ld a multiple of 64, zero padded)
+__device__ __forceinline__ void tile_fetch_t(TileRegs& t, const u16* __restrict__ g, int c0, int ld) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (threadIdx.x >> 3) + 32 * i, c = (threadIdx.x & 7) * 8;
+    t.v[i] = *(const uint4*)(g + (int64_t)r * ld + c0 + c);
+  }
+}
+__device__ __forceinline__ void tile_put_t(u16* T, const TileRegs& t) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (threadIdx.x >> 3) + 32 * i, u = (threadIdx.x & 7) * 2;
+    *(uint2*)(T + swt(r, u)) = make_uint2(t.v[i].x, t.v[i].y);
+    *(uint2*)(T + swt(r, u + 1)) = make_uint2(t.v[i].z, t.v[i].w);
+  }
+}
+
+}  // namespace bsp

@@ -1,0 +1,744 @@
+// The FP8 store of attention probabilities (gfx950, dh = 64) and the per-use estimates of its
+// two uses: the gradient of V reads p, p_q or a new rounding a; the softmax's backward reads
+// J(p), J(p_q), J(a), K(a), J2(a, b) or J2(p_q, a) (App. B.2-B.4).
+//
+// Every pass recomputes its 64 x 64 tiles of scores the same way, so that P is bit-identical in
+// all of them: with m the row max of x = fl(c log2(e) S) (fl: rounded, never contracted into an
+// FMA), p = 2^(x - m) / l. The largest probability of a row is then exactly 1 / l, and the
+// store's amax is the largest 1 / l. Query-major passes (forward, row sums, dQ) hold in each lane
+// one query and 16 keys: the lane's scores are an MFMA result tile of K Q^T (keys on the tile's
+// rows), and the products with K and V take them as register operands (k-step order as in the
+// attention backward). The key-major pass (dK, dV) reads the bias fields the dQ pass stored.
+//
+// Collapsed trials. With r = p_q - p, a new rounding a_k = p + e + u_k h (e = lo - p, h the grid
+// step, u_k its up-decision) and a row's D = p . dp, each policy's mean over the K trials of
+// Jhat dp - J(p) dp is a combination of per-row sums (Ga_k = sum u_k h dp, Ha_k = sum u_k h,
+// ...) and per-element sums over trials (n = sum u_k, sum u_k Ga_k, ...): the trials never
+// materialize, and the dQ / dK contractions run once per field.
+#include "k_attn_tiles.h"
+#include "k_pstore.h"
+
+namespace bsp {
+
+namespace {
+
+// grid value (code's value) of an OCP FP8 code by the conversion instruction
+template <int FMT>
+__device__ __forceinline__ float f8_val(uint32_t word, int byte) {
+  switch (byte) {
+    case 0: return FMT == BS_E5M2 ? __builtin_amdgcn_cvt_f32_bf8((int)word, 0) : __builtin_amdgcn_cvt_f32_fp8((int)word, 0);
+    case 1: return FMT == BS_E5M2 ? __builtin_amdgcn_cvt_f32_bf8((int)word, 1) : __builtin_amdgcn_cvt_f32_fp8((int)word, 1);
+    case 2: return FMT == BS_E5M2 ? __builtin_amdgcn_cvt_f32_bf8((int)word, 2) : __builtin_amdgcn_cvt_f32_fp8((int)word, 2);
+    default: return FMT == BS_E5M2 ? __builtin_amdgcn_cvt_f32_bf8((int)word, 3) : __builtin_amdgcn_cvt_f32_fp8((int)word, 3);
+  }
+}
+
+// The query-major scaffold shared by the forward, row-sum and dQ passes: block (bh, query block),
+// wave w's lane (g, c16) owns query q = q0 + 16 w + c16 and, within a key block, the keys
+// k0 + 16 t + 4 g + r (t, r < 4).
+struct QMajor {
+  int bh, qb, q0, q, w, g, c16;
+  bool qok;
+  int64_t hb, tb, rb;
+  float mq, ilq;
+  bf16x8 fq[2], fdo[2];
+};
+
+__device__ __forceinline__ QMajor qmajor_setup(const PstoreArgs& a, bool need_do) {
+  QMajor z;
+  const int lane = threadIdx.x & 63;
+  z.w = threadIdx.x >> 6;
+  z.g = lane >> 4;
+  z.c16 = lane & 15;
+  z.bh = blockIdx.x;
+  z.qb = a.causal ? (int)gridDim.y - 1 - (int)blockIdx.y : (int)blockIdx.y;  // heaviest first
+  z.q0 = z.qb * AT;
+  z.q = z.q0 + 16 * z.w + z.c16;
+  z.qok = z.q < a.S;
+  z.hb = (int64_t)z.bh * a.S * AT;
+  z.tb = (int64_t)z.bh * AT * a.Sp;
+  z.rb = (int64_t)z.bh * a.S;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int64_t e = z.hb + (int64_t)z.q * AT + 32 * s + 8 * z.g;
+    z.fq[s] = __builtin_bit_cast(bf16x8, z.qok ? *(const uint4*)(a.Q + e) : make_uint4(0, 0, 0, 0));
+    z.fdo[s] = __builtin_bit_cast(bf16x8, (need_do && z.qok) ? *(const uint4*)(a.dO + e) : make_uint4(0, 0, 0, 0));
+  }
+  z.mq = z.qok ? a.m[z.rb + z.q] : 0.0f;
+  z.ilq = z.qok ? 1.0f / a.l[z.rb + z.q] : 0.0f;
+  return z;
+}
+
+// p of the lane's 16 keys of key block k0 (tK: K rows of the block in LDS)
+__device__ __forceinline__ void probs(const PstoreArgs& a, const QMajor& z, const u16* tK, int k0, float (&p)[4][4]) {
+#pragma clang fp contract(off)  // x = fl(c log2(e) s) is rounded before m is subtracted
+  floatx4 sv[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) sv[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) sv[t] = mfma(*(const bf16x8*)(tK + sw(16 * t + z.c16, 32 * s + 8 * z.g)), z.fq[s], sv[t]);
+  const float c2 = a.scale * kLog2e;
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int key = k0 + 16 * t + 4 * z.g + r;
+      const bool ok = z.qok && key < a.S && (!a.causal || key <= z.q);
+      const float x = c2 * sv[t][r];
+      p[t][r] = ok ? __builtin_amdgcn_exp2f(x - z.mq) * z.ilq : 0.0f;
+    }
+}
+
+// dp = dO . v_key of the lane's query and 16 keys (tV: V rows of the block in LDS)
+__device__ __forceinline__ void dprobs(const QMajor& z, const u16* tV, float (&dp)[4][4]) {
+  floatx4 dv[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) dv[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) dv[t] = mfma(*(const bf16x8*)(tV + sw(16 * t + z.c16, 32 * s + 8 * z.g)), z.fdo[s], dv[t]);
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dp[t][r] = dv[t][r];
+}
+
+// the element index of P[bh][q][key] (a multiple of 4 for key = 16 t + 4 g, since S % 4 == 0)
+__device__ __forceinline__ uint64_t pelem(const PstoreArgs& a, const QMajor& z, int key) {
+  return ((uint64_t)z.rb + (uint64_t)z.q) * (uint64_t)a.S + (uint64_t)key;
+}
+
+// first element of the bias-field tile (query block qb, key block kb) of head bh
+__device__ __forceinline__ int64_t fld_tile(const PstoreArgs& a, int bh, int qb, int kb, int nqb) {
+  const int64_t per = pstore_tiles(nqb, a.causal);
+  const int64_t t = a.causal ? (int64_t)qb * (qb + 1) / 2 + kb : (int64_t)qb * nqb + kb;
+  return ((int64_t)bh * per + t) * AT * AT;
+}
+
+// residuals of one element: r = p_q - p, e = lo - p, h = step (real units), F = SR threshold
+struct Resid {
+  float r, e, h;
+  uint32_t F;
+};
+__device__ __forceinline__ Resid resid(float p, float val, float s, double rs, F8 f) {
+  Resid o;
+  const float y = fminf(div_scale(p, rs), f.fmax);
+  const Bracket b = f8_bracket(y, f);
+  const float step = f8_step(b);
+  o.r = fmaf(s, val, -p);
+  o.e = fmaf(s, (float)b.mi * step, -p);
+  o.h = s * step;
+  o.F = b.F;
+  return o;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------------
+// the store's scale: amax = max over rows of 1 / l, s = fl32(amax / FMAX)
+// ------------------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void pstore_scale_kernel(const float* __restrict__ l, int64_t rows, float fmax,
+                                                            bs_diag* __restrict__ diag, float* __restrict__ scale_out) {
+  uint32_t m = 0;
+  bool bad = false;
+  for (int64_t i = threadIdx.x; i < rows; i += blockDim.x) {
+    const float v = l[i];
+    bad |= !(v > 0.0f) || !isfinite(v);
+    m = max(m, __float_as_uint(1.0f / v));
+  }
+  m = wave_max_u32(m);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __shared__ uint32_t red[16];
+  __shared__ int anybad;
+  if (threadIdx.x == 0) anybad = 0;
+  __syncthreads();
+  if (bad) anybad = 1;
+  if (lane == 0) red[w] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < (int)(blockDim.x >> 6); ++k) m = max(m, red[k]);
+    m = max(m, red[0]);
+    const float amax = __uint_as_float(m);
+    diag->amax = amax;
+    diag->nonfinite = anybad ? 1u : 0u;
+    diag->n_saturated = 0;
+    const float sc = (anybad || !(amax > 0.0f)) ? 1.0f : __fdiv_rn(amax, fmax);
+    diag->scale = sc;
+    if (scale_out) *scale_out = sc;
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// forward: codes of P (RNE or SR), P_out, O = s val(C) V (val(C) exact in bf16, one MFMA term)
+// ------------------------------------------------------------------------------------
+template <int FMT>
+__global__ __launch_bounds__(256, 2) void pstore_fwd_kernel(PstoreArgs a) {
+  __shared__ __attribute__((aligned(16))) u16 sm[2][2][AT * AT];  // K, V^T
+  if (a.diag->nonfinite) return;
+  const QMajor z = qmajor_setup(a, false);
+  const float s = a.diag->scale;
+  const double rs = 1.0 / (double)s;
+  const F8 f = a.f;
+  const float min_normal = __uint_as_float((uint32_t)(128 - f.bias) << 23);
+  floatx4 acc[4];
+#pragma unroll
+  for (int n = 0; n < 4; ++n) acc[n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  TileRegs pf[2];
+  auto fetch = [&](int k0) {
+    tile_fetch(pf[0], a.K + z.hb, k0, a.S);
+    tile_fetch_t(pf[1], a.Vt + z.tb, k0, a.Sp);
+  };
+  auto put = [&](int st) {
+    tile_put(sm[st][0], pf[0]);
+    tile_put_t(sm[st][1], pf[1]);
+  };
+  const int nkb_all = (a.S + AT - 1) / AT;
+  const int nkb = a.causal ? z.qb + 1 : nkb_all;
+  uint32_t nsat = 0;
+  fetch(0);
+  put(0);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int st = kb & 1, k0 = kb * AT;
+    if (kb + 1 < nkb) fetch(k0 + AT);
+    float p[4][4];
+    probs(a, z, sm[st][0], k0, p);
+    float val[4][4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int key = k0 + 16 * t + 4 * z.g;
+      float y[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float yy = div_scale(p[t][r], rs);
+        nsat += yy > f.fmax ? 1u : 0u;
+        y[r] = fminf(yy, f.fmax);
+      }
+      uint32_t w;
+      if (a.fwd_mode == BS_SR) {
+        const Philox4 ph = philox_group(a.seed, pelem(a, z, key) >> 2, 0, a.use_fwd);
+        const uint32_t R[4] = {ph.w0, ph.w1, ph.w2, ph.w3};
+        w = FMT == BS_E5M2 ? (uint32_t)__builtin_amdgcn_cvt_sr_bf8_f32(y[0], (int)R[0], 0, 0)
+                           : (uint32_t)__builtin_amdgcn_cvt_sr_fp8_f32(y[0], (int)R[0], 0, 0);
+        w = FMT == BS_E5M2 ? (uint32_t)__builtin_amdgcn_cvt_sr_bf8_f32(y[1], (int)R[1], (int)w, 1)
+                           : (uint32_t)__builtin_amdgcn_cvt_sr_fp8_f32(y[1], (int)R[1], (int)w, 1);
+        w = FMT == BS_E5M2 ? (uint32_t)__builtin_amdgcn_cvt_sr_bf8_f32(y[2], (int)R[2], (int)w, 2)
+                           : (uint32_t)__builtin_amdgcn_cvt_sr_fp8_f32(y[2], (int)R[2], (int)w, 2);
+        w = FMT == BS_E5M2 ? (uint32_t)__builtin_amdgcn_cvt_sr_bf8_f32(y[3], (int)R[3], (int)w, 3)
+                           : (uint32_t)__builtin_amdgcn_cvt_sr_fp8_f32(y[3], (int)R[3], (int)w, 3);
+        // below the smallest normal magnitude the instruction does not resolve F to 32 bits
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (y[r] < min_normal && y[r] != 0.0f) {
+            const Bracket b = f8_bracket(y[r], f);
+            w = (w & ~(0xFFu << (8 * r))) | ((b.base + b.mi + sr_up(b.F, R[r])) << (8 * r));
+          }
+      } else {
+        w = FMT == BS_E5M2 ? (uint32_t)__builtin_amdgcn_cvt_pk_bf8_f32(y[0], y[1], 0, false)
+                           : (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[0], y[1], 0, false);
+        w = FMT == BS_E5M2 ? (uint32_t)__builtin_amdgcn_cvt_pk_bf8_f32(y[2], y[3], (int)w, true)
+                           : (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[2], y[3], (int)w, true);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) val[t][r] = f8_val<FMT>(w, r);
+      if (z.qok && key < a.S) {
+        const int64_t e = (int64_t)pelem(a, z, key);
+        *(uint32_t*)(a.codes + e) = w;
+        if (a.P_out) *(float4*)(a.P_out + e) = make_float4(p[t][0], p[t][1], p[t][2], p[t][3]);
+      }
+    }
+    // O += val(C) V^T (k-step s takes keys 32 s + 16 (v >> 2) + 4 g + (v & 3))
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      uint32_t pk[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int v = 2 * i;
+        pk[i] = pk_bf16(val[2 * s2 + (v >> 2)][v & 3], val[2 * s2 + ((v + 1) >> 2)][(v + 1) & 3]);
+      }
+      const bf16x8 tv = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+#pragma unroll
+      for (int n = 0; n < 4; ++n) acc[n] = mfma(tv, frag_t(sm[st][1], 16 * n + z.c16, s2, z.g), acc[n]);
+    }
+    if (kb + 1 < nkb) put(st ^ 1);
+    __syncthreads();
+  }
+  // zero codes (and probabilities) above the causal diagonal
+  if (z.qok) {
+    for (int kb = nkb; kb < nkb_all; ++kb)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int key = kb * AT + 16 * t + 4 * z.g;
+        if (key < a.S) {
+          const int64_t e = (int64_t)pelem(a, z, key);
+          *(uint32_t*)(a.codes + e) = 0u;
+          if (a.P_out) *(float4*)(a.P_out + e) = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+  }
+  nsat = wave_sum_u32(nsat);
+  if ((threadIdx.x & 63) == 0 && nsat) atomicAdd(&a.diag->n_saturated, nsat);
+  // O rows 16 w + 4 g + r, columns 16 n + c16
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int qr = z.q0 + 16 * z.w + 4 * z.g + r;
+    if (qr >= a.S) continue;
+#pragma unroll
+    for (int n = 0; n < 4; ++n) a.O[z.hb + (int64_t)qr * AT + 16 * n + z.c16] = s * acc[n][r];
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// row sums (per query) over keys: D, DR, E, Ee, Ps1 (fp64), and per trial Ga, Ha, Gb (fp32).
+// The key blocks are walked once per chunk of RC trials (their sums in registers); the first
+// walk also forms the trial-independent sums.
+// ------------------------------------------------------------------------------------
+constexpr int RC = 8;
+template <int FMT>
+__global__ __launch_bounds__(256) void pstore_rows_kernel(PstoreArgs a) {
+  __shared__ __attribute__((aligned(16))) u16 sm[2][2][AT * AT];  // K, V
+  if (a.diag->nonfinite) return;
+  const QMajor z = qmajor_setup(a, true);
+  const float s = a.diag->scale;
+  const double rs = 1.0 / (double)s;
+  const F8 f = a.f;
+  const int64_t row = z.rb + z.q, rows = (int64_t)a.BH * a.S;
+  double sD = 0.0, sDR = 0.0, sE = 0.0, sEe = 0.0, sP = 0.0;
+  TileRegs pf[2];
+  auto fetch = [&](int k0) {
+    tile_fetch(pf[0], a.K + z.hb, k0, a.S);
+    tile_fetch(pf[1], a.V + z.hb, k0, a.S);
+  };
+  auto put = [&](int st) {
+    tile_put(sm[st][0], pf[0]);
+    tile_put(sm[st][1], pf[1]);
+  };
+  auto red32 = [](float v) { v += __shfl_xor(v, 16, 64); return v + __shfl_xor(v, 32, 64); };
+  const int nkb = a.causal ? z.qb + 1 : (a.S + AT - 1) / AT;
+  for (int k0t = 0; k0t < a.ntrial; k0t += RC) {
+    float ga[RC], ha[RC], gb[RC];
+#pragma unroll
+    for (int j = 0; j < RC; ++j) ga[j] = ha[j] = gb[j] = 0.0f;
+    fetch(0);
+    put(0);
+    __syncthreads();
+    for (int kb = 0; kb < nkb; ++kb) {
+      const int st = kb & 1, k0 = kb * AT;
+      if (kb + 1 < nkb) fetch(k0 + AT);
+      float p[4][4], dp[4][4];
+      probs(a, z, sm[st][0], k0, p);
+      dprobs(z, sm[st][1], dp);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int key = k0 + 16 * t + 4 * z.g;
+        const bool ok = z.qok && key < a.S;
+        const uint32_t cw = ok ? *(const uint32_t*)(a.codes + pelem(a, z, key)) : 0u;
+        Resid x[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) x[r] = resid(p[t][r], f8_val<FMT>(cw, r), s, rs, f);
+        if (k0t == 0) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            sD += (double)p[t][r] * dp[t][r];
+            sDR += (double)x[r].r * dp[t][r];
+            sE += (double)x[r].e * dp[t][r];
+            sEe += (double)x[r].e;
+            sP += (double)p[t][r];
+          }
+        }
+        const uint64_t grp = pelem(a, z, key) >> 2;
+#pragma unroll
+        for (int j = 0; j < RC; ++j) {
+          const int k = k0t + j;
+          if (k >= a.ntrial) continue;
+          const Philox4 pa = philox_group(a.seed, grp, (uint32_t)(k + 1), a.use_a);
+          const Philox4 pb = philox_group(a.seed, grp, (uint32_t)(k + 1), a.use_b);
+          const uint32_t Ra[4] = {pa.w0, pa.w1, pa.w2, pa.w3}, Rb[4] = {pb.w0, pb.w1, pb.w2, pb.w3};
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float hd = x[r].h * dp[t][r];
+            if (sr_up(x[r].F, Ra[r])) {
+              ga[j] += hd;
+              ha[j] += x[r].h;
+            }
+            if (sr_up(x[r].F, Rb[r])) gb[j] += hd;
+          }
+        }
+      }
+      if (kb + 1 < nkb) put(st ^ 1);
+      __syncthreads();
+    }
+    // the four lane groups of a query column hold its four key quarters
+#pragma unroll
+    for (int j = 0; j < RC; ++j) {
+      ga[j] = red32(ga[j]);
+      ha[j] = red32(ha[j]);
+      gb[j] = red32(gb[j]);
+    }
+    if (z.g == 0 && z.qok) {
+#pragma unroll
+      for (int j = 0; j < RC; ++j) {
+        const int k = k0t + j;
+        if (k >= a.ntrial) continue;
+        a.Ga[k * rows + row] = ga[j];
+        a.Ha[k * rows + row] = ha[j];
+        a.Gb[k * rows + row] = gb[j];
+      }
+    }
+  }
+  auto red64 = [](double v) { v += __shfl_xor(v, 16, 64); return v + __shfl_xor(v, 32, 64); };
+  sD = red64(sD);
+  sDR = red64(sDR);
+  sE = red64(sE);
+  sEe = red64(sEe);
+  sP = red64(sP);
+  if (z.g == 0 && z.qok) {
+    a.D[row] = (float)sD;
+    a.DR[row] = (float)sDR;
+    a.E[row] = (float)sE;
+    a.Ee[row] = (float)sEe;
+    a.Ps1[row] = (float)(sP - 1.0);
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// bias fields and dQ: per element the sums over trials, then the fields of every read; the
+// fields go to memory for the key-major pass and into dQ = c sum_k field K (three bf16 terms)
+// ------------------------------------------------------------------------------------
+template <int FMT>
+__global__ __launch_bounds__(256) void pstore_dq_kernel(PstoreArgs a) {
+  __shared__ __attribute__((aligned(16))) u16 sm[2][3][AT * AT];  // K, V, K^T
+  __shared__ float tv[3][AT][PSTORE_KMAX];                         // Ga, Ha, Gb of the block's queries
+  if (a.diag->nonfinite) return;
+  const QMajor z = qmajor_setup(a, true);
+  const float s = a.diag->scale;
+  const double rs = 1.0 / (double)s;
+  const F8 f = a.f;
+  const int64_t row = z.rb + z.q, rows = (int64_t)a.BH * a.S;
+  // this lane's query: row sums; the block's per-trial sums in LDS
+  const float D = z.qok ? a.D[row] : 0.f, DR = z.qok ? a.DR[row] : 0.f, E = z.qok ? a.E[row] : 0.f;
+  const float Ee = z.qok ? a.Ee[row] : 0.f, Ps = z.qok ? 1.0f + a.Ps1[row] : 0.f;
+  const float Ps1 = z.qok ? a.Ps1[row] : 0.f;
+  for (int i = threadIdx.x; i < AT * a.ntrial; i += blockDim.x) {
+    const int qq = i / a.ntrial, k = i - qq * a.ntrial;
+    const bool ok = z.q0 + qq < a.S;
+    const int64_t rr = z.rb + z.q0 + qq;
+    tv[0][qq][k] = ok ? a.Ga[k * rows + rr] : 0.f;
+    tv[1][qq][k] = ok ? a.Ha[k * rows + rr] : 0.f;
+    tv[2][qq][k] = ok ? a.Gb[k * rows + rr] : 0.f;
+  }
+  __syncthreads();
+  const int ql = 16 * z.w + z.c16;
+  float mGa = 0.f, mHa = 0.f, mGb = 0.f;
+  for (int k = 0; k < a.ntrial; ++k) {
+    mGa += tv[0][ql][k];
+    mHa += tv[1][ql][k];
+    mGb += tv[2][ql][k];
+  }
+  const float iK = 1.0f / (float)a.ntrial;
+  mGa *= iK;
+  mHa *= iK;
+  mGb *= iK;
+  const float dDa = E + mGa, dDb = E + mGb, rho = Ee + mHa;
+  const int nqb = (a.S + AT - 1) / AT;
+
+  floatx4 aq[PF_SOFTMAX][4];
+#pragma unroll
+  for (int i = 0; i < PF_SOFTMAX; ++i)
+#pragma unroll
+    for (int n = 0; n < 4; ++n) aq[i][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  TileRegs pf[3];
+  auto fetch = [&](int k0) {
+    tile_fetch(pf[0], a.K + z.hb, k0, a.S);
+    tile_fetch(pf[1], a.V + z.hb, k0, a.S);
+    tile_fetch_t(pf[2], a.Kt + z.tb, k0, a.Sp);
+  };
+  auto put = [&](int st) {
+    tile_put(sm[st][0], pf[0]);
+    tile_put(sm[st][1], pf[1]);
+    tile_put_t(sm[st][2], pf[2]);
+  };
+  const int nkb = a.causal ? z.qb + 1 : nqb;
+  fetch(0);
+  put(0);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int st = kb & 1, k0 = kb * AT;
+    if (kb + 1 < nkb) fetch(k0 + AT);
+    float p[4][4], dp[4][4];
+    probs(a, z, sm[st][0], k0, p);
+    dprobs(z, sm[st][1], dp);
+    const int64_t tile = fld_tile(a, z.bh, z.qb, kb, nqb);
+    // one k-step (key sub-tiles t = 2 s2, 2 s2 + 1) at a time: fields, their store, their dQ terms
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      float fl[PF_COUNT][2][4];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
+        const int t = 2 * s2 + tt;
+        const int key = k0 + 16 * t + 4 * z.g;
+        const bool ok = z.qok && key < a.S;
+        const uint32_t cw = ok ? *(const uint32_t*)(a.codes + pelem(a, z, key)) : 0u;
+        Resid x[4];
+        float na[4] = {0.f, 0.f, 0.f, 0.f}, nb[4] = {0.f, 0.f, 0.f, 0.f};
+        float uga[4] = {0.f, 0.f, 0.f, 0.f}, uha[4] = {0.f, 0.f, 0.f, 0.f};
+        float ugab[4] = {0.f, 0.f, 0.f, 0.f}, ugba[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) x[r] = resid(p[t][r], f8_val<FMT>(cw, r), s, rs, f);
+        const uint64_t grp = pelem(a, z, key) >> 2;
+        for (int k = 0; k < a.ntrial; ++k) {
+          const Philox4 pa = philox_group(a.seed, grp, (uint32_t)(k + 1), a.use_a);
+          const Philox4 pb = philox_group(a.seed, grp, (uint32_t)(k + 1), a.use_b);
+          const uint32_t Ra[4] = {pa.w0, pa.w1, pa.w2, pa.w3}, Rb[4] = {pb.w0, pb.w1, pb.w2, pb.w3};
+          const float gak = tv[0][ql][k], hak = tv[1][ql][k], gbk = tv[2][ql][k];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            if (sr_up(x[r].F, Ra[r])) {
+              na[r] += 1.0f;
+              uga[r] += gak;
+              uha[r] += hak;
+              ugab[r] += gbk;
+            }
+            if (sr_up(x[r].F, Rb[r])) {
+              nb[r] += 1.0f;
+              ugba[r] += gak;
+            }
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float pp = p[t][r], d = dp[t][r], rr = x[r].r, e = x[r].e, h = x[r].h;
+          const float dpm = d - D;
+          const float m1a = e + h * na[r] * iK, m1b = e + h * nb[r] * iK;
+          const float mrDa = e * dDa + h * (E * na[r] + uga[r]) * iK;  // mean r_a dD_a
+          const float mrRa = e * rho + h * (Ee * na[r] + uha[r]) * iK;  // mean r_a rho_a
+          const float mrab = e * dDb + h * (E * na[r] + ugab[r]) * iK;  // mean r_a dD_b
+          const float mrba = e * dDa + h * (E * nb[r] + ugba[r]) * iK;  // mean r_b dD_a
+          fl[PF_REF][tt][r] = pp * dpm;
+          fl[PF_R][tt][r] = rr * (dpm - DR) - pp * DR;
+          fl[PF_N][tt][r] = m1a * dpm - pp * dDa - mrDa;
+          fl[PF_K][tt][r] = pp * ((Ps1 + rho) * d - dDa) + (Ps * m1a + mrRa) * d - D * m1a - mrDa;
+          fl[PF_J2][tt][r] = 0.5f * ((m1a + m1b) * dpm - pp * (dDa + dDb) - (mrab + mrba));
+          fl[PF_Q2][tt][r] = 0.5f * ((m1a + rr) * dpm - pp * (dDa + DR) - (m1a * DR + rr * dDa));
+          fl[PF_VU][tt][r] = -rr;
+          fl[PF_VN][tt][r] = m1a - rr;
+        }
+        // store: tile (qb, kb) as [key][query]
+#pragma unroll
+        for (int i = 0; i < PF_COUNT; ++i) {
+          float* T = a.fld[i] + tile;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) T[(16 * t + 4 * z.g + r) * AT + 16 * z.w + z.c16] = fl[i][tt][r];
+        }
+      }
+      // dQ terms of the softmax fields (k index: keys 32 s2 + 16 (v >> 2) + 4 g + (v & 3))
+      bf16x8 fk[4];
+#pragma unroll
+      for (int n = 0; n < 4; ++n) fk[n] = frag_t(sm[st][2], 16 * n + z.c16, s2, z.g);
+#pragma unroll
+      for (int i = 0; i < PF_SOFTMAX; ++i) {
+        float vd[8];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) vd[v] = fl[i][v >> 2][v & 3];
+        bf16x8 td[3];
+        pack3(vd, td);
+#pragma unroll
+        for (int n = 0; n < 4; ++n)
+#pragma unroll
+          for (int j = 0; j < 3; ++j) aq[i][n] = mfma(td[j], fk[n], aq[i][n]);
+      }
+    }
+    if (kb + 1 < nkb) put(st ^ 1);
+    __syncthreads();
+  }
+  const float c = a.scale;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int qr = z.q0 + 16 * z.w + 4 * z.g + r;
+    if (qr >= a.S) continue;
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      const int64_t e = z.hb + (int64_t)qr * AT + 16 * n + z.c16;
+      a.dQ_ref[e] = c * aq[PF_REF][n][r];
+#pragma unroll
+      for (int i = 1; i < PF_SOFTMAX; ++i) a.dQ_b[i][e] = c * aq[i][n][r];
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// key-major: dK = c sum_q field Q (three bf16 terms per field), dV = sum_q val(C) dO s (one
+// term) and the dV biases sum_q (p - p_q) dO, sum_q (mean a - p_q) dO (three terms)
+// ------------------------------------------------------------------------------------
+template <int FMT>
+__global__ __launch_bounds__(256) void pstore_dkv_kernel(PstoreArgs a) {
+  __shared__ __attribute__((aligned(16))) u16 sm[2][2][AT * AT];  // Q^T, dO^T
+  if (a.diag->nonfinite) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, c16 = lane & 15;
+  const int bh = blockIdx.x, kb = blockIdx.y;
+  const int k0 = kb * AT;
+  const int key = k0 + 16 * w + c16;
+  const int64_t hb = (int64_t)bh * a.S * AT, tb = (int64_t)bh * AT * a.Sp;
+  const int nqb = (a.S + AT - 1) / AT;
+  const float s = a.diag->scale;
+  floatx4 ak[PF_SOFTMAX][4], av[3][4];
+#pragma unroll
+  for (int n = 0; n < 4; ++n) {
+#pragma unroll
+    for (int i = 0; i < PF_SOFTMAX; ++i) ak[i][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 3; ++i) av[i][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+  TileRegs pf[2];
+  auto fetch = [&](int q0) {
+    tile_fetch_t(pf[0], a.Qt + tb, q0, a.Sp);
+    tile_fetch_t(pf[1], a.dOt + tb, q0, a.Sp);
+  };
+  auto put = [&](int st) {
+    tile_put_t(sm[st][0], pf[0]);
+    tile_put_t(sm[st][1], pf[1]);
+  };
+  const int qb0 = a.causal ? kb : 0;
+  fetch(qb0 * AT);
+  put(0);
+  __syncthreads();
+  for (int qb = qb0; qb < nqb; ++qb) {
+    const int st = (qb - qb0) & 1, q0 = qb * AT;
+    if (qb + 1 < nqb) fetch(q0 + AT);
+    const int64_t tile = fld_tile(a, bh, qb, kb, nqb);
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      // queries 32 s2 + 16 h + 4 g + (0..3) of this lane's key, as the k index of the products
+      bf16x8 fq[4], fo[4];
+#pragma unroll
+      for (int n = 0; n < 4; ++n) {
+        fq[n] = frag_t(sm[st][0], 16 * n + c16, s2, g);
+        fo[n] = frag_t(sm[st][1], 16 * n + c16, s2, g);
+      }
+      float vals[PF_COUNT][8];
+#pragma unroll
+      for (int i = 0; i < PF_COUNT; ++i) {
+        const float* T = a.fld[i] + tile + (int64_t)(16 * w + c16) * AT;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const float4 v = *(const float4*)(T + 32 * s2 + 16 * hh + 4 * g);
+          vals[i][4 * hh + 0] = v.x;
+          vals[i][4 * hh + 1] = v.y;
+          vals[i][4 * hh + 2] = v.z;
+          vals[i][4 * hh + 3] = v.w;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < PF_SOFTMAX; ++i) {
+        bf16x8 td[3];
+        pack3(vals[i], td);
+#pragma unroll
+        for (int n = 0; n < 4; ++n)
+#pragma unroll
+          for (int j = 0; j < 3; ++j) ak[i][n] = mfma(td[j], fq[n], ak[i][n]);
+      }
+      // dV: val(C) of (query, key) for the same eight queries (exact in bf16)
+      float cv[8];
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        const int qq = q0 + 32 * s2 + 16 * (v >> 2) + 4 * g + (v & 3);
+        const bool ok = qq < a.S && key < a.S;
+        const uint32_t b = ok ? a.codes[((int64_t)bh * a.S + qq) * a.S + key] : 0u;
+        cv[v] = f8_val<FMT>(b, 0);
+      }
+      uint32_t pk[4];
+#pragma unroll
+      for (int i2 = 0; i2 < 4; ++i2) pk[i2] = pk_bf16(cv[2 * i2], cv[2 * i2 + 1]);
+      const bf16x8 tv = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+      bf16x8 tu[3], tn[3];
+      pack3(vals[PF_VU], tu);
+      pack3(vals[PF_VN], tn);
+#pragma unroll
+      for (int n = 0; n < 4; ++n) {
+        av[0][n] = mfma(tv, fo[n], av[0][n]);
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+          av[1][n] = mfma(tu[j], fo[n], av[1][n]);
+          av[2][n] = mfma(tn[j], fo[n], av[2][n]);
+        }
+      }
+    }
+    if (qb + 1 < nqb) put(st ^ 1);
+    __syncthreads();
+  }
+  const float c = a.scale;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int kr = k0 + 16 * w + 4 * g + r;
+    if (kr >= a.S) continue;
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      const int64_t e = hb + (int64_t)kr * AT + 16 * n + c16;
+      a.dK_ref[e] = c * ak[PF_REF][n][r];
+#pragma unroll
+      for (int i = 1; i < PF_SOFTMAX; ++i) a.dK_b[i][e] = c * ak[i][n][r];
+      a.dV_ref[e] = s * av[0][n][r];
+      a.dV_b[0][e] = av[1][n][r];
+      a.dV_b[1][e] = av[2][n][r];
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------
+bs_status launch_pstore_scale(const PstoreArgs& a, hipStream_t st) {
+  pstore_scale_kernel<<<1, 1024, 0, st>>>(a.l, (int64_t)a.BH * a.S, a.f.fmax, a.diag, a.P_scale);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+static dim3 pstore_grid(const PstoreArgs& a) { return dim3((unsigned)a.BH, (unsigned)((a.S + AT - 1) / AT)); }
+
+bs_status launch_pstore_fwd(const PstoreArgs& a, hipStream_t st) {
+  ProfScope prof("pstore_fwd", st);
+  if (a.fmt == BS_E5M2)
+    pstore_fwd_kernel<BS_E5M2><<<pstore_grid(a), 256, 0, st>>>(a);
+  else
+    pstore_fwd_kernel<BS_E4M3><<<pstore_grid(a), 256, 0, st>>>(a);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+#define BS_PSTORE_KM(KERNEL, FMTV) KERNEL<FMTV><<<pstore_grid(a), 256, 0, st>>>(a)
+
+bs_status launch_pstore_rows(const PstoreArgs& a, hipStream_t st) {
+  if (a.ntrial < 1 || a.ntrial > PSTORE_KMAX) return BS_EINVAL;
+  ProfScope prof("pstore_rows", st);
+  if (a.fmt == BS_E5M2)
+    BS_PSTORE_KM(pstore_rows_kernel, BS_E5M2);
+  else
+    BS_PSTORE_KM(pstore_rows_kernel, BS_E4M3);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+bs_status launch_pstore_dq(const PstoreArgs& a, hipStream_t st) {
+  if (a.ntrial < 1 || a.ntrial > PSTORE_KMAX) return BS_EINVAL;
+  ProfScope prof("pstore_dq", st);
+  if (a.fmt == BS_E5M2)
+    BS_PSTORE_KM(pstore_dq_kernel, BS_E5M2);
+  else
+    BS_PSTORE_KM(pstore_dq_kernel, BS_E4M3);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+#undef BS_PSTORE_KM
+
+bs_status launch_pstore_dkv(const PstoreArgs& a, hipStream_t st) {
+  ProfScope prof("pstore_dkv", st);
+  if (a.fmt == BS_E5M2)
+    pstore_dkv_kernel<BS_E5M2><<<pstore_grid(a), 256, 0, st>>>(a);
+  else
+    pstore_dkv_kernel<BS_E4M3><<<pstore_grid(a), 256, 0, st>>>(a);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+}  // namespace bsp

@@ -1,0 +1,123 @@
+"""GPU parity: bs_attn_pstore_policy against the oracle (oracle/pstore.py).
+
+The library's realized fp32 probabilities (P_out) are handed to the oracle, which stores and
+differentiates them in fp64: the FP8 codes and the scale must agree bit for bit, the forward
+output, the reference gradients and every policy's mean and bias within 1e-5 (normwise
+relative). P itself is checked against the oracle's fp64 softmax of the same bf16 inputs.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import fp8, pstore, qround as oq
+from paper_2609_39813_amd import synth
+from tests.parity import assert_rel, assert_zero_where_oracle_zero, to_np
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-5
+ALL = ("U/R", "R/R", "U/U", "N/N", "R/U", "K/R", "J2/R", "Q2/R")
+FMTS = {"e4m3": fp8.E4M3, "e5m2": fp8.E5M2}
+MODES = {"rne": oq.RNE, "sr": oq.SR}
+
+
+def inputs(B, H, S, seed):
+    return [t.to(torch.bfloat16) for t in synth.attention_inputs(B, H, S, 64, torch.float32, config=300 + seed)]
+
+
+def run(lib, Q, K, V, dO, *, causal=True, fmt="e4m3", fwd_mode="rne", pols=ALL, Kt=8, seed=3, store_id=2, scale=None):
+    print(f"[pstore] shape={tuple(Q.shape)} causal={causal} fmt={fmt} fwd={fwd_mode} pols={pols} K={Kt} seed={seed}",
+          flush=True)
+    out = lib.attn_pstore_policy(Q.cuda(), K.cuda(), V.cuda(), dO.cuda(), causal=causal, scale=scale, fmt=fmt,
+                                 fwd_mode=fwd_mode, policies=pols, K=Kt, seed=seed, store_id=store_id, want_p=True)
+    torch.cuda.synchronize()
+    return out
+
+
+def oracle_of(out, Q, K, V, dO, *, causal, fmt, fwd_mode, pols, Kt, seed, store_id=2, scale=None, heads=None):
+    c = 1.0 / 8.0 if scale is None else scale
+    return pstore.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.float().numpy(), causal=causal,
+                        c=c, fmt=FMTS[fmt], fwd_mode=MODES[fwd_mode], policies=tuple(dict.fromkeys(pols)), K=Kt,
+                        seed=seed, store_id=store_id, P=out["P"].cpu().numpy(), heads=heads)
+
+
+def compare(out, ref, pols, Q, K, causal, scale=None):
+    B, H, S, dh = out["dQ_ref"].shape
+    idx = [b * H + h for b, h in ref["heads"]]
+    sel = lambda t: to_np(t).reshape(B * H, *t.shape[2:])[idx]
+    # the store and the forward
+    assert np.array_equal(out["P_codes"].cpu().numpy(), ref["codes"])
+    assert float(out["P_scale"].cpu()[0]) == float(ref["scale"])
+    c = 1.0 / 8.0 if scale is None else scale
+    P64 = pstore.probabilities(Q.float().numpy(), K.float().numpy(), causal, c)
+    assert_rel(to_np(out["P"]), P64, TOL, "P against the fp64 softmax")
+    assert_rel(sel(out["O"]), ref["O"].reshape(B * H, S, dh)[idx], TOL, "O")
+    for name in ("dQ", "dK", "dV"):
+        assert_rel(sel(out[name + "_ref"]), ref[name + "_ref"], TOL, name + "_ref")
+    shp = out["dQ_ref"].shape
+    for i, p in enumerate(pols):
+        for name in ("dQ", "dK", "dV"):
+            m = sel(out[name]["mean"][i].reshape(shp))
+            b = sel(out[name]["bias"][i].reshape(shp))
+            om, ob, _ = ref[p][name]
+            assert_rel(m, om, TOL, f"{p} {name} mean")
+            if not assert_zero_where_oracle_zero(b, ob, f"{p} {name} bias"):
+                assert_rel(b, ob, TOL, f"{p} {name} bias")
+
+
+@pytest.mark.parametrize("S", [136, 64, 4])
+def test_causal_ragged_all_policies(lib, S):
+    Q, K, V, dO = inputs(1, 2, S, seed=S)
+    out = run(lib, Q, K, V, dO, Kt=8, seed=5)
+    ref = oracle_of(out, Q, K, V, dO, causal=True, fmt="e4m3", fwd_mode="rne", pols=ALL, Kt=8, seed=5)
+    compare(out, ref, ALL, Q, K, True)
+    d = lib.diag_dict(out["diag"])
+    assert d["nonfinite"] == 0 and d["n_saturated"] == 0
+    assert d["amax"] == float(out["P"].max().cpu())
+
+
+def test_noncausal_e5m2_sr_forward(lib):
+    Q, K, V, dO = inputs(2, 1, 200, seed=7)
+    out = run(lib, Q, K, V, dO, causal=False, fmt="e5m2", fwd_mode="sr", Kt=5, seed=11)
+    # without the causal mask no row has a single key: amax = max_rows 1/l is a real test
+    assert lib.diag_dict(out["diag"])["amax"] == float(out["P"].max().cpu())
+    ref = oracle_of(out, Q, K, V, dO, causal=False, fmt="e5m2", fwd_mode="sr", pols=ALL, Kt=5, seed=11)
+    compare(out, ref, ALL, Q, K, False)
+
+
+@pytest.mark.parametrize("Kt", [1, 32])
+def test_trial_count_limits_and_policy_order(lib, Kt):
+    Q, K, V, dO = inputs(1, 1, 132, seed=Kt)
+    pols = ("N/N", "J2/R", "U/R", "N/N", "Q2/U", "K/N")
+    out = run(lib, Q, K, V, dO, fwd_mode="sr", pols=pols, Kt=Kt, seed=2, scale=0.3)
+    ref = oracle_of(out, Q, K, V, dO, causal=True, fmt="e4m3", fwd_mode="sr", pols=pols, Kt=Kt, seed=2, scale=0.3)
+    compare(out, ref, pols, Q, K, True, scale=0.3)
+    # a policy repeated in the list gives the same bits
+    for name in ("dQ", "dK", "dV"):
+        assert torch.equal(out[name]["mean"][0], out[name]["mean"][3])
+
+
+def test_exact_zeros_of_the_table(lib):
+    """U/R and R/R read the reference at dV, U/U and U/R at the softmax: their biases are 0."""
+    Q, K, V, dO = inputs(1, 1, 100, seed=9)
+    pols = ("U/R", "R/R", "U/U")
+    out = run(lib, Q, K, V, dO, pols=pols, Kt=4)
+    for i in (0, 1):
+        assert torch.count_nonzero(out["dV"]["bias"][i]) == 0
+    for i in (0, 2):
+        assert torch.count_nonzero(out["dQ"]["bias"][i]) == 0
+        assert torch.count_nonzero(out["dK"]["bias"][i]) == 0
+
+
+def test_rejected_arguments(lib):
+    Q, K, V, dO = (t.cuda() for t in inputs(1, 1, 64, seed=1))
+    ws = torch.empty(1 << 24, dtype=torch.uint8, device="cuda")
+    with pytest.raises(lib.BspError) as e:
+        lib.attn_pstore_policy(Q, K, V, dO, K=33, ws=ws)
+    assert e.value.code == 1
+    with pytest.raises(lib.BspError) as e:                        # a short workspace
+        lib.attn_pstore_policy(Q, K, V, dO, K=4, ws=ws[:4096])
+    assert e.value.code == 5
+    Q6, K6, V6, dO6 = (t.cuda() for t in inputs(1, 1, 6, seed=1))
+    with pytest.raises(lib.BspError) as e:
+        lib.attn_pstore_policy(Q6, K6, V6, dO6, K=4, ws=ws)
+    assert e.value.code == 2
