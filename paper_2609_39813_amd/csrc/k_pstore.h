@@ -14,6 +14,7 @@ enum { PF_REF = 0, PF_R, PF_N, PF_K, PF_J2, PF_Q2, PF_VU, PF_VN, PF_COUNT };
 constexpr int PF_SOFTMAX = 6;   // PF_REF .. PF_Q2 enter dQ and dK
 constexpr int PSTORE_KMAX = 32; // trials per call (their per-row sums live in registers)
 constexpr int PSTORE_T = 64;     // head dimension, and the side of a score tile
+constexpr int PSTORE_RC = 16;    // trials per walk of the row-sum pass (16 bits of up-decisions)
 
 // 64 x 64 tiles per head of a bias field: the tiles (qb, kb) on or below the diagonal when
 // causal (kb <= qb, row-major within the triangle), else all nqb^2
@@ -39,6 +40,10 @@ struct PstoreArgs {
   float* O;                         // [BH][S][64] forward output p_q V
   float *D, *DR, *E, *Ee, *Ps1;     // per row (query) sums, [BH][S] (see launch_pstore_rows)
   float *Ga, *Ha, *Gb;              // per trial and row, [ntrial][BH][S]
+  uint32_t* ubits;                  // up-decisions, per chunk c of 16 trials a plane of one word per
+                                    // element (bit j: a of trial 16c + j; bit 16 + j: b), tiles as
+                                    // the fields, each tile's words thread-major (16 per thread)
+  int draw_a, draw_b;               // a policy reads new rounding a / b (else their draws are skipped)
   float* fld[PF_COUNT];             // [BH][pstore_tiles][64 k][64 q] fp32, tile by (query block, key block)
   float *dQ_ref, *dK_ref, *dV_ref;  // [BH][S][64]
   float* dQ_b[PF_SOFTMAX];          // per-field dQ and dK (entry PF_REF unused) and dV biases,

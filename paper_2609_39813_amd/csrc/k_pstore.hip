@@ -14,7 +14,9 @@
 // step, u_k its up-decision) and a row's D = p . dp, each policy's mean over the K trials of
 // Jhat dp - J(p) dp is a combination of per-row sums (Ga_k = sum u_k h dp, Ha_k = sum u_k h,
 // ...) and per-element sums over trials (n = sum u_k, sum u_k Ga_k, ...): the trials never
-// materialize, and the dQ / dK contractions run once per field.
+// materialize, and the dQ / dK contractions run once per field. The row-sum pass draws each
+// up-decision once (one Philox call per 4 elements, trial and use) and leaves them as bits for
+// the dQ pass.
 #include "k_attn_tiles.h"
 #include "k_pstore.h"
 
@@ -292,19 +294,23 @@ __global__ __launch_bounds__(256, 2) void pstore_fwd_kernel(PstoreArgs a) {
 }
 
 // ------------------------------------------------------------------------------------
-// row sums (per query) over keys: D, DR, E, Ee, Ps1 (fp64), and per trial Ga, Ha, Gb (fp32).
-// The key blocks are walked once per chunk of RC trials (their sums in registers); the first
-// walk also forms the trial-independent sums.
+// row sums (per query) over keys: D, DR, E, Ee, Ps1 (fp64), and per trial Ga, Ha, Gb (fp32),
+// and the up-decision words. The key blocks are walked once per chunk of RC trials; the first
+// walk also forms the trial-independent sums. Within a tile the trial loop is outermost: the
+// 4 groups x 2 uses of Philox calls of one trial are independent, and each thread's per-trial
+// partial sums live in its own LDS slots (added in key-block order, so the result is fixed).
 // ------------------------------------------------------------------------------------
-constexpr int RC = 8;
-template <int FMT>
-__global__ __launch_bounds__(256) void pstore_rows_kernel(PstoreArgs a) {
+constexpr int RC = PSTORE_RC;
+template <int FMT, int DRAW>  // DRAW: 0 no new rounding is read, 1 only a, 2 a and b
+__global__ __launch_bounds__(256, 2) void pstore_rows_kernel(PstoreArgs a) {
   __shared__ __attribute__((aligned(16))) u16 sm[2][2][AT * AT];  // K, V
+  __shared__ float acc[3][RC][256];                                // per thread: Ga, Ha, Gb per trial
   if (a.diag->nonfinite) return;
   const QMajor z = qmajor_setup(a, true);
   const float s = a.diag->scale;
   const double rs = 1.0 / (double)s;
   const F8 f = a.f;
+  const int tid = threadIdx.x;
   const int64_t row = z.rb + z.q, rows = (int64_t)a.BH * a.S;
   double sD = 0.0, sDR = 0.0, sE = 0.0, sEe = 0.0, sP = 0.0;
   TileRegs pf[2];
@@ -317,11 +323,16 @@ __global__ __launch_bounds__(256) void pstore_rows_kernel(PstoreArgs a) {
     tile_put(sm[st][1], pf[1]);
   };
   auto red32 = [](float v) { v += __shfl_xor(v, 16, 64); return v + __shfl_xor(v, 32, 64); };
-  const int nkb = a.causal ? z.qb + 1 : (a.S + AT - 1) / AT;
+  const int nqb = (a.S + AT - 1) / AT;
+  const int nkb = a.causal ? z.qb + 1 : nqb;
+  const int64_t plane = (int64_t)a.BH * pstore_tiles(nqb, a.causal) * AT * AT;
   for (int k0t = 0; k0t < a.ntrial; k0t += RC) {
-    float ga[RC], ha[RC], gb[RC];
+    const int jn = min(RC, a.ntrial - k0t);
+    uint32_t* bits = a.ubits + (k0t / RC) * plane;
 #pragma unroll
-    for (int j = 0; j < RC; ++j) ga[j] = ha[j] = gb[j] = 0.0f;
+    for (int i = 0; i < 3; ++i)
+#pragma unroll
+      for (int j = 0; j < RC; ++j) acc[i][j][tid] = 0.0f;
     fetch(0);
     put(0);
     __syncthreads();
@@ -331,63 +342,87 @@ __global__ __launch_bounds__(256) void pstore_rows_kernel(PstoreArgs a) {
       float p[4][4], dp[4][4];
       probs(a, z, sm[st][0], k0, p);
       dprobs(z, sm[st][1], dp);
+      float hh[4][4], hd[4][4];
+      uint32_t FF[4][4], ub[4][4];
+      uint64_t grp[4];
+      bool need[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int key = k0 + 16 * t + 4 * z.g;
         const bool ok = z.qok && key < a.S;
         const uint32_t cw = ok ? *(const uint32_t*)(a.codes + pelem(a, z, key)) : 0u;
-        Resid x[4];
+        uint32_t any = 0u;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) x[r] = resid(p[t][r], f8_val<FMT>(cw, r), s, rs, f);
-        if (k0t == 0) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
+        for (int r = 0; r < 4; ++r) {
+          const Resid x = resid(p[t][r], f8_val<FMT>(cw, r), s, rs, f);
+          if (k0t == 0) {
             sD += (double)p[t][r] * dp[t][r];
-            sDR += (double)x[r].r * dp[t][r];
-            sE += (double)x[r].e * dp[t][r];
-            sEe += (double)x[r].e;
+            sDR += (double)x.r * dp[t][r];
+            sE += (double)x.e * dp[t][r];
+            sEe += (double)x.e;
             sP += (double)p[t][r];
           }
+          hh[t][r] = x.h;
+          hd[t][r] = x.h * dp[t][r];
+          FF[t][r] = x.F;
+          ub[t][r] = 0u;
+          any |= x.F;
         }
-        const uint64_t grp = pelem(a, z, key) >> 2;
+        grp[t] = pelem(a, z, key) >> 2;
+        // a group with no fraction (on the grid, masked, past S) never rounds up; the test is
+        // taken for the whole wave
+        need[t] = __ballot(any != 0u) != 0ull;
+      }
+      if (DRAW >= 1) {
+        for (int j = 0; j < jn; ++j) {
+          const uint32_t trial = (uint32_t)(k0t + j + 1);
+          float gaj = 0.0f, haj = 0.0f, gbj = 0.0f;
 #pragma unroll
-        for (int j = 0; j < RC; ++j) {
-          const int k = k0t + j;
-          if (k >= a.ntrial) continue;
-          const Philox4 pa = philox_group(a.seed, grp, (uint32_t)(k + 1), a.use_a);
-          const Philox4 pb = philox_group(a.seed, grp, (uint32_t)(k + 1), a.use_b);
-          const uint32_t Ra[4] = {pa.w0, pa.w1, pa.w2, pa.w3}, Rb[4] = {pb.w0, pb.w1, pb.w2, pb.w3};
+          for (int t = 0; t < 4; ++t) {
+            if (!need[t]) continue;
+            const Philox4 pa = philox_group(a.seed, grp[t], trial, a.use_a);
+            const uint32_t Ra[4] = {pa.w0, pa.w1, pa.w2, pa.w3};
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float hd = x[r].h * dp[t][r];
-            if (sr_up(x[r].F, Ra[r])) {
-              ga[j] += hd;
-              ha[j] += x[r].h;
+            for (int r = 0; r < 4; ++r) {
+              const uint32_t u = sr_up(FF[t][r], Ra[r]);
+              ub[t][r] |= u << j;
+              gaj += u ? hd[t][r] : 0.0f;
+              haj += u ? hh[t][r] : 0.0f;
             }
-            if (sr_up(x[r].F, Rb[r])) gb[j] += hd;
+            if (DRAW == 2) {
+              const Philox4 pb = philox_group(a.seed, grp[t], trial, a.use_b);
+              const uint32_t Rb[4] = {pb.w0, pb.w1, pb.w2, pb.w3};
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const uint32_t u = sr_up(FF[t][r], Rb[r]);
+                ub[t][r] |= u << (j + 16);
+                gbj += u ? hd[t][r] : 0.0f;
+              }
+            }
           }
+          acc[0][j][tid] += gaj;
+          acc[1][j][tid] += haj;
+          if (DRAW == 2) acc[2][j][tid] += gbj;
         }
       }
+      // the thread's 16 decision words of this tile are contiguous (the dQ pass reads them alike)
+      uint4* T = (uint4*)(bits + fld_tile(a, z.bh, z.qb, kb, nqb) + (int64_t)tid * 16);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) T[t] = make_uint4(ub[t][0], ub[t][1], ub[t][2], ub[t][3]);
       if (kb + 1 < nkb) put(st ^ 1);
       __syncthreads();
     }
     // the four lane groups of a query column hold its four key quarters
-#pragma unroll
-    for (int j = 0; j < RC; ++j) {
-      ga[j] = red32(ga[j]);
-      ha[j] = red32(ha[j]);
-      gb[j] = red32(gb[j]);
-    }
-    if (z.g == 0 && z.qok) {
-#pragma unroll
-      for (int j = 0; j < RC; ++j) {
+    for (int j = 0; j < jn; ++j) {
+      const float ga = red32(acc[0][j][tid]), ha = red32(acc[1][j][tid]), gb = red32(acc[2][j][tid]);
+      if (z.g == 0 && z.qok) {
         const int k = k0t + j;
-        if (k >= a.ntrial) continue;
-        a.Ga[k * rows + row] = ga[j];
-        a.Ha[k * rows + row] = ha[j];
-        a.Gb[k * rows + row] = gb[j];
+        a.Ga[k * rows + row] = ga;
+        a.Ha[k * rows + row] = ha;
+        a.Gb[k * rows + row] = gb;
       }
     }
+    __syncthreads();
   }
   auto red64 = [](double v) { v += __shfl_xor(v, 16, 64); return v + __shfl_xor(v, 32, 64); };
   sD = red64(sD);
@@ -411,7 +446,7 @@ __global__ __launch_bounds__(256) void pstore_rows_kernel(PstoreArgs a) {
 template <int FMT>
 __global__ __launch_bounds__(256) void pstore_dq_kernel(PstoreArgs a) {
   __shared__ __attribute__((aligned(16))) u16 sm[2][3][AT * AT];  // K, V, K^T
-  __shared__ float tv[3][AT][PSTORE_KMAX];                         // Ga, Ha, Gb of the block's queries
+  __shared__ float tv[3][AT][PSTORE_KMAX + 1];                     // Ga, Ha, Gb of the block's queries
   if (a.diag->nonfinite) return;
   const QMajor z = qmajor_setup(a, true);
   const float s = a.diag->scale;
@@ -444,6 +479,8 @@ __global__ __launch_bounds__(256) void pstore_dq_kernel(PstoreArgs a) {
   mGb *= iK;
   const float dDa = E + mGa, dDb = E + mGb, rho = Ee + mHa;
   const int nqb = (a.S + AT - 1) / AT;
+  const int nchunk = (a.ntrial + PSTORE_RC - 1) / PSTORE_RC;
+  const int64_t plane = (int64_t)a.BH * pstore_tiles(nqb, a.causal) * AT * AT;
 
   floatx4 aq[PF_SOFTMAX][4];
 #pragma unroll
@@ -462,6 +499,22 @@ __global__ __launch_bounds__(256) void pstore_dq_kernel(PstoreArgs a) {
     tile_put_t(sm[st][2], pf[2]);
   };
   const int nkb = a.causal ? z.qb + 1 : nqb;
+  // one k-step's (key sub-tiles t = 2 s2, 2 s2 + 1) codes and decision words [chunk][tt], loaded
+  // one k-step ahead of their use
+  auto load_step = [&](int kb_, int s2_, uint32_t (&cw)[2], uint4 (&bw)[2][2]) {
+    const int64_t base = fld_tile(a, z.bh, z.qb, kb_, nqb) + (int64_t)threadIdx.x * 16 + 8 * s2_;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      const int key = kb_ * AT + 16 * (2 * s2_ + tt) + 4 * z.g;
+      cw[tt] = (z.qok && key < a.S) ? *(const uint32_t*)(a.codes + pelem(a, z, key)) : 0u;
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        bw[c][tt] = c < nchunk ? *(const uint4*)(a.ubits + c * plane + base + 4 * tt) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  uint32_t cw_cur[2];
+  uint4 bw_cur[2][2];
+  load_step(0, 0, cw_cur, bw_cur);
   fetch(0);
   put(0);
   __syncthreads();
@@ -472,51 +525,63 @@ __global__ __launch_bounds__(256) void pstore_dq_kernel(PstoreArgs a) {
     probs(a, z, sm[st][0], k0, p);
     dprobs(z, sm[st][1], dp);
     const int64_t tile = fld_tile(a, z.bh, z.qb, kb, nqb);
-    // one k-step (key sub-tiles t = 2 s2, 2 s2 + 1) at a time: fields, their store, their dQ terms
+    // one k-step at a time: fields, their store, their dQ terms
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
+      uint32_t cw_nxt[2] = {0u, 0u};
+      uint4 bw_nxt[2][2] = {};
+      if (s2 == 0)
+        load_step(kb, 1, cw_nxt, bw_nxt);
+      else if (kb + 1 < nkb)
+        load_step(kb + 1, 0, cw_nxt, bw_nxt);
       float fl[PF_COUNT][2][4];
+      Resid x[2][4];
+      uint32_t am[2][4], bm[2][4];  // up-decisions of a and b over the trials
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt) {
         const int t = 2 * s2 + tt;
-        const int key = k0 + 16 * t + 4 * z.g;
-        const bool ok = z.qok && key < a.S;
-        const uint32_t cw = ok ? *(const uint32_t*)(a.codes + pelem(a, z, key)) : 0u;
-        Resid x[4];
-        float na[4] = {0.f, 0.f, 0.f, 0.f}, nb[4] = {0.f, 0.f, 0.f, 0.f};
-        float uga[4] = {0.f, 0.f, 0.f, 0.f}, uha[4] = {0.f, 0.f, 0.f, 0.f};
-        float ugab[4] = {0.f, 0.f, 0.f, 0.f}, ugba[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int r = 0; r < 4; ++r) x[r] = resid(p[t][r], f8_val<FMT>(cw, r), s, rs, f);
-        const uint64_t grp = pelem(a, z, key) >> 2;
-        for (int k = 0; k < a.ntrial; ++k) {
-          const Philox4 pa = philox_group(a.seed, grp, (uint32_t)(k + 1), a.use_a);
-          const Philox4 pb = philox_group(a.seed, grp, (uint32_t)(k + 1), a.use_b);
-          const uint32_t Ra[4] = {pa.w0, pa.w1, pa.w2, pa.w3}, Rb[4] = {pb.w0, pb.w1, pb.w2, pb.w3};
-          const float gak = tv[0][ql][k], hak = tv[1][ql][k], gbk = tv[2][ql][k];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            if (sr_up(x[r].F, Ra[r])) {
-              na[r] += 1.0f;
-              uga[r] += gak;
-              uha[r] += hak;
-              ugab[r] += gbk;
-            }
-            if (sr_up(x[r].F, Rb[r])) {
-              nb[r] += 1.0f;
-              ugba[r] += gak;
-            }
-          }
-        }
+        const uint32_t w4[4] = {bw_cur[0][tt].x, bw_cur[0][tt].y, bw_cur[0][tt].z, bw_cur[0][tt].w};
+        const uint32_t v4[4] = {bw_cur[1][tt].x, bw_cur[1][tt].y, bw_cur[1][tt].z, bw_cur[1][tt].w};
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float pp = p[t][r], d = dp[t][r], rr = x[r].r, e = x[r].e, h = x[r].h;
+          x[tt][r] = resid(p[t][r], f8_val<FMT>(cw_cur[tt], r), s, rs, f);
+          am[tt][r] = (w4[r] & 0xFFFFu) | (v4[r] << 16);
+          bm[tt][r] = (w4[r] >> 16) | (v4[r] & 0xFFFF0000u);
+        }
+      }
+      // per element: sum over trials of the up-decision times the row's per-trial sums
+      float uga[2][4], uha[2][4], ugab[2][4], ugba[2][4];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) uga[tt][r] = uha[tt][r] = ugab[tt][r] = ugba[tt][r] = 0.0f;
+#pragma unroll 2
+      for (int k = 0; k < a.ntrial; ++k) {
+        const float gak = tv[0][ql][k], hak = tv[1][ql][k], gbk = tv[2][ql][k];
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float ua = (float)((am[tt][r] >> k) & 1u), vb = (float)((bm[tt][r] >> k) & 1u);
+            uga[tt][r] = fmaf(ua, gak, uga[tt][r]);
+            uha[tt][r] = fmaf(ua, hak, uha[tt][r]);
+            ugab[tt][r] = fmaf(ua, gbk, ugab[tt][r]);
+            ugba[tt][r] = fmaf(vb, gak, ugba[tt][r]);
+          }
+      }
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
+        const int t = 2 * s2 + tt;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float pp = p[t][r], d = dp[t][r], rr = x[tt][r].r, e = x[tt][r].e, h = x[tt][r].h;
+          const float na = (float)__popc(am[tt][r]), nb = (float)__popc(bm[tt][r]);
           const float dpm = d - D;
-          const float m1a = e + h * na[r] * iK, m1b = e + h * nb[r] * iK;
-          const float mrDa = e * dDa + h * (E * na[r] + uga[r]) * iK;  // mean r_a dD_a
-          const float mrRa = e * rho + h * (Ee * na[r] + uha[r]) * iK;  // mean r_a rho_a
-          const float mrab = e * dDb + h * (E * na[r] + ugab[r]) * iK;  // mean r_a dD_b
-          const float mrba = e * dDa + h * (E * nb[r] + ugba[r]) * iK;  // mean r_b dD_a
+          const float m1a = e + h * na * iK, m1b = e + h * nb * iK;
+          const float mrDa = e * dDa + h * (E * na + uga[tt][r]) * iK;   // mean r_a dD_a
+          const float mrRa = e * rho + h * (Ee * na + uha[tt][r]) * iK;  // mean r_a rho_a
+          const float mrab = e * dDb + h * (E * na + ugab[tt][r]) * iK;  // mean r_a dD_b
+          const float mrba = e * dDa + h * (E * nb + ugba[tt][r]) * iK;  // mean r_b dD_a
           fl[PF_REF][tt][r] = pp * dpm;
           fl[PF_R][tt][r] = rr * (dpm - DR) - pp * DR;
           fl[PF_N][tt][r] = m1a * dpm - pp * dDa - mrDa;
@@ -549,6 +614,12 @@ __global__ __launch_bounds__(256) void pstore_dq_kernel(PstoreArgs a) {
         for (int n = 0; n < 4; ++n)
 #pragma unroll
           for (int j = 0; j < 3; ++j) aq[i][n] = mfma(td[j], fk[n], aq[i][n]);
+      }
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
+        cw_cur[tt] = cw_nxt[tt];
+        bw_cur[0][tt] = bw_nxt[0][tt];
+        bw_cur[1][tt] = bw_nxt[1][tt];
       }
     }
     if (kb + 1 < nkb) put(st ^ 1);
@@ -708,13 +779,24 @@ bs_status launch_pstore_fwd(const PstoreArgs& a, hipStream_t st) {
 
 #define BS_PSTORE_KM(KERNEL, FMTV) KERNEL<FMTV><<<pstore_grid(a), 256, 0, st>>>(a)
 
+template <int FMT>
+static void rows_draw(const PstoreArgs& a, hipStream_t st) {
+  const dim3 grid = pstore_grid(a);
+  if (a.draw_b)
+    pstore_rows_kernel<FMT, 2><<<grid, 256, 0, st>>>(a);
+  else if (a.draw_a)
+    pstore_rows_kernel<FMT, 1><<<grid, 256, 0, st>>>(a);
+  else
+    pstore_rows_kernel<FMT, 0><<<grid, 256, 0, st>>>(a);
+}
+
 bs_status launch_pstore_rows(const PstoreArgs& a, hipStream_t st) {
   if (a.ntrial < 1 || a.ntrial > PSTORE_KMAX) return BS_EINVAL;
   ProfScope prof("pstore_rows", st);
   if (a.fmt == BS_E5M2)
-    BS_PSTORE_KM(pstore_rows_kernel, BS_E5M2);
+    rows_draw<BS_E5M2>(a, st);
   else
-    BS_PSTORE_KM(pstore_rows_kernel, BS_E4M3);
+    rows_draw<BS_E4M3>(a, st);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

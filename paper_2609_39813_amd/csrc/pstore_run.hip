@@ -19,6 +19,7 @@ struct PstoreWs {
   u16 *Qt, *Kt, *Vt, *dOt;
   float *m, *l, *D, *DR, *E, *Ee, *Ps1, *Ga, *Ha, *Gb, *O;
   float* fld[PF_COUNT];
+  uint32_t* ubits;
   float *dQ_b[PF_SOFTMAX], *dK_b[PF_SOFTMAX], *dV_b[2];
 };
 
@@ -34,6 +35,7 @@ PstoreWs carve_pstore(Carver& c, int64_t bh, int S, int K, int causal, bool need
   for (float** p : {&w.Ga, &w.Ha, &w.Gb}) *p = c.take<float>((int64_t)K * rows);
   const int64_t nf = bh * pstore_tiles(nqb, causal) * PSTORE_T * PSTORE_T;
   for (int i = 0; i < PF_COUNT; ++i) w.fld[i] = c.take<float>(nf);
+  w.ubits = c.take<uint32_t>((int64_t)((K + PSTORE_RC - 1) / PSTORE_RC) * nf);
   for (int i = 1; i < PF_SOFTMAX; ++i) {
     w.dQ_b[i] = c.take<float>(numel);
     w.dK_b[i] = c.take<float>(numel);
@@ -154,6 +156,12 @@ bs_status pstore_run(const PstoreIO& io, void* ws, size_t ws_bytes, hipStream_t 
   a.Ha = w.Ha;
   a.Gb = w.Gb;
   for (int i = 0; i < PF_COUNT; ++i) a.fld[i] = w.fld[i];
+  a.ubits = w.ubits;
+  for (int i = 0; i < io.n_pol; ++i) {
+    const int sm = io.pol[i].softmax_read;
+    a.draw_a |= (sm == BS_SM_N || sm == BS_SM_K || sm == BS_SM_J2 || sm == BS_SM_Q2 || io.pol[i].v_read == BS_READ_N);
+    a.draw_b |= sm == BS_SM_J2;
+  }
   a.dQ_ref = io.dQ_ref;
   a.dK_ref = io.dK_ref;
   a.dV_ref = io.dV_ref;
