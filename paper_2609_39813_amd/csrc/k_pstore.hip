@@ -369,17 +369,16 @@ __global__ __launch_bounds__(256, 2) void pstore_rows_kernel(PstoreArgs a) {
           any |= x.F;
         }
         grp[t] = pelem(a, z, key) >> 2;
-        // a group with no fraction (on the grid, masked, past S) never rounds up; the test is
-        // taken for the whole wave
+        // a group with no fraction (on the grid, masked, past S) never rounds up; a tile
+        // with no such group in the whole wave skips the draws
         need[t] = __ballot(any != 0u) != 0ull;
       }
-      if (DRAW >= 1) {
+      if (DRAW >= 1 && (need[0] || need[1] || need[2] || need[3])) {
         for (int j = 0; j < jn; ++j) {
           const uint32_t trial = (uint32_t)(k0t + j + 1);
           float gaj = 0.0f, haj = 0.0f, gbj = 0.0f;
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
-            if (!need[t]) continue;
             const Philox4 pa = philox_group(a.seed, grp[t], trial, a.use_a);
             const uint32_t Ra[4] = {pa.w0, pa.w1, pa.w2, pa.w3};
 #pragma unroll
