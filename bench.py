@@ -35,6 +35,12 @@ OPS_PER_ELEMENT_TRIAL = 1408 / 128
 # Ceiling on element-trials per second: 3.57e12.
 ALU_PEAK_ETPS = VALU_LANE_OPS / OPS_PER_ELEMENT_TRIAL
 
+# The P store's row-sum pass as compiled for gfx950: one trial of its draw loop over a thread's 16
+# elements (a and b, 32 element-draws) issues 471 VALU instructions, 272 of them Philox4x32-10
+# (128 v_mad_u64_u32 + 144 v_bitop3_b32), the rest the up-decision, its bit and the per-trial
+# sums: 14.7 per element-draw; ceiling 2.67e12 element-draws/s.
+PSTORE_ROWS_PEAK_DPS = VALU_LANE_OPS / (471 / 32)
+
 # HBM bytes per launch of the counter at the benchmark shape, from two rocprofv3 --pmc passes
 # (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) over this script, each scaled by what the
 # counter reads for the 256 MiB device copy at the end of this script: FETCH_SIZE read
@@ -115,7 +121,8 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
     store's HBM rate on the 16384 x 8192 bf16 gradient (E5M2, SR); the attention backward's MFMA
     rate at B4 H16 S1024 d64 (causal, D read by U / R / N, K = 32); the E5M2 Linear backward at
     16384 x 2048 x 8192 (shared and per-use new roundings, K = 64); one decoder layer at
-    B8 S2048 d1024 H16 F4096 (K = 16, all four stores, every use)."""
+    B8 S2048 d1024 H16 F4096 (K = 16, all four stores, every use); the FP8 store of attention
+    probabilities at B4 H16 S1024 d64 (every policy of App. B's table, K = 32)."""
     out = {}
     cfg4 = synth.CONFIGS[4]
     X4, W4, dy4, _, _ = synth.linear_bwd_inputs(cfg4["M"], cfg4["k"], cfg4["n"], torch.bfloat16, 4)
@@ -167,6 +174,31 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
         "call_ms": round(wall * 1e3, 4),
         "policy_trials_per_s": round(len(cfg3["policies"]) * cfg3["K"] / wall, 1),
         "flops": "8 causal S x S x dh matmuls per head (5 of the reference backward + 3 bias contractions)"}
+    del Q, K, V, dO, ws
+    torch.cuda.empty_cache()
+
+    # the FP8 store of attention probabilities and its two uses (every policy of App. B's table)
+    cp = synth.PSTORE
+    Q, K, V, dO = (t_.to(dev) for t_ in synth.attention_inputs(cp["B"], cp["H"], cp["S"], cp["dh"], cp["dtype"],
+                                                               cp["config"]))
+    ws = bsp.attn_pstore_workspace(cp["B"], cp["H"], cp["S"], cp["dh"], cp["K"], True, dev)
+    names = ("attn_prep", "attn_fwd", "pstore_fwd", "pstore_rows", "pstore_dq", "pstore_dkv")
+    wall, t = _timed(bsp, torch, lambda: bsp.attn_pstore_policy(Q, K, V, dO, causal=True, fmt="e4m3",
+                                                                 fwd_mode=cp["fwd_mode"], policies=cp["policies"],
+                                                                 K=cp["K"], seed=cp["seed"], ws=ws), names, reps)
+    heads, S = cp["B"] * cp["H"], cp["S"]
+    nqb = (S + 63) // 64
+    elems = heads * nqb * (nqb + 1) // 2 * 64 * 64    # elements of the causal tiles the passes walk
+    draws = elems * cp["K"] * 2                         # new roundings a and b per element and trial
+    r_s = t["pstore_rows"] / 1e3
+    out[cp["name"]] = {
+        "call_ms": round(wall * 1e3, 3), "policy_trials_per_s": round(len(cp["policies"]) * cp["K"] / wall, 1),
+        "kernel_ms": {k: round(v, 4) for k, v in t.items()},
+        "rows_Gdraws_per_s": round(draws / r_s / 1e9, 1),
+        "rows_alu_frac": round(draws / r_s / PSTORE_ROWS_PEAK_DPS, 4),
+        "dkv_field_GBps": round(elems * (8 * 4 + 1) / (t["pstore_dkv"] / 1e3) / 1e9, 1),
+        "work": f"{len(cp['policies'])} policies, K = {cp['K']}: {draws} element-draws (Philox words) in the "
+                "row-sum pass; bias fields written by the dQ pass and read by the dK/dV pass (8 x 4 B per element)"}
     del Q, K, V, dO, ws
     torch.cuda.empty_cache()
 

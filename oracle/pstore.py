@@ -139,12 +139,14 @@ def new_rounding(y, fmt, s, seed, trial, use, elems):
 
 def check(Q, Kt, V, dO, *, causal=True, c=None, fmt=fp8.E4M3, fwd_mode=qround.RNE,
           policies=("U/R", "R/R", "U/U", "N/N", "R/U", "K/R", "J2/R", "Q2/R"), K=16, seed=0,
-          store_id=0, P=None, heads=None):
+          store_id=0, P=None, heads=None, rows=None):
     """Reference gradients and each policy's trial statistics for the P store.
 
     Q, Kt, V, dO: [B, H, S, dh]. P: the realized fp32 probabilities [B, H, S, S] to store
     (default: this oracle's fp64 P rounded to fp32). heads: list of (b, h) to compute
-    (default all); the store's scale always comes from the whole P.
+    (default all); the store's scale always comes from the whole P. rows: query indices to
+    compute (default all): dQ is then exact on those rows, while dK and dV sum only over them
+    (exact for a key whose every contributing query is among them).
     Returns the forward (codes, scale, O), the reference dQ, dK, dV per head and, per
     policy, (mean, bias, se) of dQ, dK and dV over the K trials.
     """
@@ -155,13 +157,16 @@ def check(Q, Kt, V, dO, *, causal=True, c=None, fmt=fp8.E4M3, fwd_mode=qround.RN
     codes, s, pq, y = store(P32, fmt, fwd_mode, seed, store_id)
     p = P32.astype(np.float64)
     heads = [(b, h) for b in range(B) for h in range(H)] if heads is None else list(heads)
+    rows = np.arange(S) if rows is None else np.asarray(rows)
     base = store_id * 256
-    elem = np.arange(P32.size, dtype=np.uint64).reshape(P32.shape)
-    out = {"codes": codes, "scale": s, "O": pq @ V, "P": P32, "heads": heads}
+    out = {"codes": codes, "scale": s, "O": pq @ V, "P": P32, "heads": heads, "rows": rows}
     refs = {"dQ": [], "dK": [], "dV": []}
     tr = {code: {"dQ": [], "dK": [], "dV": []} for code in policies}
     for (bb, hh) in heads:
-        pi, pqi, Vi, dOi, Qi, Ki = p[bb, hh], pq[bb, hh], V[bb, hh], dO[bb, hh], Q[bb, hh], Kt[bb, hh]
+        # the element index of P[bb, hh, i, j] is ((bb H + hh) S + i) S + j
+        elem = ((bb * H + hh) * S + rows[:, None].astype(np.uint64)) * S + np.arange(S, dtype=np.uint64)[None, :]
+        yi = y[bb, hh][rows]
+        pi, pqi, Vi, dOi, Qi, Ki = p[bb, hh][rows], pq[bb, hh][rows], V[bb, hh], dO[bb, hh][rows], Q[bb, hh][rows], Kt[bb, hh]
         dp = dOi @ Vi.T
         grads = lambda ds, pv: (c * (ds @ Ki), c * (ds.T @ Qi), pv.T @ dOi)
         for name, g in zip(("dQ", "dK", "dV"), grads(J_apply(pi, dp), pqi)):
@@ -171,8 +176,8 @@ def check(Q, Kt, V, dO, *, causal=True, c=None, fmt=fp8.E4M3, fwd_mode=qround.RN
             nd = draws(code)
             per = {"dQ": [], "dK": [], "dV": []}
             for k in range(1, (K if nd else 1) + 1):
-                a = new_rounding(y[bb, hh], fmt, s, seed, k, base + 1, elem[bb, hh]) if nd >= 1 else None
-                b = new_rounding(y[bb, hh], fmt, s, seed, k, base + 2, elem[bb, hh]) if nd >= 2 else None
+                a = new_rounding(yi, fmt, s, seed, k, base + 1, elem) if nd >= 1 else None
+                b = new_rounding(yi, fmt, s, seed, k, base + 2, elem) if nd >= 2 else None
                 ds = softmax_backward(sm, pi, pqi, a, b, dp)
                 for name, g in zip(("dQ", "dK", "dV"), grads(ds, v_read(vl, pi, pqi, a))):
                     per[name].append(g)

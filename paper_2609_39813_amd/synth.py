@@ -24,6 +24,12 @@ CONFIGS = {
             sharings=("shared", "per_use"), seed=0xB5F4),
 }
 
+# The FP8 store of attention probabilities (App. B.2-B.4) at the attention shape above: every
+# policy of the paper's table, new roundings drawn K times, the forward's store RNE (as TE's).
+PSTORE = dict(name="attention_pstore_b4_h16_s1024_d64", B=4, H=16, S=1024, dh=64, dtype=torch.bfloat16, K=32,
+              fwd_mode="rne", policies=("U/R", "R/R", "U/U", "N/N", "R/U", "K/R", "J2/R", "Q2/R"), seed=0xB5F6,
+              config=6)
+
 
 def _gen(config, i):
     g = torch.Generator()

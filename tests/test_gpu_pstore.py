@@ -121,3 +121,44 @@ def test_rejected_arguments(lib):
     with pytest.raises(lib.BspError) as e:
         lib.attn_pstore_policy(Q6, K6, V6, dO6, K=4, ws=ws)
     assert e.value.code == 2
+
+
+@pytest.mark.slow
+def test_full_size_sampled_rows(lib):
+    """The benchmark's workload and launch (B4 H16 S1024, every policy, K = 32): every code, and
+    dQ on sampled rows, dK and dV on the last 16 keys (whose contributing queries, under the
+    causal mask, are the last 16 rows), for two heads."""
+    cp = synth.PSTORE
+    B, H, S = cp["B"], cp["H"], cp["S"]
+    Q, K, V, dO = synth.attention_inputs(B, H, S, cp["dh"], cp["dtype"], cp["config"])
+    out = run(lib, Q, K, V, dO, pols=cp["policies"], Kt=cp["K"], seed=cp["seed"], fwd_mode=cp["fwd_mode"])
+    heads = [(0, 0), (3, 15)]
+    g = np.random.default_rng(5)
+    rows = np.concatenate([np.sort(g.choice(S - 16, 16, replace=False)), np.arange(S - 16, S)])
+    ref = pstore.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.float().numpy(), causal=True,
+                       c=1.0 / 8.0, fmt=fp8.E4M3, fwd_mode=MODES[cp["fwd_mode"]], policies=cp["policies"], K=cp["K"],
+                       seed=cp["seed"], store_id=2, P=out["P"].cpu().numpy(), heads=heads, rows=rows)
+    assert np.array_equal(out["P_codes"].cpu().numpy(), ref["codes"])
+    assert float(out["P_scale"].cpu()[0]) == float(ref["scale"])
+    idx = [b * H + h for b, h in heads]
+    Pn = out["P"].cpu().numpy().reshape(B * H, S, S)[idx]
+    P64 = pstore.probabilities(Q.float().numpy().reshape(B * H, S, 64)[idx], K.float().numpy().reshape(B * H, S, 64)[idx],
+                               True, 1.0 / 8.0)
+    assert_rel(Pn, P64, TOL, "P against the fp64 softmax")
+    keys = np.arange(S - 16, S)
+    pick = {"dQ": lambda a: a[:, rows], "dK": lambda a: a[:, keys], "dV": lambda a: a[:, keys]}
+    shp = out["dQ_ref"].shape
+    sel = lambda t: to_np(t).reshape(B * H, S, 64)[idx]
+    for name in ("dQ", "dK", "dV"):
+        own = ref[name + "_ref"] if name == "dQ" else ref[name + "_ref"][:, keys]
+        assert_rel(pick[name](sel(out[name + "_ref"])), own, TOL, name + "_ref")
+    for i, p in enumerate(cp["policies"]):
+        for name in ("dQ", "dK", "dV"):
+            om, ob, _ = ref[p][name]
+            if name != "dQ":
+                om, ob = om[:, keys], ob[:, keys]
+            m = pick[name](sel(out[name]["mean"][i].reshape(shp)))
+            b = pick[name](sel(out[name]["bias"][i].reshape(shp)))
+            assert_rel(m, om, TOL, f"{p} {name} mean")
+            if not assert_zero_where_oracle_zero(b, ob, f"{p} {name} bias"):
+                assert_rel(b, ob, TOL, f"{p} {name} bias")
