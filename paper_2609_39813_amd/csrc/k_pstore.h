@@ -22,6 +22,14 @@ inline __host__ __device__ int64_t pstore_tiles(int nqb, int causal) {
   return causal ? (int64_t)nqb * (nqb + 1) / 2 : (int64_t)nqb * nqb;
 }
 
+constexpr int PSTORE_MAXPOL = 8;
+
+// one gradient's per-policy outputs [BH][S][64] each (nullable)
+struct PstoreOut {
+  float* mean[PSTORE_MAXPOL];
+  float* bias[PSTORE_MAXPOL];
+};
+
 struct PstoreArgs {
   const u16 *Q, *K, *V, *dO;        // [BH][S][64] bf16
   const u16 *Qt, *Kt, *Vt, *dOt;    // transposed copies [BH][64][Sp] (zero past S)
@@ -46,9 +54,11 @@ struct PstoreArgs {
   int draw_a, draw_b;               // a policy reads new rounding a / b (else their draws are skipped)
   float* fld[PF_COUNT];             // [BH][pstore_tiles][64 k][64 q] fp32, tile by (query block, key block)
   float *dQ_ref, *dK_ref, *dV_ref;  // [BH][S][64]
-  float* dQ_b[PF_SOFTMAX];          // per-field dQ and dK (entry PF_REF unused) and dV biases,
-  float* dK_b[PF_SOFTMAX];          // [BH][S][64] each
-  float* dV_b[2];                   // p - p_q (U) and mean a - p_q (N)
+  // the policies' estimates, written by the passes' epilogues: mean = reference + bias
+  int n_pol;
+  int sm_field[PSTORE_MAXPOL];      // bias field of the softmax read: PF_R .. PF_Q2, or PF_REF = none
+  int v_field[PSTORE_MAXPOL];       // dV read: 0 none (R), 1 p - p_q (U), 2 mean a - p_q (N)
+  PstoreOut dQ, dK, dV;
 };
 
 // amax = max over rows of 1 / l (the largest probability of each row), s = fl32(amax / FMAX)
@@ -59,9 +69,10 @@ bs_status launch_pstore_fwd(const PstoreArgs& a, hipStream_t st);
 // D = sum p dp, DR = sum r dp, E = sum e dp, Ee = sum e, Ps1 = sum p - 1; per trial k (u_k the
 // up-decision of new rounding a, v_k of b): Ga = sum u_k h dp, Ha = sum u_k h, Gb = sum v_k h dp
 bs_status launch_pstore_rows(const PstoreArgs& a, hipStream_t st);
-// bias fields (stored for the key-major pass) and dQ_ref, dQ biases
+// bias fields (stored for the key-major passes), dQ_ref and the policies' dQ estimates
 bs_status launch_pstore_dq(const PstoreArgs& a, hipStream_t st);
-// dK_ref, dK biases, dV_ref, dV biases from the stored fields and codes
+// dK_ref and the policies' dK estimates, then dV_ref and their dV estimates, from the stored
+// fields and codes
 bs_status launch_pstore_dkv(const PstoreArgs& a, hipStream_t st);
 
 }  // namespace bsp

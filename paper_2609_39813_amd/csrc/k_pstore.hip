@@ -137,6 +137,23 @@ __device__ __forceinline__ Resid resid(float p, float val, float s, double rs, F
   return o;
 }
 
+// one output element of every policy: mean = ref + bias[field], bias = bias[field] (b[0] = 0
+// for a read that is the reference's own)
+template <int NF>
+__device__ __forceinline__ void write_policies(const PstoreArgs& a, const int (&field)[PSTORE_MAXPOL],
+                                               const PstoreOut& o, int64_t e, float ref, const float (&b)[NF]) {
+#pragma unroll
+  for (int i = 0; i < PSTORE_MAXPOL; ++i) {
+    if (i >= a.n_pol) break;
+    const int fi = field[i];
+    float bi = 0.0f;
+#pragma unroll
+    for (int j = 1; j < NF; ++j) bi = fi == j ? b[j] : bi;
+    if (o.mean[i]) o.mean[i][e] = fi ? ref + bi : ref;
+    if (o.bias[i]) o.bias[i][e] = bi;
+  }
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------------------------
@@ -632,111 +649,110 @@ __global__ __launch_bounds__(256) void pstore_dq_kernel(PstoreArgs a) {
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
       const int64_t e = z.hb + (int64_t)qr * AT + 16 * n + z.c16;
-      a.dQ_ref[e] = c * aq[PF_REF][n][r];
+      const float ref = c * aq[PF_REF][n][r];
+      float b[PF_SOFTMAX];
 #pragma unroll
-      for (int i = 1; i < PF_SOFTMAX; ++i) a.dQ_b[i][e] = c * aq[i][n][r];
+      for (int i = 0; i < PF_SOFTMAX; ++i) b[i] = c * aq[i][n][r];
+      a.dQ_ref[e] = ref;
+      write_policies(a, a.sm_field, a.dQ, e, ref, b);
     }
   }
 }
 
 // ------------------------------------------------------------------------------------
-// key-major: dK = c sum_q field Q (three bf16 terms per field), dV = sum_q val(C) dO s (one
-// term) and the dV biases sum_q (p - p_q) dO, sum_q (mean a - p_q) dO (three terms)
+// key-major, one launch per gradient (PART 0: dK, PART 1: dV). dK = c sum_q field Q (three bf16
+// terms per field); dV = s sum_q val(C) dO (one term), its biases sum_q (p - p_q) dO and
+// sum_q (mean a - p_q) dO (three terms each). Lane (g, c16) of wave w owns key k0 + 16 w + c16.
 // ------------------------------------------------------------------------------------
-template <int FMT>
+template <int FMT, int PART>
 __global__ __launch_bounds__(256) void pstore_dkv_kernel(PstoreArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 sm[2][2][AT * AT];  // Q^T, dO^T
+  constexpr int NACC = PART == 0 ? PF_SOFTMAX : 3;
+  __shared__ __attribute__((aligned(16))) u16 sm[2][AT * AT];  // Q^T (dK) or dO^T (dV)
   if (a.diag->nonfinite) return;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, c16 = lane & 15;
-  const int bh = blockIdx.x, kb = blockIdx.y;
+  const int bh = blockIdx.x;
+  const int kb = blockIdx.y;  // under the causal mask block 0 walks the most query blocks: first out
   const int k0 = kb * AT;
   const int key = k0 + 16 * w + c16;
   const int64_t hb = (int64_t)bh * a.S * AT, tb = (int64_t)bh * AT * a.Sp;
   const int nqb = (a.S + AT - 1) / AT;
   const float s = a.diag->scale;
-  floatx4 ak[PF_SOFTMAX][4], av[3][4];
+  const u16* src = PART == 0 ? a.Qt : a.dOt;
+  floatx4 acc[NACC][4];
 #pragma unroll
-  for (int n = 0; n < 4; ++n) {
+  for (int n = 0; n < 4; ++n)
 #pragma unroll
-    for (int i = 0; i < PF_SOFTMAX; ++i) ak[i][n] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int i = 0; i < 3; ++i) av[i][n] = floatx4{0.f, 0.f, 0.f, 0.f};
-  }
-  TileRegs pf[2];
-  auto fetch = [&](int q0) {
-    tile_fetch_t(pf[0], a.Qt + tb, q0, a.Sp);
-    tile_fetch_t(pf[1], a.dOt + tb, q0, a.Sp);
-  };
-  auto put = [&](int st) {
-    tile_put_t(sm[st][0], pf[0]);
-    tile_put_t(sm[st][1], pf[1]);
-  };
+    for (int i = 0; i < NACC; ++i) acc[i][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  TileRegs pf;
   const int qb0 = a.causal ? kb : 0;
-  fetch(qb0 * AT);
-  put(0);
+  tile_fetch_t(pf, src + tb, qb0 * AT, a.Sp);
+  tile_put_t(sm[0], pf);
   __syncthreads();
   for (int qb = qb0; qb < nqb; ++qb) {
     const int st = (qb - qb0) & 1, q0 = qb * AT;
-    if (qb + 1 < nqb) fetch(q0 + AT);
+    if (qb + 1 < nqb) tile_fetch_t(pf, src + tb, q0 + AT, a.Sp);
     const int64_t tile = fld_tile(a, bh, qb, kb, nqb);
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      // queries 32 s2 + 16 h + 4 g + (0..3) of this lane's key, as the k index of the products
-      bf16x8 fq[4], fo[4];
+      // queries 32 s2 + 16 hh + 4 g + (0..3) of this lane's key, as the k index of the products
+      bf16x8 fo[4];
 #pragma unroll
-      for (int n = 0; n < 4; ++n) {
-        fq[n] = frag_t(sm[st][0], 16 * n + c16, s2, g);
-        fo[n] = frag_t(sm[st][1], 16 * n + c16, s2, g);
-      }
-      float vals[PF_COUNT][8];
-#pragma unroll
-      for (int i = 0; i < PF_COUNT; ++i) {
-        const float* T = a.fld[i] + tile + (int64_t)(16 * w + c16) * AT;
+      for (int n = 0; n < 4; ++n) fo[n] = frag_t(sm[st], 16 * n + c16, s2, g);
+      auto fields = [&](int i, float (&v)[8]) {
+        const float* T = a.fld[i] + tile + (int64_t)(16 * w + c16) * AT + 32 * s2 + 4 * g;
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
-          const float4 v = *(const float4*)(T + 32 * s2 + 16 * hh + 4 * g);
-          vals[i][4 * hh + 0] = v.x;
-          vals[i][4 * hh + 1] = v.y;
-          vals[i][4 * hh + 2] = v.z;
-          vals[i][4 * hh + 3] = v.w;
+          const float4 x = *(const float4*)(T + 16 * hh);
+          v[4 * hh + 0] = x.x;
+          v[4 * hh + 1] = x.y;
+          v[4 * hh + 2] = x.z;
+          v[4 * hh + 3] = x.w;
         }
-      }
+      };
+      if (PART == 0) {
+        float vals[PF_SOFTMAX][8];
 #pragma unroll
-      for (int i = 0; i < PF_SOFTMAX; ++i) {
-        bf16x8 td[3];
-        pack3(vals[i], td);
+        for (int i = 0; i < PF_SOFTMAX; ++i) fields(i, vals[i]);
 #pragma unroll
-        for (int n = 0; n < 4; ++n)
+        for (int i = 0; i < PF_SOFTMAX; ++i) {
+          bf16x8 td[3];
+          pack3(vals[i], td);
 #pragma unroll
-          for (int j = 0; j < 3; ++j) ak[i][n] = mfma(td[j], fq[n], ak[i][n]);
-      }
-      // dV: val(C) of (query, key) for the same eight queries (exact in bf16)
-      float cv[8];
+          for (int n = 0; n < 4; ++n)
 #pragma unroll
-      for (int v = 0; v < 8; ++v) {
-        const int qq = q0 + 32 * s2 + 16 * (v >> 2) + 4 * g + (v & 3);
-        const bool ok = qq < a.S && key < a.S;
-        const uint32_t b = ok ? a.codes[((int64_t)bh * a.S + qq) * a.S + key] : 0u;
-        cv[v] = f8_val<FMT>(b, 0);
-      }
-      uint32_t pk[4];
+            for (int j = 0; j < 3; ++j) acc[i][n] = mfma(td[j], fo[n], acc[i][n]);
+        }
+      } else {
+        float vu[8], vn[8], cv[8];
+        fields(PF_VU, vu);
+        fields(PF_VN, vn);
+        // val(C) of (query, key) for the same eight queries (exact in bf16)
 #pragma unroll
-      for (int i2 = 0; i2 < 4; ++i2) pk[i2] = pk_bf16(cv[2 * i2], cv[2 * i2 + 1]);
-      const bf16x8 tv = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
-      bf16x8 tu[3], tn[3];
-      pack3(vals[PF_VU], tu);
-      pack3(vals[PF_VN], tn);
+        for (int v = 0; v < 8; ++v) {
+          const int qq = q0 + 32 * s2 + 16 * (v >> 2) + 4 * g + (v & 3);
+          const bool ok = qq < a.S && key < a.S;
+          const uint32_t b = ok ? a.codes[((int64_t)bh * a.S + qq) * a.S + key] : 0u;
+          cv[v] = f8_val<FMT>(b, 0);
+        }
+        uint32_t pk[4];
 #pragma unroll
-      for (int n = 0; n < 4; ++n) {
-        av[0][n] = mfma(tv, fo[n], av[0][n]);
+        for (int i2 = 0; i2 < 4; ++i2) pk[i2] = pk_bf16(cv[2 * i2], cv[2 * i2 + 1]);
+        const bf16x8 tv = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+        bf16x8 tu[3], tn[3];
+        pack3(vu, tu);
+        pack3(vn, tn);
 #pragma unroll
-        for (int j = 0; j < 3; ++j) {
-          av[1][n] = mfma(tu[j], fo[n], av[1][n]);
-          av[2][n] = mfma(tn[j], fo[n], av[2][n]);
+        for (int n = 0; n < 4; ++n) {
+          acc[0][n] = mfma(tv, fo[n], acc[0][n]);
+#pragma unroll
+          for (int j = 0; j < 3; ++j) {
+            acc[1][n] = mfma(tu[j], fo[n], acc[1][n]);
+            acc[2][n] = mfma(tn[j], fo[n], acc[2][n]);
+          }
         }
       }
     }
-    if (qb + 1 < nqb) put(st ^ 1);
+    if (qb + 1 < nqb) tile_put_t(sm[st ^ 1], pf);
     __syncthreads();
   }
   const float c = a.scale;
@@ -747,12 +763,19 @@ __global__ __launch_bounds__(256) void pstore_dkv_kernel(PstoreArgs a) {
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
       const int64_t e = hb + (int64_t)kr * AT + 16 * n + c16;
-      a.dK_ref[e] = c * ak[PF_REF][n][r];
+      if (PART == 0) {
+        const float ref = c * acc[PF_REF][n][r];
+        float b[PF_SOFTMAX];
 #pragma unroll
-      for (int i = 1; i < PF_SOFTMAX; ++i) a.dK_b[i][e] = c * ak[i][n][r];
-      a.dV_ref[e] = s * av[0][n][r];
-      a.dV_b[0][e] = av[1][n][r];
-      a.dV_b[1][e] = av[2][n][r];
+        for (int i = 0; i < PF_SOFTMAX; ++i) b[i] = c * acc[i][n][r];
+        a.dK_ref[e] = ref;
+        write_policies(a, a.sm_field, a.dK, e, ref, b);
+      } else {
+        const float ref = s * acc[0][n][r];
+        const float b[3] = {0.0f, acc[1][n][r], acc[2][n][r]};
+        a.dV_ref[e] = ref;
+        write_policies(a, a.v_field, a.dV, e, ref, b);
+      }
     }
   }
 }
@@ -814,10 +837,13 @@ bs_status launch_pstore_dq(const PstoreArgs& a, hipStream_t st) {
 
 bs_status launch_pstore_dkv(const PstoreArgs& a, hipStream_t st) {
   ProfScope prof("pstore_dkv", st);
-  if (a.fmt == BS_E5M2)
-    pstore_dkv_kernel<BS_E5M2><<<pstore_grid(a), 256, 0, st>>>(a);
-  else
-    pstore_dkv_kernel<BS_E4M3><<<pstore_grid(a), 256, 0, st>>>(a);
+  if (a.fmt == BS_E5M2) {
+    pstore_dkv_kernel<BS_E5M2, 0><<<pstore_grid(a), 256, 0, st>>>(a);
+    pstore_dkv_kernel<BS_E5M2, 1><<<pstore_grid(a), 256, 0, st>>>(a);
+  } else {
+    pstore_dkv_kernel<BS_E4M3, 0><<<pstore_grid(a), 256, 0, st>>>(a);
+    pstore_dkv_kernel<BS_E4M3, 1><<<pstore_grid(a), 256, 0, st>>>(a);
+  }
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

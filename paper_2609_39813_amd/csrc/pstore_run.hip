@@ -20,7 +20,6 @@ struct PstoreWs {
   float *m, *l, *D, *DR, *E, *Ee, *Ps1, *Ga, *Ha, *Gb, *O;
   float* fld[PF_COUNT];
   uint32_t* ubits;
-  float *dQ_b[PF_SOFTMAX], *dK_b[PF_SOFTMAX], *dV_b[2];
 };
 
 PstoreWs carve_pstore(Carver& c, int64_t bh, int S, int K, int causal, bool need_o) {
@@ -36,16 +35,11 @@ PstoreWs carve_pstore(Carver& c, int64_t bh, int S, int K, int causal, bool need
   const int64_t nf = bh * pstore_tiles(nqb, causal) * PSTORE_T * PSTORE_T;
   for (int i = 0; i < PF_COUNT; ++i) w.fld[i] = c.take<float>(nf);
   w.ubits = c.take<uint32_t>((int64_t)((K + PSTORE_RC - 1) / PSTORE_RC) * nf);
-  for (int i = 1; i < PF_SOFTMAX; ++i) {
-    w.dQ_b[i] = c.take<float>(numel);
-    w.dK_b[i] = c.take<float>(numel);
-  }
-  for (int i = 0; i < 2; ++i) w.dV_b[i] = c.take<float>(numel);
   if (need_o) w.O = c.take<float>(numel);
   return w;
 }
 
-// the bias field a softmax's-backward read selects (-1: the reference J(p) itself)
+// the bias field a softmax's-backward read selects (PF_REF: the reference J(p) itself, no bias)
 int softmax_field(int r) {
   switch (r) {
     case BS_SM_R: return PF_R;
@@ -53,7 +47,7 @@ int softmax_field(int r) {
     case BS_SM_K: return PF_K;
     case BS_SM_J2: return PF_J2;
     case BS_SM_Q2: return PF_Q2;
-    default: return -1;
+    default: return PF_REF;
   }
 }
 
@@ -88,7 +82,7 @@ bs_status pstore_run(const PstoreIO& io, void* ws, size_t ws_bytes, hipStream_t 
       !io.pol)
     return BS_EINVAL;
   if (io.B < 1 || io.H < 1 || io.S < 1 || io.ntrial < 1 || io.ntrial > PSTORE_KMAX) return BS_EINVAL;
-  if (io.n_pol < 1 || io.n_pol > 8) return BS_EINVAL;
+  if (io.n_pol < 1 || io.n_pol > PSTORE_MAXPOL) return BS_EINVAL;
   if (!(io.scale > 0.0f) || (io.fmt != BS_E4M3 && io.fmt != BS_E5M2) ||
       (io.fwd_mode != BS_RNE && io.fwd_mode != BS_SR))
     return BS_EINVAL;
@@ -165,12 +159,19 @@ bs_status pstore_run(const PstoreIO& io, void* ws, size_t ws_bytes, hipStream_t 
   a.dQ_ref = io.dQ_ref;
   a.dK_ref = io.dK_ref;
   a.dV_ref = io.dV_ref;
-  for (int i = 0; i < PF_SOFTMAX; ++i) {
-    a.dQ_b[i] = w.dQ_b[i];
-    a.dK_b[i] = w.dK_b[i];
+  a.n_pol = io.n_pol;
+  for (int i = 0; i < io.n_pol; ++i) {
+    const int vr = io.pol[i].v_read;
+    a.sm_field[i] = softmax_field(io.pol[i].softmax_read);
+    a.v_field[i] = vr == BS_READ_U ? 1 : (vr == BS_READ_N ? 2 : 0);
+    auto at = [&](float* base) { return base ? base + (int64_t)i * numel : nullptr; };
+    a.dQ.mean[i] = at(io.dQ.mean);
+    a.dQ.bias[i] = at(io.dQ.bias);
+    a.dK.mean[i] = at(io.dK.mean);
+    a.dK.bias[i] = at(io.dK.bias);
+    a.dV.mean[i] = at(io.dV.mean);
+    a.dV.bias[i] = at(io.dV.bias);
   }
-  a.dV_b[0] = w.dV_b[0];
-  a.dV_b[1] = w.dV_b[1];
 
   BS_TRY(launch_pstore_scale(a, st));
   BS_TRY(launch_pstore_fwd(a, st));
@@ -178,18 +179,6 @@ bs_status pstore_run(const PstoreIO& io, void* ws, size_t ws_bytes, hipStream_t 
   BS_TRY(launch_pstore_dq(a, st));
   BS_TRY(launch_pstore_dkv(a, st));
 
-  // per policy: mean = reference + the selected field's bias (no field: the reference read)
-  for (int i = 0; i < io.n_pol; ++i) {
-    const int fs = softmax_field(io.pol[i].softmax_read);
-    const float* bq = fs < 0 ? nullptr : w.dQ_b[fs];
-    const float* bk = fs < 0 ? nullptr : w.dK_b[fs];
-    const int vr = io.pol[i].v_read;
-    const float* bv = vr == BS_READ_U ? w.dV_b[0] : (vr == BS_READ_N ? w.dV_b[1] : nullptr);
-    auto at = [&](float* base) { return base ? base + (int64_t)i * numel : nullptr; };
-    BS_TRY(launch_combine(io.dQ_ref, bq, nullptr, numel, at(io.dQ.mean), at(io.dQ.bias), nullptr, st));
-    BS_TRY(launch_combine(io.dK_ref, bk, nullptr, numel, at(io.dK.mean), at(io.dK.bias), nullptr, st));
-    BS_TRY(launch_combine(io.dV_ref, bv, nullptr, numel, at(io.dV.mean), at(io.dV.bias), nullptr, st));
-  }
   return BS_OK;
 }
 
