@@ -48,9 +48,10 @@ struct PstoreArgs {
   float* O;                         // [BH][S][64] forward output p_q V
   float *D, *DR, *E, *Ee, *Ps1;     // per row (query) sums, [BH][S] (see launch_pstore_rows)
   float *Ga, *Ha, *Gb;              // per trial and row, [ntrial][BH][S]
-  uint32_t* ubits;                  // up-decisions, per chunk c of 16 trials a plane of one word per
-                                    // element (bit j: a of trial 16c + j; bit 16 + j: b), tiles as
-                                    // the fields, each tile's words thread-major (16 per thread)
+  uint32_t* ubits;                  // up-decisions, per chunk c of jn <= 16 trials a plane of one word
+                                    // per element (trial 16c + j: a at bit 2 (jn - 1 - j) + 1, b at
+                                    // bit 2 (jn - 1 - j)), tiles as the fields, each tile's words
+                                    // thread-major (16 per thread)
   int draw_a, draw_b;               // a policy reads new rounding a / b (else their draws are skipped)
   float* fld[PF_COUNT];             // [BH][pstore_tiles][64 k][64 q] fp32, tile by (query block, key block)
   float *dQ_ref, *dK_ref, *dV_ref;  // [BH][S][64]

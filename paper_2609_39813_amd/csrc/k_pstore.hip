@@ -360,6 +360,9 @@ __global__ __launch_bounds__(256, 2) void pstore_rows_kernel(PstoreArgs a) {
       probs(a, z, sm[st][0], k0, p);
       dprobs(z, sm[st][1], dp);
       float hh[4][4], hd[4][4];
+      // per element: the decisions of this chunk's trials, two bits per trial shifted in from
+      // the bottom (a, then b), so that trial j of jn ends at bits 2 (jn - 1 - j) + 1 (a) and
+      // 2 (jn - 1 - j) (b)
       uint32_t FF[4][4], ub[4][4];
       uint64_t grp[4];
       bool need[4];
@@ -401,9 +404,10 @@ __global__ __launch_bounds__(256, 2) void pstore_rows_kernel(PstoreArgs a) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const uint32_t u = sr_up(FF[t][r], Ra[r]);
-              ub[t][r] |= u << j;
-              gaj += u ? hd[t][r] : 0.0f;
-              haj += u ? hh[t][r] : 0.0f;
+              ub[t][r] = ub[t][r] + ub[t][r] + u;
+              const float uf = u ? 1.0f : 0.0f;
+              gaj = fmaf(uf, hd[t][r], gaj);
+              haj = fmaf(uf, hh[t][r], haj);
             }
             if (DRAW == 2) {
               const Philox4 pb = philox_group(a.seed, grp[t], trial, a.use_b);
@@ -411,9 +415,12 @@ __global__ __launch_bounds__(256, 2) void pstore_rows_kernel(PstoreArgs a) {
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
                 const uint32_t u = sr_up(FF[t][r], Rb[r]);
-                ub[t][r] |= u << (j + 16);
+                ub[t][r] = ub[t][r] + ub[t][r] + u;
                 gbj += u ? hd[t][r] : 0.0f;
               }
+            } else {
+#pragma unroll
+              for (int r = 0; r < 4; ++r) ub[t][r] += ub[t][r];
             }
           }
           acc[0][j][tid] += gaj;
@@ -497,6 +504,10 @@ __global__ __launch_bounds__(256) void pstore_dq_kernel(PstoreArgs a) {
   const int nqb = (a.S + AT - 1) / AT;
   const int nchunk = (a.ntrial + PSTORE_RC - 1) / PSTORE_RC;
   const int64_t plane = (int64_t)a.BH * pstore_tiles(nqb, a.causal) * AT * AT;
+  // a chunk of jn trials fills the top 2 jn bits of its reversed word (an absent chunk: 0)
+  int sh[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) sh[c] = c < nchunk ? 32 - 2 * min(PSTORE_RC, a.ntrial - PSTORE_RC * c) : 0;
 
   floatx4 aq[PF_SOFTMAX][4];
 #pragma unroll
@@ -552,17 +563,21 @@ __global__ __launch_bounds__(256) void pstore_dq_kernel(PstoreArgs a) {
         load_step(kb + 1, 0, cw_nxt, bw_nxt);
       float fl[PF_COUNT][2][4];
       Resid x[2][4];
-      uint32_t am[2][4], bm[2][4];  // up-decisions of a and b over the trials
+      uint32_t nw[2][2][4];          // per chunk: the elements' decision words, normalized
+      float na[2][4], nb[2][4];      // up-counts of a and b over the trials
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt) {
         const int t = 2 * s2 + tt;
-        const uint32_t w4[4] = {bw_cur[0][tt].x, bw_cur[0][tt].y, bw_cur[0][tt].z, bw_cur[0][tt].w};
-        const uint32_t v4[4] = {bw_cur[1][tt].x, bw_cur[1][tt].y, bw_cur[1][tt].z, bw_cur[1][tt].w};
+        const uint32_t w4[2][4] = {{bw_cur[0][tt].x, bw_cur[0][tt].y, bw_cur[0][tt].z, bw_cur[0][tt].w},
+                                   {bw_cur[1][tt].x, bw_cur[1][tt].y, bw_cur[1][tt].z, bw_cur[1][tt].w}};
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           x[tt][r] = resid(p[t][r], f8_val<FMT>(cw_cur[tt], r), s, rs, f);
-          am[tt][r] = (w4[r] & 0xFFFFu) | (v4[r] << 16);
-          bm[tt][r] = (w4[r] >> 16) | (v4[r] & 0xFFFF0000u);
+          // chunk c's word with trial j's a at bit 2 j and b at bit 2 j + 1
+#pragma unroll
+          for (int c = 0; c < 2; ++c) nw[c][tt][r] = __builtin_bitreverse32(w4[c][r]) >> sh[c];
+          na[tt][r] = (float)(__popc(nw[0][tt][r] & 0x55555555u) + __popc(nw[1][tt][r] & 0x55555555u));
+          nb[tt][r] = (float)(__popc(nw[0][tt][r] & 0xAAAAAAAAu) + __popc(nw[1][tt][r] & 0xAAAAAAAAu));
         }
       }
       // per element: sum over trials of the up-decision times the row's per-trial sums
@@ -571,19 +586,26 @@ __global__ __launch_bounds__(256) void pstore_dq_kernel(PstoreArgs a) {
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) uga[tt][r] = uha[tt][r] = ugab[tt][r] = ugba[tt][r] = 0.0f;
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        if (c >= nchunk) break;
+        const int jn = min(PSTORE_RC, a.ntrial - PSTORE_RC * c);
 #pragma unroll 2
-      for (int k = 0; k < a.ntrial; ++k) {
-        const float gak = tv[0][ql][k], hak = tv[1][ql][k], gbk = tv[2][ql][k];
+        for (int j = 0; j < jn; ++j) {
+          const int k = PSTORE_RC * c + j;
+          const float gak = tv[0][ql][k], hak = tv[1][ql][k], gbk = tv[2][ql][k];
 #pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
+          for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float ua = (float)((am[tt][r] >> k) & 1u), vb = (float)((bm[tt][r] >> k) & 1u);
-            uga[tt][r] = fmaf(ua, gak, uga[tt][r]);
-            uha[tt][r] = fmaf(ua, hak, uha[tt][r]);
-            ugab[tt][r] = fmaf(ua, gbk, ugab[tt][r]);
-            ugba[tt][r] = fmaf(vb, gak, ugba[tt][r]);
-          }
+            for (int r = 0; r < 4; ++r) {
+              const float ua = (float)((nw[c][tt][r] >> (2 * j)) & 1u);
+              const float vb = (float)((nw[c][tt][r] >> (2 * j + 1)) & 1u);
+              uga[tt][r] = fmaf(ua, gak, uga[tt][r]);
+              uha[tt][r] = fmaf(ua, hak, uha[tt][r]);
+              ugab[tt][r] = fmaf(ua, gbk, ugab[tt][r]);
+              ugba[tt][r] = fmaf(vb, gak, ugba[tt][r]);
+            }
+        }
       }
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt) {
@@ -591,13 +613,13 @@ __global__ __launch_bounds__(256) void pstore_dq_kernel(PstoreArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float pp = p[t][r], d = dp[t][r], rr = x[tt][r].r, e = x[tt][r].e, h = x[tt][r].h;
-          const float na = (float)__popc(am[tt][r]), nb = (float)__popc(bm[tt][r]);
+          const float na_ = na[tt][r], nb_ = nb[tt][r];
           const float dpm = d - D;
-          const float m1a = e + h * na * iK, m1b = e + h * nb * iK;
-          const float mrDa = e * dDa + h * (E * na + uga[tt][r]) * iK;   // mean r_a dD_a
-          const float mrRa = e * rho + h * (Ee * na + uha[tt][r]) * iK;  // mean r_a rho_a
-          const float mrab = e * dDb + h * (E * na + ugab[tt][r]) * iK;  // mean r_a dD_b
-          const float mrba = e * dDa + h * (E * nb + ugba[tt][r]) * iK;  // mean r_b dD_a
+          const float m1a = e + h * na_ * iK, m1b = e + h * nb_ * iK;
+          const float mrDa = e * dDa + h * (E * na_ + uga[tt][r]) * iK;   // mean r_a dD_a
+          const float mrRa = e * rho + h * (Ee * na_ + uha[tt][r]) * iK;  // mean r_a rho_a
+          const float mrab = e * dDb + h * (E * na_ + ugab[tt][r]) * iK;  // mean r_a dD_b
+          const float mrba = e * dDa + h * (E * nb_ + ugba[tt][r]) * iK;  // mean r_b dD_a
           fl[PF_REF][tt][r] = pp * dpm;
           fl[PF_R][tt][r] = rr * (dpm - DR) - pp * DR;
           fl[PF_N][tt][r] = m1a * dpm - pp * dDa - mrDa;
