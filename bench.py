@@ -36,10 +36,10 @@ OPS_PER_ELEMENT_TRIAL = 1408 / 128
 ALU_PEAK_ETPS = VALU_LANE_OPS / OPS_PER_ELEMENT_TRIAL
 
 # The P store's row-sum pass as compiled for gfx950: one trial of its draw loop over a thread's 16
-# elements (a and b, 32 element-draws) issues 471 VALU instructions, 272 of them Philox4x32-10
+# elements (a and b, 32 element-draws) issues 452 VALU instructions, 272 of them Philox4x32-10
 # (128 v_mad_u64_u32 + 144 v_bitop3_b32), the rest the up-decision, its bit and the per-trial
-# sums: 14.7 per element-draw; ceiling 2.67e12 element-draws/s.
-PSTORE_ROWS_PEAK_DPS = VALU_LANE_OPS / (471 / 32)
+# sums: 14.1 per element-draw; ceiling 2.78e12 element-draws/s.
+PSTORE_ROWS_PEAK_DPS = VALU_LANE_OPS / (452 / 32)
 
 # HBM bytes per launch of the counter at the benchmark shape, from two rocprofv3 --pmc passes
 # (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) over this script, each scaled by what the
