@@ -173,6 +173,38 @@ bs_status bs_attn_bwd_policy(const void* Q, const void* Kt, const void* V, const
                              bs_diag* diag, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------
+ * bs_attn_level2_policy -- the D use of the attention output store averaged over the
+ * forward's own rounding as well (App. C.1's level of averaging, the forward's inputs fixed),
+ * with an incoming gradient that can depend on that rounding (Sec. 4.2; App. B.3), and the
+ * split of the use's average error into a mean error and a coupling (App. C.1).
+ *
+ * As bs_attn_bwd_policy, except: in trial k = 1..K the forward's store of O rounds anew
+ * (mode fwd_mode, trial k, use store_id*256; scale s from amax(O) as always) with error
+ * r_k = deq(C_k) - O, and the incoming gradient is g_k = dO + beta r_k (beta = 0: fixed;
+ * beta = 1: the output's deviation added, as the loss 1/2 ||o||^2 gives up to its fixed part).
+ * U reads O, R reads deq(C_k), N a new rounding (trial k, use store_id*256 + 1). Each trial's
+ * reference is the backward of the forward as it ran (incoming g_k, D_ref,k = rowsum(g_k O)).
+ * Outputs are means over the K trials: dQ_ref, dK_ref, dV (= P^T mean g), D_ref; per policy
+ * dQ, dK mean and bias (the mean of the per-trial difference; se must be NULL). For the D use
+ * of each policy, d_use [n_pol][4][B*H*S]: the mean of its error rowsum(g_k e_k) (e_k the
+ * copy's deviation from O), the mean-error part rowsum(mean e * mean g), the coupling (the
+ * remainder) and the se over trials of the error. T [2][B*H*S]: mean and se of the paired
+ * statistic T_k = 1/2 rowsum((r_k - r'_k)(g(O + r_k) - g(O + r'_k))) of App. E.4, whose mean
+ * is R's error minus N's. dO_mean [B,H,S,dh] (nullable): the mean incoming gradient.
+ *
+ *   Q, Kt, V, dO bf16 [B,H,S,dh], dh == 64; O, O_out, D_ref as bs_attn_bwd_policy; O_scale [1].
+ *   d_pol (host) [n_pol] in {U, R, N}, n_pol in [1, 8]; K in [1, 4096].
+ *   Workspace: bs_attn_workspace_size(B, H, S, dh, n_pol, K).
+ * Returns BS_EINVAL for a NULL dO or a NaN beta; otherwise as bs_attn_bwd_policy.
+ * ---------------------------------------------------------------------------------- */
+bs_status bs_attn_level2_policy(const void* Q, const void* Kt, const void* V, const void* dO, int B, int H, int S,
+                                int dh, int causal, float softmax_scale, const float* O, bs_fp8 fmt, bs_round fwd_mode,
+                                float beta, const bs_read* d_pol, int n_pol, int K, uint64_t seed, uint32_t store_id,
+                                float* O_out, float* O_scale, float* dO_mean, float* dQ_ref, float* dK_ref, float* dV,
+                                float* D_ref, bs_est dQ, bs_est dK, float* d_use, float* T, bs_diag* diag, void* ws,
+                                size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
  * bs_attn_pstore_policy -- attention whose probabilities P pass through an FP8 store, and
  * the two uses of that store in the backward: the gradient of V and the softmax's backward
  * (App. B.2, Eq. app-ref and Eq. app-errors; App. B.3; App. B.4; Table app-theory-errors).
@@ -338,7 +370,8 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* w, cons
  *   bs_profile_enable(1) clears earlier records and starts recording a pair of HIP
  *   events on the launch stream around each launch of the instrumented kernels
  *   ("fresh_count", "fresh_count_se", "fresh_count_kappa", "amax", "quantize", "gemm",
- *   "rmsnorm_fwd", "attn_fwd", "attn_bwd", "pstore_fwd", "pstore_rows", "pstore_dq", "pstore_dkv");
+ *   "rmsnorm_fwd", "attn_fwd", "attn_bwd", "attn_l2", "pstore_fwd", "pstore_rows", "pstore_dq",
+ *   "pstore_dkv");
  *   bs_profile_enable(0) stops and frees them. bs_profile_read waits for the recorded
  *   events of `kernel` (NULL: all) and returns their summed elapsed time and count.
  *   Return values are bs_status codes.

@@ -94,16 +94,15 @@ def check(Q, Kt, V, dO, *, causal=True, c=None, fmt=fp8.E4M3, fwd_mode=qround.SR
     y = qround.scaled(O32, s)
     heads = [(b, h) for b in range(B) for h in range(H)] if heads is None else list(heads)
     elem = np.arange(O32.size, dtype=np.uint64).reshape(O32.shape)
-    # the forward's rounding of each trial over the whole tensor (its scale is the trials' common s)
-    r_all = [qround.dequant(qround.qround(O32, fmt, fwd_mode, seed, k, base, scale=s).codes, s, fmt)
-             - O32.astype(np.float64) for k in range(1, K + 1)]
     out = {"O32": O32, "scale": s, "heads": heads}
     acc = {"ref": {"dQ": [], "dK": [], "dV": [], "D": [], "g": []}}
     per = {p: {"dQ": [], "dK": [], "dh": []} for p in policies}
     T_h = []
     for (b, h) in heads:
         o = O32[b, h].astype(np.float64)
-        r = np.stack([ra[b, h] for ra in r_all])                                    # [K, S, dh]
+        # the forward's rounding of each trial (the store of O at the trials' common scale s)
+        r = np.stack([qround.dequant(qround.round_scaled(y[b, h], fmt, fwd_mode, seed, k, base, elem[b, h])[0], s, fmt)
+                      - o for k in range(1, K + 1)])                                 # [K, S, dh]
         rp = np.stack([fresh_values(y[b, h], elem[b, h], fmt, s, seed, k, base + 1) - o
                        for k in range(1, K + 1)])
         g = dO[b, h][None] + beta * r                                               # g_k

@@ -72,6 +72,9 @@ _ps_ws = _sig("bs_attn_pstore_workspace_size", _sz, [_int] * 6)
 _ps = _sig("bs_attn_pstore_policy", _int,
            [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _int, _int, ctypes.POINTER(PstorePolicy), _int,
             _int, _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, Est, _vp, _vp, _sz, _vp])
+_attn2 = _sig("bs_attn_level2_policy", _int,
+              [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _vp, _int, _int, _f32, ctypes.POINTER(_int), _int,
+               _int, _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, _vp, _vp, _vp, _vp, _sz, _vp])
 _lin_ws = _sig("bs_linear_bwd_workspace_size", _sz, [_i64, _i64, _i64, _int, _int])
 _lin = _sig("bs_linear_bwd_policy", _int,
             [_vp, _vp, _vp, _int, _i64, _i64, _i64, _int, ctypes.POINTER(_int), _int, _int, _u64, _u32, _vp, _vp,
@@ -117,7 +120,7 @@ def profile_read(kernel=None):
 
 EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
             "bs_policy_bias_estimate", "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
-            "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_attn_pstore_workspace_size", "bs_attn_pstore_policy", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
+            "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_attn_pstore_workspace_size", "bs_attn_pstore_policy", "bs_attn_level2_policy", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
             "bs_decoder_layer_workspace_size", "bs_decoder_layer_policy", "bs_profile_enable", "bs_profile_read"]
 
 
@@ -285,6 +288,39 @@ def attn_bwd_policy(Q, Kt, V, dO, *, causal=True, scale=None, O=None, fmt="e4m3"
                  len(policies), K, seed, store_id, _p(out["O"]), _p(out["O_codes"]), _p(out["O_scale"]),
                  _p(out["dQ_ref"]), _p(out["dK_ref"]), _p(out["dV"]), _p(out["D_ref"]), cq, ck, _p(out["diag"]),
                  _p(ws), ws.numel(), _stream()), "bs_attn_bwd_policy")
+    out["dQ"], out["dK"] = eq, ek
+    return out
+
+
+def attn_level2_policy(Q, Kt, V, dO, *, causal=True, scale=None, O=None, fmt="e4m3", fwd_mode="sr", beta=1.0,
+                       policies=("U", "R", "N"), K=32, seed=0, store_id=0, want_o=False, ws=None):
+    """The D use averaged over the forward's rounding too, with incoming gradient dO + beta r_k
+    (bs_attn_level2_policy)."""
+    _dev_check(Q, Kt, V, dO, O)
+    B, H, S, dh = Q.shape
+    dev = Q.device
+    c = 1.0 / dh ** 0.5 if scale is None else scale
+    pol = (_int * len(policies))(*[READ[p] for p in policies])
+    shp, rows = (B, H, S, dh), B * H * S
+    out = {"O": torch.empty(shp, dtype=torch.float32, device=dev) if want_o else None,
+           "O_scale": torch.empty(1, dtype=torch.float32, device=dev),
+           "dO_mean": torch.empty(shp, dtype=torch.float32, device=dev),
+           "dQ_ref": torch.empty(shp, dtype=torch.float32, device=dev),
+           "dK_ref": torch.empty(shp, dtype=torch.float32, device=dev),
+           "dV": torch.empty(shp, dtype=torch.float32, device=dev),
+           "D_ref": torch.empty(B, H, S, dtype=torch.float32, device=dev),
+           "d_use": torch.empty(len(policies), 4, rows, dtype=torch.float32, device=dev),
+           "T": torch.empty(2, rows, dtype=torch.float32, device=dev),
+           "diag": new_diag(dev)}
+    numel = B * H * S * dh
+    eq, cq = _est(len(policies), numel, dev, False)
+    ek, ck = _est(len(policies), numel, dev, False)
+    if ws is None:
+        ws = _workspace(_attn_ws(B, H, S, dh, len(policies), K), dev)
+    _check(_attn2(_p(Q), _p(Kt), _p(V), _p(dO), B, H, S, dh, int(causal), c, _p(O), _FMT[fmt], _MODE[fwd_mode], beta,
+                  pol, len(policies), K, seed, store_id, _p(out["O"]), _p(out["O_scale"]), _p(out["dO_mean"]),
+                  _p(out["dQ_ref"]), _p(out["dK_ref"]), _p(out["dV"]), _p(out["D_ref"]), cq, ck, _p(out["d_use"]),
+                  _p(out["T"]), _p(out["diag"]), _p(ws), ws.numel(), _stream()), "bs_attn_level2_policy")
     out["dQ"], out["dK"] = eq, ek
     return out
 

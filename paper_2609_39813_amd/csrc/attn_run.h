@@ -22,6 +22,14 @@ struct AttnIO {
   float *dQ_ref, *dK_ref, *dV, *D_ref;
   bs_est dQ, dK;
   bs_diag* diag;
+  // level-2 averaging (the forward's rounding resampled per trial, incoming gradient
+  // dO + beta r_k; dO bf16 only): the D use's split per policy [n_pol][4][B*H*S] (nullable),
+  // the paired statistic [2][B*H*S] (nullable), the mean incoming gradient (nullable)
+  int level2 = 0;
+  float beta = 0.0f;
+  float* d_use = nullptr;
+  float* T = nullptr;
+  float* dO_mean = nullptr;
 };
 
 size_t attn_ws_size(int B, int H, int S, int dh);

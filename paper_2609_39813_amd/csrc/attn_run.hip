@@ -15,10 +15,17 @@ namespace {
 struct AttnWs {
   float *m, *l, *O, *D_ref, *dD_R, *dD_N, *sd_N;
   u16 *Vt, *Qt, *Kt, *dOp[3], *dOt[3];
+  float *dO_mean, *stat;   // level 2: mean incoming gradient; split of R and N [2][4][rows]
+  uint8_t* codes;          // level 2: the trial-0 store when the caller takes none
 };
 AttnWs carve_attn(Carver& c, int64_t rows, int64_t numel, bool need_o, bool need_dref, int64_t bh = 0, int64_t Sp = 0,
-                  int ndo = 0) {
+                  int ndo = 0, bool level2 = false) {
   AttnWs w{};
+  if (level2) {
+    w.dO_mean = c.take<float>(numel);
+    w.stat = c.take<float>(8 * rows);
+    w.codes = c.take<uint8_t>(numel);
+  }
   w.Vt = c.take<u16>(bh * 64 * Sp);
   if (ndo > 0) {  // operand copies for the backward
     w.Qt = c.take<u16>(bh * 64 * Sp);
@@ -42,13 +49,15 @@ size_t attn_ws_size(int B, int H, int S, int dh) {
   if (B < 0 || H < 0 || S < 0 || dh < 0) return 0;
   Carver c;
   const int64_t rows = (int64_t)B * H * S;
-  carve_attn(c, rows, rows * dh, true, true, (int64_t)B * H, (S + 63) / 64 * 64, 3);
+  carve_attn(c, rows, rows * dh, true, true, (int64_t)B * H, (S + 63) / 64 * 64, 3, true);
   return c.used();
 }
 
 bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
   const bool fwd_only = !io.dO && !io.dO32;
-  if (!io.Q || !io.Kt || !io.V || !io.O_codes || !io.O_scale || !io.diag) return BS_EINVAL;
+  const bool l2 = io.level2 != 0;
+  if (l2 && (!io.dO || io.dO32 || !(io.beta == io.beta))) return BS_EINVAL;
+  if (!io.Q || !io.Kt || !io.V || (!io.O_codes && !l2) || !io.O_scale || !io.diag) return BS_EINVAL;
   if (!fwd_only && (!io.dQ_ref || !io.dK_ref || !io.dV || !io.pol)) return BS_EINVAL;
   if (io.B < 1 || io.H < 1 || io.S < 1 || io.K < 1 || io.K > 4096) return BS_EINVAL;
   if (!fwd_only && (io.n_pol < 1 || io.n_pol > ATTN_MAX_POL)) return BS_EINVAL;
@@ -59,7 +68,7 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   for (const void* p : {io.Q, io.Kt, io.V, io.dO, (const void*)io.dO32, (const void*)io.O})
     if ((uintptr_t)p & 15) return BS_EINVAL;  // 16-byte vector loads
   if ((int64_t)io.B * io.H > 65535 || (io.S + 63) / 64 > 65535) return BS_ESHAPE;
-  if (io.dK.se) return BS_EUNSUPPORTED;
+  if (io.dK.se || (l2 && io.dQ.se)) return BS_EUNSUPPORTED;
   bool want_r = false, want_n = false;
   for (int i = 0; i < (fwd_only ? 0 : io.n_pol); ++i) {
     if (io.pol[i] < BS_READ_U || io.pol[i] > BS_READ_N) return BS_EINVAL;
@@ -69,19 +78,22 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   const int64_t rows = (int64_t)io.B * io.H * io.S, numel = rows * io.dh;
   const bool need_o = !io.O && !io.O_out;
   const int64_t bh = (int64_t)io.B * io.H, Sp = (io.S + 63) / 64 * 64;
-  const int ndo = fwd_only ? 0 : (io.dO32 ? 3 : 1);
+  const int ndo = fwd_only ? 0 : ((io.dO32 || l2) ? 3 : 1);
   Carver probe;
-  carve_attn(probe, rows, numel, need_o, !io.D_ref, bh, Sp, ndo);
+  carve_attn(probe, rows, numel, need_o, !io.D_ref, bh, Sp, ndo, l2);
   if (!ws || ((uintptr_t)ws & 255) || ws_bytes < probe.used()) return BS_EWORKSPACE;
   Carver c(ws, ws_bytes);
-  AttnWs w = carve_attn(c, rows, numel, need_o, !io.D_ref, bh, Sp, ndo);
+  AttnWs w = carve_attn(c, rows, numel, need_o, !io.D_ref, bh, Sp, ndo, l2);
   float* dref = io.D_ref ? io.D_ref : w.D_ref;
+  uint8_t* O_codes = io.O_codes ? io.O_codes : w.codes;
+  // level 2: the mean incoming gradient replaces dO in the backward (fp32, three bf16 planes)
+  const float* dO32 = l2 ? (io.dO_mean ? io.dO_mean : w.dO_mean) : io.dO32;
 
   // forward: m, l (and O when the caller does not hand it in)
   {  // transposed operand copies: V^T for the forward; Q^T, K^T (and dO^T) for the backward
     const u16* src[4] = {(const u16*)io.V, (const u16*)io.Q, (const u16*)io.Kt, (const u16*)io.dO};
     u16* dst[4] = {w.Vt, w.Qt, w.Kt, w.dOt[0]};
-    const int n = fwd_only ? 1 : (io.dO32 ? 3 : 4);
+    const int n = fwd_only ? 1 : (dO32 ? 3 : 4);
     BS_TRY(launch_attn_transpose(src, dst, n, (int)bh, io.S, (int)Sp, st));
   }
   AttnArgs fa{(const u16*)io.Q, (const u16*)io.Kt, (const u16*)io.V, io.S, io.causal, io.scale, w.m, w.l, nullptr,
@@ -99,16 +111,31 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
 
   // the store of O (trial 0, use store_id*256)
   const uint32_t base = io.store_id * 256u;
-  BS_TRY(launch_store(Oorig, BS_F32, numel, io.fmt, io.fwd_mode, io.seed, 0, base, nullptr, io.O_codes, io.O_scale,
+  BS_TRY(launch_store(Oorig, BS_F32, numel, io.fmt, io.fwd_mode, io.seed, 0, base, nullptr, O_codes, io.O_scale,
                       io.diag, st, false));
   if (fwd_only) return BS_OK;
 
   // D variants
-  AttnDArgs da{Oorig, (const u16*)io.dO, io.dO32, io.O_codes, io.O_scale, rows, f8_format(io.fmt), io.seed, base + 1,
-               io.K, want_n ? 1 : 0, dref, w.dD_R, w.dD_N, w.sd_N};
-  BS_TRY(launch_attn_d(da, st));
+  if (l2) {
+    AttnL2Args la{Oorig, (const u16*)io.dO, io.O_scale, rows, f8_format(io.fmt), io.fwd_mode, io.seed, base,
+                  base + 1, io.K, io.beta, (float*)dO32, dref, w.dD_R, w.dD_N, w.stat, w.stat + 4 * rows,
+                  io.T};
+    BS_TRY(launch_attn_l2(la, st));
+    for (int i = 0; i < (io.d_use ? io.n_pol : 0); ++i) {
+      float* dst = io.d_use + (int64_t)i * 4 * rows;
+      if (io.pol[i] == BS_READ_U)  // U reads the original: its error is zero in every trial
+        BS_TRY(launch_combine(w.stat, nullptr, nullptr, 4 * rows, nullptr, dst, nullptr, st));
+      else
+        BS_TRY(launch_combine(w.stat + (io.pol[i] == BS_READ_R ? 0 : 4 * rows), nullptr, nullptr, 4 * rows, dst,
+                              nullptr, nullptr, st));
+    }
+  } else {
+    AttnDArgs da{Oorig, (const u16*)io.dO, io.dO32, O_codes, io.O_scale, rows, f8_format(io.fmt), io.seed, base + 1,
+                 io.K, want_n ? 1 : 0, dref, w.dD_R, w.dD_N, w.sd_N};
+    BS_TRY(launch_attn_d(da, st));
+  }
 
-  if (io.dO32) BS_TRY(launch_attn_split(io.dO32, (int)bh, io.S, (int)Sp, w.dOp, w.dOt, st));
+  if (dO32) BS_TRY(launch_attn_split(dO32, (int)bh, io.S, (int)Sp, w.dOp, w.dOt, st));
   AttnBwdArgs ba{};
   ba.Qt = w.Qt;
   ba.Kt = w.Kt;
@@ -121,13 +148,13 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   ba.K = (const u16*)io.Kt;
   ba.V = (const u16*)io.V;
   ba.dO = (const u16*)io.dO;
-  ba.dO32 = io.dO32;
+  ba.dO32 = dO32;
   ba.m = w.m;
   ba.l = w.l;
   ba.D_ref = dref;
   ba.dD_R = want_r ? w.dD_R : nullptr;
   ba.dD_N = want_n ? w.dD_N : nullptr;
-  ba.sd_N = want_n ? w.sd_N : nullptr;
+  ba.sd_N = (want_n && !l2) ? w.sd_N : nullptr;
   ba.S = io.S;
   ba.causal = io.causal;
   ba.ntrial = io.K;

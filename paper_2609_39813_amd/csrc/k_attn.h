@@ -31,6 +31,27 @@ struct AttnDArgs {
   float *D_ref, *dD_R, *dD_N, *sd_N;  // [rows]
 };
 
+// Level-2 averaging at the D use: trial k rounds O anew (trial k, use_fwd) and its incoming
+// gradient is g_k = dO + beta r_k, r_k the forward's rounding error; a new rounding r'_k uses
+// (trial k, use_n). Per row: the means over trials of D_ref and of the R and N errors, their
+// mean-error parts, couplings and se, and the paired statistic T; per element the mean g.
+struct AttnL2Args {
+  const float* O;         // original output, fp32 [rows][64]
+  const u16* dO;          // bf16 [rows][64]
+  const float* scale;     // device s of the store
+  int64_t rows;
+  F8 f;
+  int fwd_mode;
+  uint64_t seed;
+  uint32_t use_fwd, use_n;
+  int K;
+  float beta;
+  float* dO_mean;         // [rows][64] mean incoming gradient
+  float *D_ref, *dD_R, *dD_N;  // [rows] means over trials
+  float *stat_R, *stat_N; // nullable [4][rows]: mean error, its mean-error part, coupling, se
+  float* T;               // nullable [2][rows]: mean and se of the paired statistic
+};
+
 struct AttnBwdArgs {
   const u16 *Q, *K, *V, *dO;
   const float* dO32;  // nullable: fp32 incoming gradient (enters as three exact bf16 terms)
@@ -55,6 +76,7 @@ struct AttnBwdArgs {
 
 bs_status launch_attn_fwd(const AttnArgs& a, int B, int H, hipStream_t st);
 bs_status launch_attn_d(const AttnDArgs& a, hipStream_t st);
+bs_status launch_attn_l2(const AttnL2Args& a, hipStream_t st);
 // X_i^T [BH][64][Sp] (zero past S) of n <= 4 bf16 X_i [BH][S][64] (16-byte aligned)
 bs_status launch_attn_transpose(const u16* const* X, u16* const* Xt, int n, int BH, int S, int Sp, hipStream_t st);
 // the three bf16 planes of an fp32 incoming gradient [BH][S][64] and their transposes

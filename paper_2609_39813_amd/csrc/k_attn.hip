@@ -625,6 +625,194 @@ bs_status launch_attn_fwd(const AttnArgs& a, int B, int H, hipStream_t st) {
   return BS_OK;
 }
 
+// ------------------------------------------------------------------------------------
+// Level-2 D use, one row per 4 lanes (16 elements per lane). Per element, with the bracket of
+// y = fl32(O/s) (sign sg, lower magnitude mi step): A = s sg mi step - O (fp64, exact) and
+// w = s sg step; trial k's forward rounding error is r_k = A + u_k w and a new rounding's is
+// r'_k = A + u'_k w (u, u' the up-decisions; for an RNE forward u_k is the fixed RNE decision).
+// With g_k = dO + beta r_k:
+//   R error  rowsum(g_k r_k)  = rowsum(dO A + beta A^2) + sum u_k (dO w + beta (2 A w + w^2))
+//   N error  rowsum(g_k r'_k) = rowsum(dO A + beta A^2) + sum u'_k (dO w + beta A w)
+//                               + sum u_k beta A w + sum u_k u'_k beta w^2
+//   T_k      = beta / 2 sum (u_k xor u'_k) w^2
+// The fixed parts are summed in fp64, the trial parts in fp32 per trial (they hold no
+// trial-independent term) and their mean and SD over trials from fp64 sums shifted by trial 1.
+// ------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void attn_l2_kernel(AttnL2Args a) {
+  constexpr int EPL = 16;
+  const int64_t row = (int64_t)blockIdx.x * 64 + (threadIdx.x >> 2);
+  const int sub = threadIdx.x & 3;
+  const bool ok = row < a.rows;
+  const int64_t e0 = row * AT + EPL * sub;
+  const float s = *a.scale;
+  const double rs = 1.0 / (double)s;
+  const double beta = a.beta;
+  // one element's bracket terms: A = s sg mi step - O (fp64, exact) and w = s sg step
+  auto terms = [&](float o, double& A, double& w, Bracket& b) {
+    const float y = div_scale(o, rs);
+    b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
+    const double sg = signbit(y) ? -1.0 : 1.0;
+    w = (double)s * sg * (double)f8_step(b);
+    A = (double)s * sg * (double)b.mi * (double)f8_step(b) - (double)o;
+  };
+  auto load4 = [&](int j, float (&ov)[4], float (&dv)[4]) {
+    const int64_t e = e0 + 4 * j;
+    const float4 o4 = *(const float4*)(a.O + e);
+    const uint2 d2 = *(const uint2*)(a.dO + e);
+    ov[0] = o4.x; ov[1] = o4.y; ov[2] = o4.z; ov[3] = o4.w;
+    dv[0] = bf16_to_f32((u16)(d2.x & 0xFFFF));
+    dv[1] = bf16_to_f32((u16)(d2.x >> 16));
+    dv[2] = bf16_to_f32((u16)(d2.y & 0xFFFF));
+    dv[3] = bf16_to_f32((u16)(d2.y >> 16));
+  };
+  // trial coefficients: R gains cR where u_k = 1; N gains cN1 where u'_k = 1, cN2 where
+  // u_k = 1 and cN3 where both are; T gains cN3 / 2 where they differ
+  float cR[EPL], cN1[EPL], cN2[EPL], cN3[EPL];
+  uint32_t F[EPL];
+  uint32_t ufix = 0u;  // bit i: RNE decision of element i
+  double fixed = 0.0;
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    cR[q] = cN1[q] = cN2[q] = cN3[q] = 0.0f;
+    F[q] = 0u;
+  }
+  if (ok) {
+#pragma unroll
+    for (int j = 0; j < EPL / 4; ++j) {
+      float ov[4], dv[4];
+      load4(j, ov, dv);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = 4 * j + q;
+        double A, w;
+        Bracket b;
+        terms(ov[q], A, w, b);
+        fixed += ((double)dv[q] + beta * A) * A;
+        cN1[i] = (float)((double)dv[q] * w + beta * A * w);
+        cN2[i] = (float)(beta * A * w);
+        cN3[i] = (float)(beta * w * w);
+        cR[i] = (float)((double)dv[q] * w + beta * (2.0 * A * w + w * w));
+        F[i] = b.F;
+        ufix |= (a.fwd_mode == BS_RNE ? rne_up(b) : 0u) << i;
+      }
+    }
+  }
+  auto rowsum = [&](auto v) {
+    v += __shfl_xor(v, 1, 64);
+    v += __shfl_xor(v, 2, 64);
+    return v;
+  };
+  // per element: up-counts of the forward's and the new roundings over the trials
+  uint32_t n[EPL], np[EPL];
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) n[q] = np[q] = 0u;
+  double s1[3] = {0.0, 0.0, 0.0}, d1[3] = {0.0, 0.0, 0.0}, d2[3] = {0.0, 0.0, 0.0};
+  const uint64_t g0 = (uint64_t)(e0 >> 2);
+  for (int k = 1; k <= a.K; ++k) {
+    float tR = 0.0f, tN = 0.0f, tT = 0.0f;
+#pragma unroll
+    for (int j = 0; j < EPL / 4; ++j) {
+      const Philox4 pn = philox_group(a.seed, g0 + j, (uint32_t)k, a.use_n);
+      const uint32_t Rn[4] = {pn.w0, pn.w1, pn.w2, pn.w3};
+      uint32_t uf[4];
+      if (a.fwd_mode == BS_SR) {
+        const Philox4 pf = philox_group(a.seed, g0 + j, (uint32_t)k, a.use_fwd);
+        const uint32_t Rf[4] = {pf.w0, pf.w1, pf.w2, pf.w3};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) uf[q] = sr_up(F[4 * j + q], Rf[q]);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) uf[q] = (ufix >> (4 * j + q)) & 1u;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = 4 * j + q;
+        const uint32_t u = uf[q], up = sr_up(F[i], Rn[q]);
+        n[i] += u;
+        np[i] += up;
+        tR += u ? cR[i] : 0.0f;
+        tN += up ? cN1[i] : 0.0f;
+        tN += u ? cN2[i] : 0.0f;
+        tN += (u & up) ? cN3[i] : 0.0f;
+        tT += (u ^ up) ? cN3[i] : 0.0f;
+      }
+    }
+    const float t3[3] = {rowsum(tR), rowsum(tN), 0.5f * rowsum(tT)};
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+      if (k == 1) s1[c] = t3[c];
+      const double dl = (double)t3[c] - s1[c];
+      d1[c] += dl;
+      d2[c] += dl * dl;
+    }
+  }
+  const double iK = 1.0 / a.K;
+  double mean[3], se[3];
+#pragma unroll
+  for (int c = 0; c < 3; ++c) {
+    mean[c] = s1[c] + d1[c] * iK;
+    const double var = a.K > 1 ? fmax(d2[c] - d1[c] * d1[c] * iK, 0.0) / (a.K - 1) : 0.0;
+    se[c] = sqrt(var * iK);
+  }
+  // means over trials per element (mean r = A + (n / K) w), the reference D and the split
+  double dref = 0.0, meR = 0.0, meN = 0.0;
+  if (ok) {
+#pragma unroll
+    for (int j = 0; j < EPL / 4; ++j) {
+      float ov[4], dv[4], gm[4];
+      load4(j, ov, dv);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = 4 * j + q;
+        double A, w;
+        Bracket b;
+        terms(ov[q], A, w, b);
+        const double mr = A + (double)n[i] * iK * w, mrp = A + (double)np[i] * iK * w;
+        const double mg = (double)dv[q] + beta * mr;
+        dref += mg * (double)ov[q];
+        meR += mr * mg;
+        meN += mrp * mg;
+        gm[q] = (float)mg;
+      }
+      *(float4*)(a.dO_mean + e0 + 4 * j) = make_float4(gm[0], gm[1], gm[2], gm[3]);
+    }
+  }
+  dref = rowsum(dref);
+  meR = rowsum(meR);
+  meN = rowsum(meN);
+  fixed = rowsum(fixed);
+  if (ok && sub == 0) {
+    const double mR = fixed + mean[0], mN = fixed + mean[1];
+    a.D_ref[row] = (float)dref;
+    a.dD_R[row] = (float)mR;
+    a.dD_N[row] = (float)mN;
+    if (a.stat_R) {
+      a.stat_R[row] = (float)mR;
+      a.stat_R[a.rows + row] = (float)meR;
+      a.stat_R[2 * a.rows + row] = (float)(mR - meR);
+      a.stat_R[3 * a.rows + row] = (float)se[0];
+    }
+    if (a.stat_N) {
+      a.stat_N[row] = (float)mN;
+      a.stat_N[a.rows + row] = (float)meN;
+      a.stat_N[2 * a.rows + row] = (float)(mN - meN);
+      a.stat_N[3 * a.rows + row] = (float)se[1];
+    }
+    if (a.T) {
+      a.T[row] = (float)mean[2];
+      a.T[a.rows + row] = (float)se[2];
+    }
+  }
+}
+
+bs_status launch_attn_l2(const AttnL2Args& a, hipStream_t st) {
+  if (a.rows <= 0) return BS_OK;
+  ProfScope prof("attn_l2", st);
+  attn_l2_kernel<<<(unsigned)((a.rows + 63) / 64), 256, 0, st>>>(a);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
 bs_status launch_attn_d(const AttnDArgs& a, hipStream_t st) {
   if (a.rows <= 0) return BS_OK;
   ProfScope prof("attn_d", st);
