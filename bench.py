@@ -177,6 +177,26 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
     del Q, K, V, dO, ws
     torch.cuda.empty_cache()
 
+    # level-2 averaging at the same attention shape: the forward's rounding resampled per trial,
+    # incoming gradient dO + r_k (App. C.1's split, App. E.4's paired statistic)
+    Q, K, V, dO = (t_.to(dev) for t_ in synth.attention_inputs(cfg3["B"], cfg3["H"], cfg3["S"], cfg3["dh"],
+                                                               cfg3["dtype"], 3))
+    ws = bsp.attn_workspace(cfg3["B"], cfg3["H"], cfg3["S"], cfg3["dh"], 3, cfg3["K"], dev)
+    wall, t = _timed(bsp, torch, lambda: bsp.attn_level2_policy(Q, K, V, dO, causal=True, policies=cfg3["policies"],
+                                                                 K=cfg3["K"], seed=cfg3["seed"], fwd_mode="sr",
+                                                                 beta=1.0, ws=ws),
+                     ("attn_l2", "attn_bwd", "attn_fwd", "attn_prep", "amax", "quantize"), reps)
+    et = cfg3["B"] * cfg3["H"] * cfg3["S"] * cfg3["dh"] * cfg3["K"]     # element-trials, 2 draws each
+    l2_s = t["attn_l2"] / 1e3
+    out["attention_level2_b4_h16_s1024_d64"] = {
+        "call_ms": round(wall * 1e3, 4), "policy_trials_per_s": round(len(cfg3["policies"]) * cfg3["K"] / wall, 1),
+        "kernel_ms": {k: round(v, 4) for k, v in t.items()},
+        "l2_Gelement_trials_per_s": round(et / l2_s / 1e9, 1),
+        "work": f"K = {cfg3['K']} trials, each drawing the forward's rounding and a new rounding of every element "
+                "of O (2 Philox words per element-trial), then one multi-D backward on the mean incoming gradient"}
+    del Q, K, V, dO, ws
+    torch.cuda.empty_cache()
+
     # the FP8 store of attention probabilities and its two uses (every policy of App. B's table)
     cp = synth.PSTORE
     Q, K, V, dO = (t_.to(dev) for t_ in synth.attention_inputs(cp["B"], cp["H"], cp["S"], cp["dh"], cp["dtype"],
