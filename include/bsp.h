@@ -205,6 +205,29 @@ bs_status bs_attn_level2_policy(const void* Q, const void* Kt, const void* V, co
                                 size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------
+ * bs_logsoftmax_reuse_check -- the log-softmax operator test (Sec. 4.3; App. C.5), in fp64.
+ * The operator's backward returns h - exp(S) (1^T h) from a saved output S. Per trial k =
+ * 1..K the saved output is S = l + r with l = log_softmax(logits) per row and r_j = +eps where
+ * the element's Philox word (trial k, use store_id*256; element row*C + j) is >= 2^31, -eps
+ * otherwise; reuse reads S, an independent copy reads l + r' (use store_id*256 + 1). With p =
+ * exp(l), g the returned gradient and g* the operator's gradient from l, the trial's statistic
+ * is the mean over rows and classes of (g - g*)/p for: [0] the likelihood (h = -e_y, y =
+ * target) with reuse, [1] the likelihood with the independent copy, [2] the constructed loss
+ * (h = r) with reuse, [3] the constructed loss with the independent copy. calibrate != 0
+ * divides the reconstruction exp(S) by cosh(eps) (LS5a/LS5b).
+ *
+ *   logits [rows, C] fp64; target [rows] int32 (a value outside [0, C) matches no class);
+ *   rows >= 1; C >= 4 a multiple of 4; 0 < eps < 1; K in [1, 2^20].
+ *   stats [4][2] fp64 (device): mean over the K trials and its se (sample SD / sqrt(K)).
+ *   ws: bs_logsoftmax_check_workspace_size(rows, C, K) bytes (0 for shapes the call rejects).
+ * Returns BS_EINVAL for a NULL pointer or eps, K out of range; BS_ESHAPE for C.
+ * ---------------------------------------------------------------------------------- */
+size_t bs_logsoftmax_check_workspace_size(int64_t rows, int C, int K);
+bs_status bs_logsoftmax_reuse_check(const double* logits, const int32_t* target, int64_t rows, int C, double eps,
+                                    int K, uint64_t seed, uint32_t store_id, int calibrate, double* stats, void* ws,
+                                    size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
  * bs_attn_pstore_policy -- attention whose probabilities P pass through an FP8 store, and
  * the two uses of that store in the backward: the gradient of V and the softmax's backward
  * (App. B.2, Eq. app-ref and Eq. app-errors; App. B.3; App. B.4; Table app-theory-errors).
@@ -371,7 +394,7 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* w, cons
  *   events on the launch stream around each launch of the instrumented kernels
  *   ("fresh_count", "fresh_count_se", "fresh_count_kappa", "amax", "quantize", "gemm",
  *   "rmsnorm_fwd", "attn_fwd", "attn_bwd", "attn_l2", "pstore_fwd", "pstore_rows", "pstore_dq",
- *   "pstore_dkv");
+ *   "pstore_dkv", "lsm_prep", "lsm_trial");
  *   bs_profile_enable(0) stops and frees them. bs_profile_read waits for the recorded
  *   events of `kernel` (NULL: all) and returns their summed elapsed time and count.
  *   Return values are bs_status codes.

@@ -75,6 +75,9 @@ _ps = _sig("bs_attn_pstore_policy", _int,
 _attn2 = _sig("bs_attn_level2_policy", _int,
               [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _vp, _int, _int, _f32, ctypes.POINTER(_int), _int,
                _int, _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, _vp, _vp, _vp, _vp, _sz, _vp])
+_lsm_ws = _sig("bs_logsoftmax_check_workspace_size", _sz, [_i64, _int, _int])
+_lsm = _sig("bs_logsoftmax_reuse_check", _int,
+            [_vp, _vp, _i64, _int, ctypes.c_double, _int, _u64, _u32, _int, _vp, _vp, _sz, _vp])
 _lin_ws = _sig("bs_linear_bwd_workspace_size", _sz, [_i64, _i64, _i64, _int, _int])
 _lin = _sig("bs_linear_bwd_policy", _int,
             [_vp, _vp, _vp, _int, _i64, _i64, _i64, _int, ctypes.POINTER(_int), _int, _int, _u64, _u32, _vp, _vp,
@@ -120,7 +123,8 @@ def profile_read(kernel=None):
 
 EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
             "bs_policy_bias_estimate", "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
-            "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_attn_pstore_workspace_size", "bs_attn_pstore_policy", "bs_attn_level2_policy", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
+            "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_attn_pstore_workspace_size", "bs_attn_pstore_policy", "bs_attn_level2_policy",
+            "bs_logsoftmax_check_workspace_size", "bs_logsoftmax_reuse_check", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
             "bs_decoder_layer_workspace_size", "bs_decoder_layer_policy", "bs_profile_enable", "bs_profile_read"]
 
 
@@ -323,6 +327,26 @@ def attn_level2_policy(Q, Kt, V, dO, *, causal=True, scale=None, O=None, fmt="e4
                   _p(out["T"]), _p(out["diag"]), _p(ws), ws.numel(), _stream()), "bs_attn_level2_policy")
     out["dQ"], out["dK"] = eq, ek
     return out
+
+
+LSM_STATS = ("likelihood_reuse", "likelihood_independent", "constructed_reuse", "constructed_independent")
+
+
+def logsoftmax_reuse_check(logits, target, *, eps=0.1, K=4096, seed=0, store_id=0, calibrate=False, ws=None):
+    """The log-softmax operator test (bs_logsoftmax_reuse_check): {statistic: (mean, se)} over K trials."""
+    _dev_check(logits, target)
+    if logits.dtype != torch.float64 or target.dtype != torch.int32:
+        raise ValueError("logits must be fp64 and target int32")
+    rows, C = logits.shape
+    stats = torch.empty(4, 2, dtype=torch.float64, device=logits.device)
+    if ws is None:
+        n = _lsm_ws(rows, C, K)
+        if n == 0:
+            raise BspError(2, "bs_logsoftmax_check_workspace_size")
+        ws = _workspace(n, logits.device)
+    _check(_lsm(_p(logits), _p(target), rows, C, eps, K, seed, store_id, int(calibrate), _p(stats), _p(ws), ws.numel(),
+                _stream()), "bs_logsoftmax_reuse_check")
+    return stats
 
 
 def attn_workspace(B, H, S, dh, n_pol, K, device):

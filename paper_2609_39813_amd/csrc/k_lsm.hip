@@ -1,0 +1,182 @@
+// The log-softmax operator test (Sec. 4.3; App. C.5) on the GPU, in fp64 as the paper's test:
+// the operator's backward h - exp(S) (1^T h) reads a saved output S = l + r (r_j = +-eps) under
+// reuse, or l + r' with r' drawn anew; per trial the statistic is the mean over rows and classes
+// of (g - g*) / p under the likelihood (h = -e_y) and the constructed loss (h = r).
+//
+// One wave per (row, chunk of trials); a lane takes groups of 4 consecutive classes (one Philox
+// call per group, draw and trial). Per trial the wave first sums r over the row (the constructed
+// loss's 1^T h), then forms the four errors literally (g and g* in fp64, then / p). Per-trial
+// row sums go to the workspace; a second kernel sums them over rows in row order and takes the
+// mean and se over trials.
+#include "bsp_kernels.h"
+
+namespace bsp {
+
+namespace {
+
+constexpr int LSM_TCH = 32;  // trials per wave
+
+__device__ __forceinline__ double wsum(double v) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// l = z - max - log(sum exp(z - max)) per row, one wave per row
+__global__ __launch_bounds__(64) void lsm_prep_kernel(const double* __restrict__ z, int64_t rows, int C,
+                                                      double* __restrict__ l) {
+  const int64_t row = blockIdx.x;
+  const int lane = threadIdx.x;
+  const double* zr = z + row * C;
+  double m = -INFINITY;
+  for (int j = lane; j < C; j += 64) m = fmax(m, zr[j]);
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) m = fmax(m, __shfl_xor(m, off, 64));
+  double se = 0.0;
+  for (int j = lane; j < C; j += 64) se += exp(zr[j] - m);
+  const double lse = m + log(wsum(se));
+  for (int j = lane; j < C; j += 64) l[row * C + j] = zr[j] - lse;
+}
+
+// per (row, trial): the row sums of the four entry errors, [4][K][rows]
+__global__ __launch_bounds__(64) void lsm_trial_kernel(const double* __restrict__ l, const int32_t* __restrict__ y,
+                                                       int64_t rows, int C, double eps, double cal, int K,
+                                                       uint64_t seed, uint32_t use_r, uint32_t use_p,
+                                                       double* __restrict__ part) {
+  const int64_t row = blockIdx.x;
+  const int lane = threadIdx.x;
+  const double* lr = l + row * C;
+  const int yt = y[row];
+  const int ngroups = C / 4;
+  const int k_end = min(K, (int)(blockIdx.y + 1) * LSM_TCH);
+  for (int k = blockIdx.y * LSM_TCH; k < k_end; ++k) {
+    const uint32_t trial = (uint32_t)(k + 1);
+    // 1^T r over the row
+    double sr = 0.0;
+    for (int gi = lane; gi < ngroups; gi += 64) {
+      const Philox4 pr = philox_group(seed, (uint64_t)(row * C) / 4 + gi, trial, use_r);
+      const uint32_t R[4] = {pr.w0, pr.w1, pr.w2, pr.w3};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sr += R[q] >= 0x80000000u ? eps : -eps;
+    }
+    sr = wsum(sr);
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int gi = lane; gi < ngroups; gi += 64) {
+      const uint64_t grp = (uint64_t)(row * C) / 4 + gi;
+      const Philox4 pr = philox_group(seed, grp, trial, use_r);
+      const Philox4 pp = philox_group(seed, grp, trial, use_p);
+      const uint32_t R[4] = {pr.w0, pr.w1, pr.w2, pr.w3}, Rp[4] = {pp.w0, pp.w1, pp.w2, pp.w3};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = 4 * gi + q;
+        const double lj = lr[j], p = exp(lj);
+        const double r = R[q] >= 0x80000000u ? eps : -eps, rp = Rp[q] >= 0x80000000u ? eps : -eps;
+        const double er = exp(lj + r) / cal, erp = exp(lj + rp) / cal;
+        // likelihood: h = -e_y, 1^T h = -1
+        const double hl = j == yt ? -1.0 : 0.0;
+        const double gl_star = hl + p;
+        acc[0] += ((hl + er) - gl_star) / p;
+        acc[1] += ((hl + erp) - gl_star) / p;
+        // constructed: h = r, 1^T h = sr
+        const double gc_star = r - p * sr;
+        acc[2] += ((r - er * sr) - gc_star) / p;
+        acc[3] += ((r - erp * sr) - gc_star) / p;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const double v = wsum(acc[c]);
+      if (lane == 0) part[((int64_t)c * K + k) * rows + row] = v;
+    }
+  }
+}
+
+// per statistic: t_k = sum over rows (row order) / (rows C); mean and se over trials
+__global__ __launch_bounds__(256) void lsm_reduce_kernel(const double* __restrict__ part, int64_t rows, int C, int K,
+                                                         double* __restrict__ stats) {
+  const int c = blockIdx.x;
+  __shared__ double red[256];
+  double s1 = 0.0, s2 = 0.0, t0 = 0.0;
+  // trial 0's value, as the shift of the sums (every thread needs it)
+  for (int64_t i = 0; i < rows; ++i) t0 += part[(int64_t)c * K * rows + i];
+  t0 /= (double)rows * C;
+  for (int k = threadIdx.x; k < K; k += blockDim.x) {
+    double t = 0.0;
+    for (int64_t i = 0; i < rows; ++i) t += part[((int64_t)c * K + k) * rows + i];
+    const double d = t / ((double)rows * C) - t0;
+    s1 += d;
+    s2 += d * d;
+  }
+  // fixed-order block sums
+  red[threadIdx.x] = s1;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
+    __syncthreads();
+  }
+  const double S1 = red[0];
+  __syncthreads();
+  red[threadIdx.x] = s2;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double S2 = red[0];
+    const double mean = t0 + S1 / K;
+    const double var = K > 1 ? fmax(S2 - S1 * S1 / K, 0.0) / (K - 1) : 0.0;
+    stats[2 * c] = mean;
+    stats[2 * c + 1] = sqrt(var / K);
+  }
+}
+
+}  // namespace
+
+size_t lsm_ws_size(int64_t rows, int C, int K) {
+  if (rows < 1 || C < 4 || (C & 3) || K < 1) return 0;
+  Carver c;
+  c.take<double>(rows * C);
+  c.take<double>((int64_t)4 * K * rows);
+  return c.used();
+}
+
+}  // namespace bsp
+
+using namespace bsp;
+
+extern "C" {
+
+size_t bs_logsoftmax_check_workspace_size(int64_t rows, int C, int K) { return lsm_ws_size(rows, C, K); }
+
+bs_status bs_logsoftmax_reuse_check(const double* logits, const int32_t* target, int64_t rows, int C, double eps,
+                                    int K, uint64_t seed, uint32_t store_id, int calibrate, double* stats, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  if (!logits || !target || !stats) return BS_EINVAL;
+  if (rows < 1 || K < 1 || K > (1 << 20) || !(eps > 0.0) || !(eps < 1.0)) return BS_EINVAL;
+  if (C < 4 || (C & 3) || rows > 0x7FFFFFFF) return BS_ESHAPE;
+  const size_t need = lsm_ws_size(rows, C, K);
+  if (!ws || ((uintptr_t)ws & 255) || ws_bytes < need) return BS_EWORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  Carver c(ws, ws_bytes);
+  double* l = c.take<double>(rows * C);
+  double* part = c.take<double>((int64_t)4 * K * rows);
+  {
+    ProfScope prof("lsm_prep", st);
+    lsm_prep_kernel<<<(unsigned)rows, 64, 0, st>>>(logits, rows, C, l);
+    BS_CHECK_LAUNCH();
+  }
+  const uint32_t base = store_id * 256u;
+  {
+    ProfScope prof("lsm_trial", st);
+    const dim3 grid((unsigned)rows, (unsigned)((K + LSM_TCH - 1) / LSM_TCH));
+    lsm_trial_kernel<<<grid, 64, 0, st>>>(l, target, rows, C, eps, calibrate ? cosh(eps) : 1.0, K, seed, base,
+                                          base + 1, part);
+    BS_CHECK_LAUNCH();
+  }
+  lsm_reduce_kernel<<<4, 256, 0, st>>>(part, rows, C, K, stats);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+}  // extern "C"

@@ -57,3 +57,10 @@ def test_decoder_layer_workspace_rejects_bad_shapes():
     # sized for the whole layer: at least the fp32 activations and the four stores' estimates
     T, d, F = 48, 128, 256
     assert f(2, 24, d, 2, F, 4) >= 4 * T * (10 * d + 6 * F)
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="libbsp.so not built")
+def test_binding_signs_every_declared_call():
+    """The Python binding loads (its ctypes signatures resolve) and names every declared call."""
+    from paper_2609_39813_amd import bsp
+    assert sorted(bsp.EXPORTED) == declared()
