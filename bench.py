@@ -222,6 +222,25 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
     del Q, K, V, dO, ws
     torch.cuda.empty_cache()
 
+    # the log-softmax operator test at the paper's configuration (fp64: eps = 0.1, 128 classes,
+    # 64 rows, 4096 trials) and at a vocabulary-sized row (32768 classes, 512 rows, 64 trials)
+    for rows_, C_, K_, tag in ((64, 128, 4096, "logsoftmax_check_64x128_k4096"),
+                               (512, 32768, 64, "logsoftmax_check_512x32768_k64")):
+        gz = torch.Generator().manual_seed(7)
+        z = (torch.randn(rows_, C_, generator=gz, dtype=torch.float64) * 2.0).to(dev)
+        yv = torch.randint(0, C_, (rows_,), generator=gz, dtype=torch.int32).to(dev)
+        ws = torch.empty(max(bsp._lsm_ws(rows_, C_, K_), 256), dtype=torch.uint8, device=dev)
+        wall, t = _timed(bsp, torch, lambda: bsp.logsoftmax_reuse_check(z, yv, eps=0.1, K=K_, seed=7, ws=ws),
+                         ("lsm_prep", "lsm_trial"), reps)
+        et = rows_ * C_ * K_
+        st_ = bsp.logsoftmax_reuse_check(z, yv, eps=0.1, K=K_, seed=7, ws=ws).cpu().tolist()
+        out[tag] = {"call_ms": round(wall * 1e3, 4), "kernel_ms": {k: round(v, 4) for k, v in t.items()},
+                    "Gelement_trials_per_s": round(et / (t["lsm_trial"] / 1e3) / 1e9, 2),
+                    "stats_mean_se": dict(zip(bsp.LSM_STATS, [[round(a, 8), round(b, 8)] for a, b in st_])),
+                    "work": f"{et} element-trials in fp64 (3 Philox words, 3 exp per element-trial)"}
+        del z, yv, ws
+    torch.cuda.empty_cache()
+
     # one decoder layer with four stores and the per-use check of each
     cfg5 = synth.CONFIGS[5]
     (x, p, dOut), (B, S5, H) = synth.decoder_inputs(cfg5["B"], cfg5["S"], cfg5["d"], cfg5["H"], cfg5["F"], config=5)
