@@ -144,6 +144,43 @@ bs_status bs_rmsnorm_linear_fwd_bwd(const void* X, const float* gain, const void
                                     size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------
+ * bs_rmsnorm_linear_grid_fwd_bwd -- RMSNorm feeding a Linear through the paper's own store of
+ * the normalized output: a per-token b-bit uniform grid with stochastic rounding (App. D.4),
+ * and the eight policies of its Table "Store policies" (Sec. 3.1, Eq. norm-uses).
+ *
+ * Forward as bs_rmsnorm_linear_fwd_bwd up to u (same fixed fp32 order). Store, per token t:
+ * s_t = fl32(max_j |u_tj| / M) with M = 2^(bits-1) - 1 (s_t = 1 for an all-zero row);
+ * y = fl32(u / s_t); |y| > M is clamped and counted (diag.n_saturated); with lo = floor(|y|)
+ * and F = floor((|y| - lo) 2^32) the code rounds up iff R + F >= 2^32 (R the element's Philox
+ * word: trial 0, use store_id*256; element t*d + j); code q = sign * (lo + up) in [-M, M];
+ * u_q = fl32(q s_t); Y = u_q W. Backward: du = dY W^T; dW = u_W^T dY; dgain = sum_t z_g du,
+ * dX with the unrounded z. The new rounding u_f (trials 1..K, use store_id*256 + 1, the same
+ * law) is read by both uses. Policies (gain use first): the gain use reads z (U), u_q/gain (R)
+ * or u_f/gain (N); the weight use reads u (U), u_q (R), u_f (N) or u_q + (u_f - u) (R+eps).
+ * U/R is the reference: dgain_ref = sum z du, dW_ref = u_q^T dY.
+ *
+ *   X [T,d] dt, gain [d] fp32, W [d,n] dt, dY [T,n] dt (dt fp32 or bf16); 1 <= T <= 2^24 - 256;
+ *   d, n multiples of 8, d <= 8192; bits in [2, 8]; K in [1, 4096]; pol (host) [n_pol] in [1, 16].
+ *   Y [T,n] fp32 (nullable); u_codes [T,d] int8; u_step [T] fp32; dgain_ref [d], dW_ref [d,n],
+ *   dX_ref [T,d] fp32; estimates dgain [n_pol][d], dW [n_pol][d*n] (se must be NULL:
+ *   BS_EUNSUPPORTED otherwise). diag: nonfinite, n_saturated, amax = max |u| (scale unused).
+ *   ws: bs_rmsnorm_linear_grid_workspace_size(T, d, n) bytes.
+ * ---------------------------------------------------------------------------------- */
+typedef enum { BS_WREAD_U = 0, BS_WREAD_R = 1, BS_WREAD_N = 2, BS_WREAD_R_EPS = 3 } bs_weight_read;
+typedef struct {
+  bs_read gain_use;
+  bs_weight_read weight_use;
+} bs_grid_policy;
+
+size_t bs_rmsnorm_linear_grid_workspace_size(int64_t T, int64_t d, int64_t n);
+bs_status bs_rmsnorm_linear_grid_fwd_bwd(const void* X, const float* gain, const void* W, const void* dY, bs_dtype dt,
+                                         int64_t T, int64_t d, int64_t n, float eps, int bits,
+                                         const bs_grid_policy* pol, int n_pol, int K, uint64_t seed,
+                                         uint32_t store_id, float* Y, int8_t* u_codes, float* u_step,
+                                         float* dgain_ref, float* dW_ref, float* dX_ref, bs_est dgain, bs_est dW,
+                                         bs_diag* diag, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
  * bs_attn_bwd_policy -- attention backward whose correction term D reads a stored
  * copy of the output (Sec. 2.1, Eq. dterm; App. D.2).
  *
@@ -394,7 +431,7 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* w, cons
  *   events on the launch stream around each launch of the instrumented kernels
  *   ("fresh_count", "fresh_count_se", "fresh_count_kappa", "amax", "quantize", "gemm",
  *   "rmsnorm_fwd", "attn_fwd", "attn_bwd", "attn_l2", "pstore_fwd", "pstore_rows", "pstore_dq",
- *   "pstore_dkv", "lsm_prep", "lsm_trial");
+ *   "pstore_dkv", "lsm_prep", "lsm_trial", "grid_store", "grid_fresh");
  *   bs_profile_enable(0) stops and frees them. bs_profile_read waits for the recorded
  *   events of `kernel` (NULL: all) and returns their summed elapsed time and count.
  *   Return values are bs_status codes.

@@ -84,12 +84,14 @@ def value(q, s):
     return (np.asarray(q, dtype=np.float32) * np.asarray(s, dtype=np.float32)[..., None]).astype(np.float32)
 
 
-def store(u, bits, seed, trial, use):
-    """(codes q, steps s, values fl32(q s), clamp count) of one stochastic rounding of u."""
+def store(u, bits, seed, trial, use, cols=None):
+    """(codes q, steps s, values fl32(q s), clamp count) of one stochastic rounding of u (of its
+    columns ``cols`` only, if given; the steps always come from whole rows)."""
     s = step_of(u, bits)
-    lo, F, neg, nsat = bracket(u, s, bits)
     T, d = np.asarray(u).shape
-    elem = np.arange(T * d, dtype=np.uint64).reshape(T, d)
+    cols = np.arange(d) if cols is None else np.asarray(cols)
+    lo, F, neg, nsat = bracket(np.asarray(u)[:, cols], s, bits)
+    elem = (np.arange(T, dtype=np.uint64)[:, None] * np.uint64(d) + cols.astype(np.uint64)[None, :])
     q = rounded(lo, F, neg, philox.words(seed, trial, use, elem))
     return q.astype(np.int32), s, value(q, s), nsat
 
@@ -109,8 +111,13 @@ def draws(code):
     return lg == "N" or lw in ("N", "R+e")
 
 
-def check(X, gamma, W, dY, *, bits=6, eps=1e-5, policies=POLICIES, K=16, seed=0, store_id=0):
-    """Reference gradients and each policy's trial statistics (mean, bias, se) of dgamma, dW."""
+def check(X, gamma, W, dY, *, bits=6, eps=1e-5, policies=POLICIES, K=16, seed=0, store_id=0, dw_rows=None,
+          dw_cols=None, gain_cols=None, full=True):
+    """Reference gradients and each policy's trial statistics (mean, bias, se) of dgamma, dW.
+
+    dw_rows / dw_cols select the entries of dW (rows i, columns j) and gain_cols those of dgamma
+    to compute; None means all (the store is always of the whole tensor). full=False skips Y and
+    dX_ref and forms du only on the selected columns."""
     X = np.asarray(X, dtype=np.float32)
     g64 = np.asarray(gamma, dtype=np.float32).astype(np.float64)
     W64 = np.asarray(W, dtype=np.float32).astype(np.float64)
@@ -118,17 +125,37 @@ def check(X, gamma, W, dY, *, bits=6, eps=1e-5, policies=POLICIES, K=16, seed=0,
     z, u, rstd = rmsnorm_fp32(X, gamma, eps)
     base = store_id * 256
     q, s, uq, nsat = store(u, bits, seed, 0, base)
-    du = dY64 @ W64.T
     uq64 = uq.astype(np.float64)
+    T, d = u.shape
+    rows = np.arange(d) if dw_rows is None else np.asarray(dw_rows)
+    cols = np.arange(dY64.shape[1]) if dw_cols is None else np.asarray(dw_cols)
+    gcols = np.arange(d) if gain_cols is None else np.asarray(gain_cols)
+    if full:
+        du = dY64 @ W64.T
+    else:                                   # du on the selected columns only
+        du = np.zeros((T, d))
+        sel = np.union1d(rows, gcols)
+        du[:, sel] = dY64 @ W64[sel].T
     out = {"codes": q, "step": s, "uq": uq, "n_saturated": nsat, "u": u, "z": z, "du": du,
-           "Y": uq64 @ W64, "dW_ref": uq64.T @ dY64, "dgamma_ref": (z.astype(np.float64) * du).sum(axis=0),
-           "dX_ref": norm_backward(z, rstd, g64 * du)}
-    fresh = [store(u, bits, seed, k, base + 1)[2] for k in range(1, K + 1)] if any(draws(c) for c in policies) else []
+           "dW_ref": uq64[:, rows].T @ dY64[:, cols],
+           "dgamma_ref": (z.astype(np.float64)[:, gcols] * du[:, gcols]).sum(axis=0)}
+    if full:
+        out["Y"] = uq64 @ W64
+        out["dX_ref"] = norm_backward(z, rstd, g64 * du)
+    need = np.union1d(rows, gcols)
+    at = {int(j): i for i, j in enumerate(need)}
+    ir, ig = [at[int(j)] for j in rows], [at[int(j)] for j in gcols]
+    fresh = ([store(u, bits, seed, k, base + 1, cols=need)[2] for k in range(1, K + 1)]
+             if any(draws(c) for c in policies) else [])
     for code in policies:
         ntr = K if draws(code) else 1
         dg, dw = [], []
         for k in range(ntr):
-            a, b = policy_grads(code, z, u, uq, fresh[k] if draws(code) else None, gamma, du, dY64)
+            f = fresh[k] if draws(code) else None
+            a, _ = policy_grads(code, z[:, gcols], u[:, gcols], uq[:, gcols], None if f is None else f[:, ig],
+                                gamma[gcols], du[:, gcols], dY64[:, :1])
+            _, b = policy_grads(code, z[:, rows], u[:, rows], uq[:, rows], None if f is None else f[:, ir],
+                                gamma[rows], du[:, rows], dY64[:, cols])
             dg.append(a)
             dw.append(b)
         reps = 1 if draws(code) else K

@@ -78,6 +78,18 @@ _attn2 = _sig("bs_attn_level2_policy", _int,
 _lsm_ws = _sig("bs_logsoftmax_check_workspace_size", _sz, [_i64, _int, _int])
 _lsm = _sig("bs_logsoftmax_reuse_check", _int,
             [_vp, _vp, _i64, _int, ctypes.c_double, _int, _u64, _u32, _int, _vp, _vp, _sz, _vp])
+
+
+class GridPolicy(ctypes.Structure):
+    _fields_ = [("gain_use", _int), ("weight_use", _int)]
+
+
+WEIGHT_READ = {"U": 0, "R": 1, "N": 2, "R+e": 3}
+GRID_POLICIES = ("U/R", "U/U", "U/N", "R/R", "R/N", "N/R", "N/N", "U/R+e")
+_grid_ws = _sig("bs_rmsnorm_linear_grid_workspace_size", _sz, [_i64, _i64, _i64])
+_grid = _sig("bs_rmsnorm_linear_grid_fwd_bwd", _int,
+             [_vp, _vp, _vp, _vp, _int, _i64, _i64, _i64, _f32, _int, ctypes.POINTER(GridPolicy), _int, _int, _u64,
+              _u32, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, _vp, _vp, _sz, _vp])
 _lin_ws = _sig("bs_linear_bwd_workspace_size", _sz, [_i64, _i64, _i64, _int, _int])
 _lin = _sig("bs_linear_bwd_policy", _int,
             [_vp, _vp, _vp, _int, _i64, _i64, _i64, _int, ctypes.POINTER(_int), _int, _int, _u64, _u32, _vp, _vp,
@@ -124,7 +136,8 @@ def profile_read(kernel=None):
 EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
             "bs_policy_bias_estimate", "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
             "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_attn_pstore_workspace_size", "bs_attn_pstore_policy", "bs_attn_level2_policy",
-            "bs_logsoftmax_check_workspace_size", "bs_logsoftmax_reuse_check", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
+            "bs_logsoftmax_check_workspace_size", "bs_logsoftmax_reuse_check",
+            "bs_rmsnorm_linear_grid_workspace_size", "bs_rmsnorm_linear_grid_fwd_bwd", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
             "bs_decoder_layer_workspace_size", "bs_decoder_layer_policy", "bs_profile_enable", "bs_profile_read"]
 
 
@@ -257,6 +270,37 @@ def rmsnorm_linear(X, gain, W, dY, *, eps=1e-5, fmt="e4m3", fwd_mode="rne", poli
                  _p(out["dW_ref"]), _p(out["dX_ref"]), cg, cw, cx, _p(out["diag"]), _p(ws), ws.numel(), _stream()),
            "bs_rmsnorm_linear_fwd_bwd")
     out["dgain"], out["dW"], out["dX"] = eg, ew, ex
+    out["policies"] = list(policies)
+    return out
+
+
+def rmsnorm_linear_grid(X, gain, W, dY, *, bits=6, eps=1e-5, policies=GRID_POLICIES, K=16, seed=0, store_id=0,
+                        want_y=True, ws=None):
+    """RMSNorm -> per-token b-bit grid store -> Linear, and the policies of the paper's table
+    (bs_rmsnorm_linear_grid_fwd_bwd). Policy codes name the gain use first; 'U/R+e' reads
+    u_q + (u_f - u) at the weight use."""
+    _dev_check(X, gain, W, dY)
+    T, d = X.shape
+    n = W.shape[1]
+    dev = X.device
+    pol = (GridPolicy * len(policies))(*[GridPolicy(READ[c.split("/")[0]], WEIGHT_READ[c.split("/")[1]])
+                                          for c in policies])
+    out = {"u_codes": torch.empty(T, d, dtype=torch.int8, device=dev),
+           "u_step": torch.empty(T, dtype=torch.float32, device=dev),
+           "dgain_ref": torch.empty(d, dtype=torch.float32, device=dev),
+           "dW_ref": torch.empty(d, n, dtype=torch.float32, device=dev),
+           "dX_ref": torch.empty(T, d, dtype=torch.float32, device=dev),
+           "Y": torch.empty(T, n, dtype=torch.float32, device=dev) if want_y else None,
+           "diag": new_diag(dev)}
+    eg, cg = _est(len(policies), d, dev, False)
+    ew, cw = _est(len(policies), d * n, dev, False)
+    if ws is None:
+        ws = _workspace(_grid_ws(T, d, n), dev)
+    _check(_grid(_p(X), _p(gain), _p(W), _p(dY), _dt(X), T, d, n, eps, bits, pol, len(policies), K, seed, store_id,
+                 _p(out["Y"]), _p(out["u_codes"]), _p(out["u_step"]), _p(out["dgain_ref"]), _p(out["dW_ref"]),
+                 _p(out["dX_ref"]), cg, cw, _p(out["diag"]), _p(ws), ws.numel(), _stream()),
+           "bs_rmsnorm_linear_grid_fwd_bwd")
+    out["dgain"], out["dW"] = eg, ew
     out["policies"] = list(policies)
     return out
 
