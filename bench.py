@@ -222,6 +222,23 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
     del Q, K, V, dO, ws
     torch.cuda.empty_cache()
 
+    # the paper's own normalization store (per-token 6-bit grid) at the benchmark's shape, every
+    # policy of its table, K = 256
+    Xg, gg, Wg, dYg = (t_.to(dev) for t_ in synth.rmsnorm_linear_inputs(8192, 1024, 4096, torch.bfloat16, 8))
+    ws = torch.empty(bsp._grid_ws(8192, 1024, 4096), dtype=torch.uint8, device=dev)
+    wall, t = _timed(bsp, torch, lambda: bsp.rmsnorm_linear_grid(Xg, gg, Wg, dYg, bits=6, K=256, seed=21, ws=ws),
+                     ("gemm", "gemm_split_sum", "grid_store", "grid_fresh", "rmsnorm_fwd"), reps)
+    et = 8192 * 1024 * 256
+    out["grid_store_6bit_8192x1024x4096_k256"] = {
+        "call_ms": round(wall * 1e3, 3), "policy_trials_per_s": round(8 * 256 / wall, 1),
+        "kernel_ms": {k: round(v, 4) for k, v in t.items()},
+        "fresh_Gelement_trials_per_s": round(et / (t["grid_fresh"] / 1e3) / 1e9, 1),
+        "gemm_TFLOPs": round(16 * 2.0 * 8192 * 1024 * 4096 / ((t["gemm"] + t["gemm_split_sum"]) / 1e3) / 1e12, 1),
+        "work": "8 policies, K = 256 new roundings (one Philox word per element-trial); 16 bf16 contractions of "
+                "2 T d n (Y, du, dW_ref and the U, N, R+e biases with 3-term residual operands)"}
+    del Xg, gg, Wg, dYg, ws
+    torch.cuda.empty_cache()
+
     # the log-softmax operator test at the paper's configuration (fp64: eps = 0.1, 128 classes,
     # 64 rows, 4096 trials) and at a vocabulary-sized row (32768 classes, 512 rows, 64 trials)
     for rows_, C_, K_, tag in ((64, 128, 4096, "logsoftmax_check_64x128_k4096"),
