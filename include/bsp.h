@@ -312,6 +312,48 @@ bs_status bs_attn_pstore_policy(const void* Q, const void* Kt, const void* V, co
                                 void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------
+ * bs_te_attn_bwd -- an emulation of an FP8 attention backward with delayed scaling, whose
+ * correction term D reads a saved copy of the output (App. D.2, the forks' dense backward;
+ * App. E.3, the saturated-row repair).
+ *
+ * With scales = (s_P, s_dO, s_dS, s_g) (device fp32, > 0; delayed scales from the caller's
+ * amax histories) and Q8(x; s, F) = s * RNE_F(clamp(fl32(x / s), +-FMAX_F)):
+ *   dO_q = Q8(dO; s_dO, E5M2); P re-formed from Q, K (the forward's realized fp32 probabilities);
+ *   P_q = Q8(P; s_P, E4M3); dV = P_q^T dO_q; dP = dO_q V^T; dS = P (dP - D) (zero above the
+ *   causal diagonal); dS_q = Q8(dS; s_dS, E5M2); dQ = c dS_q K; dK = c dS_q^T Q; the three
+ *   gradients are returned as Q8(.; s_g, E5M2).
+ * D per row, by source: FROM_P rowsum(dO_q * P V) (equal to rowsum(P dP)); U rowsum(dO_q * O);
+ *   R rowsum(dO_q * deq(O_codes)); N rowsum(dO_q * N(O)), N(O) a new stochastic rounding of
+ *   fl32(O / O_scale) in E4M3 (trial `trial`, use store_id*256 + 1, element b,h,s,d row-major);
+ *   REPAIR FROM_P on rows whose largest probability (exactly fl32(1/l)) is >= threshold, R on
+ *   the others.
+ *
+ *   Q, Kt (the keys), V, dO [B,H,S,dh] bf16, 16-byte aligned; dh == 64; S >= 4 a multiple of 4;
+ *   B*H <= 65535. O [B,H,S,dh] fp32 (U, N; else nullable); O_codes [B,H,S,dh] uint8 E4M3
+ *   (R, REPAIR) and O_scale [1] fp32 device (R, N, REPAIR): the forward's store of O.
+ *   dQ, dK, dV [B,H,S,dh] fp32 out: the returned (cast) gradients, fl32(code value * s_g).
+ *   amax [3] fp32 out: max |dO|, max |dS| (pre-cast), max of the pre-cast gradients.
+ *   counts [4] uint32 out: rows with fl32(1/l) >= threshold; clamped entries of dO, of dS and of
+ *   the three gradients.
+ *   Nullable outputs: P_out, dS_out [B,H,S,S] fp32 (the realized P and pre-cast dS), P_codes,
+ *   dS_codes [B,H,S,S] uint8 (4-byte aligned) and grad_pre [3][B,H,S,dh] fp32 (pre-cast dQ,
+ *   dK, dV); [B,H,S,S] entries above the causal diagonal's 64 x 64 tiles are not written.
+ *   ws: bs_te_attn_workspace_size(B, H, S, dh, causal, source) bytes (0 for shapes the call
+ *   rejects); about 2 causal-half S^2 bytes per head plus 7 [B,H,S,dh] bf16/fp32 arrays.
+ * Returns BS_EINVAL for a null required pointer, a bad source, a misaligned pointer;
+ * BS_ESHAPE for dh != 64 or S not a multiple of 4.
+ * ---------------------------------------------------------------------------------- */
+typedef enum { BS_D_FROM_P = 0, BS_D_U = 1, BS_D_R = 2, BS_D_N = 3, BS_D_REPAIR = 4 } bs_d_source;
+
+size_t bs_te_attn_workspace_size(int B, int H, int S, int dh, int causal, bs_d_source source);
+bs_status bs_te_attn_bwd(const void* Q, const void* Kt, const void* V, const void* dO, int B, int H, int S, int dh,
+                         int causal, float softmax_scale, const float* O, const uint8_t* O_codes, const float* O_scale,
+                         bs_d_source source, float threshold, const float* scales, uint64_t seed, uint32_t store_id,
+                         uint32_t trial, float* dQ, float* dK, float* dV, float* amax, uint32_t* counts, float* P_out,
+                         float* dS_out, uint8_t* P_codes, uint8_t* dS_codes, float* grad_pre, void* ws,
+                         size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------------------
  * bs_linear_bwd_policy -- Linear backward whose incoming gradient is stochastically
  * rounded to FP8 (E5M2 in the HYBRID recipe, App. D.1), read by two uses.
  *
@@ -431,7 +473,8 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* w, cons
  *   events on the launch stream around each launch of the instrumented kernels
  *   ("fresh_count", "fresh_count_se", "fresh_count_kappa", "amax", "quantize", "gemm",
  *   "rmsnorm_fwd", "attn_fwd", "attn_bwd", "attn_l2", "pstore_fwd", "pstore_rows", "pstore_dq",
- *   "pstore_dkv", "lsm_prep", "lsm_trial", "grid_store", "grid_fresh");
+ *   "pstore_dkv", "lsm_prep", "lsm_trial", "grid_store", "grid_fresh", "te_prep", "te_d", "te_dq",
+ *   "te_dkv");
  *   bs_profile_enable(0) stops and frees them. bs_profile_read waits for the recorded
  *   events of `kernel` (NULL: all) and returns their summed elapsed time and count.
  *   Return values are bs_status codes.

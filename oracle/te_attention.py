@@ -79,7 +79,9 @@ def check(Q, Kt, V, dO, *, P, dS=None, O, O_codes, O_scale, causal=True, c=None,
 
     Q, Kt, V, dO [B, H, S, dh]; P: the realized fp32 probabilities [B, H, S, S]; dS: the realized
     fp32 pre-cast dS (None: cast the oracle's own); O: the original fp32 output; O_codes,
-    O_scale: its E4M3 store (the R copy); scales: (s_P, s_dO, s_dS, s_g) as fp32.
+    O_scale: its E4M3 store (the R copy); scales: (s_P, s_dO, s_dS, s_g) as fp32. Besides the
+    values, the clamp counts of dO, dS and the three gradients and the rows at or over the
+    threshold are reported.
     """
     Q, Kt, V, dO = (np.asarray(a, dtype=np.float32).astype(np.float64) for a in (Q, Kt, V, dO))
     B, H, S, dh = Q.shape
@@ -95,7 +97,7 @@ def check(Q, Kt, V, dO, *, P, dS=None, O, O_codes, O_scale, causal=True, c=None,
     heads = [(b, h) for b in range(B) for h in range(H)] if heads is None else list(heads)
     out = {"heads": heads, "P_codes": Pcodes, "amax_dO": float(np.abs(dO).max()), "sat_dO": sat_dO,
            "dS": [], "D": [], "dQ_pre": [], "dK_pre": [], "dV_pre": [], "dQ": [], "dK": [], "dV": [],
-           "dS_codes": [], "sat_rows": []}
+           "dS_codes": [], "sat_rows": [], "sat_dS": 0, "sat_grad": 0}
     for (b, h) in heads:
         p = P[b, h].astype(np.float64)
         dP = dOq[b, h] @ V[b, h].T
@@ -105,7 +107,8 @@ def check(Q, Kt, V, dO, *, P, dS=None, O, O_codes, O_scale, causal=True, c=None,
         ds = p * (dP - D[:, None])
         if causal:
             ds = np.where(np.tril(np.ones((S, S), dtype=bool)), ds, 0.0)
-        dsq, dscodes, _ = cast(ds if dS is None else dS[b, h], sdS, fp8.E5M2)
+        dsq, dscodes, nsat = cast(ds if dS is None else dS[b, h], sdS, fp8.E5M2)
+        out["sat_dS"] += nsat
         dQp = c * dsq @ Kt[b, h]
         dKp = c * dsq.T @ Q[b, h]
         dVp = Pq[b, h].T @ dOq[b, h]
@@ -113,7 +116,9 @@ def check(Q, Kt, V, dO, *, P, dS=None, O, O_codes, O_scale, causal=True, c=None,
                         ("dS_codes", dscodes)):
             out[name].append(v)
         for name, v in (("dQ", dQp), ("dK", dKp), ("dV", dVp)):
-            out[name].append(cast64(v, sg, fp8.E5M2)[0])
+            val, _, nsat = cast64(v, sg, fp8.E5M2)
+            out[name].append(val)
+            out["sat_grad"] += nsat
         out["sat_rows"].append(int((p.max(axis=-1) >= thr).sum()))
     for name in ("dS", "D", "dQ_pre", "dK_pre", "dV_pre", "dQ", "dK", "dV", "dS_codes"):
         out[name] = np.stack(out[name])

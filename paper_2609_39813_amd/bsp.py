@@ -75,6 +75,11 @@ _ps = _sig("bs_attn_pstore_policy", _int,
 _attn2 = _sig("bs_attn_level2_policy", _int,
               [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _vp, _int, _int, _f32, ctypes.POINTER(_int), _int,
                _int, _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, _vp, _vp, _vp, _vp, _sz, _vp])
+D_SOURCE = {"P": 0, "U": 1, "R": 2, "N": 3, "repair": 4}
+_te_ws = _sig("bs_te_attn_workspace_size", _sz, [_int] * 6)
+_te = _sig("bs_te_attn_bwd", _int,
+           [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _vp, _vp, _vp, _int, _f32, _vp, _u64, _u32, _u32,
+            _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp])
 _lsm_ws = _sig("bs_logsoftmax_check_workspace_size", _sz, [_i64, _int, _int])
 _lsm = _sig("bs_logsoftmax_reuse_check", _int,
             [_vp, _vp, _i64, _int, ctypes.c_double, _int, _u64, _u32, _int, _vp, _vp, _sz, _vp])
@@ -136,6 +141,7 @@ def profile_read(kernel=None):
 EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
             "bs_policy_bias_estimate", "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
             "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_attn_pstore_workspace_size", "bs_attn_pstore_policy", "bs_attn_level2_policy",
+            "bs_te_attn_workspace_size", "bs_te_attn_bwd",
             "bs_logsoftmax_check_workspace_size", "bs_logsoftmax_reuse_check",
             "bs_rmsnorm_linear_grid_workspace_size", "bs_rmsnorm_linear_grid_fwd_bwd", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
             "bs_decoder_layer_workspace_size", "bs_decoder_layer_policy", "bs_profile_enable", "bs_profile_read"]
@@ -439,6 +445,41 @@ def attn_pstore_policy(Q, Kt, V, dO, *, causal=True, scale=None, fmt="e4m3", fwd
                _p(out["diag"]), _p(ws), ws.numel(), _stream()), "bs_attn_pstore_policy")
     out["dQ"], out["dK"], out["dV"] = (e[0] for e in ests)
     out["policies"] = list(policies)
+    return out
+
+
+def te_attn_workspace(B, H, S, dh, causal, source, device):
+    n = _te_ws(B, H, S, dh, int(causal), D_SOURCE[source])
+    if n == 0:
+        raise BspError(2, "bs_te_attn_workspace_size")
+    return _workspace(n, device)
+
+
+def te_attn_bwd(Q, Kt, V, dO, scales, *, O=None, O_codes=None, O_scale=None, source="R", threshold=0.9, causal=True,
+                scale=None, seed=0, store_id=0, trial=1, want_p=False, want_ds=False, want_codes=False, want_pre=False,
+                ws=None):
+    """The emulated FP8 attention backward with delayed scales (bs_te_attn_bwd). scales: device
+    fp32 [4] = (s_P, s_dO, s_dS, s_g)."""
+    _dev_check(Q, Kt, V, dO, scales, O, O_codes, O_scale)
+    B, H, S, dh = Q.shape
+    dev = Q.device
+    c = 1.0 / dh ** 0.5 if scale is None else scale
+    shp = (B, H, S, dh)
+    sq = lambda dt, on: torch.zeros(B, H, S, S, dtype=dt, device=dev) if on else None
+    out = {"dQ": torch.empty(shp, dtype=torch.float32, device=dev),
+           "dK": torch.empty(shp, dtype=torch.float32, device=dev),
+           "dV": torch.empty(shp, dtype=torch.float32, device=dev),
+           "amax": torch.empty(3, dtype=torch.float32, device=dev),
+           "counts": torch.empty(4, dtype=torch.int32, device=dev),
+           "P": sq(torch.float32, want_p), "dS": sq(torch.float32, want_ds),
+           "P_codes": sq(torch.uint8, want_codes), "dS_codes": sq(torch.uint8, want_codes),
+           "pre": torch.empty((3,) + shp, dtype=torch.float32, device=dev) if want_pre else None}
+    if ws is None:
+        ws = te_attn_workspace(B, H, S, dh, causal, source, dev)
+    _check(_te(_p(Q), _p(Kt), _p(V), _p(dO), B, H, S, dh, int(causal), c, _p(O), _p(O_codes), _p(O_scale),
+               D_SOURCE[source], threshold, _p(scales), seed, store_id, trial, _p(out["dQ"]), _p(out["dK"]),
+               _p(out["dV"]), _p(out["amax"]), _p(out["counts"]), _p(out["P"]), _p(out["dS"]), _p(out["P_codes"]),
+               _p(out["dS_codes"]), _p(out["pre"]), _p(ws), ws.numel(), _stream()), "bs_te_attn_bwd")
     return out
 
 

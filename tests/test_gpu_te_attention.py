@@ -1,0 +1,150 @@
+"""GPU parity: bs_te_attn_bwd against the oracle (oracle/te_attention.py).
+
+The forward's fp32 output O and its E4M3 store come from the oracle; the delayed scales from
+the oracle's own fp64 pass (the amaxes a previous step would have seen), scaled to provoke
+clamps or flushes. The library's realized P and pre-cast dS are handed to the oracle, which
+casts them: the P and dS codes agree bit for bit, P matches the fp64 softmax, dS and the
+pre-cast gradients match the oracle's fp64 values within 1e-5 (normwise relative). The returned
+gradients (fp32 values of code times s_g) are the E5M2 casts of the library's own pre-cast
+values bit for bit; against the oracle's casts of its fp64 values they may differ only where
+the value sits within 1e-4 of a rounding midpoint. amaxes and counts match.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention, fp8, pstore, qround as oq, te_attention as te
+from paper_2609_39813_amd import synth
+from tests.parity import assert_rel, to_np
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-5
+F32 = np.float32
+
+
+def inputs(B, H, S, seed, sharp=1):
+    Q, K, V, dO = synth.attention_inputs(B, H, S, 64, torch.float32, config=500 + seed)
+    return [t.to(torch.bfloat16) for t in (Q * sharp, K, V, dO)]
+
+
+def forward_store(Q, K, V, causal, c, seed, store_id):
+    """The forward's fp32 output and its E4M3 stochastic store (oracle only)."""
+    O64, P64, _, _ = attention.forward(Q.float().numpy(), K.float().numpy(), V.float().numpy(), causal, c)
+    O32 = O64.astype(np.float32)
+    q = oq.qround(O32, fp8.E4M3, oq.SR, seed, 0, store_id * 256)
+    return O32, P64.astype(np.float32), q
+
+
+def delayed_scales(Q, K, V, dO, P32, O32, q, causal, c, factors):
+    """Scales from the amaxes of the oracle's own pass, each times its factor."""
+    probe = (F32(1 / 448), F32(np.abs(dO.float().numpy()).max() / 57344), F32(1.0), F32(1.0))
+    ref = te.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.float().numpy(), P=P32, O=O32,
+                   O_codes=q.codes, O_scale=q.scale, causal=causal, c=c, scales=probe, source="P")
+    am = (1.0 / 448, ref["amax_dO"] / 57344, ref["amax_dS"] / 57344, ref["amax_grad"] / 57344)
+    return tuple(F32(a * f) for a, f in zip(am, factors))
+
+
+def run_case(lib, B, H, S, *, causal=True, source="R", factors=(1, 1, 1, 1), sharp=1, thr=0.9, seed=1, store_id=4,
+             trial=3):
+    c = 0.125
+    Q, K, V, dO = inputs(B, H, S, seed, sharp)
+    O32, P32, q = forward_store(Q, K, V, causal, c, seed, store_id)
+    sc = delayed_scales(Q, K, V, dO, P32, O32, q, causal, c, factors)
+    print(f"[te] B={B} H={H} S={S} causal={causal} source={source} factors={factors} sharp={sharp} scales={sc}",
+          flush=True)
+    dev = torch.device("cuda")
+    out = lib.te_attn_bwd(Q.to(dev), K.to(dev), V.to(dev), dO.to(dev), torch.tensor(sc, device=dev),
+                          O=torch.from_numpy(O32).to(dev), O_codes=torch.from_numpy(q.codes).to(dev),
+                          O_scale=torch.tensor([q.scale], dtype=torch.float32, device=dev), source=source,
+                          threshold=thr, causal=causal, scale=c, seed=seed, store_id=store_id, trial=trial,
+                          want_p=True, want_ds=True, want_codes=True, want_pre=True)
+    torch.cuda.synchronize()
+    ref = te.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.float().numpy(),
+                   P=out["P"].cpu().numpy(), dS=out["dS"].cpu().numpy(), O=O32, O_codes=q.codes, O_scale=q.scale,
+                   causal=causal, c=c, scales=sc, source=source, thr=F32(thr), seed=seed, store_id=store_id,
+                   trial=trial)
+    compare(out, ref, Q, K, causal, c, sc)
+    return out, ref
+
+
+def fl32(x):
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def compare(out, ref, Q, K, causal, c, sc):
+    B, H, S, dh = out["dQ"].shape
+    flat = lambda t: to_np(t).reshape(B * H, *t.shape[2:])
+    assert_rel(to_np(out["P"]), pstore.probabilities(Q.float().numpy(), K.float().numpy(), causal, c), TOL,
+               "P against the fp64 softmax")
+    assert np.array_equal(out["P_codes"].cpu().numpy(), ref["P_codes"])
+    assert np.array_equal(out["dS_codes"].cpu().numpy().reshape(B * H, S, S), ref["dS_codes"])
+    assert_rel(flat(out["dS"]), ref["dS"], TOL, "dS")
+    pre = out["pre"].cpu().numpy().astype(np.float64)
+    n_miss, n_sat, n_edge = 0, 0, 0
+    for i, name in enumerate(("dQ", "dK", "dV")):
+        p = pre[i].reshape(B * H, S, dh)
+        assert_rel(p, ref[name + "_pre"], TOL, name + " pre-cast")
+        val, _, ns = te.cast64(p, sc[3], fp8.E5M2)
+        n_sat += ns
+        got = flat(out[name])                                   # fp32 values fl32(code value * s_g)
+        assert np.array_equal(got, fl32(val)), f"{name}: the returned values are not the cast of the pre-cast values"
+        want = fl32(ref[name])
+        n_edge += int((np.abs(np.abs(ref[name + "_pre"]) / np.float64(sc[3]) - 57344.0) <= 1e-4 * 57344.0).sum())
+        miss = got != want
+        n_miss += int(miss.sum())
+        if miss.any():
+            mid = 0.5 * (got[miss] + want[miss])
+            dist = np.abs(ref[name + "_pre"][miss] - mid)
+            assert np.all(dist <= 1e-4 * np.abs(mid)), f"{name}: a cast differs away from a rounding midpoint"
+    assert n_miss <= max(2, 1e-4 * 3 * pre[0].size), f"{n_miss} near-tie cast differences"
+    amax = out["amax"].cpu().numpy()
+    assert amax[0] == F32(ref["amax_dO"]) and amax[1] == F32(ref["amax_dS"])
+    assert abs(amax[2] - ref["amax_grad"]) <= TOL * ref["amax_grad"]
+    counts = out["counts"].cpu().numpy()
+    assert counts[0] == sum(ref["sat_rows"])
+    assert counts[1] == ref["sat_dO"] and counts[2] == ref["sat_dS"]
+    # the clamp count may differ only at entries within 1e-4 of FMAX (same returned value)
+    assert counts[3] == n_sat and abs(int(counts[3]) - ref["sat_grad"]) <= n_edge
+
+
+@pytest.mark.parametrize("source", ["R", "P", "U", "N"])
+def test_causal_ragged_sources(lib, source):
+    run_case(lib, 1, 2, 200, source=source, seed=2)
+
+
+def test_clamped_scales_noncausal(lib):
+    """Stale delayed scales: dO, dS and the gradients clamp at their largest entries."""
+    out, ref = run_case(lib, 2, 1, 128, causal=False, source="R", factors=(1, 0.5, 0.25, 0.5), seed=3)
+    c = out["counts"].cpu().numpy()
+    assert c[1] > 0 and c[2] > 0 and c[3] > 0
+
+
+def test_coarse_scales_subnormal_and_zero_codes(lib):
+    """Scales far above the amaxes: most dS entries land on E5M2 subnormals or zero."""
+    out, _ = run_case(lib, 1, 2, 64, source="P", factors=(1, 2 ** 8, 2 ** 24, 2 ** 16), seed=4)
+    mag = out["dS_codes"].cpu().numpy()[..., np.tril(np.ones((64, 64), dtype=bool))] & 0x7F
+    assert (mag == 0).mean() > 0.05 and (mag < 4).mean() > 0.3
+
+
+def test_repair_selects_saturated_rows(lib):
+    out, ref = run_case(lib, 1, 2, 136, source="repair", sharp=4, seed=5)
+    n = int(out["counts"].cpu()[0])
+    assert 0 < n < 2 * 136 and n == sum(ref["sat_rows"])
+
+
+@pytest.mark.parametrize("S", [4, 64])
+def test_small_and_single_tile(lib, S):
+    run_case(lib, 1, 1, S, source="R", seed=6 + S)
+
+
+def test_errors(lib):
+    dev = torch.device("cuda")
+    Q, K, V, dO = (t.to(dev) for t in inputs(1, 1, 64, 9))
+    sc = torch.ones(4, device=dev)
+    with pytest.raises(lib.BspError):
+        lib.te_attn_bwd(Q, K, V, dO, sc, source="R")                     # no O store
+    with pytest.raises(lib.BspError):
+        lib.te_attn_bwd(Q, K, V, dO, sc, source="U")                     # no O
+    Q6 = torch.zeros(1, 1, 66, 64, dtype=torch.bfloat16, device=dev)
+    with pytest.raises(lib.BspError):
+        lib.te_attn_bwd(Q6, Q6, Q6, Q6, sc, source="P", ws=torch.empty(1 << 20, dtype=torch.uint8, device=dev))
