@@ -122,7 +122,8 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
     rate at B4 H16 S1024 d64 (causal, D read by U / R / N, K = 32); the E5M2 Linear backward at
     16384 x 2048 x 8192 (shared and per-use new roundings, K = 64); one decoder layer at
     B8 S2048 d1024 H16 F4096 (K = 16, all four stores, every use); the FP8 store of attention
-    probabilities at B4 H16 S1024 d64 (every policy of App. B's table, K = 32)."""
+    probabilities at B4 H16 S1024 d64 (every policy of App. B's table, K = 32); the emulated FP8
+    attention backward with delayed scaling at the same shape."""
     out = {}
     cfg4 = synth.CONFIGS[4]
     X4, W4, dy4, _, _ = synth.linear_bwd_inputs(cfg4["M"], cfg4["k"], cfg4["n"], torch.bfloat16, 4)
@@ -220,6 +221,29 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
         "work": f"{len(cp['policies'])} policies, K = {cp['K']}: {draws} element-draws (Philox words) in the "
                 "row-sum pass; bias fields written by the dQ pass and read by the dK/dV pass (8 x 4 B per element)"}
     del Q, K, V, dO, ws
+    torch.cuda.empty_cache()
+
+    # the emulated FP8 attention backward with delayed scaling (E5M2 dO, dS and gradients, E4M3 P),
+    # D from the saturated-row repair, at the same attention shape
+    Q, K, V, dO = (t_.to(dev) for t_ in synth.attention_inputs(cp["B"], cp["H"], cp["S"], cp["dh"], cp["dtype"],
+                                                               cp["config"] + 1))
+    O = torch.randn(cp["B"], cp["H"], cp["S"], cp["dh"], device=dev) * 0.3      # a stand-in saved output
+    Oc, Os, _ = bsp.qround(O, fmt="e4m3", mode="sr", seed=5)                    # the forward's store of O
+    sc = torch.tensor([1 / 448, float(dO.abs().max()) / 57344, 2e-5, 2e-5], dtype=torch.float32, device=dev)
+    ws = bsp.te_attn_workspace(cp["B"], cp["H"], cp["S"], cp["dh"], True, "repair", dev)
+    names = ("attn_prep", "attn_fwd", "te_prep", "te_d", "te_dq", "te_dkv")
+    wall, t = _timed(bsp, torch, lambda: bsp.te_attn_bwd(Q, K, V, dO, sc, O=O, O_codes=Oc, O_scale=Os,
+                                                          source="repair", causal=True, ws=ws), names, reps)
+    heads, S = cp["B"] * cp["H"], cp["S"]
+    tiles = heads * ((S + 63) // 64) * ((S + 63) // 64 + 1) // 2
+    fl_dq, fl_dkv = tiles * 3 * 2 * 64 ** 3, tiles * 2 * 2 * 64 ** 3   # P, dP, dQ / dK, dV per causal tile
+    out["te_attention_b4_h16_s1024_d64"] = {
+        "call_ms": round(wall * 1e3, 3), "kernel_ms": {k: round(v, 4) for k, v in t.items()},
+        "dq_TFLOPs": round(fl_dq / (t["te_dq"] / 1e3) / 1e12, 1),
+        "dkv_TFLOPs": round(fl_dkv / (t["te_dkv"] / 1e3) / 1e12, 1),
+        "work": f"{tiles} causal 64 x 64 tiles: P re-formed, dP, dS and its E5M2 / P's E4M3 codes and dQ in the "
+                "query-major pass, dK and dV from the codes in the key-major pass (5 x 2 x 64^3 flop per tile)"}
+    del Q, K, V, dO, O, Oc, Os, ws
     torch.cuda.empty_cache()
 
     # the paper's own normalization store (per-token 6-bit grid) at the benchmark's shape, every

@@ -12,6 +12,8 @@
 #include "k_attn.h"
 #include "k_qmajor.h"
 
+#include <algorithm>
+
 #define BS_TRY(x)               \
   do {                          \
     const bs_status _s = (x);   \
@@ -30,16 +32,16 @@ struct TeArgs {
   const float *m, *l;
   const float* sc;             // device [4]: s_P, s_dO, s_dS, s_g
   const float* D;              // [rows] the correction term
-  uint8_t *dsq, *pq;           // tile-major codes [BH][tiles][64 key][64 query]
+  uint8_t *dsq, *pq;           // tile-major codes [BH][tiles][64 key][64 query, in code_pos order]
   float *P_out, *dS_out;       // nullable [BH][S][S]: the realized P and pre-cast dS
   uint8_t *P_codes, *dS_codes; // nullable [BH][S][S]
   float* pre;                  // nullable [3][BH][S][64]: pre-cast dQ, dK, dV
   float *dQ, *dK, *dV;
-  uint32_t* amax;              // [3] fp32 bits: dO, dS, gradients
-  uint32_t* counts;            // [4]: saturated rows, clamps of dO, dS and the gradients
+  uint32_t *part_dq, *part_dkv; // per-block partials (amaxes as fp32 bits, clamp counts)
 };
 
 constexpr float kE5M2Max = 57344.0f, kE4M3Max = 448.0f;
+constexpr int TE_BLOCK = 256;  // threads per block of every kernel here
 
 // RNE codes of 4 values already divided by their scale, clamped to +-FMAX first; returns the
 // number of clamped values in nsat
@@ -60,57 +62,127 @@ __device__ __forceinline__ uint32_t codes4(const float (&y)[4], uint32_t& nsat) 
   return w;
 }
 
-// largest of v >= 0 over the wave, folded into *p (fp32 bits of non-negative values order as integers)
-__device__ __forceinline__ void atomic_amax(uint32_t* p, float v) {
-  const uint32_t m = wave_max_u32(__float_as_uint(v));
-  if ((threadIdx.x & 63) == 0 && m) atomicMax(p, m);
-}
-__device__ __forceinline__ void atomic_count(uint32_t* p, uint32_t v) {
-  v = wave_sum_u32(v);
-  if ((threadIdx.x & 63) == 0 && v) atomicAdd(p, v);
+// The block's totals of N quantities written to out[0..N-1]: MAX[i] selects the largest (fp32 bits
+// of non-negative values order as integers) or the sum. Every thread of the block must call it.
+// (Per-block partials instead of atomics on shared counters: those serialize, and the order of
+// the final reduction is fixed.)
+template <int N>
+__device__ __forceinline__ void block_total(const uint32_t (&v)[N], const bool (&MAX)[N], uint32_t* out) {
+  __shared__ uint32_t part[N][TE_BLOCK / 64];
+  const int w = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const uint32_t r = MAX[i] ? wave_max_u32(v[i]) : wave_sum_u32(v[i]);
+    if ((threadIdx.x & 63) == 0) part[i][w] = r;
+  }
+  __syncthreads();
+  if (threadIdx.x < N) {
+    const int i = threadIdx.x;
+    uint32_t r = part[i][0];
+#pragma unroll
+    for (int k = 1; k < TE_BLOCK / 64; ++k) r = MAX[i] ? max(r, part[i][k]) : r + part[i][k];
+    out[i] = r;
+  }
 }
 
-__global__ void te_init_kernel(uint32_t* amax, uint32_t* counts) {
-  if (threadIdx.x < 3) amax[threadIdx.x] = 0u;
-  if (threadIdx.x < 4) counts[threadIdx.x] = 0u;
+// Byte position of tile-local query q in a tile row of the code arrays: 16 (q >> 2 & 3) +
+// 8 (q >> 5) + 4 (q >> 4 & 1) + (q & 3), so that the 8 queries 32 s2 + 16 hh + 4 g + r (s2, hh < 2,
+// r < 4) a key-major lane reads for group g are the 16 bytes at 16 g.
+__device__ __forceinline__ int code_pos(int q) {
+  return 16 * ((q >> 2) & 3) + 8 * (q >> 5) + 4 * ((q >> 4) & 1) + (q & 3);
 }
 
-// dO -> its E5M2 code values (bf16, exact), 4 elements per thread
-__global__ __launch_bounds__(256) void te_prep_kernel(const u16* __restrict__ dO, int64_t n, const float* sc,
-                                                      u16* __restrict__ dOq, uint32_t* amax, uint32_t* counts) {
-  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  const float s = sc[1];
+// 4 x 4 byte transpose within a quad of lanes: lane j's byte i becomes lane i's byte j (two DPP
+// exchanges, with the lane j ^ 2 and then with the lane j ^ 1)
+__device__ __forceinline__ uint32_t quad_transpose(uint32_t w, int j) {
+  const uint32_t x = (uint32_t)__builtin_amdgcn_mov_dpp((int)w, 0x4E, 0xF, 0xF, false);  // quad_perm 2,3,0,1
+  const uint32_t n = (j & 2) ? ((x >> 16) | (w & 0xFFFF0000u)) : ((w & 0x0000FFFFu) | (x << 16));
+  const uint32_t y = (uint32_t)__builtin_amdgcn_mov_dpp((int)n, 0xB1, 0xF, 0xF, false);  // quad_perm 1,0,3,2
+  return (j & 1) ? (((y >> 8) & 0x00FF00FFu) | (n & 0xFF00FF00u)) : ((n & 0x00FF00FFu) | ((y & 0x00FF00FFu) << 8));
+}
+
+__device__ __forceinline__ int block_linear() { return (int)(blockIdx.y * gridDim.x + blockIdx.x); }
+
+// Per-block partials of every kernel: [n][width] words each
+struct TeParts {
+  uint32_t *prep, *d, *dq, *dkv;  // widths 2 (amax dO, clamps dO), 1 (rows), 4 (amax dS, clamps dS,
+  int n_prep, n_d, n_dq, n_dkv;   // amax gradients, clamps gradients), 2 (amax gradients, clamps)
+};
+
+// column `col` of an [n][width] partial array reduced over the block (result in every thread)
+__device__ uint32_t reduce_col(const uint32_t* p, int n, int width, int col, bool is_max) {
+  __shared__ uint32_t red[TE_BLOCK / 64];
+  uint32_t r = 0;
+  for (int i = threadIdx.x; i < n; i += TE_BLOCK) r = is_max ? max(r, p[i * width + col]) : r + p[i * width + col];
+  r = is_max ? wave_max_u32(r) : wave_sum_u32(r);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = r;
+  __syncthreads();
+  uint32_t t = red[0];
+#pragma unroll
+  for (int k = 1; k < TE_BLOCK / 64; ++k) t = is_max ? max(t, red[k]) : t + red[k];
+  __syncthreads();
+  return t;
+}
+
+__global__ __launch_bounds__(TE_BLOCK) void te_final_kernel(TeParts q, float* amax, uint32_t* counts) {
+  const uint32_t a0 = reduce_col(q.prep, q.n_prep, 2, 0, true), c1 = reduce_col(q.prep, q.n_prep, 2, 1, false);
+  const uint32_t c0 = reduce_col(q.d, q.n_d, 1, 0, false);
+  const uint32_t a1 = reduce_col(q.dq, q.n_dq, 4, 0, true), c2 = reduce_col(q.dq, q.n_dq, 4, 1, false);
+  const uint32_t a2 = max(reduce_col(q.dq, q.n_dq, 4, 2, true), reduce_col(q.dkv, q.n_dkv, 2, 0, true));
+  const uint32_t c3 = reduce_col(q.dq, q.n_dq, 4, 3, false) + reduce_col(q.dkv, q.n_dkv, 2, 1, false);
+  if (threadIdx.x == 0) {
+    amax[0] = __uint_as_float(a0);
+    amax[1] = __uint_as_float(a1);
+    amax[2] = __uint_as_float(a2);
+    counts[0] = c0;
+    counts[1] = c1;
+    counts[2] = c2;
+    counts[3] = c3;
+  }
+}
+
+// dO -> its E5M2 code values (bf16, exact), 8 elements per thread and step (grid-stride)
+__global__ __launch_bounds__(TE_BLOCK) void te_prep_kernel(const u16* __restrict__ dO, int64_t n, const float* sc,
+                                                           u16* __restrict__ dOq, uint32_t* part) {
+  const double rs = 1.0 / (double)sc[1];
   float am = 0.0f;
   uint32_t nsat = 0;
-  if (i < n) {
-    const uint2 d2 = *(const uint2*)(dO + i);
-    const float x[4] = {bf16_to_f32((u16)(d2.x & 0xFFFF)), bf16_to_f32((u16)(d2.x >> 16)),
-                        bf16_to_f32((u16)(d2.y & 0xFFFF)), bf16_to_f32((u16)(d2.y >> 16))};
-    float y[4];
+  for (int64_t i = ((int64_t)blockIdx.x * TE_BLOCK + threadIdx.x) * 8; i < n; i += (int64_t)gridDim.x * TE_BLOCK * 8) {
+    const uint4 d4 = *(const uint4*)(dO + i);
+    const uint32_t dw[4] = {d4.x, d4.y, d4.z, d4.w};
+    uint32_t ow[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      am = fmaxf(am, fabsf(x[r]));
-      y[r] = x[r] / s;
+    for (int h = 0; h < 2; ++h) {
+      float y[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float x = bf16_to_f32((u16)(dw[2 * h + (r >> 1)] >> (16 * (r & 1))));
+        am = fmaxf(am, fabsf(x));
+        y[r] = div_scale(x, rs);
+      }
+      uint32_t ns;
+      const uint32_t w = codes4<BS_E5M2>(y, ns);
+      nsat += ns;
+      // the code values are exact in bf16: their fp32 bit patterns' upper halves
+      ow[2 * h] = (__float_as_uint(f8_val<BS_E5M2>(w, 0)) >> 16) | (__float_as_uint(f8_val<BS_E5M2>(w, 1)) & 0xFFFF0000u);
+      ow[2 * h + 1] = (__float_as_uint(f8_val<BS_E5M2>(w, 2)) >> 16) | (__float_as_uint(f8_val<BS_E5M2>(w, 3)) & 0xFFFF0000u);
     }
-    const uint32_t w = codes4<BS_E5M2>(y, nsat);
-    u16 v[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) v[r] = (u16)(__float_as_uint(f8_val<BS_E5M2>(w, r)) >> 16);  // exact in bf16
-    *(uint2*)(dOq + i) = make_uint2((uint32_t)v[0] | ((uint32_t)v[1] << 16), (uint32_t)v[2] | ((uint32_t)v[3] << 16));
+    *(uint4*)(dOq + i) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
   }
-  atomic_amax(&amax[0], am);
-  atomic_count(&counts[1], nsat);
+  const uint32_t v[2] = {__float_as_uint(am), nsat};
+  const bool mx[2] = {true, false};
+  block_total(v, mx, part + 2 * block_linear());
 }
 
 // D per row (4 lanes per row, 16 elements each), in fp64 from exact operands: dO_q against the
 // forward's P V (P), the original O (U), the E4M3 store of O (R), a new stochastic rounding of O
 // at the store's scale (N), or the repair (P where the row's largest probability, exactly
 // fl32(1 / l), reaches the threshold, R elsewhere). Rows at or over the threshold are counted.
-__global__ __launch_bounds__(256) void te_d_kernel(const u16* __restrict__ dOq, const float* __restrict__ OP,
+__global__ __launch_bounds__(TE_BLOCK) void te_d_kernel(const u16* __restrict__ dOq, const float* __restrict__ OP,
                                                    const float* __restrict__ O, const uint8_t* __restrict__ Oc,
                                                    const float* Os, const float* __restrict__ l, int64_t rows,
                                                    int source, float thr, uint64_t seed, uint32_t trial, uint32_t use,
-                                                   const float* sc, float* __restrict__ D, uint32_t* counts) {
+                                                   const float* sc, float* __restrict__ D, uint32_t* part) {
   const int64_t row = (int64_t)blockIdx.x * 64 + (threadIdx.x >> 2);
   const int sub = threadIdx.x & 3;
   const bool ok = row < rows;
@@ -159,15 +231,18 @@ __global__ __launch_bounds__(256) void te_d_kernel(const u16* __restrict__ dOq, 
   acc += __shfl_xor(acc, 1, 64);
   acc += __shfl_xor(acc, 2, 64);
   if (ok && sub == 0) D[row] = (float)((double)sc[1] * acc);
-  atomic_count(&counts[0], (ok && sub == 0 && sat) ? 1u : 0u);
+  const uint32_t v[1] = {(ok && sub == 0 && sat) ? 1u : 0u};
+  const bool mx[1] = {false};
+  block_total(v, mx, part + block_linear());
 }
 
 // query-major: dS = P (dP - D), its E5M2 codes at s_dS and P's E4M3 codes at s_P (tile-major),
 // dQ = c s_dS val(dS_q) K cast at s_g
-__global__ __launch_bounds__(256) void te_dq_kernel(TeArgs a) {
+__global__ __launch_bounds__(TE_BLOCK) void te_dq_kernel(TeArgs a) {
   __shared__ __attribute__((aligned(16))) u16 sm[2][3][AT * AT];  // K, V, K^T
   const QMajor z = qmajor_setup(a, true);
-  const float sP = a.sc[0], sdO = a.sc[1], sdS = a.sc[2], sg = a.sc[3];
+  const float sdO = a.sc[1], sdS = a.sc[2];
+  const double rP = 1.0 / (double)a.sc[0], rdS = 1.0 / (double)sdS, rg = 1.0 / (double)a.sc[3];
   const float Dq = z.qok ? a.D[z.rb + z.q] : 0.0f;
   const int nqb = (a.S + AT - 1) / AT;
   floatx4 aq[4];
@@ -206,19 +281,19 @@ __global__ __launch_bounds__(256) void te_dq_kernel(TeArgs a) {
       for (int r = 0; r < 4; ++r) {
         ds[r] = p[t][r] * (sdO * dp[t][r] - Dq);
         amds = fmaxf(amds, fabsf(ds[r]));
-        y[r] = ds[r] / sdS;
-        yp[r] = p[t][r] / sP;
+        y[r] = div_scale(ds[r], rdS);
+        yp[r] = div_scale(p[t][r], rP);
       }
       uint32_t ns, nsp;
       const uint32_t wd = codes4<BS_E5M2>(y, ns), wp = codes4<BS_E4M3>(yp, nsp);
       nsat += ns;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        dv[t][r] = f8_val<BS_E5M2>(wd, r);
-        const int64_t o = tile + (16 * t + 4 * z.g + r) * AT + 16 * z.w + z.c16;
-        a.dsq[o] = (uint8_t)(wd >> (8 * r));
-        a.pq[o] = (uint8_t)(wp >> (8 * r));
-      }
+      for (int r = 0; r < 4; ++r) dv[t][r] = f8_val<BS_E5M2>(wd, r);
+      // after the quad transpose lane j (= c16 & 3) holds key 16 t + 4 g + j at the quad's 4
+      // consecutive positions
+      const int64_t o = tile + (16 * t + 4 * z.g + (z.c16 & 3)) * AT + code_pos(16 * z.w + (z.c16 & ~3));
+      *(uint32_t*)(a.dsq + o) = quad_transpose(wd, z.c16 & 3);
+      *(uint32_t*)(a.pq + o) = quad_transpose(wp, z.c16 & 3);
       if (z.qok && key < a.S) {
         const uint64_t e = pelem(a, z, key);
         if (a.dS_out) *(float4*)(a.dS_out + e) = make_float4(ds[0], ds[1], ds[2], ds[3]);
@@ -243,8 +318,6 @@ __global__ __launch_bounds__(256) void te_dq_kernel(TeArgs a) {
     if (kb + 1 < nkb) put(st ^ 1);
     __syncthreads();
   }
-  atomic_amax(&a.amax[1], amds);
-  atomic_count(&a.counts[2], nsat);
   // dQ = c s_dS acc, cast at the gradients' scale
   const float cs = a.scale * sdS;
   float amg = 0.0f;
@@ -257,7 +330,7 @@ __global__ __launch_bounds__(256) void te_dq_kernel(TeArgs a) {
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
       pre[n] = cs * aq[n][r];
-      y[n] = pre[n] / sg;
+      y[n] = div_scale(pre[n], rg);
       amg = fmaxf(amg, fabsf(pre[n]));
     }
     uint32_t ns;
@@ -266,16 +339,17 @@ __global__ __launch_bounds__(256) void te_dq_kernel(TeArgs a) {
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
       const int64_t e = z.hb + (int64_t)qr * AT + 16 * n + z.c16;
-      a.dQ[e] = f8_val<BS_E5M2>(w, n) * sg;
+      a.dQ[e] = f8_val<BS_E5M2>(w, n) * a.sc[3];
       if (a.pre) a.pre[e] = pre[n];
     }
   }
-  atomic_amax(&a.amax[2], amg);
-  atomic_count(&a.counts[3], nsg);
+  const uint32_t v[4] = {__float_as_uint(amds), nsat, __float_as_uint(amg), nsg};
+  const bool mx[4] = {true, false, true, false};
+  block_total(v, mx, a.part_dq + 4 * block_linear());
 }
 
 // key-major: dK = c s_dS sum_q val(dS_q) Q, dV = s_P s_dO sum_q val(P_q) val(dO_q), both cast at s_g
-__global__ __launch_bounds__(256) void te_dkv_kernel(TeArgs a) {
+__global__ __launch_bounds__(TE_BLOCK) void te_dkv_kernel(TeArgs a) {
   __shared__ __attribute__((aligned(16))) u16 sm[2][2][AT * AT];  // Q^T, dO_q^T
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, c16 = lane & 15;
   const int bh = blockIdx.x, kb = blockIdx.y;  // under the causal mask block 0 walks the most query blocks
@@ -295,22 +369,32 @@ __global__ __launch_bounds__(256) void te_dkv_kernel(TeArgs a) {
     tile_put_t(sm[st][0], pf[0]);
     tile_put_t(sm[st][1], pf[1]);
   };
+  // the lane's key's codes of one query block: bytes 16 g .. 16 g + 15 of its tile row (queries
+  // 32 s2 + 16 hh + 4 g + r at byte 8 s2 + 4 hh + r), loaded one step ahead of their use
+  auto load_codes = [&](int qb_, uint4& d, uint4& p) {
+    const int64_t o = fld_tile(a, bh, qb_, kb, nqb) + (int64_t)(16 * w + c16) * AT + 16 * g;
+    d = *(const uint4*)(a.dsq + o);
+    p = *(const uint4*)(a.pq + o);
+  };
   const int qb0 = a.causal ? kb : 0;
+  uint4 cd, cp;
+  load_codes(qb0, cd, cp);
   fetch(qb0 * AT);
   put(0);
   __syncthreads();
   for (int qb = qb0; qb < nqb; ++qb) {
     const int st = (qb - qb0) & 1, q0 = qb * AT;
     if (qb + 1 < nqb) fetch(q0 + AT);
-    const int64_t tile = fld_tile(a, bh, qb, kb, nqb) + (int64_t)(16 * w + c16) * AT;
+    uint4 nd = make_uint4(0, 0, 0, 0), np = make_uint4(0, 0, 0, 0);
+    if (qb + 1 < nqb) load_codes(qb + 1, nd, np);
+    const uint32_t dwd[4] = {cd.x, cd.y, cd.z, cd.w}, dwp[4] = {cp.x, cp.y, cp.z, cp.w};
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       // queries 32 s2 + 16 hh + 4 g + (0..3) of this lane's key, as the k index of the products
       float dsv[8], pv[8];
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        const uint32_t wd = *(const uint32_t*)(a.dsq + tile + 32 * s2 + 16 * hh + 4 * g);
-        const uint32_t wp = *(const uint32_t*)(a.pq + tile + 32 * s2 + 16 * hh + 4 * g);
+        const uint32_t wd = dwd[2 * s2 + hh], wp = dwp[2 * s2 + hh];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           dsv[4 * hh + r] = f8_val<BS_E5M2>(wd, r);
@@ -331,10 +415,13 @@ __global__ __launch_bounds__(256) void te_dkv_kernel(TeArgs a) {
         av[n] = mfma(tp, frag_t(sm[st][1], 16 * n + c16, s2, g), av[n]);
       }
     }
+    cd = nd;
+    cp = np;
     if (qb + 1 < nqb) put(st ^ 1);
     __syncthreads();
   }
   const float ck = a.scale * sdS, cv = sP * sdO;
+  const double rg = 1.0 / (double)sg;
   const int64_t numel = (int64_t)a.BH * a.S * AT;
   float amg = 0.0f;
   uint32_t nsg = 0;
@@ -347,8 +434,8 @@ __global__ __launch_bounds__(256) void te_dkv_kernel(TeArgs a) {
     for (int n = 0; n < 4; ++n) {
       prk[n] = ck * ak[n][r];
       prv[n] = cv * av[n][r];
-      yk[n] = prk[n] / sg;
-      yv[n] = prv[n] / sg;
+      yk[n] = div_scale(prk[n], rg);
+      yv[n] = div_scale(prv[n], rg);
       amg = fmaxf(amg, fmaxf(fabsf(prk[n]), fabsf(prv[n])));
     }
     uint32_t nk, nv;
@@ -365,20 +452,35 @@ __global__ __launch_bounds__(256) void te_dkv_kernel(TeArgs a) {
       }
     }
   }
-  atomic_amax(&a.amax[2], amg);
-  atomic_count(&a.counts[3], nsg);
+  const uint32_t v[2] = {__float_as_uint(amg), nsg};
+  const bool mx[2] = {true, false};
+  block_total(v, mx, a.part_dkv + 2 * block_linear());
 }
+
+constexpr int TE_PREP_BLOCKS = 256;  // grid-stride cast of dO: few blocks, few partials
 
 struct TeWs {
   u16 *dOq, *Qt, *Kt, *Vt, *dOt;
   float *m, *l, *D, *OP;
   uint8_t *dsq, *pq;
+  TeParts parts;
 };
+
+int prep_blocks(int64_t numel) {
+  return (int)std::min<int64_t>((numel / 8 + TE_BLOCK - 1) / TE_BLOCK, TE_PREP_BLOCKS);
+}
 
 TeWs carve_te(Carver& c, int64_t bh, int S, int causal, bool need_op) {
   TeWs w{};
   const int64_t Sp = round_up(S, AT), rows = bh * S;
   const int nqb = (int)(Sp / AT);
+  w.parts.n_prep = prep_blocks(rows * AT);
+  w.parts.n_d = (int)((rows + 63) / 64);
+  w.parts.n_dq = w.parts.n_dkv = (int)(bh * nqb);
+  w.parts.prep = c.take<uint32_t>(2 * (int64_t)w.parts.n_prep);
+  w.parts.d = c.take<uint32_t>(w.parts.n_d);
+  w.parts.dq = c.take<uint32_t>(4 * (int64_t)w.parts.n_dq);
+  w.parts.dkv = c.take<uint32_t>(2 * (int64_t)w.parts.n_dkv);
   w.dOq = c.take<u16>(rows * AT);
   for (u16** p : {&w.Qt, &w.Kt, &w.Vt, &w.dOt}) *p = c.take<u16>(bh * AT * Sp);
   for (float** p : {&w.m, &w.l, &w.D}) *p = c.take<float>(rows);
@@ -440,13 +542,11 @@ bs_status te_run(const TeIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
   if (!ws || ((uintptr_t)ws & 255) || ws_bytes < probe.used()) return BS_EWORKSPACE;
   Carver c(ws, ws_bytes);
   const TeWs w = carve_te(c, bh, io.S, causal, needs_op(io.source));
-  uint32_t* amax = (uint32_t*)io.amax;
 
   {
     ProfScope prof("te_prep", st);
-    te_init_kernel<<<1, 64, 0, st>>>(amax, io.counts);
-    te_prep_kernel<<<(unsigned)((numel / 4 + 255) / 256), 256, 0, st>>>((const u16*)io.dO, numel, io.scales, w.dOq,
-                                                                         amax, io.counts);
+    te_prep_kernel<<<(unsigned)w.parts.n_prep, TE_BLOCK, 0, st>>>((const u16*)io.dO, numel, io.scales, w.dOq,
+                                                                  w.parts.prep);
     BS_CHECK_LAUNCH();
   }
   {
@@ -459,9 +559,9 @@ bs_status te_run(const TeIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
   BS_TRY(launch_attn_fwd(fa, io.B, io.H, st));
   {
     ProfScope prof("te_d", st);
-    te_d_kernel<<<(unsigned)((rows + 63) / 64), 256, 0, st>>>(
+    te_d_kernel<<<(unsigned)((rows + 63) / 64), TE_BLOCK, 0, st>>>(
         w.dOq, w.OP, io.O, io.O_codes, io.O_scale, w.l, rows, io.source, io.thr, io.seed, io.trial,
-        io.store_id * 256u + 1u, io.scales, w.D, io.counts);
+        io.store_id * 256u + 1u, io.scales, w.D, w.parts.d);
     BS_CHECK_LAUNCH();
   }
   TeArgs a{};
@@ -491,19 +591,21 @@ bs_status te_run(const TeIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
   a.dQ = io.dQ;
   a.dK = io.dK;
   a.dV = io.dV;
-  a.amax = amax;
-  a.counts = io.counts;
+  a.part_dq = w.parts.dq;
+  a.part_dkv = w.parts.dkv;
   const dim3 grid((unsigned)bh, (unsigned)(Sp / AT));
   {
     ProfScope prof("te_dq", st);
-    te_dq_kernel<<<grid, 256, 0, st>>>(a);
+    te_dq_kernel<<<grid, TE_BLOCK, 0, st>>>(a);
     BS_CHECK_LAUNCH();
   }
   {
     ProfScope prof("te_dkv", st);
-    te_dkv_kernel<<<grid, 256, 0, st>>>(a);
+    te_dkv_kernel<<<grid, TE_BLOCK, 0, st>>>(a);
     BS_CHECK_LAUNCH();
   }
+  te_final_kernel<<<1, TE_BLOCK, 0, st>>>(w.parts, io.amax, io.counts);
+  BS_CHECK_LAUNCH();
   return BS_OK;
 }
 

@@ -71,7 +71,7 @@ def fl32(x):
     return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
 
 
-def compare(out, ref, Q, K, causal, c, sc):
+def compare(out, ref, Q, K, causal, c, sc, totals=True):
     B, H, S, dh = out["dQ"].shape
     flat = lambda t: to_np(t).reshape(B * H, *t.shape[2:])
     assert_rel(to_np(out["P"]), pstore.probabilities(Q.float().numpy(), K.float().numpy(), causal, c), TOL,
@@ -97,6 +97,8 @@ def compare(out, ref, Q, K, causal, c, sc):
             dist = np.abs(ref[name + "_pre"][miss] - mid)
             assert np.all(dist <= 1e-4 * np.abs(mid)), f"{name}: a cast differs away from a rounding midpoint"
     assert n_miss <= max(2, 1e-4 * 3 * pre[0].size), f"{n_miss} near-tie cast differences"
+    if not totals:
+        return
     amax = out["amax"].cpu().numpy()
     assert amax[0] == F32(ref["amax_dO"]) and amax[1] == F32(ref["amax_dS"])
     assert abs(amax[2] - ref["amax_grad"]) <= TOL * ref["amax_grad"]
@@ -148,3 +150,40 @@ def test_errors(lib):
     Q6 = torch.zeros(1, 1, 66, 64, dtype=torch.bfloat16, device=dev)
     with pytest.raises(lib.BspError):
         lib.te_attn_bwd(Q6, Q6, Q6, Q6, sc, source="P", ws=torch.empty(1 << 20, dtype=torch.uint8, device=dev))
+
+
+@pytest.mark.slow
+def test_full_size_sampled_heads(lib):
+    """B 4, H 16, S 1024, causal, D from the repair (the benchmark's launch): every output of two
+    sampled heads against the oracle; the amaxes and counts over the whole call."""
+    B, H, S, c, thr, store_id = 4, 16, 1024, 0.125, 0.9, 4
+    Q, K, V, dO = inputs(B, H, S, 11)
+    heads = [(0, 3), (3, 14)]
+    O32 = np.empty((B, H, S, 64), dtype=np.float32)
+    for b in range(B):                      # the forward's output, head batch by head batch
+        O32[b] = attention.forward(Q[b].float().numpy(), K[b].float().numpy(), V[b].float().numpy(), True, c)[0]
+    q = oq.qround(O32, fp8.E4M3, oq.SR, 11, 0, store_id * 256)
+    sub = lambda t, b, h: t[b:b + 1, h:h + 1]
+    sc = tuple(np.float32(x) for x in (1 / 448, np.abs(dO.float().numpy()).max() / 57344, 4e-5, 2e-5))
+    print(f"[te] full size B={B} H={H} S={S} repair scales={sc}", flush=True)
+    dev = torch.device("cuda")
+    out = lib.te_attn_bwd(Q.to(dev), K.to(dev), V.to(dev), dO.to(dev), torch.tensor(sc, device=dev),
+                          O=torch.from_numpy(O32).to(dev), O_codes=torch.from_numpy(q.codes).to(dev),
+                          O_scale=torch.tensor([q.scale], dtype=torch.float32, device=dev), source="repair",
+                          threshold=thr, causal=True, scale=c, seed=11, store_id=store_id, want_p=True, want_ds=True,
+                          want_codes=True, want_pre=True)
+    torch.cuda.synchronize()
+    for b, h in heads:
+        o = {k: (sub(v, b, h) if k != "pre" else v[:, b:b + 1, h:h + 1].contiguous())
+             for k, v in out.items() if v is not None and v.dim() == 4 or k == "pre"}
+        ref = te.check(*(sub(t, b, h).float().numpy() for t in (Q, K, V, dO)), P=o["P"].cpu().numpy(),
+                       dS=o["dS"].cpu().numpy(), O=sub(O32, b, h), O_codes=sub(q.codes, b, h), O_scale=q.scale,
+                       causal=True, c=c, scales=sc, source="repair", thr=np.float32(thr))
+        compare(o, ref, sub(Q, b, h), sub(K, b, h), True, c, sc, totals=False)
+    P = out["P"].cpu().numpy()
+    amax, counts = out["amax"].cpu().numpy(), out["counts"].cpu().numpy()
+    assert counts[0] == int((P.max(axis=-1) >= np.float32(thr)).sum())
+    del P
+    assert amax[0] == np.abs(dO.float().numpy()).max() and counts[1] == te.cast(dO.float().numpy(), sc[1], fp8.E5M2)[2]
+    dS = out["dS"].cpu().numpy()
+    assert amax[1] == np.abs(dS).max() and counts[2] == int((np.abs(dS / sc[2]) > np.float32(57344)).sum())
