@@ -332,7 +332,8 @@ bs_status bs_attn_pstore_policy(const void* Q, const void* Kt, const void* V, co
  *   B*H <= 65535. O [B,H,S,dh] fp32 (U, N; else nullable); O_codes [B,H,S,dh] uint8 E4M3
  *   (R, REPAIR) and O_scale [1] fp32 device (R, N, REPAIR): the forward's store of O.
  *   dQ, dK, dV [B,H,S,dh] fp32 out: the returned (cast) gradients, fl32(code value * s_g).
- *   amax [3] fp32 out: max |dO|, max |dS| (pre-cast), max of the pre-cast gradients.
+ *   amax [4] fp32 out, in the order of scales: max P (= max over rows of fl32(1/l)), max |dO|,
+ *   max |dS| (pre-cast), max of the pre-cast gradients.
  *   counts [4] uint32 out: rows with fl32(1/l) >= threshold; clamped entries of dO, of dS and of
  *   the three gradients.
  *   Nullable outputs: P_out, dS_out [B,H,S,S] fp32 (the realized P and pre-cast dS), P_codes,
@@ -344,6 +345,17 @@ bs_status bs_attn_pstore_policy(const void* Q, const void* Kt, const void* V, co
  * BS_ESHAPE for dh != 64 or S not a multiple of 4.
  * ---------------------------------------------------------------------------------- */
 typedef enum { BS_D_FROM_P = 0, BS_D_U = 1, BS_D_R = 2, BS_D_N = 3, BS_D_REPAIR = 4 } bs_d_source;
+
+/* bs_te_delayed_scales -- one step of delayed scaling for the four tensors of bs_te_attn_bwd
+ * (TE's recipe as the forks ran it, App. D.1: amax history of `len` steps, the maximum, margin 0).
+ *   amax [4] fp32 device (P, dO, dS, gradients: bs_te_attn_bwd's amax output); history [4][len]
+ *   fp32 device, a ring buffer the caller zeroes once; scales [4] fp32 device, in/out.
+ * The step's amax is stored at history[i][step % len]; then scales[i] = fl32(m_i / FMAX_i) with
+ * m_i the largest |amax| in history i (FMAX 448 for P, 57344 for the others), left unchanged when
+ * m_i is zero, infinite or NaN (a non-finite amax stays in the history). len >= 1, step >= 0.
+ * Returns BS_EINVAL for a NULL pointer or a bad len / step. No workspace. */
+bs_status bs_te_delayed_scales(const float* amax, float* history, int len, int64_t step, float* scales,
+                               void* stream);
 
 size_t bs_te_attn_workspace_size(int B, int H, int S, int dh, int causal, bs_d_source source);
 bs_status bs_te_attn_bwd(const void* Q, const void* Kt, const void* V, const void* dO, int B, int H, int S, int dh,

@@ -12,9 +12,10 @@ correction term D is computed from the saved output:
   * dS is cast to E5M2 at its delayed scale s_dS; dQ = c dS_q K and dK = c dS_q^T Q;
   * dQ, dK and dV are cast to E5M2 at the gradients' delayed scale s_g before they return.
 
-Three delayed scales (dO, dS, the gradients) come from histories of past amaxes (TE keeps the
-largest of 1024, margin 0, App. D.1): they are inputs here, and the call reports the amaxes it
-saw (of dO, of dS and of the pre-cast gradients) for the caller's history. Every cast rounds to
+The delayed scales (P's from the forward; dO, dS, the gradients) come from histories of past
+amaxes (TE keeps the largest of 1024, margin 0, App. D.1): they are inputs of the backward,
+which reports the amaxes it saw (P, dO, the pre-cast dS and gradients) for the histories;
+``delayed_scales`` is one step of that recipe. Every cast rounds to
 nearest even, clamps |x/s| > FMAX to FMAX and counts it (the store of reading 1 at a given
 scale).
 
@@ -40,6 +41,24 @@ from . import fp8, qround
 from .norm_store import fresh_values
 
 D_SOURCES = ("P", "U", "R", "N", "repair")
+FMAX = (448.0, 57344.0, 57344.0, 57344.0)  # P in E4M3; dO, dS and the gradients in E5M2
+
+
+def delayed_scales(history, amax, step, scales):
+    """One step of delayed scaling (App. D.1: history of past amaxes, their maximum, margin 0).
+
+    history [4, len] fp32, amax [4] (P, dO, dS, gradients), scales [4] fp32. The step's amax is
+    recorded at slot step % len; a tensor's new scale is fl32(largest |amax| in its history /
+    FMAX), or its old scale when that largest amax is zero or not finite. Returns the new
+    (history, scales)."""
+    h = np.array(history, dtype=np.float32, copy=True)
+    h[:, step % h.shape[1]] = np.asarray(amax, dtype=np.float32)
+    new = np.array(scales, dtype=np.float32, copy=True)
+    for i in range(h.shape[0]):
+        m = np.float32(np.max(np.abs(h[i])))
+        if np.isfinite(m) and m > 0:
+            new[i] = np.float32(m / np.float32(FMAX[i]))
+    return h, new
 
 
 def cast(x, s, fmt):
@@ -122,6 +141,7 @@ def check(Q, Kt, V, dO, *, P, dS=None, O, O_codes, O_scale, causal=True, c=None,
         out["sat_rows"].append(int((p.max(axis=-1) >= thr).sum()))
     for name in ("dS", "D", "dQ_pre", "dK_pre", "dV_pre", "dQ", "dK", "dV", "dS_codes"):
         out[name] = np.stack(out[name])
+    out["amax_P"] = float(np.max([P[b, h].max() for b, h in heads]))
     out["amax_dS"] = float(np.abs(out["dS"] if dS is None else np.asarray(dS)[[b for b, _ in heads], [h for _, h in heads]]).max())
     out["amax_grad"] = float(max(np.abs(out[k]).max() for k in ("dQ_pre", "dK_pre", "dV_pre")))
     return out

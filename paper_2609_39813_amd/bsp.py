@@ -80,6 +80,7 @@ _te_ws = _sig("bs_te_attn_workspace_size", _sz, [_int] * 6)
 _te = _sig("bs_te_attn_bwd", _int,
            [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _vp, _vp, _vp, _int, _f32, _vp, _u64, _u32, _u32,
             _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp])
+_te_sc = _sig("bs_te_delayed_scales", _int, [_vp, _vp, _int, _i64, _vp, _vp])
 _lsm_ws = _sig("bs_logsoftmax_check_workspace_size", _sz, [_i64, _int, _int])
 _lsm = _sig("bs_logsoftmax_reuse_check", _int,
             [_vp, _vp, _i64, _int, ctypes.c_double, _int, _u64, _u32, _int, _vp, _vp, _sz, _vp])
@@ -141,7 +142,7 @@ def profile_read(kernel=None):
 EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
             "bs_policy_bias_estimate", "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
             "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_attn_pstore_workspace_size", "bs_attn_pstore_policy", "bs_attn_level2_policy",
-            "bs_te_attn_workspace_size", "bs_te_attn_bwd",
+            "bs_te_attn_workspace_size", "bs_te_attn_bwd", "bs_te_delayed_scales",
             "bs_logsoftmax_check_workspace_size", "bs_logsoftmax_reuse_check",
             "bs_rmsnorm_linear_grid_workspace_size", "bs_rmsnorm_linear_grid_fwd_bwd", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
             "bs_decoder_layer_workspace_size", "bs_decoder_layer_policy", "bs_profile_enable", "bs_profile_read"]
@@ -469,7 +470,7 @@ def te_attn_bwd(Q, Kt, V, dO, scales, *, O=None, O_codes=None, O_scale=None, sou
     out = {"dQ": torch.empty(shp, dtype=torch.float32, device=dev),
            "dK": torch.empty(shp, dtype=torch.float32, device=dev),
            "dV": torch.empty(shp, dtype=torch.float32, device=dev),
-           "amax": torch.empty(3, dtype=torch.float32, device=dev),
+           "amax": torch.empty(4, dtype=torch.float32, device=dev),
            "counts": torch.empty(4, dtype=torch.int32, device=dev),
            "P": sq(torch.float32, want_p), "dS": sq(torch.float32, want_ds),
            "P_codes": sq(torch.uint8, want_codes), "dS_codes": sq(torch.uint8, want_codes),
@@ -481,6 +482,14 @@ def te_attn_bwd(Q, Kt, V, dO, scales, *, O=None, O_codes=None, O_scale=None, sou
                _p(out["dV"]), _p(out["amax"]), _p(out["counts"]), _p(out["P"]), _p(out["dS"]), _p(out["P_codes"]),
                _p(out["dS_codes"]), _p(out["pre"]), _p(ws), ws.numel(), _stream()), "bs_te_attn_bwd")
     return out
+
+
+def te_delayed_scales(amax, history, step, scales):
+    """One step of delayed scaling (bs_te_delayed_scales): history [4, len] and scales [4] are
+    updated in place."""
+    _dev_check(amax, history, scales)
+    _check(_te_sc(_p(amax), _p(history), history.shape[1], step, _p(scales), _stream()), "bs_te_delayed_scales")
+    return scales
 
 
 def linear_bwd_policy(X, W, dY, *, fmt="e5m2", sharings=("shared", "per_use"), K=16, seed=0, store_id=0,

@@ -105,8 +105,8 @@ __device__ __forceinline__ int block_linear() { return (int)(blockIdx.y * gridDi
 
 // Per-block partials of every kernel: [n][width] words each
 struct TeParts {
-  uint32_t *prep, *d, *dq, *dkv;  // widths 2 (amax dO, clamps dO), 1 (rows), 4 (amax dS, clamps dS,
-  int n_prep, n_d, n_dq, n_dkv;   // amax gradients, clamps gradients), 2 (amax gradients, clamps)
+  uint32_t *prep, *d, *dq, *dkv;  // widths 2 (amax dO, clamps dO), 2 (rows, amax P), 4 (amax dS, clamps
+  int n_prep, n_d, n_dq, n_dkv;   // dS, amax gradients, clamps gradients), 2 (amax gradients, clamps)
 };
 
 // column `col` of an [n][width] partial array reduced over the block (result in every thread)
@@ -126,14 +126,15 @@ __device__ uint32_t reduce_col(const uint32_t* p, int n, int width, int col, boo
 
 __global__ __launch_bounds__(TE_BLOCK) void te_final_kernel(TeParts q, float* amax, uint32_t* counts) {
   const uint32_t a0 = reduce_col(q.prep, q.n_prep, 2, 0, true), c1 = reduce_col(q.prep, q.n_prep, 2, 1, false);
-  const uint32_t c0 = reduce_col(q.d, q.n_d, 1, 0, false);
+  const uint32_t c0 = reduce_col(q.d, q.n_d, 2, 0, false), ap = reduce_col(q.d, q.n_d, 2, 1, true);
   const uint32_t a1 = reduce_col(q.dq, q.n_dq, 4, 0, true), c2 = reduce_col(q.dq, q.n_dq, 4, 1, false);
   const uint32_t a2 = max(reduce_col(q.dq, q.n_dq, 4, 2, true), reduce_col(q.dkv, q.n_dkv, 2, 0, true));
   const uint32_t c3 = reduce_col(q.dq, q.n_dq, 4, 3, false) + reduce_col(q.dkv, q.n_dkv, 2, 1, false);
   if (threadIdx.x == 0) {
-    amax[0] = __uint_as_float(a0);
-    amax[1] = __uint_as_float(a1);
-    amax[2] = __uint_as_float(a2);
+    amax[0] = __uint_as_float(ap);
+    amax[1] = __uint_as_float(a0);
+    amax[2] = __uint_as_float(a1);
+    amax[3] = __uint_as_float(a2);
     counts[0] = c0;
     counts[1] = c1;
     counts[2] = c2;
@@ -187,7 +188,8 @@ __global__ __launch_bounds__(TE_BLOCK) void te_d_kernel(const u16* __restrict__ 
   const int sub = threadIdx.x & 3;
   const bool ok = row < rows;
   const F8 f = f8_format(BS_E4M3);
-  const bool sat = ok && 1.0f / l[ok ? row : 0] >= thr;
+  const float pmax = ok ? 1.0f / l[row] : 0.0f;  // the row's largest probability
+  const bool sat = ok && pmax >= thr;
   const int src = source == BS_D_REPAIR ? (sat ? BS_D_FROM_P : BS_D_R) : source;
   double acc = 0.0;
   if (ok) {
@@ -231,9 +233,9 @@ __global__ __launch_bounds__(TE_BLOCK) void te_d_kernel(const u16* __restrict__ 
   acc += __shfl_xor(acc, 1, 64);
   acc += __shfl_xor(acc, 2, 64);
   if (ok && sub == 0) D[row] = (float)((double)sc[1] * acc);
-  const uint32_t v[1] = {(ok && sub == 0 && sat) ? 1u : 0u};
-  const bool mx[1] = {false};
-  block_total(v, mx, part + block_linear());
+  const uint32_t v[2] = {(ok && sub == 0 && sat) ? 1u : 0u, __float_as_uint(pmax)};
+  const bool mx[2] = {false, true};
+  block_total(v, mx, part + 2 * block_linear());
 }
 
 // query-major: dS = P (dP - D), its E5M2 codes at s_dS and P's E4M3 codes at s_P (tile-major),
@@ -459,6 +461,32 @@ __global__ __launch_bounds__(TE_BLOCK) void te_dkv_kernel(TeArgs a) {
 
 constexpr int TE_PREP_BLOCKS = 256;  // grid-stride cast of dO: few blocks, few partials
 
+// One step of delayed scaling for the four tensors of the call (P in E4M3; dO, dS and the
+// gradients in E5M2): the step's amax enters the ring history at step % len, and the scale for
+// the next step is the largest amax in the history divided by FMAX (fl32), kept unchanged when
+// that largest amax is zero or not finite. Block i serves tensor i.
+__global__ __launch_bounds__(TE_BLOCK) void te_scales_kernel(const float* amax, float* history, int len, int pos,
+                                                             float* scales) {
+  __shared__ uint32_t red[TE_BLOCK / 64];
+  const int i = blockIdx.x;
+  const float a = amax[i];
+  float* h = history + (int64_t)i * len;
+  // non-negative finite amaxes order as their bits; a NaN (or infinite) one wins the max as well
+  uint32_t m = threadIdx.x == 0 ? __float_as_uint(fabsf(a)) : 0u;
+  for (int j = threadIdx.x; j < len; j += TE_BLOCK)
+    if (j != pos) m = max(m, __float_as_uint(fabsf(h[j])));
+  m = wave_max_u32(m);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < TE_BLOCK / 64; ++k) m = max(m, red[k]);
+    h[pos] = a;
+    const float am = __uint_as_float(m);
+    const float fm = i == 0 ? kE4M3Max : kE5M2Max;
+    if (am > 0.0f && am <= 3.402823466e38f) scales[i] = am / fm;
+  }
+}
+
 struct TeWs {
   u16 *dOq, *Qt, *Kt, *Vt, *dOt;
   float *m, *l, *D, *OP;
@@ -478,7 +506,7 @@ TeWs carve_te(Carver& c, int64_t bh, int S, int causal, bool need_op) {
   w.parts.n_d = (int)((rows + 63) / 64);
   w.parts.n_dq = w.parts.n_dkv = (int)(bh * nqb);
   w.parts.prep = c.take<uint32_t>(2 * (int64_t)w.parts.n_prep);
-  w.parts.d = c.take<uint32_t>(w.parts.n_d);
+  w.parts.d = c.take<uint32_t>(2 * (int64_t)w.parts.n_d);
   w.parts.dq = c.take<uint32_t>(4 * (int64_t)w.parts.n_dq);
   w.parts.dkv = c.take<uint32_t>(2 * (int64_t)w.parts.n_dkv);
   w.dOq = c.take<u16>(rows * AT);
@@ -617,6 +645,14 @@ extern "C" {
 
 size_t bs_te_attn_workspace_size(int B, int H, int S, int dh, int causal, bs_d_source source) {
   return te_ws_size(B, H, S, dh, causal, (int)source);
+}
+
+bs_status bs_te_delayed_scales(const float* amax, float* history, int len, int64_t step, float* scales,
+                               void* stream) {
+  if (!amax || !history || !scales || len < 1 || step < 0) return BS_EINVAL;
+  te_scales_kernel<<<4, TE_BLOCK, 0, (hipStream_t)stream>>>(amax, history, len, (int)(step % len), scales);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
 }
 
 bs_status bs_te_attn_bwd(const void* Q, const void* Kt, const void* V, const void* dO, int B, int H, int S, int dh,

@@ -100,8 +100,8 @@ def compare(out, ref, Q, K, causal, c, sc, totals=True):
     if not totals:
         return
     amax = out["amax"].cpu().numpy()
-    assert amax[0] == F32(ref["amax_dO"]) and amax[1] == F32(ref["amax_dS"])
-    assert abs(amax[2] - ref["amax_grad"]) <= TOL * ref["amax_grad"]
+    assert amax[0] == F32(ref["amax_P"]) and amax[1] == F32(ref["amax_dO"]) and amax[2] == F32(ref["amax_dS"])
+    assert abs(amax[3] - ref["amax_grad"]) <= TOL * ref["amax_grad"]
     counts = out["counts"].cpu().numpy()
     assert counts[0] == sum(ref["sat_rows"])
     assert counts[1] == ref["sat_dO"] and counts[2] == ref["sat_dS"]
@@ -137,6 +137,59 @@ def test_repair_selects_saturated_rows(lib):
 @pytest.mark.parametrize("S", [4, 64])
 def test_small_and_single_tile(lib, S):
     run_case(lib, 1, 1, S, source="R", seed=6 + S)
+
+
+def test_delayed_scale_steps(lib):
+    """bs_te_delayed_scales against the oracle's step over a sequence with zeros, an infinity and
+    a NaN, bit for bit (history and scales)."""
+    rng = np.random.default_rng(8)
+    L, T = 5, 14
+    seq = rng.uniform(1e-3, 50.0, size=(T, 4)).astype(np.float32)
+    seq[3:9, 0] = 0.0
+    seq[7, 2] = np.inf
+    seq[9, 3] = np.nan
+    dev = torch.device("cuda")
+    hist_g, sc_g = torch.zeros(4, L, device=dev), torch.ones(4, device=dev)
+    hist_o, sc_o = np.zeros((4, L), np.float32), np.ones(4, np.float32)
+    for t in range(T):
+        lib.te_delayed_scales(torch.from_numpy(seq[t]).to(dev), hist_g, t, sc_g)
+        hist_o, sc_o = te.delayed_scales(hist_o, seq[t], t, sc_o)
+        assert np.array_equal(sc_g.cpu().numpy(), sc_o), t
+        assert np.array_equal(hist_g.cpu().numpy(), hist_o, equal_nan=True), t
+
+
+def test_delayed_scaling_loop(lib):
+    """Three backward steps whose scales come from the amax history of the steps before (the
+    first from a warm-up amax): each step against the oracle, the library's scales against the
+    oracle's history of its own amaxes (P, dO, dS bit for bit; the gradients' within 1e-5)."""
+    B, H, S, c, store_id, L = 1, 2, 136, 0.125, 4, 16
+    dev = torch.device("cuda")
+    hist_g, hist_o = torch.zeros(4, L, device=dev), np.zeros((4, L), np.float32)
+    sc_o = np.ones(4, np.float32)
+    warm = np.array([1.0, 3.0, 5e-3, 1.0], np.float32)
+    hist_o, sc_o = te.delayed_scales(hist_o, warm, 0, sc_o)
+    sc_g = torch.ones(4, device=dev)
+    lib.te_delayed_scales(torch.from_numpy(warm).to(dev), hist_g, 0, sc_g)
+    for step in range(1, 4):
+        Q, K, V, dO = inputs(B, H, S, 20 + step)
+        O32, _, q = forward_store(Q, K, V, True, c, step, store_id)
+        sc = tuple(np.float32(x) for x in sc_g.cpu().numpy())
+        assert sc[:3] == tuple(sc_o[:3]) and abs(sc[3] - sc_o[3]) <= 1e-5 * sc_o[3]
+        print(f"[te] delayed-scaling step {step} scales={sc}", flush=True)
+        out = lib.te_attn_bwd(Q.to(dev), K.to(dev), V.to(dev), dO.to(dev), sc_g.clone(),
+                              O=torch.from_numpy(O32).to(dev), O_codes=torch.from_numpy(q.codes).to(dev),
+                              O_scale=torch.tensor([q.scale], dtype=torch.float32, device=dev), source="R",
+                              causal=True, scale=c, seed=step, store_id=store_id, want_p=True, want_ds=True,
+                              want_codes=True, want_pre=True)
+        torch.cuda.synchronize()
+        ref = te.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.float().numpy(),
+                       P=out["P"].cpu().numpy(), dS=out["dS"].cpu().numpy(), O=O32, O_codes=q.codes,
+                       O_scale=q.scale, causal=True, c=c, scales=sc, source="R", thr=F32(0.9), seed=step,
+                       store_id=store_id)
+        compare(out, ref, Q, K, True, c, sc)
+        lib.te_delayed_scales(out["amax"], hist_g, step, sc_g)
+        hist_o, sc_o = te.delayed_scales(hist_o, [ref["amax_P"], ref["amax_dO"], ref["amax_dS"], ref["amax_grad"]],
+                                         step, sc_o)
 
 
 def test_errors(lib):
@@ -182,8 +235,8 @@ def test_full_size_sampled_heads(lib):
         compare(o, ref, sub(Q, b, h), sub(K, b, h), True, c, sc, totals=False)
     P = out["P"].cpu().numpy()
     amax, counts = out["amax"].cpu().numpy(), out["counts"].cpu().numpy()
-    assert counts[0] == int((P.max(axis=-1) >= np.float32(thr)).sum())
+    assert counts[0] == int((P.max(axis=-1) >= np.float32(thr)).sum()) and amax[0] == P.max()
     del P
-    assert amax[0] == np.abs(dO.float().numpy()).max() and counts[1] == te.cast(dO.float().numpy(), sc[1], fp8.E5M2)[2]
+    assert amax[1] == np.abs(dO.float().numpy()).max() and counts[1] == te.cast(dO.float().numpy(), sc[1], fp8.E5M2)[2]
     dS = out["dS"].cpu().numpy()
-    assert amax[1] == np.abs(dS).max() and counts[2] == int((np.abs(dS / sc[2]) > np.float32(57344)).sum())
+    assert amax[2] == np.abs(dS).max() and counts[2] == int((np.abs(dS / sc[2]) > np.float32(57344)).sum())

@@ -72,3 +72,26 @@ def test_repair_selects_saturated_rows():
     assert 0 < sat.sum() < len(sat) and rep["sat_rows"][0] == sat.sum()
     np.testing.assert_array_equal(rep["D"][0][sat], fromP["D"][0][sat])
     np.testing.assert_array_equal(rep["D"][0][~sat], fromR["D"][0][~sat])
+
+
+def test_delayed_scales_are_the_window_maximum():
+    """The ring history gives, at every step, the largest amax of the last `len` steps over FMAX,
+    and keeps the old scale while that window holds only zeros (or a non-finite value)."""
+    rng = np.random.default_rng(3)
+    L, T = 4, 23
+    seq = rng.uniform(0.1, 10.0, size=(T, 4)).astype(np.float32)
+    seq[6:12, 1] = 0.0                     # a window of zeros for dO: its scale must hold
+    seq[15, 2] = np.inf                    # a non-finite amax blocks dS's updates for L steps
+    hist, scales = np.zeros((4, L), np.float32), np.ones(4, np.float32)
+    prev = scales
+    for t in range(T):
+        hist, scales = te.delayed_scales(hist, seq[t], t, scales)
+        for i in range(4):
+            win = seq[max(0, t - L + 1):t + 1, i]
+            m = win.max()
+            if np.isfinite(m) and m > 0:
+                assert scales[i] == np.float32(m / np.float32(te.FMAX[i]))
+            else:
+                assert scales[i] == prev[i]
+        prev = scales
+    assert te.FMAX[0] == fp8.E4M3.fmax and te.FMAX[1] == fp8.E5M2.fmax
