@@ -272,7 +272,7 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
         yv = torch.randint(0, C_, (rows_,), generator=gz, dtype=torch.int32).to(dev)
         ws = torch.empty(max(bsp._lsm_ws(rows_, C_, K_), 256), dtype=torch.uint8, device=dev)
         wall, t = _timed(bsp, torch, lambda: bsp.logsoftmax_reuse_check(z, yv, eps=0.1, K=K_, seed=7, ws=ws),
-                         ("lsm_prep", "lsm_trial"), reps)
+                         ("lsm_prep", "lsm_trial", "lsm_reduce"), reps)
         et = rows_ * C_ * K_
         st_ = bsp.logsoftmax_reuse_check(z, yv, eps=0.1, K=K_, seed=7, ws=ws).cpu().tolist()
         out[tag] = {"call_ms": round(wall * 1e3, 4), "kernel_ms": {k: round(v, 4) for k, v in t.items()},

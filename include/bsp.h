@@ -486,7 +486,7 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* w, cons
  *   ("fresh_count", "fresh_count_se", "fresh_count_kappa", "amax", "quantize", "gemm",
  *   "rmsnorm_fwd", "attn_fwd", "attn_bwd", "attn_l2", "pstore_fwd", "pstore_rows", "pstore_dq",
  *   "pstore_dkv", "lsm_prep", "lsm_trial", "grid_store", "grid_fresh", "te_prep", "te_d", "te_dq",
- *   "te_dkv");
+ *   "te_dkv", "lsm_reduce");
  *   bs_profile_enable(0) stops and frees them. bs_profile_read waits for the recorded
  *   events of `kernel` (NULL: all) and returns their summed elapsed time and count.
  *   Return values are bs_status codes.

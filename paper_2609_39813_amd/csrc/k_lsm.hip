@@ -92,41 +92,73 @@ __global__ __launch_bounds__(64) void lsm_trial_kernel(const double* __restrict_
 }
 
 // per statistic: t_k = sum over rows (row order) / (rows C); mean and se over trials
+constexpr int LSM_RT = 64;  // trials per block of the first reduction stage
+
+// mean over rows and classes of statistic c in trial k: one wave, rows lane-strided, combined by
+// a fixed xor tree (every lane ends with the total)
+__device__ __forceinline__ double lsm_trial_mean(const double* __restrict__ part, int64_t rows, int C, int K, int c,
+                                                 int k) {
+  const int lane = threadIdx.x & 63;
+  double t = 0.0;
+  for (int64_t i = lane; i < rows; i += 64) t += part[((int64_t)c * K + k) * rows + i];
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) t += __shfl_xor(t, off, 64);
+  return t / ((double)rows * C);
+}
+
+// first stage: block (j, c) takes trials 64 j .. 64 j + 63 of statistic c and writes their sums of
+// d_k = m_k - m_0 and d_k^2 (shifted by trial 0's mean m_0, which block (0, c) also writes)
 __global__ __launch_bounds__(256) void lsm_reduce_kernel(const double* __restrict__ part, int64_t rows, int C, int K,
-                                                         double* __restrict__ stats) {
-  const int c = blockIdx.x;
-  __shared__ double red[256];
-  double s1 = 0.0, s2 = 0.0, t0 = 0.0;
-  // trial 0's value, as the shift of the sums (every thread needs it)
-  for (int64_t i = 0; i < rows; ++i) t0 += part[(int64_t)c * K * rows + i];
-  t0 /= (double)rows * C;
-  for (int k = threadIdx.x; k < K; k += blockDim.x) {
-    double t = 0.0;
-    for (int64_t i = 0; i < rows; ++i) t += part[((int64_t)c * K + k) * rows + i];
-    const double d = t / ((double)rows * C) - t0;
+                                                         double* __restrict__ acc, double* __restrict__ m0) {
+  const int c = blockIdx.y, w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const double t0 = lsm_trial_mean(part, rows, C, K, c, 0);
+  double s1 = 0.0, s2 = 0.0;
+  for (int j = w; j < LSM_RT; j += 4) {
+    const int k = blockIdx.x * LSM_RT + j;
+    if (k >= K) break;  // wave-uniform
+    const double d = lsm_trial_mean(part, rows, C, K, c, k) - t0;
     s1 += d;
     s2 += d * d;
   }
-  // fixed-order block sums
-  red[threadIdx.x] = s1;
-  __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if ((int)threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
-    __syncthreads();
+  __shared__ double red[2][4];
+  if (lane == 0) {
+    red[0][w] = s1;
+    red[1][w] = s2;
   }
-  const double S1 = red[0];
   __syncthreads();
-  red[threadIdx.x] = s2;
+  if (threadIdx.x == 0) {
+    double* o = acc + 2 * ((int64_t)c * gridDim.x + blockIdx.x);
+    o[0] = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    o[1] = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    if (blockIdx.x == 0) m0[c] = t0;
+  }
+}
+
+// second stage: block c sums its nb partials (thread-strided, then a fixed tree) into the mean
+// and its standard error over the K trials
+__global__ __launch_bounds__(256) void lsm_final_kernel(const double* __restrict__ acc, const double* __restrict__ m0,
+                                                        int nb, int K, double* __restrict__ stats) {
+  const int c = blockIdx.x;
+  __shared__ double red[2][256];
+  double s1 = 0.0, s2 = 0.0;
+  for (int j = threadIdx.x; j < nb; j += 256) {
+    s1 += acc[2 * ((int64_t)c * nb + j)];
+    s2 += acc[2 * ((int64_t)c * nb + j) + 1];
+  }
+  red[0][threadIdx.x] = s1;
+  red[1][threadIdx.x] = s2;
   __syncthreads();
   for (int off = 128; off > 0; off >>= 1) {
-    if ((int)threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
+    if ((int)threadIdx.x < off) {
+      red[0][threadIdx.x] += red[0][threadIdx.x + off];
+      red[1][threadIdx.x] += red[1][threadIdx.x + off];
+    }
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    const double S2 = red[0];
-    const double mean = t0 + S1 / K;
+    const double S1 = red[0][0], S2 = red[1][0];
     const double var = K > 1 ? fmax(S2 - S1 * S1 / K, 0.0) / (K - 1) : 0.0;
-    stats[2 * c] = mean;
+    stats[2 * c] = m0[c] + S1 / K;
     stats[2 * c + 1] = sqrt(var / K);
   }
 }
@@ -138,6 +170,8 @@ size_t lsm_ws_size(int64_t rows, int C, int K) {
   Carver c;
   c.take<double>(rows * C);
   c.take<double>((int64_t)4 * K * rows);
+  c.take<double>((int64_t)8 * ((K + LSM_RT - 1) / LSM_RT));
+  c.take<double>(4);
   return c.used();
 }
 
@@ -161,6 +195,9 @@ bs_status bs_logsoftmax_reuse_check(const double* logits, const int32_t* target,
   Carver c(ws, ws_bytes);
   double* l = c.take<double>(rows * C);
   double* part = c.take<double>((int64_t)4 * K * rows);
+  const int nb = (K + LSM_RT - 1) / LSM_RT;
+  double* acc = c.take<double>((int64_t)8 * nb);
+  double* m0 = c.take<double>(4);
   {
     ProfScope prof("lsm_prep", st);
     lsm_prep_kernel<<<(unsigned)rows, 64, 0, st>>>(logits, rows, C, l);
@@ -174,8 +211,12 @@ bs_status bs_logsoftmax_reuse_check(const double* logits, const int32_t* target,
                                           base + 1, part);
     BS_CHECK_LAUNCH();
   }
-  lsm_reduce_kernel<<<4, 256, 0, st>>>(part, rows, C, K, stats);
-  BS_CHECK_LAUNCH();
+  {
+    ProfScope prof("lsm_reduce", st);
+    lsm_reduce_kernel<<<dim3((unsigned)nb, 4), 256, 0, st>>>(part, rows, C, K, acc, m0);
+    lsm_final_kernel<<<4, 256, 0, st>>>(acc, m0, nb, K, stats);
+    BS_CHECK_LAUNCH();
+  }
   return BS_OK;
 }
 
