@@ -19,6 +19,10 @@ struct NormPlaneArgs {
   int64_t ldo;
 };
 
+// rows per block of the gain use's column partial sums (the partial array holds one row of
+// partials per tile of GAIN_RT rows)
+constexpr int GAIN_RT = 16;
+
 template <typename XT>
 struct GainArgs {
   const XT* X;
@@ -82,6 +86,17 @@ bs_status launch_trial_accum(const float* delta, int nb, int k0, int64_t m, floa
                              hipStream_t st);
 // se = sqrt(max(S2 - S1^2 / K, 0) / (K - 1) / K) (0 for K = 1)
 bs_status launch_trial_se(const double* S1, const double* S2, int K, int64_t m, float* se, hipStream_t st);
+
+constexpr int COMBINE_MAX_POL = 16;
+struct CombineMulti {
+  const float* ref;
+  int n_pol, vec;
+  const float* bias[COMBINE_MAX_POL];
+  const float* se[COMBINE_MAX_POL];
+  const float* alt[COMBINE_MAX_POL];
+  float *mean, *bias_out, *se_out;  // bases of [n_pol][n] outputs (nullable)
+};
+bs_status launch_combine_multi(CombineMulti c, int64_t n, hipStream_t st);
 
 bs_status launch_combine_alt(const float* ref, const float* alt, int64_t n, float* mean_out, float* bias_out,
                              float* se_out, hipStream_t st);

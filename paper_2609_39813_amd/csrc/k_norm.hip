@@ -202,23 +202,23 @@ __global__ __launch_bounds__(256) void gain_partials_kernel(GainArgs<T> a) {
   const double s = *a.scale;
   const float sf = *a.scale;
   const double rsf = 1.0 / (double)sf;
-  const double g = a.gain[j];
+  const double g = a.gain[j], ig = 1.0 / g;
   double q0 = 0.0, q1 = 0.0, q2 = 0.0;
-  const int64_t tend = (rt + 1) * 64 < a.T ? (rt + 1) * 64 : a.T;
-  for (int64_t t = rt * 64; t < tend; ++t) {
+  const int64_t tend = (rt + 1) * GAIN_RT < a.T ? (rt + 1) * GAIN_RT : a.T;
+  for (int64_t t = rt * GAIN_RT; t < tend; ++t) {
     const int64_t e = t * a.d + j;
     const float z = load_f32(a.X, e) * a.rstd[t];
     const double du = a.du[e];
     const double gz = g * (double)z;
     q0 += (double)z * du;
-    if (a.want_r) q1 += (s * (double)f8_value(a.codes[e], a.f) - gz) / g * du;
+    if (a.want_r) q1 += (s * (double)f8_value(a.codes[e], a.f) - gz) * ig * du;
     if (a.counts) {
       const float y = div_scale(a.u[e], rsf);
       const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
       const double step = f8_step(b);
       double mv = (double)b.mi * step + (double)a.counts[e] * step / a.K;
       if (signbit(y)) mv = -mv;
-      q2 += (s * mv - gz) / g * du;
+      q2 += (s * mv - gz) * ig * du;
     }
   }
   const int64_t nrt = gridDim.y;
@@ -227,28 +227,34 @@ __global__ __launch_bounds__(256) void gain_partials_kernel(GainArgs<T> a) {
   a.part[(2 * nrt + rt) * a.d + j] = q2;
 }
 
-// Sums the row-tile partials of each column: 4 segments of row tiles per column, each
-// summed in order, then the segments in order (fixed order, deterministic).
+// Sums the row-tile partials of each column: 16 segments of row tiles per column, each summed
+// in order, then the segments by a fixed tree (deterministic). 16 columns per block.
 __global__ __launch_bounds__(256) void gain_final_kernel(const double* __restrict__ part, int64_t nrt, int64_t d,
                                                          float* __restrict__ ref, float* __restrict__ bias_r,
                                                          float* __restrict__ bias_n) {
-  __shared__ double red[3][4][64];
-  const int c = threadIdx.x & 63, sgi = threadIdx.x >> 6;
-  const int64_t j = (int64_t)blockIdx.x * 64 + c;
-  const int64_t per = (nrt + 3) / 4;
+  __shared__ double red[3][16][17];
+  const int c = threadIdx.x & 15, sgi = threadIdx.x >> 4;
+  const int64_t j = (int64_t)blockIdx.x * 16 + c;
+  const int64_t per = (nrt + 15) / 16;
   const int64_t r0 = sgi * per, r1 = (r0 + per) < nrt ? (r0 + per) : nrt;
   double q[3] = {0.0, 0.0, 0.0};
   if (j < d)
-    for (int i = 0; i < 3; ++i)
-      for (int64_t rt = r0; rt < r1; ++rt) q[i] += part[(i * nrt + rt) * d + j];
+    for (int64_t rt = r0; rt < r1; ++rt)
+#pragma unroll
+      for (int i = 0; i < 3; ++i) q[i] += part[(i * nrt + rt) * d + j];
+#pragma unroll
   for (int i = 0; i < 3; ++i) red[i][sgi][c] = q[i];
   __syncthreads();
+  for (int h = 8; h >= 1; h >>= 1) {
+    if (sgi < h)
+#pragma unroll
+      for (int i = 0; i < 3; ++i) red[i][sgi][c] += red[i][sgi + h][c];
+    __syncthreads();
+  }
   if (sgi == 0 && j < d) {
-    double t[3];
-    for (int i = 0; i < 3; ++i) t[i] = ((red[i][0][c] + red[i][1][c]) + red[i][2][c]) + red[i][3][c];
-    ref[j] = (float)t[0];
-    if (bias_r) bias_r[j] = (float)t[1];
-    if (bias_n) bias_n[j] = (float)t[2];
+    ref[j] = (float)red[0][0][c];
+    if (bias_r) bias_r[j] = (float)red[1][0][c];
+    if (bias_n) bias_n[j] = (float)red[2][0][c];
   }
 }
 
@@ -445,7 +451,7 @@ bs_status launch_val_rows(const uint8_t* codes, int64_t n, int fmt, u16* out, hi
 template <typename T>
 bs_status launch_gain_t(const GainArgs<T>& a, float* ref, float* bias_r, float* bias_n, hipStream_t st) {
   if (a.d <= 0) return BS_OK;
-  const int64_t nrt = (a.T + 63) / 64;
+  const int64_t nrt = (a.T + GAIN_RT - 1) / GAIN_RT;
   if (nrt == 0) {
     if (ref) launch_fill2d(ref, 1, a.d, a.d, 0.0f, st);
     if (bias_r) launch_fill2d(bias_r, 1, a.d, a.d, 0.0f, st);
@@ -455,7 +461,7 @@ bs_status launch_gain_t(const GainArgs<T>& a, float* ref, float* bias_r, float* 
   }
   dim3 grid((unsigned)((a.d + 255) / 256), (unsigned)nrt);
   gain_partials_kernel<T><<<grid, 256, 0, st>>>(a);
-  gain_final_kernel<<<(unsigned)((a.d + 63) / 64), 256, 0, st>>>(a.part, nrt, a.d, ref, bias_r, bias_n);
+  gain_final_kernel<<<(unsigned)((a.d + 15) / 16), 256, 0, st>>>(a.part, nrt, a.d, ref, bias_r, bias_n);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
@@ -480,6 +486,59 @@ bs_status launch_dx_t(const DxArgs<T>& a, hipStream_t st) {
 }
 template bs_status launch_dx_t<float>(const DxArgs<float>&, hipStream_t);
 template bs_status launch_dx_t<u16>(const DxArgs<u16>&, hipStream_t);
+
+// Every policy's estimate of one gradient in one pass over ref: policy p writes mean_p = ref +
+// bias_p (or alt_p, with bias_p = alt_p - ref, when alt_p is set), bias_p and se_p (bias_p / se_p
+// inputs nullable = 0) at offset p n of the nullable output bases.
+__global__ __launch_bounds__(256) void combine_multi_kernel(CombineMulti c, int64_t n) {
+  const int64_t n4 = c.vec ? n / 4 : 0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    const float4 r = ((const float4*)c.ref)[i];
+    for (int p = 0; p < c.n_pol; ++p) {
+      const int64_t o = (int64_t)p * n4 + i;
+      float4 m, b;
+      if (c.alt[p]) {
+        m = ((const float4*)c.alt[p])[i];
+        b = make_float4(m.x - r.x, m.y - r.y, m.z - r.z, m.w - r.w);
+      } else {
+        b = c.bias[p] ? ((const float4*)c.bias[p])[i] : z;
+        m = c.bias[p] ? make_float4(r.x + b.x, r.y + b.y, r.z + b.z, r.w + b.w) : r;
+      }
+      if (c.mean) ((float4*)c.mean)[o] = m;
+      if (c.bias_out) ((float4*)c.bias_out)[o] = b;
+      if (c.se_out) ((float4*)c.se_out)[o] = c.se[p] ? ((const float4*)c.se[p])[i] : z;
+    }
+  }
+  for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const float r = c.ref[i];
+    for (int p = 0; p < c.n_pol; ++p) {
+      const int64_t o = (int64_t)p * n + i;
+      const float m = c.alt[p] ? c.alt[p][i] : (c.bias[p] ? r + c.bias[p][i] : r);
+      const float b = c.alt[p] ? m - r : (c.bias[p] ? c.bias[p][i] : 0.0f);
+      if (c.mean) c.mean[o] = m;
+      if (c.bias_out) c.bias_out[o] = b;
+      if (c.se_out) c.se_out[o] = c.se[p] ? c.se[p][i] : 0.0f;
+    }
+  }
+}
+
+bs_status launch_combine_multi(CombineMulti c, int64_t n, hipStream_t st) {
+  if (n <= 0 || c.n_pol < 1 || (!c.mean && !c.bias_out && !c.se_out)) return BS_OK;
+  if (c.n_pol > COMBINE_MAX_POL) return BS_EINVAL;
+  // the float4 path needs every array 16-byte aligned, including each policy's output slice
+  bool vec = n % 4 == 0;
+  for (const void* q : {(const void*)c.ref, (const void*)c.mean, (const void*)c.bias_out, (const void*)c.se_out})
+    vec = vec && ((uintptr_t)q & 15) == 0;
+  for (int p = 0; p < c.n_pol; ++p)
+    for (const void* q : {(const void*)c.bias[p], (const void*)c.se[p], (const void*)c.alt[p]})
+      vec = vec && ((uintptr_t)q & 15) == 0;
+  c.vec = vec ? 1 : 0;
+  combine_multi_kernel<<<grid1d((n + 3) / 4, 4096), 256, 0, st>>>(c, n);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
 
 bs_status launch_combine(const float* ref, const float* bias, const float* se, int64_t n, float* mean_out,
                          float* bias_out, float* se_out, hipStream_t st) {

@@ -99,6 +99,33 @@ __global__ __launch_bounds__(256) void planes_t_kernel(const T* __restrict__ in,
   }
 }
 
+// The transpose of a bf16 [R, C] matrix (C and ldi multiples of 8, 16-byte aligned rows) into
+// [C][ldo] with zeros in rows R .. ldo - 1 of every output row: one 64 x 64 tile per block,
+// 16-byte loads and stores, the tile held in LDS with rows padded to 144 bytes.
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const u16* __restrict__ in, int64_t R, int64_t C,
+                                                             int64_t ldi, u16* __restrict__ out, int64_t ldo) {
+  __shared__ __attribute__((aligned(16))) u16 tile[64][72];
+  const int t = threadIdx.x, q = (t & 7) * 8;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int rr = (t >> 3) + 32 * pass;
+    const int64_t r = r0 + rr, c = c0 + q;
+    const uint4 v = (r < R && c < C) ? *(const uint4*)(in + r * ldi + c) : make_uint4(0, 0, 0, 0);
+    *(uint4*)&tile[rr][q] = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int cc = (t >> 3) + 32 * pass;
+    const int64_t c = c0 + cc;
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = (uint32_t)tile[q + 2 * i][cc] | ((uint32_t)tile[q + 2 * i + 1][cc] << 16);
+    if (c < C) *(uint4*)(out + c * ldo + r0 + q) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
 bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64_t ldi, bool transpose,
                         u16* const* outp, int nterms, int64_t ldo, float scale, hipStream_t st) {
   if (nterms < 1 || nterms > 3) return BS_EINVAL;
@@ -106,7 +133,11 @@ bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64
   if (transpose) {
     if (C <= 0 || ldo <= 0) return BS_OK;
     dim3 grid((unsigned)((C + 63) / 64), (unsigned)((ldo + 63) / 64));
-    if (dt == BS_F32)
+    const bool vec = dt == BS_BF16 && nterms == 1 && scale == 1.0f && C % 8 == 0 && ldi % 8 == 0 && ldo % 64 == 0 &&
+                     ((uintptr_t)in & 15) == 0 && ((uintptr_t)outp[0] & 15) == 0;
+    if (vec)
+      transpose_bf16_kernel<<<grid, 256, 0, st>>>((const u16*)in, R, C, ldi, outp[0], ldo);
+    else if (dt == BS_F32)
       planes_t_kernel<float><<<grid, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
     else
       planes_t_kernel<u16><<<grid, 256, 0, st>>>((const u16*)in, R, C, ldi, out, nterms, ldo, scale);

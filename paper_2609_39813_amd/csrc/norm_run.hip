@@ -59,7 +59,7 @@ NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype wt
   w.bias_rg = c.take<float>(d);
   w.bias_ng = c.take<float>(d);
   w.se_g = c.take<float>(d);
-  w.gain_part = c.take<double>(3 * ((T + 63) / 64) * d + 1);
+  w.gain_part = c.take<double>(3 * ((T + GAIN_RT - 1) / GAIN_RT) * d + 1);
   if (p.weight_u) {
     for (int i = 0; i < 3; ++i) w.resU[i] = c.take<u16>(d * Tp);
     w.bias_u = c.take<float>(d * n);
@@ -325,27 +325,34 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     BS_TRY(launch_dx_t(da, st));
   }
 
-  // per-policy estimates
-  for (int i = 0; i < (fwd_only ? 0 : n_pol); ++i) {
-    const bs_norm_policy& q = pol[i];
-    const float* bg = q.gain_use == BS_READ_R ? w.bias_rg : (q.gain_use == BS_READ_N ? w.bias_ng : nullptr);
-    const float* sg = (q.gain_use == BS_READ_N && p.gain_se) ? w.se_g : nullptr;
-    BS_TRY(launch_combine(dgain_ref, bg, sg, d, dgain.mean ? dgain.mean + i * d : nullptr,
-                          dgain.bias ? dgain.bias + i * d : nullptr, dgain.se ? dgain.se + i * d : nullptr, st));
-    const float* bw = q.weight_use == BS_READ_U ? w.bias_u
-                      : (q.weight_use == BS_READ_N ? w.bias_n[q.fresh_shared ? 0 : 1] : nullptr);
-    const int64_t dn = d * n;
-    const float* sw = (q.weight_use == BS_READ_N && p.weight_se[q.fresh_shared ? 0 : 1]) ? w.se_w[q.fresh_shared ? 0 : 1]
-                                                                                        : nullptr;
-    BS_TRY(launch_combine(dW_ref, bw, sw, dn, dW.mean ? dW.mean + i * dn : nullptr,
-                          dW.bias ? dW.bias + i * dn : nullptr, dW.se ? dW.se + i * dn : nullptr, st));
-    const int64_t td = T * d;
-    if (q.norm_input_use == BS_READ_R)
-      BS_TRY(launch_combine_alt(dX_ref, w.dx_r, td, dX.mean ? dX.mean + i * td : nullptr,
-                                dX.bias ? dX.bias + i * td : nullptr, dX.se ? dX.se + i * td : nullptr, st));
-    else
-      BS_TRY(launch_combine(dX_ref, nullptr, nullptr, td, dX.mean ? dX.mean + i * td : nullptr,
-                            dX.bias ? dX.bias + i * td : nullptr, dX.se ? dX.se + i * td : nullptr, st));
+  // per-policy estimates: one pass per gradient over its reference
+  if (!fwd_only) {
+    CombineMulti cg{}, cw{}, cx{};
+    cg.ref = dgain_ref;
+    cw.ref = dW_ref;
+    cx.ref = dX_ref;
+    for (CombineMulti* c : {&cg, &cw, &cx}) c->n_pol = n_pol;
+    cg.mean = dgain.mean;
+    cg.bias_out = dgain.bias;
+    cg.se_out = dgain.se;
+    cw.mean = dW.mean;
+    cw.bias_out = dW.bias;
+    cw.se_out = dW.se;
+    cx.mean = dX.mean;
+    cx.bias_out = dX.bias;
+    cx.se_out = dX.se;
+    for (int i = 0; i < n_pol; ++i) {
+      const bs_norm_policy& q = pol[i];
+      const int fs = q.fresh_shared ? 0 : 1;
+      cg.bias[i] = q.gain_use == BS_READ_R ? w.bias_rg : (q.gain_use == BS_READ_N ? w.bias_ng : nullptr);
+      cg.se[i] = (q.gain_use == BS_READ_N && p.gain_se) ? w.se_g : nullptr;
+      cw.bias[i] = q.weight_use == BS_READ_U ? w.bias_u : (q.weight_use == BS_READ_N ? w.bias_n[fs] : nullptr);
+      cw.se[i] = (q.weight_use == BS_READ_N && p.weight_se[fs]) ? w.se_w[fs] : nullptr;
+      cx.alt[i] = q.norm_input_use == BS_READ_R ? w.dx_r : nullptr;
+    }
+    BS_TRY(launch_combine_multi(cg, d, st));
+    BS_TRY(launch_combine_multi(cw, d * n, st));
+    BS_TRY(launch_combine_multi(cx, T * d, st));
   }
   return BS_OK;
 }
