@@ -55,6 +55,96 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(const T* __restrict__ 
   }
 }
 
+// The same forward with vector accesses (d a multiple of 8; X, gain and u 16-byte aligned) and
+// the same fixed fp32 order: each 512-element chunk of a row is loaded 8 elements per lane, its
+// squares pass through LDS, and lane l adds the entries l, l + 64, ... of the chunk, chunks in
+// order, so partial l still takes j = l, l + 64, ... ascending. A wave takes RMS_RPW rows (the
+// same trip count in every wave, so the block barriers are uniform); one amax atomic per block.
+constexpr int RMS_RPW = 4;
+
+template <typename T>
+__device__ __forceinline__ void load8_f32(const T* p, float (&x)[8]);
+template <>
+__device__ __forceinline__ void load8_f32<float>(const float* p, float (&x)[8]) {
+  const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+template <>
+__device__ __forceinline__ void load8_f32<u16>(const u16* p, float (&x)[8]) {
+  const uint4 v = *(const uint4*)p;
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_fwd8_kernel(const T* __restrict__ X, const float* __restrict__ gain,
+                                                           int64_t Tn, int64_t d, float eps, float* __restrict__ u,
+                                                           float* __restrict__ rstd, uint32_t* __restrict__ amax_bits) {
+#pragma clang fp contract(off)
+  __shared__ float sq[4][512];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  uint32_t m = 0;
+  for (int k = 0; k < RMS_RPW; ++k) {
+    const int64_t t = ((int64_t)blockIdx.x * RMS_RPW + k) * 4 + w;
+    const bool ok = t < Tn;
+    const T* xr = X + (ok ? t : 0) * d;
+    float p = 0.0f;
+    for (int64_t c0 = 0; c0 < d; c0 += 512) {
+      const int64_t j8 = c0 + 8 * lane;
+      if (ok && j8 < d) {
+        float x[8];
+        load8_f32(xr + j8, x);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) sq[w][8 * lane + i] = x[i] * x[i];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (ok && c0 + lane + 64 * i < d) p = p + sq[w][lane + 64 * i];
+      __syncthreads();
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const float o = __shfl_down(p, off, 64);
+      if (lane < off) p = p + o;
+    }
+    const float ss = __shfl(p, 0, 64);
+    if (!ok) continue;
+    const float ms = __fdiv_rn(ss, (float)d);
+    const float r = 1.0f / sqrtf(ms + eps);
+    float* ur = u + t * d;
+    for (int64_t j8 = 8 * lane; j8 < d; j8 += 512) {
+      float x[8], g[8], o[8];
+      load8_f32(xr + j8, x);
+      load8_f32(gain + j8, g);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float z = x[i] * r;
+        o[i] = g[i] * z;
+        const uint32_t b = __float_as_uint(fabsf(o[i]));
+        m = m > b ? m : b;
+      }
+      *(float4*)(ur + j8) = make_float4(o[0], o[1], o[2], o[3]);
+      *(float4*)(ur + j8 + 4) = make_float4(o[4], o[5], o[6], o[7]);
+    }
+    if (lane == 0) rstd[t] = r;
+  }
+  m = wave_max_u32(m);
+  __shared__ uint32_t red[4];
+  if (lane == 0) red[w] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t b = red[0];
+    for (int i = 1; i < 4; ++i) b = b > red[i] ? b : red[i];
+    if (b) atomicMax(amax_bits, b);
+  }
+}
+
 // Transposed planes [d][ldo] of per-element operands of the weight-use contractions.
 //   NP_VAL : val(C_u)                                      (1 term, exact)
 //   NP_RESU: u - s * val(C_u)  (= minus the forward's rounding error; 3 terms)
@@ -95,6 +185,80 @@ __global__ __launch_bounds__(256) void norm_planes_t_kernel(NormPlaneArgs a) {
     const int64_t j = c0 + cc, t = r0 + tx;
     if (j < a.d && t < a.ldo)
       for (int p = 0; p < a.nterms; ++p) a.out[p][j * a.ldo + t] = tile[p][tx][cc];
+  }
+}
+
+// The same planes with vector accesses (d a multiple of 4, ldo of 64, 16-byte aligned u, 4-byte
+// aligned codes, 8-byte aligned counts): a thread forms 4 consecutive columns of a row, and each
+// output row (one column j) leaves the LDS tile as 16-byte stores of 8 consecutive t.
+template <int MODE>
+__global__ __launch_bounds__(256) void norm_planes_t4_kernel(NormPlaneArgs a) {
+  __shared__ __attribute__((aligned(16))) u16 tile[3][64][72];
+  const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  const float s = *a.scale;
+  const double rs = 1.0 / (double)s;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int rr = rg + 16 * i;
+    const int64_t t = r0 + rr, j = c0 + 4 * cg;
+    u16 o[3][4] = {{0, 0, 0, 0}, {0, 0, 0, 0}, {0, 0, 0, 0}};
+    if (t < a.T && j < a.d) {
+      const int64_t e = t * a.d + j;
+      const uint32_t cw = *(const uint32_t*)(a.codes + e);
+      float uv[4] = {0.f, 0.f, 0.f, 0.f};
+      if (MODE != NP_VAL) {
+        const float4 u4 = *(const float4*)(a.u + e);
+        uv[0] = u4.x;
+        uv[1] = u4.y;
+        uv[2] = u4.z;
+        uv[3] = u4.w;
+      }
+      uint32_t cn[4] = {0, 0, 0, 0};
+      if (MODE == NP_RESN) {
+        const uint2 c2 = *(const uint2*)(a.counts + e);
+        cn[0] = c2.x & 0xFFFFu;
+        cn[1] = c2.x >> 16;
+        cn[2] = c2.y & 0xFFFFu;
+        cn[3] = c2.y >> 16;
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t code = (cw >> (8 * c)) & 0xFFu;
+        if (MODE == NP_VAL) {
+          o[0][c] = bf16_bits(f8_value(code, a.f));
+        } else if (MODE == NP_RESU) {
+          split3(fmaf(-s, f8_value(code, a.f), uv[c]), o[0][c], o[1][c], o[2][c]);
+        } else {
+          const float y = div_scale(uv[c], rs);
+          const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
+          const int h = (code & 0x7Fu) != b.base + b.mi;
+          const float v = (float)((int)cn[c] - a.K * h) * f8_step(b);
+          split3(signbit(y) ? -v : v, o[0][c], o[1][c], o[2][c]);
+        }
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < 3; ++p)
+      if (p < a.nterms)
+        *(uint2*)&tile[p][rr][4 * cg] = make_uint2((uint32_t)o[p][0] | ((uint32_t)o[p][1] << 16),
+                                                   (uint32_t)o[p][2] | ((uint32_t)o[p][3] << 16));
+  }
+  __syncthreads();
+  const int q = (threadIdx.x & 7) * 8;
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int cc = (threadIdx.x >> 3) + 32 * pass;
+    const int64_t j = c0 + cc;
+    if (j >= a.d) continue;
+#pragma unroll
+    for (int p = 0; p < 3; ++p) {
+      if (p >= a.nterms) break;
+      uint32_t w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)tile[p][q + 2 * i][cc] | ((uint32_t)tile[p][q + 2 * i + 1][cc] << 16);
+      *(uint4*)(a.out[p] + j * a.ldo + r0 + q) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
   }
 }
 
@@ -397,7 +561,15 @@ bs_status launch_rmsnorm_fwd(const void* X, bs_dtype dt, const float* gain, int6
   if (T > 0) {
     const unsigned blocks = (unsigned)((T + 3) / 4);
     ProfScope prof("rmsnorm_fwd", st);
-    if (dt == BS_F32)
+    const bool vec = d % 8 == 0 && ((uintptr_t)X & 15) == 0 && ((uintptr_t)gain & 15) == 0 && ((uintptr_t)u & 15) == 0;
+    const unsigned blocks8 = (unsigned)((T + 4 * RMS_RPW - 1) / (4 * RMS_RPW));
+    if (vec && dt == BS_F32)
+      rmsnorm_fwd8_kernel<float><<<blocks8, 256, 0, st>>>((const float*)X, gain, T, d, eps, u, rstd,
+                                                          (uint32_t*)&diag->amax);
+    else if (vec)
+      rmsnorm_fwd8_kernel<u16><<<blocks8, 256, 0, st>>>((const u16*)X, gain, T, d, eps, u, rstd,
+                                                        (uint32_t*)&diag->amax);
+    else if (dt == BS_F32)
       rmsnorm_fwd_kernel<float><<<blocks, 256, 0, st>>>((const float*)X, gain, T, d, eps, u, rstd,
                                                         (uint32_t*)&diag->amax);
     else
@@ -411,7 +583,17 @@ bs_status launch_rmsnorm_fwd(const void* X, bs_dtype dt, const float* gain, int6
 bs_status launch_norm_planes(int mode, const NormPlaneArgs& a, hipStream_t st) {
   if (a.d <= 0 || a.ldo <= 0) return BS_OK;
   dim3 grid((unsigned)((a.d + 63) / 64), (unsigned)((a.ldo + 63) / 64));
-  if (mode == NP_VAL)
+  bool vec = a.d % 4 == 0 && a.ldo % 64 == 0 && ((uintptr_t)a.u & 15) == 0 && ((uintptr_t)a.codes & 3) == 0 &&
+             ((uintptr_t)a.counts & 7) == 0;
+  for (int p = 0; p < a.nterms; ++p) vec = vec && ((uintptr_t)a.out[p] & 15) == 0;
+  if (vec) {
+    if (mode == NP_VAL)
+      norm_planes_t4_kernel<NP_VAL><<<grid, 256, 0, st>>>(a);
+    else if (mode == NP_RESU)
+      norm_planes_t4_kernel<NP_RESU><<<grid, 256, 0, st>>>(a);
+    else
+      norm_planes_t4_kernel<NP_RESN><<<grid, 256, 0, st>>>(a);
+  } else if (mode == NP_VAL)
     norm_planes_t_kernel<NP_VAL><<<grid, 256, 0, st>>>(a);
   else if (mode == NP_RESU)
     norm_planes_t_kernel<NP_RESU><<<grid, 256, 0, st>>>(a);
