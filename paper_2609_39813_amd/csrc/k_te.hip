@@ -240,7 +240,7 @@ __global__ __launch_bounds__(TE_BLOCK) void te_d_kernel(const u16* __restrict__ 
 
 // query-major: dS = P (dP - D), its E5M2 codes at s_dS and P's E4M3 codes at s_P (tile-major),
 // dQ = c s_dS val(dS_q) K cast at s_g
-__global__ __launch_bounds__(TE_BLOCK) void te_dq_kernel(TeArgs a) {
+__global__ __launch_bounds__(TE_BLOCK) __attribute__((amdgpu_waves_per_eu(3, 8))) void te_dq_kernel(TeArgs a) {
   __shared__ __attribute__((aligned(16))) u16 sm[2][3][AT * AT];  // K, V, K^T
   const QMajor z = qmajor_setup(a, true);
   const float sdO = a.sc[1], sdS = a.sc[2];
