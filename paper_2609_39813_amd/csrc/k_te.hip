@@ -109,36 +109,46 @@ struct TeParts {
   int n_prep, n_d, n_dq, n_dkv;   // dS, amax gradients, clamps gradients), 2 (amax gradients, clamps)
 };
 
-// column `col` of an [n][width] partial array reduced over the block (result in every thread)
-__device__ uint32_t reduce_col(const uint32_t* p, int n, int width, int col, bool is_max) {
-  __shared__ uint32_t red[TE_BLOCK / 64];
-  uint32_t r = 0;
-  for (int i = threadIdx.x; i < n; i += TE_BLOCK) r = is_max ? max(r, p[i * width + col]) : r + p[i * width + col];
-  r = is_max ? wave_max_u32(r) : wave_sum_u32(r);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = r;
-  __syncthreads();
-  uint32_t t = red[0];
-#pragma unroll
-  for (int k = 1; k < TE_BLOCK / 64; ++k) t = is_max ? max(t, red[k]) : t + red[k];
-  __syncthreads();
-  return t;
-}
-
+// The call's amaxes and counts from the per-block partials: one block; every thread folds its
+// share of each partial array (all nine quantities at once), then one fixed tree over the waves.
 __global__ __launch_bounds__(TE_BLOCK) void te_final_kernel(TeParts q, float* amax, uint32_t* counts) {
-  const uint32_t a0 = reduce_col(q.prep, q.n_prep, 2, 0, true), c1 = reduce_col(q.prep, q.n_prep, 2, 1, false);
-  const uint32_t c0 = reduce_col(q.d, q.n_d, 2, 0, false), ap = reduce_col(q.d, q.n_d, 2, 1, true);
-  const uint32_t a1 = reduce_col(q.dq, q.n_dq, 4, 0, true), c2 = reduce_col(q.dq, q.n_dq, 4, 1, false);
-  const uint32_t a2 = max(reduce_col(q.dq, q.n_dq, 4, 2, true), reduce_col(q.dkv, q.n_dkv, 2, 0, true));
-  const uint32_t c3 = reduce_col(q.dq, q.n_dq, 4, 3, false) + reduce_col(q.dkv, q.n_dkv, 2, 1, false);
-  if (threadIdx.x == 0) {
-    amax[0] = __uint_as_float(ap);
-    amax[1] = __uint_as_float(a0);
-    amax[2] = __uint_as_float(a1);
-    amax[3] = __uint_as_float(a2);
-    counts[0] = c0;
-    counts[1] = c1;
-    counts[2] = c2;
-    counts[3] = c3;
+  // quantities: 0 amax P, 1 amax dO, 2 amax dS, 3 amax gradients (max); 4 rows, 5 clamps dO,
+  // 6 clamps dS, 7 clamps gradients (sum)
+  uint32_t v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int i = threadIdx.x; i < q.n_prep; i += TE_BLOCK) {
+    v[1] = max(v[1], q.prep[2 * i]);
+    v[5] += q.prep[2 * i + 1];
+  }
+  for (int i = threadIdx.x; i < q.n_d; i += TE_BLOCK) {
+    v[4] += q.d[2 * i];
+    v[0] = max(v[0], q.d[2 * i + 1]);
+  }
+  for (int i = threadIdx.x; i < q.n_dq; i += TE_BLOCK) {
+    const uint4 w = *(const uint4*)(q.dq + 4 * (int64_t)i);
+    v[2] = max(v[2], w.x);
+    v[6] += w.y;
+    v[3] = max(v[3], w.z);
+    v[7] += w.w;
+  }
+  for (int i = threadIdx.x; i < q.n_dkv; i += TE_BLOCK) {
+    v[3] = max(v[3], q.dkv[2 * i]);
+    v[7] += q.dkv[2 * i + 1];
+  }
+  __shared__ uint32_t red[8][TE_BLOCK / 64];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const uint32_t r = k < 4 ? wave_max_u32(v[k]) : wave_sum_u32(v[k]);
+    if ((threadIdx.x & 63) == 0) red[k][threadIdx.x >> 6] = r;
+  }
+  __syncthreads();
+  if (threadIdx.x < 8) {
+    const int k = threadIdx.x;
+    uint32_t r = red[k][0];
+    for (int w = 1; w < TE_BLOCK / 64; ++w) r = k < 4 ? max(r, red[k][w]) : r + red[k][w];
+    if (k < 4)
+      amax[k] = __uint_as_float(r);
+    else
+      counts[k - 4] = r;
   }
 }
 
