@@ -16,6 +16,14 @@ namespace bsp {
 //   trial-independent term, so it is summed in fp32 (per lane in element order, then over the
 //   row's 4 lanes); its mean and sample SD over k come from fp64 sums of S_k - S_1.
 // ------------------------------------------------------------------------------------
+// (v_l + v_(l^1)) + (v_(l^2) + v_(l^3)) within a quad of lanes by two DPP exchanges (no LDS
+// round trip): the same value in the four lanes, equal to two xor shuffles' sum
+__device__ __forceinline__ float quad_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));  // quad_perm 1,0,3,2
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));  // quad_perm 2,3,0,1
+  return v;
+}
+
 __global__ __launch_bounds__(256) void attn_d_kernel(AttnDArgs a) {
   constexpr int EPL = 16;
   const int64_t row = (int64_t)blockIdx.x * 64 + (threadIdx.x >> 2);
@@ -88,7 +96,7 @@ __global__ __launch_bounds__(256) void attn_d_kernel(AttnDArgs a) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) Sk += sr_up(F[4 * j + q], R[q]) ? w[4 * j + q] : 0.0f;
       }
-      Sk = rowsum(Sk);
+      Sk = quad_sum(Sk);
       if (k == 1) s1 = Sk;
       const double dl = (double)Sk - s1;
       d1 += dl;
@@ -737,7 +745,7 @@ __global__ __launch_bounds__(256) void attn_l2_kernel(AttnL2Args a) {
         tT += (u ^ up) ? cN3[i] : 0.0f;
       }
     }
-    const float t3[3] = {rowsum(tR), rowsum(tN), 0.5f * rowsum(tT)};
+    const float t3[3] = {quad_sum(tR), quad_sum(tN), 0.5f * quad_sum(tT)};
 #pragma unroll
     for (int c = 0; c < 3; ++c) {
       if (k == 1) s1[c] = t3[c];
