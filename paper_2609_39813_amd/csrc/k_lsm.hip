@@ -22,9 +22,12 @@ __device__ __forceinline__ double wsum(double v) {
   return v;
 }
 
-// l = z - max - log(sum exp(z - max)) per row, one wave per row
-__global__ __launch_bounds__(64) void lsm_prep_kernel(const double* __restrict__ z, int64_t rows, int C,
-                                                      double* __restrict__ l) {
+// l = z - max - log(sum exp(z - max)) per row, one wave per row, and the three values every
+// trial's exponentials take (the saved output is l + r with r = +eps or -eps exactly):
+// p = exp(l), ep = exp(l + eps) / cal and em = exp(l - eps) / cal
+__global__ __launch_bounds__(64) void lsm_prep_kernel(const double* __restrict__ z, int64_t rows, int C, double eps,
+                                                      double cal, double* __restrict__ p, double* __restrict__ ep,
+                                                      double* __restrict__ em) {
   const int64_t row = blockIdx.x;
   const int lane = threadIdx.x;
   const double* zr = z + row * C;
@@ -35,17 +38,22 @@ __global__ __launch_bounds__(64) void lsm_prep_kernel(const double* __restrict__
   double se = 0.0;
   for (int j = lane; j < C; j += 64) se += exp(zr[j] - m);
   const double lse = m + log(wsum(se));
-  for (int j = lane; j < C; j += 64) l[row * C + j] = zr[j] - lse;
+  for (int j = lane; j < C; j += 64) {
+    const double lj = zr[j] - lse;
+    const int64_t e = row * C + j;
+    p[e] = exp(lj);
+    ep[e] = exp(lj + eps) / cal;
+    em[e] = exp(lj + -eps) / cal;
+  }
 }
 
 // per (row, trial): the row sums of the four entry errors, [4][K][rows]
-__global__ __launch_bounds__(64) void lsm_trial_kernel(const double* __restrict__ l, const int32_t* __restrict__ y,
-                                                       int64_t rows, int C, double eps, double cal, int K,
-                                                       uint64_t seed, uint32_t use_r, uint32_t use_p,
-                                                       double* __restrict__ part) {
+__global__ __launch_bounds__(64) void lsm_trial_kernel(const double* __restrict__ pv, const double* __restrict__ epv,
+                                                       const double* __restrict__ emv, const int32_t* __restrict__ y,
+                                                       int64_t rows, int C, double eps, int K, uint64_t seed,
+                                                       uint32_t use_r, uint32_t use_p, double* __restrict__ part) {
   const int64_t row = blockIdx.x;
   const int lane = threadIdx.x;
-  const double* lr = l + row * C;
   const int yt = y[row];
   const int ngroups = C / 4;
   const int k_end = min(K, (int)(blockIdx.y + 1) * LSM_TCH);
@@ -69,9 +77,11 @@ __global__ __launch_bounds__(64) void lsm_trial_kernel(const double* __restrict_
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int j = 4 * gi + q;
-        const double lj = lr[j], p = exp(lj);
-        const double r = R[q] >= 0x80000000u ? eps : -eps, rp = Rp[q] >= 0x80000000u ? eps : -eps;
-        const double er = exp(lj + r) / cal, erp = exp(lj + rp) / cal;
+        const int64_t e = row * C + j;
+        const double p = pv[e];
+        const bool ur = R[q] >= 0x80000000u, urp = Rp[q] >= 0x80000000u;
+        const double r = ur ? eps : -eps;
+        const double er = ur ? epv[e] : emv[e], erp = urp ? epv[e] : emv[e];
         // likelihood: h = -e_y, 1^T h = -1
         const double hl = j == yt ? -1.0 : 0.0;
         const double gl_star = hl + p;
@@ -168,7 +178,7 @@ __global__ __launch_bounds__(256) void lsm_final_kernel(const double* __restrict
 size_t lsm_ws_size(int64_t rows, int C, int K) {
   if (rows < 1 || C < 4 || (C & 3) || K < 1) return 0;
   Carver c;
-  c.take<double>(rows * C);
+  for (int i = 0; i < 3; ++i) c.take<double>(rows * C);
   c.take<double>((int64_t)4 * K * rows);
   c.take<double>((int64_t)8 * ((K + LSM_RT - 1) / LSM_RT));
   c.take<double>(4);
@@ -193,22 +203,23 @@ bs_status bs_logsoftmax_reuse_check(const double* logits, const int32_t* target,
   if (!ws || ((uintptr_t)ws & 255) || ws_bytes < need) return BS_EWORKSPACE;
   hipStream_t st = (hipStream_t)stream;
   Carver c(ws, ws_bytes);
-  double* l = c.take<double>(rows * C);
+  double* pv = c.take<double>(rows * C);
+  double* epv = c.take<double>(rows * C);
+  double* emv = c.take<double>(rows * C);
   double* part = c.take<double>((int64_t)4 * K * rows);
   const int nb = (K + LSM_RT - 1) / LSM_RT;
   double* acc = c.take<double>((int64_t)8 * nb);
   double* m0 = c.take<double>(4);
   {
     ProfScope prof("lsm_prep", st);
-    lsm_prep_kernel<<<(unsigned)rows, 64, 0, st>>>(logits, rows, C, l);
+    lsm_prep_kernel<<<(unsigned)rows, 64, 0, st>>>(logits, rows, C, eps, calibrate ? cosh(eps) : 1.0, pv, epv, emv);
     BS_CHECK_LAUNCH();
   }
   const uint32_t base = store_id * 256u;
   {
     ProfScope prof("lsm_trial", st);
     const dim3 grid((unsigned)rows, (unsigned)((K + LSM_TCH - 1) / LSM_TCH));
-    lsm_trial_kernel<<<grid, 64, 0, st>>>(l, target, rows, C, eps, calibrate ? cosh(eps) : 1.0, K, seed, base,
-                                          base + 1, part);
+    lsm_trial_kernel<<<grid, 64, 0, st>>>(pv, epv, emv, target, rows, C, eps, K, seed, base, base + 1, part);
     BS_CHECK_LAUNCH();
   }
   {
