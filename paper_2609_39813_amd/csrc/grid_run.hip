@@ -127,6 +127,10 @@ __global__ __launch_bounds__(256) void grid_fresh_kernel(const float* __restrict
 
 // gain use, fp64 column partials over token chunks of 256: [3][nchunk][d]
 //   ref  sum z du;  R  sum (u/gain - z - eU/gain) du;  N  sum (u/gain - z + eE/gain) du
+// rows per chunk of the gain use's column partial sums: T / 32 chunks (grid x) x d / 64 one-wave
+// blocks (grid y)
+constexpr int GRID_GAIN_RT = 32;
+
 template <typename XT>
 __global__ __launch_bounds__(64) void grid_gain_kernel(const XT* __restrict__ X, const float* __restrict__ rstd,
                                                        const float* __restrict__ gain, const float* __restrict__ u,
@@ -134,13 +138,13 @@ __global__ __launch_bounds__(64) void grid_gain_kernel(const XT* __restrict__ X,
                                                        const float* __restrict__ eE, int64_t T, int64_t d,
                                                        double* __restrict__ part) {
 #pragma clang fp contract(off)
-  const int64_t j = (int64_t)blockIdx.x * 64 + threadIdx.x;
-  const int64_t c = blockIdx.y, nch = gridDim.y;
+  const int64_t j = (int64_t)blockIdx.y * 64 + threadIdx.x;
+  const int64_t c = blockIdx.x, nch = gridDim.x;
   if (j >= d) return;
   const double g = gain[j];
   double a0 = 0.0, a1 = 0.0, a2 = 0.0;
-  const int64_t t1 = min(T, (c + 1) * 256);
-  for (int64_t t = c * 256; t < t1; ++t) {
+  const int64_t t1 = min(T, (c + 1) * GRID_GAIN_RT);
+  for (int64_t t = c * GRID_GAIN_RT; t < t1; ++t) {
     const int64_t e = t * d + j;
     const double z = (double)(load_f32(X, e) * rstd[t]);
     const double dd = du[e];
@@ -152,19 +156,6 @@ __global__ __launch_bounds__(64) void grid_gain_kernel(const XT* __restrict__ X,
   part[(0 * nch + c) * d + j] = a0;
   part[(1 * nch + c) * d + j] = a1;
   part[(2 * nch + c) * d + j] = a2;
-}
-
-__global__ __launch_bounds__(256) void grid_gain_final_kernel(const double* __restrict__ part, int64_t nch, int64_t d,
-                                                              float* __restrict__ ref, float* __restrict__ br,
-                                                              float* __restrict__ bn) {
-  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= d) return;
-  double s[3] = {0.0, 0.0, 0.0};
-  for (int i = 0; i < 3; ++i)
-    for (int64_t c = 0; c < nch; ++c) s[i] += part[(i * nch + c) * d + j];
-  ref[j] = (float)s[0];
-  br[j] = (float)s[1];
-  bn[j] = (float)s[2];
 }
 
 struct GridWs {
@@ -194,7 +185,7 @@ GridWs carve_grid(Carver& c, int64_t T, int64_t d, int64_t n, bs_dtype wt, bs_dt
   w.bias_rg = c.take<float>(d);
   w.bias_ng = c.take<float>(d);
   for (int i = 0; i < 3; ++i) w.bias_w[i] = c.take<float>(d * n);
-  w.gpart = c.take<double>(3 * ((T + 255) / 256 + 1) * d);
+  w.gpart = c.take<double>(3 * ((T + GRID_GAIN_RT - 1) / GRID_GAIN_RT + 1) * d);
   w.gemm_part_cap = 4 * d * std::max<int64_t>(std::max<int64_t>(T, n), 64);
   w.gemm_part = c.take<float>(w.gemm_part_cap);
   return w;
@@ -336,8 +327,8 @@ bs_status grid_run(const GridIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   }
   // gain use: fp64 column sums
   {
-    const int64_t nch = (T + 255) / 256;
-    const dim3 grid((unsigned)((d + 63) / 64), (unsigned)nch);
+    const int64_t nch = (T + GRID_GAIN_RT - 1) / GRID_GAIN_RT;
+    const dim3 grid((unsigned)nch, (unsigned)((d + 63) / 64));
     if (xt == BS_F32)
       grid_gain_kernel<float><<<grid, 64, 0, st>>>((const float*)io.X, w.rstd, io.gain, w.u, w.du, w.eU, w.eE, T, d,
                                                    w.gpart);
@@ -345,9 +336,7 @@ bs_status grid_run(const GridIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       grid_gain_kernel<u16><<<grid, 64, 0, st>>>((const u16*)io.X, w.rstd, io.gain, w.u, w.du, w.eU, w.eE, T, d,
                                                  w.gpart);
     BS_CHECK_LAUNCH();
-    grid_gain_final_kernel<<<(unsigned)((d + 255) / 256), 256, 0, st>>>(w.gpart, nch, d, io.dgain_ref, w.bias_rg,
-                                                                        w.bias_ng);
-    BS_CHECK_LAUNCH();
+    BS_TRY(launch_gain_final(w.gpart, nch, d, io.dgain_ref, w.bias_rg, w.bias_ng, st));
   }
   // the normalization input gradient with unrounded values
   if (xt == BS_F32) {

@@ -97,6 +97,10 @@ struct CombineMulti {
   float *mean, *bias_out, *se_out;  // bases of [n_pol][n] outputs (nullable)
 };
 bs_status launch_combine_multi(CombineMulti c, int64_t n, hipStream_t st);
+// column sums of [3][nrt][d] fp64 partials (row tiles in order within 16 segments, the segments by
+// a fixed tree) into ref, bias_r and bias_n [d] (bias_r / bias_n nullable)
+bs_status launch_gain_final(const double* part, int64_t nrt, int64_t d, float* ref, float* bias_r, float* bias_n,
+                            hipStream_t st);
 
 bs_status launch_combine_alt(const float* ref, const float* alt, int64_t n, float* mean_out, float* bias_out,
                              float* se_out, hipStream_t st);

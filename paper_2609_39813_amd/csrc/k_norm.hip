@@ -706,6 +706,14 @@ __global__ __launch_bounds__(256) void combine_multi_kernel(CombineMulti c, int6
   }
 }
 
+bs_status launch_gain_final(const double* part, int64_t nrt, int64_t d, float* ref, float* bias_r, float* bias_n,
+                            hipStream_t st) {
+  if (d <= 0 || nrt <= 0) return BS_OK;
+  gain_final_kernel<<<(unsigned)((d + 15) / 16), 256, 0, st>>>(part, nrt, d, ref, bias_r, bias_n);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
 bs_status launch_combine_multi(CombineMulti c, int64_t n, hipStream_t st) {
   if (n <= 0 || c.n_pol < 1 || (!c.mean && !c.bias_out && !c.se_out)) return BS_OK;
   if (c.n_pol > COMBINE_MAX_POL) return BS_EINVAL;
