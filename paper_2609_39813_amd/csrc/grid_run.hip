@@ -347,19 +347,25 @@ bs_status grid_run(const GridIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     BS_TRY(launch_dx_t(da, st));
   }
   // per-policy estimates
+  // every policy's estimates, one pass per gradient over its reference
+  CombineMulti cg{}, cw{};
+  cg.ref = io.dgain_ref;
+  cw.ref = io.dW_ref;
+  cg.n_pol = cw.n_pol = io.n_pol;
+  cg.mean = io.dgain.mean;
+  cg.bias_out = io.dgain.bias;
+  cw.mean = io.dW.mean;
+  cw.bias_out = io.dW.bias;
   for (int i = 0; i < io.n_pol; ++i) {
     const bs_grid_policy& q = io.pol[i];
-    const float* bg = q.gain_use == BS_READ_R ? w.bias_rg : (q.gain_use == BS_READ_N ? w.bias_ng : nullptr);
-    BS_TRY(launch_combine(io.dgain_ref, bg, nullptr, d, io.dgain.mean ? io.dgain.mean + i * d : nullptr,
-                          io.dgain.bias ? io.dgain.bias + i * d : nullptr, nullptr, st));
-    const float* bw = q.weight_use == BS_WREAD_U   ? w.bias_w[0]
-                      : q.weight_use == BS_WREAD_N ? w.bias_w[1]
-                      : q.weight_use == BS_WREAD_R_EPS ? w.bias_w[2]
-                                                       : nullptr;
-    const int64_t dn = d * n;
-    BS_TRY(launch_combine(io.dW_ref, bw, nullptr, dn, io.dW.mean ? io.dW.mean + i * dn : nullptr,
-                          io.dW.bias ? io.dW.bias + i * dn : nullptr, nullptr, st));
+    cg.bias[i] = q.gain_use == BS_READ_R ? w.bias_rg : (q.gain_use == BS_READ_N ? w.bias_ng : nullptr);
+    cw.bias[i] = q.weight_use == BS_WREAD_U       ? w.bias_w[0]
+                 : q.weight_use == BS_WREAD_N     ? w.bias_w[1]
+                 : q.weight_use == BS_WREAD_R_EPS ? w.bias_w[2]
+                                                  : nullptr;
   }
+  BS_TRY(launch_combine_multi(cg, d, st));
+  BS_TRY(launch_combine_multi(cw, d * n, st));
   return BS_OK;
 }
 

@@ -126,6 +126,50 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const u16* __restri
   }
 }
 
+// The transposed planes of an fp32 [R, C] matrix (C and ldi multiples of 4, 16-byte aligned rows,
+// ldo a multiple of 64) split into nterms bf16 terms per value (the split of planes_t_kernel): a
+// thread splits 4 consecutive columns of a row, each output row leaves the LDS tile as 16-byte
+// stores of 8 consecutive rows of the input.
+__global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* __restrict__ in, int64_t R, int64_t C,
+                                                                  int64_t ldi, PlaneOut out, int nterms, int64_t ldo,
+                                                                  float scale) {
+  __shared__ __attribute__((aligned(16))) u16 tile[3][64][72];
+  const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int rr = rg + 16 * i;
+    const int64_t r = r0 + rr, c = c0 + 4 * cg;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < R && c < C) v = *(const float4*)(in + r * ldi + c);
+    const float x[4] = {v.x * scale, v.y * scale, v.z * scale, v.w * scale};
+    u16 o[4][3];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) split_to(x[q], nterms, o[q]);
+#pragma unroll
+    for (int p = 0; p < 3; ++p)
+      if (p < nterms)
+        *(uint2*)&tile[p][rr][4 * cg] = make_uint2((uint32_t)o[0][p] | ((uint32_t)o[1][p] << 16),
+                                                   (uint32_t)o[2][p] | ((uint32_t)o[3][p] << 16));
+  }
+  __syncthreads();
+  const int q8 = (threadIdx.x & 7) * 8;
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int cc = (threadIdx.x >> 3) + 32 * pass;
+    const int64_t c = c0 + cc;
+    if (c >= C) continue;
+#pragma unroll
+    for (int p = 0; p < 3; ++p) {
+      if (p >= nterms) break;
+      uint32_t w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)tile[p][q8 + 2 * i][cc] | ((uint32_t)tile[p][q8 + 2 * i + 1][cc] << 16);
+      *(uint4*)(out.p[p] + c * ldo + r0 + q8) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+}
+
 bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64_t ldi, bool transpose,
                         u16* const* outp, int nterms, int64_t ldo, float scale, hipStream_t st) {
   if (nterms < 1 || nterms > 3) return BS_EINVAL;
@@ -135,8 +179,12 @@ bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64
     dim3 grid((unsigned)((C + 63) / 64), (unsigned)((ldo + 63) / 64));
     const bool vec = dt == BS_BF16 && nterms == 1 && scale == 1.0f && C % 8 == 0 && ldi % 8 == 0 && ldo % 64 == 0 &&
                      ((uintptr_t)in & 15) == 0 && ((uintptr_t)outp[0] & 15) == 0;
+    bool vecf = dt == BS_F32 && C % 4 == 0 && ldi % 4 == 0 && ldo % 64 == 0 && ((uintptr_t)in & 15) == 0;
+    for (int p = 0; p < nterms; ++p) vecf = vecf && ((uintptr_t)outp[p] & 15) == 0;
     if (vec)
       transpose_bf16_kernel<<<grid, 256, 0, st>>>((const u16*)in, R, C, ldi, outp[0], ldo);
+    else if (vecf)
+      transpose_split_f32_kernel<<<grid, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
     else if (dt == BS_F32)
       planes_t_kernel<float><<<grid, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
     else
