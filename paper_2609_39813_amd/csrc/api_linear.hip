@@ -1,5 +1,6 @@
 // C-ABI entry point of the Linear backward whose incoming gradient is rounded to FP8.
 #include "bsp_kernels.h"
+#include "k_combine.h"
 #include "k_linear.h"
 
 using namespace bsp;
@@ -172,12 +173,24 @@ bs_status bs_linear_bwd_policy(const void* X, const void* W, const void* dY, bs_
 
   // per-policy estimates and coupling
   const int64_t mk = M * k, kn = k * n;
+  {
+    CombineMulti cx{}, cw{};
+    cx.ref = dX_ref;
+    cw.ref = dW_ref;
+    cx.n_pol = cw.n_pol = n_pol;
+    cx.mean = dX.mean;
+    cx.bias_out = dX.bias;
+    cw.mean = dW.mean;
+    cw.bias_out = dW.bias;
+    for (int i = 0; i < n_pol; ++i) {
+      cx.bias[i] = w.bx[0];
+      cw.bias[i] = w.bw[sharing[i]];
+    }
+    BS_TRY(launch_combine_multi(cx, mk, st));
+    BS_TRY(launch_combine_multi(cw, kn, st));
+  }
   for (int i = 0; i < n_pol; ++i) {
     const int sh = sharing[i];
-    BS_TRY(launch_combine(dX_ref, w.bx[0], nullptr, mk, dX.mean ? dX.mean + i * mk : nullptr,
-                          dX.bias ? dX.bias + i * mk : nullptr, nullptr, st));
-    BS_TRY(launch_combine(dW_ref, w.bw[sh], nullptr, kn, dW.mean ? dW.mean + i * kn : nullptr,
-                          dW.bias ? dW.bias + i * kn : nullptr, nullptr, st));
     if (coupling_on) {
       if (sh == 0)
         BS_TRY(launch_kappa_final(w.fixed, w.part1, 0, w.part1, 1, nblk, K, dY_scale, coupling + i, st));

@@ -1,6 +1,7 @@
 // Argument blocks and launchers of the normalization-store kernels.
 #pragma once
 #include "bsp_kernels.h"
+#include "k_combine.h"
 
 namespace bsp {
 
@@ -87,16 +88,6 @@ bs_status launch_trial_accum(const float* delta, int nb, int k0, int64_t m, floa
 // se = sqrt(max(S2 - S1^2 / K, 0) / (K - 1) / K) (0 for K = 1)
 bs_status launch_trial_se(const double* S1, const double* S2, int K, int64_t m, float* se, hipStream_t st);
 
-constexpr int COMBINE_MAX_POL = 16;
-struct CombineMulti {
-  const float* ref;
-  int n_pol, vec;
-  const float* bias[COMBINE_MAX_POL];
-  const float* se[COMBINE_MAX_POL];
-  const float* alt[COMBINE_MAX_POL];
-  float *mean, *bias_out, *se_out;  // bases of [n_pol][n] outputs (nullable)
-};
-bs_status launch_combine_multi(CombineMulti c, int64_t n, hipStream_t st);
 // column sums of [3][nrt][d] fp64 partials (row tiles in order within 16 segments, the segments by
 // a fixed tree) into ref, bias_r and bias_n [d] (bias_r / bias_n nullable)
 bs_status launch_gain_final(const double* part, int64_t nrt, int64_t d, float* ref, float* bias_r, float* bias_n,
