@@ -123,11 +123,18 @@ __global__ void add_kernel(const TA* __restrict__ a, const float* __restrict__ b
 __global__ __launch_bounds__(256) void sumsq_batch_kernel(SumsqBatch b, double* __restrict__ part) {
   const SumsqJob j = b.job[blockIdx.y];
   double s = 0.0;
-  if (j.x)
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < j.n; i += (int64_t)SUMSQ_BLOCKS * 256) {
+  if (j.x) {
+    // 16-byte loads when the array allows them, then the scalar tail (fixed order per thread)
+    const int64_t n4 = ((uintptr_t)j.x & 15) == 0 ? j.n / 4 : 0;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)SUMSQ_BLOCKS * 256) {
+      const float4 v = ((const float4*)j.x)[i];
+      s += (double)v.x * v.x + (double)v.y * v.y + (double)v.z * v.z + (double)v.w * v.w;
+    }
+    for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * 256 + threadIdx.x; i < j.n; i += (int64_t)SUMSQ_BLOCKS * 256) {
       const double v = j.x[i];
       s += v * v;
     }
+  }
   __shared__ double red[4];
   s = wave_sum_f64(s);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;

@@ -73,6 +73,29 @@ __global__ __launch_bounds__(256) void planes_rows_kernel(const T* __restrict__ 
   }
 }
 
+// The same planes of an fp32 matrix 4 elements per thread (C, ldi and ldo multiples of 4, 16-byte
+// aligned input rows, 8-byte aligned planes): one index division per 4 elements, 16-byte loads,
+// 8-byte stores per plane.
+__global__ __launch_bounds__(256) void planes_rows4_kernel(const float* __restrict__ in, int64_t R, int64_t C,
+                                                           int64_t ldi, PlaneOut out, int nterms, int64_t ldo,
+                                                           float scale) {
+  const int64_t q = ldo / 4, n = R * q;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / q, c = 4 * (i - r * q);
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (c < C) v = *(const float4*)(in + r * ldi + c);
+    const float x[4] = {v.x * scale, v.y * scale, v.z * scale, v.w * scale};
+    u16 o[4][3];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) split_to(x[k], nterms, o[k]);
+#pragma unroll
+    for (int p = 0; p < 3; ++p)
+      if (p < nterms)
+        *(uint2*)(out.p[p] + 4 * i) = make_uint2((uint32_t)o[0][p] | ((uint32_t)o[1][p] << 16),
+                                                 (uint32_t)o[2][p] | ((uint32_t)o[3][p] << 16));
+  }
+}
+
 // Transposed: out_p[c * ldo + r] for r < ldo (zero for r >= R). Tile 64 x 64 through LDS.
 template <typename T>
 __global__ __launch_bounds__(256) void planes_t_kernel(const T* __restrict__ in, int64_t R, int64_t C, int64_t ldi,
@@ -194,7 +217,13 @@ bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64
     if (n <= 0) return BS_OK;
     const int64_t want = (n + 255) / 256;
     const unsigned blocks = (unsigned)(want < 8192 ? want : 8192);
-    if (dt == BS_F32)
+    bool vec4 = dt == BS_F32 && C % 4 == 0 && ldi % 4 == 0 && ldo % 4 == 0 && ((uintptr_t)in & 15) == 0;
+    for (int p = 0; p < nterms; ++p) vec4 = vec4 && ((uintptr_t)outp[p] & 7) == 0;
+    if (vec4) {
+      const int64_t want4 = (n / 4 + 255) / 256;
+      planes_rows4_kernel<<<(unsigned)(want4 < 8192 ? want4 : 8192), 256, 0, st>>>((const float*)in, R, C, ldi, out,
+                                                                                   nterms, ldo, scale);
+    } else if (dt == BS_F32)
       planes_rows_kernel<float><<<blocks, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
     else
       planes_rows_kernel<u16><<<blocks, 256, 0, st>>>((const u16*)in, R, C, ldi, out, nterms, ldo, scale);
