@@ -65,26 +65,37 @@ __device__ __forceinline__ void write_policies(const PstoreArgs& a, const int (&
 // ------------------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void pstore_scale_kernel(const float* __restrict__ l, int64_t rows, float fmax,
                                                             bs_diag* __restrict__ diag, float* __restrict__ scale_out) {
-  uint32_t m = 0;
+  // the largest probability of a row is fl32(1 / l); correctly rounded reciprocals are monotone,
+  // so the largest over rows is fl32(1 / min l) (rows with a bad sum are flagged, not counted)
+  float mn = INFINITY;
   bool bad = false;
-  for (int64_t i = threadIdx.x; i < rows; i += blockDim.x) {
-    const float v = l[i];
-    bad |= !(v > 0.0f) || !isfinite(v);
-    m = max(m, __float_as_uint(1.0f / v));
+  auto take = [&](float v) {
+    const bool ok = v > 0.0f && isfinite(v);
+    bad |= !ok;
+    mn = ok ? fminf(mn, v) : mn;
+  };
+  const int64_t n4 = ((uintptr_t)l & 15) == 0 ? rows / 4 : 0;
+  for (int64_t i = threadIdx.x; i < n4; i += blockDim.x) {
+    const float4 v = ((const float4*)l)[i];
+    take(v.x);
+    take(v.y);
+    take(v.z);
+    take(v.w);
   }
-  m = wave_max_u32(m);
+  for (int64_t i = 4 * n4 + threadIdx.x; i < rows; i += blockDim.x) take(l[i]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mn = fminf(mn, __shfl_xor(mn, off, 64));
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  __shared__ uint32_t red[16];
+  __shared__ float red[16];
   __shared__ int anybad;
   if (threadIdx.x == 0) anybad = 0;
   __syncthreads();
   if (bad) anybad = 1;
-  if (lane == 0) red[w] = m;
+  if (lane == 0) red[w] = mn;
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int k = 1; k < (int)(blockDim.x >> 6); ++k) m = max(m, red[k]);
-    m = max(m, red[0]);
-    const float amax = __uint_as_float(m);
+    for (int k = 1; k < (int)(blockDim.x >> 6); ++k) mn = fminf(mn, red[k]);
+    const float amax = isfinite(mn) ? 1.0f / mn : 0.0f;
     diag->amax = amax;
     diag->nonfinite = anybad ? 1u : 0u;
     diag->n_saturated = 0;
