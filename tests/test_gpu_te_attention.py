@@ -64,6 +64,7 @@ def run_case(lib, B, H, S, *, causal=True, source="R", factors=(1, 1, 1, 1), sha
                    causal=causal, c=c, scales=sc, source=source, thr=F32(thr), seed=seed, store_id=store_id,
                    trial=trial)
     compare(out, ref, Q, K, causal, c, sc)
+    ref.update(O32=O32, Oc=q.codes, Os=q.scale, sc=sc)
     return out, ref
 
 
@@ -132,6 +133,19 @@ def test_repair_selects_saturated_rows(lib):
     out, ref = run_case(lib, 1, 2, 136, source="repair", sharp=4, seed=5)
     n = int(out["counts"].cpu()[0])
     assert 0 < n < 2 * 136 and n == sum(ref["sat_rows"])
+
+
+@pytest.mark.parametrize("thr", [0.0, 1.5])
+def test_repair_threshold_extremes(lib, thr):
+    """Threshold 0: every row reads D from P (the same D as the P source); above 1: no row does
+    (the same D as the R source). Checked through dS against the oracle of the plain source."""
+    out, ref = run_case(lib, 1, 2, 72, source="repair", thr=thr, seed=12, causal=False)
+    n = int(out["counts"].cpu()[0])
+    assert n == (2 * 72 if thr == 0.0 else 0)
+    plain = te.check(*(t.float().numpy() for t in inputs(1, 2, 72, 12)), P=out["P"].cpu().numpy(),
+                     dS=out["dS"].cpu().numpy(), O=ref["O32"], O_codes=ref["Oc"], O_scale=ref["Os"], causal=False,
+                     c=0.125, scales=ref["sc"], source="P" if thr == 0.0 else "R", seed=12, store_id=4, trial=3)
+    np.testing.assert_array_equal(plain["D"], ref["D"])
 
 
 @pytest.mark.parametrize("S", [4, 64])
