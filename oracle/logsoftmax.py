@@ -54,8 +54,9 @@ def signs(eps, seed, trial, use, elements):
 def entry_errors(l, y, r, rp, calibrate=1.0):
     """(g - g*) / p per entry for the four (loss, copy) pairs, given the draws r (consumed) and rp."""
     p = np.exp(l)
-    onehot = np.zeros_like(l)
-    np.put_along_axis(onehot, np.asarray(y)[:, None], 1.0, axis=-1)
+    # h = -e_y; a target outside the classes selects none (h = 0 on that row)
+    y = np.asarray(y)
+    onehot = (np.arange(l.shape[-1])[None, :] == y[:, None]).astype(l.dtype)
     out = {}
     for loss, h in (("likelihood", -onehot), ("constructed", r)):
         gstar = backward(h, l)

@@ -68,3 +68,21 @@ def test_monte_carlo_statistics_at_the_papers_shape():
         m, se = out[k]
         assert se > 0 and abs(m - t) < 5 * se, (k, m, t, se)
     assert abs(out["constructed_reuse"][0]) > 20 * out["constructed_reuse"][1]    # resolved
+
+
+def test_target_outside_the_classes_selects_none():
+    """h = -e_y has no entry for a target outside [0, C): the likelihood's errors vanish on that
+    row (g = g* = 0), under reuse and with the independent copy; other rows are unchanged."""
+    rng = np.random.default_rng(5)
+    z = rng.normal(0, 2, size=(3, 6))
+    l = ls.log_softmax(z)
+    r = np.where(rng.random((3, 6)) < 0.5, 0.1, -0.1)
+    rp = np.where(rng.random((3, 6)) < 0.5, 0.1, -0.1)
+    base = ls.entry_errors(l, np.array([2, 4, 1]), r, rp)
+    for bad in (-1, 6):
+        e = ls.entry_errors(l, np.array([2, bad, 1]), r, rp)
+        for k in ("likelihood_reuse", "likelihood_independent"):
+            assert np.all(e[k][1] == 0.0)
+            np.testing.assert_array_equal(e[k][[0, 2]], base[k][[0, 2]])
+        for k in ("constructed_reuse", "constructed_independent"):
+            np.testing.assert_array_equal(e[k], base[k])
