@@ -55,6 +55,7 @@ __global__ __launch_bounds__(64) void lsm_trial_kernel(const double* __restrict_
   const int64_t row = blockIdx.x;
   const int lane = threadIdx.x;
   const int yt = y[row];
+  const double sh = (yt >= 0 && yt < C) ? -1.0 : 0.0;
   const int ngroups = C / 4;
   const int k_end = min(K, (int)(blockIdx.y + 1) * LSM_TCH);
   for (int k = blockIdx.y * LSM_TCH; k < k_end; ++k) {
@@ -82,11 +83,11 @@ __global__ __launch_bounds__(64) void lsm_trial_kernel(const double* __restrict_
         const bool ur = R[q] >= 0x80000000u, urp = Rp[q] >= 0x80000000u;
         const double r = ur ? eps : -eps;
         const double er = ur ? epv[e] : emv[e], erp = urp ? epv[e] : emv[e];
-        // likelihood: h = -e_y, 1^T h = -1
+        // likelihood: h = -e_y, 1^T h = sh (-1, or 0 for a target outside the classes)
         const double hl = j == yt ? -1.0 : 0.0;
-        const double gl_star = hl + p;
-        acc[0] += ((hl + er) - gl_star) / p;
-        acc[1] += ((hl + erp) - gl_star) / p;
+        const double gl_star = hl - p * sh;
+        acc[0] += ((hl - er * sh) - gl_star) / p;
+        acc[1] += ((hl - erp * sh) - gl_star) / p;
         // constructed: h = r, 1^T h = sr
         const double gc_star = r - p * sr;
         acc[2] += ((r - er * sr) - gc_star) / p;

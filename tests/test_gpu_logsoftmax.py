@@ -30,7 +30,8 @@ def run(lib, rows, C, K, eps, seed, calibrate=False):
 
 
 @pytest.mark.parametrize("rows,C,K,eps,calibrate", [(3, 8, 40, 0.1, False), (5, 132, 33, 0.35, True),
-                                                    (1, 4, 1, 0.2, False), (7, 260, 70, 0.05, False)])
+                                                    (1, 4, 1, 0.2, False), (7, 260, 70, 0.05, False),
+                                                    (4, 16, 300, 0.1, False)])
 def test_statistics_match_oracle(lib, rows, C, K, eps, calibrate):
     z, y, got = run(lib, rows, C, K, eps, seed=rows, calibrate=calibrate)
     ref = ls.check(z.numpy(), y.numpy(), eps=eps, K=K, seed=rows, store_id=1, calibrate=calibrate)
@@ -39,6 +40,17 @@ def test_statistics_match_oracle(lib, rows, C, K, eps, calibrate):
         scale = max(abs(m), se, 1e-300)
         assert abs(got[i, 0] - m) <= 1e-9 * scale, (name, got[i, 0], m)
         assert abs(got[i, 1] - se) <= 1e-9 * max(se, 1e-300) or (K == 1 and got[i, 1] == 0), (name, got[i, 1], se)
+
+
+def test_targets_outside_the_classes_match_none(lib):
+    """A target outside [0, C) makes the likelihood's h zero on that row, on both sides."""
+    z, y = inputs(4, 12, 3)
+    y[1], y[3] = -1, 12
+    got = lib.logsoftmax_reuse_check(z.cuda(), y.cuda(), eps=0.1, K=50, seed=3, store_id=1).cpu().numpy()
+    ref = ls.check(z.numpy(), y.numpy(), eps=0.1, K=50, seed=3, store_id=1)
+    for i, name in enumerate(ls.STATS):
+        m, se = ref[name]
+        assert abs(got[i, 0] - m) <= 1e-9 * max(abs(m), se, 1e-300), (name, got[i, 0], m)
 
 
 def test_papers_configuration_matches_closed_forms(lib):
