@@ -127,3 +127,30 @@ def test_weight_use_se_per_trial(lib):
                                fmt=fp8.E4M3, fwd_mode=oq.RNE, policies=pols, K=K, seed=31, fresh_shared=shared)
         assert out["dW"]["se"] is not None
         compare(out, ref, pols, d=d, n=n)
+
+
+def test_forward_only_and_no_tokens(lib):
+    """dY NULL: the store and Y only (against the oracle); T = 0 with a non-NULL dY: references
+    and estimates are zero, the store reports amax 0 and scale 1."""
+    X, g, W, dY = synth.rmsnorm_linear_inputs(40, 32, 16, torch.bfloat16, config=41)
+    print("[norm_store] forward only T=40 d=32 n=16", flush=True)
+    out = lib.rmsnorm_linear(X.cuda(), g.cuda(), W.cuda(), None, K=4, seed=2)
+    torch.cuda.synchronize()
+    ref = norm_store.check(X.float().numpy(), g.numpy(), W.float().numpy(), dY.float().numpy(), fmt=fp8.E4M3,
+                           fwd_mode=oq.RNE, policies=("U/U",), K=4, seed=2)
+    assert np.array_equal(out["u_codes"].cpu().numpy(), ref["codes"])
+    assert float(out["u_scale"].cpu()[0]) == float(ref["scale"])
+    assert_rel(out["Y"], ref["Y"], TOL, "Y")
+    print("[norm_store] no tokens T=0 d=32 n=16", flush=True)
+    X0 = torch.empty(0, 32, dtype=torch.bfloat16, device="cuda")
+    # torch gives an empty tensor a NULL pointer, which asks for the forward only: a one-row
+    # gradient supplies a valid pointer, of which T = 0 rows are read
+    dY0 = torch.zeros(1, 16, dtype=torch.bfloat16, device="cuda")
+    out = lib.rmsnorm_linear(X0, g.cuda(), W.cuda(), dY0, K=4, seed=2)
+    torch.cuda.synchronize()
+    d = lib.diag_dict(out["diag"])
+    assert d["amax"] == 0.0 and d["scale"] == 1.0 and d["nonfinite"] == 0
+    for name in ("dgain_ref", "dW_ref"):
+        assert not torch.any(out[name] != 0), name
+    for name in ("dgain", "dW"):
+        assert not torch.any(out[name]["mean"] != 0) and not torch.any(out[name]["bias"] != 0), name
