@@ -33,6 +33,22 @@ def test_codes_bit_exact(lib, dtype, fmt, mode, n):
 
 @pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
 @pytest.mark.parametrize("mode", ["rne", "sr"])
+@pytest.mark.parametrize("factor", [0.25, 8.0])
+def test_given_scale_clamps_and_coarse(lib, fmt, mode, factor):
+    """A caller's scale (a delayed scale): a quarter of the amax scale clamps the largest entries
+    (counted), eight times it sends the small entries to subnormals and zero; codes bit for bit."""
+    g = torch.Generator().manual_seed(31)
+    x = torch.randn(20011, generator=g) * 2
+    s_in = np.float32(np.float32(np.abs(x.numpy()).max()) / np.float32(FMT[fmt].fmax) * np.float32(factor))
+    codes, s, dg = run(lib, x, fmt, mode, seed=41, trial=2, use=513, scale=torch.tensor([s_in]))
+    ref = oq.qround(x.numpy(), FMT[fmt], oq.RNE if mode == "rne" else oq.SR, 41, 2, 513, scale=s_in)
+    assert s == float(s_in) and dg["n_saturated"] == ref.n_saturated
+    assert (ref.n_saturated > 0) == (factor < 1)
+    assert np.array_equal(codes, ref.codes)
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+@pytest.mark.parametrize("mode", ["rne", "sr"])
 def test_codec_edge_values_unit_scale(lib, fmt, mode):
     f = FMT[fmt]
     grid = np.unique(np.abs(fp8.decode(np.arange(256, dtype=np.uint8), f)))
