@@ -672,6 +672,13 @@ template bs_status launch_dx_t<u16>(const DxArgs<u16>&, hipStream_t);
 // Every policy's estimate of one gradient in one pass over ref: policy p writes mean_p = ref +
 // bias_p (or alt_p, with bias_p = alt_p - ref, when alt_p is set), bias_p and se_p (bias_p / se_p
 // inputs nullable = 0) at offset p n of the nullable output bases.
+// a 16-byte non-temporal store (p 16-byte aligned)
+__device__ __forceinline__ void store4_nt(float* p, float4 v) {
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  const f32x4 w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, (f32x4*)p);
+}
+
 __global__ __launch_bounds__(256) void combine_multi_kernel(CombineMulti c, int64_t n) {
   const int64_t n4 = c.vec ? n / 4 : 0;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -688,9 +695,10 @@ __global__ __launch_bounds__(256) void combine_multi_kernel(CombineMulti c, int6
         b = c.bias[p] ? ((const float4*)c.bias[p])[i] : z;
         m = c.bias[p] ? make_float4(r.x + b.x, r.y + b.y, r.z + b.z, r.w + b.w) : r;
       }
-      if (c.mean) ((float4*)c.mean)[o] = m;
-      if (c.bias_out) ((float4*)c.bias_out)[o] = b;
-      if (c.se_out) ((float4*)c.se_out)[o] = c.se[p] ? ((const float4*)c.se[p])[i] : z;
+      // streaming outputs: non-temporal stores keep them from displacing the inputs in the caches
+      if (c.mean) store4_nt(c.mean + 4 * o, m);
+      if (c.bias_out) store4_nt(c.bias_out + 4 * o, b);
+      if (c.se_out) store4_nt(c.se_out + 4 * o, c.se[p] ? ((const float4*)c.se[p])[i] : z);
     }
   }
   for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
