@@ -90,10 +90,11 @@ int bs_version(void);
  * bs_qround -- the FP8 store of one tensor (Sec. 2.1; App. D.2, "at the TE output scale").
  *   x        [n] fp32 or bf16 (xt).
  *   fmt/mode format and rounding rule; seed/trial/use key the Philox words (SR only).
- *   scale_in NULL: s = amax/FMAX from x; else s = *scale_in (device fp32, > 0).
+ *   scale_in NULL: s = amax/FMAX from x; else s = *scale_in (device fp32, > 0), a delayed
+ *            scale: it replaces s only; amax and the NaN / infinity check still run over x.
  *   codes    [n] uint8 out.  scale_out [1] fp32 out (the s used).
- *   diag     [1] out.
- * n may be 0 (diag then reports amax 0, scale 1). No workspace.
+ *   diag     [1] out: amax of x (also with scale_in), scale, nonfinite, n_saturated.
+ * n may be 0 (diag then reports amax 0, scale 1, or *scale_in). No workspace.
  * ---------------------------------------------------------------------------------- */
 bs_status bs_qround(const void* x, bs_dtype xt, int64_t n, bs_fp8 fmt, bs_round mode,
                     uint64_t seed, uint32_t trial, uint32_t use, const float* scale_in,

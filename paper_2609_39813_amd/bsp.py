@@ -225,7 +225,11 @@ def gemm_bf16_nt(A, B, alpha=1.0, out=None, accumulate=False):
 def policy_bias_estimate(delta, g_ref=None):
     """Trial statistics of per-trial errors delta [K, m]: (mean_err, se, summary[3])."""
     _dev_check(delta, g_ref)
+    if delta.dim() != 2 or delta.dtype != torch.float32:
+        raise TypeError("delta must be a [K, m] float32 tensor")
     K, m = delta.shape
+    if g_ref is not None and (g_ref.dtype != torch.float32 or g_ref.numel() != m):
+        raise TypeError("g_ref must be a float32 tensor of m elements")
     mean = torch.empty(m, dtype=torch.float32, device=delta.device)
     se = torch.empty(m, dtype=torch.float32, device=delta.device)
     summ = torch.empty(3, dtype=torch.float64, device=delta.device)

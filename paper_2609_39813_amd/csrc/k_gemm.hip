@@ -142,10 +142,8 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs g) {
 // of row r sits at unit u ^ swz(r) of its LDS row, so that the rows one ds_read_b128 serves
 // together fall on distinct banks.
 constexpr int LBK = 64, LNST = 2;
-#ifndef BSP_GEMM_SWZ
-#define BSP_GEMM_SWZ(r) ((r) & 7)
-#endif
-__device__ __forceinline__ int lds_swz(int r, int u) { return r * 128 + ((u ^ BSP_GEMM_SWZ(r)) << 4); }
+__device__ __forceinline__ int swz_of(int r) { return r & 7; }
+__device__ __forceinline__ int lds_swz(int r, int u) { return r * 128 + ((u ^ swz_of(r)) << 4); }
 
 // Block tile BM x BN, WGM x WGN wave64s, each owning a (BM / WGM) x (BN / WGN) tile.
 template <int BM, int BN, int WGM, int WGN>
@@ -182,8 +180,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
   // swz(row) = swz(l / 8) because the row's other terms are multiples of 8. One per-lane byte
   // offset per operand; the load index and the k position enter as scalar offsets.
   const int rows_a = min(g.M - bm, BM), rows_b = min(g.N - bn, BN);
-  const uint32_t lane_a = (uint32_t)(((wave * AI * 8 + (lane >> 3)) * g.lda + (((lane & 7) ^ BSP_GEMM_SWZ(lane >> 3)) << 3)) * 2);
-  const uint32_t lane_b = (uint32_t)(((wave * BI * 8 + (lane >> 3)) * g.ldb + (((lane & 7) ^ BSP_GEMM_SWZ(lane >> 3)) << 3)) * 2);
+  const uint32_t lane_a = (uint32_t)(((wave * AI * 8 + (lane >> 3)) * g.lda + (((lane & 7) ^ swz_of(lane >> 3)) << 3)) * 2);
+  const uint32_t lane_b = (uint32_t)(((wave * BI * 8 + (lane >> 3)) * g.ldb + (((lane & 7) ^ swz_of(lane >> 3)) << 3)) * 2);
   const uint32_t step_a = (uint32_t)(8 * g.lda * 2), step_b = (uint32_t)(8 * g.ldb * 2);
   auto rsrc = [](const u16* base, int64_t row0, int rows, int64_t ld) {
     return __builtin_amdgcn_make_buffer_rsrc((void*)(base + row0 * ld), (short)0, (int)(rows * ld * 2), 0x00020000);
@@ -395,25 +393,18 @@ bs_status launch_gemm(const GemmArgs& g, hipStream_t st) {
   if (g.nseg < 1 || g.nseg > GEMM_MAX_SEG) return BS_EINVAL;
   if ((g.K & 7) || (g.lda & 7) || (g.ldb & 7) || g.lda < g.K || g.ldb < g.K) return BS_ESHAPE;
   if (g.K == 0) return g.accumulate ? BS_OK : launch_fill2d(g.C, g.M, g.N, g.ldc, 0.0f, st);
-#ifdef BSP_GEMM_CFG
-  return BSP_GEMM_CFG(g, st);
-#else
   // pipelined kernel for 64-aligned K and 16-byte aligned operands
   // (buffer offsets of one 256-row tile fit in 31 bits)
   bool lds_ok = (g.K % LBK) == 0 && g.M >= 1 && g.N >= 1 && g.lda < (1 << 21) && g.ldb < (1 << 21);
   for (int i = 0; i < g.nseg; ++i) lds_ok = lds_ok && ((uintptr_t)g.A[i] & 15) == 0 && ((uintptr_t)g.B[i] & 15) == 0;
   if (lds_ok) {
-#ifndef BSP_GEMM_BIG
-#define BSP_GEMM_BIG 256, 256, 2, 4
-#endif
-    if ((int64_t)g.M * g.N >= (int64_t)256 * 256 * 16) return launch_gemm_lds<BSP_GEMM_BIG>(g, st);
+    if ((int64_t)g.M * g.N >= (int64_t)256 * 256 * 16) return launch_gemm_lds<256, 256, 2, 4>(g, st);
     return launch_gemm_lds<128, 128, 2, 2>(g, st);
   }
   // 256 x 256 tiles once they still give every CU a tile; 128 x 128 below that
   const int64_t big = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256);
   if (big >= 256) return launch_gemm_cfg<256, 256, 2, 2>(g, st);
   return launch_gemm_cfg<128, 128, 2, 2>(g, st);
-#endif
 }
 
 }  // namespace bsp

@@ -377,7 +377,9 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
   const F8 f = f8_format(fmt);
   if (!amax_done) {
     init_diag_kernel<<<1, 64, 0, st>>>(diag);
-    if (n > 0 && !scale_in) {
+    // amax runs with a caller's scale too: it flags NaN / infinity (no codes then) and reports the
+    // tensor's amax to a delayed-scaling caller's history; the caller's scale replaces only s
+    if (n > 0) {
       // four blocks per CU, each streaming a contiguous range with eight 16-byte loads in flight
       // per thread; the per-block atomics stay few (same-address atomics serialize)
       const int64_t want = (n / (16 / (xt == BS_F32 ? 4 : 2)) + 255) / 256 + 1;

@@ -272,14 +272,26 @@ __global__ __launch_bounds__(256) void trial_stats_kernel(const float* __restric
   }
 }
 
-__global__ void trial_summary_kernel(const double* __restrict__ part, int64_t nblk, double* __restrict__ summary) {
-  if (threadIdx.x != 0) return;
+// One block of 256 threads: thread i adds the partials of blocks i, i + 256, ... in order, then a
+// fixed pairwise tree (offsets 128, 64, ..., 1) combines the threads (deterministic).
+__global__ __launch_bounds__(256) void trial_summary_kernel(const double* __restrict__ part, int64_t nblk,
+                                                            double* __restrict__ summary) {
+  __shared__ double red[3][256];
   double s[3] = {0.0, 0.0, 0.0};
-  for (int64_t b = 0; b < nblk; ++b)
+  for (int64_t b = threadIdx.x; b < nblk; b += 256)
     for (int i = 0; i < 3; ++i) s[i] += part[b * 3 + i];
-  summary[0] = sqrt(s[0]);
-  summary[1] = sqrt(s[1]);
-  summary[2] = s[2] > 0.0 ? s[0] / s[2] : __builtin_nan("");
+  for (int i = 0; i < 3; ++i) red[i][threadIdx.x] = s[i];
+  __syncthreads();
+  for (int off = 128; off >= 1; off >>= 1) {
+    if ((int)threadIdx.x < off)
+      for (int i = 0; i < 3; ++i) red[i][threadIdx.x] += red[i][threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    summary[0] = sqrt(red[0][0]);
+    summary[1] = sqrt(red[1][0]);
+    summary[2] = red[2][0] > 0.0 ? red[0][0] / red[2][0] : __builtin_nan("");
+  }
 }
 
 bs_status launch_policy_bias(const float* delta, int K, int64_t m, const float* g_ref, float* mean_err, float* se,
@@ -287,7 +299,7 @@ bs_status launch_policy_bias(const float* delta, int K, int64_t m, const float* 
   const int64_t nblk = (m + 255) / 256;
   if (nblk > 0)
     trial_stats_kernel<<<(unsigned)nblk, 256, 0, st>>>(delta, K, m, g_ref, mean_err, se, ws);
-  if (summary) trial_summary_kernel<<<1, 64, 0, st>>>(ws, nblk, summary);
+  if (summary) trial_summary_kernel<<<1, 256, 0, st>>>(ws, nblk, summary);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

@@ -1,6 +1,8 @@
 // Kernel timing instrumentation: when enabled, a pair of HIP events is recorded on the
 // launch stream around each instrumented kernel launch; bs_profile_read() waits for the
-// events and sums the elapsed time per kernel name. Off by default (no events recorded).
+// events and sums the elapsed time per kernel name. Off by default (no events recorded): a
+// launch then reads one atomic flag and takes no lock.
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -15,7 +17,7 @@ struct Rec {
   hipEvent_t a, b;
 };
 std::mutex g_mu;
-bool g_on = false;
+std::atomic<bool> g_on{false};
 std::vector<hipEvent_t> g_pool;
 size_t g_next = 0;
 std::vector<Rec> g_recs;
@@ -30,8 +32,9 @@ void release_all() {
 }  // namespace
 
 ProfScope::ProfScope(const char* name, hipStream_t st) : name_(name), st_(st), a_(nullptr), b_(nullptr) {
+  if (!g_on.load(std::memory_order_acquire)) return;
   std::lock_guard<std::mutex> lk(g_mu);
-  if (!g_on || g_next + 2 > g_pool.size()) return;
+  if (!g_on.load(std::memory_order_relaxed) || g_next + 2 > g_pool.size()) return;
   a_ = g_pool[g_next++];
   b_ = g_pool[g_next++];
   hipEventRecord(a_, st_);
@@ -51,12 +54,13 @@ extern "C" {
 int bs_profile_enable(int on) {
   using namespace bsp;
   std::lock_guard<std::mutex> lk(g_mu);
+  g_on.store(false, std::memory_order_release);
   release_all();
-  g_on = on != 0;
-  if (g_on) {
+  if (on != 0) {
     g_pool.resize(kPool);
     for (auto& e : g_pool)
       if (hipEventCreate(&e) != hipSuccess) return BS_EHIP;
+    g_on.store(true, std::memory_order_release);
   }
   return BS_OK;
 }

@@ -43,6 +43,7 @@ def test_given_scale_clamps_and_coarse(lib, fmt, mode, factor):
     codes, s, dg = run(lib, x, fmt, mode, seed=41, trial=2, use=513, scale=torch.tensor([s_in]))
     ref = oq.qround(x.numpy(), FMT[fmt], oq.RNE if mode == "rne" else oq.SR, 41, 2, 513, scale=s_in)
     assert s == float(s_in) and dg["n_saturated"] == ref.n_saturated
+    assert dg["amax"] == float(ref.amax) and dg["nonfinite"] == 0    # reported for the caller's history
     assert (ref.n_saturated > 0) == (factor < 1)
     assert np.array_equal(codes, ref.codes)
 
@@ -80,6 +81,9 @@ def test_nonfinite_flagged(lib, bad):
     x[1234] = bad
     _, _, dg = run(lib, x, "e4m3", "rne")
     assert dg["nonfinite"] == 1
+    # with a caller's scale the tensor is checked as well
+    _, s, dg = run(lib, x, "e5m2", "sr", seed=3, scale=torch.tensor([0.5]))
+    assert dg["nonfinite"] == 1 and s == 0.5
 
 
 def test_large_tensor_sampled_sr(lib):

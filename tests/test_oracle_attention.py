@@ -1,8 +1,9 @@
 """Pins of the attention oracle (oracle/attention.py)."""
 import numpy as np
+import pytest
 import torch
 
-from oracle import attention, fp8, qround
+from oracle import attention, fp8, policy, qround
 from tests import attn_example
 
 
@@ -88,3 +89,22 @@ def test_new_rounding_mean_within_band():
     assert np.all(np.abs(mean[0] - dq) <= 4.5 * se[0] + 1e-12)
     mean, _, se = out["N"]["dK"]
     assert np.all(np.abs(mean[0] - dk) <= 4.5 * se[0] + 1e-12)
+
+
+def test_planted_d_from_the_wrong_copy_fails_the_pins(monkeypatch):
+    """D read from the forward's rounded copy where the original was handed in (the reference's
+    D), or the R policy reading the original: the autograd pin, resp. the closed form of R's bias,
+    must fail."""
+    d_from = attention.d_from_copy
+
+    def rounded_copy(dO, Ohat):
+        q = qround.qround(np.asarray(Ohat, np.float32), fp8.E4M3, qround.RNE)
+        return d_from(dO, qround.dequant(q.codes, q.scale, fp8.E4M3))
+    monkeypatch.setattr(attention, "d_from_copy", rounded_copy)
+    with pytest.raises(AssertionError):
+        test_reference_matches_autograd()
+    monkeypatch.undo()
+    read = policy.read
+    monkeypatch.setattr(policy, "read", lambda l, o, r, f: read({"R": "U"}.get(l, l), o, r, f))
+    with pytest.raises(AssertionError):
+        test_policy_biases_have_row_scaled_form()

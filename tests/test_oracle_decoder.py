@@ -1,5 +1,6 @@
 """Pins of the decoder-layer oracle (oracle/decoder.py)."""
 import numpy as np
+import pytest
 import torch
 
 from oracle import decoder, fp8, qround
@@ -65,3 +66,102 @@ def test_per_use_reference_letters_are_exact_zeros_and_weight_closed_form():
     rows = decoder.table(t)
     assert rows[("a", "weight", "dW", "R")]["rel_bias"] == 0.0
     assert rows[("O", "D", "dQ", "R")]["rel_bias"] > 0.0
+
+
+# ---------------------------------------------------------------------------------------------
+# The forward itself, pinned stage by stage against an independent torch fp64 program written
+# from App. D.1's block (pre-norm RMSNorm, causal multi-head attention, SwiGLU MLP, no biases),
+# with torch's own float8 casts (round to nearest even) as the codec of the four stores. Each
+# stage is recomputed from the oracle's realized value of the stage before it, so a wrong
+# formula anywhere (a swapped weight or gain, a dropped residual, a wrong mask) fails at its own
+# stage, while fp32 rounding of the oracle's values stays within FWD_TOL.
+# ---------------------------------------------------------------------------------------------
+FWD_TOL = 1e-6
+
+
+def _torch_store(u, fmax=448.0):
+    """Per-tensor FP8 E4M3 store by torch's cast: s = fl32(amax / FMAX), y = fl32(u / s) clamped
+    to +-FMAX, code = RNE cast; returns (code bytes, dequantized fp64 values, s)."""
+    u32 = torch.as_tensor(np.asarray(u, np.float32))
+    amax = u32.abs().max()
+    s = (amax / torch.tensor(fmax, dtype=torch.float32)) if float(amax) > 0 else torch.tensor(1.0)
+    y = (u32 / s).clamp(-fmax, fmax)
+    c8 = y.to(torch.float8_e4m3fn)
+    return c8.view(torch.uint8).numpy(), c8.to(torch.float64) * float(s), np.float32(s)
+
+
+def forward_stage_errors(f, x, p, B, S, H, eps=1e-5):
+    """{stage: relative error or code mismatch count} of the oracle's realized forward f."""
+    T, d = x.shape
+    dh = d // H
+    t64 = lambda a: torch.as_tensor(np.asarray(a, np.float32)).to(torch.float64)
+    W = {k: t64(p[k]) for k in ("Wqkv", "Wo", "Wg", "Wu", "Wd")}
+    g1, g2 = t64(p["gain1"]), t64(p["gain2"])
+    rel = lambda got, want: float(torch.linalg.norm(t64(got) - want) / torch.linalg.norm(want))
+    rms = lambda v, g: g * v / torch.sqrt((v * v).mean(-1, keepdim=True) + eps)
+    hs = lambda m: m.reshape(B, S, H, dh).permute(0, 2, 1, 3)
+    err = {}
+
+    def store(name, value, q):
+        codes, deq, s = _torch_store(value)
+        err[name + "_codes"] = int((codes != q.codes.reshape(codes.shape)).sum())
+        err[name + "_scale"] = int(s != q.scale)
+        return deq
+
+    err["u1"] = rel(f["u1"], rms(t64(x), g1))
+    u1q = store("u1", f["u1"], f["q1"])
+    err["QKV"] = rel(f["QKV"], u1q @ W["Wqkv"])
+    qkv16 = torch.as_tensor(f["QKV"]).to(torch.bfloat16).to(torch.float64)
+    for i, n in enumerate("QKV"):
+        err[n] = int((t64(f[n]) != hs(qkv16[:, i * d:(i + 1) * d])).sum())
+    Q, K, V = (t64(f[n]) for n in "QKV")
+    sc = (Q @ K.transpose(-1, -2)) / np.sqrt(dh)
+    sc = sc.masked_fill(~torch.tril(torch.ones(S, S, dtype=torch.bool)), float("-inf"))
+    err["O"] = rel(f["O"], torch.softmax(sc, -1) @ V)
+    Oq = store("O", f["O"], f["qO"])
+    err["h"] = rel(f["h"], t64(x) + Oq.permute(0, 2, 1, 3).reshape(T, d) @ W["Wo"])
+    err["u2"] = rel(f["u2"], rms(t64(f["h"]), g2))
+    u2q = store("u2", f["u2"], f["q2"])
+    err["g"] = rel(f["g"], u2q @ W["Wg"])
+    err["hh"] = rel(f["hh"], u2q @ W["Wu"])
+    err["a"] = rel(f["a"], torch.nn.functional.silu(t64(f["g"])) * t64(f["hh"]))
+    aq = store("a", f["a"], f["qa"])
+    err["out"] = rel(f["out"], t64(f["h"]) + aq @ W["Wd"])
+    return err
+
+
+def forward_failures(err):
+    return {k: v for k, v in err.items() if (v > FWD_TOL if isinstance(v, float) else v != 0)}
+
+
+def _pin_case(seed=0):
+    (x, p, dOut), (B, S, H) = small(seed=seed)
+    pn = {k: v.float().numpy() for k, v in p.items()}
+    g = torch.Generator().manual_seed(77 + seed)
+    pn["gain1"] = (1 + 0.1 * torch.randn(x.shape[1], generator=g)).numpy()   # distinct gains: a swap shows
+    pn["gain2"] = (1 + 0.1 * torch.randn(x.shape[1], generator=g)).numpy()
+    return x.float().numpy(), pn, (B, S, H)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_forward_matches_independent_torch_program(seed):
+    x, pn, (B, S, H) = _pin_case(seed)
+    f = decoder.forward(x, pn, B=B, S=S, H=H, seed=3)
+    err = forward_stage_errors(f, x, pn, B, S, H)
+    assert not forward_failures(err), forward_failures(err)
+
+
+@pytest.mark.parametrize("plant", ["Wg<->Wu", "gain1<->gain2", "Wo transposed"])
+def test_forward_pin_rejects_planted_formula_errors(plant):
+    """A forward computed with a planted formula error (two weights or gains swapped, a weight
+    transposed) must fail the pin against the intended parameters."""
+    x, pn, (B, S, H) = _pin_case(0)
+    bad = dict(pn)
+    if plant == "Wg<->Wu":
+        bad["Wg"], bad["Wu"] = pn["Wu"], pn["Wg"]
+    elif plant == "gain1<->gain2":
+        bad["gain1"], bad["gain2"] = pn["gain2"], pn["gain1"]
+    else:
+        bad["Wo"] = np.ascontiguousarray(pn["Wo"].T)
+    f = decoder.forward(x, bad, B=B, S=S, H=H, seed=3)
+    assert forward_failures(forward_stage_errors(f, x, pn, B, S, H)), plant

@@ -128,3 +128,22 @@ def test_sr_monte_carlo_frequency(fmt):
     se = np.sqrt(p * (1 - p) / K) + 1e-12
     z = np.abs(ups / K - p) / se
     assert np.all(z[(p > 0.01) & (p < 0.99)] < 5)
+
+
+def test_planted_sr_threshold_off_by_one_fails_the_pins(monkeypatch):
+    """Round up only when R + F exceeds 2^32 (one too strict), or a threshold F one too large:
+    the boundary pin and the exact-probability pin must fail."""
+    threshold = fp8.sr_threshold
+
+    def strict(a, fmt, R):
+        F, lo, step = threshold(a, fmt)
+        up = (np.asarray(R, dtype=np.uint64) + F) > np.uint64(1 << 32)
+        return np.where(up & (F > 0), lo + step, lo)
+    monkeypatch.setattr(fp8, "sr_mag", strict)
+    with pytest.raises(AssertionError):
+        test_sr_threshold_boundaries()
+    monkeypatch.undo()
+    monkeypatch.setattr(fp8, "sr_threshold", lambda a, fmt: (lambda F, lo, s: (F + np.uint64(1), lo, s))(
+        *threshold(a, fmt)))
+    with pytest.raises(AssertionError):
+        test_sr_probability_is_exact_fraction(fp8.E4M3)

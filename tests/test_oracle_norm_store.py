@@ -16,9 +16,10 @@ import itertools
 from fractions import Fraction as Fr
 
 import numpy as np
+import pytest
 import torch
 
-from oracle import fp8, norm_store, qround
+from oracle import fp8, norm_store, policy, qround
 
 
 def make(T, d, n, seed=0, scale=1.0):
@@ -158,3 +159,18 @@ def test_reuse_equals_new_rounding_over_both_roundings():
         e_r = expect(oc, gain)                        # reads the forward's rounding
         e_n = expect(oc + oc, lambda v: gain(v[len(oc):]))   # reads a new, independent one
         assert e_r == e_n
+
+
+def test_planted_reuse_original_swap_at_the_weight_use_fails_the_closed_forms(monkeypatch):
+    """The weight use reading R where the policy says U and U where it says R (the gain use
+    untouched) must fail the closed forms of Eq. norm-uses."""
+    read = policy.read
+    calls = {"n": 0}
+    swap = {"U": "R", "R": "U", "N": "N"}
+
+    def planted(letter, original, forward_rounding, fresh):
+        calls["n"] += 1                      # per trial: the gain use, then the weight use
+        return read(swap[letter] if calls["n"] % 2 == 0 else letter, original, forward_rounding, fresh)
+    monkeypatch.setattr(policy, "read", planted)
+    with pytest.raises(AssertionError):
+        test_closed_form_biases()

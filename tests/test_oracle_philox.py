@@ -80,3 +80,27 @@ def test_uniformity_and_independence():
     w3 = philox.words(0xB5F0, 1, 258, e).astype(np.float64) / 2**32
     for a, b in ((w[:-1], w[1:]), (w, w2), (w, w3)):
         assert abs(np.corrcoef(a, b)[0, 1]) < 5 / np.sqrt(n)
+
+
+# Planted errors: a generator keyed or countered wrongly must fail the comparison above.
+_words = philox.words
+
+
+def _key_halves_swapped(seed, trial, use, elements):
+    return _words(((seed & 0xFFFFFFFF) << 32) | (seed >> 32), trial, use, elements)
+
+
+def _trial_use_swapped(seed, trial, use, elements):
+    return _words(seed, use, trial, elements)
+
+
+def _element_word_shifted(seed, trial, use, elements):
+    return _words(seed, trial, use, np.asarray(elements, dtype=np.uint64) ^ np.uint64(1))
+
+
+@pytest.mark.parametrize("plant", [_key_halves_swapped, _trial_use_swapped, _element_word_shifted],
+                         ids=lambda f: f.__name__.strip("_"))
+def test_planted_generator_errors_fail_the_pin(aten, monkeypatch, plant):
+    monkeypatch.setattr(philox, "words", plant)
+    with pytest.raises(AssertionError):
+        test_matches_aten_engine(aten)

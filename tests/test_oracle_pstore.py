@@ -196,3 +196,17 @@ def test_attention_policy_zeros_and_draw_counts():
     assert np.any(out["N/N"]["dQ"][2] > 0) and np.any(out["J2/R"]["dK"][2] > 0)
     # the store: codes above the causal diagonal are zero, p_q = s val(codes) reproduces O
     assert np.all(out["codes"][0, 0][np.triu_indices(S, 1)] == 0)
+
+
+@pytest.mark.parametrize("name,lawname,printed", [("A", "sr", "0.4808"), ("A", "sym", "0.5598"),
+                                                  ("B", "sr", "0.4222"), ("B", "sym", "0.4254")])
+def test_new_rounding_over_reuse_ratio_printed_in_app_b3(name, lawname, printed):
+    """App. B.3 prints, to four places, the L1 norm of N/N's average error at the softmax's
+    backward as a fraction of R/R's, in cells A and B under both laws; the oracle's enumerated
+    averages must give the same four digits."""
+    p, V, step = cell(name)
+    law = law_sr(p, step) if lawname == "sr" else law_sym(p)
+    es_n = enumerate_policy("N/N", p, V, law)[0]
+    es_r = enumerate_policy("R/R", p, V, law)[0]
+    ratio = sum(abs(x) for x in es_n) / sum(abs(x) for x in es_r)
+    assert f"{float(ratio):.4f}" == printed, (name, lawname, float(ratio))
