@@ -319,20 +319,29 @@ bs_status bs_attn_pstore_policy(const void* Q, const void* Kt, const void* V, co
  *
  * With scales = (s_P, s_dO, s_dS, s_g) (device fp32, > 0; delayed scales from the caller's
  * amax histories) and Q8(x; s, F) = s * RNE_F(clamp(fl32(x / s), +-FMAX_F)):
+ *   the operands Q, K, V are the forward's FP8 tensors, read as their dequantized values
+ *   (qkv_scales != NULL: E4M3 codes at scales s_Q, s_K, s_V; App. D.2 recomputes the output from
+ *   the dequantized FP8 Q, K and V), or bf16 tensors (qkv_scales NULL);
  *   dO_q = Q8(dO; s_dO, E5M2); P re-formed from Q, K (the forward's realized fp32 probabilities);
  *   P_q = Q8(P; s_P, E4M3); dV = P_q^T dO_q; dP = dO_q V^T; dS = P (dP - D) (zero above the
  *   causal diagonal); dS_q = Q8(dS; s_dS, E5M2); dQ = c dS_q K; dK = c dS_q^T Q; the three
- *   gradients are returned as Q8(.; s_g, E5M2).
+ *   gradients return as the fp32 dequantization fl32(val(C) s_g) of C = RNE_E5M2(clamp(fl32(g /
+ *   s_g))), in BF16 (grad_type BS_BF16, rounded to nearest even: App. D.2 returns them in BF16)
+ *   or in fp32 (BS_F32).
+ *   FP8 operands enter the products as their exact code values with the scales applied in fp32
+ *   after the accumulation (s_Q s_K on the scores, s_V on dP and on P V, s_K on dQ, s_Q on dK), so
+ *   the results differ from fp32-dequantized operands by rounding only.
  * D per row, by source: FROM_P rowsum(dO_q * P V) (equal to rowsum(P dP)); U rowsum(dO_q * O);
  *   R rowsum(dO_q * deq(O_codes)); N rowsum(dO_q * N(O)), N(O) a new stochastic rounding of
  *   fl32(O / O_scale) in E4M3 (trial `trial`, use store_id*256 + 1, element b,h,s,d row-major);
  *   REPAIR FROM_P on rows whose largest probability (exactly fl32(1/l)) is >= threshold, R on
  *   the others.
  *
- *   Q, Kt (the keys), V, dO [B,H,S,dh] bf16, 16-byte aligned; dh == 64; S >= 4 a multiple of 4;
+ *   Q, Kt (the keys), V [B,H,S,dh] bf16, or uint8 E4M3 codes with qkv_scales [3] fp32 (device);
+ *   dO [B,H,S,dh] bf16; all 16-byte aligned; dh == 64; S >= 4 a multiple of 4;
  *   B*H <= 65535. O [B,H,S,dh] fp32 (U, N; else nullable); O_codes [B,H,S,dh] uint8 E4M3
  *   (R, REPAIR) and O_scale [1] fp32 device (R, N, REPAIR): the forward's store of O.
- *   dQ, dK, dV [B,H,S,dh] fp32 out: the returned (cast) gradients, fl32(code value * s_g).
+ *   dQ, dK, dV [B,H,S,dh] out, bf16 or fp32 (grad_type): the returned (cast) gradients.
  *   amax [4] fp32 out, in the order of scales: max P (= max over rows of fl32(1/l)), max |dO|,
  *   max |dS| (pre-cast), max of the pre-cast gradients.
  *   counts [4] uint32 out: rows with fl32(1/l) >= threshold; clamped entries of dO, of dS and of
@@ -340,10 +349,12 @@ bs_status bs_attn_pstore_policy(const void* Q, const void* Kt, const void* V, co
  *   Nullable outputs: P_out, dS_out [B,H,S,S] fp32 (the realized P and pre-cast dS), P_codes,
  *   dS_codes [B,H,S,S] uint8 (4-byte aligned) and grad_pre [3][B,H,S,dh] fp32 (pre-cast dQ,
  *   dK, dV); [B,H,S,S] entries above the causal diagonal's 64 x 64 tiles are not written.
- *   ws: bs_te_attn_workspace_size(B, H, S, dh, causal, source) bytes (0 for shapes the call
- *   rejects); about 2 causal-half S^2 bytes per head plus 7 [B,H,S,dh] bf16/fp32 arrays.
+ *   ws: bs_te_attn_workspace_size(B, H, S, dh, causal, source, fp8_qkv) bytes, fp8_qkv != 0 when
+ *   qkv_scales is set (0 for shapes the call rejects); about 2 causal-half S^2 bytes per head
+ *   plus 7 (10 with FP8 operands) [B,H,S,dh] bf16/fp32 arrays.
  * Returns BS_EINVAL for a null required pointer, a bad source, a misaligned pointer;
- * BS_ESHAPE for dh != 64 or S not a multiple of 4.
+ * BS_EDTYPE for a grad_type other than BS_F32 / BS_BF16; BS_ESHAPE for dh != 64 or S not a
+ * multiple of 4.
  * ---------------------------------------------------------------------------------- */
 typedef enum { BS_D_FROM_P = 0, BS_D_U = 1, BS_D_R = 2, BS_D_N = 3, BS_D_REPAIR = 4 } bs_d_source;
 
@@ -358,13 +369,13 @@ typedef enum { BS_D_FROM_P = 0, BS_D_U = 1, BS_D_R = 2, BS_D_N = 3, BS_D_REPAIR 
 bs_status bs_te_delayed_scales(const float* amax, float* history, int len, int64_t step, float* scales,
                                void* stream);
 
-size_t bs_te_attn_workspace_size(int B, int H, int S, int dh, int causal, bs_d_source source);
-bs_status bs_te_attn_bwd(const void* Q, const void* Kt, const void* V, const void* dO, int B, int H, int S, int dh,
-                         int causal, float softmax_scale, const float* O, const uint8_t* O_codes, const float* O_scale,
-                         bs_d_source source, float threshold, const float* scales, uint64_t seed, uint32_t store_id,
-                         uint32_t trial, float* dQ, float* dK, float* dV, float* amax, uint32_t* counts, float* P_out,
-                         float* dS_out, uint8_t* P_codes, uint8_t* dS_codes, float* grad_pre, void* ws,
-                         size_t ws_bytes, void* stream);
+size_t bs_te_attn_workspace_size(int B, int H, int S, int dh, int causal, bs_d_source source, int fp8_qkv);
+bs_status bs_te_attn_bwd(const void* Q, const void* Kt, const void* V, const float* qkv_scales, const void* dO, int B,
+                         int H, int S, int dh, int causal, float softmax_scale, const float* O, const uint8_t* O_codes,
+                         const float* O_scale, bs_d_source source, float threshold, const float* scales, uint64_t seed,
+                         uint32_t store_id, uint32_t trial, bs_dtype grad_type, void* dQ, void* dK, void* dV,
+                         float* amax, uint32_t* counts, float* P_out, float* dS_out, uint8_t* P_codes,
+                         uint8_t* dS_codes, float* grad_pre, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------
  * bs_linear_bwd_policy -- Linear backward whose incoming gradient is stochastically

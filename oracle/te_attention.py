@@ -5,12 +5,16 @@ Test infrastructure (see ``oracle/__init__``).
 The forks' backward (App. D.2) is a dense emulation of TE's FP8 attention backward, whose
 correction term D is computed from the saved output:
 
+  * the operands Q, K and V are the forward's FP8 tensors: E4M3 codes at their scales, read as
+    their fp32 dequantization fl32(val(C) s) (App. D.2 recomputes the output in fp32 from the
+    dequantized FP8 Q, K and V); bf16 Q, K, V are accepted as well (qkv_scales None);
   * dO is cast to E5M2 at its delayed scale s_dO: dO_q = Q8(dO);
   * P is recomputed; dV = P_q^T dO_q with P_q the E4M3 store of P at the forward's scale s_P;
   * dP = dO_q V^T; D is taken from the assigned output copy, rowsum(dO_q * O_copy), or from P,
     rowsum(P * dP); dS = P * (dP - D);
   * dS is cast to E5M2 at its delayed scale s_dS; dQ = c dS_q K and dK = c dS_q^T Q;
-  * dQ, dK and dV are cast to E5M2 at the gradients' delayed scale s_g before they return.
+  * dQ, dK and dV are cast to E5M2 at the gradients' delayed scale s_g, then return in BF16:
+    bf16(fl32(val(C) s_g)), the fp32 dequantization rounded to nearest even (fp32 on request).
 
 The delayed scales (P's from the forward; dO, dS, the gradients) come from histories of past
 amaxes (TE keeps the largest of 1024, margin 0, App. D.1): they are inputs of the backward,
@@ -75,6 +79,30 @@ def cast64(x, s, fmt):
     return qround.dequant(codes, s, fmt), codes, nsat
 
 
+def bf16(x):
+    """Round fp32 values to nearest even into bfloat16 (returned as fp64 values)."""
+    b = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    lsb = (b >> np.uint64(16)) & np.uint64(1)
+    r = ((b + np.uint64(0x7FFF) + lsb) >> np.uint64(16)) << np.uint64(16)
+    return r.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def returned(codes, s, fmt, grad_dtype="bf16"):
+    """A gradient as it returns after its FP8 cast: the fp32 dequantization fl32(val(C) s), in
+    BF16 (rounded to nearest even; App. D.2) or left in fp32."""
+    v = (fp8.decode(codes, fmt).astype(np.float32) * np.float32(s)).astype(np.float32)
+    return bf16(v) if grad_dtype == "bf16" else v.astype(np.float64)
+
+
+def operands(Q, Kt, V, qkv_scales):
+    """The operands of the backward: bf16 inputs as they are, or E4M3 codes read as their fp32
+    dequantization fl32(val(C) s) (the emulation's dense fp32 arithmetic, App. D.2)."""
+    if qkv_scales is None:
+        return tuple(np.asarray(a, dtype=np.float32).astype(np.float64) for a in (Q, Kt, V))
+    return tuple((fp8.decode(np.asarray(a, dtype=np.uint8), fp8.E4M3).astype(np.float32) * np.float32(sc))
+                 .astype(np.float32).astype(np.float64) for a, sc in zip((Q, Kt, V), qkv_scales))
+
+
 def d_term(source, P, dP, dOq, O, Or, On, thr):
     """The correction term D per row for a D source."""
     fromP = (P * dP).sum(axis=-1)
@@ -93,16 +121,18 @@ def d_term(source, P, dP, dOq, O, Or, On, thr):
 
 
 def check(Q, Kt, V, dO, *, P, dS=None, O, O_codes, O_scale, causal=True, c=None, scales, source="R", thr=0.9,
-          seed=0, store_id=0, trial=1, heads=None):
+          seed=0, store_id=0, trial=1, heads=None, qkv_scales=None, grad_dtype="bf16"):
     """The emulated backward per head.
 
-    Q, Kt, V, dO [B, H, S, dh]; P: the realized fp32 probabilities [B, H, S, S]; dS: the realized
-    fp32 pre-cast dS (None: cast the oracle's own); O: the original fp32 output; O_codes,
-    O_scale: its E4M3 store (the R copy); scales: (s_P, s_dO, s_dS, s_g) as fp32. Besides the
-    values, the clamp counts of dO, dS and the three gradients and the rows at or over the
-    threshold are reported.
+    Q, Kt, V [B, H, S, dh]: bf16 values, or E4M3 codes at qkv_scales = (s_Q, s_K, s_V); dO
+    [B, H, S, dh]; P: the realized fp32 probabilities [B, H, S, S]; dS: the realized fp32 pre-cast
+    dS (None: cast the oracle's own); O: the original fp32 output; O_codes, O_scale: its E4M3 store
+    (the R copy); scales: (s_P, s_dO, s_dS, s_g) as fp32; grad_dtype: "bf16" (App. D.2) or "f32",
+    the format the cast gradients return in. Besides the values, the clamp counts of dO, dS and
+    the three gradients and the rows at or over the threshold are reported.
     """
-    Q, Kt, V, dO = (np.asarray(a, dtype=np.float32).astype(np.float64) for a in (Q, Kt, V, dO))
+    Q, Kt, V = operands(Q, Kt, V, qkv_scales)
+    dO = np.asarray(dO, dtype=np.float32).astype(np.float64)
     B, H, S, dh = Q.shape
     c = 1.0 / np.sqrt(dh) if c is None else c
     sP, sdO, sdS, sg = (np.float32(x) for x in scales)
@@ -135,8 +165,8 @@ def check(Q, Kt, V, dO, *, P, dS=None, O, O_codes, O_scale, causal=True, c=None,
                         ("dS_codes", dscodes)):
             out[name].append(v)
         for name, v in (("dQ", dQp), ("dK", dKp), ("dV", dVp)):
-            val, _, nsat = cast64(v, sg, fp8.E5M2)
-            out[name].append(val)
+            _, codes, nsat = cast64(v, sg, fp8.E5M2)
+            out[name].append(returned(codes, sg, fp8.E5M2, grad_dtype))
             out["sat_grad"] += nsat
         out["sat_rows"].append(int((p.max(axis=-1) >= thr).sum()))
     for name in ("dS", "D", "dQ_pre", "dK_pre", "dV_pre", "dQ", "dK", "dV", "dS_codes"):

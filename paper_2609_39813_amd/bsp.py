@@ -76,10 +76,10 @@ _attn2 = _sig("bs_attn_level2_policy", _int,
               [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _vp, _int, _int, _f32, ctypes.POINTER(_int), _int,
                _int, _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, _vp, _vp, _vp, _vp, _sz, _vp])
 D_SOURCE = {"P": 0, "U": 1, "R": 2, "N": 3, "repair": 4}
-_te_ws = _sig("bs_te_attn_workspace_size", _sz, [_int] * 6)
+_te_ws = _sig("bs_te_attn_workspace_size", _sz, [_int] * 7)
 _te = _sig("bs_te_attn_bwd", _int,
-           [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _vp, _vp, _vp, _int, _f32, _vp, _u64, _u32, _u32,
-            _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp])
+           [_vp, _vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _f32, _vp, _vp, _vp, _int, _f32, _vp, _u64, _u32,
+            _u32, _int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp])
 _te_sc = _sig("bs_te_delayed_scales", _int, [_vp, _vp, _int, _i64, _vp, _vp])
 _lsm_ws = _sig("bs_logsoftmax_check_workspace_size", _sz, [_i64, _int, _int])
 _lsm = _sig("bs_logsoftmax_reuse_check", _int,
@@ -453,36 +453,44 @@ def attn_pstore_policy(Q, Kt, V, dO, *, causal=True, scale=None, fmt="e4m3", fwd
     return out
 
 
-def te_attn_workspace(B, H, S, dh, causal, source, device):
-    n = _te_ws(B, H, S, dh, int(causal), D_SOURCE[source])
+def te_attn_workspace(B, H, S, dh, causal, source, device, fp8_qkv=False):
+    n = _te_ws(B, H, S, dh, int(causal), D_SOURCE[source], int(fp8_qkv))
     if n == 0:
         raise BspError(2, "bs_te_attn_workspace_size")
     return _workspace(n, device)
 
 
-def te_attn_bwd(Q, Kt, V, dO, scales, *, O=None, O_codes=None, O_scale=None, source="R", threshold=0.9, causal=True,
-                scale=None, seed=0, store_id=0, trial=1, want_p=False, want_ds=False, want_codes=False, want_pre=False,
-                ws=None):
+def te_attn_bwd(Q, Kt, V, dO, scales, *, qkv_scales=None, O=None, O_codes=None, O_scale=None, source="R",
+                threshold=0.9, causal=True, scale=None, seed=0, store_id=0, trial=1, grad_dtype="bf16", want_p=False,
+                want_ds=False, want_codes=False, want_pre=False, ws=None):
     """The emulated FP8 attention backward with delayed scales (bs_te_attn_bwd). scales: device
-    fp32 [4] = (s_P, s_dO, s_dS, s_g)."""
-    _dev_check(Q, Kt, V, dO, scales, O, O_codes, O_scale)
+    fp32 [4] = (s_P, s_dO, s_dS, s_g). qkv_scales: None (Q, Kt, V bf16) or device fp32 [3] with
+    Q, Kt, V the forward's E4M3 codes (uint8). grad_dtype: "bf16" or "f32" returned gradients."""
+    _dev_check(Q, Kt, V, dO, scales, O, O_codes, O_scale, qkv_scales)
+    want = torch.uint8 if qkv_scales is not None else torch.bfloat16
+    if any(t.dtype != want for t in (Q, Kt, V)):
+        raise TypeError(f"Q, K and V must be {want} {'(E4M3 codes)' if qkv_scales is not None else ''}")
+    if qkv_scales is not None and (qkv_scales.dtype != torch.float32 or qkv_scales.numel() != 3):
+        raise TypeError("qkv_scales must be a float32 tensor of 3 scales")
+    gdt = {"bf16": torch.bfloat16, "f32": torch.float32}[grad_dtype]
     B, H, S, dh = Q.shape
     dev = Q.device
     c = 1.0 / dh ** 0.5 if scale is None else scale
     shp = (B, H, S, dh)
     sq = lambda dt, on: torch.zeros(B, H, S, S, dtype=dt, device=dev) if on else None
-    out = {"dQ": torch.empty(shp, dtype=torch.float32, device=dev),
-           "dK": torch.empty(shp, dtype=torch.float32, device=dev),
-           "dV": torch.empty(shp, dtype=torch.float32, device=dev),
+    out = {"dQ": torch.empty(shp, dtype=gdt, device=dev),
+           "dK": torch.empty(shp, dtype=gdt, device=dev),
+           "dV": torch.empty(shp, dtype=gdt, device=dev),
            "amax": torch.empty(4, dtype=torch.float32, device=dev),
            "counts": torch.empty(4, dtype=torch.int32, device=dev),
            "P": sq(torch.float32, want_p), "dS": sq(torch.float32, want_ds),
            "P_codes": sq(torch.uint8, want_codes), "dS_codes": sq(torch.uint8, want_codes),
            "pre": torch.empty((3,) + shp, dtype=torch.float32, device=dev) if want_pre else None}
     if ws is None:
-        ws = te_attn_workspace(B, H, S, dh, causal, source, dev)
-    _check(_te(_p(Q), _p(Kt), _p(V), _p(dO), B, H, S, dh, int(causal), c, _p(O), _p(O_codes), _p(O_scale),
-               D_SOURCE[source], threshold, _p(scales), seed, store_id, trial, _p(out["dQ"]), _p(out["dK"]),
+        ws = te_attn_workspace(B, H, S, dh, causal, source, dev, qkv_scales is not None)
+    _check(_te(_p(Q), _p(Kt), _p(V), _p(qkv_scales), _p(dO), B, H, S, dh, int(causal), c, _p(O), _p(O_codes),
+               _p(O_scale), D_SOURCE[source], threshold, _p(scales), seed, store_id, trial,
+               BF16 if grad_dtype == "bf16" else F32, _p(out["dQ"]), _p(out["dK"]),
                _p(out["dV"]), _p(out["amax"]), _p(out["counts"]), _p(out["P"]), _p(out["dS"]), _p(out["P_codes"]),
                _p(out["dS_codes"]), _p(out["pre"]), _p(ws), ws.numel(), _stream()), "bs_te_attn_bwd")
     return out

@@ -15,6 +15,7 @@ struct AttnArgs {
   float* O_out;  // nullable [B*H][S][64] fp32
   const u16* Vt; // V^T [B*H][64][Sp] (zero past S), from launch_attn_transpose
   int Sp;
+  const float* scale_mul;  // nullable device [1]: the scores' scale is scale * scale_mul[0]
 };
 
 struct AttnDArgs {

@@ -144,7 +144,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
   for (int s = 0; s < 2; ++s)
     fq[s] = __builtin_bit_cast(bf16x8, qok ? *(const uint4*)(a.Q + hb + (int64_t)q * AT + 32 * s + 8 * g)
                                            : make_uint4(0, 0, 0, 0));
-  const float c2 = a.scale * kLog2e;
+  const float c2 = scores_scale(a.scale, a.scale_mul) * kLog2e;
   float m2 = -INFINITY, l = 0.0f;  // running max of c log2(e) S and sum, for query q (this lane's column)
   floatx4 acc[4];
 #pragma unroll

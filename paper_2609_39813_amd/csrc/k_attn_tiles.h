@@ -10,6 +10,10 @@
 
 namespace bsp {
 
+// the scores' scale c of an argument block with an optional device multiplier (FP8 operands
+// whose scales are applied after the products); the same fp32 product wherever P is formed
+__device__ __forceinline__ float scores_scale(float c, const float* mul) { return mul ? c * mul[0] : c; }
+
 constexpr int AT = 64;  // block rows / keys, and dh
 
 __device__ __forceinline__ int sw(int row, int col) { return row * AT + ((((col >> 3) ^ (row & 7)) << 3) | (col & 7)); }

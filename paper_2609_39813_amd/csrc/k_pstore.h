@@ -35,6 +35,7 @@ struct PstoreArgs {
   const u16 *Qt, *Kt, *Vt, *dOt;    // transposed copies [BH][64][Sp] (zero past S)
   int S, Sp, causal, BH;
   float scale;                      // softmax scale c
+  const float* scale_mul;           // null (the scores' scale is c)
   const float *m, *l;               // row max of c log2(e) S and row sum, [BH][S]
   F8 f;
   int fmt, fwd_mode;

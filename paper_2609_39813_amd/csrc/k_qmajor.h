@@ -1,7 +1,7 @@
 // The query-major scaffold of the attention passes that re-form P tile by tile (dh = 64): the
 // lane of a 64-query block that owns one query and 16 keys of each key block, P and dP of those
 // keys by MFMA, and the element / tile indexing. The argument block A provides Q, dO, m, l (the
-// forward's row max of c log2(e) S and row sum), S, Sp, causal and scale.
+// forward's row max of c log2(e) S and row sum), S, Sp, causal, scale and scale_mul.
 #pragma once
 #include "k_attn_tiles.h"
 
@@ -70,7 +70,7 @@ __device__ __forceinline__ void probs(const A& a, const QMajor& z, const u16* tK
   for (int s = 0; s < 2; ++s)
 #pragma unroll
     for (int t = 0; t < 4; ++t) sv[t] = mfma(*(const bf16x8*)(tK + sw(16 * t + z.c16, 32 * s + 8 * z.g)), z.fq[s], sv[t]);
-  const float c2 = a.scale * kLog2e;
+  const float c2 = scores_scale(a.scale, a.scale_mul) * kLog2e;
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll

@@ -6,9 +6,14 @@
 // amaxes of dO, of the pre-cast dS and of the pre-cast gradients are reported for the caller's
 // histories.
 //
+// Q, K and V are bf16, or the forward's E4M3 stores at scales s_Q, s_K, s_V (App. D.2: the
+// forward recomputes its output from the dequantized FP8 Q, K and V); the returned gradients are
+// BF16 (App. D.2) or fp32 values of code times s_g.
+//
 // Every product has exact bf16 operands (FP8 values and bf16 inputs), one MFMA term each, with
-// the scales applied in fp32 after the accumulation. The query-major pass writes the dS and P
-// codes tile by tile ([key][query], one byte each) for the key-major pass.
+// the scales applied in fp32 after the accumulation (s_Q s_K on the scores, s_V on dP and P V,
+// s_K on dQ, s_Q on dK). The query-major pass writes the dS and P codes tile by tile ([key][query],
+// one byte each) for the key-major pass.
 #include "k_attn.h"
 #include "k_qmajor.h"
 
@@ -29,6 +34,9 @@ struct TeArgs {
   const u16 *Qt, *Kt, *dOt;    // transposed copies [BH][64][Sp]
   int S, Sp, causal, BH;
   float scale;                 // softmax scale c
+  const float* scale_mul;      // nullable device [1]: s_Q s_K (FP8 operands)
+  const float* qkv;            // nullable device [3]: s_Q, s_K, s_V (FP8 operands)
+  int grad_bf16;               // returned gradients: bf16 (1) or fp32 (0)
   const float *m, *l;
   const float* sc;             // device [4]: s_P, s_dO, s_dS, s_g
   const float* D;              // [rows] the correction term
@@ -36,7 +44,7 @@ struct TeArgs {
   float *P_out, *dS_out;       // nullable [BH][S][S]: the realized P and pre-cast dS
   uint8_t *P_codes, *dS_codes; // nullable [BH][S][S]
   float* pre;                  // nullable [3][BH][S][64]: pre-cast dQ, dK, dV
-  float *dQ, *dK, *dV;
+  void *dQ, *dK, *dV;          // returned gradients, bf16 or fp32 (grad_bf16)
   uint32_t *part_dq, *part_dkv; // per-block partials (amaxes as fp32 bits, clamp counts)
 };
 
@@ -102,6 +110,41 @@ __device__ __forceinline__ uint32_t quad_transpose(uint32_t w, int j) {
 }
 
 __device__ __forceinline__ int block_linear() { return (int)(blockIdx.y * gridDim.x + blockIdx.x); }
+
+// a returned gradient: the fp32 dequantization fl32(val(C) s_g) of its E5M2 code, in BF16 (rounded
+// to nearest even) or left in fp32
+__device__ __forceinline__ void put_grad(void* out, int64_t e, float v, int as_bf16) {
+  if (as_bf16)
+    ((u16*)out)[e] = bf16_bits(v);
+  else
+    ((float*)out)[e] = v;
+}
+
+// E4M3 codes of Q, K and V -> their code values as bf16 (exact), 16 per thread and step; block 0
+// also writes s_Q s_K (the scores' scale multiplier)
+__global__ __launch_bounds__(256) void te_qkv_kernel(const uint8_t* __restrict__ Qc, const uint8_t* __restrict__ Kc,
+                                                     const uint8_t* __restrict__ Vc, int64_t n, const float* qkv,
+                                                     u16* __restrict__ Qv, u16* __restrict__ Kv, u16* __restrict__ Vv,
+                                                     float* qk) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) qk[0] = qkv[0] * qkv[1];
+  const uint8_t* src[3] = {Qc, Kc, Vc};
+  u16* dst[3] = {Qv, Kv, Vv};
+  for (int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 16; i < n; i += (int64_t)gridDim.x * 256 * 16) {
+#pragma unroll
+    for (int t = 0; t < 3; ++t) {
+      const uint4 c = *(const uint4*)(src[t] + i);
+      const uint32_t cw[4] = {c.x, c.y, c.z, c.w};
+      uint32_t o[8];
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        o[2 * h] = (__float_as_uint(f8_val<BS_E4M3>(cw[h], 0)) >> 16) | (__float_as_uint(f8_val<BS_E4M3>(cw[h], 1)) & 0xFFFF0000u);
+        o[2 * h + 1] = (__float_as_uint(f8_val<BS_E4M3>(cw[h], 2)) >> 16) | (__float_as_uint(f8_val<BS_E4M3>(cw[h], 3)) & 0xFFFF0000u);
+      }
+      *(uint4*)(dst[t] + i) = make_uint4(o[0], o[1], o[2], o[3]);
+      *(uint4*)(dst[t] + i + 8) = make_uint4(o[4], o[5], o[6], o[7]);
+    }
+  }
+}
 
 // Per-block partials of every kernel: [n][width] words each
 struct TeParts {
@@ -193,7 +236,8 @@ __global__ __launch_bounds__(TE_BLOCK) void te_d_kernel(const u16* __restrict__ 
                                                    const float* __restrict__ O, const uint8_t* __restrict__ Oc,
                                                    const float* Os, const float* __restrict__ l, int64_t rows,
                                                    int source, float thr, uint64_t seed, uint32_t trial, uint32_t use,
-                                                   const float* sc, float* __restrict__ D, uint32_t* part) {
+                                                   const float* sc, const float* qkv, float* __restrict__ D,
+                                                   uint32_t* part) {
   const int64_t row = (int64_t)blockIdx.x * 64 + (threadIdx.x >> 2);
   const int sub = threadIdx.x & 3;
   const bool ok = row < rows;
@@ -242,7 +286,9 @@ __global__ __launch_bounds__(TE_BLOCK) void te_d_kernel(const u16* __restrict__ 
   }
   acc += __shfl_xor(acc, 1, 64);
   acc += __shfl_xor(acc, 2, 64);
-  if (ok && sub == 0) D[row] = (float)((double)sc[1] * acc);
+  // the forward's P V was formed from V's code values: s_V applies here
+  const double sv = (src == BS_D_FROM_P && qkv) ? (double)qkv[2] : 1.0;
+  if (ok && sub == 0) D[row] = (float)((double)sc[1] * sv * acc);
   const uint32_t v[2] = {(ok && sub == 0 && sat) ? 1u : 0u, __float_as_uint(pmax)};
   const bool mx[2] = {false, true};
   block_total(v, mx, part + 2 * block_linear());
@@ -253,7 +299,8 @@ __global__ __launch_bounds__(TE_BLOCK) void te_d_kernel(const u16* __restrict__ 
 __global__ __launch_bounds__(TE_BLOCK) __attribute__((amdgpu_waves_per_eu(3, 8))) void te_dq_kernel(TeArgs a) {
   __shared__ __attribute__((aligned(16))) u16 sm[2][3][AT * AT];  // K, V, K^T
   const QMajor z = qmajor_setup(a, true);
-  const float sdO = a.sc[1], sdS = a.sc[2];
+  const float sdS = a.sc[2];
+  const float sdO = a.qkv ? a.sc[1] * a.qkv[2] : a.sc[1];  // dP = s_dO (s_V) val(dO_q) V
   const double rP = 1.0 / (double)a.sc[0], rdS = 1.0 / (double)sdS, rg = 1.0 / (double)a.sc[3];
   const float Dq = z.qok ? a.D[z.rb + z.q] : 0.0f;
   const int nqb = (a.S + AT - 1) / AT;
@@ -330,8 +377,8 @@ __global__ __launch_bounds__(TE_BLOCK) __attribute__((amdgpu_waves_per_eu(3, 8))
     if (kb + 1 < nkb) put(st ^ 1);
     __syncthreads();
   }
-  // dQ = c s_dS acc, cast at the gradients' scale
-  const float cs = a.scale * sdS;
+  // dQ = c (s_K) s_dS acc, cast at the gradients' scale
+  const float cs = (a.qkv ? a.scale * a.qkv[1] : a.scale) * sdS;
   float amg = 0.0f;
   uint32_t nsg = 0;
 #pragma unroll
@@ -351,7 +398,7 @@ __global__ __launch_bounds__(TE_BLOCK) __attribute__((amdgpu_waves_per_eu(3, 8))
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
       const int64_t e = z.hb + (int64_t)qr * AT + 16 * n + z.c16;
-      a.dQ[e] = f8_val<BS_E5M2>(w, n) * a.sc[3];
+      put_grad(a.dQ, e, f8_val<BS_E5M2>(w, n) * a.sc[3], a.grad_bf16);
       if (a.pre) a.pre[e] = pre[n];
     }
   }
@@ -432,7 +479,7 @@ __global__ __launch_bounds__(TE_BLOCK) void te_dkv_kernel(TeArgs a) {
     if (qb + 1 < nqb) put(st ^ 1);
     __syncthreads();
   }
-  const float ck = a.scale * sdS, cv = sP * sdO;
+  const float ck = (a.qkv ? a.scale * a.qkv[0] : a.scale) * sdS, cv = sP * sdO;  // dK: c (s_Q) s_dS
   const double rg = 1.0 / (double)sg;
   const int64_t numel = (int64_t)a.BH * a.S * AT;
   float amg = 0.0f;
@@ -456,8 +503,8 @@ __global__ __launch_bounds__(TE_BLOCK) void te_dkv_kernel(TeArgs a) {
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
       const int64_t e = hb + (int64_t)kr * AT + 16 * n + c16;
-      a.dK[e] = f8_val<BS_E5M2>(wk, n) * sg;
-      a.dV[e] = f8_val<BS_E5M2>(wv, n) * sg;
+      put_grad(a.dK, e, f8_val<BS_E5M2>(wk, n) * sg, a.grad_bf16);
+      put_grad(a.dV, e, f8_val<BS_E5M2>(wv, n) * sg, a.grad_bf16);
       if (a.pre) {
         a.pre[numel + e] = prk[n];
         a.pre[2 * numel + e] = prv[n];
@@ -499,6 +546,8 @@ __global__ __launch_bounds__(TE_BLOCK) void te_scales_kernel(const float* amax, 
 
 struct TeWs {
   u16 *dOq, *Qt, *Kt, *Vt, *dOt;
+  u16 *Qv, *Kv, *Vv;  // FP8 operands: the code values as bf16
+  float* qk;          // FP8 operands: s_Q s_K
   float *m, *l, *D, *OP;
   uint8_t *dsq, *pq;
   TeParts parts;
@@ -508,7 +557,7 @@ int prep_blocks(int64_t numel) {
   return (int)std::min<int64_t>((numel / 8 + TE_BLOCK - 1) / TE_BLOCK, TE_PREP_BLOCKS);
 }
 
-TeWs carve_te(Carver& c, int64_t bh, int S, int causal, bool need_op) {
+TeWs carve_te(Carver& c, int64_t bh, int S, int causal, bool need_op, bool fp8_qkv) {
   TeWs w{};
   const int64_t Sp = round_up(S, AT), rows = bh * S;
   const int nqb = (int)(Sp / AT);
@@ -526,6 +575,10 @@ TeWs carve_te(Carver& c, int64_t bh, int S, int causal, bool need_op) {
   const int64_t nt = bh * causal_tiles(nqb, causal) * AT * AT;
   w.dsq = c.take<uint8_t>(nt);
   w.pq = c.take<uint8_t>(nt);
+  if (fp8_qkv) {
+    for (u16** p : {&w.Qv, &w.Kv, &w.Vv}) *p = c.take<u16>(rows * AT);
+    w.qk = c.take<float>(1);
+  }
   return w;
 }
 
@@ -537,6 +590,7 @@ struct TeIO {
   const void *Q, *K, *V, *dO;
   int B, H, S, dh, causal;
   float scale;
+  const float* qkv_scales;  // nullable: Q, K, V are E4M3 codes at these scales
   const float* O;
   const uint8_t* O_codes;
   const float* O_scale;
@@ -545,17 +599,19 @@ struct TeIO {
   const float* scales;
   uint64_t seed;
   uint32_t store_id, trial;
-  float *dQ, *dK, *dV, *amax;
+  int grad_type;
+  void *dQ, *dK, *dV;
+  float* amax;
   uint32_t* counts;
   float *P_out, *dS_out;
   uint8_t *P_codes, *dS_codes;
   float* grad_pre;
 };
 
-size_t te_ws_size(int B, int H, int S, int dh, int causal, int source) {
+size_t te_ws_size(int B, int H, int S, int dh, int causal, int source, int fp8_qkv) {
   if (B < 1 || H < 1 || S < 1 || dh != AT || source < BS_D_FROM_P || source > BS_D_REPAIR) return 0;
   Carver c;
-  carve_te(c, (int64_t)B * H, S, causal ? 1 : 0, needs_op(source));
+  carve_te(c, (int64_t)B * H, S, causal ? 1 : 0, needs_op(source), fp8_qkv != 0);
   return c.used();
 }
 
@@ -564,6 +620,7 @@ bs_status te_run(const TeIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
     return BS_EINVAL;
   if (io.B < 1 || io.H < 1 || io.S < 1 || !(io.scale > 0.0f)) return BS_EINVAL;
   if (io.source < BS_D_FROM_P || io.source > BS_D_REPAIR) return BS_EINVAL;
+  if (io.grad_type != BS_F32 && io.grad_type != BS_BF16) return BS_EDTYPE;
   const bool need_codes = io.source == BS_D_R || io.source == BS_D_REPAIR;
   if ((need_codes && !io.O_codes) || ((need_codes || io.source == BS_D_N) && !io.O_scale)) return BS_EINVAL;
   if ((io.source == BS_D_U || io.source == BS_D_N) && !io.O) return BS_EINVAL;
@@ -571,15 +628,27 @@ bs_status te_run(const TeIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
   if ((int64_t)io.B * io.H > 65535 || (io.S + AT - 1) / AT > 65535) return BS_ESHAPE;
   for (const void* p : {io.Q, io.K, io.V, io.dO, (const void*)io.O, (const void*)io.P_out, (const void*)io.dS_out})
     if ((uintptr_t)p & 15) return BS_EINVAL;  // 16-byte vector loads and stores
+  if ((uintptr_t)io.qkv_scales & 3) return BS_EINVAL;
   for (const void* p : {(const void*)io.O_codes, (const void*)io.P_codes, (const void*)io.dS_codes})
     if ((uintptr_t)p & 3) return BS_EINVAL;
   const int64_t bh = (int64_t)io.B * io.H, Sp = round_up(io.S, AT), rows = bh * io.S, numel = rows * AT;
   const int causal = io.causal ? 1 : 0;
+  const bool fq = io.qkv_scales != nullptr;
   Carver probe;
-  carve_te(probe, bh, io.S, causal, needs_op(io.source));
+  carve_te(probe, bh, io.S, causal, needs_op(io.source), fq);
   if (!ws || ((uintptr_t)ws & 255) || ws_bytes < probe.used()) return BS_EWORKSPACE;
   Carver c(ws, ws_bytes);
-  const TeWs w = carve_te(c, bh, io.S, causal, needs_op(io.source));
+  const TeWs w = carve_te(c, bh, io.S, causal, needs_op(io.source), fq);
+  // the operands: bf16 inputs, or the FP8 stores' code values (exact in bf16)
+  const u16* Qo = fq ? w.Qv : (const u16*)io.Q;
+  const u16* Ko = fq ? w.Kv : (const u16*)io.K;
+  const u16* Vo = fq ? w.Vv : (const u16*)io.V;
+  if (fq) {
+    te_qkv_kernel<<<prep_blocks(numel / 2), 256, 0, st>>>((const uint8_t*)io.Q, (const uint8_t*)io.K,
+                                                         (const uint8_t*)io.V, numel, io.qkv_scales, w.Qv, w.Kv,
+                                                         w.Vv, w.qk);
+    BS_CHECK_LAUNCH();
+  }
 
   {
     ProfScope prof("te_prep", st);
@@ -588,24 +657,23 @@ bs_status te_run(const TeIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
     BS_CHECK_LAUNCH();
   }
   {
-    const u16* src[4] = {(const u16*)io.V, (const u16*)io.Q, (const u16*)io.K, w.dOq};
+    const u16* src[4] = {Vo, Qo, Ko, w.dOq};
     u16* dst[4] = {w.Vt, w.Qt, w.Kt, w.dOt};
     BS_TRY(launch_attn_transpose(src, dst, 4, (int)bh, io.S, (int)Sp, st));
   }
-  AttnArgs fa{(const u16*)io.Q, (const u16*)io.K, (const u16*)io.V, io.S, causal, io.scale, w.m, w.l, w.OP,
-              w.Vt, (int)Sp};
+  AttnArgs fa{Qo, Ko, Vo, io.S, causal, io.scale, w.m, w.l, w.OP, w.Vt, (int)Sp, fq ? w.qk : nullptr};
   BS_TRY(launch_attn_fwd(fa, io.B, io.H, st));
   {
     ProfScope prof("te_d", st);
     te_d_kernel<<<(unsigned)((rows + 63) / 64), TE_BLOCK, 0, st>>>(
         w.dOq, w.OP, io.O, io.O_codes, io.O_scale, w.l, rows, io.source, io.thr, io.seed, io.trial,
-        io.store_id * 256u + 1u, io.scales, w.D, w.parts.d);
+        io.store_id * 256u + 1u, io.scales, io.qkv_scales, w.D, w.parts.d);
     BS_CHECK_LAUNCH();
   }
   TeArgs a{};
-  a.Q = (const u16*)io.Q;
-  a.K = (const u16*)io.K;
-  a.V = (const u16*)io.V;
+  a.Q = Qo;
+  a.K = Ko;
+  a.V = Vo;
   a.dO = w.dOq;
   a.Qt = w.Qt;
   a.Kt = w.Kt;
@@ -615,6 +683,9 @@ bs_status te_run(const TeIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
   a.causal = causal;
   a.BH = (int)bh;
   a.scale = io.scale;
+  a.scale_mul = fq ? w.qk : nullptr;
+  a.qkv = io.qkv_scales;
+  a.grad_bf16 = io.grad_type == BS_BF16 ? 1 : 0;
   a.m = w.m;
   a.l = w.l;
   a.sc = io.scales;
@@ -653,8 +724,8 @@ using namespace bsp;
 
 extern "C" {
 
-size_t bs_te_attn_workspace_size(int B, int H, int S, int dh, int causal, bs_d_source source) {
-  return te_ws_size(B, H, S, dh, causal, (int)source);
+size_t bs_te_attn_workspace_size(int B, int H, int S, int dh, int causal, bs_d_source source, int fp8_qkv) {
+  return te_ws_size(B, H, S, dh, causal, (int)source, fp8_qkv);
 }
 
 bs_status bs_te_delayed_scales(const float* amax, float* history, int len, int64_t step, float* scales,
@@ -665,15 +736,16 @@ bs_status bs_te_delayed_scales(const float* amax, float* history, int len, int64
   return BS_OK;
 }
 
-bs_status bs_te_attn_bwd(const void* Q, const void* Kt, const void* V, const void* dO, int B, int H, int S, int dh,
-                         int causal, float softmax_scale, const float* O, const uint8_t* O_codes, const float* O_scale,
-                         bs_d_source source, float threshold, const float* scales, uint64_t seed, uint32_t store_id,
-                         uint32_t trial, float* dQ, float* dK, float* dV, float* amax, uint32_t* counts, float* P_out,
-                         float* dS_out, uint8_t* P_codes, uint8_t* dS_codes, float* grad_pre, void* ws,
-                         size_t ws_bytes, void* stream) {
-  TeIO io{Q,      Kt,      V,       dO,          B,         H,      S,    dh,       causal, softmax_scale,
-          O,      O_codes, O_scale, (int)source, threshold, scales, seed, store_id, trial,  dQ,
-          dK,     dV,      amax,    counts,      P_out,     dS_out, P_codes, dS_codes, grad_pre};
+bs_status bs_te_attn_bwd(const void* Q, const void* Kt, const void* V, const float* qkv_scales, const void* dO, int B,
+                         int H, int S, int dh, int causal, float softmax_scale, const float* O, const uint8_t* O_codes,
+                         const float* O_scale, bs_d_source source, float threshold, const float* scales, uint64_t seed,
+                         uint32_t store_id, uint32_t trial, bs_dtype grad_type, void* dQ, void* dK, void* dV,
+                         float* amax, uint32_t* counts, float* P_out, float* dS_out, uint8_t* P_codes,
+                         uint8_t* dS_codes, float* grad_pre, void* ws, size_t ws_bytes, void* stream) {
+  TeIO io{Q,       Kt,      V,         dO,     B,        H,     S,          dh,   causal, softmax_scale,
+          qkv_scales, O,    O_codes,   O_scale, (int)source, threshold, scales, seed, store_id, trial,
+          (int)grad_type, dQ, dK,      dV,     amax,     counts, P_out,     dS_out, P_codes, dS_codes,
+          grad_pre};
   return te_run(io, ws, ws_bytes, (hipStream_t)stream);
 }
 

@@ -2,12 +2,13 @@
 
 The forward's fp32 output O and its E4M3 store come from the oracle; the delayed scales from
 the oracle's own fp64 pass (the amaxes a previous step would have seen), scaled to provoke
-clamps or flushes. The library's realized P and pre-cast dS are handed to the oracle, which
-casts them: the P and dS codes agree bit for bit, P matches the fp64 softmax, dS and the
-pre-cast gradients match the oracle's fp64 values within 1e-5 (normwise relative). The returned
-gradients (fp32 values of code times s_g) are the E5M2 casts of the library's own pre-cast
-values bit for bit; against the oracle's casts of its fp64 values they may differ only where
-the value sits within 1e-4 of a rounding midpoint. amaxes and counts match.
+clamps or flushes. Q, K and V are bf16, or the forward's E4M3 stores at their scales (App. D.2).
+The library's realized P and pre-cast dS are handed to the oracle, which casts them: the P and
+dS codes agree bit for bit, P matches the fp64 softmax, dS and the pre-cast gradients match the
+oracle's fp64 values within 1e-5. The returned gradients (BF16, or fp32, values of code times
+s_g) are those of the E5M2 casts of the library's own pre-cast values bit for bit; against the
+oracle's casts of its fp64 values the codes may differ only where a rounding boundary lies
+between the two pre-cast values (rare). amaxes and counts match.
 """
 import numpy as np
 import pytest
@@ -25,6 +26,20 @@ F32 = np.float32
 def inputs(B, H, S, seed, sharp=1):
     Q, K, V, dO = synth.attention_inputs(B, H, S, 64, torch.float32, config=500 + seed)
     return [t.to(torch.bfloat16) for t in (Q * sharp, K, V, dO)]
+
+
+def fp8_operands(Q, K, V, factors=(1.0, 1.0, 1.0)):
+    """The forward's E4M3 stores of Q, K, V at scales amax / 448 times a factor (a stale delayed
+    scale clamps): (codes, scales, fp32 dequantized values)."""
+    codes, scales, deq = [], [], []
+    for t, f in zip((Q, K, V), factors):
+        x = t.float().numpy()
+        s = F32(oq.scale_of(np.abs(x).max(), fp8.E4M3) * F32(f))
+        q = oq.qround(x, fp8.E4M3, oq.RNE, scale=s)
+        codes.append(q.codes)
+        scales.append(s)
+        deq.append((fp8.decode(q.codes, fp8.E4M3).astype(F32) * s).astype(F32))
+    return codes, scales, deq
 
 
 def forward_store(Q, K, V, causal, c, seed, store_id):
@@ -45,25 +60,36 @@ def delayed_scales(Q, K, V, dO, P32, O32, q, causal, c, factors):
 
 
 def run_case(lib, B, H, S, *, causal=True, source="R", factors=(1, 1, 1, 1), sharp=1, thr=0.9, seed=1, store_id=4,
-             trial=3):
+             trial=3, fp8_qkv=None, grad_dtype="bf16"):
+    """fp8_qkv: None (bf16 Q, K, V) or the factors of the E4M3 stores' scales of Q, K, V."""
     c = 0.125
     Q, K, V, dO = inputs(B, H, S, seed, sharp)
-    O32, P32, q = forward_store(Q, K, V, causal, c, seed, store_id)
-    sc = delayed_scales(Q, K, V, dO, P32, O32, q, causal, c, factors)
-    print(f"[te] B={B} H={H} S={S} causal={causal} source={source} factors={factors} sharp={sharp} scales={sc}",
-          flush=True)
+    qkv_sc = None
+    if fp8_qkv is not None:
+        codes, qkv_sc, deq = fp8_operands(Q, K, V, fp8_qkv)
+        ops = [torch.from_numpy(d) for d in deq]          # the operands the forward used
+        args = [torch.from_numpy(cd) for cd in codes]
+        ref_ops = codes
+    else:
+        ops = [Q, K, V]
+        args = [Q, K, V]
+        ref_ops = [t.float().numpy() for t in (Q, K, V)]
+    O32, P32, q = forward_store(*ops, causal, c, seed, store_id)
+    sc = delayed_scales(*ops, dO, P32, O32, q, causal, c, factors)
+    print(f"[te] B={B} H={H} S={S} causal={causal} source={source} factors={factors} sharp={sharp} scales={sc} "
+          f"fp8_qkv={fp8_qkv} grad={grad_dtype}", flush=True)
     dev = torch.device("cuda")
-    out = lib.te_attn_bwd(Q.to(dev), K.to(dev), V.to(dev), dO.to(dev), torch.tensor(sc, device=dev),
+    out = lib.te_attn_bwd(*(t.to(dev) for t in args), dO.to(dev), torch.tensor(sc, device=dev),
+                          qkv_scales=None if qkv_sc is None else torch.tensor(qkv_sc, device=dev),
                           O=torch.from_numpy(O32).to(dev), O_codes=torch.from_numpy(q.codes).to(dev),
                           O_scale=torch.tensor([q.scale], dtype=torch.float32, device=dev), source=source,
                           threshold=thr, causal=causal, scale=c, seed=seed, store_id=store_id, trial=trial,
-                          want_p=True, want_ds=True, want_codes=True, want_pre=True)
+                          grad_dtype=grad_dtype, want_p=True, want_ds=True, want_codes=True, want_pre=True)
     torch.cuda.synchronize()
-    ref = te.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.float().numpy(),
-                   P=out["P"].cpu().numpy(), dS=out["dS"].cpu().numpy(), O=O32, O_codes=q.codes, O_scale=q.scale,
-                   causal=causal, c=c, scales=sc, source=source, thr=F32(thr), seed=seed, store_id=store_id,
-                   trial=trial)
-    compare(out, ref, Q, K, causal, c, sc)
+    ref = te.check(*ref_ops, dO.float().numpy(), P=out["P"].cpu().numpy(), dS=out["dS"].cpu().numpy(), O=O32,
+                   O_codes=q.codes, O_scale=q.scale, causal=causal, c=c, scales=sc, source=source, thr=F32(thr),
+                   seed=seed, store_id=store_id, trial=trial, qkv_scales=qkv_sc, grad_dtype=grad_dtype)
+    compare(out, ref, ops[0], ops[1], causal, c, sc, grad_dtype=grad_dtype)
     ref.update(O32=O32, Oc=q.codes, Os=q.scale, sc=sc)
     return out, ref
 
@@ -72,7 +98,7 @@ def fl32(x):
     return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
 
 
-def compare(out, ref, Q, K, causal, c, sc, totals=True):
+def compare(out, ref, Q, K, causal, c, sc, totals=True, grad_dtype="bf16"):
     B, H, S, dh = out["dQ"].shape
     flat = lambda t: to_np(t).reshape(B * H, *t.shape[2:])
     assert_rel(to_np(out["P"]), pstore.probabilities(Q.float().numpy(), K.float().numpy(), causal, c), TOL,
@@ -82,21 +108,30 @@ def compare(out, ref, Q, K, causal, c, sc, totals=True):
     assert_rel(flat(out["dS"]), ref["dS"], TOL, "dS")
     pre = out["pre"].cpu().numpy().astype(np.float64)
     n_miss, n_sat, n_edge = 0, 0, 0
+    want_dt = torch.bfloat16 if grad_dtype == "bf16" else torch.float32
     for i, name in enumerate(("dQ", "dK", "dV")):
+        assert out[name].dtype == want_dt, (name, out[name].dtype)
         p = pre[i].reshape(B * H, S, dh)
         assert_rel(p, ref[name + "_pre"], TOL, name + " pre-cast")
-        val, _, ns = te.cast64(p, sc[3], fp8.E5M2)
+        _, gcodes, ns = te.cast64(p, sc[3], fp8.E5M2)
         n_sat += ns
-        got = flat(out[name])                                   # fp32 values fl32(code value * s_g)
-        assert np.array_equal(got, fl32(val)), f"{name}: the returned values are not the cast of the pre-cast values"
-        want = fl32(ref[name])
+        got = flat(out[name])                     # BF16 (or fp32) values of fl32(code value * s_g)
+        assert np.array_equal(got, te.returned(gcodes, sc[3], fp8.E5M2, grad_dtype)), \
+            f"{name}: the returned values are not the cast of the pre-cast values"
+        assert np.array_equal(fl32(ref[name]), te.returned(te.cast64(ref[name + "_pre"], sc[3], fp8.E5M2)[1], sc[3],
+                                                           fp8.E5M2, grad_dtype))
+        _, ocodes, _ = te.cast64(ref[name + "_pre"], sc[3], fp8.E5M2)
         n_edge += int((np.abs(np.abs(ref[name + "_pre"]) / np.float64(sc[3]) - 57344.0) <= 1e-4 * 57344.0).sum())
-        miss = got != want
+        miss = gcodes != ocodes
         n_miss += int(miss.sum())
         if miss.any():
-            mid = 0.5 * (got[miss] + want[miss])
+            # the cast is monotone, so two codes differ only where the rounding boundary (the midpoint
+            # of their values, up to the rounding of x / s_g) lies between the two pre-cast values
+            mid = 0.5 * (oq.dequant(gcodes[miss], sc[3], fp8.E5M2) + oq.dequant(ocodes[miss], sc[3], fp8.E5M2))
             dist = np.abs(ref[name + "_pre"][miss] - mid)
-            assert np.all(dist <= 1e-4 * np.abs(mid)), f"{name}: a cast differs away from a rounding midpoint"
+            gap = np.abs(ref[name + "_pre"][miss] - p[miss])
+            assert np.all(dist <= gap + 1e-7 * np.abs(mid)), f"{name}: a cast differs away from a rounding midpoint"
+            assert np.all(gap <= TOL * np.abs(ref[name + "_pre"]).max())
     assert n_miss <= max(2, 1e-4 * 3 * pre[0].size), f"{n_miss} near-tie cast differences"
     if not totals:
         return
@@ -113,6 +148,17 @@ def compare(out, ref, Q, K, causal, c, sc, totals=True):
 @pytest.mark.parametrize("source", ["R", "P", "U", "N"])
 def test_causal_ragged_sources(lib, source):
     run_case(lib, 1, 2, 200, source=source, seed=2)
+
+
+@pytest.mark.parametrize("source", ["P", "R", "repair"])
+def test_fp8_operands_and_bf16_return(lib, source):
+    """App. D.2's emulation: Q, K, V are the forward's E4M3 stores, the gradients return in BF16."""
+    run_case(lib, 1, 2, 200, source=source, seed=13, fp8_qkv=(1.0, 1.0, 1.0), sharp=2 if source == "repair" else 1)
+
+
+def test_fp8_operands_stale_scales_fp32_return(lib):
+    """E4M3 stores of Q and V at half their amax scale (clamped entries), non-causal, fp32 return."""
+    run_case(lib, 2, 1, 128, causal=False, source="N", seed=14, fp8_qkv=(0.5, 1.0, 0.5), grad_dtype="f32")
 
 
 def test_clamped_scales_noncausal(lib):
@@ -210,6 +256,8 @@ def test_errors(lib):
     dev = torch.device("cuda")
     Q, K, V, dO = (t.to(dev) for t in inputs(1, 1, 64, 9))
     sc = torch.ones(4, device=dev)
+    with pytest.raises(TypeError):
+        lib.te_attn_bwd(Q, K, V, dO, sc, source="P", qkv_scales=torch.ones(3, device=dev))   # bf16, not codes
     with pytest.raises(lib.BspError):
         lib.te_attn_bwd(Q, K, V, dO, sc, source="R")                     # no O store
     with pytest.raises(lib.BspError):

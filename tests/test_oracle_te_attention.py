@@ -53,9 +53,20 @@ def test_casts_and_gradients():
     np.testing.assert_array_equal(out["dV_pre"][0], Pq[0, 0].T @ dOq[0, 0])
     dsq = qround.dequant(out["dS_codes"][0], scales[2], fp8.E5M2)
     np.testing.assert_allclose(out["dQ_pre"][0], c * dsq @ K[0, 0].numpy(), rtol=1e-15)
+    # returned in BF16 (App. D.2): torch's own E5M2 cast of fl32(pre / s_g), its fp32 dequantization,
+    # then torch's bf16 cast
+    sg = torch.tensor(scales[3])
     for name in ("dQ", "dK", "dV"):
-        vals = out[name][0] / np.float64(scales[3])
-        assert np.all(np.isin(np.abs(vals), fp8.decode(np.arange(128, dtype=np.uint8), fp8.E5M2)))
+        y = (torch.from_numpy(out[name + "_pre"][0]).to(torch.float32).double() / sg.double()).float()
+        c8 = y.clamp(-57344.0, 57344.0).to(torch.float8_e5m2)
+        want = (c8.to(torch.float32) * sg).to(torch.bfloat16).double().numpy()
+        np.testing.assert_array_equal(out[name][0], want)
+    f32 = te.check(Q.numpy(), K.numpy(), V.numpy(), dO.numpy(), P=P32, O=O32, O_codes=q.codes, O_scale=q.scale,
+                   c=c, scales=scales, source="R", grad_dtype="f32")
+    for name in ("dQ", "dK", "dV"):
+        y = (torch.from_numpy(out[name + "_pre"][0]).double() / sg.double()).float()
+        want = (y.clamp(-57344.0, 57344.0).to(torch.float8_e5m2).to(torch.float32) * sg).double().numpy()
+        np.testing.assert_array_equal(f32[name][0], want)
     # the R copy: D reads the E4M3 store of O
     Or = qround.dequant(q.codes, q.scale, fp8.E4M3)
     np.testing.assert_allclose(out["D"][0], (dOq[0, 0] * Or[0, 0]).sum(-1), rtol=1e-14)
@@ -95,3 +106,39 @@ def test_delayed_scales_are_the_window_maximum():
                 assert scales[i] == prev[i]
         prev = scales
     assert te.FMAX[0] == fp8.E4M3.fmax and te.FMAX[1] == fp8.E5M2.fmax
+
+
+def test_fp8_operands_are_the_dequantized_codes():
+    """With Q, K and V stored in E4M3 at their scales, the backward reads their dequantized values
+    (App. D.2): dS with D from P is autograd's softmax backward of the program built on torch's own
+    dequantization of the codes, and the pre-cast gradients are c dS_q K_deq, c dS_q^T Q_deq,
+    P_q^T dO_q."""
+    g = torch.Generator().manual_seed(4)
+    S, dh, c = 24, 8, 0.5
+    x = [torch.randn(1, 1, S, dh, generator=g) * 2 for _ in range(4)]
+    sc = [torch.tensor(float(t.abs().max()) / 448 * f, dtype=torch.float32) for t, f in zip(x[:3], (1.0, 0.5, 1.0))]
+    codes = [(t / s).clamp(-448, 448).to(torch.float8_e4m3fn) for t, s in zip(x[:3], sc)]
+    deq = [(cd.to(torch.float32) * s).double() for cd, s in zip(codes, sc)]       # torch's dequantization
+    dO = x[3]
+    Qd, Kd, Vd = deq
+    mask = torch.tril(torch.ones(S, S, dtype=torch.bool))
+    P32 = torch.softmax((c * Qd @ Kd.transpose(-1, -2)).masked_fill(~mask, float("-inf")), -1).float()
+    O32 = (P32.double() @ Vd).float().numpy()
+    q = qround.qround(O32, fp8.E4M3, qround.SR, 3, 0, 0)
+    scales = (np.float32(1 / 448), np.float32(float(dO.abs().max()) / 57344), np.float32(1e-3), np.float32(1e-2))
+    u8 = [cd.view(torch.uint8).numpy() for cd in codes]
+    out = te.check(*u8, dO.numpy(), P=P32.numpy(), O=O32, O_codes=q.codes, O_scale=q.scale, c=c, scales=scales,
+                   source="P", qkv_scales=tuple(float(s) for s in sc))
+    dOq, _, _ = te.cast(dO.numpy(), scales[1], fp8.E5M2)
+    s_ = torch.from_numpy(np.log(np.maximum(P32.double().numpy(), 1e-300))).requires_grad_(True)
+    Pt = torch.softmax(s_.masked_fill(P32 == 0, float("-inf")), dim=-1)
+    ((Pt @ Vd) * torch.from_numpy(dOq)).sum().backward()
+    ref = s_.grad[0, 0].numpy()
+    np.testing.assert_allclose(out["dS"][0], ref, rtol=0, atol=1e-6 * np.abs(ref).max())
+    dsq = qround.dequant(out["dS_codes"][0], scales[2], fp8.E5M2)
+    np.testing.assert_allclose(out["dQ_pre"][0], c * dsq @ Kd[0, 0].numpy(), rtol=1e-13, atol=0)
+    np.testing.assert_allclose(out["dK_pre"][0], c * dsq.T @ Qd[0, 0].numpy(), rtol=1e-13, atol=0)
+    # bf16 operands instead of the codes change the result: the option is not a no-op
+    plain = te.check(*(t.numpy() for t in x[:3]), dO.numpy(), P=P32.numpy(), O=O32, O_codes=q.codes,
+                     O_scale=q.scale, c=c, scales=scales, source="P")
+    assert not np.allclose(plain["dQ_pre"], out["dQ_pre"], rtol=1e-3)
