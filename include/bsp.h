@@ -414,6 +414,19 @@ size_t bs_policy_bias_workspace_size(int K, int64_t m);
 bs_status bs_policy_bias_estimate(const float* delta, int K, int64_t m, const float* g_ref, float* mean_err,
                                   float* se, double* summary, void* ws, size_t ws_bytes, void* stream);
 
+/* bs_policy_bias_estimate_noalloc -- bs_policy_bias_estimate for callers that cannot allocate:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc. It takes no
+ * workspace and allocates nothing: its scratch (the per-block partials) is a file-scope device
+ * array of the library, 6 MiB, which each GPU the library runs on holds until the process ends.
+ * Arguments and results as bs_policy_bias_estimate; m <= bs_policy_bias_noalloc_max() (2^26),
+ * BS_ESHAPE above. Calls on one GPU share that GPU's scratch: calls that overlap in time on one
+ * GPU (different streams without ordering, several host threads) race and must not be issued;
+ * calls ordered on one stream are safe. The first call on a device looks up the array's address
+ * on that device (BS_EHIP if that fails). */
+int64_t bs_policy_bias_noalloc_max(void);
+bs_status bs_policy_bias_estimate_noalloc(const float* delta, int K, int64_t m, const float* g_ref, float* mean_err,
+                                          float* se, double* summary, void* stream);
+
 /* ------------------------------------------------------------------------------------
  * bs_gemm_bf16_nt -- the contraction the backward uses for dW/dX/du (building block).
  *   C[M,N] = alpha * A[M,K] B[N,K]^T (+ C if accumulate), A and B bf16 with K contiguous

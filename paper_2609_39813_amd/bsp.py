@@ -53,6 +53,8 @@ _qround = _sig("bs_qround", _int, [_vp, _int, _i64, _int, _int, _u64, _u32, _u32
 _gemm = _sig("bs_gemm_bf16_nt", _int, [_vp, _i64, _vp, _i64, _vp, _i64, _i64, _i64, _i64, _f32, _int, _vp])
 _pb_ws = _sig("bs_policy_bias_workspace_size", _sz, [_int, _i64])
 _pb = _sig("bs_policy_bias_estimate", _int, [_vp, _int, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp])
+_pb_na_max = _sig("bs_policy_bias_noalloc_max", _i64, [])
+_pb_na = _sig("bs_policy_bias_estimate_noalloc", _int, [_vp, _int, _i64, _vp, _vp, _vp, _vp, _vp])
 _norm_ws = _sig("bs_rmsnorm_linear_workspace_size", _sz, [_i64, _i64, _i64, _int, _int])
 _norm = _sig("bs_rmsnorm_linear_fwd_bwd", _int,
              [_vp, _vp, _vp, _vp, _int, _i64, _i64, _i64, _f32, _int, _int, ctypes.POINTER(NormPolicy), _int, _int,
@@ -140,7 +142,8 @@ def profile_read(kernel=None):
 
 
 EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
-            "bs_policy_bias_estimate", "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
+            "bs_policy_bias_estimate", "bs_policy_bias_noalloc_max", "bs_policy_bias_estimate_noalloc",
+            "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
             "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_attn_pstore_workspace_size", "bs_attn_pstore_policy", "bs_attn_level2_policy",
             "bs_te_attn_workspace_size", "bs_te_attn_bwd", "bs_te_delayed_scales",
             "bs_logsoftmax_check_workspace_size", "bs_logsoftmax_reuse_check",
@@ -237,6 +240,30 @@ def policy_bias_estimate(delta, g_ref=None):
     _check(_pb(_p(delta), K, m, _p(g_ref), _p(mean), _p(se), _p(summ), _p(ws), ws.numel(), _stream()),
            "bs_policy_bias_estimate")
     return mean, se, summ
+
+
+def policy_bias_estimate_noalloc(delta, g_ref=None, out=None):
+    """bs_policy_bias_estimate_noalloc: the same statistics with the library's own device scratch
+    (no workspace; m <= policy_bias_noalloc_max()). out: optional (mean_err, se, summary) tensors
+    to write into."""
+    _dev_check(delta, g_ref)
+    if delta.dim() != 2 or delta.dtype != torch.float32:
+        raise TypeError("delta must be a [K, m] float32 tensor")
+    K, m = delta.shape
+    if g_ref is not None and (g_ref.dtype != torch.float32 or g_ref.numel() != m):
+        raise TypeError("g_ref must be a float32 tensor of m elements")
+    if out is None:
+        out = (torch.empty(m, dtype=torch.float32, device=delta.device),
+               torch.empty(m, dtype=torch.float32, device=delta.device),
+               torch.empty(3, dtype=torch.float64, device=delta.device))
+    mean, se, summ = out
+    _check(_pb_na(_p(delta), K, m, _p(g_ref), _p(mean), _p(se), _p(summ), _stream()),
+           "bs_policy_bias_estimate_noalloc")
+    return mean, se, summ
+
+
+def policy_bias_noalloc_max():
+    return int(_pb_na_max())
 
 
 def _est(n_pol, numel, device, want_se):
