@@ -514,10 +514,14 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* w, cons
  *   "te_dkv", "lsm_reduce");
  *   bs_profile_enable(0) stops and frees them. bs_profile_read waits for the recorded
  *   events of `kernel` (NULL: all) and returns their summed elapsed time and count.
- *   Return values are bs_status codes.
+ *   bs_profile_work returns the summed algorithmic work of those launches (work): for "gemm",
+ *   2 M N K flop per distinct product (the extra terms of a split bf16 operand do not count), and
+ *   the work the matrix cores execute (exec: 2 M N K per bf16 term product); 0 for kernels that
+ *   record none. Either pointer may be NULL. Return values are bs_status codes.
  * ---------------------------------------------------------------------------------- */
 int bs_profile_enable(int on);
 int bs_profile_read(const char* kernel, double* total_ms, int* launches);
+int bs_profile_work(const char* kernel, double* work, double* exec);
 
 #ifdef __cplusplus
 }

@@ -127,6 +127,8 @@ _layer = _sig("bs_decoder_layer_policy", _int,
 
 _prof_enable = _sig("bs_profile_enable", _int, [_int])
 _prof_read = _sig("bs_profile_read", _int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_int)])
+_prof_work = _sig("bs_profile_work", _int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                            ctypes.POINTER(ctypes.c_double)])
 
 
 def profile_enable(on=True):
@@ -141,6 +143,14 @@ def profile_read(kernel=None):
     return ms.value, n.value
 
 
+def profile_work(kernel=None):
+    """(algorithmic, executed) work (flop for "gemm") of the instrumented launches since profile_enable."""
+    w, x = ctypes.c_double(), ctypes.c_double()
+    _check(_prof_work(None if kernel is None else kernel.encode(), ctypes.byref(w), ctypes.byref(x)),
+           "bs_profile_work")
+    return w.value, x.value
+
+
 EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
             "bs_policy_bias_estimate", "bs_policy_bias_noalloc_max", "bs_policy_bias_estimate_noalloc",
             "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
@@ -148,7 +158,8 @@ EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "b
             "bs_te_attn_workspace_size", "bs_te_attn_bwd", "bs_te_delayed_scales",
             "bs_logsoftmax_check_workspace_size", "bs_logsoftmax_reuse_check",
             "bs_rmsnorm_linear_grid_workspace_size", "bs_rmsnorm_linear_grid_fwd_bwd", "bs_linear_bwd_workspace_size", "bs_linear_bwd_policy",
-            "bs_decoder_layer_workspace_size", "bs_decoder_layer_policy", "bs_profile_enable", "bs_profile_read"]
+            "bs_decoder_layer_workspace_size", "bs_decoder_layer_policy", "bs_profile_enable", "bs_profile_read",
+            "bs_profile_work"]
 
 
 class BspError(RuntimeError):

@@ -17,10 +17,21 @@ struct GemmArgs {
   float* C;
   float* part = nullptr;    // nullable: split-K partials, part_cap floats (device workspace)
   int64_t part_cap = 0;
+  int nprod = 0;            // distinct products among the segments (split terms of one product
+                            // count once); 0: every segment is a product of its own
 };
+
+// algorithmic flop of a contraction launch: 2 M N K per distinct product
+inline double gemm_flops(const GemmArgs& g) {
+  return 2.0 * g.M * g.N * (double)g.K * (g.nprod > 0 ? g.nprod : g.nseg);
+}
+// flop the matrix cores execute: 2 M N K per segment (every bf16 term of a split operand)
+inline double gemm_exec_flops(const GemmArgs& g) { return 2.0 * g.M * g.N * (double)g.K * g.nseg; }
 
 // Append the products A_i B_j (i + j <= 2) of nA and nB bf16 terms to g's segments.
 inline bool gemm_add_products(GemmArgs& g, const u16* const* A, int nA, const u16* const* B, int nB) {
+  if (g.nprod == 0 && g.nseg > 0) g.nprod = g.nseg;  // segments set before: one product each
+  ++g.nprod;
   for (int s = 0; s <= 2; ++s)
     for (int i = 0; i < nA; ++i) {
       const int j = s - i;
@@ -36,14 +47,17 @@ inline bool gemm_add_products(GemmArgs& g, const u16* const* A, int nA, const u1
 bs_status launch_gemm(const GemmArgs& g, hipStream_t st);
 
 // Records HIP events around a kernel launch while profiling is enabled (bs_profile_enable).
+// `work` is the launch's algorithmic work (flop for a contraction) and `exec` the work its units
+// execute (flop of every split term), summed by bs_profile_work.
 class ProfScope {
  public:
-  ProfScope(const char* name, hipStream_t st);
+  ProfScope(const char* name, hipStream_t st, double work = 0.0, double exec = 0.0);
   ~ProfScope();
 
  private:
   const char* name_;
   hipStream_t st_;
+  double work_, exec_;
   hipEvent_t a_, b_;
 };
 

@@ -364,7 +364,7 @@ static bs_status launch_gemm_lds(const GemmArgs& g0, hipStream_t st) {
   if (splits == 1) g.part = nullptr;
   if (tiles * splits > 0x7FFFFFFF) return BS_ESHAPE;
   {
-    ProfScope prof("gemm", st);
+    ProfScope prof("gemm", st, gemm_flops(g), gemm_exec_flops(g));
     gemm_lds_kernel<BM, BN, WGM, WGN><<<(unsigned)(tiles * splits), 64 * WGM * WGN, 0, st>>>(g, cps);
     BS_CHECK_LAUNCH();
   }
@@ -382,7 +382,7 @@ template <int BM, int BN, int WGM, int WGN>
 static bs_status launch_gemm_cfg(const GemmArgs& g, hipStream_t st) {
   const int64_t tiles = (int64_t)((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles > 0x7FFFFFFF) return BS_ESHAPE;
-  ProfScope prof("gemm", st);
+  ProfScope prof("gemm", st, gemm_flops(g), gemm_exec_flops(g));
   gemm_nt_kernel<BM, BN, WGM, WGN><<<(unsigned)tiles, 256, 0, st>>>(g);
   BS_CHECK_LAUNCH();
   return BS_OK;

@@ -15,6 +15,7 @@ namespace {
 struct Rec {
   std::string name;
   hipEvent_t a, b;
+  double work, exec;
 };
 std::mutex g_mu;
 std::atomic<bool> g_on{false};
@@ -31,7 +32,8 @@ void release_all() {
 }
 }  // namespace
 
-ProfScope::ProfScope(const char* name, hipStream_t st) : name_(name), st_(st), a_(nullptr), b_(nullptr) {
+ProfScope::ProfScope(const char* name, hipStream_t st, double work, double exec)
+    : name_(name), st_(st), work_(work), exec_(exec), a_(nullptr), b_(nullptr) {
   if (!g_on.load(std::memory_order_acquire)) return;
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on.load(std::memory_order_relaxed) || g_next + 2 > g_pool.size()) return;
@@ -44,7 +46,7 @@ ProfScope::~ProfScope() {
   if (!a_) return;
   hipEventRecord(b_, st_);
   std::lock_guard<std::mutex> lk(g_mu);
-  g_recs.push_back({name_, a_, b_});
+  g_recs.push_back({name_, a_, b_, work_, exec_});
 }
 
 }  // namespace bsp
@@ -80,6 +82,20 @@ int bs_profile_read(const char* kernel, double* total_ms, int* launches) {
   }
   if (total_ms) *total_ms = tot;
   if (launches) *launches = n;
+  return BS_OK;
+}
+
+int bs_profile_work(const char* kernel, double* work, double* exec) {
+  using namespace bsp;
+  std::lock_guard<std::mutex> lk(g_mu);
+  double tot = 0.0, ex = 0.0;
+  for (auto& r : g_recs)
+    if (!kernel || r.name == kernel) {
+      tot += r.work;
+      ex += r.exec;
+    }
+  if (work) *work = tot;
+  if (exec) *exec = ex;
   return BS_OK;
 }
 
