@@ -18,7 +18,9 @@ rounded to those formats; the backward passes gradients through every rounding u
 (the straight-through reference, Sec. 1, App. B.2).
 
 Per-use check (Sec. 4.1): each use of each store is evaluated at its own operator with the
-incoming gradient the reference backward delivers there, under each letter U / R / N:
+incoming gradient the reference backward delivers there, under each letter U / R / N (and, in
+``all_uses``, each letter applied at every use of every store at once, the backward carrying the
+changed incoming gradients on to the earlier uses):
 
   store u1: gain use, weight use (dWqkv), normalization-input use  -- oracle.norm_store
   store O:  D use (dQ, dK of the attention backward)               -- oracle.attention
@@ -100,34 +102,99 @@ def forward(x, p, *, B, S, H, eps=1e-5, fmt=fp8.E4M3, fwd_mode=qround.RNE, seed=
     return f
 
 
-def reference_backward(f, p, dOut):
-    """Straight-through reference gradients and the incoming gradient at every use (fp64)."""
+def reference_reads(f):
+    """What each use reads in the straight-through reference: the rounded value at the weight uses,
+    the original at the gain, normalization-input and D uses (Eq. norm-uses; Eq. dterm)."""
+    return {"a_W": f["aq"], "u2_g": f["z2"], "u2_W": f["u2q"], "u2_x": f["z2"], "O_W": tokens(f["Oq"]),
+            "O_D": f["O"], "u1_g": f["z1"], "u1_W": f["u1q"], "u1_x": f["z1"]}
+
+
+def layer_backward(f, p, dOut, reads):
+    """The layer's backward (fp64) with the value each use reads given in `reads`: a_W (weight use
+    of Wd), u2_g / u1_g (gain uses, the normalized value z), u2_W / u1_W (weight uses of [Wg | Wu]
+    and Wqkv), u2_x / u1_x (normalization-input uses, z), O_W (weight use of Wo, token-major), O_D
+    (the D use, head-major). Returns the gradients and the incoming gradient at every use."""
     dOut = np.asarray(dOut, dtype=np.float32).astype(np.float64)
     W = {k: p[k].astype(np.float64) for k in ("Wqkv", "Wo", "Wg", "Wu", "Wd")}
     B, S, H = f["B"], f["S"], f["H"]
+    rd = {k: np.asarray(v, dtype=np.float64) for k, v in reads.items()}
     r = {"dOut": dOut}
-    r["dWd"] = f["aq"].T @ dOut
+    r["dWd"] = rd["a_W"].T @ dOut
     da = dOut @ W["Wd"].T
     g = f["g"].astype(np.float64)
     sg = 1.0 / (1.0 + np.exp(-g))
     r["dg"] = da * f["hh"].astype(np.float64) * sg * (1.0 + g * (1.0 - sg))
     r["dhh"] = da * g * sg
     du2 = r["dg"] @ W["Wg"].T + r["dhh"] @ W["Wu"].T
-    r["dWg"] = f["u2q"].T @ r["dg"]
-    r["dWu"] = f["u2q"].T @ r["dhh"]
-    r["dgain2"] = (f["z2"].astype(np.float64) * du2).sum(0)
-    r["dh"] = dOut + norm_backward(f["z2"], f["r2"], p["gain2"].astype(np.float64) * du2)
+    r["dWg"] = rd["u2_W"].T @ r["dg"]
+    r["dWu"] = rd["u2_W"].T @ r["dhh"]
+    r["dgain2"] = (rd["u2_g"] * du2).sum(0)
+    r["dh"] = dOut + norm_backward(rd["u2_x"], f["r2"], p["gain2"].astype(np.float64) * du2)
     r["dO_tok"] = r["dh"] @ W["Wo"].T
-    r["dWo"] = tokens(f["Oq"]).T @ r["dh"]
+    r["dWo"] = rd["O_W"].T @ r["dh"]
     dO = heads(r["dO_tok"], B, S, H)
-    D = attention.d_from_copy(dO, f["O"].astype(np.float64))
+    D = attention.d_from_copy(dO, rd["O_D"])
     dQ, dK, dV = attention.backward(f["Q"], f["K"], f["V"], dO, f["P"], D, f["c"])
     r["dQKV"] = np.concatenate([tokens(dQ), tokens(dK), tokens(dV)], axis=1)
     du1 = r["dQKV"] @ W["Wqkv"].T
-    r["dWqkv"] = f["u1q"].T @ r["dQKV"]
-    r["dgain1"] = (f["z1"].astype(np.float64) * du1).sum(0)
-    r["dx"] = r["dh"] + norm_backward(f["z1"], f["r1"], p["gain1"].astype(np.float64) * du1)
+    r["dWqkv"] = rd["u1_W"].T @ r["dQKV"]
+    r["dgain1"] = (rd["u1_g"] * du1).sum(0)
+    r["dx"] = r["dh"] + norm_backward(rd["u1_x"], f["r1"], p["gain1"].astype(np.float64) * du1)
     return r
+
+
+def reference_backward(f, p, dOut):
+    """Straight-through reference gradients and the incoming gradient at every use (fp64)."""
+    return layer_backward(f, p, dOut, reference_reads(f))
+
+
+GRADS = ("dx", "dgain1", "dWqkv", "dWo", "dgain2", "dWg", "dWu", "dWd")
+
+
+def all_uses_reads(f, p, letter, *, seed, trial, fmt=fp8.E4M3):
+    """What every use reads when the letter is applied at all uses together: the original (U), the
+    forward's rounding (R) or, per use, a new stochastic rounding at the store's scale (N: trial
+    `trial`; use id store*256 + 1 at a gain use and the D use, + 2 at a weight use, + 3 at a
+    normalization-input use; the store's elements in its own layout, token-major except the D use's
+    head-major O)."""
+    if letter == "U":
+        return {"a_W": f["a"], "u2_g": f["z2"], "u2_W": f["u2"], "u2_x": f["z2"], "O_W": tokens(f["O"]),
+                "O_D": f["O"], "u1_g": f["z1"], "u1_W": f["u1"], "u1_x": f["z1"]}
+    g1, g2 = (np.asarray(p[k], np.float32).astype(np.float64) for k in ("gain1", "gain2"))
+    if letter == "R":
+        return {"a_W": f["aq"], "u2_g": f["u2q"] / g2, "u2_W": f["u2q"], "u2_x": f["u2q"] / g2,
+                "O_W": tokens(f["Oq"]), "O_D": f["Oq"], "u1_g": f["u1q"] / g1, "u1_W": f["u1q"],
+                "u1_x": f["u1q"] / g1}
+    assert letter == "N", letter
+
+    def fresh(x, q, store, j):
+        x = np.asarray(x, dtype=np.float32)
+        y = qround.scaled(x, q.scale)
+        el = np.arange(x.size, dtype=np.uint64).reshape(x.shape)
+        return fresh_values(y, el, fmt, q.scale, seed, trial, STORES.index(store) * 256 + j)
+    return {"a_W": fresh(f["a"], f["qa"], "a", 2),
+            "u2_g": fresh(f["u2"], f["q2"], "u2", 1) / g2, "u2_W": fresh(f["u2"], f["q2"], "u2", 2),
+            "u2_x": fresh(f["u2"], f["q2"], "u2", 3) / g2,
+            "O_W": fresh(tokens(f["O"]), f["qO"], "O", 2), "O_D": fresh(f["O"], f["qO"], "O", 1),
+            "u1_g": fresh(f["u1"], f["q1"], "u1", 1) / g1, "u1_W": fresh(f["u1"], f["q1"], "u1", 2),
+            "u1_x": fresh(f["u1"], f["q1"], "u1", 3) / g1}
+
+
+def all_uses(f, p, dOut, r, *, K, seed, fmt=fp8.E4M3, letters=("U", "R", "N")):
+    """The letter applied at every use of every store in one backward (config 5's policy applied to
+    every stored rounded tensor), K trials with the forward held fixed (one pass for U and R, which
+    draw nothing): {letter: {gradient: (mean, bias, se)}} against the reference gradients r."""
+    out = {}
+    for letter in letters:
+        ntr = K if letter == "N" else 1
+        tr = {gname: [] for gname in GRADS}
+        for k in range(1, ntr + 1):
+            g = layer_backward(f, p, dOut, all_uses_reads(f, p, letter, seed=seed, trial=k, fmt=fmt))
+            for gname in GRADS:
+                tr[gname].append(g[gname])
+        out[letter] = {gname: trial_stats(np.stack(tr[gname] * (K if ntr == 1 else 1)), r[gname])
+                       for gname in GRADS}
+    return out
 
 
 def weight_use(Xs, q, dY, fmt, letter, K, seed, use):

@@ -165,3 +165,105 @@ def test_forward_pin_rejects_planted_formula_errors(plant):
         bad["Wo"] = np.ascontiguousarray(pn["Wo"].T)
     f = decoder.forward(x, bad, B=B, S=S, H=H, seed=3)
     assert forward_failures(forward_stage_errors(f, x, pn, B, S, H)), plant
+
+
+# ---------------------------------------------------------------------------------------------
+# The letter applied at every use of every store together (decoder.all_uses)
+# ---------------------------------------------------------------------------------------------
+def _all_case(seed=2, B=1, S=12, d=64, H=1, F=96, fmt=fp8.E4M3):
+    (x, p, dOut), _ = synth.decoder_inputs(B, S, d, H, F, config=520 + seed)
+    pn = {k: v.float().numpy() for k, v in p.items()}
+    g = torch.Generator().manual_seed(90 + seed)
+    pn["gain1"] = (1 + 0.1 * torch.randn(d, generator=g)).numpy()
+    pn["gain2"] = (1 + 0.1 * torch.randn(d, generator=g)).numpy()
+    f = decoder.forward(x.float().numpy(), pn, B=B, S=S, H=H, seed=7, fmt=fmt)
+    r = decoder.reference_backward(f, pn, dOut.float().numpy())
+    return x, pn, dOut, f, r, (B, S, H)
+
+
+def test_all_uses_original_is_autograd_without_stores():
+    """U at every use: the backward of the realized forward in which no store is seen by the
+    backward (every use reads the original), by torch.autograd in fp64."""
+    x, pn, dOut, f, r, (B, S, H) = _all_case()
+    out = decoder.all_uses(f, pn, dOut.float().numpy(), r, K=3, seed=7, letters=("U",))
+    t = lambda a: torch.tensor(np.asarray(a, np.float64), requires_grad=True)
+    X = t(x.float().numpy())
+    P = {k: t(v) for k, v in pn.items()}
+    ste = lambda v, target: v + (torch.tensor(np.asarray(target, np.float64)) - v).detach()
+    rms = lambda v, g: g * (v * ((v * v).mean(-1, keepdim=True) + 1e-5).rsqrt())
+    T, d = X.shape
+    u1 = rms(X, P["gain1"])
+    qkv = ste(u1 @ P["Wqkv"], f["QKV"])
+    hs = lambda m: m.reshape(B, S, H, d // H).permute(0, 2, 1, 3)
+    Q, K, V = (ste(hs(qkv[:, i * d:(i + 1) * d]), f[n]) for i, n in enumerate("QKV"))
+    sc = f["c"] * Q @ K.transpose(-1, -2)
+    mask = torch.tril(torch.ones(S, S, dtype=torch.bool))
+    O = ste(torch.softmax(sc.masked_fill(~mask, float("-inf")), -1) @ V, f["O"])
+    h = ste(X + O.permute(0, 2, 1, 3).reshape(T, d) @ P["Wo"], f["h"])
+    u2 = rms(h, P["gain2"])
+    a = ste(torch.nn.functional.silu(ste(u2 @ P["Wg"], f["g"])) * ste(u2 @ P["Wu"], f["hh"]), f["a"])
+    (((h + a @ P["Wd"]) * torch.tensor(dOut.double().numpy())).sum()).backward()
+    rel = lambda a_, b_: np.linalg.norm(a_ - b_.detach().numpy()) / np.linalg.norm(b_.detach().numpy())
+    for name, grad in (("dx", X.grad), ("dgain1", P["gain1"].grad), ("dWqkv", P["Wqkv"].grad), ("dWo", P["Wo"].grad),
+                       ("dgain2", P["gain2"].grad), ("dWg", P["Wg"].grad), ("dWu", P["Wu"].grad),
+                       ("dWd", P["Wd"].grad)):
+        m, b, s = out["U"][name]
+        assert rel(m, grad) < 2e-6, (name, rel(m, grad))
+        assert np.all(s == 0)
+
+
+def test_all_uses_agrees_with_the_per_use_checks_where_the_incoming_gradient_is_fixed():
+    """The uses reached first by the backward (a's and u2's weight uses, u2's gain use) see the
+    reference incoming gradient whatever the letter, and draw under the same (trial, use) keys as
+    the per-use checks: their means equal the per-use oracles' exactly; R reads what the weight
+    uses need (no bias)."""
+    x, pn, dOut, f, r, (B, S, H) = _all_case(seed=3)
+    K = 4
+    al = decoder.all_uses(f, pn, dOut.float().numpy(), r, K=K, seed=7)
+    pu = decoder.per_use_table(f, pn, r, K=K, seed=7)
+    # (the per-use check of u2 takes its incoming gradient rounded to fp32, as the library holds it)
+    rel = lambda a_, b_: np.linalg.norm(a_ - b_) / np.linalg.norm(b_)
+    for l in ("U", "R", "N"):
+        np.testing.assert_allclose(al[l]["dWd"][0], pu[("a", "weight", "dW", l)][0], rtol=1e-12, atol=1e-14)
+        assert rel(al[l]["dgain2"][0], pu[("u2", "gain", "dgain", l)][0]) < 1e-6
+        F = pn["Wg"].shape[1]
+        dW2 = pu[("u2", "weight", "dW", l)][0]
+        assert rel(al[l]["dWg"][0], dW2[:, :F]) < 1e-6 and rel(al[l]["dWu"][0], dW2[:, F:]) < 1e-6
+    for name in ("dWd", "dWg", "dWu"):
+        assert np.all(al["R"][name][1] == 0)
+    # R's other gradients change through the normalization-input and D uses: biased, unlike the
+    # per-use reading of the same weight gradient
+    assert np.linalg.norm(al["R"]["dWo"][1]) > 0 and np.linalg.norm(al["R"]["dWqkv"][1]) > 0
+
+
+def _n_against_u(f, pn, dOut, r, K, seed):
+    al = decoder.all_uses(f, pn, dOut.float().numpy(), r, K=K, seed=seed, letters=("U", "N"))
+    zmax = {}
+    for name in decoder.GRADS:
+        mN, _, se = al["N"][name]
+        mU = al["U"][name][0]
+        ok = se > 0
+        assert np.all(mN[~ok] == mU[~ok]), name
+        zmax[name] = float((np.abs(mN - mU)[ok] / se[ok]).max()) if ok.any() else 0.0
+    return zmax
+
+
+def test_all_uses_new_rounding_is_unbiased_to_first_order(monkeypatch):
+    """N at every use, many trials: every use reads an independent unbiased rounding, so each
+    gradient's mean is U's (every use reading the original) up to second-order terms (the
+    normalization input's backward is quadratic in what it reads: a bias of order step^2, below
+    this Monte Carlo's resolution): every entry within 5.5 se. A planted error that reads the
+    forward's rounding of O at the D use instead of a new rounding fails it."""
+    x, pn, dOut, f, r, (B, S, H) = _all_case(seed=4, S=8, d=64, F=64)
+    z = _n_against_u(f, pn, dOut, r, 600, 11)
+    assert max(z.values()) < 5.5, z
+    reads = decoder.all_uses_reads
+
+    def planted(f_, p_, letter, **kw):
+        rd = reads(f_, p_, letter, **kw)
+        if letter == "N":
+            rd["O_D"] = f_["Oq"]
+        return rd
+    monkeypatch.setattr(decoder, "all_uses_reads", planted)
+    z = _n_against_u(f, pn, dOut, r, 600, 11)
+    assert z["dWqkv"] > 8 and z["dx"] > 8, z
