@@ -467,10 +467,19 @@ bs_status bs_gemm_bf16_nt(const void* A, int64_t lda, const void* B, int64_t ldb
  *   has no estimate (N at a normalization-input use, se of a weight use or of dK under N).
  *   Rows: 0 u1 gain, 1 u1 weight (dWqkv), 2 u1 norm-input (dX), 3 O D (dQ), 4 O D (dK),
  *   5 O weight (dWo), 6 u2 gain, 7 u2 weight ([dWg | dWu]), 8 u2 norm-input, 9 a weight (dWd).
+ *   all (nullable): each letter read at every use of every store together, in one backward whose
+ *   moved incoming gradients reach the earlier uses (config 5's policy applied to every stored
+ *   tensor): U reads every original, R every forward rounding, N per use a new rounding (trials
+ *   1..K; use +1 at a gain use and at the D use, +2 at a weight use, +3 at a normalization-input
+ *   use). Per letter l (U, R, N): bias[l] (mean over trials minus the reference) and se[l] of each
+ *   of dx, dgain1, dWqkv, dWo, dgain2, dWg, dWu, dWd (each nullable; se 0 for U and R, NaN where
+ *   N has no estimate: dWd, dWg, dWu, whose incoming gradients do not move, as at the per-use
+ *   weight uses); table [8][3][3] fp64 (nullable) in that gradient order: sum of squared bias,
+ *   squared reference, squared se. Runs K + 2 backward passes of the moved part of the layer.
  *   diags [4] (nullable; one per store). Every pointer is device memory (the structs themselves
  *   are host memory); outputs are owned by the caller.
- *   ws: device workspace, 256-byte aligned, of bs_decoder_layer_workspace_size(B,S,d,H,F,K) bytes
- *   (0 for shapes the call rejects).
+ *   ws: device workspace, 256-byte aligned, of bs_decoder_layer_workspace_size(B,S,d,H,F,K,
+ *   all_uses) bytes, all_uses != 0 when `all` is set (0 for shapes the call rejects).
  *   Returns BS_EINVAL for a null required pointer, K outside [1, 4096], eps < 0, an unknown
  *   format or mode, or a partly set `fixed`; BS_ESHAPE unless d = 64*H <= 8192, F a multiple of
  *   8 and B*H <= 65535; BS_EWORKSPACE for a short or misaligned workspace; BS_EHIP on a failed
@@ -497,12 +506,18 @@ typedef struct {
   uint8_t *u1, *O, *u2, *a;
   float* scales;
 } bs_layer_stores;
+typedef struct {
+  bs_layer_grads bias[3];  /* U, R, N */
+  bs_layer_grads se[3];
+  double* table;           /* [8][3][3] */
+} bs_layer_all;
 
-size_t bs_decoder_layer_workspace_size(int B, int S, int d, int H, int F, int K);
+size_t bs_decoder_layer_workspace_size(int B, int S, int d, int H, int F, int K, int all_uses);
 bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* w, const void* dOut, int B, int S, int d,
                                   int H, int F, float eps, bs_fp8 fmt, bs_round fwd_mode, int K, uint64_t seed,
                                   const bs_layer_forward* fixed, bs_layer_grads grads, bs_layer_stores stores,
-                                  double* table, bs_diag* diags, void* ws, size_t ws_bytes, void* stream);
+                                  double* table, const bs_layer_all* all, bs_diag* diags, void* ws, size_t ws_bytes,
+                                  void* stream);
 
 /* ------------------------------------------------------------------------------------
  * Kernel timing instrumentation (host calls; for benchmarks and profiling).

@@ -120,10 +120,15 @@ class LayerStores(ctypes.Structure):
     _fields_ = [(k, _vp) for k in ("u1", "O", "u2", "a", "scales")]
 
 
-_layer_ws = _sig("bs_decoder_layer_workspace_size", _sz, [_int] * 6)
+class LayerAll(ctypes.Structure):
+    _fields_ = [("bias", LayerGrads * 3), ("se", LayerGrads * 3), ("table", _vp)]
+
+
+_layer_ws = _sig("bs_decoder_layer_workspace_size", _sz, [_int] * 7)
 _layer = _sig("bs_decoder_layer_policy", _int,
               [_vp, ctypes.POINTER(LayerWeights), _vp, _int, _int, _int, _int, _int, _f32, _int, _int, _int, _u64,
-               ctypes.POINTER(LayerForward), LayerGrads, LayerStores, _vp, _vp, _vp, _sz, _vp])
+               ctypes.POINTER(LayerForward), LayerGrads, LayerStores, _vp, ctypes.POINTER(LayerAll), _vp, _vp, _sz,
+               _vp])
 
 _prof_enable = _sig("bs_profile_enable", _int, [_int])
 _prof_read = _sig("bs_profile_read", _int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_int)])
@@ -575,20 +580,25 @@ LAYER_ROWS = (("u1", "gain", "dgain"), ("u1", "weight", "dW"), ("u1", "norm_inpu
               ("u2", "norm_input", "dX"), ("a", "weight", "dW"))
 
 
-def decoder_layer_workspace(B, S, d, H, F, K, device):
-    n = _layer_ws(B, S, d, H, F, K)
+LAYER_GRADS = ("dx", "dgain1", "dWqkv", "dWo", "dgain2", "dWg", "dWu", "dWd")
+
+
+def decoder_layer_workspace(B, S, d, H, F, K, device, all_uses=False):
+    n = _layer_ws(B, S, d, H, F, K, int(all_uses))
     if n == 0:
         raise BspError(3, "bs_decoder_layer_workspace_size")
     return _workspace(n, device)
 
 
 def decoder_layer_policy(x, p, dOut, *, B, S, H, eps=1e-5, fmt="e4m3", fwd_mode="rne", K=16, seed=0, fixed=None,
-                         ws=None):
+                         all_uses=False, all_outputs=True, ws=None):
     """One decoder layer with four FP8 stores and the per-use check of every store
     (bs_decoder_layer_policy). p: gain1, gain2 fp32 [d]; Wqkv, Wo, Wg, Wu, Wd bf16. fixed:
     None, or the realized forward {Q, K, V (bf16 [B,H,S,64]), O ([B,H,S,64]), h, gh ([T,2F]),
     a ([T,F]) fp32}. Returns the table as {(store, use, grad, letter): (bias^2, ref^2, se^2)}
-    plus reference gradients, store codes and scales."""
+    plus reference gradients, store codes and scales. all_uses: also each letter read at every use
+    together ("all_bias" / "all_se": {letter: {gradient: tensor}}, only with all_outputs, and
+    "all_table_raw" [8][3][3])."""
     T, d = x.shape
     F = p["Wg"].shape[1]
     dev = x.device
@@ -611,12 +621,32 @@ def decoder_layer_policy(x, p, dOut, *, B, S, H, eps=1e-5, fmt="e4m3", fwd_mode=
            "table_raw": torch.empty(len(LAYER_ROWS), 3, 3, dtype=torch.float64, device=dev)}
     grads = LayerGrads(*[out[k].data_ptr() for k in ("dx", "dgain1", "dWqkv", "dWo", "dgain2", "dWg", "dWu", "dWd")])
     stores = LayerStores(*[out[k].data_ptr() for k in ("codes_u1", "codes_O", "codes_u2", "codes_a", "scales")])
+    allp = None
+    if all_uses:
+        shp = {"dx": (T, d), "dgain1": (d,), "dWqkv": (d, 3 * d), "dWo": (d, d), "dgain2": (d,), "dWg": (d, F),
+               "dWu": (d, F), "dWd": (F, d)}
+        out["all_table_raw"] = torch.empty(8, 3, 3, dtype=torch.float64, device=dev)
+        al = LayerAll()
+        al.table = out["all_table_raw"].data_ptr()
+        if all_outputs:
+            out["all_bias"] = {l: {g: e(*shp[g]) for g in LAYER_GRADS} for l in "URN"}
+            out["all_se"] = {l: {g: e(*shp[g]) for g in LAYER_GRADS} for l in "URN"}
+            for i, l in enumerate("URN"):
+                al.bias[i] = LayerGrads(*[out["all_bias"][l][g].data_ptr() for g in LAYER_GRADS])
+                al.se[i] = LayerGrads(*[out["all_se"][l][g].data_ptr() for g in LAYER_GRADS])
+        allp = ctypes.byref(al)
     if ws is None:
-        ws = decoder_layer_workspace(B, S, d, H, F, K, dev)
+        ws = decoder_layer_workspace(B, S, d, H, F, K, dev, all_uses)
     _check(_layer(_p(x), ctypes.byref(wts), _p(dOut), B, S, d, H, F, eps, _FMT[fmt], _MODE[fwd_mode], K, seed, fx,
-                  grads, stores, _p(out["table_raw"]), _p(out["diags"]), _p(ws), ws.numel(), _stream()),
+                  grads, stores, _p(out["table_raw"]), allp, _p(out["diags"]), _p(ws), ws.numel(), _stream()),
            "bs_decoder_layer_policy")
     return out
+
+
+def layer_all_table(raw):
+    """{(gradient, letter): (bias^2, ref^2, se^2)} from the [8][3][3] every-use table (host)."""
+    raw = raw.cpu().numpy() if hasattr(raw, "cpu") else raw
+    return {(g, l): tuple(float(v) for v in raw[r, i]) for r, g in enumerate(LAYER_GRADS) for i, l in enumerate("URN")}
 
 
 def layer_table(raw):

@@ -4,6 +4,7 @@
 #include "bsp_kernels.h"
 #include "k_layer.h"
 #include "k_norm.h"
+#include "layer_allu.h"
 #include "norm_run.h"
 
 using namespace bsp;
@@ -129,7 +130,7 @@ struct NormEst {
 
 struct LayerWs {
   float *qkv, *O, *Otok, *h, *gh, *a, *da, *dgh, *dxn2, *dh, *dOtok, *dOh, *dQ, *dK, *dV, *dqkv, *dxn1, *dWgu;
-  float *dWqkv, *dWo, *dWd, *dgain1, *dgain2, *scales;
+  float *dWqkv, *dWo, *dWd, *dgain1, *dgain2, *dx, *scales;
   u16 *Q, *K, *V, *Wgu, *WoT, *Oval;
   uint8_t *c_u1, *c_O, *c_Otok, *c_u2, *c_a;
   NormEst e1, e2;
@@ -138,6 +139,8 @@ struct LayerWs {
   bs_diag* diag;
   void* sub;
   size_t sub_bytes;
+  void* allu;  // the every-use-at-once check (nullptr when not asked for)
+  size_t allu_bytes;
 };
 
 size_t sub_ws_size(int B, int S, int d, int H, int F, int K) {
@@ -161,7 +164,7 @@ NormEst carve_est(Carver& c, int64_t T, int64_t d, int64_t n) {
   return e;
 }
 
-LayerWs carve_layer(Carver& c, int B, int S, int d, int H, int F, int K) {
+LayerWs carve_layer(Carver& c, int B, int S, int d, int H, int F, int K, bool all_uses) {
   LayerWs w{};
   const int64_t T = (int64_t)B * S, Td = T * d, TF = T * (int64_t)F;
   w.qkv = c.take<float>(3 * Td);
@@ -187,6 +190,7 @@ LayerWs carve_layer(Carver& c, int B, int S, int d, int H, int F, int K) {
   w.dWd = c.take<float>((int64_t)F * d);
   w.dgain1 = c.take<float>(d);
   w.dgain2 = c.take<float>(d);
+  w.dx = c.take<float>(Td);
   w.scales = c.take<float>(4);
   w.Q = c.take<u16>(Td);
   w.K = c.take<u16>(Td);
@@ -210,6 +214,10 @@ LayerWs carve_layer(Carver& c, int B, int S, int d, int H, int F, int K) {
   w.diag = c.take<bs_diag>(4);
   w.sub_bytes = sub_ws_size(B, S, d, H, F, K);
   w.sub = c.take<char>(w.sub_bytes);
+  if (all_uses) {
+    w.allu_bytes = allu_ws_size(B, S, d, H, F);
+    w.allu = c.take<char>(w.allu_bytes);
+  }
   return w;
 }
 
@@ -223,17 +231,18 @@ bool layer_shape_ok(int B, int S, int d, int H, int F) {
 
 extern "C" {
 
-size_t bs_decoder_layer_workspace_size(int B, int S, int d, int H, int F, int K) {
+size_t bs_decoder_layer_workspace_size(int B, int S, int d, int H, int F, int K, int all_uses) {
   if (!layer_shape_ok(B, S, d, H, F) || K < 1 || K > 4096) return 0;
   Carver c;
-  carve_layer(c, B, S, d, H, F, K);
+  carve_layer(c, B, S, d, H, F, K, all_uses != 0);
   return c.used();
 }
 
 bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, const void* dOut, int B, int S, int d,
                                   int H, int F, float eps, bs_fp8 fmt, bs_round fwd_mode, int K, uint64_t seed,
                                   const bs_layer_forward* fixed, bs_layer_grads grads, bs_layer_stores stores,
-                                  double* table, bs_diag* diags, void* ws, size_t ws_bytes, void* stream) {
+                                  double* table, const bs_layer_all* all, bs_diag* diags, void* ws, size_t ws_bytes,
+                                  void* stream) {
   hipStream_t st = (hipStream_t)stream;
   if (!x || !wt || !dOut || !table || !wt->gain1 || !wt->Wqkv || !wt->Wo || !wt->gain2 || !wt->Wg || !wt->Wu ||
       !wt->Wd)
@@ -243,10 +252,10 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
   if (!layer_shape_ok(B, S, d, H, F)) return BS_ESHAPE;
   if (fixed && (!fixed->Q || !fixed->K || !fixed->V || !fixed->O || !fixed->h || !fixed->gh || !fixed->a))
     return BS_EINVAL;
-  if (!ws || ((uintptr_t)ws & 255) || ws_bytes < bs_decoder_layer_workspace_size(B, S, d, H, F, K))
+  if (!ws || ((uintptr_t)ws & 255) || ws_bytes < bs_decoder_layer_workspace_size(B, S, d, H, F, K, all ? 1 : 0))
     return BS_EWORKSPACE;
   Carver c(ws, ws_bytes);
-  const LayerWs w = carve_layer(c, B, S, d, H, F, K);
+  const LayerWs w = carve_layer(c, B, S, d, H, F, K, all != nullptr);
   const int64_t T = (int64_t)B * S, Td = T * d, TF = T * (int64_t)F;
   const int64_t d3d = (int64_t)d * 3 * d, d2F = (int64_t)d * 2 * F, dd = (int64_t)d * d, Fd = (int64_t)F * d;
   bs_diag* dg = diags ? diags : w.diag;
@@ -384,7 +393,8 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
                   bs_est{nullptr, w.e1.g_bias, w.e1.g_se}, bs_est{nullptr, w.e1.w_bias, nullptr},
                   bs_est{nullptr, w.e1.x_bias, nullptr}, dg + 0};
   BS_TRY(norm_run(b1, w.sub, w.sub_bytes, st));
-  if (grads.dx) BS_TRY(launch_add(w.dh, BS_F32, w.dxn1, grads.dx, Td, st));
+  float* dx = grads.dx ? grads.dx : w.dx;
+  if (grads.dx || all) BS_TRY(launch_add(w.dh, BS_F32, w.dxn1, dx, Td, st));
   if (grads.dWg || grads.dWu) BS_TRY(launch_split_cols(w.dWgu, grads.dWg, grads.dWu, d, F, st));
 
   // ---------------- table: sums of squares (fp64, fixed order), one batch ----------------
@@ -422,6 +432,61 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
     row(9, l, w.wd_bias + l * Fd, dWd, wse, Fd);
   }
   BS_TRY(launch_sumsq_batch(batch, w.part, st));
+
+  // ---------------- every letter at every use together ----------------
+  if (all) {
+    AlluIO ai{};
+    ai.B = B;
+    ai.S = S;
+    ai.d = d;
+    ai.H = H;
+    ai.F = F;
+    ai.K = K;
+    ai.eps = eps;
+    ai.fmt = fmt;
+    ai.seed = seed;
+    ai.x = (const u16*)x;
+    ai.gain1 = wt->gain1;
+    ai.gain2 = wt->gain2;
+    ai.Wqkv = (const u16*)wt->Wqkv;
+    ai.Wo = (const u16*)wt->Wo;
+    ai.Wgu = w.Wgu;
+    ai.Q = (const u16*)Q;
+    ai.Kk = (const u16*)Kk;
+    ai.V = (const u16*)V;
+    ai.O = O;
+    ai.Otok = w.Otok;
+    ai.h = h;
+    ai.a = a;
+    ai.c_u1 = c_u1;
+    ai.c_O = c_O;
+    ai.c_Otok = w.c_Otok;
+    ai.c_u2 = c_u2;
+    ai.c_a = c_a;
+    ai.scales = scales;
+    ai.dgh = w.dgh;
+    ai.dh = w.dh;
+    ai.dOh = w.dOh;
+    ai.dqkv = w.dqkv;
+    const float* refs[8] = {dx, dgain1, dWqkv, dWo, dgain2, w.dWgu, nullptr, dWd};
+    for (int i = 0; i < 8; ++i) ai.ref[i] = refs[i];
+    ai.wd_bias = w.wd_bias;
+    ai.wgu_bias = w.e2.w_bias;
+    ai.g2_bias = w.e2.g_bias;
+    ai.g2_se = w.e2.g_se;
+    for (int l = 0; l < 3; ++l) {
+      const bs_layer_grads& b = all->bias[l];
+      const bs_layer_grads& e = all->se[l];
+      float* bp[8] = {b.dx, b.dgain1, b.dWqkv, b.dWo, b.dgain2, b.dWg, b.dWu, b.dWd};
+      float* ep[8] = {e.dx, e.dgain1, e.dWqkv, e.dWo, e.dgain2, e.dWg, e.dWu, e.dWd};
+      for (int i = 0; i < 8; ++i) {
+        ai.bias[l][i] = bp[i];
+        ai.se[l][i] = ep[i];
+      }
+    }
+    ai.table = all->table;
+    BS_TRY(allu_run(ai, w.allu, w.allu_bytes, st));
+  }
   return BS_OK;
 }
 

@@ -1,0 +1,222 @@
+// Kernels of the "every use at once" check of the decoder layer (declared in k_allu.h).
+#include "k_allu.h"
+
+namespace bsp {
+
+namespace {
+
+// What a use reads of four consecutive store elements e0 .. e0 + 3 (e0 a multiple of 4): the
+// original x (U), the forward's rounding s val(C) (R), or a new stochastic rounding of fl32(x / s)
+// at the same scale (N; Philox word e & 3 of the call keyed (seed; e0 >> 2, trial, use)). fp64.
+__device__ __forceinline__ void read4(const StoreRead& r, int64_t e0, const float (&x)[4], double rs, float s,
+                                      double (&v)[4]) {
+  if (r.letter == LETTER_U) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = x[i];
+  } else if (r.letter == LETTER_R) {
+    const uint32_t w = *(const uint32_t*)(r.codes + e0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = (double)s * (double)f8_value((w >> (8 * i)) & 0xFFu, r.f);
+  } else {
+    const Philox4 p = philox_group(r.seed, (uint64_t)(e0 >> 2), r.trial, r.use);
+    const uint32_t R[4] = {p.w0, p.w1, p.w2, p.w3};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float y = div_scale(x[i], rs);
+      const Bracket b = f8_bracket(fminf(fabsf(y), r.f.fmax), r.f);
+      const double mag = (double)(b.mi + sr_up(b.F, R[i])) * (double)f8_step(b);
+      v[i] = (signbit(y) ? -mag : mag) * (double)s;
+    }
+  }
+}
+
+__device__ __forceinline__ void load4(const float* p, int64_t e, float (&v)[4]) {
+  const float4 q = *(const float4*)(p + e);
+  v[0] = q.x;
+  v[1] = q.y;
+  v[2] = q.z;
+  v[3] = q.w;
+}
+__device__ __forceinline__ void load4(const u16* p, int64_t e, float (&v)[4]) {
+  const uint2 q = *(const uint2*)(p + e);
+  v[0] = bf16_to_f32((u16)(q.x & 0xFFFF));
+  v[1] = bf16_to_f32((u16)(q.x >> 16));
+  v[2] = bf16_to_f32((u16)(q.y & 0xFFFF));
+  v[3] = bf16_to_f32((u16)(q.y >> 16));
+}
+
+constexpr int ALLU_RT = 16;  // rows per tile of the gain use's partial sums
+
+// block: 256 threads x 4 consecutive columns (1024 columns), rows [16 y, 16 y + 16)
+template <typename XT>
+__global__ __launch_bounds__(256) void allu_gain_kernel(AlluGainArgs<XT> a) {
+  const int64_t j0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (j0 >= a.d) return;
+  const int64_t t0 = (int64_t)blockIdx.y * ALLU_RT;
+  const float s = a.rd.scale ? *a.rd.scale : 1.0f;
+  const double rs = 1.0 / (double)s;
+  float g[4];
+  load4(a.gain, j0, g);
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int i = 0; i < ALLU_RT; ++i) {
+    const int64_t t = t0 + i;
+    if (t >= a.T) break;
+    const int64_t e = t * a.d + j0;
+    const float r = a.rstd[t];
+    float x[4], u[4], du[4], ddu[4] = {0.f, 0.f, 0.f, 0.f};
+    load4(a.X, e, x);
+    load4(a.rd.x, e, u);
+    load4(a.du, e, du);
+    if (a.ddu) load4(a.ddu, e, ddu);
+    double v[4];
+    read4(a.rd, e, u, rs, s, v);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const float z = x[c] * r;  // the forward's fp32 z
+      const double zg = a.rd.letter == LETTER_U ? (double)z : v[c] / (double)g[c];
+      // z_g (du + ddu) - z du = (z_g - z)(du + ddu) + z ddu
+      acc[c] += (zg - (double)z) * ((double)du[c] + (double)ddu[c]) + (double)z * (double)ddu[c];
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < 4; ++c) a.part[(int64_t)blockIdx.y * a.d + j0 + c] = acc[c];
+}
+
+// one wave per row, 4 rows per block; columns in groups of 4 per lane
+template <typename XT>
+__global__ __launch_bounds__(256) void allu_dx_kernel(AlluDxArgs<XT> a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= a.T) return;  // uniform per wave
+  const float s = a.rd.scale ? *a.rd.scale : 1.0f;
+  const double rs = 1.0 / (double)s;
+  const float r = a.rstd[t];
+  const int64_t rowe = t * a.d;
+  double dref = 0.0, dl = 0.0;
+  for (int64_t j0 = 4 * (int64_t)lane; j0 < a.d; j0 += 256) {
+    float x[4], u[4], du[4], ddu[4] = {0.f, 0.f, 0.f, 0.f}, g[4];
+    load4(a.X, rowe + j0, x);
+    load4(a.rd.x, rowe + j0, u);
+    load4(a.du, rowe + j0, du);
+    load4(a.gain, j0, g);
+    if (a.ddu) load4(a.ddu, rowe + j0, ddu);
+    double v[4];
+    read4(a.rd, rowe + j0, u, rs, s, v);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const double z = (double)(x[c] * r);
+      const double zx = a.rd.letter == LETTER_U ? z : v[c] / (double)g[c];
+      dref += (double)g[c] * (double)du[c] * z;
+      dl += (double)g[c] * ((double)du[c] + (double)ddu[c]) * zx;
+    }
+  }
+  dref = __shfl(wave_sum_f64(dref), 0, 64);  // the wave sum is valid in lane 0: broadcast it
+  dl = __shfl(wave_sum_f64(dl), 0, 64);
+  const double inv_d = 1.0 / (double)a.d;
+  for (int64_t j0 = 4 * (int64_t)lane; j0 < a.d; j0 += 256) {
+    float x[4], u[4], ddu[4] = {0.f, 0.f, 0.f, 0.f}, g[4], ad[4] = {0.f, 0.f, 0.f, 0.f};
+    load4(a.X, rowe + j0, x);
+    load4(a.rd.x, rowe + j0, u);
+    load4(a.gain, j0, g);
+    if (a.ddu) load4(a.ddu, rowe + j0, ddu);
+    if (a.add) load4(a.add, rowe + j0, ad);
+    double v[4];
+    read4(a.rd, rowe + j0, u, rs, s, v);
+    float o[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const double z = (double)(x[c] * r);
+      const double zx = a.rd.letter == LETTER_U ? z : v[c] / (double)g[c];
+      o[c] = (float)((double)r * ((double)g[c] * (double)ddu[c] - (zx * dl - z * dref) * inv_d) + (double)ad[c]);
+    }
+    *(float4*)(a.out + rowe + j0) = make_float4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+// 16 lanes per row of 64, 4 elements each; 16 rows per block
+__global__ __launch_bounds__(256) void allu_d_kernel(AlluDArgs a) {
+  const int64_t row = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+  const int sub = threadIdx.x & 15;
+  const bool ok = row < a.rows;
+  double acc = 0.0;
+  if (ok) {
+    const float s = *a.rd.scale;
+    const double rs = 1.0 / (double)s;
+    const int64_t e = row * 64 + 4 * sub;
+    float o[4], dO[4], ddO[4] = {0.f, 0.f, 0.f, 0.f};
+    load4(a.rd.x, e, o);
+    load4(a.dO, e, dO);
+    if (a.ddO) load4(a.ddO, e, ddO);
+    double v[4];
+    read4(a.rd, e, o, rs, s, v);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc += (double)ddO[c] * v[c] + (double)dO[c] * (v[c] - (double)o[c]);
+  }
+#pragma unroll
+  for (int m = 1; m < 16; m <<= 1) acc += __shfl_xor(acc, m, 64);
+  if (ok && sub == 0) a.out[row] = (float)acc;
+}
+
+__global__ __launch_bounds__(256) void trial_mean_kernel(const float* __restrict__ d1, const double* __restrict__ S1,
+                                                         int K, int64_t m, float* __restrict__ out) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = (float)((double)d1[i] + S1[i] / (double)K);
+}
+
+__global__ __launch_bounds__(256) void fill_kernel(float* __restrict__ out, int64_t n, float v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = v;
+}
+
+unsigned blocks1d(int64_t n) {
+  const int64_t b = (n + 255) / 256;
+  return (unsigned)(b < 8192 ? (b > 0 ? b : 1) : 8192);
+}
+
+}  // namespace
+
+template <typename XT>
+bs_status launch_allu_gain(const AlluGainArgs<XT>& a, hipStream_t st) {
+  if (a.T <= 0 || a.d <= 0) return BS_OK;
+  if (a.d & 3) return BS_ESHAPE;
+  const dim3 grid((unsigned)((a.d + 1023) / 1024), (unsigned)((a.T + ALLU_RT - 1) / ALLU_RT));
+  allu_gain_kernel<XT><<<grid, 256, 0, st>>>(a);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+template bs_status launch_allu_gain<float>(const AlluGainArgs<float>&, hipStream_t);
+template bs_status launch_allu_gain<u16>(const AlluGainArgs<u16>&, hipStream_t);
+
+template <typename XT>
+bs_status launch_allu_dx(const AlluDxArgs<XT>& a, hipStream_t st) {
+  if (a.T <= 0 || a.d <= 0) return BS_OK;
+  if (a.d & 3) return BS_ESHAPE;
+  allu_dx_kernel<XT><<<(unsigned)((a.T + 3) / 4), 256, 0, st>>>(a);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+template bs_status launch_allu_dx<float>(const AlluDxArgs<float>&, hipStream_t);
+template bs_status launch_allu_dx<u16>(const AlluDxArgs<u16>&, hipStream_t);
+
+bs_status launch_allu_d(const AlluDArgs& a, hipStream_t st) {
+  if (a.rows <= 0) return BS_OK;
+  allu_d_kernel<<<(unsigned)((a.rows + 15) / 16), 256, 0, st>>>(a);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+bs_status launch_trial_mean(const float* d1, const double* S1, int K, int64_t m, float* out, hipStream_t st) {
+  if (m <= 0) return BS_OK;
+  trial_mean_kernel<<<blocks1d(m), 256, 0, st>>>(d1, S1, K, m, out);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+bs_status launch_fill(float* out, int64_t n, float v, hipStream_t st) {
+  if (n <= 0) return BS_OK;
+  fill_kernel<<<blocks1d(n), 256, 0, st>>>(out, n, v);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+}  // namespace bsp

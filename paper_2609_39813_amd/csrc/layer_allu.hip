@@ -1,0 +1,359 @@
+// The decoder layer's "every use at once" check (layer_allu.h). With letter L read at every use,
+// the backward's incoming gradients move away from the reference's at the uses the backward
+// reaches after u2's normalization-input use; each move is formed from residual operands:
+//   dh     = dOut + (u2's normalization-input backward reading z_x)         move: dh_d
+//   dWo    = O_W^T dh_L          = ref + (O_W - O_q)^T dh_L + O_q^T dh_d
+//   dO     = dh_L Wo^T           move: dh_d Wo^T
+//   D      = rowsum(dO_L O_D)    move: rowsum(dO_d O_D) + rowsum(dO (O_D - O))
+//   dQ, dK, dV: the attention backward is linear in (dO, D): its move is the backward of the moves
+//   dWqkv  = u1_W^T dQKV_L       = ref + (u1_W - u1_q)^T dQKV_L + u1_q^T dQKV_d
+//   du1    = dQKV_L Wqkv^T       move: dQKV_d Wqkv^T
+//   dgain1, dx: gain and normalization-input uses of u1 (k_allu.h)
+// The uses the backward reaches first (a's weight use, u2's gain and weight uses) see the
+// reference incoming gradient whatever the letter, with the per-use check's draws: their
+// estimates are the per-use ones. N draws every use's own new rounding per trial; its K trials
+// are reduced by shifted fp64 sums (mean and se over trials, App. C.4).
+#include "layer_allu.h"
+
+#include <algorithm>
+
+#include "k_allu.h"
+#include "k_attn.h"
+#include "k_layer.h"
+#include "k_norm.h"
+
+#define BS_TRY(x)               \
+  do {                          \
+    const bs_status _s = (x);   \
+    if (_s != BS_OK) return _s; \
+  } while (0)
+
+namespace bsp {
+
+namespace {
+
+constexpr int DH = 64;
+constexpr float kAttnScale = 0.125f;  // 1 / sqrt(64)
+enum { G_DX = 0, G_DGAIN1, G_DWQKV, G_DWO, G_DGAIN2, G_DWG, G_DWU, G_DWD, NGRAD };
+constexpr int NCOMP = 4;  // gradients formed here per trial: dx, dgain1, dWqkv, dWo
+
+struct AlluWs {
+  float *u1, *u2, *r1, *r2, *du1, *du2, *m, *l;
+  u16 *Vt, *Qt, *Kt, *valT_u1, *valT_O, *dqkvT[3], *dhT[3];
+  u16 *pA[3], *rows3[3], *tA[3], *tB[3], *dOp[3], *dOt[3];
+  float *dh_d, *dh_L, *dO_dt, *dO_dh, *dD, *dQ_d, *dK_d, *dV_d, *dqkv_d, *dqkv_L, *du1_d;
+  double* gpart;
+  float* delta[NCOMP];      // this pass's moves
+  float* bias[3][NCOMP];    // per letter
+  float* se_n[NCOMP];       // N's se
+  float *d1[NCOMP];
+  double *S1[NCOMP], *S2[NCOMP];
+  float *wg[3], *wu[3], *ref_g, *ref_u, *nan_buf;
+  float* part;
+  int64_t part_cap;
+  double* sumsq_part;
+  bs_diag* diag;
+};
+
+AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
+  AlluWs w{};
+  const int64_t T = (int64_t)B * S, Td = T * d, Tp = round_up(T > 0 ? T : 1, 64), bh = (int64_t)B * H;
+  const int64_t Sp = round_up(S, 64), d3 = 3 * (int64_t)d, F2 = 2 * (int64_t)F;
+  const int64_t nc[NCOMP] = {Td, d, (int64_t)d * d3, (int64_t)d * d};
+  for (float** p : {&w.u1, &w.u2, &w.du1, &w.du2}) *p = c.take<float>(Td);
+  for (float** p : {&w.r1, &w.r2}) *p = c.take<float>(T);
+  w.m = c.take<float>(bh * S);
+  w.l = c.take<float>(bh * S);
+  for (u16** p : {&w.Vt, &w.Qt, &w.Kt}) *p = c.take<u16>(bh * DH * Sp);
+  w.valT_u1 = c.take<u16>(d * Tp);
+  w.valT_O = c.take<u16>(d * Tp);
+  for (int i = 0; i < 3; ++i) {
+    w.dqkvT[i] = c.take<u16>(d3 * Tp);
+    w.dhT[i] = c.take<u16>(d * Tp);
+    w.pA[i] = c.take<u16>(d * Tp);
+    w.rows3[i] = c.take<u16>(T * std::max(F2, d3));
+    w.tA[i] = c.take<u16>(d3 * Tp);
+    w.tB[i] = c.take<u16>(d3 * Tp);
+    w.dOp[i] = c.take<u16>(Td);
+    w.dOt[i] = c.take<u16>(bh * DH * Sp);
+  }
+  for (float** p : {&w.dh_d, &w.dh_L, &w.dO_dt, &w.dO_dh, &w.dQ_d, &w.dK_d, &w.dV_d, &w.du1_d}) *p = c.take<float>(Td);
+  w.dD = c.take<float>(bh * S);
+  w.dqkv_d = c.take<float>(3 * Td);
+  w.dqkv_L = c.take<float>(3 * Td);
+  w.gpart = c.take<double>(3 * ((T + 15) / 16) * (int64_t)d);
+  for (int i = 0; i < NCOMP; ++i) {
+    w.delta[i] = c.take<float>(nc[i]);
+    for (int l = 0; l < 3; ++l) w.bias[l][i] = c.take<float>(nc[i]);
+    w.se_n[i] = c.take<float>(nc[i]);
+    w.d1[i] = c.take<float>(nc[i]);
+    w.S1[i] = c.take<double>(nc[i]);
+    w.S2[i] = c.take<double>(nc[i]);
+  }
+  for (int l = 0; l < 3; ++l) {
+    w.wg[l] = c.take<float>((int64_t)d * F);
+    w.wu[l] = c.take<float>((int64_t)d * F);
+  }
+  w.ref_g = c.take<float>((int64_t)d * F);
+  w.ref_u = c.take<float>((int64_t)d * F);
+  w.nan_buf = c.take<float>(std::max<int64_t>({Td, (int64_t)d * F2, (int64_t)d * d3}));
+  w.part_cap = 8 * (int64_t)d * d3;  // split-K partials of the few-tile weight contractions
+  w.part = c.take<float>(w.part_cap);
+  w.sumsq_part = c.take<double>(sumsq_part_size());
+  w.diag = c.take<bs_diag>(1);
+  return w;
+}
+
+// C = alpha * (sum of the products A_i B_j of the given term lists) for NT operands
+struct Gemm {
+  GemmArgs g{};
+  Gemm(int M, int N, int K, int64_t lda, int64_t ldb, float* C, int64_t ldc, const float* alpha_dev) {
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    g.lda = lda;
+    g.ldb = ldb;
+    g.ldc = ldc;
+    g.alpha = 1.0f;
+    g.alpha_dev = alpha_dev;
+    g.C = C;
+  }
+  Gemm& add(const u16* const* A, int nA, const u16* const* B, int nB) {
+    ok = ok && gemm_add_products(g, A, nA, B, nB);
+    return *this;
+  }
+  bs_status run(float* part, int64_t cap, hipStream_t st) {
+    if (!ok) return BS_EINVAL;
+    g.part = part;
+    g.part_cap = cap;
+    return launch_gemm(g, st);
+  }
+  bool ok = true;
+};
+
+bs_status copy_f32(float* dst, const float* src, int64_t n, hipStream_t st) {
+  if (!dst || n <= 0) return BS_OK;
+  return hipMemcpyAsync(dst, src, sizeof(float) * n, hipMemcpyDeviceToDevice, st) == hipSuccess ? BS_OK : BS_EHIP;
+}
+
+}  // namespace
+
+size_t allu_ws_size(int B, int S, int d, int H, int F) {
+  Carver c;
+  carve_allu(c, B, S, d, H, F);
+  return c.used();
+}
+
+bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
+  const int B = io.B, S = io.S, d = io.d, H = io.H, F = io.F, K = io.K;
+  const int64_t T = (int64_t)B * S, Td = T * d, Tp = round_up(T > 0 ? T : 1, 64), bh = (int64_t)B * H;
+  const int64_t Sp = round_up(S, 64), rows_h = bh * S, d3 = 3 * (int64_t)d, F2 = 2 * (int64_t)F;
+  const int64_t nc[NCOMP] = {Td, d, (int64_t)d * d3, (int64_t)d * d};
+  Carver probe;
+  carve_allu(probe, B, S, d, H, F);
+  if (ws_bytes < probe.used()) return BS_EWORKSPACE;
+  Carver c(ws, ws_bytes);
+  const AlluWs w = carve_allu(c, B, S, d, H, F);
+  const F8 f = f8_format(io.fmt);
+  const float *s_u1 = io.scales + 0, *s_O = io.scales + 1, *s_u2 = io.scales + 2;
+
+  // ---- fixed: the stores' inputs and inverse rms, du at u1 and u2, the attention rows ----
+  BS_TRY(launch_init_diag(w.diag, st));
+  BS_TRY(launch_rmsnorm_fwd(io.x, BS_BF16, io.gain1, T, d, io.eps, w.u1, w.r1, w.diag, st));
+  BS_TRY(launch_rmsnorm_fwd(io.h, BS_F32, io.gain2, T, d, io.eps, w.u2, w.r2, w.diag, st));
+  BS_TRY(launch_planes(io.dgh, BS_F32, T, F2, F2, false, w.rows3, 3, F2, 1.0f, st));
+  BS_TRY(Gemm((int)T, d, (int)F2, F2, F2, w.du2, d, nullptr).add(w.rows3, 3, &io.Wgu, 1).run(nullptr, 0, st));
+  BS_TRY(launch_planes(io.dqkv, BS_F32, T, d3, d3, false, w.rows3, 3, d3, 1.0f, st));
+  BS_TRY(Gemm((int)T, d, (int)d3, d3, d3, w.du1, d, nullptr).add(w.rows3, 3, &io.Wqkv, 1).run(nullptr, 0, st));
+  {
+    const u16* src[3] = {io.V, io.Q, io.Kk};
+    u16* dst[3] = {w.Vt, w.Qt, w.Kt};
+    BS_TRY(launch_attn_transpose(src, dst, 3, (int)bh, S, (int)Sp, st));
+    AttnArgs fa{io.Q, io.Kk, io.V, S, 1, kAttnScale, w.m, w.l, nullptr, w.Vt, (int)Sp};
+    BS_TRY(launch_attn_fwd(fa, B, H, st));
+  }
+  NormPlaneArgs pa{};
+  pa.f = f;
+  pa.T = T;
+  pa.d = d;
+  pa.ldo = Tp;
+  pa.K = 1;
+  pa.nterms = 1;
+  auto planes_of = [&](int mode, const float* u, const uint8_t* codes, const float* scale, u16* const* out,
+                       int nterms) {
+    pa.u = u;
+    pa.codes = codes;
+    pa.scale = scale;
+    pa.nterms = nterms;
+    for (int i = 0; i < 3; ++i) pa.out[i] = i < nterms ? out[i] : nullptr;
+    return launch_norm_planes(mode, pa, st);
+  };
+  BS_TRY(planes_of(NP_VAL, w.u1, io.c_u1, s_u1, &w.valT_u1, 1));
+  BS_TRY(planes_of(NP_VAL, io.Otok, io.c_Otok, s_O, &w.valT_O, 1));
+  BS_TRY(launch_planes(io.dqkv, BS_F32, T, d3, d3, true, w.dqkvT, 3, Tp, 1.0f, st));
+  BS_TRY(launch_planes(io.dh, BS_F32, T, d, d, true, w.dhT, 3, Tp, 1.0f, st));
+
+  // ---- one pass per letter (K per-trial passes for N) ----
+  for (int l = 0; l < 3; ++l) {
+    const int ntr = l == LETTER_N ? K : 1;
+    for (int k = 1; k <= ntr; ++k) {
+      const auto rd = [&](const float* x, const uint8_t* codes, const float* scale, uint32_t use) {
+        return StoreRead{x, codes, scale, f, l, io.seed, (uint32_t)k, use};
+      };
+      float* dWo = w.delta[3];
+      float* dWqkv = w.delta[2];
+      // u2's normalization-input use: the move of dh
+      if (l != LETTER_U) {
+        const AlluDxArgs<float> ax{io.h, w.r2, io.gain2, rd(w.u2, io.c_u2, s_u2, 2 * 256 + 3), w.du2, nullptr,
+                                   nullptr, T, d, w.dh_d};
+        BS_TRY(launch_allu_dx(ax, st));
+      }
+      // O's weight use (Wo)
+      if (l == LETTER_U) {
+        BS_TRY(planes_of(NP_RESU, io.Otok, io.c_Otok, s_O, w.pA, 3));
+        BS_TRY(Gemm(d, d, (int)Tp, Tp, Tp, dWo, d, nullptr).add(w.pA, 3, w.dhT, 3).run(w.part, w.part_cap, st));
+      } else {
+        BS_TRY(launch_planes(w.dh_d, BS_F32, T, d, d, true, w.tB, 3, Tp, 1.0f, st));
+        Gemm gw(d, d, (int)Tp, Tp, Tp, dWo, d, s_O);
+        gw.add(&w.valT_O, 1, w.tB, 3);
+        if (l == LETTER_N) {
+          BS_TRY(launch_add(io.dh, BS_F32, w.dh_d, w.dh_L, Td, st));
+          BS_TRY(launch_planes(w.dh_L, BS_F32, T, d, d, true, w.tA, 3, Tp, 1.0f, st));
+          const TrialPlaneArgs ta{io.Otok, io.c_Otok, s_O, f, T, d, Tp, io.seed, 1 * 256 + 2, k, 1, w.pA[0]};
+          BS_TRY(launch_trial_planes(ta, st));
+          gw.add(&w.pA[0], 1, w.tA, 3);
+        }
+        BS_TRY(gw.run(w.part, w.part_cap, st));
+        // the move of dO (token-major, then head-major)
+        BS_TRY(launch_planes(w.dh_d, BS_F32, T, d, d, false, w.rows3, 3, d, 1.0f, st));
+        BS_TRY(Gemm((int)T, d, d, d, d, w.dO_dt, d, nullptr).add(w.rows3, 3, &io.Wo, 1).run(nullptr, 0, st));
+        BS_TRY(launch_heads_tokens_f32(w.dO_dt, w.dO_dh, B, S, H, DH, false, st));
+      }
+      // the D use: U reads the original and dO does not move: no move downstream of it
+      if (l == LETTER_U) {
+        BS_TRY(planes_of(NP_RESU, w.u1, io.c_u1, s_u1, w.pA, 3));
+        BS_TRY(Gemm(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, nullptr).add(w.pA, 3, w.dqkvT, 3)
+                   .run(w.part, w.part_cap, st));
+        BS_TRY(launch_fill(w.delta[0], Td, 0.0f, st));
+        BS_TRY(launch_fill(w.delta[1], d, 0.0f, st));
+      } else {
+        const AlluDArgs ad{rd(io.O, io.c_O, s_O, 1 * 256 + 1), io.dOh, w.dO_dh, rows_h, w.dD};
+        BS_TRY(launch_allu_d(ad, st));
+        BS_TRY(launch_attn_split(w.dO_dh, (int)bh, S, (int)Sp, w.dOp, w.dOt, st));
+        AttnBwdArgs ba{};
+        ba.Qt = w.Qt;
+        ba.Kt = w.Kt;
+        for (int i = 0; i < 3; ++i) {
+          ba.dOp[i] = w.dOp[i];
+          ba.dOt[i] = w.dOt[i];
+        }
+        ba.Sp = (int)Sp;
+        ba.Q = io.Q;
+        ba.K = io.Kk;
+        ba.V = io.V;
+        ba.dO32 = w.dO_dh;
+        ba.m = w.m;
+        ba.l = w.l;
+        ba.D_ref = w.dD;
+        ba.S = S;
+        ba.causal = 1;
+        ba.ntrial = 1;
+        ba.scale = kAttnScale;
+        ba.dQ_ref = w.dQ_d;
+        ba.dK_ref = w.dK_d;
+        ba.dV = w.dV_d;
+        ba.n_pol = 0;
+        BS_TRY(launch_attn_bwd(ba, B, H, st));
+        BS_TRY(launch_dqkv_tokens(w.dQ_d, w.dK_d, w.dV_d, w.dqkv_d, B, S, H, DH, st));
+        // u1's weight use (Wqkv)
+        BS_TRY(launch_planes(w.dqkv_d, BS_F32, T, d3, d3, true, w.tB, 3, Tp, 1.0f, st));
+        Gemm gq(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, s_u1);
+        gq.add(&w.valT_u1, 1, w.tB, 3);
+        if (l == LETTER_N) {
+          BS_TRY(launch_add(io.dqkv, BS_F32, w.dqkv_d, w.dqkv_L, 3 * Td, st));
+          BS_TRY(launch_planes(w.dqkv_L, BS_F32, T, d3, d3, true, w.tA, 3, Tp, 1.0f, st));
+          const TrialPlaneArgs ta{w.u1, io.c_u1, s_u1, f, T, d, Tp, io.seed, 0 * 256 + 2, k, 1, w.pA[0]};
+          BS_TRY(launch_trial_planes(ta, st));
+          gq.add(&w.pA[0], 1, w.tA, 3);
+        }
+        BS_TRY(gq.run(w.part, w.part_cap, st));
+        // the move of du1, then u1's gain and normalization-input uses
+        BS_TRY(launch_planes(w.dqkv_d, BS_F32, T, d3, d3, false, w.rows3, 3, d3, 1.0f, st));
+        BS_TRY(Gemm((int)T, d, (int)d3, d3, d3, w.du1_d, d, nullptr).add(w.rows3, 3, &io.Wqkv, 1).run(nullptr, 0, st));
+        const AlluGainArgs<u16> ag{io.x, w.r1, io.gain1, rd(w.u1, io.c_u1, s_u1, 0 * 256 + 1), w.du1, w.du1_d, T, d,
+                                   w.gpart};
+        BS_TRY(launch_allu_gain(ag, st));
+        BS_TRY(launch_gain_final(w.gpart, (T + 15) / 16, d, w.delta[1], nullptr, nullptr, st));
+        const AlluDxArgs<u16> ax{io.x, w.r1, io.gain1, rd(w.u1, io.c_u1, s_u1, 0 * 256 + 3), w.du1, w.du1_d, w.dh_d,
+                                 T, d, w.delta[0]};
+        BS_TRY(launch_allu_dx(ax, st));
+      }
+      // this pass's moves: the letter's bias (U, R) or one trial of N
+      for (int i = 0; i < NCOMP; ++i) {
+        if (l == LETTER_N)
+          BS_TRY(launch_trial_accum(w.delta[i], 1, k, nc[i], w.d1[i], w.S1[i], w.S2[i], st));
+        else
+          BS_TRY(copy_f32(w.bias[l][i], w.delta[i], nc[i], st));
+      }
+    }
+  }
+  for (int i = 0; i < NCOMP; ++i) {
+    BS_TRY(launch_trial_mean(w.d1[i], w.S1[i], K, nc[i], w.bias[LETTER_N][i], st));
+    BS_TRY(launch_trial_se(w.S1[i], w.S2[i], K, nc[i], w.se_n[i], st));
+  }
+
+  // ---- every gradient's bias and se per letter, and the table ----
+  const int64_t dF = (int64_t)d * F, Fd = (int64_t)F * d;
+  BS_TRY(launch_split_cols(io.ref[G_DWG], w.ref_g, w.ref_u, d, F, st));
+  for (int l = 0; l < 3; ++l)
+    BS_TRY(launch_split_cols(io.wgu_bias + (int64_t)l * d * F2, w.wg[l], w.wu[l], d, F, st));
+  BS_TRY(launch_fill(w.nan_buf, std::max<int64_t>({Td, (int64_t)d * F2, (int64_t)d * d3}), __builtin_nanf(""),
+                     st));
+  const int64_t n_of[NGRAD] = {Td, d, (int64_t)d * d3, (int64_t)d * d, d, dF, dF, Fd};
+  const float* ref_of[NGRAD] = {io.ref[G_DX], io.ref[G_DGAIN1], io.ref[G_DWQKV], io.ref[G_DWO], io.ref[G_DGAIN2],
+                                w.ref_g, w.ref_u, io.ref[G_DWD]};
+  SumsqBatch batch{};
+  const float* const kZero = (const float*)1;
+  const float* const kNaN = (const float*)2;
+  for (int gi = 0; gi < NGRAD; ++gi)
+    for (int l = 0; l < 3; ++l) {
+      const float* bias = nullptr;
+      const float* se = l == LETTER_N ? kNaN : kZero;
+      switch (gi) {
+        case G_DX: bias = w.bias[l][0]; break;
+        case G_DGAIN1: bias = w.bias[l][1]; break;
+        case G_DWQKV: bias = w.bias[l][2]; break;
+        case G_DWO: bias = w.bias[l][3]; break;
+        case G_DGAIN2: bias = io.g2_bias + (int64_t)l * d; break;
+        case G_DWG: bias = w.wg[l]; break;
+        case G_DWU: bias = w.wu[l]; break;
+        default: bias = io.wd_bias + (int64_t)l * Fd; break;
+      }
+      if (l == LETTER_N) {
+        if (gi <= G_DWO) se = w.se_n[gi];
+        if (gi == G_DGAIN2) se = io.g2_se + (int64_t)l * d;
+      }
+      BS_TRY(copy_f32(io.bias[l][gi], bias, n_of[gi], st));
+      if (io.se[l][gi]) {
+        if (se == kZero)
+          BS_TRY(launch_fill(io.se[l][gi], n_of[gi], 0.0f, st));
+        else
+          BS_TRY(copy_f32(io.se[l][gi], se == kNaN ? w.nan_buf : se, n_of[gi], st));
+      }
+      if (io.table) {
+        double* out = io.table + ((int64_t)gi * 3 + l) * 3;
+        batch.job[batch.count++] = SumsqJob{bias, n_of[gi], out};
+        batch.job[batch.count++] = SumsqJob{ref_of[gi], n_of[gi], out + 1};
+        if (se == kZero)
+          batch.job[batch.count++] = SumsqJob{nullptr, 1, out + 2};
+        else if (se == kNaN)
+          batch.job[batch.count++] = SumsqJob{nullptr, 0, out + 2};
+        else
+          batch.job[batch.count++] = SumsqJob{se, n_of[gi], out + 2};
+      }
+    }
+  if (io.table) BS_TRY(launch_sumsq_batch(batch, w.sumsq_part, st));
+  return BS_OK;
+}
+
+}  // namespace bsp
