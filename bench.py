@@ -2,9 +2,10 @@
 
 A step is one full check of the ~390M-model decoder layer (B8 x S2048 tokens, d 1024, 16 heads
 of 64, SwiGLU F 4096, pre-norm, bf16, four E4M3 stores): the forward, the straight-through
-reference backward, and every use of every store under U, R and N with K = 16 new roundings per
-use, reduced to the per-use bias table. Inputs are resident in HBM before the timed region. The
-metric is policy-trials per second: (#policies x K) / step time.
+reference backward, every use of every store under U, R and N with K = 16 new roundings per use
+(the per-use bias table), and each letter read at every use of every store together (K backward
+passes for N). Inputs are resident in HBM before the timed region. The metric is policy-trials
+per second: (#policies x K) / step time, with 6 policies (U, R, N per use and at every use).
 
 Prints one JSON line. `roofline` is the step's dominant kernel, the bf16 MFMA contraction, timed
 live with HIP events on its launch stream (algorithmic flop per launch over the average launch
@@ -277,7 +278,7 @@ def log(msg):
 
 def cpu_baseline_decoder(cfg):
     """The plain fp64 oracle of the decoder-layer check (forward, reference backward, every use of
-    every store under U / R / N with K trials) on one sequence of S = 16 and of S = 32 tokens at the
+    every store under U / R / N with K trials, alone and all together) on one sequence of S = 16 and of S = 32 tokens at the
     layer's full widths, all host threads; the step time is extrapolated linearly in the token
     count to the benchmark's B x S tokens (its attention part grows as S^2, so the extrapolation
     favours the CPU). The same S = 16 sample is also timed on one thread."""
@@ -291,6 +292,7 @@ def cpu_baseline_decoder(cfg):
         f = decoder.forward(x.float().numpy(), pn, B=1, S=S, H=cfg["H"], seed=cfg["seed"])
         r = decoder.reference_backward(f, pn, dOut.float().numpy())
         decoder.per_use_table(f, pn, r, K=cfg["K"], seed=cfg["seed"])
+        decoder.all_uses(f, pn, dOut.float().numpy(), r, K=cfg["K"], seed=cfg["seed"])
         return time.perf_counter() - t0
 
     run(8)                                   # warm-up (first BLAS calls, page-in)
@@ -305,11 +307,11 @@ def cpu_baseline_decoder(cfg):
     T = cfg["B"] * cfg["S"]
     per_tok = max(t32 - t16, 1e-9) / 16
     full = t16 + per_tok * (T - 16)
-    pt = 3 * cfg["K"]
+    pt = 6 * cfg["K"]
     return {"value": round(pt / full, 6), "unit": "policy-trials/s", "cores": int(threads), "kind": "oracle",
             "value_1thread": round(pt / (full * t16_1 / t16), 6), "cores_1thread": 1,
-            "sample": (f"plain fp64 oracle (forward, reference backward, U/R/N at every use of the 4 stores, "
-                       f"K={cfg['K']}) on one sequence of 16 and of 32 tokens at d={cfg['d']}, H={cfg['H']}, "
+            "sample": (f"plain fp64 oracle (forward, reference backward, U/R/N at each use of the 4 stores and at "
+                       f"every use together, K={cfg['K']}) on one sequence of 16 and of 32 tokens at d={cfg['d']}, H={cfg['H']}, "
                        f"F={cfg['F']}: {t16:.1f} s and {t32:.1f} s on {threads} threads ({t16_1:.1f} s for 16 tokens "
                        f"on 1 thread); linear extrapolation to {T} tokens = {full:.0f} s per step")}
 
@@ -392,11 +394,12 @@ def main():
     log("inputs of the decoder layer (B8 S2048 d1024 H16 F4096)")
     (x, p, dOut), (B, S, H) = synth.decoder_inputs(cfg["B"], cfg["S"], cfg["d"], cfg["H"], cfg["F"], config=5)
     xd, pd, dOd = x.to(dev), {k: v.to(dev) for k, v in p.items()}, dOut.to(dev)
-    ws = bsp.decoder_layer_workspace(B, S, cfg["d"], H, cfg["F"], cfg["K"], dev)
+    ws = bsp.decoder_layer_workspace(B, S, cfg["d"], H, cfg["F"], cfg["K"], dev, all_uses=True)
+    n_pol = 6   # U, R, N at each use alone, and at every use together
 
     def step():
         return bsp.decoder_layer_policy(xd, pd, dOd, B=B, S=S, H=H, fmt="e4m3", fwd_mode=cfg["fwd_mode"], K=cfg["K"],
-                                        seed=cfg["seed"], ws=ws)
+                                        seed=cfg["seed"], all_uses=True, all_outputs=False, ws=ws)
 
     for _ in range(args.warmup):
         step()
@@ -414,7 +417,7 @@ def main():
     flop, xflop = bsp.profile_work("gemm")
     bsp.profile_enable(False)
     ms_per_step = elapsed / args.steps * 1e3
-    value = 3 * cfg["K"] * args.steps / elapsed
+    value = n_pol * cfg["K"] * args.steps / elapsed
 
     # dominant kernel: the bf16 MFMA contraction (every contraction launch of the step)
     g_ms, g_n = prof["gemm"]
@@ -435,8 +438,8 @@ def main():
                                  "for 1e-5 parity; executed flop counts every term product"}
     extra = {"kernel_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in prof.items()},
              "gemm_TFLOP_per_step": round(flop / args.steps / 1e12, 4),
-             "work": "forward, reference backward, and U/R/N at the 10 uses of the 4 stores, K = 16 new roundings "
-                     "per use"}
+             "work": "forward, reference backward, U/R/N at the 10 uses of the 4 stores (K = 16 new roundings per "
+                     "use), and U/R/N at every use together (K = 16 backward passes for N)"}
     del xd, pd, dOd, ws
     torch.cuda.empty_cache()
     if not args.headline_only:
@@ -454,9 +457,9 @@ def main():
             "data": "synthetic",
             "config": {"workload": "decoder_layer_b8_s2048_d1024_h16_f4096: one pre-norm decoder layer (B8 x S2048, "
                                    "d 1024, 16 heads of 64, SwiGLU F 4096, bf16, N(0, 0.02^2) weights), four E4M3 RNE "
-                                   "stores, U/R/N at every use, K=16",
+                                   "stores, U/R/N at each use and at every use together, K=16",
                        "B": B, "S": S, "d": cfg["d"], "H": H, "F": cfg["F"], "K": cfg["K"],
-                       "policies": ["U", "R", "N"]},
+                       "policies": ["U", "R", "N", "U everywhere", "R everywhere", "N everywhere"]},
             "roofline": roofline, "extra": extra}
     if not args.no_cpu_baseline and not args.headline_only:
         log("cpu baseline (the plain oracle on a bounded sample)")
