@@ -35,7 +35,9 @@ SHARED, PER_USE = "shared", "per_use"
 
 def check(X, W, dY, *, fmt=fp8.E5M2, sharings=(SHARED, PER_USE), K=16, seed=0, store_id=0,
           A=None, B=None, dx_rows=None, dw_rows=None, dw_cols=None):
-    """dx_rows selects rows of dX; dw_rows x dw_cols selects entries of dW (None: all)."""
+    """dx_rows selects rows of dX; dw_rows x dw_cols selects entries of dW (None: all). With a
+    selection, the probes must vanish outside it (A outside the rows of dX, B outside the entries
+    of dW), so that the coupling statistic needs the selected outputs only."""
     X64 = np.asarray(X, dtype=np.float32).astype(np.float64)
     W64 = np.asarray(W, dtype=np.float32).astype(np.float64)
     dY32 = np.asarray(dY, dtype=np.float32)
@@ -52,6 +54,15 @@ def check(X, W, dY, *, fmt=fp8.E5M2, sharings=(SHARED, PER_USE), K=16, seed=0, s
     elem = np.arange(dY32.size, dtype=np.uint64).reshape(dY32.shape)
     out = {"scale": s, "dX_ref": dY64[xr] @ W64.T, "dW_ref": X64[:, wr].T @ dY64[:, wc]}
     base = store_id * 256
+    if A is not None and not full:
+        A = np.asarray(A, dtype=np.float64)
+        B = np.asarray(B, dtype=np.float64)
+        inside_a = np.zeros(A.shape, dtype=bool)
+        inside_a[xr] = True
+        inside_b = np.zeros(B.shape, dtype=bool)
+        inside_b[np.ix_(wr, wc)] = True
+        if np.any(A[~inside_a] != 0) or np.any(B[~inside_b] != 0):
+            raise ValueError("probes must vanish outside the selected outputs")
     for sh in sharings:
         use1, use2 = base + 1, (base + 1 if sh == SHARED else base + 2)
         tx, tw, kap = [], [], []
@@ -66,6 +77,9 @@ def check(X, W, dY, *, fmt=fp8.E5M2, sharings=(SHARED, PER_USE), K=16, seed=0, s
                 g1 = fresh_values(y[xr], elem[xr], fmt, s, seed, k, use1)
                 g2 = fresh_values(y[:, wc], elem[:, wc], fmt, s, seed, k, use2)
                 dXk, dWk = g1 @ W64.T, X64[:, wr].T @ g2
+                if A is not None:
+                    kap.append(np.sum((dXk - out["dX_ref"]) * A[xr]) *
+                               np.sum((dWk - out["dW_ref"]) * B[np.ix_(wr, wc)]))
             tx.append(dXk)
             tw.append(dWk)
         out[sh] = {"dX": trial_stats(np.stack(tx), out["dX_ref"]),

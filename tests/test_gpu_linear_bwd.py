@@ -12,8 +12,10 @@ TOL = 1e-5
 
 
 def run_both(lib, M, k, n, K, sharings=("shared", "per_use"), seed=5, coupling=True, oracle_kw=None, config=40,
-             fmt="e5m2"):
+             fmt="e5m2", probes=None):
     X, W, dY, A, B = synth.linear_bwd_inputs(M, k, n, torch.bfloat16, config)
+    if probes is not None:
+        A, B = probes
     print(f"[linear_bwd] M={M} k={k} n={n} K={K} {sharings} coupling={coupling} fmt={fmt}", flush=True)
     out = lib.linear_bwd_policy(X.cuda(), W.cuda(), dY.cuda(), fmt=fmt, sharings=sharings, K=K, seed=seed, store_id=2,
                                 probeA=A.cuda() if coupling else None, probeB=B.cuda() if coupling else None)
@@ -58,12 +60,20 @@ def test_e4m3_gradient_store_and_no_coupling(lib):
 
 @pytest.mark.slow
 def test_config4_full_size_sampled(lib):
+    """The 16384 x 2048 x 8192 launch: sampled rows of dX and entries of dW, and the coupling
+    statistic kappa with probes supported on exactly those outputs (A on the sampled rows, B on the
+    sampled entries), so the oracle's plain K trials over the samples give kappa exactly."""
     cfg = synth.CONFIGS[4]
     M, k, n = cfg["M"], cfg["k"], cfg["n"]
     rng = np.random.default_rng(4)
     xr = np.sort(rng.choice(M, 6, replace=False))
     wr = np.sort(rng.choice(k, 3, replace=False))
     wc = np.sort(rng.choice(n, 5, replace=False))
-    out, ref = run_both(lib, M, k, n, cfg["K"], sharings=cfg["sharings"], seed=cfg["seed"], coupling=False,
-                        oracle_kw=dict(dx_rows=xr, dw_rows=wr, dw_cols=wc), config=4)
-    compare(out, ref, cfg["sharings"], M, k, n, xr=xr, wr=wr, wc=wc, coupling=False)
+    g = torch.Generator().manual_seed(44)
+    A = torch.zeros(M, k)
+    A[xr] = torch.randn(len(xr), k, generator=g)
+    B = torch.zeros(k, n)
+    B[np.ix_(wr, wc)] = torch.randn(len(wr), len(wc), generator=g)
+    out, ref = run_both(lib, M, k, n, cfg["K"], sharings=cfg["sharings"], seed=cfg["seed"], coupling=True,
+                        oracle_kw=dict(dx_rows=xr, dw_rows=wr, dw_cols=wc), config=4, probes=(A, B))
+    compare(out, ref, cfg["sharings"], M, k, n, xr=xr, wr=wr, wc=wc, coupling=True)

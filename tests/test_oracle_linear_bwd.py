@@ -8,6 +8,7 @@ import itertools
 from fractions import Fraction as Fr
 
 import numpy as np
+import pytest
 
 from oracle import fp8, linear_bwd, qround
 
@@ -99,3 +100,25 @@ def test_sampled_entries_equal_full():
     for sh in ("shared", "per_use"):
         assert np.allclose(part[sh]["dX"][0], full[sh]["dX"][0][[1, 4]], rtol=1e-13, atol=0)
         assert np.allclose(part[sh]["dW"][0], full[sh]["dW"][0][np.ix_([0, 3], [2, 6])], rtol=1e-13, atol=0)
+
+
+def test_coupling_on_selected_outputs_equals_the_full_statistic():
+    """With probes that vanish outside the selected rows of dX and entries of dW, the selected
+    outputs give the same coupling statistic, trial by trial, as the full tensors; probes that do
+    not vanish there are refused."""
+    rng = np.random.default_rng(12)
+    M, k, n = 40, 16, 24
+    X, W = rng.normal(size=(M, k)), rng.normal(size=(k, n)) / 4
+    dY = (rng.normal(size=(M, n)) * 0.1).astype(np.float32)
+    xr, wr, wc = np.array([3, 17, 39]), np.array([0, 5]), np.array([2, 11, 23])
+    A = np.zeros((M, k))
+    A[xr] = rng.normal(size=(len(xr), k))
+    B = np.zeros((k, n))
+    B[np.ix_(wr, wc)] = rng.normal(size=(len(wr), len(wc)))
+    full = linear_bwd.check(X, W, dY, K=6, seed=4, A=A, B=B)
+    part = linear_bwd.check(X, W, dY, K=6, seed=4, A=A, B=B, dx_rows=xr, dw_rows=wr, dw_cols=wc)
+    for sh in ("shared", "per_use"):
+        np.testing.assert_allclose(part[sh]["kappa_trials"], full[sh]["kappa_trials"], rtol=1e-12, atol=1e-18)
+    A[0, 0] = 1.0
+    with pytest.raises(ValueError):
+        linear_bwd.check(X, W, dY, K=2, seed=4, A=A, B=B, dx_rows=xr, dw_rows=wr, dw_cols=wc)
