@@ -390,12 +390,15 @@ bs_status bs_te_attn_bwd(const void* Q, const void* Kt, const void* V, const flo
  *
  *   X [M,k] dt, W [k,n] dt, dY [M,n] dt; dt bf16; k and n multiples of 8; M >= 0.
  *   sharing (host) [n_pol] in {0, 1}, n_pol in [1, 4]; K in [1, 4096].
- *   dX_ref [M,k], dW_ref [k,n] fp32; estimates dX [n_pol][M*k], dW [n_pol][k*n]
- *   (se must be NULL: BS_EUNSUPPORTED otherwise).
+ *   dX_ref [M,k], dW_ref [k,n] fp32; estimates dX [n_pol][M*k], dW [n_pol][k*n]. The means
+ *   collapse the K trials by linearity; a non-NULL dX.se or dW.se runs the per-trial path (App.
+ *   C.4's sample SD over trials / sqrt(K)): trial k's residual fresh_k - dY moves dX and dW by K
+ *   per-trial contractions (2 M k n flop each per gradient, three bf16 terms), and its
+ *   workspace is bs_linear_bwd_workspace_size(..., want_se = 1).
  *   probeA [M,k], probeB [k,n] fp32 and coupling [n_pol] fp64: all NULL or all set.
  *   dY_scale [1] fp32 out.
  * ---------------------------------------------------------------------------------- */
-size_t bs_linear_bwd_workspace_size(int64_t M, int64_t k, int64_t n, int n_pol, int K);
+size_t bs_linear_bwd_workspace_size(int64_t M, int64_t k, int64_t n, int n_pol, int K, int want_se);
 bs_status bs_linear_bwd_policy(const void* X, const void* W, const void* dY, bs_dtype dt, int64_t M,
                                int64_t k, int64_t n, bs_fp8 fmt, const int* sharing, int n_pol, int K,
                                uint64_t seed, uint32_t store_id, float* dX_ref, float* dW_ref, bs_est dX,

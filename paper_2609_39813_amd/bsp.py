@@ -98,7 +98,7 @@ _grid_ws = _sig("bs_rmsnorm_linear_grid_workspace_size", _sz, [_i64, _i64, _i64]
 _grid = _sig("bs_rmsnorm_linear_grid_fwd_bwd", _int,
              [_vp, _vp, _vp, _vp, _int, _i64, _i64, _i64, _f32, _int, ctypes.POINTER(GridPolicy), _int, _int, _u64,
               _u32, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, _vp, _vp, _sz, _vp])
-_lin_ws = _sig("bs_linear_bwd_workspace_size", _sz, [_i64, _i64, _i64, _int, _int])
+_lin_ws = _sig("bs_linear_bwd_workspace_size", _sz, [_i64, _i64, _i64, _int, _int, _int])
 _lin = _sig("bs_linear_bwd_policy", _int,
             [_vp, _vp, _vp, _int, _i64, _i64, _i64, _int, ctypes.POINTER(_int), _int, _int, _u64, _u32, _vp, _vp,
              Est, Est, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp])
@@ -548,8 +548,9 @@ def te_delayed_scales(amax, history, step, scales):
 
 
 def linear_bwd_policy(X, W, dY, *, fmt="e5m2", sharings=("shared", "per_use"), K=16, seed=0, store_id=0,
-                      probeA=None, probeB=None, ws=None):
-    """Linear backward with an FP8-rounded incoming gradient (bs_linear_bwd_policy)."""
+                      probeA=None, probeB=None, want_se=False, ws=None):
+    """Linear backward with an FP8-rounded incoming gradient (bs_linear_bwd_policy). want_se: the
+    se of dX and dW over trials (the per-trial path: K per-trial contractions per gradient)."""
     _dev_check(X, W, dY, probeA, probeB)
     M, k = X.shape
     n = W.shape[1]
@@ -560,10 +561,10 @@ def linear_bwd_policy(X, W, dY, *, fmt="e5m2", sharings=("shared", "per_use"), K
            "dY_scale": torch.empty(1, dtype=torch.float32, device=dev),
            "coupling": torch.empty(len(sharings), dtype=torch.float64, device=dev) if probeA is not None else None,
            "diag": new_diag(dev)}
-    ex, cx = _est(len(sharings), M * k, dev, False)
-    ew, cw = _est(len(sharings), k * n, dev, False)
+    ex, cx = _est(len(sharings), M * k, dev, want_se)
+    ew, cw = _est(len(sharings), k * n, dev, want_se)
     if ws is None:
-        ws = _workspace(_lin_ws(M, k, n, len(sharings), K), dev)
+        ws = _workspace(_lin_ws(M, k, n, len(sharings), K, int(want_se)), dev)
     _check(_lin(_p(X), _p(W), _p(dY), _dt(X), M, k, n, _FMT[fmt], sh, len(sharings), K, seed, store_id,
                 _p(out["dX_ref"]), _p(out["dW_ref"]), cx, cw, _p(probeA), _p(probeB), _p(out["coupling"]),
                 _p(out["dY_scale"]), _p(out["diag"]), _p(ws), ws.numel(), _stream()), "bs_linear_bwd_policy")
@@ -571,8 +572,8 @@ def linear_bwd_policy(X, W, dY, *, fmt="e5m2", sharings=("shared", "per_use"), K
     return out
 
 
-def linear_bwd_workspace(M, k, n, n_pol, K, device):
-    return _workspace(_lin_ws(M, k, n, n_pol, K), device)
+def linear_bwd_workspace(M, k, n, n_pol, K, device, want_se=False):
+    return _workspace(_lin_ws(M, k, n, n_pol, K, int(want_se)), device)
 
 
 LAYER_ROWS = (("u1", "gain", "dgain"), ("u1", "weight", "dW"), ("u1", "norm_input", "dX"), ("O", "D", "dQ"),

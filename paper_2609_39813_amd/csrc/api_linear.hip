@@ -2,6 +2,7 @@
 #include "bsp_kernels.h"
 #include "k_combine.h"
 #include "k_linear.h"
+#include "k_norm.h"
 
 using namespace bsp;
 
@@ -13,13 +14,16 @@ using namespace bsp;
 
 namespace {
 struct LinWs {
-  u16 *xT, *dyT, *e1r[3], *e1c[3], *e2c[3], *wT[3], *pa[3], *pbT[3];
+  u16 *xT, *dyT, *e1r[3], *e1c[3], *e2c[3], *wT[3], *pa[3], *pbT[3], *tc[3];
+  float *tdx, *tdw, *d1x, *d1w[2];
+  double *S1x, *S2x, *S1w[2], *S2w[2];
   u16 *cnt1, *cnt2;
   float *AW, *XB, *bx[2], *bw[2];
   double *part1, *part2, *fixpart, *fixed;
   float* scale_tmp;
 };
-LinWs carve_lin(Carver& c, int64_t M, int64_t k, int64_t n, bool any_shared, bool any_per_use, bool coupling) {
+LinWs carve_lin(Carver& c, int64_t M, int64_t k, int64_t n, bool any_shared, bool any_per_use, bool coupling,
+                bool want_se) {
   LinWs w{};
   const int64_t Mp = round_up(M > 0 ? M : 1, 64);
   w.xT = c.take<u16>(k * Mp);
@@ -42,17 +46,30 @@ LinWs carve_lin(Carver& c, int64_t M, int64_t k, int64_t n, bool any_shared, boo
     w.AW = c.take<float>(M * n);
     w.XB = c.take<float>(M * n);
   }
+  if (want_se) {  // the per-trial path: one trial's residual planes, moves and shifted sums
+    for (int i = 0; i < 3; ++i) w.tc[i] = c.take<u16>(n * Mp);
+    w.tdx = c.take<float>(M * k);
+    w.tdw = c.take<float>(k * n);
+    w.d1x = c.take<float>(M * k);
+    w.S1x = c.take<double>(M * k);
+    w.S2x = c.take<double>(M * k);
+    for (int i = 0; i < 2; ++i) {
+      w.d1w[i] = c.take<float>(k * n);
+      w.S1w[i] = c.take<double>(k * n);
+      w.S2w[i] = c.take<double>(k * n);
+    }
+  }
   return w;
 }
 }  // namespace
 
 extern "C" {
 
-size_t bs_linear_bwd_workspace_size(int64_t M, int64_t k, int64_t n, int n_pol, int K) {
+size_t bs_linear_bwd_workspace_size(int64_t M, int64_t k, int64_t n, int n_pol, int K, int want_se) {
   (void)n_pol;
   if (M < 0 || k < 0 || n < 0 || K < 1) return 0;
   Carver c;
-  carve_lin(c, M, k, n, true, true, true);
+  carve_lin(c, M, k, n, true, true, true, want_se != 0);
   const int64_t nblk = fresh_count_blocks(M, n);
   c.take<double>((int64_t)K * 2 * nblk);
   c.take<double>((int64_t)K * 2 * nblk);
@@ -71,7 +88,7 @@ bs_status bs_linear_bwd_policy(const void* X, const void* W, const void* dY, bs_
   if (dt != BS_BF16) return BS_EDTYPE;
   if ((fmt != BS_E4M3 && fmt != BS_E5M2) || n_pol < 1 || n_pol > 2 * 2 || K < 1 || K > 4096) return BS_EINVAL;
   if (k < 8 || (k & 7) || n < 8 || (n & 7) || M > 0x7FFFFFFF || k > 0x7FFFFFFF || n > 0x7FFFFFFF) return BS_ESHAPE;
-  if (dX.se || dW.se) return BS_EUNSUPPORTED;
+  const bool want_se = dX.se || dW.se;
   const bool coupling_on = coupling != nullptr;
   if (coupling_on != (probeA != nullptr) || coupling_on != (probeB != nullptr)) return BS_EINVAL;
   bool any_shared = false, any_per_use = false;
@@ -82,7 +99,7 @@ bs_status bs_linear_bwd_policy(const void* X, const void* W, const void* dY, bs_
   }
   const int64_t nblk = fresh_count_blocks(M, n);
   auto carve_all = [&](Carver& c, LinWs& w) {
-    w = carve_lin(c, M, k, n, any_shared, any_per_use, coupling_on);
+    w = carve_lin(c, M, k, n, any_shared, any_per_use, coupling_on, want_se);
     if (coupling_on) {
       w.part1 = c.take<double>((int64_t)K * 2 * nblk);
       if (any_per_use) w.part2 = c.take<double>((int64_t)K * 2 * nblk);
@@ -189,6 +206,41 @@ bs_status bs_linear_bwd_policy(const void* X, const void* W, const void* dY, bs_
     BS_TRY(launch_combine_multi(cx, mk, st));
     BS_TRY(launch_combine_multi(cw, kn, st));
   }
+  // se over trials (App. C.4), the per-trial path: trial k's residual fresh_k - dY moves dX and dW
+  // by contractions of its planes; shifted fp64 sums over trials. dX reads use +1 under both
+  // sharings, dW use +1 (shared) or +2 (per use).
+  if (want_se && M > 0) {
+    for (int kk = 1; kk <= K; ++kk) {
+      for (int u = 0; u < 2; ++u) {
+        if (u == 1 && !any_per_use) continue;
+        FreshArgs<u16> ft{(const u16*)dY, M, n, f, dY_scale, seed, base + 1 + u, 1, u == 0 ? w.cnt1 : w.cnt2,
+                          nullptr, nullptr, nullptr};
+        ft.trial0 = kk;
+        BS_TRY(launch_fresh_count_t(ft, FC_COUNT, st));
+        const bool need_w = u == 1 || any_shared;
+        ResidArgs rt{(const u16*)dY, u == 0 ? w.cnt1 : w.cnt2, dY_scale, 1, f, M, n,
+                     {u == 0 ? w.e1r[0] : nullptr, w.e1r[1], w.e1r[2]},
+                     {need_w ? w.tc[0] : nullptr, w.tc[1], w.tc[2]}, Mp};
+        BS_TRY(launch_resid_planes(rt, st));
+        if (u == 0 && dX.se) {
+          BS_TRY(gemm((int)M, (int)k, (int)n, n, n, w.e1r, 3, &Wp, 1, w.tdx, 1.0f));
+          BS_TRY(launch_trial_accum(w.tdx, 1, kk, mk, w.d1x, w.S1x, w.S2x, st));
+        }
+        if (need_w && dW.se) {
+          BS_TRY(gemm((int)k, (int)n, (int)Mp, Mp, Mp, &w.xT, 1, w.tc, 3, w.tdw, 1.0f));
+          BS_TRY(launch_trial_accum(w.tdw, 1, kk, kn, w.d1w[u], w.S1w[u], w.S2w[u], st));
+        }
+      }
+    }
+    for (int i = 0; i < n_pol; ++i) {
+      if (dX.se) BS_TRY(launch_trial_se(w.S1x, w.S2x, K, mk, dX.se + i * mk, st));
+      if (dW.se) BS_TRY(launch_trial_se(w.S1w[sharing[i]], w.S2w[sharing[i]], K, kn, dW.se + i * kn, st));
+    }
+  } else if (want_se) {
+    for (int i = 0; i < n_pol; ++i)
+      if (dW.se) BS_TRY(launch_fill2d(dW.se + i * kn, 1, kn, kn, 0.0f, st));
+  }
+
   for (int i = 0; i < n_pol; ++i) {
     const int sh = sharing[i];
     if (coupling_on) {

@@ -79,6 +79,7 @@ struct FreshArgs {
   const float* w2;     // [T][d] second weight (FC_BLOCKSUM, nullable)
   double* partial;     // FC_BLOCKSUM: [K][2][nblocks]
   float* colsum = nullptr;  // FC_COLSUM: [K][ceil(T/32)][d]
+  int trial0 = 1;      // the K trials are trial0 .. trial0 + K - 1
 };
 template <typename X>
 bs_status launch_fresh_count_t(const FreshArgs<X>& a, int mode, hipStream_t st);

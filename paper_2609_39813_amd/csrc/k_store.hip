@@ -291,7 +291,7 @@ __device__ __forceinline__ void fresh_count_body(const FreshArgs<X>& a) {
       for (int r = 0; r < RPT; ++r) {
         const int64_t t = t0 + ty + 4 * r;
         const uint64_t g = (uint64_t)((t * a.d + j0) >> 2);
-        const Philox4 p = philox_group(a.seed, g, (uint32_t)k, a.use);
+        const Philox4 p = philox_group(a.seed, g, (uint32_t)(k - 1 + a.trial0), a.use);
         const uint32_t R[4] = {p.w0, p.w1, p.w2, p.w3};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {

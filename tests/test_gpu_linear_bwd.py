@@ -12,13 +12,14 @@ TOL = 1e-5
 
 
 def run_both(lib, M, k, n, K, sharings=("shared", "per_use"), seed=5, coupling=True, oracle_kw=None, config=40,
-             fmt="e5m2", probes=None):
+             fmt="e5m2", probes=None, want_se=False):
     X, W, dY, A, B = synth.linear_bwd_inputs(M, k, n, torch.bfloat16, config)
     if probes is not None:
         A, B = probes
     print(f"[linear_bwd] M={M} k={k} n={n} K={K} {sharings} coupling={coupling} fmt={fmt}", flush=True)
     out = lib.linear_bwd_policy(X.cuda(), W.cuda(), dY.cuda(), fmt=fmt, sharings=sharings, K=K, seed=seed, store_id=2,
-                                probeA=A.cuda() if coupling else None, probeB=B.cuda() if coupling else None)
+                                probeA=A.cuda() if coupling else None, probeB=B.cuda() if coupling else None,
+                                want_se=want_se)
     torch.cuda.synchronize()
     ref = linear_bwd.check(X.float().numpy(), W.float().numpy(), dY.float().numpy(),
                            fmt=fp8.E5M2 if fmt == "e5m2" else fp8.E4M3, sharings=sharings, K=K, seed=seed,
@@ -41,6 +42,9 @@ def compare(out, ref, sharings, M, k, n, xr=None, wr=None, wc=None, coupling=Tru
             assert_rel(m, om, TOL, f"{sh} {name} mean")
             if not assert_zero_where_oracle_zero(b, ob, f"{sh} {name} bias"):
                 assert_rel(b, ob, TOL, f"{sh} {name} bias")
+            if out[name]["se"] is not None:
+                se = sel(to_np(out[name]["se"][i]).reshape(shape))
+                assert_rel(se, ref[sh][name][2], TOL, f"{sh} {name} se")
         if coupling:
             g = float(out["coupling"][i].cpu())
             r = ref[sh]["kappa"]
@@ -49,8 +53,16 @@ def compare(out, ref, sharings, M, k, n, xr=None, wr=None, wc=None, coupling=Tru
 
 @pytest.mark.parametrize("M,k,n", [(200, 72, 136), (64, 64, 64), (1, 8, 8)])
 def test_ragged_shared_and_per_use_with_coupling(lib, M, k, n):
-    out, ref = run_both(lib, M, k, n, 12, seed=M)
+    out, ref = run_both(lib, M, k, n, 12, seed=M, want_se=M == 200)
     compare(out, ref, ("shared", "per_use"), M, k, n)
+
+
+def test_se_over_trials_per_use_only_and_one_trial(lib):
+    """The per-trial path: se of dX and dW for a per-use policy alone (its dW series is use +2),
+    and K = 1 (se 0)."""
+    for K in (9, 1):
+        out, ref = run_both(lib, 130, 64, 96, K, sharings=("per_use",), seed=7 + K, want_se=True)
+        compare(out, ref, ("per_use",), 130, 64, 96)
 
 
 def test_e4m3_gradient_store_and_no_coupling(lib):
@@ -75,5 +87,5 @@ def test_config4_full_size_sampled(lib):
     B = torch.zeros(k, n)
     B[np.ix_(wr, wc)] = torch.randn(len(wr), len(wc), generator=g)
     out, ref = run_both(lib, M, k, n, cfg["K"], sharings=cfg["sharings"], seed=cfg["seed"], coupling=True,
-                        oracle_kw=dict(dx_rows=xr, dw_rows=wr, dw_cols=wc), config=4, probes=(A, B))
+                        oracle_kw=dict(dx_rows=xr, dw_rows=wr, dw_cols=wc), config=4, probes=(A, B), want_se=True)
     compare(out, ref, cfg["sharings"], M, k, n, xr=xr, wr=wr, wc=wc, coupling=True)
