@@ -199,10 +199,13 @@ bs_status bs_rmsnorm_linear_grid_fwd_bwd(const void* X, const float* gain, const
  *   forward (written to O_out if O_out != NULL).
  *   d_pol (host) [n_pol] in {U, R, N}, n_pol in [1, 8]; K in [1, 4096].
  *   O_codes [B,H,S,dh] uint8; O_scale [1]; dQ_ref, dK_ref, dV [B,H,S,dh] fp32;
- *   D_ref [B,H,S] fp32 (nullable); estimates dQ, dK [n_pol][B*H*S*dh]
- *   (dK.se must be NULL: BS_EUNSUPPORTED otherwise).
+ *   D_ref [B,H,S] fp32 (nullable); estimates dQ, dK [n_pol][B*H*S*dh]. dQ's se under N is
+ *   exact from the trial SD of the rows' dD (dQ moves by -c dD_k P K, row-scaled); a non-NULL
+ *   dK.se runs the per-trial path: trial k's move -c (P dD_k)^T Q by one key-major pass per
+ *   trial, shifted fp64 sums (App. C.4), with workspace
+ *   bs_attn_workspace_size(..., want_dk_se = 1); 0 for U and R.
  * ---------------------------------------------------------------------------------- */
-size_t bs_attn_workspace_size(int B, int H, int S, int dh, int n_pol, int K);
+size_t bs_attn_workspace_size(int B, int H, int S, int dh, int n_pol, int K, int want_dk_se);
 bs_status bs_attn_bwd_policy(const void* Q, const void* Kt, const void* V, const void* dO, bs_dtype dO_type,
                              int B, int H, int S, int dh, int causal, float softmax_scale, const float* O, bs_fp8 fmt,
                              bs_round fwd_mode, const bs_read* d_pol, int n_pol, int K, uint64_t seed,
@@ -232,7 +235,7 @@ bs_status bs_attn_bwd_policy(const void* Q, const void* Kt, const void* V, const
  *
  *   Q, Kt, V, dO bf16 [B,H,S,dh], dh == 64; O, O_out, D_ref as bs_attn_bwd_policy; O_scale [1].
  *   d_pol (host) [n_pol] in {U, R, N}, n_pol in [1, 8]; K in [1, 4096].
- *   Workspace: bs_attn_workspace_size(B, H, S, dh, n_pol, K).
+ *   Workspace: bs_attn_workspace_size(B, H, S, dh, n_pol, K, 0).
  * Returns BS_EINVAL for a NULL dO or a NaN beta; otherwise as bs_attn_bwd_policy.
  * ---------------------------------------------------------------------------------- */
 bs_status bs_attn_level2_policy(const void* Q, const void* Kt, const void* V, const void* dO, int B, int H, int S,

@@ -59,7 +59,7 @@ _norm_ws = _sig("bs_rmsnorm_linear_workspace_size", _sz, [_i64, _i64, _i64, _int
 _norm = _sig("bs_rmsnorm_linear_fwd_bwd", _int,
              [_vp, _vp, _vp, _vp, _int, _i64, _i64, _i64, _f32, _int, _int, ctypes.POINTER(NormPolicy), _int, _int,
               _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, Est, _vp, _vp, _sz, _vp])
-_attn_ws = _sig("bs_attn_workspace_size", _sz, [_int, _int, _int, _int, _int, _int])
+_attn_ws = _sig("bs_attn_workspace_size", _sz, [_int, _int, _int, _int, _int, _int, _int])
 _attn = _sig("bs_attn_bwd_policy", _int,
              [_vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _int, _f32, _vp, _int, _int, ctypes.POINTER(_int), _int,
               _int, _u64, _u32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, Est, Est, _vp, _vp, _sz, _vp])
@@ -364,8 +364,10 @@ def rmsnorm_linear_workspace(T, d, n, n_pol, K, device):
 
 
 def attn_bwd_policy(Q, Kt, V, dO, *, causal=True, scale=None, O=None, fmt="e4m3", fwd_mode="sr",
-                    policies=("U", "R", "N"), K=32, seed=0, store_id=0, want_o=True, want_se=True, ws=None):
-    """Attention backward with D read from each policy's copy of O (bs_attn_bwd_policy)."""
+                    policies=("U", "R", "N"), K=32, seed=0, store_id=0, want_o=True, want_se=True, want_dk_se=False,
+                    ws=None):
+    """Attention backward with D read from each policy's copy of O (bs_attn_bwd_policy).
+    want_dk_se: also dK's se (the per-trial path: one key-major pass per trial under N)."""
     _dev_check(Q, Kt, V, dO, O)
     B, H, S, dh = Q.shape
     dev = Q.device
@@ -382,9 +384,9 @@ def attn_bwd_policy(Q, Kt, V, dO, *, causal=True, scale=None, O=None, fmt="e4m3"
            "diag": new_diag(dev)}
     numel = B * H * S * dh
     eq, cq = _est(len(policies), numel, dev, want_se)
-    ek, ck = _est(len(policies), numel, dev, False)
+    ek, ck = _est(len(policies), numel, dev, want_dk_se)
     if ws is None:
-        ws = _workspace(_attn_ws(B, H, S, dh, len(policies), K), dev)
+        ws = _workspace(_attn_ws(B, H, S, dh, len(policies), K, int(want_dk_se)), dev)
     _check(_attn(_p(Q), _p(Kt), _p(V), _p(dO), F32 if dO is not None and dO.dtype == torch.float32 else BF16,
                  B, H, S, dh, int(causal), c, _p(O), _FMT[fmt], _MODE[fwd_mode], pol,
                  len(policies), K, seed, store_id, _p(out["O"]), _p(out["O_codes"]), _p(out["O_scale"]),
@@ -418,7 +420,7 @@ def attn_level2_policy(Q, Kt, V, dO, *, causal=True, scale=None, O=None, fmt="e4
     eq, cq = _est(len(policies), numel, dev, False)
     ek, ck = _est(len(policies), numel, dev, False)
     if ws is None:
-        ws = _workspace(_attn_ws(B, H, S, dh, len(policies), K), dev)
+        ws = _workspace(_attn_ws(B, H, S, dh, len(policies), K, 0), dev)
     _check(_attn2(_p(Q), _p(Kt), _p(V), _p(dO), B, H, S, dh, int(causal), c, _p(O), _FMT[fmt], _MODE[fwd_mode], beta,
                   pol, len(policies), K, seed, store_id, _p(out["O"]), _p(out["O_scale"]), _p(out["dO_mean"]),
                   _p(out["dQ_ref"]), _p(out["dK_ref"]), _p(out["dV"]), _p(out["D_ref"]), cq, ck, _p(out["d_use"]),
@@ -447,8 +449,8 @@ def logsoftmax_reuse_check(logits, target, *, eps=0.1, K=4096, seed=0, store_id=
     return stats
 
 
-def attn_workspace(B, H, S, dh, n_pol, K, device):
-    return _workspace(_attn_ws(B, H, S, dh, n_pol, K), device)
+def attn_workspace(B, H, S, dh, n_pol, K, device, want_dk_se=False):
+    return _workspace(_attn_ws(B, H, S, dh, n_pol, K, int(want_dk_se)), device)
 
 
 def parse_pstore_policy(code):

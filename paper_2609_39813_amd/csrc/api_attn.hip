@@ -5,10 +5,9 @@ using namespace bsp;
 
 extern "C" {
 
-size_t bs_attn_workspace_size(int B, int H, int S, int dh, int n_pol, int K) {
+size_t bs_attn_workspace_size(int B, int H, int S, int dh, int n_pol, int K, int want_dk_se) {
   (void)n_pol;
-  (void)K;
-  return attn_ws_size(B, H, S, dh);
+  return attn_ws_size(B, H, S, dh, K, want_dk_se != 0);
 }
 
 bs_status bs_attn_bwd_policy(const void* Q, const void* Kt, const void* V, const void* dO, bs_dtype dO_type, int B,

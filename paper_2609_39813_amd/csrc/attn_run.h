@@ -32,7 +32,8 @@ struct AttnIO {
   float* dO_mean = nullptr;
 };
 
-size_t attn_ws_size(int B, int H, int S, int dh);
+// K and dk_se size the per-trial path of dK's se (K trials of the key-major pass under N)
+size_t attn_ws_size(int B, int H, int S, int dh, int K = 1, bool dk_se = false);
 bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st);
 
 }  // namespace bsp

@@ -2,6 +2,7 @@
 // O, the D variants of every policy, and the two-pass multi-D backward.
 #include "attn_run.h"
 #include "k_attn.h"
+#include "k_norm.h"
 
 #define BS_TRY(x)               \
   do {                          \
@@ -17,10 +18,18 @@ struct AttnWs {
   u16 *Vt, *Qt, *Kt, *dOp[3], *dOt[3];
   float *dO_mean, *stat;   // level 2: mean incoming gradient; split of R and N [2][4][rows]
   uint8_t* codes;          // level 2: the trial-0 store when the caller takes none
+  float *dD_tr, *tdk, *d1, *sek, *dK_s, *dV_s;  // dK's se: per-trial dD, one trial's dK move, shift, scratch
+  double *S1, *S2;
 };
 AttnWs carve_attn(Carver& c, int64_t rows, int64_t numel, bool need_o, bool need_dref, int64_t bh = 0, int64_t Sp = 0,
-                  int ndo = 0, bool level2 = false) {
+                  int ndo = 0, bool level2 = false, int K = 0) {
   AttnWs w{};
+  if (K > 0) {
+    w.dD_tr = c.take<float>((int64_t)K * rows);
+    for (float** p : {&w.tdk, &w.d1, &w.sek, &w.dK_s, &w.dV_s}) *p = c.take<float>(numel);
+    w.S1 = c.take<double>(numel);
+    w.S2 = c.take<double>(numel);
+  }
   if (level2) {
     w.dO_mean = c.take<float>(numel);
     w.stat = c.take<float>(8 * rows);
@@ -45,11 +54,11 @@ AttnWs carve_attn(Carver& c, int64_t rows, int64_t numel, bool need_o, bool need
 }
 }  // namespace
 
-size_t attn_ws_size(int B, int H, int S, int dh) {
-  if (B < 0 || H < 0 || S < 0 || dh < 0) return 0;
+size_t attn_ws_size(int B, int H, int S, int dh, int K, bool dk_se) {
+  if (B < 0 || H < 0 || S < 0 || dh < 0 || K < 1) return 0;
   Carver c;
   const int64_t rows = (int64_t)B * H * S;
-  carve_attn(c, rows, rows * dh, true, true, (int64_t)B * H, (S + 63) / 64 * 64, 3, true);
+  carve_attn(c, rows, rows * dh, true, true, (int64_t)B * H, (S + 63) / 64 * 64, 3, true, dk_se ? K : 0);
   return c.used();
 }
 
@@ -68,7 +77,7 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   for (const void* p : {io.Q, io.Kt, io.V, io.dO, (const void*)io.dO32, (const void*)io.O})
     if ((uintptr_t)p & 15) return BS_EINVAL;  // 16-byte vector loads
   if ((int64_t)io.B * io.H > 65535 || (io.S + 63) / 64 > 65535) return BS_ESHAPE;
-  if (io.dK.se || (l2 && io.dQ.se)) return BS_EUNSUPPORTED;
+  if (l2 && (io.dK.se || io.dQ.se)) return BS_EUNSUPPORTED;
   bool want_r = false, want_n = false;
   for (int i = 0; i < (fwd_only ? 0 : io.n_pol); ++i) {
     if (io.pol[i] < BS_READ_U || io.pol[i] > BS_READ_N) return BS_EINVAL;
@@ -79,11 +88,12 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   const bool need_o = !io.O && !io.O_out;
   const int64_t bh = (int64_t)io.B * io.H, Sp = (io.S + 63) / 64 * 64;
   const int ndo = fwd_only ? 0 : ((io.dO32 || l2) ? 3 : 1);
+  const int dk_trials = (!fwd_only && io.dK.se && want_n) ? io.K : 0;
   Carver probe;
-  carve_attn(probe, rows, numel, need_o, !io.D_ref, bh, Sp, ndo, l2);
+  carve_attn(probe, rows, numel, need_o, !io.D_ref, bh, Sp, ndo, l2, dk_trials);
   if (!ws || ((uintptr_t)ws & 255) || ws_bytes < probe.used()) return BS_EWORKSPACE;
   Carver c(ws, ws_bytes);
-  AttnWs w = carve_attn(c, rows, numel, need_o, !io.D_ref, bh, Sp, ndo, l2);
+  AttnWs w = carve_attn(c, rows, numel, need_o, !io.D_ref, bh, Sp, ndo, l2, dk_trials);
   float* dref = io.D_ref ? io.D_ref : w.D_ref;
   uint8_t* O_codes = io.O_codes ? io.O_codes : w.codes;
   // level 2: the mean incoming gradient replaces dO in the backward (fp32, three bf16 planes)
@@ -132,6 +142,7 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   } else {
     AttnDArgs da{Oorig, (const u16*)io.dO, io.dO32, O_codes, io.O_scale, rows, f8_format(io.fmt), io.seed, base + 1,
                  io.K, want_n ? 1 : 0, dref, w.dD_R, w.dD_N, w.sd_N};
+    da.dD_trials = dk_trials ? w.dD_tr : nullptr;
     BS_TRY(launch_attn_d(da, st));
   }
 
@@ -172,6 +183,37 @@ bs_status attn_run(const AttnIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     ba.kbias[i] = io.dK.bias ? io.dK.bias + i * numel : nullptr;
   }
   BS_TRY(launch_attn_bwd(ba, io.B, io.H, st));
+
+  // se of dK over trials under N (App. C.4), the per-trial path: trial k's move of dK is the
+  // key-major pass's R-bias term with dD_k in place of dD_R (-c (P dD_k)^T Q); shifted fp64 sums
+  if (io.dK.se) {
+    if (dk_trials) {
+      AttnBwdArgs bt = ba;
+      bt.k_only = 1;
+      bt.dK_ref = w.dK_s;
+      bt.dV = w.dV_s;
+      bt.dD_N = nullptr;
+      bt.sd_N = nullptr;
+      bt.n_pol = 1;
+      bt.pol[0] = BS_READ_R;
+      bt.kmean[0] = nullptr;
+      bt.kbias[0] = w.tdk;
+      bt.mean[0] = bt.bias[0] = bt.se[0] = nullptr;
+      for (int k = 1; k <= io.K; ++k) {
+        bt.dD_R = w.dD_tr + (int64_t)(k - 1) * rows;
+        BS_TRY(launch_attn_bwd(bt, io.B, io.H, st));
+        BS_TRY(launch_trial_accum(w.tdk, 1, k, numel, w.d1, w.S1, w.S2, st));
+      }
+      BS_TRY(launch_trial_se(w.S1, w.S2, io.K, numel, w.sek, st));
+    }
+    for (int i = 0; i < io.n_pol; ++i) {
+      float* dst = io.dK.se + i * numel;
+      if (io.pol[i] == BS_READ_N)
+        BS_TRY(launch_combine(w.sek, nullptr, nullptr, numel, dst, nullptr, nullptr, st));
+      else
+        BS_TRY(launch_fill2d(dst, 1, numel, numel, 0.0f, st));
+    }
+  }
   return BS_OK;
 }
 

@@ -30,6 +30,7 @@ struct AttnDArgs {
   uint32_t use;           // new roundings' use id
   int K, want_n;
   float *D_ref, *dD_R, *dD_N, *sd_N;  // [rows]
+  float* dD_trials = nullptr;         // nullable [K][rows]: each trial's dD_k (want_n)
 };
 
 // Level-2 averaging at the D use: trial k rounds O anew (trial k, use_fwd) and its incoming
@@ -73,6 +74,7 @@ struct AttnBwdArgs {
   float* se[ATTN_MAX_POL];
   float* kmean[ATTN_MAX_POL];  // dK estimates
   float* kbias[ATTN_MAX_POL];
+  int k_only = 0;              // 1: the key-major pass only (dK, dV and their estimates)
 };
 
 bs_status launch_attn_fwd(const AttnArgs& a, int B, int H, hipStream_t st);

@@ -97,6 +97,7 @@ __global__ __launch_bounds__(256) void attn_d_kernel(AttnDArgs a) {
         for (int q = 0; q < 4; ++q) Sk += sr_up(F[4 * j + q], R[q]) ? w[4 * j + q] : 0.0f;
       }
       Sk = quad_sum(Sk);
+      if (a.dD_trials && ok && sub == 0) a.dD_trials[(int64_t)(k - 1) * a.rows + row] = (float)(A + (double)s * Sk);
       if (k == 1) s1 = Sk;
       const double dl = (double)Sk - s1;
       d1 += dl;
@@ -889,10 +890,10 @@ bs_status launch_attn_bwd(const AttnBwdArgs& a, int B, int H, hipStream_t st) {
   ProfScope prof("attn_bwd", st);
   if (a.dO32) {
     attn_bwd_k_kernel<3><<<grid, 256, 0, st>>>(a);
-    attn_bwd_q_kernel<3><<<grid, 256, 0, st>>>(a);
+    if (!a.k_only) attn_bwd_q_kernel<3><<<grid, 256, 0, st>>>(a);
   } else {
     attn_bwd_k_kernel<1><<<grid, 256, 0, st>>>(a);
-    attn_bwd_q_kernel<1><<<grid, 256, 0, st>>>(a);
+    if (!a.k_only) attn_bwd_q_kernel<1><<<grid, 256, 0, st>>>(a);
   }
   BS_CHECK_LAUNCH();
   return BS_OK;

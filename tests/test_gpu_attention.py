@@ -22,12 +22,12 @@ def inputs(B, H, S, seed):
     return [t.to(torch.bfloat16) for t in synth.attention_inputs(B, H, S, 64, torch.float32, config=100 + seed)]
 
 
-def run(lib, Q, K, V, dO, O=None, causal=True, pols=("U", "R", "N"), Kt=8, seed=3, fwd_mode="sr"):
+def run(lib, Q, K, V, dO, O=None, causal=True, pols=("U", "R", "N"), Kt=8, seed=3, fwd_mode="sr", dk_se=True):
     print(f"[attn] shape={tuple(Q.shape)} causal={causal} pols={pols} K={Kt} O={'given' if O is not None else 'computed'}",
           flush=True)
     out = lib.attn_bwd_policy(Q.cuda(), K.cuda(), V.cuda(), dO.cuda(), causal=causal, O=None if O is None else
                               torch.from_numpy(np.ascontiguousarray(O)).cuda(), fwd_mode=fwd_mode, policies=pols, K=Kt,
-                              seed=seed, store_id=1)
+                              seed=seed, store_id=1, want_dk_se=dk_se)
     torch.cuda.synchronize()
     return out
 
