@@ -416,6 +416,18 @@ bs_status bs_linear_bwd_policy(const void* X, const void* W, const void* dY, bs_
  *   R = ||mean_err||^2 / sum_j se_j^2 (NaN when the sum is 0).
  *   K >= 1, m >= 0. Sums run in a fixed order (deterministic).
  * ---------------------------------------------------------------------------------- */
+/* ------------------------------------------------------------------------------------
+ * bs_estimate_summary -- App. D.4's detection summary of any call's estimate of one gradient
+ * (for instance one policy's slice of a bs_est):
+ *   bias [n] (required when n > 0), se [n] and ref [n] (each nullable: treated as zero) fp32.
+ *   summary [3] fp64 out (device): ||bias||_2, ||ref||_2, R = ||bias||^2 / sum_j se_j^2 (NaN
+ *   when the sum is 0: no spread over trials, e.g. a policy that draws nothing). Fixed-order sums.
+ *   ws: bs_estimate_summary_workspace_size() bytes, 256-byte aligned. n >= 0.
+ * ---------------------------------------------------------------------------------- */
+size_t bs_estimate_summary_workspace_size(void);
+bs_status bs_estimate_summary(const float* bias, const float* se, const float* ref, int64_t n, double* summary,
+                              void* ws, size_t ws_bytes, void* stream);
+
 size_t bs_policy_bias_workspace_size(int K, int64_t m);
 bs_status bs_policy_bias_estimate(const float* delta, int K, int64_t m, const float* g_ref, float* mean_err,
                                   float* se, double* summary, void* ws, size_t ws_bytes, void* stream);

@@ -53,6 +53,8 @@ _qround = _sig("bs_qround", _int, [_vp, _int, _i64, _int, _int, _u64, _u32, _u32
 _gemm = _sig("bs_gemm_bf16_nt", _int, [_vp, _i64, _vp, _i64, _vp, _i64, _i64, _i64, _i64, _f32, _int, _vp])
 _pb_ws = _sig("bs_policy_bias_workspace_size", _sz, [_int, _i64])
 _pb = _sig("bs_policy_bias_estimate", _int, [_vp, _int, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp])
+_sum_ws = _sig("bs_estimate_summary_workspace_size", _sz, [])
+_sum = _sig("bs_estimate_summary", _int, [_vp, _vp, _vp, _i64, _vp, _vp, _sz, _vp])
 _pb_na_max = _sig("bs_policy_bias_noalloc_max", _i64, [])
 _pb_na = _sig("bs_policy_bias_estimate_noalloc", _int, [_vp, _int, _i64, _vp, _vp, _vp, _vp, _vp])
 _norm_ws = _sig("bs_rmsnorm_linear_workspace_size", _sz, [_i64, _i64, _i64, _int, _int])
@@ -158,6 +160,7 @@ def profile_work(kernel=None):
 
 EXPORTED = ["bs_status_string", "bs_version", "bs_qround", "bs_gemm_bf16_nt", "bs_policy_bias_workspace_size",
             "bs_policy_bias_estimate", "bs_policy_bias_noalloc_max", "bs_policy_bias_estimate_noalloc",
+            "bs_estimate_summary_workspace_size", "bs_estimate_summary",
             "bs_rmsnorm_linear_workspace_size", "bs_rmsnorm_linear_fwd_bwd",
             "bs_attn_workspace_size", "bs_attn_bwd_policy", "bs_attn_pstore_workspace_size", "bs_attn_pstore_policy", "bs_attn_level2_policy",
             "bs_te_attn_workspace_size", "bs_te_attn_bwd", "bs_te_delayed_scales",
@@ -276,6 +279,20 @@ def policy_bias_estimate_noalloc(delta, g_ref=None, out=None):
     _check(_pb_na(_p(delta), K, m, _p(g_ref), _p(mean), _p(se), _p(summ), _stream()),
            "bs_policy_bias_estimate_noalloc")
     return mean, se, summ
+
+
+def estimate_summary(bias, se=None, ref=None):
+    """(||bias||, ||ref||, R = ||bias||^2 / sum se^2) of one gradient's estimate (bs_estimate_summary);
+    fp32 device tensors of equal size, se / ref optional."""
+    _dev_check(bias, se, ref)
+    n = bias.numel()
+    for t in (bias, se, ref):
+        if t is not None and (t.dtype != torch.float32 or t.numel() != n):
+            raise TypeError("bias, se and ref must be float32 tensors of one size")
+    summ = torch.empty(3, dtype=torch.float64, device=bias.device)
+    ws = _workspace(_sum_ws(), bias.device)
+    _check(_sum(_p(bias), _p(se), _p(ref), n, _p(summ), _p(ws), ws.numel(), _stream()), "bs_estimate_summary")
+    return summ
 
 
 def policy_bias_noalloc_max():

@@ -88,3 +88,33 @@ def test_binding_rejects_other_dtypes(lib):
         lib.policy_bias_estimate(torch.zeros(2, 8, dtype=torch.float16, device="cuda"))
     with pytest.raises(TypeError):
         lib.policy_bias_estimate(torch.zeros(2, 8, device="cuda"), torch.zeros(8, dtype=torch.float64, device="cuda"))
+
+
+def test_estimate_summary_of_a_call_against_the_oracle(lib):
+    """App. D.4's R of a call's outputs (the N policy's dgain of the RMSNorm -> Linear check): the
+    summary of the library's bias / se / ref arrays against oracle.stats.summary of the oracle's."""
+    from oracle import fp8, norm_store, qround as oq
+    from paper_2609_39813_amd import synth
+    X, g, W, dY = synth.rmsnorm_linear_inputs(300, 128, 72, torch.float32, 2)
+    out = lib.rmsnorm_linear(X.cuda(), g.cuda(), W.cuda(), dY.cuda(), policies=("U/U", "N/N"), K=24, seed=9)
+    ref = norm_store.check(X.numpy(), g.numpy(), W.numpy(), dY.numpy(), fmt=fp8.E4M3, fwd_mode=oq.RNE,
+                           policies=("U/U", "N/N"), K=24, seed=9)
+    for i, code in enumerate(("U/U", "N/N")):
+        b, s = out["dgain"]["bias"][i].contiguous(), out["dgain"]["se"][i].contiguous()
+        summ = lib.estimate_summary(b, s, out["dgain_ref"]).cpu().numpy()
+        torch.cuda.synchronize()
+        _, ob, ose = ref[code]["dgamma"]
+        want = stats.summary(ob, ose, ref["dgamma_ref"])
+        assert abs(summ[0] - want["bias_l2"]) <= TOL * want["bias_l2"] + 1e-30
+        assert abs(summ[1] - want["ref_l2"]) <= TOL * want["ref_l2"]
+        if code == "U/U":
+            assert np.isnan(summ[2]) and np.isnan(want["R"])
+        else:
+            assert abs(summ[2] - want["R"]) <= 3 * TOL * want["R"]
+        # and exactly the summary of the library's own arrays
+        bn, sn, rn = (to_np(t) for t in (b, s, out["dgain_ref"]))
+        assert abs(summ[0] - np.sqrt(np.sum(bn ** 2))) <= 1e-12 * max(summ[0], 1e-300)
+        if code == "N/N":
+            assert abs(summ[2] - np.sum(bn ** 2) / np.sum(sn ** 2)) <= 1e-12 * summ[2]
+    empty = lib.estimate_summary(torch.zeros(0, device="cuda")).cpu().numpy()
+    assert empty[0] == 0 and empty[1] == 0 and np.isnan(empty[2])
