@@ -351,13 +351,23 @@ static bs_status launch_gemm_lds(const GemmArgs& g0, hipStream_t st) {
   GemmArgs g = g0;
   const int64_t tiles = (int64_t)((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   const int total = (g.K / LBK) * g.nseg;
-  // split K while the tiles leave CUs idle, keeping at least 16 chunks (1024 of K) per block
+  // split K while the tiles leave CUs idle, keeping at least 16 chunks (1024 of K) per block. One
+  // block fits a CU (its LDS), so blocks beyond the 256 CUs run in a second round: the split count
+  // minimizes the makespan ceil(tiles * splits / 256) / splits (e.g. 48 tiles: 5 splits in one round
+  // of 240 blocks, not 6 in two rounds of 288)
   int splits = 1;
   if (g.part && tiles < 256) {
-    const int64_t want = (256 + tiles - 1) / tiles;
     const int64_t by_k = total / 16;
     const int64_t by_ws = g.part_cap / ((int64_t)g.M * g.N);
-    splits = (int)std::max<int64_t>(1, std::min(want, std::min(by_k, by_ws)));
+    const int64_t top = std::max<int64_t>(1, std::min((256 + tiles - 1) / tiles, std::min(by_k, by_ws)));
+    double best = 2.0;
+    for (int64_t sp = 1; sp <= top; ++sp) {
+      const double span = (double)((tiles * sp + 255) / 256) / (double)sp;
+      if (span < best - 1e-12) {
+        best = span;
+        splits = (int)sp;
+      }
+    }
   }
   const int cps = (total + splits - 1) / splits;
   splits = (total + cps - 1) / cps;
