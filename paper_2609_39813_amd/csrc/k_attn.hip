@@ -263,11 +263,17 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
 // (v = R, N). S = Q K^T and dP = dO V^T are formed with queries as rows, so that their
 // result tiles are the (key, query) operands of the three products.
 // ------------------------------------------------------------------------------------
-template <int NDO>
+// BIAS = 0: no policy reads R or N (no bias accumulators). With three dO planes the eight tiles
+// of a query block take one LDS stage (66 KB, two blocks per CU): each block stages a query
+// block and computes on it while the other block of its CU runs (the two-stage register-staged
+// pipeline would hold 133 KB and 64 more registers, one block and one wave per SIMD).
+template <int NDO, int BIAS>
 __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
   constexpr int NT = 2 + 2 * NDO;  // Q, Q^T, dO planes, dO^T planes
-  __shared__ __attribute__((aligned(16))) u16 sm[2][NT][AT * AT];
-  __shared__ float rows[2][5][AT];  // m, 1/l, D, dD_R, dD_N per query
+  constexpr bool ONE = NDO == 3;   // one LDS stage
+  constexpr int NST = ONE ? 1 : 2;
+  __shared__ __attribute__((aligned(16))) u16 sm[NST][NT][AT * AT];
+  __shared__ float rows[NST][5][AT];  // m, 1/l, D, dD_R, dD_N per query
   // heaviest (most query blocks) first: blocks are dispatched in index order
   const int bh = blockIdx.x, kb = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, c16 = lane & 15;
@@ -324,15 +330,23 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
   floatx4 av[4], ak[4], akr[4], akn[4];
 #pragma unroll
   for (int n = 0; n < 4; ++n) av[n] = ak[n] = akr[n] = akn[n] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const bool want_r = a.dD_R != nullptr, want_n = a.dD_N != nullptr;
+  const bool want_r = BIAS && a.dD_R != nullptr, want_n = BIAS && a.dD_N != nullptr;
   const float c2 = a.scale * kLog2e;
   const int nqb = (a.S + AT - 1) / AT, qb0 = a.causal ? kb : 0;
-  fetch(qb0 * AT);
-  put(0);
-  __syncthreads();
+  if (!ONE) {
+    fetch(qb0 * AT);
+    put(0);
+    __syncthreads();
+  }
   for (int qb = qb0; qb < nqb; ++qb) {
-    const int st = (qb - qb0) & 1, q0 = qb * AT;
-    if (qb + 1 < nqb) fetch(q0 + AT);
+    const int st = ONE ? 0 : (qb - qb0) & 1, q0 = qb * AT;
+    if (ONE) {
+      fetch(q0);
+      put(0);
+      __syncthreads();
+    } else if (qb + 1 < nqb) {
+      fetch(q0 + AT);
+    }
     const u16* tQ = sm[st][0];
     const u16* tQt = sm[st][1];
     // S, dP: query tiles t (rows), this wave's keys (columns)
@@ -418,7 +432,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
           }
       }
     }
-    if (qb + 1 < nqb) put(st ^ 1);
+    if (!ONE && qb + 1 < nqb) put(st ^ 1);
     __syncthreads();
   }
   const float c = a.scale;
@@ -889,10 +903,16 @@ bs_status launch_attn_bwd(const AttnBwdArgs& a, int B, int H, hipStream_t st) {
   dim3 grid((unsigned)(B * H), (unsigned)((a.S + AT - 1) / AT));
   ProfScope prof("attn_bwd", st);
   if (a.dO32) {
-    attn_bwd_k_kernel<3><<<grid, 256, 0, st>>>(a);
+    if (a.dD_R || a.dD_N)
+      attn_bwd_k_kernel<3, 1><<<grid, 256, 0, st>>>(a);
+    else
+      attn_bwd_k_kernel<3, 0><<<grid, 256, 0, st>>>(a);
     if (!a.k_only) attn_bwd_q_kernel<3><<<grid, 256, 0, st>>>(a);
   } else {
-    attn_bwd_k_kernel<1><<<grid, 256, 0, st>>>(a);
+    if (a.dD_R || a.dD_N)
+      attn_bwd_k_kernel<1, 1><<<grid, 256, 0, st>>>(a);
+    else
+      attn_bwd_k_kernel<1, 0><<<grid, 256, 0, st>>>(a);
     if (!a.k_only) attn_bwd_q_kernel<1><<<grid, 256, 0, st>>>(a);
   }
   BS_CHECK_LAUNCH();
