@@ -598,8 +598,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
 }
 
 // ------------------------------------------------------------------------------------
-// operand copies for the backward: X^T [BH][64][Sp] (zero past S) of bf16 X [BH][S][64];
-// for an fp32 X, its three bf16 planes (row-major) and their transposes
+// operand copies for the backward: X^T [BH][64][Sp] (zero past S, tiles in fragment order,
+// tperm) of bf16 X [BH][S][64]; for an fp32 X, its three bf16 planes (row-major) and their
+// transposes
 // ------------------------------------------------------------------------------------
 template <typename X>
 __global__ __launch_bounds__(256) void attn_prep_kernel(const X* __restrict__ x, int S, int Sp, u16* __restrict__ xt0,
@@ -632,7 +633,7 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(const X* __restrict__ x,
   for (int e = threadIdx.x; e < AT * AT; e += 256) {
     const int c = e >> 6, r = e & 63;
 #pragma unroll
-    for (int p = 0; p < NP; ++p) xt[p][tb + (int64_t)c * Sp + r0 + r] = t[p][r][c];
+    for (int p = 0; p < NP; ++p) xt[p][tb + (int64_t)c * Sp + r0 + r] = t[p][tperm(r)][c];
   }
 }
 
@@ -844,9 +845,9 @@ bs_status launch_attn_d(const AttnDArgs& a, hipStream_t st) {
   return BS_OK;
 }
 
-// X^T [BH][64][Sp] of up to four bf16 X [BH][S][64] (one per grid z): a 64 x 64 tile through
-// LDS with 16-byte accesses on both sides; chunk c of tile row r sits at c ^ ((r >> 3) & 7), so
-// the column reads of eight rows 8 apart fall on distinct banks
+// X^T [BH][64][Sp] of up to four bf16 X [BH][S][64] (one per grid z; columns of each tile in
+// fragment order, tperm): a 64 x 64 tile through LDS with 16-byte accesses on both sides; chunk
+// c of tile row r sits at c ^ ((r >> 3) & 7)
 struct TransposeJobs {
   const u16* x[4];
   u16* xt[4];
@@ -870,8 +871,8 @@ __global__ __launch_bounds__(256) void attn_transpose_kernel(TransposeJobs jobs,
     u16 o[8];
 #pragma unroll
     for (int v = 0; v < 8; ++v) {
-      const int r = 8 * m + v;
-      o[v] = t[r * AT + 8 * ((d >> 3) ^ m) + (d & 7)];
+      const int r = tperm(8 * m + v);
+      o[v] = t[r * AT + 8 * ((d >> 3) ^ ((r >> 3) & 7)) + (d & 7)];
     }
     *(uint4*)(xt + tb + (int64_t)d * Sp + r0 + 8 * m) = *(const uint4*)o;
   }

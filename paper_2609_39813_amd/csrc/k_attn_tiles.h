@@ -26,12 +26,15 @@ __device__ __forceinline__ floatx4 mfma(bf16x8 a, bf16x8 b, floatx4 c) {
 // element (a few ulps; the exponent's rounding adds |m| 2^-24, below 1e-6 for these scores)
 constexpr float kLog2e = 1.4426950408889634f;
 
-__device__ __forceinline__ int swt(int row, int unit) { return row * AT + ((unit ^ (row & 15)) << 2); }
+// Transposed copies X^T [64][Sp] store each 64-column tile in fragment order: column e of a
+// tile holds tile row tperm(e) of X, e = 32 s + 8 g + j -> 32 s + 4 g + (j & 3) + 16 (j >> 2).
+// The eight k values of an operand fragment built from a 16x16 result tile pair (result rows
+// 32 s + 4 g + 0..3 and 32 s + 16 + 4 g + 0..3, lane group g) are then one 16-byte chunk.
+__device__ __forceinline__ int tperm(int e) { return (e & 32) | ((e >> 1) & 12) | (e & 3) | ((e & 4) << 2); }
 
+// B operand of X^T stored in LDS (sw layout): row `row`, the k values of half s, lane group g
 __device__ __forceinline__ bf16x8 frag_t(const u16* T, int row, int s, int g) {
-  const uint2 a = *(const uint2*)(T + swt(row, 8 * s + g));
-  const uint2 b = *(const uint2*)(T + swt(row, 8 * s + 4 + g));
-  return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+  return *(const bf16x8*)(T + sw(row, 8 * (4 * s + g)));
 }
 
 // the three bf16 terms (round to nearest, then the exact remainders) of eight fp32 values as
@@ -87,13 +90,6 @@ __device__ __forceinline__ void tile_fetch_t(TileRegs& t, const u16* __restrict_
     t.v[i] = *(const uint4*)(g + (int64_t)r * ld + c0 + c);
   }
 }
-__device__ __forceinline__ void tile_put_t(u16* T, const TileRegs& t) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int r = (threadIdx.x >> 3) + 32 * i, u = (threadIdx.x & 7) * 2;
-    *(uint2*)(T + swt(r, u)) = make_uint2(t.v[i].x, t.v[i].y);
-    *(uint2*)(T + swt(r, u + 1)) = make_uint2(t.v[i].z, t.v[i].w);
-  }
-}
+__device__ __forceinline__ void tile_put_t(u16* T, const TileRegs& t) { tile_put(T, t); }
 
 }  // namespace bsp
