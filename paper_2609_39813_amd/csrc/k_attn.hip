@@ -262,21 +262,29 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
 // key-block-major: dV = P^T dO, dK = c dS^T Q and the dK bias terms -c P^T (dD_v * Q)
 // (v = R, N). S = Q K^T and dP = dO V^T are formed with queries as rows, so that their
 // result tiles are the (key, query) operands of the three products.
+//
+// A query block's operands sit in two LDS halves: the row-major tiles (Q and the dO planes,
+// read by S and dP) and the transposed ones (Q^T and the dO^T planes, read by the products).
+// Both arrive by buffer loads straight into LDS (no staging registers; rows past S read as
+// zero). A half is refilled for the next query block once every wave has read it: the
+// row-major half after S and dP, the transposed half after the products, so each load lands
+// while the other half is in use. BIAS = 0: no policy reads R or N (no bias accumulators);
+// BIAS = 1 forms both bias terms (a missing dD_v reads as zero).
 // ------------------------------------------------------------------------------------
-// BIAS = 0: no policy reads R or N (no bias accumulators). With three dO planes the eight tiles
-// of a query block take one LDS stage (66 KB, two blocks per CU): each block stages a query
-// block and computes on it while the other block of its CU runs (the two-stage register-staged
-// pipeline would hold 133 KB and 64 more registers, one block and one wave per SIMD).
 template <int NDO, int BIAS>
 __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
-  constexpr int NT = 2 + 2 * NDO;  // Q, Q^T, dO planes, dO^T planes
-  constexpr bool ONE = NDO == 3;   // one LDS stage
-  constexpr int NST = ONE ? 1 : 2;
-  __shared__ __attribute__((aligned(16))) u16 sm[NST][NT][AT * AT];
-  __shared__ float rows[NST][5][AT];  // m, 1/l, D, dD_R, dD_N per query
-  // heaviest (most query blocks) first: blocks are dispatched in index order
+  constexpr int NR = 1 + NDO;     // tiles per half
+  constexpr int NL = 2 * NR;      // loads per wave and half (two 1-KB loads per tile)
+  __shared__ __attribute__((aligned(1024))) u16 smR[NR][AT * AT];
+  __shared__ __attribute__((aligned(1024))) u16 smT[NR][AT * AT];
+  // m, 1/l, D, dD_R, dD_N per query for two query blocks, as two variables: the loop is
+  // unrolled by two so each access names one of them, and loads into one are not awaited
+  // before reads of the other
+  constexpr int NRW = BIAS ? 2 : 1;  // row loads per wave and query block
+  __shared__ float rows0[4 * NRW][AT], rows1[4 * NRW][AT];
   const int bh = blockIdx.x, kb = blockIdx.y;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, c16 = lane & 15;
+  const int lane = threadIdx.x & 63, g = lane >> 4, c16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int k0 = kb * AT;
   const int64_t hb = (int64_t)bh * a.S * AT, tb = (int64_t)bh * AT * a.Sp, rb = (int64_t)bh * a.S;
   const int key = k0 + 16 * w + c16;
@@ -290,65 +298,83 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
     fk[s] = __builtin_bit_cast(bf16x8, zk);
     fv[s] = __builtin_bit_cast(bf16x8, zv);
   }
-  const u16* dOrow[NDO];
-#pragma unroll
-  for (int i = 0; i < NDO; ++i) dOrow[i] = (NDO == 1 ? a.dO : a.dOp[i]) + hb;
 
-  TileRegs pf[NT];
-  float prow[5];
-  auto fetch = [&](int q0) {
-    tile_fetch(pf[0], a.Q + hb, q0, a.S);
-    tile_fetch_t(pf[1], a.Qt + tb, q0, a.Sp);
+  // resources: row-major tiles end at row S, transposed copies span their Sp columns
+  __amdgpu_buffer_rsrc_t rR[NR], rT[NR];
+  rR[0] = attn_rsrc(a.Q + hb, (int64_t)a.S * AT * 2);
+  rT[0] = attn_rsrc(a.Qt + tb, (int64_t)AT * a.Sp * 2);
 #pragma unroll
-    for (int i = 0; i < NDO; ++i) {
-      tile_fetch(pf[2 + i], dOrow[i], q0, a.S);
-      tile_fetch_t(pf[2 + NDO + i], a.dOt[i] + tb, q0, a.Sp);
-    }
-    if (threadIdx.x < AT) {
-      const int q = q0 + threadIdx.x;
-      const bool ok = q < a.S;
-      prow[0] = ok ? a.m[rb + q] : 0.0f;
-      prow[1] = ok ? 1.0f / a.l[rb + q] : 0.0f;
-      prow[2] = ok ? a.D_ref[rb + q] : 0.0f;
-      prow[3] = (ok && a.dD_R) ? a.dD_R[rb + q] : 0.0f;
-      prow[4] = (ok && a.dD_N) ? a.dD_N[rb + q] : 0.0f;
+  for (int i = 0; i < NDO; ++i) {
+    rR[1 + i] = attn_rsrc((NDO == 1 ? a.dO : a.dOp[i]) + hb, (int64_t)a.S * AT * 2);
+    rT[1 + i] = attn_rsrc(a.dOt[i] + tb, (int64_t)AT * a.Sp * 2);
+  }
+  // lane l of load j (two per wave and tile) fills tile row 8 (2 w + j) + l / 8 at chunk
+  // position l % 8, which holds logical chunk (l % 8) ^ (l / 8) of the row (the sw layout)
+  const int lr = lane >> 3, lch = (lane & 7) ^ lr;
+  const uint32_t vR = (uint32_t)(lr * AT * 2 + lch * 16), vT = (uint32_t)(lr * a.Sp * 2 + lch * 16);
+  // (each resource is copied to a scalar first: the host pass rejects a 16-byte LDS load
+  // whose resource is an array element)
+  auto issue_R = [&](int q0) {
+#pragma unroll
+    for (int t = 0; t < NR; ++t) {
+      const __amdgpu_buffer_rsrc_t r = rR[t];
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (void __attribute__((address_space(3)))*)(smR[t] + (2 * w + j) * 512),
+                                                 16, vR, (uint32_t)(q0 * AT * 2 + (2 * w + j) * 1024), 0, 0);
     }
   };
-  auto put = [&](int st) {
-    tile_put(sm[st][0], pf[0]);
-    tile_put_t(sm[st][1], pf[1]);
+  auto issue_T = [&](int q0) {
 #pragma unroll
-    for (int i = 0; i < NDO; ++i) {
-      tile_put(sm[st][2 + i], pf[2 + i]);
-      tile_put_t(sm[st][2 + NDO + i], pf[2 + NDO + i]);
+    for (int t = 0; t < NR; ++t) {
+      const __amdgpu_buffer_rsrc_t r = rT[t];
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (void __attribute__((address_space(3)))*)(smT[t] + (2 * w + j) * 512),
+                                                 16, vT, (uint32_t)(q0 * 2 + (2 * w + j) * 16 * a.Sp), 0, 0);
     }
-    if (threadIdx.x < AT)
+  };
+  // The per-query rows m, l, D (and dD_R, dD_N) go straight into LDS too, one dword per lane:
+  // wave w loads row arrays NRW w .. NRW w + NRW - 1 of (m, l, D[, dD_R, dD_N, -, -, -]).
+  // Queries past S, a missing dD_v and the padding (empty resources) read as zero; every wave
+  // issues NL + NRW loads per query block.
+  const float* row_src[8] = {a.m, a.l, a.D_ref, BIAS ? a.dD_R : nullptr, BIAS ? a.dD_N : nullptr,
+                             nullptr, nullptr, nullptr};
+  __amdgpu_buffer_rsrc_t rq[NRW];
 #pragma unroll
-      for (int k = 0; k < 5; ++k) rows[st][k][threadIdx.x] = prow[k];
+  for (int k = 0; k < NRW; ++k) {
+    const float* base = row_src[NRW * w + k];
+    rq[k] = __builtin_amdgcn_make_buffer_rsrc((void*)(base ? base + rb : a.m), (short)0, base ? a.S * 4 : 0,
+                                              0x00020000);
+  }
+  auto issue_rows = [&](float (*rows)[AT], int q0) {
+#pragma unroll
+    for (int k = 0; k < NRW; ++k) {
+      const __amdgpu_buffer_rsrc_t r = rq[k];
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (void __attribute__((address_space(3)))*)(rows[NRW * w + k]), 4,
+                                               (uint32_t)(lane * 4), (uint32_t)(q0 * 4), 0, 0);
+    }
   };
 
   floatx4 av[4], ak[4], akr[4], akn[4];
 #pragma unroll
   for (int n = 0; n < 4; ++n) av[n] = ak[n] = akr[n] = akn[n] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const bool want_r = BIAS && a.dD_R != nullptr, want_n = BIAS && a.dD_N != nullptr;
   const float c2 = a.scale * kLog2e;
   const int nqb = (a.S + AT - 1) / AT, qb0 = a.causal ? kb : 0;
-  if (!ONE) {
-    fetch(qb0 * AT);
-    put(0);
-    __syncthreads();
-  }
-  for (int qb = qb0; qb < nqb; ++qb) {
-    const int st = ONE ? 0 : (qb - qb0) & 1, q0 = qb * AT;
-    if (ONE) {
-      fetch(q0);
-      put(0);
-      __syncthreads();
-    } else if (qb + 1 < nqb) {
-      fetch(q0 + AT);
+  issue_R(qb0 * AT);
+  issue_rows(rows0, qb0 * AT);
+  issue_T(qb0 * AT);
+  ATTN_WAIT_VM(0);
+  ATTN_LDS_BARRIER();
+  // one query block; rows: its rows, nrows: the next block's
+  auto step = [&](int qb, float (*rows)[AT], float (*nrows)[AT]) {
+    const int q0 = qb * AT;
+    const bool more = qb + 1 < nqb;
+    // the rows have landed: 1/l in place (wave 1; 0 past S), read after the next barrier
+    if (w == 1) {
+      const float l = rows[1][lane];
+      rows[1][lane] = q0 + lane < a.S ? 1.0f / l : 0.0f;
     }
-    const u16* tQ = sm[st][0];
-    const u16* tQt = sm[st][1];
     // S, dP: query tiles t (rows), this wave's keys (columns)
     floatx4 sv[4], dp[4];
 #pragma unroll
@@ -357,19 +383,25 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
     for (int s = 0; s < 2; ++s) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        sv[t] = mfma(*(const bf16x8*)(tQ + sw(16 * t + c16, 32 * s + 8 * g)), fk[s], sv[t]);
+        sv[t] = mfma(*(const bf16x8*)(smR[0] + sw(16 * t + c16, 32 * s + 8 * g)), fk[s], sv[t]);
 #pragma unroll
         for (int i = 0; i < NDO; ++i)
-          dp[t] = mfma(*(const bf16x8*)(sm[st][2 + i] + sw(16 * t + c16, 32 * s + 8 * g)), fv[s], dp[t]);
+          dp[t] = mfma(*(const bf16x8*)(smR[1 + i] + sw(16 * t + c16, 32 * s + 8 * g)), fv[s], dp[t]);
       }
     }
+    // every wave has read the row-major half: the next query block's tiles and rows go in
+    // (after the last query block too: those loads read past S, as zeros, and are never used,
+    // so that every wave's count of loads in flight below is fixed)
+    ATTN_LDS_BARRIER();
+    issue_R(q0 + AT);
+    issue_rows(nrows, q0 + AT);
     // masks only where the block crosses S or the causal diagonal (a uniform test)
     const bool full = k0 + AT <= a.S && q0 + AT <= a.S && (!a.causal || k0 + AT - 1 <= q0);
     float p[4][4], ds[4][4];
 #pragma unroll
     for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) p[t][r] = fmaf(c2, sv[t][r], -rows[st][0][16 * t + 4 * g + r]);
+      for (int r = 0; r < 4; ++r) p[t][r] = fmaf(c2, sv[t][r], -rows[0][16 * t + 4 * g + r]);
     if (!full) {
 #pragma unroll
       for (int t = 0; t < 4; ++t)
@@ -384,8 +416,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int ql = 16 * t + 4 * g + r;
-        p[t][r] = __builtin_amdgcn_exp2f(p[t][r]) * rows[st][1][ql];
-        ds[t][r] = p[t][r] * (dp[t][r] - rows[st][2][ql]);
+        p[t][r] = __builtin_amdgcn_exp2f(p[t][r]) * rows[1][ql];
+        ds[t][r] = p[t][r] * (dp[t][r] - rows[2][ql]);
       }
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
@@ -395,45 +427,55 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
         vp[v] = p[2 * s + (v >> 2)][v & 3];
         vd[v] = ds[2 * s + (v >> 2)][v & 3];
       }
-      bf16x8 tp[3], td[3];
-      pack3(vp, tp);
-      pack3(vd, td);
-      bf16x8 fq[4];
+      bf16x8 tp[3], td[3], tr[3], tn[3];
+      pack3t(vp, tp);
+      pack3t(vd, td);
+      if (BIAS) {
+        // bias terms: P scaled per query by dD_v
+        float vr[8], vn[8];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+          const int ql = 32 * s + 16 * (v >> 2) + 4 * g + (v & 3);
+          vr[v] = vp[v] * rows[3][ql];
+          vn[v] = vp[v] * rows[4][ql];
+        }
+        pack3t(vr, tr);
+        pack3t(vn, tn);
+      }
+      if (s == 0) {
+        // the transposed half of this query block has landed in every wave
+        ATTN_WAIT_VM(NL + NRW);
+        ATTN_LDS_BARRIER();
+      }
 #pragma unroll
       for (int n = 0; n < 4; ++n) {
-        fq[n] = frag_t(tQt, 16 * n + c16, s, g);
+        const bf16x8 fq = frag_t(smT[0], 16 * n + c16, s, g);
 #pragma unroll
         for (int i = 0; i < NDO; ++i) {
-          const bf16x8 fo = frag_t(sm[st][2 + NDO + i], 16 * n + c16, s, g);
+          const bf16x8 fo = frag_t(smT[1 + i], 16 * n + c16, s, g);
 #pragma unroll
           for (int j = 0; j < 3; ++j)
             if (i + j <= 2) av[n] = mfma(tp[j], fo, av[n]);
         }
 #pragma unroll
-        for (int j = 0; j < 3; ++j) ak[n] = mfma(td[j], fq[n], ak[n]);
-      }
-      // bias terms: P scaled per query by dD_v
-#pragma unroll
-      for (int v2 = 0; v2 < 2; ++v2) {
-        if (v2 == 0 ? !want_r : !want_n) continue;
-        float vb[8];
-#pragma unroll
-        for (int v = 0; v < 8; ++v) vb[v] = vp[v] * rows[st][3 + v2][32 * s + 16 * (v >> 2) + 4 * g + (v & 3)];
-        bf16x8 tb3[3];
-        pack3(vb, tb3);
-#pragma unroll
-        for (int n = 0; n < 4; ++n)
+        for (int j = 0; j < 3; ++j) ak[n] = mfma(td[j], fq, ak[n]);
+        if (BIAS) {
 #pragma unroll
           for (int j = 0; j < 3; ++j) {
-            if (v2 == 0)
-              akr[n] = mfma(tb3[j], fq[n], akr[n]);
-            else
-              akn[n] = mfma(tb3[j], fq[n], akn[n]);
+            akr[n] = mfma(tr[j], fq, akr[n]);
+            akn[n] = mfma(tn[j], fq, akn[n]);
           }
+        }
       }
     }
-    if (!ONE && qb + 1 < nqb) put(st ^ 1);
-    __syncthreads();
+    // every wave has read the transposed half and the next row-major half has landed
+    ATTN_WAIT_VM(0);
+    ATTN_LDS_BARRIER();
+    if (more) issue_T(q0 + AT);
+  };
+  for (int qb = qb0; qb < nqb; qb += 2) {
+    step(qb, rows0, rows1);
+    if (qb + 1 < nqb) step(qb + 1, rows1, rows0);
   }
   const float c = a.scale;
 #pragma unroll

@@ -63,6 +63,41 @@ __device__ __forceinline__ void pack3(const float* v, bf16x8* t) {
   for (int p = 0; p < 3; ++p) t[p] = __builtin_bit_cast(bf16x8, make_uint4(w[p][0], w[p][1], w[p][2], w[p][3]));
 }
 
+// The same exact three-term split by truncation: each term is the high half of what the
+// previous ones leave (a byte permute packs two), no conversions. Terms of one sign, the
+// second below 2^-7 and the third below 2^-15 of the value.
+__device__ __forceinline__ uint32_t hi_pair(float a, float b) {
+  return __builtin_amdgcn_perm(__float_as_uint(b), __float_as_uint(a), 0x07060302u);
+}
+__device__ __forceinline__ float cut_hi(float a) { return a - __uint_as_float(__float_as_uint(a) & 0xFFFF0000u); }
+__device__ __forceinline__ void pack3t(const float* v, bf16x8* t) {
+  uint32_t w[3][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float a = v[2 * i], b = v[2 * i + 1];
+    const float ra = cut_hi(a), rb = cut_hi(b);
+    w[0][i] = hi_pair(a, b);
+    w[1][i] = hi_pair(ra, rb);
+    w[2][i] = hi_pair(cut_hi(ra), cut_hi(rb));
+  }
+#pragma unroll
+  for (int p = 0; p < 3; ++p) t[p] = __builtin_bit_cast(bf16x8, make_uint4(w[p][0], w[p][1], w[p][2], w[p][3]));
+}
+
+// buffer resource over n_bytes from base: loads past the end read as zero
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t attn_rsrc(const u16* base, int64_t n_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)n_bytes, 0x00020000);
+}
+// s_waitcnt with only a vector-memory count (lgkm and exp counts not awaited)
+#define ATTN_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
+// every LDS access of this wave done, then a barrier without a memory fence (a fence would
+// drain the loads in flight)
+#define ATTN_LDS_BARRIER()                                                       \
+  do {                                                                           \
+    __builtin_amdgcn_s_waitcnt((15 | (3 << 14)) | (7 << 4)); /* lgkmcnt(0) */   \
+    asm volatile("s_barrier" ::: "memory");                                      \
+  } while (0)
+
 // a row-major [64][64] bf16 tile (rows r0.. of a [*, 64] matrix with nrow rows, zeros past
 // them) as two 16-byte pieces per thread, and its store into LDS
 struct TileRegs {
