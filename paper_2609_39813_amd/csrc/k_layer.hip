@@ -45,6 +45,37 @@ __global__ void heads_tokens_kernel(const E* __restrict__ in, E* __restrict__ ou
   }
 }
 
+// The same permutations four elements at a time (dh a multiple of 4): one block per token row
+// t = b S + s, whose d (or 3 d) values are 16-byte pieces of H head rows; 32-bit index math.
+// heads -> tokens (to_tokens) or back, for 4-byte elements (E4 = float4) or 1-byte codes
+// (E4 = uint32_t)
+template <typename E4>
+__global__ __launch_bounds__(256) void heads_tokens4_kernel(const E4* __restrict__ in, E4* __restrict__ out, int S,
+                                                            int H, int dh, int to_tokens) {
+  const int t = blockIdx.x, b = t / S, s = t - b * S;
+  const int q = dh / 4, n = H * q;  // 4-element pieces per token row and per head row
+  for (int k = threadIdx.x; k < n; k += blockDim.x) {
+    const int h = k / q, c = k - h * q;
+    const int64_t hm = (((int64_t)b * H + h) * S + s) * q + c, tk = (int64_t)t * n + k;
+    if (to_tokens)
+      out[tk] = in[hm];
+    else
+      out[hm] = in[tk];
+  }
+}
+// dQ, dK, dV [B,H,S,dh] -> dQKV [T][3d], four elements at a time
+__global__ __launch_bounds__(256) void dqkv_tokens4_kernel(const float4* __restrict__ dQ, const float4* __restrict__ dK,
+                                                           const float4* __restrict__ dV, float4* __restrict__ out,
+                                                           int S, int H, int dh) {
+  const int t = blockIdx.x, b = t / S, s = t - b * S;
+  const int q = dh / 4, n = H * q;
+  for (int k = threadIdx.x; k < 3 * n; k += blockDim.x) {
+    const int which = k / n, kk = k - which * n, h = kk / q, c = kk - h * q;
+    const int64_t hm = (((int64_t)b * H + h) * S + s) * q + c;
+    out[(int64_t)t * 3 * n + k] = (which == 0 ? dQ : (which == 1 ? dK : dV))[hm];
+  }
+}
+
 // dQ, dK, dV [B,H,S,dh] -> dQKV [T][3d]
 __global__ void dqkv_tokens_kernel(const float* __restrict__ dQ, const float* __restrict__ dK,
                                    const float* __restrict__ dV, float* __restrict__ out, int B, int S, int H, int dh) {
@@ -116,6 +147,21 @@ template <typename TA>
 __global__ void add_kernel(const TA* __restrict__ a, const float* __restrict__ b, float* __restrict__ out, int64_t n) {
   GRID_LOOP(i, n) out[i] = load_f32(a, i) + b[i];
 }
+// the same, four elements per thread (16-byte aligned fp32 arrays, 8-byte aligned bf16)
+__device__ __forceinline__ float4 load4f(const float* p, int64_t i) { return ((const float4*)p)[i]; }
+__device__ __forceinline__ float4 load4f(const u16* p, int64_t i) {
+  const uint2 v = ((const uint2*)p)[i];
+  return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xFFFF0000u), __uint_as_float(v.y << 16),
+                     __uint_as_float(v.y & 0xFFFF0000u));
+}
+template <typename TA>
+__global__ __launch_bounds__(256) void add4_kernel(const TA* __restrict__ a, const float* __restrict__ b,
+                                                   float* __restrict__ out, int64_t n4) {
+  GRID_LOOP(i, n4) {
+    const float4 x = load4f(a, i), y = ((const float4*)b)[i];
+    ((float4*)out)[i] = make_float4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
+  }
+}
 
 // batched: grid (SUMSQ_BLOCKS, count); block b of job j sums x[i]^2 for i = b*256 + t, stepping
 // by the grid, then the 4 waves in order; the final kernel folds the job's partials in a
@@ -160,20 +206,35 @@ bs_status launch_qkv_heads(const float* qkv, int B, int S, int H, int dh, u16* Q
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
+static bool al(const void* p, int bytes) { return ((uintptr_t)p & (uintptr_t)(bytes - 1)) == 0; }
+// one block per token row (B S rows, at most 2^31 - 1)
+static bool rows_ok(int B, int S) { return (int64_t)B * S > 0 && (int64_t)B * S < 2147483647LL; }
 bs_status launch_heads_tokens_f32(const float* in, float* out, int B, int S, int H, int dh, bool to_tokens,
                                   hipStream_t st) {
-  heads_tokens_kernel<float><<<blocks_for((int64_t)B * S * H * dh), 256, 0, st>>>(in, out, B, S, H, dh, to_tokens);
+  if (dh % 4 == 0 && al(in, 16) && al(out, 16) && rows_ok(B, S))
+    heads_tokens4_kernel<float4><<<(unsigned)(B * S), 256, 0, st>>>((const float4*)in, (float4*)out, S, H, dh,
+                                                                   to_tokens);
+  else
+    heads_tokens_kernel<float><<<blocks_for((int64_t)B * S * H * dh), 256, 0, st>>>(in, out, B, S, H, dh, to_tokens);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
 bs_status launch_heads_tokens_u8(const uint8_t* in, uint8_t* out, int B, int S, int H, int dh, hipStream_t st) {
-  heads_tokens_kernel<uint8_t><<<blocks_for((int64_t)B * S * H * dh), 256, 0, st>>>(in, out, B, S, H, dh, 1);
+  if (dh % 4 == 0 && al(in, 4) && al(out, 4) && rows_ok(B, S))
+    heads_tokens4_kernel<uint32_t><<<(unsigned)(B * S), 256, 0, st>>>((const uint32_t*)in, (uint32_t*)out, S, H, dh,
+                                                                     1);
+  else
+    heads_tokens_kernel<uint8_t><<<blocks_for((int64_t)B * S * H * dh), 256, 0, st>>>(in, out, B, S, H, dh, 1);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
 bs_status launch_dqkv_tokens(const float* dQ, const float* dK, const float* dV, float* out, int B, int S, int H,
                              int dh, hipStream_t st) {
-  dqkv_tokens_kernel<<<blocks_for((int64_t)B * S * 3 * H * dh), 256, 0, st>>>(dQ, dK, dV, out, B, S, H, dh);
+  if (dh % 4 == 0 && al(dQ, 16) && al(dK, 16) && al(dV, 16) && al(out, 16) && rows_ok(B, S))
+    dqkv_tokens4_kernel<<<(unsigned)(B * S), 256, 0, st>>>((const float4*)dQ, (const float4*)dK, (const float4*)dV,
+                                                           (float4*)out, S, H, dh);
+  else
+    dqkv_tokens_kernel<<<blocks_for((int64_t)B * S * 3 * H * dh), 256, 0, st>>>(dQ, dK, dV, out, B, S, H, dh);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
@@ -206,7 +267,12 @@ bs_status launch_swiglu_bwd(const float* da, const float* gh, float* dgh, int64_
 }
 bs_status launch_add(const void* a, bs_dtype at, const float* b, float* out, int64_t n, hipStream_t st) {
   if (n <= 0) return BS_OK;
-  if (at == BS_F32)
+  const bool v4 = n % 4 == 0 && al(a, at == BS_F32 ? 16 : 8) && al(b, 16) && al(out, 16);
+  if (v4 && at == BS_F32)
+    add4_kernel<float><<<blocks_for(n / 4), 256, 0, st>>>((const float*)a, b, out, n / 4);
+  else if (v4)
+    add4_kernel<u16><<<blocks_for(n / 4), 256, 0, st>>>((const u16*)a, b, out, n / 4);
+  else if (at == BS_F32)
     add_kernel<float><<<blocks_for(n), 256, 0, st>>>((const float*)a, b, out, n);
   else
     add_kernel<u16><<<blocks_for(n), 256, 0, st>>>((const u16*)a, b, out, n);

@@ -151,44 +151,72 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const u16* __restri
 
 // The transposed planes of an fp32 [R, C] matrix (C and ldi multiples of 4, 16-byte aligned rows,
 // ldo a multiple of 64) split into nterms bf16 terms per value (the split of planes_t_kernel): a
-// thread splits 4 consecutive columns of a row, each output row leaves the LDS tile as 16-byte
-// stores of 8 consecutive rows of the input.
+// 64 x 64 tile goes into LDS as fp32 (rows padded to 65 words, so both the row writes and the
+// column reads below fall on distinct banks); a thread then splits 8 consecutive rows of one
+// column and stores them as one 16-byte piece per plane, eight threads covering 128 bytes of an
+// output row.
 __global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* __restrict__ in, int64_t R, int64_t C,
                                                                   int64_t ldi, PlaneOut out, int nterms, int64_t ldo,
                                                                   float scale) {
-  __shared__ __attribute__((aligned(16))) u16 tile[3][64][72];
-  const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  __shared__ float tile[64][65];
+  const int c4 = threadIdx.x & 15, rq = threadIdx.x >> 4;
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int rr = rg + 16 * i;
-    const int64_t r = r0 + rr, c = c0 + 4 * cg;
+    const int rr = rq + 16 * i;
+    const int64_t r = r0 + rr, c = c0 + 4 * c4;
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
     if (r < R && c < C) v = *(const float4*)(in + r * ldi + c);
-    const float x[4] = {v.x * scale, v.y * scale, v.z * scale, v.w * scale};
-    u16 o[4][3];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) split_to(x[q], nterms, o[q]);
-#pragma unroll
-    for (int p = 0; p < 3; ++p)
-      if (p < nterms)
-        *(uint2*)&tile[p][rr][4 * cg] = make_uint2((uint32_t)o[0][p] | ((uint32_t)o[1][p] << 16),
-                                                   (uint32_t)o[2][p] | ((uint32_t)o[3][p] << 16));
+    tile[rr][4 * c4] = v.x * scale;
+    tile[rr][4 * c4 + 1] = v.y * scale;
+    tile[rr][4 * c4 + 2] = v.z * scale;
+    tile[rr][4 * c4 + 3] = v.w * scale;
   }
   __syncthreads();
-  const int q8 = (threadIdx.x & 7) * 8;
+  const int rg = threadIdx.x & 7;
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
     const int cc = (threadIdx.x >> 3) + 32 * pass;
     const int64_t c = c0 + cc;
     if (c >= C) continue;
+    u16 o[8][3];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) split_to(tile[8 * rg + i][cc], nterms, o[i]);
 #pragma unroll
     for (int p = 0; p < 3; ++p) {
       if (p >= nterms) break;
       uint32_t w[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)tile[p][q8 + 2 * i][cc] | ((uint32_t)tile[p][q8 + 2 * i + 1][cc] << 16);
-      *(uint4*)(out.p[p] + c * ldo + r0 + q8) = make_uint4(w[0], w[1], w[2], w[3]);
+      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)o[2 * i][p] | ((uint32_t)o[2 * i + 1][p] << 16);
+      *(uint4*)(out.p[p] + c * ldo + r0 + 8 * rg) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+}
+
+// The row-major planes of an fp32 matrix, 8 elements per thread (C and ldi multiples of 4, ldo a
+// multiple of 8, 16-byte aligned input rows and planes): grid x over 2048-column pieces of a row,
+// grid y over rows; two 16-byte loads, one 16-byte store per plane, no index division.
+__global__ __launch_bounds__(256) void planes_rows8_kernel(const float* __restrict__ in, int64_t R, int64_t C,
+                                                           int64_t ldi, PlaneOut out, int nterms, int64_t ldo,
+                                                           float scale) {
+  const int64_t c = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
+  if (c >= ldo) return;
+  for (int64_t r = blockIdx.y; r < R; r += gridDim.y) {
+    float4 v0 = make_float4(0.f, 0.f, 0.f, 0.f), v1 = v0;
+    if (c < C) v0 = *(const float4*)(in + r * ldi + c);
+    if (c + 4 < C) v1 = *(const float4*)(in + r * ldi + c + 4);
+    const float x[8] = {v0.x * scale, v0.y * scale, v0.z * scale, v0.w * scale,
+                        v1.x * scale, v1.y * scale, v1.z * scale, v1.w * scale};
+    u16 o[8][3];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) split_to(x[k], nterms, o[k]);
+#pragma unroll
+    for (int p = 0; p < 3; ++p) {
+      if (p >= nterms) break;
+      uint32_t w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)o[2 * i][p] | ((uint32_t)o[2 * i + 1][p] << 16);
+      *(uint4*)(out.p[p] + r * ldo + c) = make_uint4(w[0], w[1], w[2], w[3]);
     }
   }
 }
@@ -217,9 +245,14 @@ bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64
     if (n <= 0) return BS_OK;
     const int64_t want = (n + 255) / 256;
     const unsigned blocks = (unsigned)(want < 8192 ? want : 8192);
+    bool vec8 = dt == BS_F32 && C % 4 == 0 && ldi % 4 == 0 && ldo % 8 == 0 && ((uintptr_t)in & 15) == 0;
+    for (int p = 0; p < nterms; ++p) vec8 = vec8 && ((uintptr_t)outp[p] & 15) == 0;
     bool vec4 = dt == BS_F32 && C % 4 == 0 && ldi % 4 == 0 && ldo % 4 == 0 && ((uintptr_t)in & 15) == 0;
     for (int p = 0; p < nterms; ++p) vec4 = vec4 && ((uintptr_t)outp[p] & 7) == 0;
-    if (vec4) {
+    if (vec8) {
+      const dim3 grid((unsigned)((ldo / 8 + 255) / 256), (unsigned)(R < 65535 ? R : 65535));
+      planes_rows8_kernel<<<grid, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
+    } else if (vec4) {
       const int64_t want4 = (n / 4 + 255) / 256;
       planes_rows4_kernel<<<(unsigned)(want4 < 8192 ? want4 : 8192), 256, 0, st>>>((const float*)in, R, C, ldi, out,
                                                                                    nterms, ldo, scale);
