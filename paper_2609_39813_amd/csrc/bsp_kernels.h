@@ -100,6 +100,12 @@ bs_status launch_init_diag(bs_diag* diag, hipStream_t st);
 // split of each fp32 value; bf16 inputs with nterms == 1 are copied).
 bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64_t ldi, bool transpose,
                         u16* const* out, int nterms, int64_t ldo, float scale, hipStream_t st);
+// The transposed planes (as launch_planes with transpose) of an fp32 in + add (add nullable), and
+// with outR non-null also the row-major planes out_R[r*ldr + c] from the same read. Needs C, ldi
+// and ldr multiples of 4, ldo of 64, 16-byte aligned in, add and outT, 8-byte aligned outR
+// (BS_EINVAL otherwise).
+bs_status launch_planes_t2(const float* in, const float* add, int64_t R, int64_t C, int64_t ldi, u16* const* outT,
+                           int nterms, int64_t ldo, u16* const* outR, int64_t ldr, hipStream_t st);
 
 // Trial statistics over per-trial rows (App. C.4, App. D.4).
 bs_status launch_policy_bias(const float* delta, int K, int64_t m, const float* g_ref, float* mean_err, float* se,

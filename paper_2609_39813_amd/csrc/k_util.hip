@@ -154,10 +154,12 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const u16* __restri
 // 64 x 64 tile goes into LDS as fp32 (rows padded to 65 words, so both the row writes and the
 // column reads below fall on distinct banks); a thread then splits 8 consecutive rows of one
 // column and stores them as one 16-byte piece per plane, eight threads covering 128 bytes of an
-// output row.
-__global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* __restrict__ in, int64_t R, int64_t C,
-                                                                  int64_t ldi, PlaneOut out, int nterms, int64_t ldo,
-                                                                  float scale) {
+// output row. Optional: add (nullable, same layout as in) is added before the split, and the
+// row-major planes (rows.p[0] non-null, leading dimension ldr) are written from the same read.
+__global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* __restrict__ in, const float* __restrict__ add,
+                                                                  int64_t R, int64_t C, int64_t ldi, PlaneOut out,
+                                                                  int nterms, int64_t ldo, float scale, PlaneOut rows,
+                                                                  int64_t ldr) {
   __shared__ float tile[64][65];
   const int c4 = threadIdx.x & 15, rq = threadIdx.x >> 4;
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
@@ -166,11 +168,26 @@ __global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* _
     const int rr = rq + 16 * i;
     const int64_t r = r0 + rr, c = c0 + 4 * c4;
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < R && c < C) v = *(const float4*)(in + r * ldi + c);
-    tile[rr][4 * c4] = v.x * scale;
-    tile[rr][4 * c4 + 1] = v.y * scale;
-    tile[rr][4 * c4 + 2] = v.z * scale;
-    tile[rr][4 * c4 + 3] = v.w * scale;
+    if (r < R && c < C) {
+      v = *(const float4*)(in + r * ldi + c);
+      if (add) {
+        const float4 b = *(const float4*)(add + r * ldi + c);
+        v = make_float4(v.x + b.x, v.y + b.y, v.z + b.z, v.w + b.w);
+      }
+    }
+    const float x[4] = {v.x * scale, v.y * scale, v.z * scale, v.w * scale};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) tile[rr][4 * c4 + q] = x[q];
+    if (rows.p[0] && r < R && c < C) {
+      u16 o[4][3];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) split_to(x[q], nterms, o[q]);
+#pragma unroll
+      for (int p = 0; p < 3; ++p)
+        if (p < nterms)
+          *(uint2*)(rows.p[p] + r * ldr + c) = make_uint2((uint32_t)o[0][p] | ((uint32_t)o[1][p] << 16),
+                                                          (uint32_t)o[2][p] | ((uint32_t)o[3][p] << 16));
+    }
   }
   __syncthreads();
   const int rg = threadIdx.x & 7;
@@ -235,7 +252,8 @@ bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64
     if (vec)
       transpose_bf16_kernel<<<grid, 256, 0, st>>>((const u16*)in, R, C, ldi, outp[0], ldo);
     else if (vecf)
-      transpose_split_f32_kernel<<<grid, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
+      transpose_split_f32_kernel<<<grid, 256, 0, st>>>((const float*)in, nullptr, R, C, ldi, out, nterms, ldo, scale,
+                                                       PlaneOut{{nullptr, nullptr, nullptr}}, 0);
     else if (dt == BS_F32)
       planes_t_kernel<float><<<grid, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
     else
@@ -261,6 +279,26 @@ bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64
     else
       planes_rows_kernel<u16><<<blocks, 256, 0, st>>>((const u16*)in, R, C, ldi, out, nterms, ldo, scale);
   }
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+bs_status launch_planes_t2(const float* in, const float* add, int64_t R, int64_t C, int64_t ldi, u16* const* outT,
+                           int nterms, int64_t ldo, u16* const* outR, int64_t ldr, hipStream_t st) {
+  if (nterms < 1 || nterms > 3) return BS_EINVAL;
+  if (C <= 0 || ldo <= 0) return BS_OK;
+  bool ok = C % 4 == 0 && ldi % 4 == 0 && ldo % 64 == 0 && ((uintptr_t)in & 15) == 0 && ((uintptr_t)add & 15) == 0 &&
+            (!outR || (ldr % 4 == 0 && ldr >= C));
+  for (int p = 0; p < nterms; ++p) {
+    ok = ok && ((uintptr_t)outT[p] & 15) == 0;
+    if (outR) ok = ok && ((uintptr_t)outR[p] & 7) == 0;
+  }
+  if (!ok) return BS_EINVAL;
+  const PlaneOut out{{outT[0], nterms > 1 ? outT[1] : nullptr, nterms > 2 ? outT[2] : nullptr}};
+  const PlaneOut rows{{outR ? outR[0] : nullptr, outR && nterms > 1 ? outR[1] : nullptr,
+                       outR && nterms > 2 ? outR[2] : nullptr}};
+  const dim3 grid((unsigned)((C + 63) / 64), (unsigned)((ldo + 63) / 64));
+  transpose_split_f32_kernel<<<grid, 256, 0, st>>>(in, add, R, C, ldi, out, nterms, ldo, 1.0f, rows, ldr);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

@@ -41,7 +41,7 @@ struct AlluWs {
   float *u1, *u2, *r1, *r2, *du1, *du2, *m, *l;
   u16 *Vt, *Qt, *Kt, *valT_u1, *valT_O, *dqkvT[3], *dhT[3];
   u16 *pA[3], *rows3[3], *tA[3], *tB[3], *dOp[3], *dOt[3];
-  float *dh_d, *dh_L, *dO_dt, *dO_dh, *dD, *dQ_d, *dK_d, *dV_d, *dqkv_d, *dqkv_L, *du1_d;
+  float *dh_d, *dO_dt, *dO_dh, *dD, *dQ_d, *dK_d, *dV_d, *dqkv_d, *du1_d;
   double* gpart;
   float* delta[NCOMP];      // this pass's moves
   float* bias[3][NCOMP];    // per letter
@@ -77,10 +77,9 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
     w.dOp[i] = c.take<u16>(Td);
     w.dOt[i] = c.take<u16>(bh * DH * Sp);
   }
-  for (float** p : {&w.dh_d, &w.dh_L, &w.dO_dt, &w.dO_dh, &w.dQ_d, &w.dK_d, &w.dV_d, &w.du1_d}) *p = c.take<float>(Td);
+  for (float** p : {&w.dh_d, &w.dO_dt, &w.dO_dh, &w.dQ_d, &w.dK_d, &w.dV_d, &w.du1_d}) *p = c.take<float>(Td);
   w.dD = c.take<float>(bh * S);
   w.dqkv_d = c.take<float>(3 * Td);
-  w.dqkv_L = c.take<float>(3 * Td);
   w.gpart = c.take<double>(3 * ((T + 15) / 16) * (int64_t)d);
   for (int i = 0; i < NCOMP; ++i) {
     w.delta[i] = c.take<float>(nc[i]);
@@ -213,19 +212,18 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         BS_TRY(planes_of(NP_RESU, io.Otok, io.c_Otok, s_O, w.pA, 3));
         BS_TRY(Gemm(d, d, (int)Tp, Tp, Tp, dWo, d, nullptr).add(w.pA, 3, w.dhT, 3).run(w.part, w.part_cap, st));
       } else {
-        BS_TRY(launch_planes(w.dh_d, BS_F32, T, d, d, true, w.tB, 3, Tp, 1.0f, st));
+        // dh_d's transposed planes (the weight use) and row planes (the move of dO), one read
+        BS_TRY(launch_planes_t2(w.dh_d, nullptr, T, d, d, w.tB, 3, Tp, w.rows3, d, st));
         Gemm gw(d, d, (int)Tp, Tp, Tp, dWo, d, s_O);
         gw.add(&w.valT_O, 1, w.tB, 3);
         if (l == LETTER_N) {
-          BS_TRY(launch_add(io.dh, BS_F32, w.dh_d, w.dh_L, Td, st));
-          BS_TRY(launch_planes(w.dh_L, BS_F32, T, d, d, true, w.tA, 3, Tp, 1.0f, st));
+          BS_TRY(launch_planes_t2(io.dh, w.dh_d, T, d, d, w.tA, 3, Tp, nullptr, 0, st));  // dh_L = dh + dh_d
           const TrialPlaneArgs ta{io.Otok, io.c_Otok, s_O, f, T, d, Tp, io.seed, 1 * 256 + 2, k, 1, w.pA[0]};
           BS_TRY(launch_trial_planes(ta, st));
           gw.add(&w.pA[0], 1, w.tA, 3);
         }
         BS_TRY(gw.run(w.part, w.part_cap, st));
         // the move of dO (token-major, then head-major)
-        BS_TRY(launch_planes(w.dh_d, BS_F32, T, d, d, false, w.rows3, 3, d, 1.0f, st));
         BS_TRY(Gemm((int)T, d, d, d, d, w.dO_dt, d, nullptr).add(w.rows3, 3, &io.Wo, 1).run(nullptr, 0, st));
         BS_TRY(launch_heads_tokens_f32(w.dO_dt, w.dO_dh, B, S, H, DH, false, st));
       }
@@ -266,19 +264,17 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         BS_TRY(launch_attn_bwd(ba, B, H, st));
         BS_TRY(launch_dqkv_tokens(w.dQ_d, w.dK_d, w.dV_d, w.dqkv_d, B, S, H, DH, st));
         // u1's weight use (Wqkv)
-        BS_TRY(launch_planes(w.dqkv_d, BS_F32, T, d3, d3, true, w.tB, 3, Tp, 1.0f, st));
+        BS_TRY(launch_planes_t2(w.dqkv_d, nullptr, T, d3, d3, w.tB, 3, Tp, w.rows3, d3, st));
         Gemm gq(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, s_u1);
         gq.add(&w.valT_u1, 1, w.tB, 3);
         if (l == LETTER_N) {
-          BS_TRY(launch_add(io.dqkv, BS_F32, w.dqkv_d, w.dqkv_L, 3 * Td, st));
-          BS_TRY(launch_planes(w.dqkv_L, BS_F32, T, d3, d3, true, w.tA, 3, Tp, 1.0f, st));
+          BS_TRY(launch_planes_t2(io.dqkv, w.dqkv_d, T, d3, d3, w.tA, 3, Tp, nullptr, 0, st));  // dqkv + dqkv_d
           const TrialPlaneArgs ta{w.u1, io.c_u1, s_u1, f, T, d, Tp, io.seed, 0 * 256 + 2, k, 1, w.pA[0]};
           BS_TRY(launch_trial_planes(ta, st));
           gq.add(&w.pA[0], 1, w.tA, 3);
         }
         BS_TRY(gq.run(w.part, w.part_cap, st));
         // the move of du1, then u1's gain and normalization-input uses
-        BS_TRY(launch_planes(w.dqkv_d, BS_F32, T, d3, d3, false, w.rows3, 3, d3, 1.0f, st));
         BS_TRY(Gemm((int)T, d, (int)d3, d3, d3, w.du1_d, d, nullptr).add(w.rows3, 3, &io.Wqkv, 1).run(nullptr, 0, st));
         const AlluGainArgs<u16> ag{io.x, w.r1, io.gain1, rd(w.u1, io.c_u1, s_u1, 0 * 256 + 1), w.du1, w.du1_d, T, d,
                                    w.gpart};
