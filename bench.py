@@ -440,7 +440,23 @@ def main():
              "gemm_TFLOP_per_step": round(flop / args.steps / 1e12, 4),
              "work": "forward, reference backward, U/R/N at the 10 uses of the 4 stores (K = 16 new roundings per "
                      "use), and U/R/N at every use together (K = 16 backward passes for N)"}
-    del xd, pd, dOd, ws
+    del ws
+    torch.cuda.empty_cache()
+    if not args.headline_only:
+        # the per-use table with every se (weight uses and dK under N by per-trial paths), the
+        # every-use rows included
+        log("side measurement: the decoder layer with the per-use se")
+        ws = bsp.decoder_layer_workspace(B, S, cfg["d"], H, cfg["F"], cfg["K"], dev, all_uses=True, per_use_se=True)
+        wall, t = _timed(bsp, torch, lambda: bsp.decoder_layer_policy(
+            xd, pd, dOd, B=B, S=S, H=H, fmt="e4m3", fwd_mode=cfg["fwd_mode"], K=cfg["K"], seed=cfg["seed"],
+            all_uses=True, all_outputs=False, per_use_se=True, ws=ws), ("gemm", "attn_bwd", "trial_planes"), 2)
+        extra["decoder_layer_with_per_use_se"] = {
+            "call_ms": round(wall * 1e3, 3), "policy_trials_per_s": round(n_pol * cfg["K"] / wall, 1),
+            "kernel_ms": {k: round(v, 4) for k, v in t.items()},
+            "work": "the headline step plus the se under N of the five weight uses (K per-trial contractions "
+                    "each) and of dK (K key-major attention passes)"}
+        del ws
+    del xd, pd, dOd
     torch.cuda.empty_cache()
     if not args.headline_only:
         log("side measurement: RMSNorm -> Linear at the MLP up-projection shape")

@@ -481,8 +481,13 @@ bs_status bs_gemm_bf16_nt(const void* A, int64_t lda, const void* B, int64_t ldb
  *   dgain2 [d], dWg [d,F], dWu [d,F], dWd [F,d].
  *   stores (each nullable): codes of u1 [T,d], O [B,H,S,64], u2 [T,d], a [T,F]; scales [4].
  *   table [BS_LAYER_ROWS][3 letters U,R,N][3] fp64: sum of squared bias, sum of squared
- *   reference, sum of squared se of the row's gradient under the letter; NaN where the build
- *   has no estimate (N at a normalization-input use, se of a weight use or of dK under N).
+ *   reference, sum of squared se of the row's gradient under the letter; NaN where there is no
+ *   estimate: N at a normalization-input use (read unrounded, App. D.4), and, unless
+ *   per_use_se is set, the se of a weight use and of dK under N.
+ *   per_use_se != 0: those se by per-trial paths (App. C.4): at each weight use trial k's
+ *   residual enters its own contraction with the incoming gradient, at the D use one key-major
+ *   attention pass per trial gives dK; shifted fp64 sums over the K trials. Costs K extra
+ *   contractions per weight use and K key-major passes.
  *   Rows: 0 u1 gain, 1 u1 weight (dWqkv), 2 u1 norm-input (dX), 3 O D (dQ), 4 O D (dK),
  *   5 O weight (dWo), 6 u2 gain, 7 u2 weight ([dWg | dWu]), 8 u2 norm-input, 9 a weight (dWd).
  *   all (nullable): each letter read at every use of every store together, in one backward whose
@@ -497,7 +502,8 @@ bs_status bs_gemm_bf16_nt(const void* A, int64_t lda, const void* B, int64_t ldb
  *   diags [4] (nullable; one per store). Every pointer is device memory (the structs themselves
  *   are host memory); outputs are owned by the caller.
  *   ws: device workspace, 256-byte aligned, of bs_decoder_layer_workspace_size(B,S,d,H,F,K,
- *   all_uses) bytes, all_uses != 0 when `all` is set (0 for shapes the call rejects).
+ *   options) bytes, options = BS_LAYER_ALL_USES when `all` is set | BS_LAYER_PER_USE_SE when
+ *   per_use_se is (0 for shapes the call rejects).
  *   Returns BS_EINVAL for a null required pointer, K outside [1, 4096], eps < 0, an unknown
  *   format or mode, or a partly set `fixed`; BS_ESHAPE unless d = 64*H <= 8192, F a multiple of
  *   8 and B*H <= 65535; BS_EWORKSPACE for a short or misaligned workspace; BS_EHIP on a failed
@@ -530,12 +536,14 @@ typedef struct {
   double* table;           /* [8][3][3] */
 } bs_layer_all;
 
-size_t bs_decoder_layer_workspace_size(int B, int S, int d, int H, int F, int K, int all_uses);
+#define BS_LAYER_ALL_USES 1   /* workspace option: the every-use-at-once check */
+#define BS_LAYER_PER_USE_SE 2 /* workspace option: the per-use se of the weight uses and of dK */
+size_t bs_decoder_layer_workspace_size(int B, int S, int d, int H, int F, int K, int options);
 bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* w, const void* dOut, int B, int S, int d,
                                   int H, int F, float eps, bs_fp8 fmt, bs_round fwd_mode, int K, uint64_t seed,
                                   const bs_layer_forward* fixed, bs_layer_grads grads, bs_layer_stores stores,
-                                  double* table, const bs_layer_all* all, bs_diag* diags, void* ws, size_t ws_bytes,
-                                  void* stream);
+                                  double* table, const bs_layer_all* all, int per_use_se, bs_diag* diags, void* ws,
+                                  size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------------------
  * Kernel timing instrumentation (host calls; for benchmarks and profiling).

@@ -129,8 +129,8 @@ class LayerAll(ctypes.Structure):
 _layer_ws = _sig("bs_decoder_layer_workspace_size", _sz, [_int] * 7)
 _layer = _sig("bs_decoder_layer_policy", _int,
               [_vp, ctypes.POINTER(LayerWeights), _vp, _int, _int, _int, _int, _int, _f32, _int, _int, _int, _u64,
-               ctypes.POINTER(LayerForward), LayerGrads, LayerStores, _vp, ctypes.POINTER(LayerAll), _vp, _vp, _sz,
-               _vp])
+               ctypes.POINTER(LayerForward), LayerGrads, LayerStores, _vp, ctypes.POINTER(LayerAll), _int, _vp, _vp,
+               _sz, _vp])
 
 _prof_enable = _sig("bs_profile_enable", _int, [_int])
 _prof_read = _sig("bs_profile_read", _int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_int)])
@@ -603,22 +603,26 @@ LAYER_ROWS = (("u1", "gain", "dgain"), ("u1", "weight", "dW"), ("u1", "norm_inpu
 LAYER_GRADS = ("dx", "dgain1", "dWqkv", "dWo", "dgain2", "dWg", "dWu", "dWd")
 
 
-def decoder_layer_workspace(B, S, d, H, F, K, device, all_uses=False):
-    n = _layer_ws(B, S, d, H, F, K, int(all_uses))
+LAYER_ALL_USES, LAYER_PER_USE_SE = 1, 2
+
+
+def decoder_layer_workspace(B, S, d, H, F, K, device, all_uses=False, per_use_se=False):
+    n = _layer_ws(B, S, d, H, F, K, (LAYER_ALL_USES if all_uses else 0) | (LAYER_PER_USE_SE if per_use_se else 0))
     if n == 0:
         raise BspError(3, "bs_decoder_layer_workspace_size")
     return _workspace(n, device)
 
 
 def decoder_layer_policy(x, p, dOut, *, B, S, H, eps=1e-5, fmt="e4m3", fwd_mode="rne", K=16, seed=0, fixed=None,
-                         all_uses=False, all_outputs=True, ws=None):
+                         all_uses=False, all_outputs=True, per_use_se=False, ws=None):
     """One decoder layer with four FP8 stores and the per-use check of every store
     (bs_decoder_layer_policy). p: gain1, gain2 fp32 [d]; Wqkv, Wo, Wg, Wu, Wd bf16. fixed:
     None, or the realized forward {Q, K, V (bf16 [B,H,S,64]), O ([B,H,S,64]), h, gh ([T,2F]),
     a ([T,F]) fp32}. Returns the table as {(store, use, grad, letter): (bias^2, ref^2, se^2)}
     plus reference gradients, store codes and scales. all_uses: also each letter read at every use
     together ("all_bias" / "all_se": {letter: {gradient: tensor}}, only with all_outputs, and
-    "all_table_raw" [8][3][3])."""
+    "all_table_raw" [8][3][3]). per_use_se: the table's se of the weight uses and of dK under N by
+    per-trial paths (NaN without)."""
     T, d = x.shape
     F = p["Wg"].shape[1]
     dev = x.device
@@ -656,9 +660,10 @@ def decoder_layer_policy(x, p, dOut, *, B, S, H, eps=1e-5, fmt="e4m3", fwd_mode=
                 al.se[i] = LayerGrads(*[out["all_se"][l][g].data_ptr() for g in LAYER_GRADS])
         allp = ctypes.byref(al)
     if ws is None:
-        ws = decoder_layer_workspace(B, S, d, H, F, K, dev, all_uses)
+        ws = decoder_layer_workspace(B, S, d, H, F, K, dev, all_uses, per_use_se)
     _check(_layer(_p(x), ctypes.byref(wts), _p(dOut), B, S, d, H, F, eps, _FMT[fmt], _MODE[fwd_mode], K, seed, fx,
-                  grads, stores, _p(out["table_raw"]), allp, _p(out["diags"]), _p(ws), ws.numel(), _stream()),
+                  grads, stores, _p(out["table_raw"]), allp, int(per_use_se), _p(out["diags"]), _p(ws), ws.numel(),
+                  _stream()),
            "bs_decoder_layer_policy")
     return out
 

@@ -21,7 +21,9 @@ namespace {
 // Weight use of a stored tensor X [T, k] (Sec. 4.1): dW = X_read^T dY [k, n] under U (the
 // original), R (the forward's rounding: no bias) and N (mean of K new roundings at the store's
 // scale, trials 1..K, use id `use`, token-major element order). The biases are contractions of
-// residual operands with dY: U adds (X - s val(C))^T dY, N adds (s/K)(n_up - K h)^T dY.
+// residual operands with dY: U adds (X - s val(C))^T dY, N adds (s/K)(n_up - K h)^T dY. With
+// se_n set, N's se over trials by the per-trial path: trial k's residual s(val(C_k) - val(C))
+// in its own contraction (trials stacked along the output rows), shifted fp64 sums over trials.
 // ------------------------------------------------------------------------------------
 struct WeightUseIO {
   const float* Xs;       // [T][k] fp32 store input
@@ -36,15 +38,22 @@ struct WeightUseIO {
   uint32_t use;
   float* dW_ref;         // [k][n]
   float* bias;           // [3][k][n] for U, R, N
+  float* se_n = nullptr; // [k][n] nullable: N's se (the per-trial path)
 };
+
+// trials per per-trial contraction (stacked along the output rows)
+inline int wu_trial_batch(int K) { return K < 8 ? K : 8; }
 
 struct WeightUseWs {
   u16 *dyT[3], *valT, *res[3], *counts;
   float *bias_u, *bias_n, *gpart;
   int64_t gpart_cap;
+  u16* tplanes;  // per-trial residual planes [BT][k][Tp]
+  float *tdelta, *td1;
+  double *tS1, *tS2;
 };
 
-WeightUseWs carve_wu(Carver& c, int64_t T, int64_t k, int64_t n) {
+WeightUseWs carve_wu(Carver& c, int64_t T, int64_t k, int64_t n, int K = 1, bool se = false) {
   WeightUseWs w{};
   const int64_t Tp = round_up(T > 0 ? T : 1, 64);
   for (int i = 0; i < 3; ++i) w.dyT[i] = c.take<u16>(n * Tp);
@@ -55,15 +64,24 @@ WeightUseWs carve_wu(Carver& c, int64_t T, int64_t k, int64_t n) {
   w.bias_n = c.take<float>(k * n);
   w.gpart_cap = 16 * k * n;  // split-K partials: the long-T contraction has few output tiles
   w.gpart = c.take<float>(w.gpart_cap);
+  if (se) {
+    const int bt = wu_trial_batch(K);
+    w.tplanes = c.take<u16>(bt * k * Tp);
+    w.tdelta = c.take<float>(bt * k * n);
+    w.td1 = c.take<float>(k * n);
+    w.tS1 = c.take<double>(k * n);
+    w.tS2 = c.take<double>(k * n);
+  }
   return w;
 }
 
 bs_status weight_use_run(const WeightUseIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
+  const bool se = io.se_n != nullptr;
   Carver probe;
-  carve_wu(probe, io.T, io.k, io.n);
+  carve_wu(probe, io.T, io.k, io.n, io.K, se);
   if (ws_bytes < probe.used()) return BS_EWORKSPACE;
   Carver c(ws, ws_bytes);
-  const WeightUseWs w = carve_wu(c, io.T, io.k, io.n);
+  const WeightUseWs w = carve_wu(c, io.T, io.k, io.n, io.K, se);
   const int64_t Tp = round_up(io.T > 0 ? io.T : 1, 64);
   const int nt = io.gt == BS_F32 ? 3 : 1;
   BS_TRY(launch_planes(io.dY, io.gt, io.T, io.n, io.n, true, w.dyT, nt, Tp, 1.0f, st));
@@ -115,6 +133,31 @@ bs_status weight_use_run(const WeightUseIO& io, void* ws, size_t ws_bytes, hipSt
   const float* b[3] = {w.bias_u, nullptr, w.bias_n};
   for (int l = 0; l < 3; ++l)
     BS_TRY(launch_combine(io.dW_ref, b[l], nullptr, kn, nullptr, io.bias + l * kn, nullptr, st));
+  if (se) {
+    const int bt = wu_trial_batch(io.K);
+    for (int k0 = 1; k0 <= io.K; k0 += bt) {
+      const int nb = io.K - k0 + 1 < bt ? io.K - k0 + 1 : bt;
+      const TrialPlaneArgs ta{io.Xs, io.codes, io.scale, pa.f, io.T, io.k, Tp, io.seed, io.use, k0, nb, w.tplanes};
+      BS_TRY(launch_trial_planes(ta, st));
+      GemmArgs g{};
+      g.M = (int)(nb * io.k);
+      g.N = (int)io.n;
+      g.K = (int)Tp;
+      g.lda = Tp;
+      g.ldb = Tp;
+      g.ldc = io.n;
+      g.alpha = 1.0f;
+      g.alpha_dev = io.scale;
+      g.C = w.tdelta;
+      g.part = w.gpart;
+      g.part_cap = w.gpart_cap;
+      const u16* A0 = w.tplanes;
+      if (!gemm_add_products(g, &A0, 1, w.dyT, nt)) return BS_EINVAL;
+      BS_TRY(launch_gemm(g, st));
+      BS_TRY(launch_trial_accum(w.tdelta, nb, k0, kn, w.td1, w.tS1, w.tS2, st));
+    }
+    BS_TRY(launch_trial_se(w.tS1, w.tS2, io.K, kn, io.se_n, st));
+  }
   return BS_OK;
 }
 
@@ -126,6 +169,7 @@ constexpr int NPOL = 4;  // U/U, R/R, N/N, and U with the R reading at the norma
 
 struct NormEst {
   float *g_bias, *g_se, *w_bias, *x_bias;  // [NPOL][d], [NPOL][d], [NPOL][d*n], [NPOL][T*d]
+  float* w_se = nullptr;                   // [NPOL][d*n] (the per-use se option)
 };
 
 struct LayerWs {
@@ -135,6 +179,7 @@ struct LayerWs {
   uint8_t *c_u1, *c_O, *c_Otok, *c_u2, *c_a;
   NormEst e1, e2;
   float *q_bias, *q_se, *k_bias, *wo_bias, *wd_bias;
+  float *k_se = nullptr, *wo_se = nullptr, *wd_se = nullptr;  // the per-use se option
   double* part;
   bs_diag* diag;
   void* sub;
@@ -143,14 +188,14 @@ struct LayerWs {
   size_t allu_bytes;
 };
 
-size_t sub_ws_size(int B, int S, int d, int H, int F, int K) {
+size_t sub_ws_size(int B, int S, int d, int H, int F, int K, bool se) {
   const int64_t T = (int64_t)B * S;
   size_t m = norm_ws_size(T, d, 3 * (int64_t)d, K);
   m = std::max(m, norm_ws_size(T, d, 2 * (int64_t)F, K));
-  m = std::max(m, attn_ws_size(B, H, S, DH));
+  m = std::max(m, attn_ws_size(B, H, S, DH, K, se));
   Carver c1, c2, c3;
-  carve_wu(c1, T, d, d);
-  carve_wu(c2, T, F, d);
+  carve_wu(c1, T, d, d, K, se);
+  carve_wu(c2, T, F, d, K, se);
   for (int i = 0; i < 3; ++i) c3.take<u16>(T * d);
   return std::max(m, std::max(c1.used(), std::max(c2.used(), c3.used())));
 }
@@ -164,7 +209,7 @@ NormEst carve_est(Carver& c, int64_t T, int64_t d, int64_t n) {
   return e;
 }
 
-LayerWs carve_layer(Carver& c, int B, int S, int d, int H, int F, int K, bool all_uses) {
+LayerWs carve_layer(Carver& c, int B, int S, int d, int H, int F, int K, bool all_uses, bool se) {
   LayerWs w{};
   const int64_t T = (int64_t)B * S, Td = T * d, TF = T * (int64_t)F;
   w.qkv = c.take<float>(3 * Td);
@@ -210,9 +255,16 @@ LayerWs carve_layer(Carver& c, int B, int S, int d, int H, int F, int K, bool al
   w.k_bias = c.take<float>(3 * Td);
   w.wo_bias = c.take<float>(3 * (int64_t)d * d);
   w.wd_bias = c.take<float>(3 * (int64_t)F * d);
+  if (se) {  // the per-use se under N of the weight uses and of dK
+    w.e1.w_se = c.take<float>(NPOL * (int64_t)d * 3 * d);
+    w.e2.w_se = c.take<float>(NPOL * (int64_t)d * 2 * F);
+    w.k_se = c.take<float>(3 * Td);
+    w.wo_se = c.take<float>((int64_t)d * d);
+    w.wd_se = c.take<float>((int64_t)F * d);
+  }
   w.part = c.take<double>(sumsq_part_size());
   w.diag = c.take<bs_diag>(4);
-  w.sub_bytes = sub_ws_size(B, S, d, H, F, K);
+  w.sub_bytes = sub_ws_size(B, S, d, H, F, K, se);
   w.sub = c.take<char>(w.sub_bytes);
   if (all_uses) {
     w.allu_bytes = allu_ws_size(B, S, d, H, F);
@@ -231,19 +283,21 @@ bool layer_shape_ok(int B, int S, int d, int H, int F) {
 
 extern "C" {
 
-size_t bs_decoder_layer_workspace_size(int B, int S, int d, int H, int F, int K, int all_uses) {
+size_t bs_decoder_layer_workspace_size(int B, int S, int d, int H, int F, int K, int options) {
   if (!layer_shape_ok(B, S, d, H, F) || K < 1 || K > 4096) return 0;
   Carver c;
-  carve_layer(c, B, S, d, H, F, K, all_uses != 0);
+  carve_layer(c, B, S, d, H, F, K, (options & BS_LAYER_ALL_USES) != 0, (options & BS_LAYER_PER_USE_SE) != 0);
   return c.used();
 }
 
 bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, const void* dOut, int B, int S, int d,
                                   int H, int F, float eps, bs_fp8 fmt, bs_round fwd_mode, int K, uint64_t seed,
                                   const bs_layer_forward* fixed, bs_layer_grads grads, bs_layer_stores stores,
-                                  double* table, const bs_layer_all* all, bs_diag* diags, void* ws, size_t ws_bytes,
-                                  void* stream) {
+                                  double* table, const bs_layer_all* all, int per_use_se, bs_diag* diags, void* ws,
+                                  size_t ws_bytes, void* stream) {
   hipStream_t st = (hipStream_t)stream;
+  const bool se = per_use_se != 0;
+  const int options = (all ? BS_LAYER_ALL_USES : 0) | (se ? BS_LAYER_PER_USE_SE : 0);
   if (!x || !wt || !dOut || !table || !wt->gain1 || !wt->Wqkv || !wt->Wo || !wt->gain2 || !wt->Wg || !wt->Wu ||
       !wt->Wd)
     return BS_EINVAL;
@@ -252,10 +306,10 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
   if (!layer_shape_ok(B, S, d, H, F)) return BS_ESHAPE;
   if (fixed && (!fixed->Q || !fixed->K || !fixed->V || !fixed->O || !fixed->h || !fixed->gh || !fixed->a))
     return BS_EINVAL;
-  if (!ws || ((uintptr_t)ws & 255) || ws_bytes < bs_decoder_layer_workspace_size(B, S, d, H, F, K, all ? 1 : 0))
+  if (!ws || ((uintptr_t)ws & 255) || ws_bytes < bs_decoder_layer_workspace_size(B, S, d, H, F, K, options))
     return BS_EWORKSPACE;
   Carver c(ws, ws_bytes);
-  const LayerWs w = carve_layer(c, B, S, d, H, F, K, all != nullptr);
+  const LayerWs w = carve_layer(c, B, S, d, H, F, K, all != nullptr, se);
   const int64_t T = (int64_t)B * S, Td = T * d, TF = T * (int64_t)F;
   const int64_t d3d = (int64_t)d * 3 * d, d2F = (int64_t)d * 2 * F, dd = (int64_t)d * d, Fd = (int64_t)F * d;
   bs_diag* dg = diags ? diags : w.diag;
@@ -334,7 +388,8 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
 
   // ---------------- reference backward, each use checked where its gradient arrives ----------------
   // store a, weight use of Wd (incoming gradient dOut)
-  const WeightUseIO wa{a, c_a, scales + 3, fmt, dOut, BS_BF16, T, F, d, K, seed, 3 * 256 + 2, dWd, w.wd_bias};
+  const WeightUseIO wa{a, c_a, scales + 3, fmt, dOut, BS_BF16, T, F, d, K, seed, 3 * 256 + 2, dWd, w.wd_bias,
+                       w.wd_se};
   BS_TRY(weight_use_run(wa, w.sub, w.sub_bytes, st));
   {  // da = dOut Wd^T
     GemmArgs g{};
@@ -355,13 +410,13 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
   // store u2: gain, weight ([Wg | Wu]) and normalization-input uses (incoming gradient [dg | dhh])
   const NormIO b2{h, BS_F32, wt->gain2, w.Wgu, BS_BF16, w.dgh, BS_F32, T, d, 2 * (int64_t)F, eps, fmt, fwd_mode,
                   npol, NPOL, K, seed, 2, nullptr, c_u2, scales + 2, dgain2, w.dWgu, w.dxn2,
-                  bs_est{nullptr, w.e2.g_bias, w.e2.g_se}, bs_est{nullptr, w.e2.w_bias, nullptr},
+                  bs_est{nullptr, w.e2.g_bias, w.e2.g_se}, bs_est{nullptr, w.e2.w_bias, w.e2.w_se},
                   bs_est{nullptr, w.e2.x_bias, nullptr}, dg + 2};
   BS_TRY(norm_run(b2, w.sub, w.sub_bytes, st));
   BS_TRY(launch_add(dOut, BS_BF16, w.dxn2, w.dh, Td, st));
   // store O, weight use of Wo (incoming gradient dh)
   const WeightUseIO wo{w.Otok, w.c_Otok, scales + 1, fmt, w.dh, BS_F32, T, d, d, K, seed, 1 * 256 + 2, dWo,
-                       w.wo_bias};
+                       w.wo_bias, w.wo_se};
   BS_TRY(weight_use_run(wo, w.sub, w.sub_bytes, st));
   {  // dO (token-major) = dh Wo^T with dh in three exact bf16 terms
     Carver cs(w.sub, w.sub_bytes);
@@ -384,13 +439,13 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
   BS_TRY(launch_heads_tokens_f32(w.dOtok, w.dOh, B, S, H, DH, false, st));
   const AttnIO ba{Q, Kk, V, nullptr, w.dOh, B, H, S, DH, 1, c_attn, O, fmt, fwd_mode, apol, 3, K, seed, 1, nullptr,
                   c_O, scales + 1, w.dQ, w.dK, w.dV, nullptr, bs_est{nullptr, w.q_bias, w.q_se},
-                  bs_est{nullptr, w.k_bias, nullptr}, dg + 1};
+                  bs_est{nullptr, w.k_bias, w.k_se}, dg + 1};
   BS_TRY(attn_run(ba, w.sub, w.sub_bytes, st));
   BS_TRY(launch_dqkv_tokens(w.dQ, w.dK, w.dV, w.dqkv, B, S, H, DH, st));
   // store u1: gain, weight (Wqkv) and normalization-input uses (incoming gradient dQKV)
   const NormIO b1{x, BS_BF16, wt->gain1, wt->Wqkv, BS_BF16, w.dqkv, BS_F32, T, d, 3 * (int64_t)d, eps, fmt, fwd_mode,
                   npol, NPOL, K, seed, 0, nullptr, c_u1, scales + 0, dgain1, dWqkv, w.dxn1,
-                  bs_est{nullptr, w.e1.g_bias, w.e1.g_se}, bs_est{nullptr, w.e1.w_bias, nullptr},
+                  bs_est{nullptr, w.e1.g_bias, w.e1.g_se}, bs_est{nullptr, w.e1.w_bias, w.e1.w_se},
                   bs_est{nullptr, w.e1.x_bias, nullptr}, dg + 0};
   BS_TRY(norm_run(b1, w.sub, w.sub_bytes, st));
   float* dx = grads.dx ? grads.dx : w.dx;
@@ -419,17 +474,18 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
       put(se, n, out + 2);
   };
   for (int l = 0; l < 3; ++l) {  // npol[l] reads letter l at the gain and weight uses
-    const float* wse = l == 2 ? kNaN : kZero;
+    // N's se at the weight uses and of dK: the per-use se option (kNaN without it)
+    auto nse = [&](float* arr, int64_t off) -> const float* { return l != 2 ? kZero : (se ? arr + off : kNaN); };
     row(0, l, w.e1.g_bias + l * d, dgain1, l == 2 ? w.e1.g_se + l * d : kZero, d);
-    row(1, l, w.e1.w_bias + l * d3d, dWqkv, wse, d3d);
+    row(1, l, w.e1.w_bias + l * d3d, dWqkv, nse(w.e1.w_se, l * d3d), d3d);
     row(2, l, l == 2 ? nullptr : w.e1.x_bias + (l == 0 ? 0 : 3) * Td, w.dxn1, kZero, Td);
     row(3, l, w.q_bias + l * Td, w.dQ, l == 2 ? w.q_se + l * Td : kZero, Td);
-    row(4, l, w.k_bias + l * Td, w.dK, wse, Td);
-    row(5, l, w.wo_bias + l * dd, dWo, wse, dd);
+    row(4, l, w.k_bias + l * Td, w.dK, nse(w.k_se, l * Td), Td);
+    row(5, l, w.wo_bias + l * dd, dWo, nse(w.wo_se, 0), dd);
     row(6, l, w.e2.g_bias + l * d, dgain2, l == 2 ? w.e2.g_se + l * d : kZero, d);
-    row(7, l, w.e2.w_bias + l * d2F, w.dWgu, wse, d2F);
+    row(7, l, w.e2.w_bias + l * d2F, w.dWgu, nse(w.e2.w_se, l * d2F), d2F);
     row(8, l, l == 2 ? nullptr : w.e2.x_bias + (l == 0 ? 0 : 3) * Td, w.dxn2, kZero, Td);
-    row(9, l, w.wd_bias + l * Fd, dWd, wse, Fd);
+    row(9, l, w.wd_bias + l * Fd, dWd, nse(w.wd_se, 0), Fd);
   }
   BS_TRY(launch_sumsq_batch(batch, w.part, st));
 

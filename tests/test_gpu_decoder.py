@@ -38,12 +38,12 @@ def fixed_of(f):
             "O": cu(f["O"]), "h": cu(f["h"]), "gh": cu(np.concatenate([f["g"], f["hh"]], axis=1)), "a": cu(f["a"])}
 
 
-def run(lib, inputs, B, S, H, K, seed, fmt, mode, fixed):
+def run(lib, inputs, B, S, H, K, seed, fmt, mode, fixed, per_use_se=False):
     x, p, dOut = inputs
     print(f"[layer] B={B} S={S} d={x.shape[1]} H={H} F={p['Wg'].shape[1]} K={K} fmt={fmt} mode={mode} "
-          f"fixed={fixed is not None}", flush=True)
+          f"fixed={fixed is not None} per_use_se={per_use_se}", flush=True)
     out = lib.decoder_layer_policy(x.cuda(), {k: v.cuda() for k, v in p.items()}, dOut.cuda(), B=B, S=S, H=H,
-                                   fmt=fmt, fwd_mode=mode, K=K, seed=seed, fixed=fixed)
+                                   fmt=fmt, fwd_mode=mode, K=K, seed=seed, fixed=fixed, per_use_se=per_use_se)
     torch.cuda.synchronize()
     return out
 
@@ -55,13 +55,15 @@ def check_sumsq(got, want, what):
         assert abs(got - want) <= TOL2 * want, (what, got, want, abs(got - want) / want)
 
 
-@pytest.mark.parametrize("B,S,d,H,F,K,seed,fmt,mode", [
-    (2, 40, 128, 2, 256, 8, 11, "e4m3", "rne"),   # T = 80: one full and one ragged 64-row tile
-    (1, 72, 64, 1, 136, 5, 12, "e5m2", "sr"),     # F = 136: ragged GEMM columns
+@pytest.mark.parametrize("B,S,d,H,F,K,seed,fmt,mode,per_use_se", [
+    (2, 40, 128, 2, 256, 8, 11, "e4m3", "rne", False),   # T = 80: one full and one ragged 64-row tile
+    (1, 72, 64, 1, 136, 5, 12, "e5m2", "sr", False),     # F = 136: ragged GEMM columns
+    (2, 40, 128, 2, 256, 11, 13, "e4m3", "rne", True),   # the per-use se (K = 11: a partial trial batch)
+    (1, 72, 64, 1, 136, 1, 14, "e5m2", "sr", True),      # K = 1: se 0
 ])
-def test_layer_matches_oracle_with_fixed_forward(lib, B, S, d, H, F, K, seed, fmt, mode):
+def test_layer_matches_oracle_with_fixed_forward(lib, B, S, d, H, F, K, seed, fmt, mode, per_use_se):
     inputs, f, r, table = oracle_case(B, S, d, H, F, K, seed, fmt, mode, config=600 + seed)
-    out = run(lib, inputs, B, S, H, K, seed, fmt, mode, fixed_of(f))
+    out = run(lib, inputs, B, S, H, K, seed, fmt, mode, fixed_of(f), per_use_se)
     # the four stores, bit for bit
     for name, q in (("u1", f["q1"]), ("O", f["qO"]), ("u2", f["q2"]), ("a", f["qa"])):
         codes = to_np(out["codes_" + name])
@@ -85,7 +87,14 @@ def test_layer_matches_oracle_with_fixed_forward(lib, B, S, d, H, F, K, seed, fm
         else:
             assert key[1] == "norm_input" and key[3] == "N" and np.isnan(b2), key
         if np.isnan(s2):
-            assert key[3] == "N" and (key[1] in ("weight", "norm_input") or key[2] == "dK"), key
+            if per_use_se:
+                assert key[3] == "N" and key[1] == "norm_input", key
+            else:
+                assert key[3] == "N" and (key[1] in ("weight", "norm_input") or key[2] == "dK"), key
+    if per_use_se:  # every N row but the normalization inputs has its se
+        for key in table:
+            if key[3] == "N":
+                assert not np.isnan(got[key][2]), key
 
 
 def test_layer_own_forward_is_a_valid_realization(lib):

@@ -49,17 +49,21 @@ def test_decoder_layer_workspace_rejects_bad_shapes():
     f = lib.bs_decoder_layer_workspace_size
     f.restype = ctypes.c_size_t
     f.argtypes = [ctypes.c_int] * 7
-    for all_uses in (0, 1):
-        assert f(2, 24, 128, 2, 256, 4, all_uses) > 0
-        assert f(2, 24, 128, 3, 256, 4, all_uses) == 0      # d != 64 * H
-        assert f(2, 24, 128, 2, 252, 4, all_uses) == 0      # F not a multiple of 8
-        assert f(2, 24, 128, 2, 256, 0, all_uses) == 0      # K < 1
-        assert f(2, 24, 128, 2, 256, 4097, all_uses) == 0   # K > 4096
+    for opts in (0, 1, 2, 3):  # bit 0: every use at once, bit 1: the per-use se
+        assert f(2, 24, 128, 2, 256, 4, opts) > 0
+        assert f(2, 24, 128, 3, 256, 4, opts) == 0      # d != 64 * H
+        assert f(2, 24, 128, 2, 252, 4, opts) == 0      # F not a multiple of 8
+        assert f(2, 24, 128, 2, 256, 0, opts) == 0      # K < 1
+        assert f(2, 24, 128, 2, 256, 4097, opts) == 0   # K > 4096
     # sized for the whole layer: at least the fp32 activations and the four stores' estimates
     T, d, F = 48, 128, 256
     assert f(2, 24, d, 2, F, 4, 0) >= 4 * T * (10 * d + 6 * F)
     # the every-use check adds its moved gradients and their trial sums
     assert f(2, 24, d, 2, F, 4, 1) >= f(2, 24, d, 2, F, 4, 0) + 20 * T * d
+    # the per-use se adds the se of both normalization stores' weight uses (4 policies each), of
+    # dK under U / R / N and of the Wo and Wd weight uses
+    se_floats = 4 * d * 3 * d + 4 * d * 2 * F + 3 * T * d + d * d + F * d
+    assert f(2, 24, d, 2, F, 4, 2) >= f(2, 24, d, 2, F, 4, 0) + 4 * se_floats
 
 
 @pytest.mark.skipif(not os.path.exists(LIB), reason="libbsp.so not built")
