@@ -503,12 +503,17 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
 //   bias_v = -c dD_v G (row-scaled), se_N = c |G| sd_N / sqrt(K).
 // S^T = K Q^T and dP^T = V dO^T put keys on the k index of the dS / P operands.
 // ------------------------------------------------------------------------------------
+// The key block's tiles (K, V, K^T) arrive by buffer loads straight into LDS, two stages as two
+// LDS variables (the loop is unrolled by two so that every access names one of them: loads into
+// one stage are then not awaited before reads of the other); one barrier per key block.
 template <int NDO>
 __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 sm[2][3][AT * AT];  // K, V, K^T
+  __shared__ __attribute__((aligned(1024))) u16 sm0[3][AT * AT];  // K, V, K^T
+  __shared__ __attribute__((aligned(1024))) u16 sm1[3][AT * AT];
   // heaviest (most key blocks) first: blocks are dispatched in index order
   const int bh = blockIdx.x, qb = a.causal ? (int)gridDim.y - 1 - (int)blockIdx.y : (int)blockIdx.y;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane >> 4, c16 = lane & 15;
+  const int lane = threadIdx.x & 63, g = lane >> 4, c16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int q0 = qb * AT;
   const int64_t hb = (int64_t)bh * a.S * AT, tb = (int64_t)bh * AT * a.Sp, rb = (int64_t)bh * a.S;
   const int q = q0 + 16 * w + c16;
@@ -529,30 +534,41 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
   const float ilq = qok ? 1.0f / a.l[rb + q] : 0.0f;
   const float dq_ref = qok ? a.D_ref[rb + q] : 0.0f;
 
-  TileRegs pf[3];
-  auto fetch = [&](int k0) {
-    tile_fetch(pf[0], a.K + hb, k0, a.S);
-    tile_fetch(pf[1], a.V + hb, k0, a.S);
-    tile_fetch_t(pf[2], a.Kt + tb, k0, a.Sp);
-  };
-  auto put = [&](int st) {
-    tile_put(sm[st][0], pf[0]);
-    tile_put(sm[st][1], pf[1]);
-    tile_put_t(sm[st][2], pf[2]);
+  // K and V end at row S (rows past it read as zero), K^T spans its Sp columns; lane l of load j
+  // (two per wave and tile) fills tile row 8 (2 w + j) + l / 8 at chunk position l % 8, which
+  // holds logical chunk (l % 8) ^ (l / 8) (the sw layout)
+  const __amdgpu_buffer_rsrc_t rK = attn_rsrc(a.K + hb, (int64_t)a.S * AT * 2);
+  const __amdgpu_buffer_rsrc_t rV = attn_rsrc(a.V + hb, (int64_t)a.S * AT * 2);
+  const __amdgpu_buffer_rsrc_t rKt = attn_rsrc(a.Kt + tb, (int64_t)AT * a.Sp * 2);
+  const int lr = lane >> 3, lch = (lane & 7) ^ lr;
+  const uint32_t vR = (uint32_t)(lr * AT * 2 + lch * 16), vT = (uint32_t)(lr * a.Sp * 2 + lch * 16);
+  auto issue = [&](u16 (*sm)[AT * AT], int k0) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t row = (uint32_t)(2 * w + j);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rK, (void __attribute__((address_space(3)))*)(sm[0] + row * 512), 16,
+                                               vR, (uint32_t)(k0 * AT * 2) + row * 1024, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rV, (void __attribute__((address_space(3)))*)(sm[1] + row * 512), 16,
+                                               vR, (uint32_t)(k0 * AT * 2) + row * 1024, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rKt, (void __attribute__((address_space(3)))*)(sm[2] + row * 512), 16,
+                                               vT, (uint32_t)(k0 * 2) + row * 16 * (uint32_t)a.Sp, 0, 0);
+    }
   };
   floatx4 aq[4], ag[4];
 #pragma unroll
   for (int n = 0; n < 4; ++n) aq[n] = ag[n] = floatx4{0.f, 0.f, 0.f, 0.f};
   const int nkb = a.causal ? qb + 1 : (a.S + AT - 1) / AT;
-  fetch(0);
-  put(0);
-  __syncthreads();
-  for (int kb = 0; kb < nkb; ++kb) {
-    const int st = kb & 1, k0 = kb * AT;
-    if (kb + 1 < nkb) fetch(k0 + AT);
-    const u16* tK = sm[st][0];
-    const u16* tV = sm[st][1];
-    const u16* tKt = sm[st][2];
+  issue(sm0, 0);
+  // key block kb from stage cur; the next block's tiles go into nxt, which every wave finished
+  // reading in the previous step (the barrier)
+  auto step = [&](int kb, u16 (*cur)[AT * AT], u16 (*nxt)[AT * AT]) {
+    const int k0 = kb * AT;
+    ATTN_WAIT_VM(0);  // this block's tiles (the only loads in flight)
+    ATTN_LDS_BARRIER();
+    if (kb + 1 < nkb) issue(nxt, k0 + AT);
+    const u16* tK = cur[0];
+    const u16* tV = cur[1];
+    const u16* tKt = cur[2];
     floatx4 sv[4], dp[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) sv[t] = dp[t] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -598,8 +614,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
         vd[v] = ds[2 * s + (v >> 2)][v & 3];
       }
       bf16x8 tp[3], td[3];
-      pack3(vp, tp);
-      pack3(vd, td);
+      pack3t(vp, tp);
+      pack3t(vd, td);
 #pragma unroll
       for (int n = 0; n < 4; ++n) {
         const bf16x8 fk = frag_t(tKt, 16 * n + c16, s, g);
@@ -610,8 +626,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
         }
       }
     }
-    if (kb + 1 < nkb) put(st ^ 1);
-    __syncthreads();
+  };
+  for (int kb = 0; kb < nkb; kb += 2) {
+    step(kb, sm0, sm1);
+    if (kb + 1 < nkb) step(kb + 1, sm1, sm0);
   }
   const float c = a.scale;
   const float rk = a.ntrial > 0 ? 1.0f / sqrtf((float)a.ntrial) : 0.0f;
