@@ -357,7 +357,7 @@ def c2_measurement(bsp, synth, torch, dev, steps, warmup):
     elapsed = time.perf_counter() - t0
     prof = {k: bsp.profile_read(k) for k in ("fresh_count", "fresh_count_se", "gemm", "gemm_split_sum", "quantize",
                                              "rmsnorm_fwd")}
-    gflop = bsp.profile_work("gemm")[0]
+    gflop, xflop = bsp.profile_work("gemm")
     bsp.profile_enable(False)
     et = cfg["T"] * cfg["d"] * cfg["K"]
     philox = {}
@@ -381,6 +381,9 @@ def c2_measurement(bsp, synth, torch, dev, steps, warmup):
            "quantize_hbm_frac": round(q_bytes / (q_ms / max(q_n, 1) / 1e3) / 1e9 / HBM_PEAK_GBPS, 4) if q_n else None,
            "gemm_TFLOPs": round(gflop / (g_ms / 1e3) / 1e12, 1) if g_ms else None,
            "gemm_mfma_frac": round(gflop / (g_ms / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4) if g_ms else None,
+           "gemm_executed_frac": round(xflop / (g_ms / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4) if g_ms else None,
+           "gemm_work": "algorithmic: 2 M N K per distinct product; executed: every bf16 term product of split "
+                        "operands",
            "kernel_ms_per_step": {k: round(v[0] / steps, 4) for k, v in prof.items()},
            "path": "collapsed (per-element up-counts; se at the gain use from per-trial sums)"}
     wall, t = _timed(bsp, torch, lambda: step(True), ("gemm", "gemm_split_sum", "trial_planes"), 2)
