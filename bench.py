@@ -111,7 +111,7 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
     probabilities at B4 H16 S1024 d64 (every policy of App. B's table, K = 32); the emulated FP8
     attention backward with delayed scaling at the same shape."""
     out = {}
-    cfg4 = synth.CONFIGS[4]
+    cfg4 = synth.WORKLOADS["linear_bwd_e5m2_16384x2048x8192"]
     X4, W4, dy4, _, _ = synth.linear_bwd_inputs(cfg4["M"], cfg4["k"], cfg4["n"], torch.bfloat16, 4)
     dy = dy4.to(dev)
     n = dy.numel()
@@ -142,7 +142,7 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
     del Xd, Wd, dy, lws
     torch.cuda.empty_cache()
 
-    cfg3 = synth.CONFIGS[3]
+    cfg3 = synth.WORKLOADS["attention_bwd_b4_h16_s1024_d64"]
     Q, K, V, dO = (t_.to(dev) for t_ in synth.attention_inputs(cfg3["B"], cfg3["H"], cfg3["S"], cfg3["dh"],
                                                                cfg3["dtype"], 3))
     ws = bsp.attn_workspace(cfg3["B"], cfg3["H"], cfg3["S"], cfg3["dh"], 3, cfg3["K"], dev)
@@ -187,7 +187,7 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
     # the FP8 store of attention probabilities and its two uses (every policy of App. B's table)
     cp = synth.PSTORE
     Q, K, V, dO = (t_.to(dev) for t_ in synth.attention_inputs(cp["B"], cp["H"], cp["S"], cp["dh"], cp["dtype"],
-                                                               cp["config"]))
+                                                               cp["stream"]))
     ws = bsp.attn_pstore_workspace(cp["B"], cp["H"], cp["S"], cp["dh"], cp["K"], True, dev)
     names = ("attn_prep", "attn_fwd", "pstore_fwd", "pstore_rows", "pstore_dq", "pstore_dkv")
     wall, t = _timed(bsp, torch, lambda: bsp.attn_pstore_policy(Q, K, V, dO, causal=True, fmt="e4m3",
@@ -212,7 +212,7 @@ def side_measurements(bsp, synth, torch, dev, reps=5):
     # the emulated FP8 attention backward with delayed scaling (E5M2 dO, dS and gradients, E4M3 P),
     # D from the saturated-row repair, at the same attention shape
     Q, K, V, dO = (t_.to(dev) for t_ in synth.attention_inputs(cp["B"], cp["H"], cp["S"], cp["dh"], cp["dtype"],
-                                                               cp["config"] + 1))
+                                                               cp["stream"] + 1))
     O = torch.randn(cp["B"], cp["H"], cp["S"], cp["dh"], device=dev) * 0.3      # a stand-in saved output
     Oc, Os, _ = bsp.qround(O, fmt="e4m3", mode="sr", seed=5)                    # the forward's store of O
     qkv = [bsp.qround(t_, fmt="e4m3", mode="rne")[:2] for t_ in (Q, K, V)]     # the forward's E4M3 Q, K, V
@@ -298,7 +298,7 @@ def cpu_baseline_decoder(cfg):
     from oracle import decoder
 
     def run(S):
-        (x, p, dOut), _ = synth_mod().decoder_inputs(1, S, cfg["d"], cfg["H"], cfg["F"], config=5)
+        (x, p, dOut), _ = synth_mod().decoder_inputs(1, S, cfg["d"], cfg["H"], cfg["F"], stream=5)
         pn = {k: v.float().numpy() for k, v in p.items()}
         t0 = time.perf_counter()
         f = decoder.forward(x.float().numpy(), pn, B=1, S=S, H=cfg["H"], seed=cfg["seed"])
@@ -337,7 +337,7 @@ def c2_measurement(bsp, synth, torch, dev, steps, warmup):
     """The RMSNorm -> FP8 store -> Linear check at the MLP up-projection shape (X [8192, 1024] bf16,
     W [1024, 4096], dY [8192, 4096], E4M3 RNE store, U/U R/R N/N, K = 256): collapsed step, its
     two Philox kernels against their ALU ceiling, and the per-trial-contraction path."""
-    cfg, (X, g, W, dY) = synth.config_inputs(2)
+    cfg, (X, g, W, dY) = synth.workload_inputs("rmsnorm_linear_390m_mlp_up")
     Xd, gd, Wd, dYd = (t.to(dev) for t in (X, g, W, dY))
     pols = cfg["policies"]
     ws = bsp.rmsnorm_linear_workspace(cfg["T"], cfg["d"], cfg["n"], len(pols), cfg["K"], dev)
@@ -404,10 +404,10 @@ def main():
     import torch
     from paper_2609_39813_amd import bsp, synth
 
-    cfg = synth.CONFIGS[5]
+    cfg = synth.WORKLOADS["decoder_layer_b8_s2048_d1024_h16_f4096"]
     dev = torch.device("cuda:0")
     log("inputs of the decoder layer (B8 S2048 d1024 H16 F4096)")
-    (x, p, dOut), (B, S, H) = synth.decoder_inputs(cfg["B"], cfg["S"], cfg["d"], cfg["H"], cfg["F"], config=5)
+    (x, p, dOut), (B, S, H) = synth.decoder_inputs(cfg["B"], cfg["S"], cfg["d"], cfg["H"], cfg["F"], stream=5)
     xd, pd, dOd = x.to(dev), {k: v.to(dev) for k, v in p.items()}, dOut.to(dev)
     ws = bsp.decoder_layer_workspace(B, S, cfg["d"], H, cfg["F"], cfg["K"], dev, all_uses=True)
     n_pol = 6   # U, R, N at each use alone, and at every use together

@@ -53,7 +53,7 @@ typedef enum {
   BS_EINVAL = 1,        /* a NULL required pointer, negative size, bad enum or option */
   BS_ESHAPE = 2,        /* sizes the kernels do not support (stated per call) */
   BS_EDTYPE = 3,        /* dtype not supported by this call */
-  BS_EUNSUPPORTED = 4,  /* a valid request this build does not implement */
+  BS_EUNSUPPORTED = 4,  /* a valid request the library does not implement */
   BS_EWORKSPACE = 5,    /* ws is NULL, misaligned or smaller than *_workspace_size() */
   BS_EHIP = 6           /* a HIP runtime error while enqueueing */
 } bs_status;
@@ -491,7 +491,7 @@ bs_status bs_gemm_bf16_nt(const void* A, int64_t lda, const void* B, int64_t ldb
  *   Rows: 0 u1 gain, 1 u1 weight (dWqkv), 2 u1 norm-input (dX), 3 O D (dQ), 4 O D (dK),
  *   5 O weight (dWo), 6 u2 gain, 7 u2 weight ([dWg | dWu]), 8 u2 norm-input, 9 a weight (dWd).
  *   all (nullable): each letter read at every use of every store together, in one backward whose
- *   moved incoming gradients reach the earlier uses (config 5's policy applied to every stored
+ *   moved incoming gradients reach the earlier uses (the policy applied to every stored
  *   tensor): U reads every original, R every forward rounding, N per use a new rounding (trials
  *   1..K; use +1 at a gain use and at the D use, +2 at a weight use, +3 at a normalization-input
  *   use). Per letter l (U, R, N): bias[l] (mean over trials minus the reference) and se[l] of each

@@ -181,7 +181,7 @@ def all_uses_reads(f, p, letter, *, seed, trial, fmt=fp8.E4M3):
 
 
 def all_uses(f, p, dOut, r, *, K, seed, fmt=fp8.E4M3, letters=("U", "R", "N")):
-    """The letter applied at every use of every store in one backward (config 5's policy applied to
+    """The letter applied at every use of every store in one backward (the policy applied to
     every stored rounded tensor), K trials with the forward held fixed (one pass for U and R, which
     draw nothing): {letter: {gradient: (mean, bias, se)}} against the reference gradients r."""
     out = {}

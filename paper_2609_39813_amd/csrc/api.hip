@@ -20,7 +20,7 @@ const char* bs_status_string(bs_status s) {
     case BS_EINVAL: return "invalid argument";
     case BS_ESHAPE: return "unsupported shape";
     case BS_EDTYPE: return "unsupported dtype";
-    case BS_EUNSUPPORTED: return "not implemented in this build";
+    case BS_EUNSUPPORTED: return "not implemented by the library";
     case BS_EWORKSPACE: return "workspace missing, misaligned or too small";
     case BS_EHIP: return "HIP runtime error";
   }

@@ -19,7 +19,7 @@ TOL = 1e-5
 
 
 def inputs(B, H, S, seed):
-    return [t.to(torch.bfloat16) for t in synth.attention_inputs(B, H, S, 64, torch.float32, config=100 + seed)]
+    return [t.to(torch.bfloat16) for t in synth.attention_inputs(B, H, S, 64, torch.float32, stream=100 + seed)]
 
 
 def run(lib, Q, K, V, dO, O=None, causal=True, pols=("U", "R", "N"), Kt=8, seed=3, fwd_mode="sr", dk_se=True):
@@ -126,7 +126,7 @@ def test_fp8_attention_example_cells_exact(lib):
 
 @pytest.mark.slow
 def test_config3_full_size_sampled_heads(lib):
-    cfg = synth.CONFIGS[3]
+    cfg = synth.WORKLOADS["attention_bwd_b4_h16_s1024_d64"]
     Q, K, V, dO = synth.attention_inputs(cfg["B"], cfg["H"], cfg["S"], cfg["dh"], cfg["dtype"], 3)
     heads = [(0, 0), (3, 15)]
     ref = attention.check(Q.float().numpy(), K.float().numpy(), V.float().numpy(), dO.float().numpy(), causal=True,

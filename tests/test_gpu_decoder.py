@@ -23,8 +23,8 @@ FMTS = {"e4m3": fp8.E4M3, "e5m2": fp8.E5M2}
 MODES = {"rne": oq.RNE, "sr": oq.SR}
 
 
-def oracle_case(B, S, d, H, F, K, seed, fmt, mode, config):
-    (x, p, dOut), _ = synth.decoder_inputs(B, S, d, H, F, config=config)
+def oracle_case(B, S, d, H, F, K, seed, fmt, mode, stream):
+    (x, p, dOut), _ = synth.decoder_inputs(B, S, d, H, F, stream=stream)
     pn = {k: v.float().numpy() for k, v in p.items()}
     f = decoder.forward(x.float().numpy(), pn, B=B, S=S, H=H, fmt=FMTS[fmt], fwd_mode=MODES[mode], seed=seed)
     r = decoder.reference_backward(f, pn, dOut.float().numpy())
@@ -62,7 +62,7 @@ def check_sumsq(got, want, what):
     (1, 72, 64, 1, 136, 1, 14, "e5m2", "sr", True),      # K = 1: se 0
 ])
 def test_layer_matches_oracle_with_fixed_forward(lib, B, S, d, H, F, K, seed, fmt, mode, per_use_se):
-    inputs, f, r, table = oracle_case(B, S, d, H, F, K, seed, fmt, mode, config=600 + seed)
+    inputs, f, r, table = oracle_case(B, S, d, H, F, K, seed, fmt, mode, stream=600 + seed)
     out = run(lib, inputs, B, S, H, K, seed, fmt, mode, fixed_of(f), per_use_se)
     # the four stores, bit for bit
     for name, q in (("u1", f["q1"]), ("O", f["qO"]), ("u2", f["q2"]), ("a", f["qa"])):
@@ -99,7 +99,7 @@ def test_layer_matches_oracle_with_fixed_forward(lib, B, S, d, H, F, K, seed, fm
 
 def test_layer_own_forward_is_a_valid_realization(lib):
     B, S, d, H, F, K, seed = 2, 40, 128, 2, 256, 4, 21
-    inputs, f, r, _ = oracle_case(B, S, d, H, F, K, seed, "e4m3", "rne", config=621)
+    inputs, f, r, _ = oracle_case(B, S, d, H, F, K, seed, "e4m3", "rne", stream=621)
     out = run(lib, inputs, B, S, H, K, seed, "e4m3", "rne", None)
     assert np.array_equal(to_np(out["codes_u1"]), f["q1"].codes)
     scales = to_np(out["scales"])

@@ -15,7 +15,7 @@ pytestmark = pytest.mark.gpu
 
 
 def run_all(lib, B, S, d, H, F, K, seed, fmt, mode):
-    inputs, f, r, _ = oracle_case(B, S, d, H, F, K, seed, fmt, mode, config=640 + seed)
+    inputs, f, r, _ = oracle_case(B, S, d, H, F, K, seed, fmt, mode, stream=640 + seed)
     x, p, dOut = inputs
     pn = {k: v.float().numpy() for k, v in p.items()}
     print(f"[layer all uses] B={B} S={S} d={d} H={H} F={F} K={K} fmt={fmt} mode={mode}", flush=True)
@@ -57,7 +57,7 @@ def test_every_use_at_once_matches_oracle(lib, B, S, d, H, F, K, seed, fmt, mode
 def test_every_use_at_once_leaves_the_per_use_outputs_unchanged(lib):
     """Asking for the every-use check does not change the reference gradients, stores or table."""
     B, S, d, H, F, K, seed = 1, 40, 64, 1, 96, 3, 33
-    inputs, f, r, _ = oracle_case(B, S, d, H, F, K, seed, "e4m3", "rne", config=640 + seed)
+    inputs, f, r, _ = oracle_case(B, S, d, H, F, K, seed, "e4m3", "rne", stream=640 + seed)
     x, p, dOut = inputs
     args = (x.cuda(), {k: v.cuda() for k, v in p.items()}, dOut.cuda())
     kw = dict(B=B, S=S, H=H, fmt="e4m3", fwd_mode="rne", K=K, seed=seed, fixed=fixed_of(f))

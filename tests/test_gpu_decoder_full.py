@@ -29,9 +29,9 @@ def say(msg):
 
 @pytest.fixture(scope="module")
 def full(lib):
-    cfg = synth.CONFIGS[5]
+    cfg = synth.WORKLOADS["decoder_layer_b8_s2048_d1024_h16_f4096"]
     B, S, d, H, F, K, seed = cfg["B"], cfg["S"], cfg["d"], cfg["H"], cfg["F"], cfg["K"], cfg["seed"]
-    (x, p, dOut), _ = synth.decoder_inputs(B, S, d, H, F, config=5)
+    (x, p, dOut), _ = synth.decoder_inputs(B, S, d, H, F, stream=5)
     pn = {k: v.float().numpy() for k, v in p.items()}
     say("oracle forward")
     f = decoder.forward(x.float().numpy(), pn, B=B, S=S, H=H, seed=seed)

@@ -38,13 +38,13 @@ def twice(fn, what):
 
 
 def test_rmsnorm_linear_and_grid_store(lib):
-    X, g, W, dY = (t.cuda() for t in synth.rmsnorm_linear_inputs(200, 96, 40, torch.bfloat16, config=51))
+    X, g, W, dY = (t.cuda() for t in synth.rmsnorm_linear_inputs(200, 96, 40, torch.bfloat16, stream=51))
     twice(lambda: lib.rmsnorm_linear(X, g, W, dY, K=24, seed=5, want_dw_se=True), "rmsnorm_linear")
     twice(lambda: lib.rmsnorm_linear_grid(X, g, W, dY, bits=6, K=24, seed=5), "rmsnorm_linear_grid")
 
 
 def test_attention_paths(lib):
-    Q, K, V, dO = (t.cuda() for t in synth.attention_inputs(1, 2, 136, 64, torch.bfloat16, config=52))
+    Q, K, V, dO = (t.cuda() for t in synth.attention_inputs(1, 2, 136, 64, torch.bfloat16, stream=52))
     twice(lambda: lib.attn_bwd_policy(Q, K, V, dO, policies=("U", "R", "N"), K=8, seed=3), "attn_bwd_policy")
     twice(lambda: lib.attn_level2_policy(Q, K, V, dO, K=8, seed=3), "attn_level2_policy")
     twice(lambda: lib.attn_pstore_policy(Q, K, V, dO, K=8, seed=3, want_p=True), "attn_pstore_policy")

@@ -16,8 +16,8 @@ pytestmark = pytest.mark.gpu
 TOL = 1e-5
 
 
-def run_both(lib, T, d, n, dtype, K, bits, policies=gs.POLICIES, seed=11, config=7, zero_row=None):
-    X, g, W, dY = synth.rmsnorm_linear_inputs(T, d, n, dtype, config)
+def run_both(lib, T, d, n, dtype, K, bits, policies=gs.POLICIES, seed=11, stream=7, zero_row=None):
+    X, g, W, dY = synth.rmsnorm_linear_inputs(T, d, n, dtype, stream)
     if zero_row is not None:
         X[zero_row] = 0
     print(f"[grid_store] T={T} d={d} n={n} {dtype} bits={bits} K={K} {policies}", flush=True)

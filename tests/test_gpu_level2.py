@@ -21,7 +21,7 @@ MODES = {"rne": oq.RNE, "sr": oq.SR}
 
 
 def inputs(B, H, S, seed):
-    return [t.to(torch.bfloat16) for t in synth.attention_inputs(B, H, S, 64, torch.float32, config=400 + seed)]
+    return [t.to(torch.bfloat16) for t in synth.attention_inputs(B, H, S, 64, torch.float32, stream=400 + seed)]
 
 
 def case(lib, B, H, S, *, seed, causal=True, fmt="e4m3", fwd_mode="sr", beta=1.0, pols=("U", "R", "N"), K=8,

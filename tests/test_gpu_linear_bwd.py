@@ -11,9 +11,9 @@ pytestmark = pytest.mark.gpu
 TOL = 1e-5
 
 
-def run_both(lib, M, k, n, K, sharings=("shared", "per_use"), seed=5, coupling=True, oracle_kw=None, config=40,
+def run_both(lib, M, k, n, K, sharings=("shared", "per_use"), seed=5, coupling=True, oracle_kw=None, stream=40,
              fmt="e5m2", probes=None, want_se=False):
-    X, W, dY, A, B = synth.linear_bwd_inputs(M, k, n, torch.bfloat16, config)
+    X, W, dY, A, B = synth.linear_bwd_inputs(M, k, n, torch.bfloat16, stream)
     if probes is not None:
         A, B = probes
     print(f"[linear_bwd] M={M} k={k} n={n} K={K} {sharings} coupling={coupling} fmt={fmt}", flush=True)
@@ -75,7 +75,7 @@ def test_config4_full_size_sampled(lib):
     """The 16384 x 2048 x 8192 launch: sampled rows of dX and entries of dW, and the coupling
     statistic kappa with probes supported on exactly those outputs (A on the sampled rows, B on the
     sampled entries), so the oracle's plain K trials over the samples give kappa exactly."""
-    cfg = synth.CONFIGS[4]
+    cfg = synth.WORKLOADS["linear_bwd_e5m2_16384x2048x8192"]
     M, k, n = cfg["M"], cfg["k"], cfg["n"]
     rng = np.random.default_rng(4)
     xr = np.sort(rng.choice(M, 6, replace=False))
@@ -87,5 +87,5 @@ def test_config4_full_size_sampled(lib):
     B = torch.zeros(k, n)
     B[np.ix_(wr, wc)] = torch.randn(len(wr), len(wc), generator=g)
     out, ref = run_both(lib, M, k, n, cfg["K"], sharings=cfg["sharings"], seed=cfg["seed"], coupling=True,
-                        oracle_kw=dict(dx_rows=xr, dw_rows=wr, dw_cols=wc), config=4, probes=(A, B), want_se=True)
+                        oracle_kw=dict(dx_rows=xr, dw_rows=wr, dw_cols=wc), stream=4, probes=(A, B), want_se=True)
     compare(out, ref, cfg["sharings"], M, k, n, xr=xr, wr=wr, wc=wc, coupling=True)

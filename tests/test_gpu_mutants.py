@@ -54,7 +54,7 @@ def test_new_roundings_under_the_wrong_use_id_fail(lib):
 
 
 def test_d_from_the_wrong_copy_fails(lib):
-    Q, K, V, dO = (t.to(torch.bfloat16) for t in synth.attention_inputs(1, 2, 96, 64, torch.float32, config=140))
+    Q, K, V, dO = (t.to(torch.bfloat16) for t in synth.attention_inputs(1, 2, 96, 64, torch.float32, stream=140))
     ref = attention.check(*(t.float().numpy() for t in (Q, K, V, dO)), policies=("U", "R"), K=2, seed=9, store_id=1)
     O = torch.from_numpy(np.ascontiguousarray(ref["O32"])).cuda()
     print("[mutant] attention D copy", flush=True)

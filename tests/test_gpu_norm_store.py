@@ -17,8 +17,8 @@ MODES = {"rne": oq.RNE, "sr": oq.SR}
 
 
 def run_both(lib, T, d, n, dtype, K, policies, fwd_mode="rne", seed=123, store_id=0, norm_input="U",
-             shared=False, oracle_kw=None, config=2):
-    X, g, W, dY = synth.rmsnorm_linear_inputs(T, d, n, dtype, config)
+             shared=False, oracle_kw=None, stream=2):
+    X, g, W, dY = synth.rmsnorm_linear_inputs(T, d, n, dtype, stream)
     codes = [p + (":R" if norm_input == "R" else "") + (":shared" if shared else "") for p in policies]
     print(f"[norm_store] T={T} d={d} n={n} {dtype} K={K} {codes} fwd={fwd_mode}", flush=True)
     out = lib.rmsnorm_linear(X.cuda(), g.cuda(), W.cuda(), dY.cuda(), fmt="e4m3", fwd_mode=fwd_mode,
@@ -93,22 +93,22 @@ def test_single_row_and_single_trial(lib):
 
 
 def test_config1_exact(lib):
-    cfg = synth.CONFIGS[1]
+    cfg = synth.WORKLOADS["rmsnorm_linear_256x64x64"]
     out, ref = run_both(lib, cfg["T"], cfg["d"], cfg["n"], cfg["dtype"], cfg["K"], cfg["policies"],
-                        seed=cfg["seed"], config=1)
+                        seed=cfg["seed"], stream=1)
     compare(out, ref, cfg["policies"], d=cfg["d"], n=cfg["n"])
 
 
 @pytest.mark.slow
 def test_config2_full_size_sampled(lib):
-    cfg = synth.CONFIGS[2]
+    cfg = synth.WORKLOADS["rmsnorm_linear_390m_mlp_up"]
     T, d, n = cfg["T"], cfg["d"], cfg["n"]
     rng = np.random.default_rng(2)
     rows = np.sort(rng.choice(d, 4, replace=False))
     cols = np.sort(rng.choice(d, 6, replace=False))
     xrows = np.sort(rng.choice(T, 16, replace=False))
     out, ref = run_both(lib, T, d, n, cfg["dtype"], cfg["K"], cfg["policies"], seed=cfg["seed"],
-                        oracle_kw=dict(dw_rows=rows, gain_cols=cols, dx_rows=xrows), config=2)
+                        oracle_kw=dict(dw_rows=rows, gain_cols=cols, dx_rows=xrows), stream=2)
     compare(out, ref, cfg["policies"], rows=rows, cols=cols, xrows=xrows, d=d, n=n)
 
 
@@ -132,7 +132,7 @@ def test_weight_use_se_per_trial(lib):
 def test_forward_only_and_no_tokens(lib):
     """dY NULL: the store and Y only (against the oracle); T = 0 with a non-NULL dY: references
     and estimates are zero, the store reports amax 0 and scale 1."""
-    X, g, W, dY = synth.rmsnorm_linear_inputs(40, 32, 16, torch.bfloat16, config=41)
+    X, g, W, dY = synth.rmsnorm_linear_inputs(40, 32, 16, torch.bfloat16, stream=41)
     print("[norm_store] forward only T=40 d=32 n=16", flush=True)
     out = lib.rmsnorm_linear(X.cuda(), g.cuda(), W.cuda(), None, K=4, seed=2)
     torch.cuda.synchronize()

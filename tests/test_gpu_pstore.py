@@ -21,7 +21,7 @@ MODES = {"rne": oq.RNE, "sr": oq.SR}
 
 
 def inputs(B, H, S, seed):
-    return [t.to(torch.bfloat16) for t in synth.attention_inputs(B, H, S, 64, torch.float32, config=300 + seed)]
+    return [t.to(torch.bfloat16) for t in synth.attention_inputs(B, H, S, 64, torch.float32, stream=300 + seed)]
 
 
 def run(lib, Q, K, V, dO, *, causal=True, fmt="e4m3", fwd_mode="rne", pols=ALL, Kt=8, seed=3, store_id=2, scale=None):
@@ -130,7 +130,7 @@ def test_full_size_sampled_rows(lib):
     causal mask, are the last 16 rows), for two heads."""
     cp = synth.PSTORE
     B, H, S = cp["B"], cp["H"], cp["S"]
-    Q, K, V, dO = synth.attention_inputs(B, H, S, cp["dh"], cp["dtype"], cp["config"])
+    Q, K, V, dO = synth.attention_inputs(B, H, S, cp["dh"], cp["dtype"], cp["stream"])
     out = run(lib, Q, K, V, dO, pols=cp["policies"], Kt=cp["K"], seed=cp["seed"], fwd_mode=cp["fwd_mode"])
     heads = [(0, 0), (3, 15)]
     g = np.random.default_rng(5)

@@ -24,7 +24,7 @@ F32 = np.float32
 
 
 def inputs(B, H, S, seed, sharp=1):
-    Q, K, V, dO = synth.attention_inputs(B, H, S, 64, torch.float32, config=500 + seed)
+    Q, K, V, dO = synth.attention_inputs(B, H, S, 64, torch.float32, stream=500 + seed)
     return [t.to(torch.bfloat16) for t in (Q * sharp, K, V, dO)]
 
 

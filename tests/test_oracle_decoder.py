@@ -8,7 +8,7 @@ from paper_2609_39813_amd import synth
 
 
 def small(seed=0, B=2, S=24, d=128, H=2, F=256):
-    return synth.decoder_inputs(B, S, d, H, F, config=500 + seed)
+    return synth.decoder_inputs(B, S, d, H, F, stream=500 + seed)
 
 
 def test_reference_backward_matches_autograd():
@@ -171,7 +171,7 @@ def test_forward_pin_rejects_planted_formula_errors(plant):
 # The letter applied at every use of every store together (decoder.all_uses)
 # ---------------------------------------------------------------------------------------------
 def _all_case(seed=2, B=1, S=12, d=64, H=1, F=96, fmt=fp8.E4M3):
-    (x, p, dOut), _ = synth.decoder_inputs(B, S, d, H, F, config=520 + seed)
+    (x, p, dOut), _ = synth.decoder_inputs(B, S, d, H, F, stream=520 + seed)
     pn = {k: v.float().numpy() for k, v in p.items()}
     g = torch.Generator().manual_seed(90 + seed)
     pn["gain1"] = (1 + 0.1 * torch.randn(d, generator=g)).numpy()
