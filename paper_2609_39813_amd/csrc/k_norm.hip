@@ -264,9 +264,10 @@ __global__ __launch_bounds__(256) void norm_planes_t4_kernel(NormPlaneArgs a) {
 
 // Per-trial residual planes of the weight use (the per-trial contraction path): a block covers
 // 64 rows t x 64 columns j; a thread holds 4 rows x 4 consecutive columns (one Philox call per
-// row and trial), the trial's values go through an LDS tile to rows of the plane [j][t].
+// row and trial), the trial's values go through an LDS tile (rows of 144 bytes) to rows of the
+// plane [j][t], leaving it as 16-byte pieces (eight consecutive t per thread and piece).
 __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
-  __shared__ u16 tile[64][66];
+  __shared__ __attribute__((aligned(16))) u16 tile[64][72];
   const int64_t t0 = (int64_t)blockIdx.y * 64, j0 = (int64_t)blockIdx.x * 64;
   const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;  // column group, row group
   const double rs = 1.0 / (double)*a.scale;
@@ -309,11 +310,10 @@ __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
     __syncthreads();
     u16* out = a.out + (int64_t)b * a.d * a.ldo;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int cc = (threadIdx.x >> 6) + 4 * i;
-      const int tx = threadIdx.x & 63;
-      const int64_t j = j0 + cc, t = t0 + tx;
-      if (j < a.d && t < a.ldo) out[j * a.ldo + t] = tile[cc][tx];
+    for (int i = 0; i < 2; ++i) {
+      const int ch = threadIdx.x + 256 * i, cc = ch >> 3, k8 = ch & 7;
+      const int64_t j = j0 + cc;
+      if (j < a.d) *(uint4*)(out + j * a.ldo + t0 + 8 * k8) = *(const uint4*)&tile[cc][8 * k8];
     }
     __syncthreads();
   }
@@ -605,6 +605,7 @@ bs_status launch_norm_planes(int mode, const NormPlaneArgs& a, hipStream_t st) {
 
 bs_status launch_trial_planes(const TrialPlaneArgs& a, hipStream_t st) {
   if (a.nb <= 0 || a.d <= 0) return BS_OK;
+  if (a.ldo % 64 || ((uintptr_t)a.out & 15)) return BS_EINVAL;  // whole 16-byte pieces of padded rows
   dim3 grid((unsigned)((a.d + 63) / 64), (unsigned)((a.ldo + 63) / 64));
   ProfScope prof("trial_planes", st);
   trial_planes_kernel<<<grid, 256, 0, st>>>(a);
