@@ -68,8 +68,8 @@ bs_status launch_dx_t(const DxArgs<T>& a, hipStream_t st);
 
 // Per-trial weight-use residual planes: for trials k0 .. k0 + nb - 1 (new roundings of u at
 // the store's scale, use id `use`), plane b [d][ldo] holds sign * (up_k - [C_u rounded up]) * step
-// (one exact bf16 term; zero for t >= T). ldo a multiple of 64 and out 16-byte aligned
-// (BS_EINVAL otherwise).
+// (one exact bf16 term; zero for t >= T). ldo a multiple of 64, d of 4, out and u 16-byte and
+// codes 4-byte aligned (BS_EINVAL otherwise).
 struct TrialPlaneArgs {
   const float* u;
   const uint8_t* codes;

@@ -276,20 +276,23 @@ __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
   uint32_t h[4];   // bit q: the forward's code was rounded up
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int64_t t = t0 + rg + 16 * q;
+    const int64_t t = t0 + rg + 16 * q, jg = j0 + 4 * cg;
     h[q] = 0;
+    // the row's four columns in one 16-byte and one 4-byte load (d % 4 == 0)
+    const bool ok = t < a.T && jg < a.d;
+    const float4 uv = ok ? *(const float4*)(a.u + t * a.d + jg) : make_float4(0.f, 0.f, 0.f, 0.f);
+    const uint32_t cw = ok ? *(const uint32_t*)(a.codes + t * a.d + jg) : 0u;
+    const float u4[4] = {uv.x, uv.y, uv.z, uv.w};
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const int64_t j = j0 + 4 * cg + c;
       F[q][c] = 0;
       sv[q][c] = 0;
-      if (t < a.T && j < a.d) {
-        const int64_t e = t * a.d + j;
-        const float y = div_scale(a.u[e], rs);
+      if (ok) {
+        const float y = div_scale(u4[c], rs);
         const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
         F[q][c] = b.F;
         sv[q][c] = bf16_bits(signbit(y) ? -f8_step(b) : f8_step(b));
-        h[q] |= (uint32_t)((a.codes[e] & 0x7Fu) != b.base + b.mi) << c;
+        h[q] |= (uint32_t)(((cw >> (8 * c)) & 0x7Fu) != b.base + b.mi) << c;
       }
     }
   }
@@ -605,7 +608,9 @@ bs_status launch_norm_planes(int mode, const NormPlaneArgs& a, hipStream_t st) {
 
 bs_status launch_trial_planes(const TrialPlaneArgs& a, hipStream_t st) {
   if (a.nb <= 0 || a.d <= 0) return BS_OK;
-  if (a.ldo % 64 || ((uintptr_t)a.out & 15)) return BS_EINVAL;  // whole 16-byte pieces of padded rows
+  // whole 16-byte pieces of padded rows out, four columns per load in
+  if (a.ldo % 64 || ((uintptr_t)a.out & 15) || (a.d & 3) || ((uintptr_t)a.u & 15) || ((uintptr_t)a.codes & 3))
+    return BS_EINVAL;
   dim3 grid((unsigned)((a.d + 63) / 64), (unsigned)((a.ldo + 63) / 64));
   ProfScope prof("trial_planes", st);
   trial_planes_kernel<<<grid, 256, 0, st>>>(a);
