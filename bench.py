@@ -7,7 +7,8 @@ reference backward, every use of every store under U, R and N with K = 16 new ro
 passes for N). Inputs are resident in HBM before the timed region. The metric is policy-trials
 per second: (#policies x K) / step time, with 6 policies (U, R, N per use and at every use).
 
-Prints one JSON line. `roofline` is the step's dominant kernel, the bf16 MFMA contraction, timed
+Prints one JSON line. `roofline` is the step's dominant kernel, the MFMA contraction (bf16, and
+fp16 for the scaled two-term splits of the every-use weight contractions; one peak for both), timed
 live with HIP events on its launch stream (algorithmic flop per launch over the average launch
 time); `cpu_baseline` times the plain CPU oracle on a bounded sample of the same workload (rank
 0, N = 1 only). `extra` holds the metric's other figures: the RMSNorm -> Linear check at the MLP
@@ -434,24 +435,27 @@ def main():
     ms_per_step = elapsed / args.steps * 1e3
     value = n_pol * cfg["K"] * args.steps / elapsed
 
-    # dominant kernel: the bf16 MFMA contraction (every contraction launch of the step)
+    # dominant kernel: the MFMA contraction (every contraction launch of the step; bf16 and fp16
+    # operands share one dense peak)
     g_ms, g_n = prof["gemm"]
     avg_s = g_ms / max(g_n, 1) / 1e3
     flop_per_launch = flop / max(g_n, 1)
     achieved = flop_per_launch / avg_s / 1e12 if g_n else 0.0
-    roofline = {"bound": "mfma", "kernel": "gemm_lds_kernel (bf16 MFMA 16x16x32, every contraction of the step)",
+    roofline = {"bound": "mfma", "kernel": "gemm_lds_kernel (bf16 and fp16 MFMA 16x16x32, every contraction of the "
+                                                     "step)",
                 "achieved": round(achieved, 1), "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / BF16_MFMA_PEAK_TFLOPS, 4),
                 "traffic": traffic_if_current(GEMM_TRAFFIC_BYTES, GEMM_TRAFFIC_SOURCES, GEMM_TRAFFIC_SHA256),
                 "avg_launch_ms": round(avg_s * 1e3, 4), "launches": g_n,
                 "algorithmic_flop_per_launch": round(flop_per_launch),
-                "work_per_launch": "2 M N K flop per distinct product (extra terms of split bf16 operands and "
+                "work_per_launch": "2 M N K flop per distinct product (extra terms of split operands and "
                                    "split-K sums not counted)",
                 "split_sum_ms_per_step": round(prof["gemm_split_sum"][0] / args.steps, 4),
                 "executed_TFLOPs": round(xflop / max(g_n, 1) / avg_s / 1e12, 1) if g_n else 0.0,
                 "executed_frac": round(xflop / max(g_n, 1) / avg_s / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4) if g_n else 0.0,
-                "executed_note": "fp32 operands (incoming gradients, residuals) enter as exact sums of 3 bf16 terms "
-                                 "for 1e-5 parity; executed flop counts every term product"}
+                "executed_note": "fp32 operands (incoming gradients, residuals) enter as exact sums of 3 bf16 terms, "
+                                 "or against FP8 values as 2 scaled fp16 terms (error <= 2^-22 relative), for "
+                                 "1e-5 parity; executed flop counts every term product"}
     extra = {"kernel_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in prof.items()},
              "gemm_TFLOP_per_step": round(flop / args.steps / 1e12, 4),
              "work": "forward, reference backward, U/R/N at the 10 uses of the 4 stores (K = 16 new roundings per "

@@ -12,6 +12,7 @@
 #define BS_WAVE 64
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef unsigned short u16;
@@ -136,6 +137,28 @@ __device__ __forceinline__ float f8_value(uint32_t code, F8 f) {
 // an fp32 value into up to three bf16 terms whose sum is the value (each term rounds the
 // remainder to nearest; three terms carry all 24 bits).
 // ---------------------------------------------------------------------------------
+// fp16 bits of x, round to nearest even
+__device__ __forceinline__ u16 f16_bits(float x) { return __builtin_bit_cast(u16, (_Float16)x); }
+
+// The two-term fp16 split of fp32 operands: a tensor bounded by `bound` in magnitude is scaled by
+// 2^e with bound 2^e in [2^14, 2^15) (no fp16 overflow), then x 2^e = hi + lo + err with hi =
+// fp16(x 2^e), lo = fp16(x 2^e - hi), |err| <= 2^-22 |x 2^e| where lo is a normal fp16 number
+// and <= 2^-25 (2^-40 of the bound) below; a contraction undoes the scale with 2^-e. e = 0 for
+// a bound of zero or not finite (finite values beyond the fp16 range then become infinite);
+// -113 <= e <= 100, so 2^e and 2^-e are normal fp32 numbers.
+__device__ __forceinline__ int f16_scale_exp(float bound) {
+  if (!(bound > 0.0f) || !__builtin_isfinite(bound)) return 0;
+  int k;
+  (void)frexpf(bound, &k);  // bound in [2^(k-1), 2^k), k <= 128
+  const int e = 15 - k;
+  return e > 100 ? 100 : e;
+}
+__device__ __forceinline__ void split2_f16(float xs, u16& hi, u16& lo) {
+  const _Float16 h = (_Float16)xs;
+  hi = __builtin_bit_cast(u16, h);
+  lo = f16_bits(xs - (float)h);
+}
+
 __device__ __forceinline__ u16 bf16_bits(float x) {
   __bf16 h = (__bf16)x;
   return __builtin_bit_cast(u16, h);
@@ -176,6 +199,29 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     v = v > o ? v : o;
   }
   return v;
+}
+// A maximum raised by many blocks lives in AMAX_SLOTS words AMAX_STRIDE words apart (block b
+// raises slot b % AMAX_SLOTS): device-scope atomics on one word serialize, on words in different
+// memory channels they do not. Its value is the max over the slots.
+constexpr int AMAX_SLOTS = 32, AMAX_STRIDE = 64;
+// The block's max of v (float bits of non-negative values; all threads of the block call it)
+// raised into its slot of `slots` by one atomic.
+__device__ __forceinline__ void block_amax_to_slot(float v, uint32_t* slots) {
+  __shared__ uint32_t red[16];
+  const uint32_t m = wave_max_u32(__float_as_uint(v));
+  if ((threadIdx.x & (BS_WAVE - 1)) == 0) red[threadIdx.x / BS_WAVE] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t b = 0;
+    for (int w = 0; w < (int)((blockDim.x + BS_WAVE - 1) / BS_WAVE); ++w) b = b > red[w] ? b : red[w];
+    if (b) atomicMax(slots + (blockIdx.x % AMAX_SLOTS) * AMAX_STRIDE, b);
+  }
+}
+__device__ __forceinline__ float amax_of_slots(const uint32_t* slots) {
+  uint32_t m = 0;
+#pragma unroll 8
+  for (int i = 0; i < AMAX_SLOTS; ++i) m = max(m, slots[i * AMAX_STRIDE]);
+  return __uint_as_float(m);
 }
 __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
 #pragma unroll

@@ -19,7 +19,17 @@ struct GemmArgs {
   int64_t part_cap = 0;
   int nprod = 0;            // distinct products among the segments (split terms of one product
                             // count once); 0: every segment is a product of its own
+  int f16 = 0;              // 1: every operand holds fp16 values (the 2-term fp16 split), else bf16
+  const float* alpha_dev2 = nullptr;  // nullable: a second device multiplier of alpha
 };
+
+// alpha of a launch with its device multipliers
+__device__ __forceinline__ float gemm_alpha(const GemmArgs& g) {
+  float a = g.alpha;
+  if (g.alpha_dev) a *= *g.alpha_dev;
+  if (g.alpha_dev2) a *= *g.alpha_dev2;
+  return a;
+}
 
 // algorithmic flop of a contraction launch: 2 M N K per distinct product
 inline double gemm_flops(const GemmArgs& g) {
@@ -28,7 +38,8 @@ inline double gemm_flops(const GemmArgs& g) {
 // flop the matrix cores execute: 2 M N K per segment (every bf16 term of a split operand)
 inline double gemm_exec_flops(const GemmArgs& g) { return 2.0 * g.M * g.N * (double)g.K * g.nseg; }
 
-// Append the products A_i B_j (i + j <= 2) of nA and nB bf16 terms to g's segments.
+// Append the products A_i B_j (i + j <= 2) of nA and nB bf16 terms to g's segments (with fp16
+// operands: A of one exact term, B of the two terms of a scaled fp16 split: both products).
 inline bool gemm_add_products(GemmArgs& g, const u16* const* A, int nA, const u16* const* B, int nB) {
   if (g.nprod == 0 && g.nseg > 0) g.nprod = g.nseg;  // segments set before: one product each
   ++g.nprod;
@@ -93,6 +104,9 @@ bs_status launch_combine(const float* ref, const float* bias, const float* se, i
 
 bs_status launch_fill2d(float* p, int64_t rows, int64_t cols, int64_t ld, float v, hipStream_t st);
 bs_status launch_fill_f64(double* p, int64_t n, double v, hipStream_t st);
+// *out (the float bits of a maximum, zeroed by the caller) raised to max |x[i]| over n floats;
+// with the other AMAX_SLOTS - 1 slots zeroed, out is a slot array
+bs_status launch_amax_f32(const float* x, int64_t n, uint32_t* out, hipStream_t st);
 bs_status launch_init_diag(bs_diag* diag, hipStream_t st);
 
 // bf16 operand planes. Row-major: out_p[r*ldo + c], c < C (ldo >= C). Transposed:
@@ -100,12 +114,23 @@ bs_status launch_init_diag(bs_diag* diag, hipStream_t st);
 // split of each fp32 value; bf16 inputs with nterms == 1 are copied).
 bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64_t ldi, bool transpose,
                         u16* const* out, int nterms, int64_t ldo, float scale, hipStream_t st);
+// The scale 2^e of a two-term fp16 split (bsp_common.h f16_scale_exp) from maxima held as
+// slots (AMAX_SLOTS words AMAX_STRIDE apart, float bits): the bound is amax_a's, or with amax_b
+// the larger of the two and e one lower, so that a sum of the two tensors (and each alone)
+// fits; inv_out (nullable) receives 2^-e, the contraction's multiplier.
+struct F16Scale {
+  const uint32_t* amax_a = nullptr;
+  const uint32_t* amax_b = nullptr;
+  float* inv_out = nullptr;
+};
 // The transposed planes (as launch_planes with transpose) of an fp32 in + add (add nullable), and
-// with outR non-null also the row-major planes out_R[r*ldr + c] from the same read. Needs C, ldi
-// and ldr multiples of 4, ldo of 64, 16-byte aligned in, add and outT, 8-byte aligned outR
-// (BS_EINVAL otherwise).
+// with outR non-null also the row-major planes out_R[r*ldr + c] (three bf16 terms) from the same
+// read. sc.amax_a non-null: the transposed planes are the two-term fp16 split (nterms = 2) at the
+// scale sc gives. Needs C, ldi and ldr multiples of 4, ldo of 64, 16-byte aligned in, add and
+// outT, 8-byte aligned outR (BS_EINVAL otherwise).
 bs_status launch_planes_t2(const float* in, const float* add, int64_t R, int64_t C, int64_t ldi, u16* const* outT,
-                           int nterms, int64_t ldo, u16* const* outR, int64_t ldr, hipStream_t st);
+                           int nterms, int64_t ldo, u16* const* outR, int64_t ldr, hipStream_t st,
+                           F16Scale sc = F16Scale{});
 
 // Trial statistics over per-trial rows (App. C.4, App. D.4).
 bs_status launch_policy_bias(const float* delta, int K, int64_t m, const float* g_ref, float* mean_err, float* se,

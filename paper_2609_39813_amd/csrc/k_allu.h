@@ -53,6 +53,7 @@ struct AlluDxArgs {
   const float* add;  // nullable [T][d]
   int64_t T, d;
   float* out;        // [T][d]
+  uint32_t* amax = nullptr;  // nullable: slots (AMAX_SLOTS) raised to max |out|
 };
 template <typename XT>
 bs_status launch_allu_dx(const AlluDxArgs<XT>& a, hipStream_t st);

@@ -84,10 +84,7 @@ __global__ __launch_bounds__(256) void allu_gain_kernel(AlluGainArgs<XT> a) {
 
 // one wave per row, 4 rows per block; columns in groups of 4 per lane
 template <typename XT>
-__global__ __launch_bounds__(256) void allu_dx_kernel(AlluDxArgs<XT> a) {
-  const int lane = threadIdx.x & 63;
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= a.T) return;  // uniform per wave
+__device__ __forceinline__ float allu_dx_row(const AlluDxArgs<XT>& a, int64_t t, int lane) {
   const float s = a.rd.scale ? *a.rd.scale : 1.0f;
   const double rs = 1.0 / (double)s;
   const float r = a.rstd[t];
@@ -113,6 +110,7 @@ __global__ __launch_bounds__(256) void allu_dx_kernel(AlluDxArgs<XT> a) {
   dref = __shfl(wave_sum_f64(dref), 0, 64);  // the wave sum is valid in lane 0: broadcast it
   dl = __shfl(wave_sum_f64(dl), 0, 64);
   const double inv_d = 1.0 / (double)a.d;
+  float mx = 0.0f;
   for (int64_t j0 = 4 * (int64_t)lane; j0 < a.d; j0 += 256) {
     float x[4], u[4], ddu[4] = {0.f, 0.f, 0.f, 0.f}, g[4], ad[4] = {0.f, 0.f, 0.f, 0.f};
     load4(a.X, rowe + j0, x);
@@ -128,9 +126,18 @@ __global__ __launch_bounds__(256) void allu_dx_kernel(AlluDxArgs<XT> a) {
       const double z = (double)(x[c] * r);
       const double zx = a.rd.letter == LETTER_U ? z : v[c] / (double)g[c];
       o[c] = (float)((double)r * ((double)g[c] * (double)ddu[c] - (zx * dl - z * dref) * inv_d) + (double)ad[c]);
+      mx = fmaxf(mx, fabsf(o[c]));
     }
     *(float4*)(a.out + rowe + j0) = make_float4(o[0], o[1], o[2], o[3]);
   }
+  return mx;
+}
+template <typename XT>
+__global__ __launch_bounds__(256) void allu_dx_kernel(AlluDxArgs<XT> a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const float mx = t < a.T ? allu_dx_row(a, t, lane) : 0.0f;  // uniform per wave
+  if (a.amax) block_amax_to_slot(mx, a.amax);
 }
 
 // 16 lanes per row of 64, 4 elements each; 16 rows per block

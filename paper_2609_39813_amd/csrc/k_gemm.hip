@@ -115,7 +115,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs g) {
 
   // D[i][j] of a 16x16 tile sits in lane (j + 16 * (i / 4)), register i % 4.
   const int oc = lane & 15, orow = (lane >> 4) * 4;
-  const float alpha = g.alpha_dev ? g.alpha * *g.alpha_dev : g.alpha;
+  const float alpha = gemm_alpha(g);
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
 #pragma unroll
@@ -145,8 +145,9 @@ constexpr int LBK = 64, LNST = 2;
 __device__ __forceinline__ int swz_of(int r) { return r & 7; }
 __device__ __forceinline__ int lds_swz(int r, int u) { return r * 128 + ((u ^ swz_of(r)) << 4); }
 
-// Block tile BM x BN, WGM x WGN wave64s, each owning a (BM / WGM) x (BN / WGN) tile.
-template <int BM, int BN, int WGM, int WGN>
+// Block tile BM x BN, WGM x WGN wave64s, each owning a (BM / WGM) x (BN / WGN) tile. F16: the
+// operands hold fp16 values (v_mfma_f32_16x16x32_f16), else bf16.
+template <int BM, int BN, int WGM, int WGN, bool F16>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, int cps) {
   constexpr int NW = WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 16, FN = WN / 16;
@@ -226,7 +227,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
   // MFMA t of a k-step, in row-major (i, j) order
   auto mfma_t = [&](int buf, int t) {
     const int i = t / FN, j = t % FN;
-    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+    if constexpr (F16)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(halfx8, fa[buf][i]),
+                                                         __builtin_bit_cast(halfx8, fb[buf][j]), acc[i][j], 0, 0, 0);
+    else
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
   };
   // read q of a k-step's fragments: B first (the first MFMAs use every B fragment), then A
   auto read_q = [&](int st, int s, int q, bf16x8* a, bf16x8* b) {
@@ -312,7 +317,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
   const int oc = lane & 15, orow = (lane >> 4) * 4;
   float* out = g.part ? g.part + (int64_t)split * g.M * g.N : g.C;
   const int64_t ldo = g.part ? g.N : g.ldc;
-  const float alpha = g.part ? 1.0f : (g.alpha_dev ? g.alpha * *g.alpha_dev : g.alpha);
+  const float alpha = g.part ? 1.0f : gemm_alpha(g);
   const bool acc_in = !g.part && g.accumulate;
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
@@ -336,7 +341,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
 // C = alpha * sum_s part[s] (+ C), splits summed in order
 __global__ __launch_bounds__(256) void gemm_split_sum_kernel(GemmArgs g, int splits) {
   const int64_t mn = (int64_t)g.M * g.N;
-  const float alpha = g.alpha_dev ? g.alpha * *g.alpha_dev : g.alpha;
+  const float alpha = gemm_alpha(g);
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < mn; i += (int64_t)gridDim.x * blockDim.x) {
     float v = g.part[i];
     for (int s = 1; s < splits; ++s) v += g.part[(int64_t)s * mn + i];
@@ -346,7 +351,7 @@ __global__ __launch_bounds__(256) void gemm_split_sum_kernel(GemmArgs g, int spl
   }
 }
 
-template <int BM, int BN, int WGM, int WGN>
+template <int BM, int BN, int WGM, int WGN, bool F16>
 static bs_status launch_gemm_lds(const GemmArgs& g0, hipStream_t st) {
   GemmArgs g = g0;
   const int64_t tiles = (int64_t)((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
@@ -375,7 +380,7 @@ static bs_status launch_gemm_lds(const GemmArgs& g0, hipStream_t st) {
   if (tiles * splits > 0x7FFFFFFF) return BS_ESHAPE;
   {
     ProfScope prof("gemm", st, gemm_flops(g), gemm_exec_flops(g));
-    gemm_lds_kernel<BM, BN, WGM, WGN><<<(unsigned)(tiles * splits), 64 * WGM * WGN, 0, st>>>(g, cps);
+    gemm_lds_kernel<BM, BN, WGM, WGN, F16><<<(unsigned)(tiles * splits), 64 * WGM * WGN, 0, st>>>(g, cps);
     BS_CHECK_LAUNCH();
   }
   if (splits > 1) {
@@ -407,10 +412,12 @@ bs_status launch_gemm(const GemmArgs& g, hipStream_t st) {
   // (buffer offsets of one 256-row tile fit in 31 bits)
   bool lds_ok = (g.K % LBK) == 0 && g.M >= 1 && g.N >= 1 && g.lda < (1 << 21) && g.ldb < (1 << 21);
   for (int i = 0; i < g.nseg; ++i) lds_ok = lds_ok && ((uintptr_t)g.A[i] & 15) == 0 && ((uintptr_t)g.B[i] & 15) == 0;
-  if (lds_ok) {
-    if ((int64_t)g.M * g.N >= (int64_t)256 * 256 * 16) return launch_gemm_lds<256, 256, 2, 4>(g, st);
-    return launch_gemm_lds<128, 128, 2, 2>(g, st);
-  }
+  const bool big_tiles = (int64_t)g.M * g.N >= (int64_t)256 * 256 * 16;
+  if (lds_ok && g.f16)
+    return big_tiles ? launch_gemm_lds<256, 256, 2, 4, true>(g, st) : launch_gemm_lds<128, 128, 2, 2, true>(g, st);
+  if (g.f16) return BS_EINVAL;  // fp16 operands: the pipelined kernel only
+  if (lds_ok)
+    return big_tiles ? launch_gemm_lds<256, 256, 2, 4, false>(g, st) : launch_gemm_lds<128, 128, 2, 2, false>(g, st);
   // 256 x 256 tiles once they still give every CU a tile; 128 x 128 below that
   const int64_t big = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256);
   if (big >= 256) return launch_gemm_cfg<256, 256, 2, 2>(g, st);

@@ -18,6 +18,7 @@ struct NormPlaneArgs {
   u16* out[3];             // planes [d][ldo]
   int nterms;
   int64_t ldo;
+  int f16 = 0;             // NP_VAL: fp16 values (exact for FP8 codes) instead of bf16
 };
 
 // rows per block of the gain use's column partial sums (the partial array holds one row of
@@ -80,6 +81,7 @@ struct TrialPlaneArgs {
   uint32_t use;
   int k0, nb;
   u16* out;  // [nb][d][ldo]
+  int f16 = 0;  // fp16 values (exact: powers of two on the FP8 grid) instead of bf16
 };
 bs_status launch_trial_planes(const TrialPlaneArgs& a, hipStream_t st);
 // Shifted fp64 sums over trials of delta [nb][m] (trials k0 ..): trial 1 is stored as the shift

@@ -165,7 +165,10 @@ __global__ __launch_bounds__(256) void norm_planes_t_kernel(NormPlaneArgs a) {
       const int64_t e = t * a.d + j;
       const uint32_t code = a.codes[e];
       if (MODE == NP_VAL) {
-        o[0] = bf16_bits(f8_value(code, a.f));
+        {
+          const float v = f8_value(code, a.f);
+          o[0] = a.f16 ? f16_bits(v) : bf16_bits(v);
+        }
       } else if (MODE == NP_RESU) {
         split3(fmaf(-s, f8_value(code, a.f), a.u[e]), o[0], o[1], o[2]);
       } else {
@@ -226,7 +229,8 @@ __global__ __launch_bounds__(256) void norm_planes_t4_kernel(NormPlaneArgs a) {
       for (int c = 0; c < 4; ++c) {
         const uint32_t code = (cw >> (8 * c)) & 0xFFu;
         if (MODE == NP_VAL) {
-          o[0][c] = bf16_bits(f8_value(code, a.f));
+          const float v = f8_value(code, a.f);
+          o[0][c] = a.f16 ? f16_bits(v) : bf16_bits(v);
         } else if (MODE == NP_RESU) {
           split3(fmaf(-s, f8_value(code, a.f), uv[c]), o[0][c], o[1][c], o[2][c]);
         } else {
@@ -291,7 +295,8 @@ __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
         const float y = div_scale(u4[c], rs);
         const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
         F[q][c] = b.F;
-        sv[q][c] = bf16_bits(signbit(y) ? -f8_step(b) : f8_step(b));
+        const float st = signbit(y) ? -f8_step(b) : f8_step(b);
+        sv[q][c] = a.f16 ? f16_bits(st) : bf16_bits(st);
         h[q] |= (uint32_t)(((cw >> (8 * c)) & 0x7Fu) != b.base + b.mi) << c;
       }
     }

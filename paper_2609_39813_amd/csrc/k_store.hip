@@ -439,4 +439,13 @@ bs_status launch_fresh_count(const float* u, int64_t T, int64_t d, int fmt, cons
   return launch_fresh_count_t(a, colsum ? FC_COLSUM : FC_COUNT, st);
 }
 
+bs_status launch_amax_f32(const float* x, int64_t n, uint32_t* out, hipStream_t st) {
+  if (n < 0 || (n > 0 && (!x || !out))) return BS_EINVAL;
+  if (n == 0) return BS_OK;
+  const int64_t want = (n / 4 + 255) / 256 + 1;
+  amax_kernel<float><<<(int)(want < 1024 ? want : 1024), 256, 0, st>>>(x, n, out);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
 }  // namespace bsp

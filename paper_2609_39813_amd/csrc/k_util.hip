@@ -155,11 +155,14 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const u16* __restri
 // column reads below fall on distinct banks); a thread then splits 8 consecutive rows of one
 // column and stores them as one 16-byte piece per plane, eight threads covering 128 bytes of an
 // output row. Optional: add (nullable, same layout as in) is added before the split, and the
-// row-major planes (rows.p[0] non-null, leading dimension ldr) are written from the same read.
+// row-major planes (rows.p[0] non-null, leading dimension ldr; three bf16 terms) are written from
+// the same read. F16T: the transposed planes are the two-term fp16 split at the scale 2^e that
+// scale sc gives (F16Scale), and 2^-e is stored to *sc.inv_out by the first thread (nullable).
+template <bool F16T>
 __global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* __restrict__ in, const float* __restrict__ add,
                                                                   int64_t R, int64_t C, int64_t ldi, PlaneOut out,
                                                                   int nterms, int64_t ldo, float scale, PlaneOut rows,
-                                                                  int64_t ldr) {
+                                                                  int64_t ldr, F16Scale sc) {
   __shared__ float tile[64][65];
   const int c4 = threadIdx.x & 15, rq = threadIdx.x >> 4;
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
@@ -181,15 +184,21 @@ __global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* _
     if (rows.p[0] && r < R && c < C) {
       u16 o[4][3];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) split_to(x[q], nterms, o[q]);
+      for (int q = 0; q < 4; ++q) split_to(x[q], 3, o[q]);
 #pragma unroll
       for (int p = 0; p < 3; ++p)
-        if (p < nterms)
-          *(uint2*)(rows.p[p] + r * ldr + c) = make_uint2((uint32_t)o[0][p] | ((uint32_t)o[1][p] << 16),
-                                                          (uint32_t)o[2][p] | ((uint32_t)o[3][p] << 16));
+        *(uint2*)(rows.p[p] + r * ldr + c) = make_uint2((uint32_t)o[0][p] | ((uint32_t)o[1][p] << 16),
+                                                        (uint32_t)o[2][p] | ((uint32_t)o[3][p] << 16));
     }
   }
   __syncthreads();
+  float scl = 1.0f;
+  if constexpr (F16T) {
+    const float a = amax_of_slots(sc.amax_a), b = sc.amax_b ? amax_of_slots(sc.amax_b) : 0.0f;
+    const int e = f16_scale_exp(fmaxf(a, b)) - (sc.amax_b ? 1 : 0);
+    scl = ldexpf(1.0f, e);
+    if (sc.inv_out && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *sc.inv_out = ldexpf(1.0f, -e);
+  }
   const int rg = threadIdx.x & 7;
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
@@ -198,7 +207,14 @@ __global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* _
     if (c >= C) continue;
     u16 o[8][3];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) split_to(tile[8 * rg + i][cc], nterms, o[i]);
+    for (int i = 0; i < 8; ++i) {
+      if constexpr (F16T) {
+        split2_f16(tile[8 * rg + i][cc] * scl, o[i][0], o[i][1]);
+        o[i][2] = 0;
+      } else {
+        split_to(tile[8 * rg + i][cc], nterms, o[i]);
+      }
+    }
 #pragma unroll
     for (int p = 0; p < 3; ++p) {
       if (p >= nterms) break;
@@ -252,8 +268,9 @@ bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64
     if (vec)
       transpose_bf16_kernel<<<grid, 256, 0, st>>>((const u16*)in, R, C, ldi, outp[0], ldo);
     else if (vecf)
-      transpose_split_f32_kernel<<<grid, 256, 0, st>>>((const float*)in, nullptr, R, C, ldi, out, nterms, ldo, scale,
-                                                       PlaneOut{{nullptr, nullptr, nullptr}}, 0);
+      transpose_split_f32_kernel<false><<<grid, 256, 0, st>>>((const float*)in, nullptr, R, C, ldi, out, nterms, ldo,
+                                                              scale, PlaneOut{{nullptr, nullptr, nullptr}}, 0,
+                                                              F16Scale{});
     else if (dt == BS_F32)
       planes_t_kernel<float><<<grid, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
     else
@@ -284,21 +301,22 @@ bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64
 }
 
 bs_status launch_planes_t2(const float* in, const float* add, int64_t R, int64_t C, int64_t ldi, u16* const* outT,
-                           int nterms, int64_t ldo, u16* const* outR, int64_t ldr, hipStream_t st) {
-  if (nterms < 1 || nterms > 3) return BS_EINVAL;
+                           int nterms, int64_t ldo, u16* const* outR, int64_t ldr, hipStream_t st, F16Scale sc) {
+  if (nterms < 1 || nterms > 3 || (sc.amax_a && nterms != 2)) return BS_EINVAL;
   if (C <= 0 || ldo <= 0) return BS_OK;
   bool ok = C % 4 == 0 && ldi % 4 == 0 && ldo % 64 == 0 && ((uintptr_t)in & 15) == 0 && ((uintptr_t)add & 15) == 0 &&
             (!outR || (ldr % 4 == 0 && ldr >= C));
-  for (int p = 0; p < nterms; ++p) {
-    ok = ok && ((uintptr_t)outT[p] & 15) == 0;
-    if (outR) ok = ok && ((uintptr_t)outR[p] & 7) == 0;
-  }
+  for (int p = 0; p < nterms; ++p) ok = ok && outT[p] && ((uintptr_t)outT[p] & 15) == 0;
+  // the row-major planes are always the three bf16 terms, whatever nterms
+  for (int p = 0; outR && p < 3; ++p) ok = ok && outR[p] && ((uintptr_t)outR[p] & 7) == 0;
   if (!ok) return BS_EINVAL;
   const PlaneOut out{{outT[0], nterms > 1 ? outT[1] : nullptr, nterms > 2 ? outT[2] : nullptr}};
-  const PlaneOut rows{{outR ? outR[0] : nullptr, outR && nterms > 1 ? outR[1] : nullptr,
-                       outR && nterms > 2 ? outR[2] : nullptr}};
+  const PlaneOut rows{{outR ? outR[0] : nullptr, outR ? outR[1] : nullptr, outR ? outR[2] : nullptr}};
   const dim3 grid((unsigned)((C + 63) / 64), (unsigned)((ldo + 63) / 64));
-  transpose_split_f32_kernel<<<grid, 256, 0, st>>>(in, add, R, C, ldi, out, nterms, ldo, 1.0f, rows, ldr);
+  if (sc.amax_a)
+    transpose_split_f32_kernel<true><<<grid, 256, 0, st>>>(in, add, R, C, ldi, out, nterms, ldo, 1.0f, rows, ldr, sc);
+  else
+    transpose_split_f32_kernel<false><<<grid, 256, 0, st>>>(in, add, R, C, ldi, out, nterms, ldo, 1.0f, rows, ldr, sc);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

@@ -53,6 +53,8 @@ struct AlluWs {
   int64_t part_cap;
   double* sumsq_part;
   bs_diag* diag;
+  uint32_t* amax[4];  // slot arrays of max |.|: dh, dQKV (per call), dh_d, dQKV_d (per pass)
+  float* inv;      // 2^-e of the fp16 splits of the Wo and Wqkv weight uses
 };
 
 AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
@@ -100,6 +102,11 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
   w.part = c.take<float>(w.part_cap);
   w.sumsq_part = c.take<double>(sumsq_part_size());
   w.diag = c.take<bs_diag>(1);
+  {
+    uint32_t* a = c.take<uint32_t>(4 * AMAX_SLOTS * AMAX_STRIDE);
+    for (int i = 0; i < 4; ++i) w.amax[i] = a + i * AMAX_SLOTS * AMAX_STRIDE;
+  }
+  w.inv = c.take<float>(2);
   return w;
 }
 
@@ -187,8 +194,15 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     for (int i = 0; i < 3; ++i) pa.out[i] = i < nterms ? out[i] : nullptr;
     return launch_norm_planes(mode, pa, st);
   };
+  // the R and N weight uses contract fp16 operands: FP8 values (exact in fp16) against the scaled
+  // two-term fp16 split of the incoming gradient and its move
+  pa.f16 = 1;
   BS_TRY(planes_of(NP_VAL, w.u1, io.c_u1, s_u1, &w.valT_u1, 1));
   BS_TRY(planes_of(NP_VAL, io.Otok, io.c_Otok, s_O, &w.valT_O, 1));
+  pa.f16 = 0;
+  BS_TRY(launch_fill2d((float*)w.amax[0], 2 * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
+  BS_TRY(launch_amax_f32(io.dh, Td, w.amax[0], st));
+  BS_TRY(launch_amax_f32(io.dqkv, 3 * Td, w.amax[1], st));
   BS_TRY(launch_planes(io.dqkv, BS_F32, T, d3, d3, true, w.dqkvT, 3, Tp, 1.0f, st));
   BS_TRY(launch_planes(io.dh, BS_F32, T, d, d, true, w.dhT, 3, Tp, 1.0f, st));
 
@@ -201,26 +215,33 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       };
       float* dWo = w.delta[3];
       float* dWqkv = w.delta[2];
-      // u2's normalization-input use: the move of dh
+      // u2's normalization-input use: the move of dh (and its max |.|)
       if (l != LETTER_U) {
-        const AlluDxArgs<float> ax{io.h, w.r2, io.gain2, rd(w.u2, io.c_u2, s_u2, 2 * 256 + 3), w.du2, nullptr,
-                                   nullptr, T, d, w.dh_d};
+        BS_TRY(launch_fill2d((float*)w.amax[2], 2 * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
+        AlluDxArgs<float> ax{io.h, w.r2, io.gain2, rd(w.u2, io.c_u2, s_u2, 2 * 256 + 3), w.du2, nullptr,
+                             nullptr, T, d, w.dh_d};
+        ax.amax = w.amax[2];
         BS_TRY(launch_allu_dx(ax, st));
       }
+      // one scale for dh_d and dh + dh_d (the contraction has one multiplier)
+      const F16Scale sc_o{w.amax[2], w.amax[0], w.inv + 0}, sc_q{w.amax[3], w.amax[1], w.inv + 1};
       // O's weight use (Wo)
       if (l == LETTER_U) {
         BS_TRY(planes_of(NP_RESU, io.Otok, io.c_Otok, s_O, w.pA, 3));
         BS_TRY(Gemm(d, d, (int)Tp, Tp, Tp, dWo, d, nullptr).add(w.pA, 3, w.dhT, 3).run(w.part, w.part_cap, st));
       } else {
         // dh_d's transposed planes (the weight use) and row planes (the move of dO), one read
-        BS_TRY(launch_planes_t2(w.dh_d, nullptr, T, d, d, w.tB, 3, Tp, w.rows3, d, st));
+        BS_TRY(launch_planes_t2(w.dh_d, nullptr, T, d, d, w.tB, 2, Tp, w.rows3, d, st, sc_o));
         Gemm gw(d, d, (int)Tp, Tp, Tp, dWo, d, s_O);
-        gw.add(&w.valT_O, 1, w.tB, 3);
+        gw.g.f16 = 1;
+        gw.g.alpha_dev2 = w.inv + 0;
+        gw.add(&w.valT_O, 1, w.tB, 2);
         if (l == LETTER_N) {
-          BS_TRY(launch_planes_t2(io.dh, w.dh_d, T, d, d, w.tA, 3, Tp, nullptr, 0, st));  // dh_L = dh + dh_d
-          const TrialPlaneArgs ta{io.Otok, io.c_Otok, s_O, f, T, d, Tp, io.seed, 1 * 256 + 2, k, 1, w.pA[0]};
+          BS_TRY(launch_planes_t2(io.dh, w.dh_d, T, d, d, w.tA, 2, Tp, nullptr, 0, st, sc_o));  // dh_L = dh + dh_d
+          TrialPlaneArgs ta{io.Otok, io.c_Otok, s_O, f, T, d, Tp, io.seed, 1 * 256 + 2, k, 1, w.pA[0]};
+          ta.f16 = 1;
           BS_TRY(launch_trial_planes(ta, st));
-          gw.add(&w.pA[0], 1, w.tA, 3);
+          gw.add(&w.pA[0], 1, w.tA, 2);
         }
         BS_TRY(gw.run(w.part, w.part_cap, st));
         // the move of dO (token-major, then head-major)
@@ -262,16 +283,19 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         ba.dV = w.dV_d;
         ba.n_pol = 0;
         BS_TRY(launch_attn_bwd(ba, B, H, st));
-        BS_TRY(launch_dqkv_tokens(w.dQ_d, w.dK_d, w.dV_d, w.dqkv_d, B, S, H, DH, st));
+        BS_TRY(launch_dqkv_tokens(w.dQ_d, w.dK_d, w.dV_d, w.dqkv_d, B, S, H, DH, st, w.amax[3]));
         // u1's weight use (Wqkv)
-        BS_TRY(launch_planes_t2(w.dqkv_d, nullptr, T, d3, d3, w.tB, 3, Tp, w.rows3, d3, st));
+        BS_TRY(launch_planes_t2(w.dqkv_d, nullptr, T, d3, d3, w.tB, 2, Tp, w.rows3, d3, st, sc_q));
         Gemm gq(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, s_u1);
-        gq.add(&w.valT_u1, 1, w.tB, 3);
+        gq.g.f16 = 1;
+        gq.g.alpha_dev2 = w.inv + 1;
+        gq.add(&w.valT_u1, 1, w.tB, 2);
         if (l == LETTER_N) {
-          BS_TRY(launch_planes_t2(io.dqkv, w.dqkv_d, T, d3, d3, w.tA, 3, Tp, nullptr, 0, st));  // dqkv + dqkv_d
-          const TrialPlaneArgs ta{w.u1, io.c_u1, s_u1, f, T, d, Tp, io.seed, 0 * 256 + 2, k, 1, w.pA[0]};
+          BS_TRY(launch_planes_t2(io.dqkv, w.dqkv_d, T, d3, d3, w.tA, 2, Tp, nullptr, 0, st, sc_q));  // dqkv + dqkv_d
+          TrialPlaneArgs ta{w.u1, io.c_u1, s_u1, f, T, d, Tp, io.seed, 0 * 256 + 2, k, 1, w.pA[0]};
+          ta.f16 = 1;
           BS_TRY(launch_trial_planes(ta, st));
-          gq.add(&w.pA[0], 1, w.tA, 3);
+          gq.add(&w.pA[0], 1, w.tA, 2);
         }
         BS_TRY(gq.run(w.part, w.part_cap, st));
         // the move of du1, then u1's gain and normalization-input uses
