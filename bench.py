@@ -8,7 +8,7 @@ passes for N). Inputs are resident in HBM before the timed region. The metric is
 per second: (#policies x K) / step time, with 6 policies (U, R, N per use and at every use).
 
 Prints one JSON line. `roofline` is the step's dominant kernel, the MFMA contraction (bf16, and
-fp16 for the scaled two-term splits of the every-use weight contractions; one peak for both), timed
+fp16 for the scaled two-term splits of the every-use passes; one peak for both), timed
 live with HIP events on its launch stream (algorithmic flop per launch over the average launch
 time); `cpu_baseline` times the plain CPU oracle on a bounded sample of the same workload (rank
 0, N = 1 only). `extra` holds the metric's other figures: the RMSNorm -> Linear check at the MLP
@@ -454,8 +454,9 @@ def main():
                 "executed_TFLOPs": round(xflop / max(g_n, 1) / avg_s / 1e12, 1) if g_n else 0.0,
                 "executed_frac": round(xflop / max(g_n, 1) / avg_s / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4) if g_n else 0.0,
                 "executed_note": "fp32 operands (incoming gradients, residuals) enter as exact sums of 3 bf16 terms, "
-                                 "or against FP8 values as 2 scaled fp16 terms (error <= 2^-22 relative), for "
-                                 "1e-5 parity; executed flop counts every term product"}
+                                 "or in the every-use passes as 2 scaled fp16 terms (error <= 2^-22 relative) "
+                                 "against FP8 values or scaled fp16 weights, for 1e-5 parity; executed flop counts "
+                                 "every term product"}
     extra = {"kernel_ms_per_step": {k: round(v[0] / args.steps, 4) for k, v in prof.items()},
              "gemm_TFLOP_per_step": round(flop / args.steps / 1e12, 4),
              "work": "forward, reference backward, U/R/N at the 10 uses of the 4 stores (K = 16 new roundings per "

@@ -107,6 +107,7 @@ bs_status launch_fill_f64(double* p, int64_t n, double v, hipStream_t st);
 // *out (the float bits of a maximum, zeroed by the caller) raised to max |x[i]| over n floats;
 // with the other AMAX_SLOTS - 1 slots zeroed, out is a slot array
 bs_status launch_amax_f32(const float* x, int64_t n, uint32_t* out, hipStream_t st);
+bs_status launch_amax_bf16(const u16* x, int64_t n, uint32_t* out, hipStream_t st);
 bs_status launch_init_diag(bs_diag* diag, hipStream_t st);
 
 // bf16 operand planes. Row-major: out_p[r*ldo + c], c < C (ldo >= C). Transposed:
@@ -123,14 +124,26 @@ struct F16Scale {
   const uint32_t* amax_b = nullptr;
   float* inv_out = nullptr;
 };
-// The transposed planes (as launch_planes with transpose) of an fp32 in + add (add nullable), and
-// with outR non-null also the row-major planes out_R[r*ldr + c] (three bf16 terms) from the same
-// read. sc.amax_a non-null: the transposed planes are the two-term fp16 split (nterms = 2) at the
-// scale sc gives. Needs C, ldi and ldr multiples of 4, ldo of 64, 16-byte aligned in, add and
-// outT, 8-byte aligned outR (BS_EINVAL otherwise).
-bs_status launch_planes_t2(const float* in, const float* add, int64_t R, int64_t C, int64_t ldi, u16* const* outT,
-                           int nterms, int64_t ldo, u16* const* outR, int64_t ldr, hipStream_t st,
-                           F16Scale sc = F16Scale{});
+// A move tensor seen as a token-major [R][C] fp32 matrix: rows[t*ldi + c], or (rows null) the
+// head-major [B][H][S][64] arrays heads[c / d] (Q, K, V gradients; d = 64 H, R = B S).
+struct MoveSrc {
+  const float* rows = nullptr;
+  int64_t ldi = 0;
+  const float* heads[3] = {nullptr, nullptr, nullptr};
+  int64_t S = 0, H = 0, d = 0;
+};
+// The scaled two-term fp16 planes (scale from sc, F16Scale) of a move m, from one read: tM =
+// transposed planes of m (tM_p[c*ldo + r], rows R..ldo zero), tS (with base non-null) those of
+// base + m (base [R][C] with leading dimension ldb), rows (nullable) the row-major planes
+// rows_p[r*ldr + c]. Needs C and the leading dimensions multiples of 4 (ldo of 64, ldo >= R),
+// 16-byte aligned inputs and transposed planes, 8-byte aligned row planes (BS_EINVAL otherwise).
+bs_status launch_split_move(const MoveSrc& m, const float* base, int64_t ldb, int64_t R, int64_t C, F16Scale sc,
+                            u16* const* tM, u16* const* tS, int64_t ldo, u16* const* rows, int64_t ldr,
+                            hipStream_t st);
+// out = fp16(in 2^e) of a bf16 tensor with e = f16_scale_exp of the max held in slots (an
+// AMAX_SLOTS array), 2^-e to inv_out (nullable). Exact where |in| 2^e >= 2^-17 (fp16 subnormal
+// spacing); below, the error is at most 2^-25 2^-e.
+bs_status launch_scale_f16(const u16* in, int64_t n, const uint32_t* slots, u16* out, float* inv_out, hipStream_t st);
 
 // Trial statistics over per-trial rows (App. C.4, App. D.4).
 bs_status launch_policy_bias(const float* delta, int K, int64_t m, const float* g_ref, float* mean_err, float* se,

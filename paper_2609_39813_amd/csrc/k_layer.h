@@ -9,7 +9,7 @@ bs_status launch_heads_tokens_f32(const float* in, float* out, int B, int S, int
                                   hipStream_t st);
 bs_status launch_heads_tokens_u8(const uint8_t* in, uint8_t* out, int B, int S, int H, int dh, hipStream_t st);
 bs_status launch_dqkv_tokens(const float* dQ, const float* dK, const float* dV, float* out, int B, int S, int H,
-                             int dh, hipStream_t st, uint32_t* amax = nullptr);
+                             int dh, hipStream_t st);
 bs_status launch_bf16_to_f32(const u16* in, float* out, int64_t n, hipStream_t st);
 bs_status launch_concat_cols(const u16* A, const u16* B, u16* out, int64_t rows, int64_t c1, int64_t c2,
                              hipStream_t st);

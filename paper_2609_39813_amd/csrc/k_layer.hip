@@ -64,21 +64,16 @@ __global__ __launch_bounds__(256) void heads_tokens4_kernel(const E4* __restrict
   }
 }
 // dQ, dK, dV [B,H,S,dh] -> dQKV [T][3d], four elements at a time
-// (amax nullable: slots (AMAX_SLOTS) raised to max |out|, one atomic per block)
 __global__ __launch_bounds__(256) void dqkv_tokens4_kernel(const float4* __restrict__ dQ, const float4* __restrict__ dK,
                                                            const float4* __restrict__ dV, float4* __restrict__ out,
-                                                           int S, int H, int dh, uint32_t* __restrict__ amax) {
+                                                           int S, int H, int dh) {
   const int t = blockIdx.x, b = t / S, s = t - b * S;
   const int q = dh / 4, n = H * q;
-  float mx = 0.0f;
   for (int k = threadIdx.x; k < 3 * n; k += blockDim.x) {
     const int which = k / n, kk = k - which * n, h = kk / q, c = kk - h * q;
     const int64_t hm = (((int64_t)b * H + h) * S + s) * q + c;
-    const float4 v = (which == 0 ? dQ : (which == 1 ? dK : dV))[hm];
-    out[(int64_t)t * 3 * n + k] = v;
-    mx = fmaxf(mx, fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w))));
+    out[(int64_t)t * 3 * n + k] = (which == 0 ? dQ : (which == 1 ? dK : dV))[hm];
   }
-  if (amax) block_amax_to_slot(mx, amax);
 }
 
 // dQ, dK, dV [B,H,S,dh] -> dQKV [T][3d]
@@ -234,12 +229,10 @@ bs_status launch_heads_tokens_u8(const uint8_t* in, uint8_t* out, int B, int S, 
   return BS_OK;
 }
 bs_status launch_dqkv_tokens(const float* dQ, const float* dK, const float* dV, float* out, int B, int S, int H,
-                             int dh, hipStream_t st, uint32_t* amax) {
+                             int dh, hipStream_t st) {
   if (dh % 4 == 0 && al(dQ, 16) && al(dK, 16) && al(dV, 16) && al(out, 16) && rows_ok(B, S))
     dqkv_tokens4_kernel<<<(unsigned)(B * S), 256, 0, st>>>((const float4*)dQ, (const float4*)dK, (const float4*)dV,
-                                                           (float4*)out, S, H, dh, amax);
-  else if (amax)
-    return BS_EINVAL;  // the max is raised by the vector kernel only
+                                                           (float4*)out, S, H, dh);
   else
     dqkv_tokens_kernel<<<blocks_for((int64_t)B * S * 3 * H * dh), 256, 0, st>>>(dQ, dK, dV, out, B, S, H, dh);
   BS_CHECK_LAUNCH();

@@ -447,5 +447,13 @@ bs_status launch_amax_f32(const float* x, int64_t n, uint32_t* out, hipStream_t 
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
+bs_status launch_amax_bf16(const u16* x, int64_t n, uint32_t* out, hipStream_t st) {
+  if (n < 0 || (n > 0 && (!x || !out))) return BS_EINVAL;
+  if (n == 0) return BS_OK;
+  const int64_t want = (n / 8 + 255) / 256 + 1;
+  amax_kernel<u16><<<(int)(want < 1024 ? want : 1024), 256, 0, st>>>(x, n, out);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
 
 }  // namespace bsp

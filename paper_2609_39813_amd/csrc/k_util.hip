@@ -154,15 +154,10 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const u16* __restri
 // 64 x 64 tile goes into LDS as fp32 (rows padded to 65 words, so both the row writes and the
 // column reads below fall on distinct banks); a thread then splits 8 consecutive rows of one
 // column and stores them as one 16-byte piece per plane, eight threads covering 128 bytes of an
-// output row. Optional: add (nullable, same layout as in) is added before the split, and the
-// row-major planes (rows.p[0] non-null, leading dimension ldr; three bf16 terms) are written from
-// the same read. F16T: the transposed planes are the two-term fp16 split at the scale 2^e that
-// scale sc gives (F16Scale), and 2^-e is stored to *sc.inv_out by the first thread (nullable).
-template <bool F16T>
-__global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* __restrict__ in, const float* __restrict__ add,
-                                                                  int64_t R, int64_t C, int64_t ldi, PlaneOut out,
-                                                                  int nterms, int64_t ldo, float scale, PlaneOut rows,
-                                                                  int64_t ldr, F16Scale sc) {
+// output row.
+__global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* __restrict__ in, int64_t R, int64_t C,
+                                                                  int64_t ldi, PlaneOut out, int nterms, int64_t ldo,
+                                                                  float scale) {
   __shared__ float tile[64][65];
   const int c4 = threadIdx.x & 15, rq = threadIdx.x >> 4;
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
@@ -171,34 +166,13 @@ __global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* _
     const int rr = rq + 16 * i;
     const int64_t r = r0 + rr, c = c0 + 4 * c4;
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < R && c < C) {
-      v = *(const float4*)(in + r * ldi + c);
-      if (add) {
-        const float4 b = *(const float4*)(add + r * ldi + c);
-        v = make_float4(v.x + b.x, v.y + b.y, v.z + b.z, v.w + b.w);
-      }
-    }
-    const float x[4] = {v.x * scale, v.y * scale, v.z * scale, v.w * scale};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) tile[rr][4 * c4 + q] = x[q];
-    if (rows.p[0] && r < R && c < C) {
-      u16 o[4][3];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) split_to(x[q], 3, o[q]);
-#pragma unroll
-      for (int p = 0; p < 3; ++p)
-        *(uint2*)(rows.p[p] + r * ldr + c) = make_uint2((uint32_t)o[0][p] | ((uint32_t)o[1][p] << 16),
-                                                        (uint32_t)o[2][p] | ((uint32_t)o[3][p] << 16));
-    }
+    if (r < R && c < C) v = *(const float4*)(in + r * ldi + c);
+    tile[rr][4 * c4 + 0] = v.x * scale;
+    tile[rr][4 * c4 + 1] = v.y * scale;
+    tile[rr][4 * c4 + 2] = v.z * scale;
+    tile[rr][4 * c4 + 3] = v.w * scale;
   }
   __syncthreads();
-  float scl = 1.0f;
-  if constexpr (F16T) {
-    const float a = amax_of_slots(sc.amax_a), b = sc.amax_b ? amax_of_slots(sc.amax_b) : 0.0f;
-    const int e = f16_scale_exp(fmaxf(a, b)) - (sc.amax_b ? 1 : 0);
-    scl = ldexpf(1.0f, e);
-    if (sc.inv_out && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *sc.inv_out = ldexpf(1.0f, -e);
-  }
   const int rg = threadIdx.x & 7;
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
@@ -207,14 +181,7 @@ __global__ __launch_bounds__(256) void transpose_split_f32_kernel(const float* _
     if (c >= C) continue;
     u16 o[8][3];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      if constexpr (F16T) {
-        split2_f16(tile[8 * rg + i][cc] * scl, o[i][0], o[i][1]);
-        o[i][2] = 0;
-      } else {
-        split_to(tile[8 * rg + i][cc], nterms, o[i]);
-      }
-    }
+    for (int i = 0; i < 8; ++i) split_to(tile[8 * rg + i][cc], nterms, o[i]);
 #pragma unroll
     for (int p = 0; p < 3; ++p) {
       if (p >= nterms) break;
@@ -268,9 +235,7 @@ bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64
     if (vec)
       transpose_bf16_kernel<<<grid, 256, 0, st>>>((const u16*)in, R, C, ldi, outp[0], ldo);
     else if (vecf)
-      transpose_split_f32_kernel<false><<<grid, 256, 0, st>>>((const float*)in, nullptr, R, C, ldi, out, nterms, ldo,
-                                                              scale, PlaneOut{{nullptr, nullptr, nullptr}}, 0,
-                                                              F16Scale{});
+      transpose_split_f32_kernel<<<grid, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
     else if (dt == BS_F32)
       planes_t_kernel<float><<<grid, 256, 0, st>>>((const float*)in, R, C, ldi, out, nterms, ldo, scale);
     else
@@ -300,23 +265,133 @@ bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64
   return BS_OK;
 }
 
-bs_status launch_planes_t2(const float* in, const float* add, int64_t R, int64_t C, int64_t ldi, u16* const* outT,
-                           int nterms, int64_t ldo, u16* const* outR, int64_t ldr, hipStream_t st, F16Scale sc) {
-  if (nterms < 1 || nterms > 3 || (sc.amax_a && nterms != 2)) return BS_EINVAL;
-  if (C <= 0 || ldo <= 0) return BS_OK;
-  bool ok = C % 4 == 0 && ldi % 4 == 0 && ldo % 64 == 0 && ((uintptr_t)in & 15) == 0 && ((uintptr_t)add & 15) == 0 &&
-            (!outR || (ldr % 4 == 0 && ldr >= C));
-  for (int p = 0; p < nterms; ++p) ok = ok && outT[p] && ((uintptr_t)outT[p] & 15) == 0;
-  // the row-major planes are always the three bf16 terms, whatever nterms
-  for (int p = 0; outR && p < 3; ++p) ok = ok && outR[p] && ((uintptr_t)outR[p] & 7) == 0;
+// ------------------------------------------------------------------------------------
+// The operands of a move's contractions as scaled two-term fp16 splits, from one read of the move
+// (and of the gradient it moves): its transposed planes (the weight use), those of gradient +
+// move, and its row-major planes (the move's own propagation). A 64 x 64 tile per block, staged
+// through LDS as in the transposed split above.
+// ------------------------------------------------------------------------------------
+__device__ __forceinline__ const float* move_at(const MoveSrc& m, int64_t t, int64_t c) {
+  if (m.rows) return m.rows + t * m.ldi + c;
+  const int64_t which = c / m.d, cc = c - which * m.d;  // which of Q, K, V; the column in it
+  const int64_t b = t / m.S, s = t - b * m.S;
+  return m.heads[which] + (((b * m.H + (cc >> 6)) * m.S + s) << 6) + (cc & 63);
+}
+
+__global__ __launch_bounds__(256) void split_move_f16_kernel(MoveSrc src, const float* __restrict__ base, int64_t ldb,
+                                                             int64_t R, int64_t C, F16Scale sc, PlaneOut tM,
+                                                             PlaneOut tS, int64_t ldo, PlaneOut rows, int64_t ldr) {
+  __shared__ float tile[64][65];
+  __shared__ float tileS[64][65];
+  const float a = amax_of_slots(sc.amax_a), b = sc.amax_b ? amax_of_slots(sc.amax_b) : 0.0f;
+  const int e = f16_scale_exp(fmaxf(a, b)) - (sc.amax_b ? 1 : 0);
+  const float scl = ldexpf(1.0f, e);
+  if (sc.inv_out && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *sc.inv_out = ldexpf(1.0f, -e);
+  const int c4 = threadIdx.x & 15, rq = threadIdx.x >> 4;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int rr = rq + 16 * i;
+    const int64_t r = r0 + rr, c = c0 + 4 * c4;
+    const bool in = r < R && c < C;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f), w = v;
+    if (in) {
+      v = *(const float4*)move_at(src, r, c);
+      if (base) {
+        const float4 g = *(const float4*)(base + r * ldb + c);
+        w = make_float4(g.x + v.x, g.y + v.y, g.z + v.z, g.w + v.w);
+      }
+    }
+    const float x[4] = {v.x * scl, v.y * scl, v.z * scl, v.w * scl};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) tile[rr][4 * c4 + q] = x[q];
+    if (base) {
+      tileS[rr][4 * c4 + 0] = w.x * scl;
+      tileS[rr][4 * c4 + 1] = w.y * scl;
+      tileS[rr][4 * c4 + 2] = w.z * scl;
+      tileS[rr][4 * c4 + 3] = w.w * scl;
+    }
+    if (rows.p[0] && in) {
+      u16 hi[4], lo[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) split2_f16(x[q], hi[q], lo[q]);
+      *(uint2*)(rows.p[0] + r * ldr + c) = make_uint2((uint32_t)hi[0] | ((uint32_t)hi[1] << 16),
+                                                      (uint32_t)hi[2] | ((uint32_t)hi[3] << 16));
+      *(uint2*)(rows.p[1] + r * ldr + c) = make_uint2((uint32_t)lo[0] | ((uint32_t)lo[1] << 16),
+                                                      (uint32_t)lo[2] | ((uint32_t)lo[3] << 16));
+    }
+  }
+  __syncthreads();
+  // a thread splits 8 consecutive rows of one column: one 16-byte piece per plane
+  const int rg = threadIdx.x & 7;
+  auto put = [&](float (*t)[65], const PlaneOut& out, int cc, int64_t c) {
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      u16 h0, l0, h1, l1;
+      split2_f16(t[8 * rg + 2 * i][cc], h0, l0);
+      split2_f16(t[8 * rg + 2 * i + 1][cc], h1, l1);
+      h[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+      l[i] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+    }
+    *(uint4*)(out.p[0] + c * ldo + r0 + 8 * rg) = make_uint4(h[0], h[1], h[2], h[3]);
+    *(uint4*)(out.p[1] + c * ldo + r0 + 8 * rg) = make_uint4(l[0], l[1], l[2], l[3]);
+  };
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int cc = (threadIdx.x >> 3) + 32 * pass;
+    const int64_t c = c0 + cc;
+    if (c >= C) continue;
+    put(tile, tM, cc, c);
+    if (base) put(tileS, tS, cc, c);
+  }
+}
+
+bs_status launch_split_move(const MoveSrc& m, const float* base, int64_t ldb, int64_t R, int64_t C, F16Scale sc,
+                            u16* const* tM, u16* const* tS, int64_t ldo, u16* const* rows, int64_t ldr,
+                            hipStream_t st) {
+  auto a16 = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  if (!sc.amax_a || !tM || !tM[0] || !tM[1] || (base && (!tS || !tS[0] || !tS[1])) ||
+      (rows && (!rows[0] || !rows[1])))
+    return BS_EINVAL;
+  if (R <= 0 || C <= 0) return BS_OK;
+  bool ok = C % 4 == 0 && ldo % 64 == 0 && ldo >= R && a16(tM[0]) && a16(tM[1]);
+  if (m.rows) {
+    ok = ok && m.ldi % 4 == 0 && m.ldi >= C && a16(m.rows);
+  } else {
+    // head-major: 64-wide heads, C / d of Q, K, V, R = B S rows
+    ok = ok && m.d > 0 && m.d % 64 == 0 && m.H * 64 == m.d && m.S > 0 && R % m.S == 0 && C % m.d == 0 &&
+         C / m.d <= 3;
+    for (int64_t i = 0; ok && i < C / m.d; ++i) ok = m.heads[i] && a16(m.heads[i]);
+  }
+  if (base) ok = ok && ldb % 4 == 0 && ldb >= C && a16(base) && a16(tS[0]) && a16(tS[1]);
+  if (rows) ok = ok && ldr % 4 == 0 && ldr >= C && ((uintptr_t)rows[0] & 7) == 0 && ((uintptr_t)rows[1] & 7) == 0;
   if (!ok) return BS_EINVAL;
-  const PlaneOut out{{outT[0], nterms > 1 ? outT[1] : nullptr, nterms > 2 ? outT[2] : nullptr}};
-  const PlaneOut rows{{outR ? outR[0] : nullptr, outR ? outR[1] : nullptr, outR ? outR[2] : nullptr}};
-  const dim3 grid((unsigned)((C + 63) / 64), (unsigned)((ldo + 63) / 64));
-  if (sc.amax_a)
-    transpose_split_f32_kernel<true><<<grid, 256, 0, st>>>(in, add, R, C, ldi, out, nterms, ldo, 1.0f, rows, ldr, sc);
-  else
-    transpose_split_f32_kernel<false><<<grid, 256, 0, st>>>(in, add, R, C, ldi, out, nterms, ldo, 1.0f, rows, ldr, sc);
+  const PlaneOut pm{{tM[0], tM[1], nullptr}};
+  const PlaneOut ps{{base ? tS[0] : nullptr, base ? tS[1] : nullptr, nullptr}};
+  const PlaneOut pr{{rows ? rows[0] : nullptr, rows ? rows[1] : nullptr, nullptr}};
+  const dim3 grid((unsigned)((C + 63) / 64), (unsigned)(ldo / 64));
+  split_move_f16_kernel<<<grid, 256, 0, st>>>(m, base, ldb, R, C, sc, pm, ps, ldo, pr, ldr);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+
+// fp16 of a bf16 tensor scaled by 2^e (the max in slots), 2^-e to inv_out
+__global__ __launch_bounds__(256) void scale_f16_kernel(const u16* __restrict__ in, int64_t n,
+                                                        const uint32_t* __restrict__ slots, u16* __restrict__ out,
+                                                        float* __restrict__ inv_out) {
+  const int e = f16_scale_exp(amax_of_slots(slots));
+  const float scl = ldexpf(1.0f, e);
+  if (inv_out && blockIdx.x == 0 && threadIdx.x == 0) *inv_out = ldexpf(1.0f, -e);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = f16_bits(__uint_as_float((uint32_t)in[i] << 16) * scl);
+}
+
+bs_status launch_scale_f16(const u16* in, int64_t n, const uint32_t* slots, u16* out, float* inv_out, hipStream_t st) {
+  if (n < 0 || (n > 0 && (!in || !slots || !out))) return BS_EINVAL;
+  if (n == 0) return BS_OK;
+  const int64_t want = (n + 255) / 256;
+  scale_f16_kernel<<<(unsigned)(want < 4096 ? want : 4096), 256, 0, st>>>(in, n, slots, out, inv_out);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

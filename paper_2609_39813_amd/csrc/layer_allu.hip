@@ -41,7 +41,8 @@ struct AlluWs {
   float *u1, *u2, *r1, *r2, *du1, *du2, *m, *l;
   u16 *Vt, *Qt, *Kt, *valT_u1, *valT_O, *dqkvT[3], *dhT[3];
   u16 *pA[3], *rows3[3], *tA[3], *tB[3], *dOp[3], *dOt[3];
-  float *dh_d, *dO_dt, *dO_dh, *dD, *dQ_d, *dK_d, *dV_d, *dqkv_d, *du1_d;
+  float *dh_d, *dO_dt, *dO_dh, *dD, *dQ_d, *dK_d, *dV_d, *du1_d;
+  u16 *Wo16, *Wqkv16;  // the weights as scaled fp16 (the moves' contractions)
   double* gpart;
   float* delta[NCOMP];      // this pass's moves
   float* bias[3][NCOMP];    // per letter
@@ -53,8 +54,9 @@ struct AlluWs {
   int64_t part_cap;
   double* sumsq_part;
   bs_diag* diag;
-  uint32_t* amax[4];  // slot arrays of max |.|: dh, dQKV (per call), dh_d, dQKV_d (per pass)
-  float* inv;      // 2^-e of the fp16 splits of the Wo and Wqkv weight uses
+  // slot arrays (AMAX_SLOTS) of max |.|: dh, dQKV (per call), dh_d, dQKV_d (per pass), Wo, Wqkv
+  uint32_t* amax[6];
+  float* inv;  // 2^-e of the fp16 splits: dh_d (and dh + dh_d), dQKV_d (and dQKV + dQKV_d), Wo, Wqkv
 };
 
 AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
@@ -79,9 +81,13 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
     w.dOp[i] = c.take<u16>(Td);
     w.dOt[i] = c.take<u16>(bh * DH * Sp);
   }
-  for (float** p : {&w.dh_d, &w.dO_dt, &w.dO_dh, &w.dQ_d, &w.dK_d, &w.dV_d, &w.du1_d}) *p = c.take<float>(Td);
+  for (float** p : {&w.dh_d, &w.dO_dt, &w.dO_dh, &w.du1_d}) *p = c.take<float>(Td);
+  w.dQ_d = c.take<float>(3 * Td);  // dQ, dK, dV of the move, one block (one max over the three)
+  w.dK_d = w.dQ_d ? w.dQ_d + Td : nullptr;
+  w.dV_d = w.dQ_d ? w.dQ_d + 2 * Td : nullptr;
   w.dD = c.take<float>(bh * S);
-  w.dqkv_d = c.take<float>(3 * Td);
+  w.Wo16 = c.take<u16>((int64_t)d * d);
+  w.Wqkv16 = c.take<u16>((int64_t)d * d3);
   w.gpart = c.take<double>(3 * ((T + 15) / 16) * (int64_t)d);
   for (int i = 0; i < NCOMP; ++i) {
     w.delta[i] = c.take<float>(nc[i]);
@@ -103,10 +109,10 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
   w.sumsq_part = c.take<double>(sumsq_part_size());
   w.diag = c.take<bs_diag>(1);
   {
-    uint32_t* a = c.take<uint32_t>(4 * AMAX_SLOTS * AMAX_STRIDE);
-    for (int i = 0; i < 4; ++i) w.amax[i] = a + i * AMAX_SLOTS * AMAX_STRIDE;
+    uint32_t* a = c.take<uint32_t>(6 * AMAX_SLOTS * AMAX_STRIDE);
+    for (int i = 0; i < 6; ++i) w.amax[i] = a ? a + i * AMAX_SLOTS * AMAX_STRIDE : nullptr;
   }
-  w.inv = c.take<float>(2);
+  w.inv = c.take<float>(4);
   return w;
 }
 
@@ -200,9 +206,13 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   BS_TRY(planes_of(NP_VAL, w.u1, io.c_u1, s_u1, &w.valT_u1, 1));
   BS_TRY(planes_of(NP_VAL, io.Otok, io.c_Otok, s_O, &w.valT_O, 1));
   pa.f16 = 0;
-  BS_TRY(launch_fill2d((float*)w.amax[0], 2 * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
+  BS_TRY(launch_fill2d((float*)w.amax[0], 6 * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
   BS_TRY(launch_amax_f32(io.dh, Td, w.amax[0], st));
   BS_TRY(launch_amax_f32(io.dqkv, 3 * Td, w.amax[1], st));
+  BS_TRY(launch_amax_bf16(io.Wo, (int64_t)d * d, w.amax[4], st));
+  BS_TRY(launch_amax_bf16(io.Wqkv, (int64_t)d * d3, w.amax[5], st));
+  BS_TRY(launch_scale_f16(io.Wo, (int64_t)d * d, w.amax[4], w.Wo16, w.inv + 2, st));
+  BS_TRY(launch_scale_f16(io.Wqkv, (int64_t)d * d3, w.amax[5], w.Wqkv16, w.inv + 3, st));
   BS_TRY(launch_planes(io.dqkv, BS_F32, T, d3, d3, true, w.dqkvT, 3, Tp, 1.0f, st));
   BS_TRY(launch_planes(io.dh, BS_F32, T, d, d, true, w.dhT, 3, Tp, 1.0f, st));
 
@@ -230,14 +240,17 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         BS_TRY(planes_of(NP_RESU, io.Otok, io.c_Otok, s_O, w.pA, 3));
         BS_TRY(Gemm(d, d, (int)Tp, Tp, Tp, dWo, d, nullptr).add(w.pA, 3, w.dhT, 3).run(w.part, w.part_cap, st));
       } else {
-        // dh_d's transposed planes (the weight use) and row planes (the move of dO), one read
-        BS_TRY(launch_planes_t2(w.dh_d, nullptr, T, d, d, w.tB, 2, Tp, w.rows3, d, st, sc_o));
+        // dh_d's transposed planes (the weight use), under N those of dh_L = dh + dh_d, and its
+        // row planes (the move of dO), one read
+        MoveSrc mo{};
+        mo.rows = w.dh_d;
+        mo.ldi = d;
+        BS_TRY(launch_split_move(mo, l == LETTER_N ? io.dh : nullptr, d, T, d, sc_o, w.tB, w.tA, Tp, w.rows3, d, st));
         Gemm gw(d, d, (int)Tp, Tp, Tp, dWo, d, s_O);
         gw.g.f16 = 1;
         gw.g.alpha_dev2 = w.inv + 0;
         gw.add(&w.valT_O, 1, w.tB, 2);
         if (l == LETTER_N) {
-          BS_TRY(launch_planes_t2(io.dh, w.dh_d, T, d, d, w.tA, 2, Tp, nullptr, 0, st, sc_o));  // dh_L = dh + dh_d
           TrialPlaneArgs ta{io.Otok, io.c_Otok, s_O, f, T, d, Tp, io.seed, 1 * 256 + 2, k, 1, w.pA[0]};
           ta.f16 = 1;
           BS_TRY(launch_trial_planes(ta, st));
@@ -245,7 +258,10 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         }
         BS_TRY(gw.run(w.part, w.part_cap, st));
         // the move of dO (token-major, then head-major)
-        BS_TRY(Gemm((int)T, d, d, d, d, w.dO_dt, d, nullptr).add(w.rows3, 3, &io.Wo, 1).run(nullptr, 0, st));
+        Gemm gm((int)T, d, d, d, d, w.dO_dt, d, w.inv + 2);
+        gm.g.f16 = 1;
+        gm.g.alpha_dev2 = w.inv + 0;
+        BS_TRY(gm.add(w.rows3, 2, &w.Wo16, 1).run(nullptr, 0, st));
         BS_TRY(launch_heads_tokens_f32(w.dO_dt, w.dO_dh, B, S, H, DH, false, st));
       }
       // the D use: U reads the original and dO does not move: no move downstream of it
@@ -283,15 +299,23 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         ba.dV = w.dV_d;
         ba.n_pol = 0;
         BS_TRY(launch_attn_bwd(ba, B, H, st));
-        BS_TRY(launch_dqkv_tokens(w.dQ_d, w.dK_d, w.dV_d, w.dqkv_d, B, S, H, DH, st, w.amax[3]));
-        // u1's weight use (Wqkv)
-        BS_TRY(launch_planes_t2(w.dqkv_d, nullptr, T, d3, d3, w.tB, 2, Tp, w.rows3, d3, st, sc_q));
+        // u1's weight use (Wqkv): the move of dQKV read head-major ([T][3d] token-major view),
+        // under N with dQKV + dQKV_d, and its row planes (the move of du1)
+        BS_TRY(launch_amax_f32(w.dQ_d, 3 * Td, w.amax[3], st));
+        MoveSrc mq{};
+        mq.heads[0] = w.dQ_d;
+        mq.heads[1] = w.dK_d;
+        mq.heads[2] = w.dV_d;
+        mq.S = S;
+        mq.H = H;
+        mq.d = d;
+        BS_TRY(launch_split_move(mq, l == LETTER_N ? io.dqkv : nullptr, d3, T, d3, sc_q, w.tB, w.tA, Tp, w.rows3, d3,
+                                 st));
         Gemm gq(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, s_u1);
         gq.g.f16 = 1;
         gq.g.alpha_dev2 = w.inv + 1;
         gq.add(&w.valT_u1, 1, w.tB, 2);
         if (l == LETTER_N) {
-          BS_TRY(launch_planes_t2(io.dqkv, w.dqkv_d, T, d3, d3, w.tA, 2, Tp, nullptr, 0, st, sc_q));  // dqkv + dqkv_d
           TrialPlaneArgs ta{w.u1, io.c_u1, s_u1, f, T, d, Tp, io.seed, 0 * 256 + 2, k, 1, w.pA[0]};
           ta.f16 = 1;
           BS_TRY(launch_trial_planes(ta, st));
@@ -299,7 +323,10 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         }
         BS_TRY(gq.run(w.part, w.part_cap, st));
         // the move of du1, then u1's gain and normalization-input uses
-        BS_TRY(Gemm((int)T, d, (int)d3, d3, d3, w.du1_d, d, nullptr).add(w.rows3, 3, &io.Wqkv, 1).run(nullptr, 0, st));
+        Gemm gu((int)T, d, (int)d3, d3, d3, w.du1_d, d, w.inv + 3);
+        gu.g.f16 = 1;
+        gu.g.alpha_dev2 = w.inv + 1;
+        BS_TRY(gu.add(w.rows3, 2, &w.Wqkv16, 1).run(nullptr, 0, st));
         const AlluGainArgs<u16> ag{io.x, w.r1, io.gain1, rd(w.u1, io.c_u1, s_u1, 0 * 256 + 1), w.du1, w.du1_d, T, d,
                                    w.gpart};
         BS_TRY(launch_allu_gain(ag, st));
