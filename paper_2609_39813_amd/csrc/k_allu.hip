@@ -83,14 +83,22 @@ __global__ __launch_bounds__(256) void allu_gain_kernel(AlluGainArgs<XT> a) {
 }
 
 // one wave per row, 4 rows per block; columns in groups of 4 per lane
-template <typename XT>
+// NI > 0: the row's columns in NI chunks of 256 (d <= 256 NI), each lane keeping x, z_x and
+// gain ddu of the first pass in registers for the second (the letter's read, a Philox draw and
+// an fp64 division per element, is taken once); NI == 0: any d, the second pass reads and
+// computes again.
+template <typename XT, int NI>
 __device__ __forceinline__ float allu_dx_row(const AlluDxArgs<XT>& a, int64_t t, int lane) {
   const float s = a.rd.scale ? *a.rd.scale : 1.0f;
   const double rs = 1.0 / (double)s;
   const float r = a.rstd[t];
   const int64_t rowe = t * a.d;
+  constexpr int NK = NI > 0 ? NI : 1;
+  float xk[NK][4];
+  double zk[NK][4], gk[NK][4];
   double dref = 0.0, dl = 0.0;
-  for (int64_t j0 = 4 * (int64_t)lane; j0 < a.d; j0 += 256) {
+  // first pass: the two row sums (and, NI > 0, the kept values)
+  auto first = [&](int64_t j0, int it) {
     float x[4], u[4], du[4], ddu[4] = {0.f, 0.f, 0.f, 0.f}, g[4];
     load4(a.X, rowe + j0, x);
     load4(a.rd.x, rowe + j0, u);
@@ -105,38 +113,65 @@ __device__ __forceinline__ float allu_dx_row(const AlluDxArgs<XT>& a, int64_t t,
       const double zx = a.rd.letter == LETTER_U ? z : v[c] / (double)g[c];
       dref += (double)g[c] * (double)du[c] * z;
       dl += (double)g[c] * ((double)du[c] + (double)ddu[c]) * zx;
+      if constexpr (NI > 0) {
+        xk[it][c] = x[c];
+        zk[it][c] = zx;
+        gk[it][c] = (double)g[c] * (double)ddu[c];
+      }
     }
+  };
+  if constexpr (NI > 0) {
+#pragma unroll
+    for (int it = 0; it < NI; ++it)
+      if (4 * (int64_t)lane + 256 * it < a.d) first(4 * (int64_t)lane + 256 * it, it);
+  } else {
+    for (int64_t j0 = 4 * (int64_t)lane; j0 < a.d; j0 += 256) first(j0, 0);
   }
   dref = __shfl(wave_sum_f64(dref), 0, 64);  // the wave sum is valid in lane 0: broadcast it
   dl = __shfl(wave_sum_f64(dl), 0, 64);
   const double inv_d = 1.0 / (double)a.d;
   float mx = 0.0f;
-  for (int64_t j0 = 4 * (int64_t)lane; j0 < a.d; j0 += 256) {
-    float x[4], u[4], ddu[4] = {0.f, 0.f, 0.f, 0.f}, g[4], ad[4] = {0.f, 0.f, 0.f, 0.f};
-    load4(a.X, rowe + j0, x);
-    load4(a.rd.x, rowe + j0, u);
-    load4(a.gain, j0, g);
-    if (a.ddu) load4(a.ddu, rowe + j0, ddu);
+  // second pass: out = r (gain ddu - (z_x dl - z dref) / d) + add
+  auto second = [&](int64_t j0, const float (&x)[4], const double (&zx)[4], const double (&gd)[4]) {
+    float ad[4] = {0.f, 0.f, 0.f, 0.f};
     if (a.add) load4(a.add, rowe + j0, ad);
-    double v[4];
-    read4(a.rd, rowe + j0, u, rs, s, v);
     float o[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const double z = (double)(x[c] * r);
-      const double zx = a.rd.letter == LETTER_U ? z : v[c] / (double)g[c];
-      o[c] = (float)((double)r * ((double)g[c] * (double)ddu[c] - (zx * dl - z * dref) * inv_d) + (double)ad[c]);
+      o[c] = (float)((double)r * (gd[c] - (zx[c] * dl - z * dref) * inv_d) + (double)ad[c]);
       mx = fmaxf(mx, fabsf(o[c]));
     }
     *(float4*)(a.out + rowe + j0) = make_float4(o[0], o[1], o[2], o[3]);
+  };
+  if constexpr (NI > 0) {
+#pragma unroll
+    for (int it = 0; it < NI; ++it)
+      if (4 * (int64_t)lane + 256 * it < a.d) second(4 * (int64_t)lane + 256 * it, xk[it], zk[it], gk[it]);
+  } else {
+    for (int64_t j0 = 4 * (int64_t)lane; j0 < a.d; j0 += 256) {
+      float x[4], u[4], ddu[4] = {0.f, 0.f, 0.f, 0.f}, g[4];
+      load4(a.X, rowe + j0, x);
+      load4(a.rd.x, rowe + j0, u);
+      load4(a.gain, j0, g);
+      if (a.ddu) load4(a.ddu, rowe + j0, ddu);
+      double v[4], zx[4], gd[4];
+      read4(a.rd, rowe + j0, u, rs, s, v);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        zx[c] = a.rd.letter == LETTER_U ? (double)(x[c] * r) : v[c] / (double)g[c];
+        gd[c] = (double)g[c] * (double)ddu[c];
+      }
+      second(j0, x, zx, gd);
+    }
   }
   return mx;
 }
-template <typename XT>
+template <typename XT, int NI>
 __global__ __launch_bounds__(256) void allu_dx_kernel(AlluDxArgs<XT> a) {
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const float mx = t < a.T ? allu_dx_row(a, t, lane) : 0.0f;  // uniform per wave
+  const float mx = t < a.T ? allu_dx_row<XT, NI>(a, t, lane) : 0.0f;  // uniform per wave
   if (a.amax) block_amax_to_slot(mx, a.amax);
 }
 
@@ -198,7 +233,15 @@ template <typename XT>
 bs_status launch_allu_dx(const AlluDxArgs<XT>& a, hipStream_t st) {
   if (a.T <= 0 || a.d <= 0) return BS_OK;
   if (a.d & 3) return BS_ESHAPE;
-  allu_dx_kernel<XT><<<(unsigned)((a.T + 3) / 4), 256, 0, st>>>(a);
+  const unsigned grid = (unsigned)((a.T + 3) / 4);
+  if (a.d <= 256)
+    allu_dx_kernel<XT, 1><<<grid, 256, 0, st>>>(a);
+  else if (a.d <= 512)
+    allu_dx_kernel<XT, 2><<<grid, 256, 0, st>>>(a);
+  else if (a.d <= 1024)
+    allu_dx_kernel<XT, 4><<<grid, 256, 0, st>>>(a);
+  else
+    allu_dx_kernel<XT, 0><<<grid, 256, 0, st>>>(a);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

@@ -36,6 +36,7 @@ constexpr int DH = 64;
 constexpr float kAttnScale = 0.125f;  // 1 / sqrt(64)
 enum { G_DX = 0, G_DGAIN1, G_DWQKV, G_DWO, G_DGAIN2, G_DWG, G_DWU, G_DWD, NGRAD };
 constexpr int NCOMP = 4;  // gradients formed here per trial: dx, dgain1, dWqkv, dWo
+constexpr int NB = 4;     // N trials per update of the shifted sums (one read-modify-write per NB)
 
 struct AlluWs {
   float *u1, *u2, *r1, *r2, *du1, *du2, *m, *l;
@@ -44,7 +45,7 @@ struct AlluWs {
   float *dh_d, *dO_dt, *dO_dh, *dD, *dQ_d, *dK_d, *dV_d, *du1_d;
   u16 *Wo16, *Wqkv16;  // the weights as scaled fp16 (the moves' contractions)
   double* gpart;
-  float* delta[NCOMP];      // this pass's moves
+  float* delta[NCOMP];      // the passes' moves, [NB][n] (N's trial k in row (k - 1) % NB)
   float* bias[3][NCOMP];    // per letter
   float* se_n[NCOMP];       // N's se
   float *d1[NCOMP];
@@ -90,7 +91,7 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
   w.Wqkv16 = c.take<u16>((int64_t)d * d3);
   w.gpart = c.take<double>(3 * ((T + 15) / 16) * (int64_t)d);
   for (int i = 0; i < NCOMP; ++i) {
-    w.delta[i] = c.take<float>(nc[i]);
+    w.delta[i] = c.take<float>(NB * nc[i]);
     for (int l = 0; l < 3; ++l) w.bias[l][i] = c.take<float>(nc[i]);
     w.se_n[i] = c.take<float>(nc[i]);
     w.d1[i] = c.take<float>(nc[i]);
@@ -223,8 +224,11 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       const auto rd = [&](const float* x, const uint8_t* codes, const float* scale, uint32_t use) {
         return StoreRead{x, codes, scale, f, l, io.seed, (uint32_t)k, use};
       };
-      float* dWo = w.delta[3];
-      float* dWqkv = w.delta[2];
+      const int slot = l == LETTER_N ? (k - 1) % NB : 0;
+      float* dl[NCOMP];
+      for (int i = 0; i < NCOMP; ++i) dl[i] = w.delta[i] + slot * nc[i];
+      float* dWo = dl[3];
+      float* dWqkv = dl[2];
       // u2's normalization-input use: the move of dh (and its max |.|)
       if (l != LETTER_U) {
         BS_TRY(launch_fill2d((float*)w.amax[2], 2 * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
@@ -269,8 +273,8 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         BS_TRY(planes_of(NP_RESU, w.u1, io.c_u1, s_u1, w.pA, 3));
         BS_TRY(Gemm(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, nullptr).add(w.pA, 3, w.dqkvT, 3)
                    .run(w.part, w.part_cap, st));
-        BS_TRY(launch_fill(w.delta[0], Td, 0.0f, st));
-        BS_TRY(launch_fill(w.delta[1], d, 0.0f, st));
+        BS_TRY(launch_fill(dl[0], Td, 0.0f, st));
+        BS_TRY(launch_fill(dl[1], d, 0.0f, st));
       } else {
         const AlluDArgs ad{rd(io.O, io.c_O, s_O, 1 * 256 + 1), io.dOh, w.dO_dh, rows_h, w.dD};
         BS_TRY(launch_allu_d(ad, st));
@@ -330,17 +334,20 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         const AlluGainArgs<u16> ag{io.x, w.r1, io.gain1, rd(w.u1, io.c_u1, s_u1, 0 * 256 + 1), w.du1, w.du1_d, T, d,
                                    w.gpart};
         BS_TRY(launch_allu_gain(ag, st));
-        BS_TRY(launch_gain_final(w.gpart, (T + 15) / 16, d, w.delta[1], nullptr, nullptr, st));
+        BS_TRY(launch_gain_final(w.gpart, (T + 15) / 16, d, dl[1], nullptr, nullptr, st));
         const AlluDxArgs<u16> ax{io.x, w.r1, io.gain1, rd(w.u1, io.c_u1, s_u1, 0 * 256 + 3), w.du1, w.du1_d, w.dh_d,
-                                 T, d, w.delta[0]};
+                                 T, d, dl[0]};
         BS_TRY(launch_allu_dx(ax, st));
       }
-      // this pass's moves: the letter's bias (U, R) or one trial of N
+      // this pass's moves: the letter's bias (U, R), or N's trials k - slot .. k, in order, once
+      // NB of them (or the last) are in
       for (int i = 0; i < NCOMP; ++i) {
-        if (l == LETTER_N)
-          BS_TRY(launch_trial_accum(w.delta[i], 1, k, nc[i], w.d1[i], w.S1[i], w.S2[i], st));
-        else
-          BS_TRY(copy_f32(w.bias[l][i], w.delta[i], nc[i], st));
+        if (l == LETTER_N) {
+          if (slot == NB - 1 || k == ntr)
+            BS_TRY(launch_trial_accum(w.delta[i], slot + 1, k - slot, nc[i], w.d1[i], w.S1[i], w.S2[i], st));
+        } else {
+          BS_TRY(copy_f32(w.bias[l][i], dl[i], nc[i], st));
+        }
       }
     }
   }
