@@ -75,6 +75,11 @@ struct AttnBwdArgs {
   float* kmean[ATTN_MAX_POL];  // dK estimates
   float* kbias[ATTN_MAX_POL];
   int k_only = 0;              // 1: the key-major pass only (dK, dV and their estimates)
+  // fp16 operands of the incoming gradient (no policies, no dD): with V16 non-null, dOp[0..1] and
+  // dOt[0..1] hold the two-term fp16 split of dO 2^e (launch_attn_split_f16), V16 = fp16(V 2^f)
+  // [B*H][S][64], f16_inv = {2^-e, 2^-f} on the device
+  const u16* V16 = nullptr;
+  const float* f16_inv = nullptr;
 };
 
 bs_status launch_attn_fwd(const AttnArgs& a, int B, int H, hipStream_t st);
@@ -85,6 +90,10 @@ bs_status launch_attn_transpose(const u16* const* X, u16* const* Xt, int n, int 
 // the three bf16 planes of an fp32 incoming gradient [BH][S][64] and their transposes
 bs_status launch_attn_split(const float* dO32, int BH, int S, int Sp, u16* const* dOp, u16* const* dOt,
                             hipStream_t st);
+// the two fp16 planes (split2_f16) of dO32 2^e, e from the max in slots (an AMAX_SLOTS array,
+// f16_scale_exp), and their transposes; 2^-e to inv_out
+bs_status launch_attn_split_f16(const float* dO32, int BH, int S, int Sp, const uint32_t* slots, float* inv_out,
+                                u16* const* dOp, u16* const* dOt, hipStream_t st);
 bs_status launch_attn_bwd(const AttnBwdArgs& a, int B, int H, hipStream_t st);
 
 }  // namespace bsp

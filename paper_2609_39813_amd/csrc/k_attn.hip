@@ -271,8 +271,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
 // while the other half is in use. BIAS = 0: no policy reads R or N (no bias accumulators);
 // BIAS = 1 forms both bias terms (a missing dD_v reads as zero).
 // ------------------------------------------------------------------------------------
-template <int NDO, int BIAS>
+// H: the incoming gradient as the two-term fp16 split of dO 2^e (NDO = 2) and V as fp16(V 2^f);
+// dP comes back by 2^-e-f, and dV = P^T dO (P split at the scale 2^14, the products of the two
+// splits' terms of order above 2^-22 taken) by 2^-e-14
+template <int NDO, int BIAS, bool H>
 __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
+  static_assert(!H || (NDO == 2 && !BIAS), "fp16 operands: two terms, no dD");
   constexpr int NR = 1 + NDO;     // tiles per half
   constexpr int NL = 2 * NR;      // loads per wave and half (two 1-KB loads per tile)
   __shared__ __attribute__((aligned(1024))) u16 smR[NR][AT * AT];
@@ -288,13 +292,15 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
   const int k0 = kb * AT;
   const int64_t hb = (int64_t)bh * a.S * AT, tb = (int64_t)bh * AT * a.Sp, rb = (int64_t)bh * a.S;
   const int key = k0 + 16 * w + c16;
+  const float dps = H ? a.f16_inv[0] * a.f16_inv[1] : 1.0f, avs = H ? a.f16_inv[0] * 0x1p-14f : 1.0f;
   // this wave's keys as the second operand of S and dP (fixed over the loop)
   bf16x8 fk[2], fv[2];
+  const u16* const Vsrc = H ? a.V16 : a.V;
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     const int64_t e = hb + (int64_t)key * AT + 32 * s + 8 * g;
     const uint4 zk = key < a.S ? *(const uint4*)(a.K + e) : make_uint4(0, 0, 0, 0);
-    const uint4 zv = key < a.S ? *(const uint4*)(a.V + e) : make_uint4(0, 0, 0, 0);
+    const uint4 zv = key < a.S ? *(const uint4*)(Vsrc + e) : make_uint4(0, 0, 0, 0);
     fk[s] = __builtin_bit_cast(bf16x8, zk);
     fv[s] = __builtin_bit_cast(bf16x8, zv);
   }
@@ -385,8 +391,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
       for (int t = 0; t < 4; ++t) {
         sv[t] = mfma(*(const bf16x8*)(smR[0] + sw(16 * t + c16, 32 * s + 8 * g)), fk[s], sv[t]);
 #pragma unroll
-        for (int i = 0; i < NDO; ++i)
-          dp[t] = mfma(*(const bf16x8*)(smR[1 + i] + sw(16 * t + c16, 32 * s + 8 * g)), fv[s], dp[t]);
+        for (int i = 0; i < NDO; ++i) {
+          const bf16x8 fo = *(const bf16x8*)(smR[1 + i] + sw(16 * t + c16, 32 * s + 8 * g));
+          dp[t] = H ? mfma_h(fo, fv[s], dp[t]) : mfma(fo, fv[s], dp[t]);
+        }
       }
     }
     // every wave has read the row-major half: the next query block's tiles and rows go in
@@ -417,7 +425,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
       for (int r = 0; r < 4; ++r) {
         const int ql = 16 * t + 4 * g + r;
         p[t][r] = __builtin_amdgcn_exp2f(p[t][r]) * rows[1][ql];
-        ds[t][r] = p[t][r] * (dp[t][r] - rows[2][ql]);
+        ds[t][r] = p[t][r] * (dp[t][r] * dps - rows[2][ql]);
       }
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
@@ -428,7 +436,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
         vd[v] = ds[2 * s + (v >> 2)][v & 3];
       }
       bf16x8 tp[3], td[3], tr[3], tn[3];
-      pack3t(vp, tp);
+      if constexpr (H) {
+        float vs[8];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) vs[v] = vp[v] * 0x1p14f;
+        pack2h(vs, tp);
+      } else {
+        pack3t(vp, tp);
+      }
       pack3t(vd, td);
       if (BIAS) {
         // bias terms: P scaled per query by dD_v
@@ -454,8 +469,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
         for (int i = 0; i < NDO; ++i) {
           const bf16x8 fo = frag_t(smT[1 + i], 16 * n + c16, s, g);
 #pragma unroll
-          for (int j = 0; j < 3; ++j)
-            if (i + j <= 2) av[n] = mfma(tp[j], fo, av[n]);
+          for (int j = 0; j < (H ? 2 : 3); ++j) {
+            if (H && i + j <= 1) av[n] = mfma_h(tp[j], fo, av[n]);
+            if (!H && i + j <= 2) av[n] = mfma(tp[j], fo, av[n]);
+          }
         }
 #pragma unroll
         for (int j = 0; j < 3; ++j) ak[n] = mfma(td[j], fq, ak[n]);
@@ -486,7 +503,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
     for (int n = 0; n < 4; ++n) {
       const int64_t e = hb + (int64_t)kr * AT + 16 * n + c16;
       const float dk = c * ak[n][r];
-      a.dV[e] = av[n][r];
+      a.dV[e] = av[n][r] * avs;
       a.dK_ref[e] = dk;
       for (int pi = 0; pi < a.n_pol; ++pi) {
         const int kind = a.pol[pi];
@@ -506,8 +523,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
 // The key block's tiles (K, V, K^T) arrive by buffer loads straight into LDS, two stages as two
 // LDS variables (the loop is unrolled by two so that every access names one of them: loads into
 // one stage are then not awaited before reads of the other); one barrier per key block.
-template <int NDO>
+// G: G = P K is formed (the per-policy estimates need it; without policies only dQ is). H: fp16
+// operands of dO and V as in the key-major pass, dP brought back by 2^-e-f.
+template <int NDO, bool G, bool H>
 __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
+  static_assert(!H || (NDO == 2 && !G), "fp16 operands: two terms, no policies");
   __shared__ __attribute__((aligned(1024))) u16 sm0[3][AT * AT];  // K, V, K^T
   __shared__ __attribute__((aligned(1024))) u16 sm1[3][AT * AT];
   // heaviest (most key blocks) first: blocks are dispatched in index order
@@ -533,12 +553,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
   const float c2 = a.scale * kLog2e;
   const float ilq = qok ? 1.0f / a.l[rb + q] : 0.0f;
   const float dq_ref = qok ? a.D_ref[rb + q] : 0.0f;
+  const float dps = H ? a.f16_inv[0] * a.f16_inv[1] : 1.0f;
 
   // K and V end at row S (rows past it read as zero), K^T spans its Sp columns; lane l of load j
   // (two per wave and tile) fills tile row 8 (2 w + j) + l / 8 at chunk position l % 8, which
   // holds logical chunk (l % 8) ^ (l / 8) (the sw layout)
   const __amdgpu_buffer_rsrc_t rK = attn_rsrc(a.K + hb, (int64_t)a.S * AT * 2);
-  const __amdgpu_buffer_rsrc_t rV = attn_rsrc(a.V + hb, (int64_t)a.S * AT * 2);
+  const __amdgpu_buffer_rsrc_t rV = attn_rsrc((H ? a.V16 : a.V) + hb, (int64_t)a.S * AT * 2);
   const __amdgpu_buffer_rsrc_t rKt = attn_rsrc(a.Kt + tb, (int64_t)AT * a.Sp * 2);
   const int lr = lane >> 3, lch = (lane & 7) ^ lr;
   const uint32_t vR = (uint32_t)(lr * AT * 2 + lch * 16), vT = (uint32_t)(lr * a.Sp * 2 + lch * 16);
@@ -579,7 +600,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
         sv[t] = mfma(*(const bf16x8*)(tK + sw(16 * t + c16, 32 * s + 8 * g)), fq[s], sv[t]);
         const bf16x8 fvv = *(const bf16x8*)(tV + sw(16 * t + c16, 32 * s + 8 * g));
 #pragma unroll
-        for (int i = 0; i < NDO; ++i) dp[t] = mfma(fvv, fdo[i][s], dp[t]);
+        for (int i = 0; i < NDO; ++i) dp[t] = H ? mfma_h(fvv, fdo[i][s], dp[t]) : mfma(fvv, fdo[i][s], dp[t]);
       }
     }
     // masks only where the block crosses S or the causal diagonal (a uniform test)
@@ -603,7 +624,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         p[t][r] = __builtin_amdgcn_exp2f(p[t][r]) * ilq;
-        ds[t][r] = p[t][r] * (dp[t][r] - dq_ref);
+        ds[t][r] = p[t][r] * (dp[t][r] * dps - dq_ref);
       }
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
@@ -614,7 +635,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
         vd[v] = ds[2 * s + (v >> 2)][v & 3];
       }
       bf16x8 tp[3], td[3];
-      pack3t(vp, tp);
+      if (G) pack3t(vp, tp);
       pack3t(vd, td);
 #pragma unroll
       for (int n = 0; n < 4; ++n) {
@@ -622,7 +643,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
 #pragma unroll
         for (int j = 0; j < 3; ++j) {
           aq[n] = mfma(td[j], fk, aq[n]);
-          ag[n] = mfma(tp[j], fk, ag[n]);
+          if (G) ag[n] = mfma(tp[j], fk, ag[n]);
         }
       }
     }
@@ -646,7 +667,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
       const float dq = c * aq[n][r];
       const float gg = ag[n][r];
       a.dQ_ref[e] = dq;
-      for (int pi = 0; pi < a.n_pol; ++pi) {
+      for (int pi = 0; G && pi < a.n_pol; ++pi) {
         const int kind = a.pol[pi];
         const float bias = kind == BS_READ_U ? 0.0f : -c * (kind == BS_READ_R ? ddr : ddn) * gg;
         if (a.mean[pi]) a.mean[pi][e] = dq + bias;
@@ -662,13 +683,22 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
 // tperm) of bf16 X [BH][S][64]; for an fp32 X, its three bf16 planes (row-major) and their
 // transposes
 // ------------------------------------------------------------------------------------
-template <typename X>
-__global__ __launch_bounds__(256) void attn_prep_kernel(const X* __restrict__ x, int S, int Sp, u16* __restrict__ xt0,
+// H (fp32 x): the two fp16 terms (split2_f16) of x 2^e, e from the max in slots, 2^-e to inv_out
+template <typename X, bool H>
+__global__ __launch_bounds__(256) void attn_prep_kernel(const X* __restrict__ x, int S, int Sp,
+                                                        const uint32_t* __restrict__ slots, float* __restrict__ inv_out,
+                                                        u16* __restrict__ xt0,
                                                         u16* __restrict__ xt1, u16* __restrict__ xt2,
                                                         u16* __restrict__ xp0, u16* __restrict__ xp1,
                                                         u16* __restrict__ xp2) {
-  constexpr int NP = sizeof(X) == 4 ? 3 : 1;
+  constexpr int NP = sizeof(X) == 4 ? (H ? 2 : 3) : 1;
   __shared__ u16 t[NP][AT][AT + 2];
+  float scl = 1.0f;
+  if constexpr (H) {
+    const int e = f16_scale_exp(amax_of_slots(slots));
+    scl = ldexpf(1.0f, e);
+    if (inv_out && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *inv_out = ldexpf(1.0f, -e);
+  }
   const int r0 = blockIdx.x * AT, bh = blockIdx.y;
   const int64_t hb = (int64_t)bh * S * AT, tb = (int64_t)bh * AT * Sp;
   u16* const xp[3] = {xp0, xp1, xp2};
@@ -681,7 +711,10 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(const X* __restrict__ x,
     } else {
       const float v = ok ? load_f32(x, hb + (int64_t)(r0 + r) * AT + c) : 0.0f;
       u16 h[3];
-      split3(v, h[0], h[1], h[2]);
+      if constexpr (H)
+        split2_f16(v * scl, h[0], h[1]);
+      else
+        split3(v, h[0], h[1], h[2]);
 #pragma unroll
       for (int p = 0; p < NP; ++p) {
         t[p][r][c] = h[p];
@@ -955,7 +988,18 @@ bs_status launch_attn_split(const float* dO32, int BH, int S, int Sp, u16* const
                             hipStream_t st) {
   dim3 grid((unsigned)(Sp / AT), (unsigned)BH);
   ProfScope prof("attn_prep", st);
-  attn_prep_kernel<float><<<grid, 256, 0, st>>>(dO32, S, Sp, dOt[0], dOt[1], dOt[2], dOp[0], dOp[1], dOp[2]);
+  attn_prep_kernel<float, false><<<grid, 256, 0, st>>>(dO32, S, Sp, nullptr, nullptr, dOt[0], dOt[1], dOt[2], dOp[0],
+                                                       dOp[1], dOp[2]);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+bs_status launch_attn_split_f16(const float* dO32, int BH, int S, int Sp, const uint32_t* slots, float* inv_out,
+                                u16* const* dOp, u16* const* dOt, hipStream_t st) {
+  if (!slots || !dO32) return BS_EINVAL;
+  dim3 grid((unsigned)(Sp / AT), (unsigned)BH);
+  ProfScope prof("attn_prep", st);
+  attn_prep_kernel<float, true><<<grid, 256, 0, st>>>(dO32, S, Sp, slots, inv_out, dOt[0], dOt[1], nullptr, dOp[0],
+                                                      dOp[1], nullptr);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
@@ -963,18 +1007,29 @@ bs_status launch_attn_split(const float* dO32, int BH, int S, int Sp, u16* const
 bs_status launch_attn_bwd(const AttnBwdArgs& a, int B, int H, hipStream_t st) {
   dim3 grid((unsigned)(B * H), (unsigned)((a.S + AT - 1) / AT));
   ProfScope prof("attn_bwd", st);
-  if (a.dO32) {
+  if (a.V16) {
+    if (a.dD_R || a.dD_N || a.n_pol > 0 || !a.f16_inv || !a.dOp[0] || !a.dOp[1] || !a.dOt[0] || !a.dOt[1])
+      return BS_EINVAL;
+    attn_bwd_k_kernel<2, 0, true><<<grid, 256, 0, st>>>(a);
+    if (!a.k_only) attn_bwd_q_kernel<2, false, true><<<grid, 256, 0, st>>>(a);
+  } else if (a.dO32) {
     if (a.dD_R || a.dD_N)
-      attn_bwd_k_kernel<3, 1><<<grid, 256, 0, st>>>(a);
+      attn_bwd_k_kernel<3, 1, false><<<grid, 256, 0, st>>>(a);
     else
-      attn_bwd_k_kernel<3, 0><<<grid, 256, 0, st>>>(a);
-    if (!a.k_only) attn_bwd_q_kernel<3><<<grid, 256, 0, st>>>(a);
+      attn_bwd_k_kernel<3, 0, false><<<grid, 256, 0, st>>>(a);
+    if (!a.k_only && a.n_pol > 0)
+      attn_bwd_q_kernel<3, true, false><<<grid, 256, 0, st>>>(a);
+    else if (!a.k_only)
+      attn_bwd_q_kernel<3, false, false><<<grid, 256, 0, st>>>(a);
   } else {
     if (a.dD_R || a.dD_N)
-      attn_bwd_k_kernel<1, 1><<<grid, 256, 0, st>>>(a);
+      attn_bwd_k_kernel<1, 1, false><<<grid, 256, 0, st>>>(a);
     else
-      attn_bwd_k_kernel<1, 0><<<grid, 256, 0, st>>>(a);
-    if (!a.k_only) attn_bwd_q_kernel<1><<<grid, 256, 0, st>>>(a);
+      attn_bwd_k_kernel<1, 0, false><<<grid, 256, 0, st>>>(a);
+    if (!a.k_only && a.n_pol > 0)
+      attn_bwd_q_kernel<1, true, false><<<grid, 256, 0, st>>>(a);
+    else if (!a.k_only)
+      attn_bwd_q_kernel<1, false, false><<<grid, 256, 0, st>>>(a);
   }
   BS_CHECK_LAUNCH();
   return BS_OK;

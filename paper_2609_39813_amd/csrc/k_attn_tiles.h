@@ -21,6 +21,11 @@ __device__ __forceinline__ int sw(int row, int col) { return row * AT + ((((col 
 __device__ __forceinline__ floatx4 mfma(bf16x8 a, bf16x8 b, floatx4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
+// the same product of operands that hold fp16 values
+__device__ __forceinline__ floatx4 mfma_h(bf16x8 a, bf16x8 b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(halfx8, a), __builtin_bit_cast(halfx8, b), c, 0, 0,
+                                                0);
+}
 
 // P = 2^(c log2(e) S - m) / l with m the row max of c log2(e) S: one hardware exp2 per
 // element (a few ulps; the exponent's rounding adds |m| 2^-24, below 1e-6 for these scores)
@@ -82,6 +87,21 @@ __device__ __forceinline__ void pack3t(const float* v, bf16x8* t) {
   }
 #pragma unroll
   for (int p = 0; p < 3; ++p) t[p] = __builtin_bit_cast(bf16x8, make_uint4(w[p][0], w[p][1], w[p][2], w[p][3]));
+}
+
+// The two-term fp16 split (bsp_common.h split2_f16) of eight fp32 values below 2^15 in magnitude.
+__device__ __forceinline__ void pack2h(const float* v, bf16x8* t) {
+  uint32_t w[2][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    u16 ha, la, hb, lb;
+    split2_f16(v[2 * i], ha, la);
+    split2_f16(v[2 * i + 1], hb, lb);
+    w[0][i] = (uint32_t)ha | ((uint32_t)hb << 16);
+    w[1][i] = (uint32_t)la | ((uint32_t)lb << 16);
+  }
+#pragma unroll
+  for (int p = 0; p < 2; ++p) t[p] = __builtin_bit_cast(bf16x8, make_uint4(w[p][0], w[p][1], w[p][2], w[p][3]));
 }
 
 // buffer resource over n_bytes from base: loads past the end read as zero

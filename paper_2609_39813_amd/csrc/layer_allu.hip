@@ -37,13 +37,19 @@ constexpr float kAttnScale = 0.125f;  // 1 / sqrt(64)
 enum { G_DX = 0, G_DGAIN1, G_DWQKV, G_DWO, G_DGAIN2, G_DWG, G_DWU, G_DWD, NGRAD };
 constexpr int NCOMP = 4;  // gradients formed here per trial: dx, dgain1, dWqkv, dWo
 constexpr int NB = 4;     // N trials per update of the shifted sums (one read-modify-write per NB)
+// maxima (slot arrays) of the scaled fp16 operands: per call dh, dQKV, Wo, Wqkv, V; per pass the
+// moves dh_d, dQKV_d, dO_d
+enum { AM_DH, AM_DQKV, AM_WO, AM_WQKV, AM_V, AM_DHD, AM_DQKVD, AM_DOD, AM_N };
+// their 2^-e: the splits of dh_d (with dh + dh_d), dQKV_d (with dQKV + dQKV_d), Wo, Wqkv, dO_d, V
+// (dO_d's and V's adjacent: the attention backward reads them as a pair)
+enum { IV_DHD, IV_DQKVD, IV_WO, IV_WQKV, IV_DOD, IV_V, IV_N };
 
 struct AlluWs {
   float *u1, *u2, *r1, *r2, *du1, *du2, *m, *l;
   u16 *Vt, *Qt, *Kt, *valT_u1, *valT_O, *dqkvT[3], *dhT[3];
   u16 *pA[3], *rows3[3], *tA[3], *tB[3], *dOp[3], *dOt[3];
   float *dh_d, *dO_dt, *dO_dh, *dD, *dQ_d, *dK_d, *dV_d, *du1_d;
-  u16 *Wo16, *Wqkv16;  // the weights as scaled fp16 (the moves' contractions)
+  u16 *Wo16, *Wqkv16, *V16;  // the weights and V as scaled fp16 (the moves' contractions)
   double* gpart;
   float* delta[NCOMP];      // the passes' moves, [NB][n] (N's trial k in row (k - 1) % NB)
   float* bias[3][NCOMP];    // per letter
@@ -55,9 +61,8 @@ struct AlluWs {
   int64_t part_cap;
   double* sumsq_part;
   bs_diag* diag;
-  // slot arrays (AMAX_SLOTS) of max |.|: dh, dQKV (per call), dh_d, dQKV_d (per pass), Wo, Wqkv
-  uint32_t* amax[6];
-  float* inv;  // 2^-e of the fp16 splits: dh_d (and dh + dh_d), dQKV_d (and dQKV + dQKV_d), Wo, Wqkv
+  uint32_t* amax[AM_N];  // slot arrays (AMAX_SLOTS) of max |.|
+  float* inv;            // [IV_N]
 };
 
 AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
@@ -89,6 +94,7 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
   w.dD = c.take<float>(bh * S);
   w.Wo16 = c.take<u16>((int64_t)d * d);
   w.Wqkv16 = c.take<u16>((int64_t)d * d3);
+  w.V16 = c.take<u16>(bh * S * DH);
   w.gpart = c.take<double>(3 * ((T + 15) / 16) * (int64_t)d);
   for (int i = 0; i < NCOMP; ++i) {
     w.delta[i] = c.take<float>(NB * nc[i]);
@@ -110,10 +116,10 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
   w.sumsq_part = c.take<double>(sumsq_part_size());
   w.diag = c.take<bs_diag>(1);
   {
-    uint32_t* a = c.take<uint32_t>(6 * AMAX_SLOTS * AMAX_STRIDE);
-    for (int i = 0; i < 6; ++i) w.amax[i] = a ? a + i * AMAX_SLOTS * AMAX_STRIDE : nullptr;
+    uint32_t* a = c.take<uint32_t>(AM_N * AMAX_SLOTS * AMAX_STRIDE);
+    for (int i = 0; i < AM_N; ++i) w.amax[i] = a ? a + i * AMAX_SLOTS * AMAX_STRIDE : nullptr;
   }
-  w.inv = c.take<float>(4);
+  w.inv = c.take<float>(IV_N);
   return w;
 }
 
@@ -207,13 +213,15 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   BS_TRY(planes_of(NP_VAL, w.u1, io.c_u1, s_u1, &w.valT_u1, 1));
   BS_TRY(planes_of(NP_VAL, io.Otok, io.c_Otok, s_O, &w.valT_O, 1));
   pa.f16 = 0;
-  BS_TRY(launch_fill2d((float*)w.amax[0], 6 * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
-  BS_TRY(launch_amax_f32(io.dh, Td, w.amax[0], st));
-  BS_TRY(launch_amax_f32(io.dqkv, 3 * Td, w.amax[1], st));
-  BS_TRY(launch_amax_bf16(io.Wo, (int64_t)d * d, w.amax[4], st));
-  BS_TRY(launch_amax_bf16(io.Wqkv, (int64_t)d * d3, w.amax[5], st));
-  BS_TRY(launch_scale_f16(io.Wo, (int64_t)d * d, w.amax[4], w.Wo16, w.inv + 2, st));
-  BS_TRY(launch_scale_f16(io.Wqkv, (int64_t)d * d3, w.amax[5], w.Wqkv16, w.inv + 3, st));
+  BS_TRY(launch_fill2d((float*)w.amax[0], AM_N * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
+  BS_TRY(launch_amax_f32(io.dh, Td, w.amax[AM_DH], st));
+  BS_TRY(launch_amax_f32(io.dqkv, 3 * Td, w.amax[AM_DQKV], st));
+  BS_TRY(launch_amax_bf16(io.Wo, (int64_t)d * d, w.amax[AM_WO], st));
+  BS_TRY(launch_amax_bf16(io.Wqkv, (int64_t)d * d3, w.amax[AM_WQKV], st));
+  BS_TRY(launch_amax_bf16(io.V, bh * S * DH, w.amax[AM_V], st));
+  BS_TRY(launch_scale_f16(io.Wo, (int64_t)d * d, w.amax[AM_WO], w.Wo16, w.inv + IV_WO, st));
+  BS_TRY(launch_scale_f16(io.Wqkv, (int64_t)d * d3, w.amax[AM_WQKV], w.Wqkv16, w.inv + IV_WQKV, st));
+  BS_TRY(launch_scale_f16(io.V, bh * S * DH, w.amax[AM_V], w.V16, w.inv + IV_V, st));
   BS_TRY(launch_planes(io.dqkv, BS_F32, T, d3, d3, true, w.dqkvT, 3, Tp, 1.0f, st));
   BS_TRY(launch_planes(io.dh, BS_F32, T, d, d, true, w.dhT, 3, Tp, 1.0f, st));
 
@@ -231,14 +239,15 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       float* dWqkv = dl[2];
       // u2's normalization-input use: the move of dh (and its max |.|)
       if (l != LETTER_U) {
-        BS_TRY(launch_fill2d((float*)w.amax[2], 2 * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
+        BS_TRY(launch_fill2d((float*)w.amax[AM_DHD], (AM_N - AM_DHD) * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
         AlluDxArgs<float> ax{io.h, w.r2, io.gain2, rd(w.u2, io.c_u2, s_u2, 2 * 256 + 3), w.du2, nullptr,
                              nullptr, T, d, w.dh_d};
-        ax.amax = w.amax[2];
+        ax.amax = w.amax[AM_DHD];
         BS_TRY(launch_allu_dx(ax, st));
       }
       // one scale for dh_d and dh + dh_d (the contraction has one multiplier)
-      const F16Scale sc_o{w.amax[2], w.amax[0], w.inv + 0}, sc_q{w.amax[3], w.amax[1], w.inv + 1};
+      const F16Scale sc_o{w.amax[AM_DHD], w.amax[AM_DH], w.inv + IV_DHD};
+      const F16Scale sc_q{w.amax[AM_DQKVD], w.amax[AM_DQKV], w.inv + IV_DQKVD};
       // O's weight use (Wo)
       if (l == LETTER_U) {
         BS_TRY(planes_of(NP_RESU, io.Otok, io.c_Otok, s_O, w.pA, 3));
@@ -252,7 +261,7 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         BS_TRY(launch_split_move(mo, l == LETTER_N ? io.dh : nullptr, d, T, d, sc_o, w.tB, w.tA, Tp, w.rows3, d, st));
         Gemm gw(d, d, (int)Tp, Tp, Tp, dWo, d, s_O);
         gw.g.f16 = 1;
-        gw.g.alpha_dev2 = w.inv + 0;
+        gw.g.alpha_dev2 = w.inv + IV_DHD;
         gw.add(&w.valT_O, 1, w.tB, 2);
         if (l == LETTER_N) {
           TrialPlaneArgs ta{io.Otok, io.c_Otok, s_O, f, T, d, Tp, io.seed, 1 * 256 + 2, k, 1, w.pA[0]};
@@ -262,9 +271,9 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         }
         BS_TRY(gw.run(w.part, w.part_cap, st));
         // the move of dO (token-major, then head-major)
-        Gemm gm((int)T, d, d, d, d, w.dO_dt, d, w.inv + 2);
+        Gemm gm((int)T, d, d, d, d, w.dO_dt, d, w.inv + IV_WO);
         gm.g.f16 = 1;
-        gm.g.alpha_dev2 = w.inv + 0;
+        gm.g.alpha_dev2 = w.inv + IV_DHD;
         BS_TRY(gm.add(w.rows3, 2, &w.Wo16, 1).run(nullptr, 0, st));
         BS_TRY(launch_heads_tokens_f32(w.dO_dt, w.dO_dh, B, S, H, DH, false, st));
       }
@@ -278,7 +287,9 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       } else {
         const AlluDArgs ad{rd(io.O, io.c_O, s_O, 1 * 256 + 1), io.dOh, w.dO_dh, rows_h, w.dD};
         BS_TRY(launch_allu_d(ad, st));
-        BS_TRY(launch_attn_split(w.dO_dh, (int)bh, S, (int)Sp, w.dOp, w.dOt, st));
+        // dO_d as the scaled two-term fp16 split (V as scaled fp16) for the attention backward
+        BS_TRY(launch_amax_f32(w.dO_dh, Td, w.amax[AM_DOD], st));
+        BS_TRY(launch_attn_split_f16(w.dO_dh, (int)bh, S, (int)Sp, w.amax[AM_DOD], w.inv + IV_DOD, w.dOp, w.dOt, st));
         AttnBwdArgs ba{};
         ba.Qt = w.Qt;
         ba.Kt = w.Kt;
@@ -291,6 +302,8 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         ba.K = io.Kk;
         ba.V = io.V;
         ba.dO32 = w.dO_dh;
+        ba.V16 = w.V16;
+        ba.f16_inv = w.inv + IV_DOD;
         ba.m = w.m;
         ba.l = w.l;
         ba.D_ref = w.dD;
@@ -305,7 +318,7 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         BS_TRY(launch_attn_bwd(ba, B, H, st));
         // u1's weight use (Wqkv): the move of dQKV read head-major ([T][3d] token-major view),
         // under N with dQKV + dQKV_d, and its row planes (the move of du1)
-        BS_TRY(launch_amax_f32(w.dQ_d, 3 * Td, w.amax[3], st));
+        BS_TRY(launch_amax_f32(w.dQ_d, 3 * Td, w.amax[AM_DQKVD], st));
         MoveSrc mq{};
         mq.heads[0] = w.dQ_d;
         mq.heads[1] = w.dK_d;
@@ -317,7 +330,7 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
                                  st));
         Gemm gq(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, s_u1);
         gq.g.f16 = 1;
-        gq.g.alpha_dev2 = w.inv + 1;
+        gq.g.alpha_dev2 = w.inv + IV_DQKVD;
         gq.add(&w.valT_u1, 1, w.tB, 2);
         if (l == LETTER_N) {
           TrialPlaneArgs ta{w.u1, io.c_u1, s_u1, f, T, d, Tp, io.seed, 0 * 256 + 2, k, 1, w.pA[0]};
@@ -327,9 +340,9 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         }
         BS_TRY(gq.run(w.part, w.part_cap, st));
         // the move of du1, then u1's gain and normalization-input uses
-        Gemm gu((int)T, d, (int)d3, d3, d3, w.du1_d, d, w.inv + 3);
+        Gemm gu((int)T, d, (int)d3, d3, d3, w.du1_d, d, w.inv + IV_WQKV);
         gu.g.f16 = 1;
-        gu.g.alpha_dev2 = w.inv + 1;
+        gu.g.alpha_dev2 = w.inv + IV_DQKVD;
         BS_TRY(gu.add(w.rows3, 2, &w.Wqkv16, 1).run(nullptr, 0, st));
         const AlluGainArgs<u16> ag{io.x, w.r1, io.gain1, rd(w.u1, io.c_u1, s_u1, 0 * 256 + 1), w.du1, w.du1_d, T, d,
                                    w.gpart};
