@@ -200,9 +200,10 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
   }
   return v;
 }
-// A maximum raised by many blocks lives in AMAX_SLOTS words AMAX_STRIDE words apart (block b
-// raises slot b % AMAX_SLOTS): device-scope atomics on one word serialize, on words in different
-// memory channels they do not. Its value is the max over the slots.
+// A maximum raised by many blocks lives in AMAX_SLOTS words AMAX_STRIDE words apart (block b,
+// the linear index of a 1-D or 2-D grid, raises slot b % AMAX_SLOTS): device-scope atomics on
+// one word serialize, on words in different memory channels they do not. Its value is the max
+// over the slots.
 constexpr int AMAX_SLOTS = 32, AMAX_STRIDE = 64;
 // The block's max of v (float bits of non-negative values; all threads of the block call it)
 // raised into its slot of `slots` by one atomic.
@@ -214,8 +215,15 @@ __device__ __forceinline__ void block_amax_to_slot(float v, uint32_t* slots) {
   if (threadIdx.x == 0) {
     uint32_t b = 0;
     for (int w = 0; w < (int)((blockDim.x + BS_WAVE - 1) / BS_WAVE); ++w) b = b > red[w] ? b : red[w];
-    if (b) atomicMax(slots + (blockIdx.x % AMAX_SLOTS) * AMAX_STRIDE, b);
+    if (b) atomicMax(slots + ((blockIdx.x + gridDim.x * blockIdx.y) % AMAX_SLOTS) * AMAX_STRIDE, b);
   }
+}
+// The same, one atomic per wave and no LDS (every lane of the wave calls it): for kernels whose
+// direct-to-LDS loads the compiler tracks only while they own every LDS variable.
+__device__ __forceinline__ void wave_amax_to_slot(float v, uint32_t* slots) {
+  const uint32_t m = wave_max_u32(__float_as_uint(v));
+  if ((threadIdx.x & (BS_WAVE - 1)) == 0 && m)
+    atomicMax(slots + ((blockIdx.x + gridDim.x * blockIdx.y) % AMAX_SLOTS) * AMAX_STRIDE, m);
 }
 __device__ __forceinline__ float amax_of_slots(const uint32_t* slots) {
   uint32_t m = 0;

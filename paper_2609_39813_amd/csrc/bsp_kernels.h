@@ -21,6 +21,8 @@ struct GemmArgs {
                             // count once); 0: every segment is a product of its own
   int f16 = 0;              // 1: every operand holds fp16 values (the 2-term fp16 split), else bf16
   const float* alpha_dev2 = nullptr;  // nullable: a second device multiplier of alpha
+  uint32_t* amax = nullptr;  // nullable: slots (AMAX_SLOTS) raised to max |C| of the values written
+                             // (C's new values, accumulate = 0 only; the pipelined kernel only)
 };
 
 // alpha of a launch with its device multipliers

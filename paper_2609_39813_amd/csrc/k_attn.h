@@ -80,6 +80,7 @@ struct AttnBwdArgs {
   // [B*H][S][64], f16_inv = {2^-e, 2^-f} on the device
   const u16* V16 = nullptr;
   const float* f16_inv = nullptr;
+  uint32_t* amax = nullptr;  // nullable: slots (AMAX_SLOTS) raised to max |.| of dQ_ref, dK_ref, dV
 };
 
 bs_status launch_attn_fwd(const AttnArgs& a, int B, int H, hipStream_t st);

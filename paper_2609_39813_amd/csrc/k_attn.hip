@@ -495,6 +495,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
     if (qb + 1 < nqb) step(qb + 1, rows1, rows0);
   }
   const float c = a.scale;
+  float mx = 0.0f;
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int kr = k0 + 16 * w + 4 * g + r;
@@ -504,6 +505,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
       const int64_t e = hb + (int64_t)kr * AT + 16 * n + c16;
       const float dk = c * ak[n][r];
       a.dV[e] = av[n][r] * avs;
+      mx = fmaxf(mx, fmaxf(fabsf(dk), fabsf(av[n][r] * avs)));
       a.dK_ref[e] = dk;
       for (int pi = 0; pi < a.n_pol; ++pi) {
         const int kind = a.pol[pi];
@@ -513,6 +515,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
       }
     }
   }
+  if (a.amax) wave_amax_to_slot(mx, a.amax);
 }
 
 // ------------------------------------------------------------------------------------
@@ -654,6 +657,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
   }
   const float c = a.scale;
   const float rk = a.ntrial > 0 ? 1.0f / sqrtf((float)a.ntrial) : 0.0f;
+  float mx = 0.0f;
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int qr = q0 + 16 * w + 4 * g + r;
@@ -667,6 +671,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
       const float dq = c * aq[n][r];
       const float gg = ag[n][r];
       a.dQ_ref[e] = dq;
+      mx = fmaxf(mx, fabsf(dq));
       for (int pi = 0; G && pi < a.n_pol; ++pi) {
         const int kind = a.pol[pi];
         const float bias = kind == BS_READ_U ? 0.0f : -c * (kind == BS_READ_R ? ddr : ddn) * gg;
@@ -676,6 +681,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
       }
     }
   }
+  if (a.amax) wave_amax_to_slot(mx, a.amax);
 }
 
 // ------------------------------------------------------------------------------------

@@ -319,6 +319,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
   const int64_t ldo = g.part ? g.N : g.ldc;
   const float alpha = g.part ? 1.0f : gemm_alpha(g);
   const bool acc_in = !g.part && g.accumulate;
+  float mx = 0.0f;
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
 #pragma unroll
@@ -332,23 +333,28 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
           float* p = out + (int64_t)m * ldo + nn;
           const float v = alpha * acc[i][j][r];
           *p = acc_in ? *p + v : v;
+          mx = fmaxf(mx, fabsf(v));
         }
       }
     }
   }
+  if (g.amax && !g.part) wave_amax_to_slot(mx, g.amax);  // split partials: the split sum takes it
 }
 
 // C = alpha * sum_s part[s] (+ C), splits summed in order
 __global__ __launch_bounds__(256) void gemm_split_sum_kernel(GemmArgs g, int splits) {
   const int64_t mn = (int64_t)g.M * g.N;
   const float alpha = gemm_alpha(g);
+  float mx = 0.0f;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < mn; i += (int64_t)gridDim.x * blockDim.x) {
     float v = g.part[i];
     for (int s = 1; s < splits; ++s) v += g.part[(int64_t)s * mn + i];
     const int64_t m = i / g.N, nn = i - m * g.N;
     float* p = g.C + m * g.ldc + nn;
     *p = g.accumulate ? *p + alpha * v : alpha * v;
+    mx = fmaxf(mx, fabsf(alpha * v));
   }
+  if (g.amax) block_amax_to_slot(mx, g.amax);
 }
 
 template <int BM, int BN, int WGM, int WGN, bool F16>
@@ -407,6 +413,7 @@ bs_status launch_gemm(const GemmArgs& g, hipStream_t st) {
   if (g.M <= 0 || g.N <= 0) return BS_OK;
   if (g.nseg < 1 || g.nseg > GEMM_MAX_SEG) return BS_EINVAL;
   if ((g.K & 7) || (g.lda & 7) || (g.ldb & 7) || g.lda < g.K || g.ldb < g.K) return BS_ESHAPE;
+  if (g.amax && g.accumulate) return BS_EINVAL;
   if (g.K == 0) return g.accumulate ? BS_OK : launch_fill2d(g.C, g.M, g.N, g.ldc, 0.0f, st);
   // pipelined kernel for 64-aligned K and 16-byte aligned operands
   // (buffer offsets of one 256-row tile fit in 31 bits)
@@ -415,7 +422,7 @@ bs_status launch_gemm(const GemmArgs& g, hipStream_t st) {
   const bool big_tiles = (int64_t)g.M * g.N >= (int64_t)256 * 256 * 16;
   if (lds_ok && g.f16)
     return big_tiles ? launch_gemm_lds<256, 256, 2, 4, true>(g, st) : launch_gemm_lds<128, 128, 2, 2, true>(g, st);
-  if (g.f16) return BS_EINVAL;  // fp16 operands: the pipelined kernel only
+  if (g.f16 || g.amax) return BS_EINVAL;  // fp16 operands, maxima: the pipelined kernel only
   if (lds_ok)
     return big_tiles ? launch_gemm_lds<256, 256, 2, 4, false>(g, st) : launch_gemm_lds<128, 128, 2, 2, false>(g, st);
   // 256 x 256 tiles once they still give every CU a tile; 128 x 128 below that

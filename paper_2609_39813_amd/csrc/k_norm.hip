@@ -409,11 +409,27 @@ __global__ __launch_bounds__(256) void gain_final_kernel(const double* __restric
   const int64_t j = (int64_t)blockIdx.x * 16 + c;
   const int64_t per = (nrt + 15) / 16;
   const int64_t r0 = sgi * per, r1 = (r0 + per) < nrt ? (r0 + per) : nrt;
+  // only the arrays asked for are read; eight rows' loads in flight ahead of their (ordered) adds
+  const int na = bias_n ? 3 : (bias_r ? 2 : 1);
   double q[3] = {0.0, 0.0, 0.0};
-  if (j < d)
-    for (int64_t rt = r0; rt < r1; ++rt)
+  if (j < d) {
+    int64_t rt = r0;
+    for (; rt + 8 <= r1; rt += 8) {
+      double v[3][8];
 #pragma unroll
-      for (int i = 0; i < 3; ++i) q[i] += part[(i * nrt + rt) * d + j];
+      for (int i = 0; i < 3; ++i)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[i][u] = i < na ? part[(i * nrt + rt + u) * d + j] : 0.0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int i = 0; i < 3; ++i) q[i] += v[i][u];
+    }
+    for (; rt < r1; ++rt)
+#pragma unroll
+      for (int i = 0; i < 3; ++i)
+        if (i < na) q[i] += part[(i * nrt + rt) * d + j];
+  }
 #pragma unroll
   for (int i = 0; i < 3; ++i) red[i][sgi][c] = q[i];
   __syncthreads();

@@ -274,6 +274,7 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         Gemm gm((int)T, d, d, d, d, w.dO_dt, d, w.inv + IV_WO);
         gm.g.f16 = 1;
         gm.g.alpha_dev2 = w.inv + IV_DHD;
+        gm.g.amax = w.amax[AM_DOD];
         BS_TRY(gm.add(w.rows3, 2, &w.Wo16, 1).run(nullptr, 0, st));
         BS_TRY(launch_heads_tokens_f32(w.dO_dt, w.dO_dh, B, S, H, DH, false, st));
       }
@@ -288,7 +289,6 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         const AlluDArgs ad{rd(io.O, io.c_O, s_O, 1 * 256 + 1), io.dOh, w.dO_dh, rows_h, w.dD};
         BS_TRY(launch_allu_d(ad, st));
         // dO_d as the scaled two-term fp16 split (V as scaled fp16) for the attention backward
-        BS_TRY(launch_amax_f32(w.dO_dh, Td, w.amax[AM_DOD], st));
         BS_TRY(launch_attn_split_f16(w.dO_dh, (int)bh, S, (int)Sp, w.amax[AM_DOD], w.inv + IV_DOD, w.dOp, w.dOt, st));
         AttnBwdArgs ba{};
         ba.Qt = w.Qt;
@@ -304,6 +304,7 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         ba.dO32 = w.dO_dh;
         ba.V16 = w.V16;
         ba.f16_inv = w.inv + IV_DOD;
+        ba.amax = w.amax[AM_DQKVD];  // the max of dQKV_d, for its split
         ba.m = w.m;
         ba.l = w.l;
         ba.D_ref = w.dD;
@@ -318,7 +319,6 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         BS_TRY(launch_attn_bwd(ba, B, H, st));
         // u1's weight use (Wqkv): the move of dQKV read head-major ([T][3d] token-major view),
         // under N with dQKV + dQKV_d, and its row planes (the move of du1)
-        BS_TRY(launch_amax_f32(w.dQ_d, 3 * Td, w.amax[AM_DQKVD], st));
         MoveSrc mq{};
         mq.heads[0] = w.dQ_d;
         mq.heads[1] = w.dK_d;
