@@ -66,6 +66,7 @@ struct AlluDArgs {
   const float* ddO;  // nullable [rows][64]
   int64_t rows;
   float* out;        // [rows]
+  uint32_t* amax = nullptr;  // nullable: slots (AMAX_SLOTS) raised to max |out|
 };
 bs_status launch_allu_d(const AlluDArgs& a, hipStream_t st);
 

@@ -197,6 +197,7 @@ __global__ __launch_bounds__(256) void allu_d_kernel(AlluDArgs a) {
 #pragma unroll
   for (int m = 1; m < 16; m <<= 1) acc += __shfl_xor(acc, m, 64);
   if (ok && sub == 0) a.out[row] = (float)acc;
+  if (a.amax) block_amax_to_slot(ok ? fabsf((float)acc) : 0.0f, a.amax);
 }
 
 __global__ __launch_bounds__(256) void trial_mean_kernel(const float* __restrict__ d1, const double* __restrict__ S1,

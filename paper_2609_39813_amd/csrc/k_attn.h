@@ -75,10 +75,13 @@ struct AttnBwdArgs {
   float* kmean[ATTN_MAX_POL];  // dK estimates
   float* kbias[ATTN_MAX_POL];
   int k_only = 0;              // 1: the key-major pass only (dK, dV and their estimates)
-  // fp16 operands of the incoming gradient (no policies, no dD): with V16 non-null, dOp[0..1] and
-  // dOt[0..1] hold the two-term fp16 split of dO 2^e (launch_attn_split_f16), V16 = fp16(V 2^f)
-  // [B*H][S][64], f16_inv = {2^-e, 2^-f} on the device
+  // fp16 operands (no policies, no dD): with V16 non-null, dOp[0..1] and dOt[0..1] hold the
+  // two-term fp16 split of dO 2^e (launch_attn_split_f16), V16 = fp16(V 2^f) [B*H][S][64], Qt16
+  // and Kt16 the transposed copies of fp16(Q 2^q) and fp16(K 2^k); dS enters as its two-term
+  // split at the scale 2^s of launch_attn_f16_scales. f16_inv (device) = {2^-e, 2^-f, 2^-q, 2^-k,
+  // 2^s, 2^-s-q, 2^-s-k}.
   const u16* V16 = nullptr;
+  const u16 *Qt16 = nullptr, *Kt16 = nullptr;
   const float* f16_inv = nullptr;
   uint32_t* amax = nullptr;  // nullable: slots (AMAX_SLOTS) raised to max |.| of dQ_ref, dK_ref, dV
 };
@@ -95,6 +98,11 @@ bs_status launch_attn_split(const float* dO32, int BH, int S, int Sp, u16* const
 // f16_scale_exp), and their transposes; 2^-e to inv_out
 bs_status launch_attn_split_f16(const float* dO32, int BH, int S, int Sp, const uint32_t* slots, float* inv_out,
                                 u16* const* dOp, u16* const* dOt, hipStream_t st);
+// dS's scale of the fp16 backward (f16_inv above, entries 4..6 from entries 2, 3): 2^s from the
+// bound 64 max|dO| max|V| + max|D| of |dS| = P |dP - D| (P <= 1, 64 terms per dP), the maxima
+// held in the slot arrays (AMAX_SLOTS) sdO, sV, sD
+bs_status launch_attn_f16_scales(const uint32_t* sdO, const uint32_t* sV, const uint32_t* sD, float* f16_inv,
+                                 hipStream_t st);
 bs_status launch_attn_bwd(const AttnBwdArgs& a, int B, int H, hipStream_t st);
 
 }  // namespace bsp

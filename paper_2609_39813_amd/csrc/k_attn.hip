@@ -273,7 +273,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
 // ------------------------------------------------------------------------------------
 // H: the incoming gradient as the two-term fp16 split of dO 2^e (NDO = 2) and V as fp16(V 2^f);
 // dP comes back by 2^-e-f, and dV = P^T dO (P split at the scale 2^14, the products of the two
-// splits' terms of order above 2^-22 taken) by 2^-e-14
+// splits' terms of order above 2^-22 taken) by 2^-e-14; dK = dS^T Q from the two-term split of
+// dS 2^s and fp16(Q 2^q), back by 2^-s-q
 template <int NDO, int BIAS, bool H>
 __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
   static_assert(!H || (NDO == 2 && !BIAS), "fp16 operands: two terms, no dD");
@@ -293,6 +294,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
   const int64_t hb = (int64_t)bh * a.S * AT, tb = (int64_t)bh * AT * a.Sp, rb = (int64_t)bh * a.S;
   const int key = k0 + 16 * w + c16;
   const float dps = H ? a.f16_inv[0] * a.f16_inv[1] : 1.0f, avs = H ? a.f16_inv[0] * 0x1p-14f : 1.0f;
+  const float dsc = H ? a.f16_inv[4] : 1.0f, dkm = H ? a.f16_inv[5] : 1.0f;
   // this wave's keys as the second operand of S and dP (fixed over the loop)
   bf16x8 fk[2], fv[2];
   const u16* const Vsrc = H ? a.V16 : a.V;
@@ -308,7 +310,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
   // resources: row-major tiles end at row S, transposed copies span their Sp columns
   __amdgpu_buffer_rsrc_t rR[NR], rT[NR];
   rR[0] = attn_rsrc(a.Q + hb, (int64_t)a.S * AT * 2);
-  rT[0] = attn_rsrc(a.Qt + tb, (int64_t)AT * a.Sp * 2);
+  rT[0] = attn_rsrc((H ? a.Qt16 : a.Qt) + tb, (int64_t)AT * a.Sp * 2);
 #pragma unroll
   for (int i = 0; i < NDO; ++i) {
     rR[1 + i] = attn_rsrc((NDO == 1 ? a.dO : a.dOp[i]) + hb, (int64_t)a.S * AT * 2);
@@ -437,14 +439,18 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
       }
       bf16x8 tp[3], td[3], tr[3], tn[3];
       if constexpr (H) {
-        float vs[8];
+        float vs[8], ws[8];
 #pragma unroll
-        for (int v = 0; v < 8; ++v) vs[v] = vp[v] * 0x1p14f;
+        for (int v = 0; v < 8; ++v) {
+          vs[v] = vp[v] * 0x1p14f;
+          ws[v] = vd[v] * dsc;
+        }
         pack2h(vs, tp);
+        pack2h(ws, td);
       } else {
         pack3t(vp, tp);
+        pack3t(vd, td);
       }
-      pack3t(vd, td);
       if (BIAS) {
         // bias terms: P scaled per query by dD_v
         float vr[8], vn[8];
@@ -474,8 +480,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
             if (!H && i + j <= 2) av[n] = mfma(tp[j], fo, av[n]);
           }
         }
+        if constexpr (H) {
 #pragma unroll
-        for (int j = 0; j < 3; ++j) ak[n] = mfma(td[j], fq, ak[n]);
+          for (int j = 0; j < 2; ++j) ak[n] = mfma_h(td[j], fq, ak[n]);
+        } else {
+#pragma unroll
+          for (int j = 0; j < 3; ++j) ak[n] = mfma(td[j], fq, ak[n]);
+        }
         if (BIAS) {
 #pragma unroll
           for (int j = 0; j < 3; ++j) {
@@ -503,7 +514,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
       const int64_t e = hb + (int64_t)kr * AT + 16 * n + c16;
-      const float dk = c * ak[n][r];
+      const float dk = c * (ak[n][r] * dkm);
       a.dV[e] = av[n][r] * avs;
       mx = fmaxf(mx, fmaxf(fabsf(dk), fabsf(av[n][r] * avs)));
       a.dK_ref[e] = dk;
@@ -527,7 +538,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
 // LDS variables (the loop is unrolled by two so that every access names one of them: loads into
 // one stage are then not awaited before reads of the other); one barrier per key block.
 // G: G = P K is formed (the per-policy estimates need it; without policies only dQ is). H: fp16
-// operands of dO and V as in the key-major pass, dP brought back by 2^-e-f.
+// operands of dO, V and dS as in the key-major pass, dP brought back by 2^-e-f, dQ = dS K (fp16(K
+// 2^k)) by 2^-s-k.
 template <int NDO, bool G, bool H>
 __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
   static_assert(!H || (NDO == 2 && !G), "fp16 operands: two terms, no policies");
@@ -557,13 +569,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
   const float ilq = qok ? 1.0f / a.l[rb + q] : 0.0f;
   const float dq_ref = qok ? a.D_ref[rb + q] : 0.0f;
   const float dps = H ? a.f16_inv[0] * a.f16_inv[1] : 1.0f;
+  const float dsc = H ? a.f16_inv[4] : 1.0f, dqm = H ? a.f16_inv[6] : 1.0f;
 
   // K and V end at row S (rows past it read as zero), K^T spans its Sp columns; lane l of load j
   // (two per wave and tile) fills tile row 8 (2 w + j) + l / 8 at chunk position l % 8, which
   // holds logical chunk (l % 8) ^ (l / 8) (the sw layout)
   const __amdgpu_buffer_rsrc_t rK = attn_rsrc(a.K + hb, (int64_t)a.S * AT * 2);
   const __amdgpu_buffer_rsrc_t rV = attn_rsrc((H ? a.V16 : a.V) + hb, (int64_t)a.S * AT * 2);
-  const __amdgpu_buffer_rsrc_t rKt = attn_rsrc(a.Kt + tb, (int64_t)AT * a.Sp * 2);
+  const __amdgpu_buffer_rsrc_t rKt = attn_rsrc((H ? a.Kt16 : a.Kt) + tb, (int64_t)AT * a.Sp * 2);
   const int lr = lane >> 3, lch = (lane & 7) ^ lr;
   const uint32_t vR = (uint32_t)(lr * AT * 2 + lch * 16), vT = (uint32_t)(lr * a.Sp * 2 + lch * 16);
   auto issue = [&](u16 (*sm)[AT * AT], int k0) {
@@ -639,14 +652,26 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
       }
       bf16x8 tp[3], td[3];
       if (G) pack3t(vp, tp);
-      pack3t(vd, td);
+      if constexpr (H) {
+        float ws[8];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) ws[v] = vd[v] * dsc;
+        pack2h(ws, td);
+      } else {
+        pack3t(vd, td);
+      }
 #pragma unroll
       for (int n = 0; n < 4; ++n) {
         const bf16x8 fk = frag_t(tKt, 16 * n + c16, s, g);
+        if constexpr (H) {
 #pragma unroll
-        for (int j = 0; j < 3; ++j) {
-          aq[n] = mfma(td[j], fk, aq[n]);
-          if (G) ag[n] = mfma(tp[j], fk, ag[n]);
+          for (int j = 0; j < 2; ++j) aq[n] = mfma_h(td[j], fk, aq[n]);
+        } else {
+#pragma unroll
+          for (int j = 0; j < 3; ++j) {
+            aq[n] = mfma(td[j], fk, aq[n]);
+            if (G) ag[n] = mfma(tp[j], fk, ag[n]);
+          }
         }
       }
     }
@@ -668,7 +693,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
       const int64_t e = hb + (int64_t)qr * AT + 16 * n + c16;
-      const float dq = c * aq[n][r];
+      const float dq = c * (aq[n][r] * dqm);
       const float gg = ag[n][r];
       a.dQ_ref[e] = dq;
       mx = fmaxf(mx, fabsf(dq));
@@ -999,6 +1024,21 @@ bs_status launch_attn_split(const float* dO32, int BH, int S, int Sp, u16* const
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
+__global__ void attn_f16_scales_kernel(const uint32_t* sdO, const uint32_t* sV, const uint32_t* sD, float* inv) {
+  if (threadIdx.x != 0) return;
+  const float bound = 64.0f * amax_of_slots(sdO) * amax_of_slots(sV) + amax_of_slots(sD);
+  const int e = f16_scale_exp(bound);
+  inv[4] = ldexpf(1.0f, e);
+  inv[5] = ldexpf(inv[2], -e);
+  inv[6] = ldexpf(inv[3], -e);
+}
+bs_status launch_attn_f16_scales(const uint32_t* sdO, const uint32_t* sV, const uint32_t* sD, float* f16_inv,
+                                 hipStream_t st) {
+  if (!sdO || !sV || !sD || !f16_inv) return BS_EINVAL;
+  attn_f16_scales_kernel<<<1, 64, 0, st>>>(sdO, sV, sD, f16_inv);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
 bs_status launch_attn_split_f16(const float* dO32, int BH, int S, int Sp, const uint32_t* slots, float* inv_out,
                                 u16* const* dOp, u16* const* dOt, hipStream_t st) {
   if (!slots || !dO32) return BS_EINVAL;
@@ -1014,7 +1054,8 @@ bs_status launch_attn_bwd(const AttnBwdArgs& a, int B, int H, hipStream_t st) {
   dim3 grid((unsigned)(B * H), (unsigned)((a.S + AT - 1) / AT));
   ProfScope prof("attn_bwd", st);
   if (a.V16) {
-    if (a.dD_R || a.dD_N || a.n_pol > 0 || !a.f16_inv || !a.dOp[0] || !a.dOp[1] || !a.dOt[0] || !a.dOt[1])
+    if (a.dD_R || a.dD_N || a.n_pol > 0 || !a.f16_inv || !a.Qt16 || !a.Kt16 || !a.dOp[0] || !a.dOp[1] || !a.dOt[0] ||
+        !a.dOt[1])
       return BS_EINVAL;
     attn_bwd_k_kernel<2, 0, true><<<grid, 256, 0, st>>>(a);
     if (!a.k_only) attn_bwd_q_kernel<2, false, true><<<grid, 256, 0, st>>>(a);

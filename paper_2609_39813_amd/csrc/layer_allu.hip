@@ -37,12 +37,12 @@ constexpr float kAttnScale = 0.125f;  // 1 / sqrt(64)
 enum { G_DX = 0, G_DGAIN1, G_DWQKV, G_DWO, G_DGAIN2, G_DWG, G_DWU, G_DWD, NGRAD };
 constexpr int NCOMP = 4;  // gradients formed here per trial: dx, dgain1, dWqkv, dWo
 constexpr int NB = 4;     // N trials per update of the shifted sums (one read-modify-write per NB)
-// maxima (slot arrays) of the scaled fp16 operands: per call dh, dQKV, Wo, Wqkv, V; per pass the
-// moves dh_d, dQKV_d, dO_d
-enum { AM_DH, AM_DQKV, AM_WO, AM_WQKV, AM_V, AM_DHD, AM_DQKVD, AM_DOD, AM_N };
-// their 2^-e: the splits of dh_d (with dh + dh_d), dQKV_d (with dQKV + dQKV_d), Wo, Wqkv, dO_d, V
-// (dO_d's and V's adjacent: the attention backward reads them as a pair)
-enum { IV_DHD, IV_DQKVD, IV_WO, IV_WQKV, IV_DOD, IV_V, IV_N };
+// maxima (slot arrays) of the scaled fp16 operands: per call dh, dQKV, Wo, Wqkv, V, Q, K; per pass
+// the moves dh_d, dQKV_d, dO_d, D_d
+enum { AM_DH, AM_DQKV, AM_WO, AM_WQKV, AM_V, AM_Q, AM_K, AM_DHD, AM_DQKVD, AM_DOD, AM_DDD, AM_N };
+// their 2^-e: the splits of dh_d (with dh + dh_d), dQKV_d (with dQKV + dQKV_d), Wo, Wqkv; then the
+// attention backward's seven in its order (dO_d, V, Q, K, dS's 2^s, 2^-s-q, 2^-s-k)
+enum { IV_DHD, IV_DQKVD, IV_WO, IV_WQKV, IV_DOD, IV_V, IV_Q, IV_K, IV_DS, IV_DKM, IV_DQM, IV_N };
 
 struct AlluWs {
   float *u1, *u2, *r1, *r2, *du1, *du2, *m, *l;
@@ -50,6 +50,7 @@ struct AlluWs {
   u16 *pA[3], *rows3[3], *tA[3], *tB[3], *dOp[3], *dOt[3];
   float *dh_d, *dO_dt, *dO_dh, *dD, *dQ_d, *dK_d, *dV_d, *du1_d;
   u16 *Wo16, *Wqkv16, *V16;  // the weights and V as scaled fp16 (the moves' contractions)
+  u16 *Q16, *K16, *Qt16, *Kt16;  // Q, K as scaled fp16 and their transposed copies
   double* gpart;
   float* delta[NCOMP];      // the passes' moves, [NB][n] (N's trial k in row (k - 1) % NB)
   float* bias[3][NCOMP];    // per letter
@@ -95,6 +96,10 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
   w.Wo16 = c.take<u16>((int64_t)d * d);
   w.Wqkv16 = c.take<u16>((int64_t)d * d3);
   w.V16 = c.take<u16>(bh * S * DH);
+  w.Q16 = c.take<u16>(bh * S * DH);
+  w.K16 = c.take<u16>(bh * S * DH);
+  w.Qt16 = c.take<u16>(bh * DH * Sp);
+  w.Kt16 = c.take<u16>(bh * DH * Sp);
   w.gpart = c.take<double>(3 * ((T + 15) / 16) * (int64_t)d);
   for (int i = 0; i < NCOMP; ++i) {
     w.delta[i] = c.take<float>(NB * nc[i]);
@@ -222,6 +227,15 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   BS_TRY(launch_scale_f16(io.Wo, (int64_t)d * d, w.amax[AM_WO], w.Wo16, w.inv + IV_WO, st));
   BS_TRY(launch_scale_f16(io.Wqkv, (int64_t)d * d3, w.amax[AM_WQKV], w.Wqkv16, w.inv + IV_WQKV, st));
   BS_TRY(launch_scale_f16(io.V, bh * S * DH, w.amax[AM_V], w.V16, w.inv + IV_V, st));
+  BS_TRY(launch_amax_bf16(io.Q, bh * S * DH, w.amax[AM_Q], st));
+  BS_TRY(launch_amax_bf16(io.Kk, bh * S * DH, w.amax[AM_K], st));
+  BS_TRY(launch_scale_f16(io.Q, bh * S * DH, w.amax[AM_Q], w.Q16, w.inv + IV_Q, st));
+  BS_TRY(launch_scale_f16(io.Kk, bh * S * DH, w.amax[AM_K], w.K16, w.inv + IV_K, st));
+  {
+    const u16* src[2] = {w.Q16, w.K16};
+    u16* dst[2] = {w.Qt16, w.Kt16};
+    BS_TRY(launch_attn_transpose(src, dst, 2, (int)bh, S, (int)Sp, st));
+  }
   BS_TRY(launch_planes(io.dqkv, BS_F32, T, d3, d3, true, w.dqkvT, 3, Tp, 1.0f, st));
   BS_TRY(launch_planes(io.dh, BS_F32, T, d, d, true, w.dhT, 3, Tp, 1.0f, st));
 
@@ -286,10 +300,12 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         BS_TRY(launch_fill(dl[0], Td, 0.0f, st));
         BS_TRY(launch_fill(dl[1], d, 0.0f, st));
       } else {
-        const AlluDArgs ad{rd(io.O, io.c_O, s_O, 1 * 256 + 1), io.dOh, w.dO_dh, rows_h, w.dD};
+        AlluDArgs ad{rd(io.O, io.c_O, s_O, 1 * 256 + 1), io.dOh, w.dO_dh, rows_h, w.dD};
+        ad.amax = w.amax[AM_DDD];
         BS_TRY(launch_allu_d(ad, st));
         // dO_d as the scaled two-term fp16 split (V as scaled fp16) for the attention backward
         BS_TRY(launch_attn_split_f16(w.dO_dh, (int)bh, S, (int)Sp, w.amax[AM_DOD], w.inv + IV_DOD, w.dOp, w.dOt, st));
+        BS_TRY(launch_attn_f16_scales(w.amax[AM_DOD], w.amax[AM_V], w.amax[AM_DDD], w.inv + IV_DOD, st));
         AttnBwdArgs ba{};
         ba.Qt = w.Qt;
         ba.Kt = w.Kt;
@@ -303,6 +319,8 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         ba.V = io.V;
         ba.dO32 = w.dO_dh;
         ba.V16 = w.V16;
+        ba.Qt16 = w.Qt16;
+        ba.Kt16 = w.Kt16;
         ba.f16_inv = w.inv + IV_DOD;
         ba.amax = w.amax[AM_DQKVD];  // the max of dQKV_d, for its split
         ba.m = w.m;
