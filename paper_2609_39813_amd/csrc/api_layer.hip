@@ -267,7 +267,7 @@ LayerWs carve_layer(Carver& c, int B, int S, int d, int H, int F, int K, bool al
   w.sub_bytes = sub_ws_size(B, S, d, H, F, K, se);
   w.sub = c.take<char>(w.sub_bytes);
   if (all_uses) {
-    w.allu_bytes = allu_ws_size(B, S, d, H, F);
+    w.allu_bytes = allu_ws_size(B, S, d, H, F, K);
     w.allu = c.take<char>(w.allu_bytes);
   }
   return w;

@@ -68,9 +68,11 @@ template <typename T>
 bs_status launch_dx_t(const DxArgs<T>& a, hipStream_t st);
 
 // Per-trial weight-use residual planes: for trials k0 .. k0 + nb - 1 (new roundings of u at
-// the store's scale, use id `use`), plane b [d][ldo] holds sign * (up_k - [C_u rounded up]) * step
-// (one exact bf16 term; zero for t >= T). ldo a multiple of 64, d of 4, out and u 16-byte and
-// codes 4-byte aligned (BS_EINVAL otherwise).
+// the store's scale, use id `use`), plane b [d][ldo] of out holds sign * (up_k - [C_u rounded
+// up]) * step (one exact bf16 term; zero for t >= T), and of outW the new rounding's value
+// val(C_u) + that step (the forward's value when they agree). Either output nullable. ldo a
+// multiple of 64, d of 4, the outputs and u 16-byte and codes 4-byte aligned (BS_EINVAL
+// otherwise).
 struct TrialPlaneArgs {
   const float* u;
   const uint8_t* codes;
@@ -81,7 +83,8 @@ struct TrialPlaneArgs {
   uint32_t use;
   int k0, nb;
   u16* out;  // [nb][d][ldo]
-  int f16 = 0;  // fp16 values (exact: powers of two on the FP8 grid) instead of bf16
+  int f16 = 0;  // fp16 values (exact: FP8 values and steps) instead of bf16
+  u16* outW = nullptr;  // [nb][d][ldo]
 };
 bs_status launch_trial_planes(const TrialPlaneArgs& a, hipStream_t st);
 // Shifted fp64 sums over trials of delta [nb][m] (trials k0 ..): trial 1 is stored as the shift

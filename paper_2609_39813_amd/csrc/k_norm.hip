@@ -272,11 +272,13 @@ __global__ __launch_bounds__(256) void norm_planes_t4_kernel(NormPlaneArgs a) {
 // plane [j][t], leaving it as 16-byte pieces (eight consecutive t per thread and piece).
 __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
   __shared__ __attribute__((aligned(16))) u16 tile[64][72];
+  __shared__ __attribute__((aligned(16))) u16 tileW[64][72];
   const int64_t t0 = (int64_t)blockIdx.y * 64, j0 = (int64_t)blockIdx.x * 64;
   const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;  // column group, row group
   const double rs = 1.0 / (double)*a.scale;
   uint32_t F[4][4];
   u16 sv[4][4];    // bf16 of sign * step
+  float ov[4][4], stp[4][4];  // the forward's value and sign * step (outW)
   uint32_t h[4];   // bit q: the forward's code was rounded up
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -291,12 +293,15 @@ __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
     for (int c = 0; c < 4; ++c) {
       F[q][c] = 0;
       sv[q][c] = 0;
+      ov[q][c] = stp[q][c] = 0.0f;
       if (ok) {
         const float y = div_scale(u4[c], rs);
         const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
         F[q][c] = b.F;
         const float st = signbit(y) ? -f8_step(b) : f8_step(b);
         sv[q][c] = a.f16 ? f16_bits(st) : bf16_bits(st);
+        ov[q][c] = f8_value((cw >> (8 * c)) & 0xFFu, a.f);
+        stp[q][c] = st;
         h[q] |= (uint32_t)(((cw >> (8 * c)) & 0x7Fu) != b.base + b.mi) << c;
       }
     }
@@ -313,15 +318,21 @@ __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
       for (int c = 0; c < 4; ++c) {
         const uint32_t up = sr_up(F[q][c], R[c]), hb = (h[q] >> c) & 1u;
         tile[4 * cg + c][rg + 16 * q] = up == hb ? (u16)0 : (up ? sv[q][c] : (u16)(sv[q][c] ^ 0x8000u));
+        if (a.outW) {
+          // the new rounding's value: exact (an FP8 value)
+          const float nv = up == hb ? ov[q][c] : (up ? ov[q][c] + stp[q][c] : ov[q][c] - stp[q][c]);
+          tileW[4 * cg + c][rg + 16 * q] = a.f16 ? f16_bits(nv) : bf16_bits(nv);
+        }
       }
     }
     __syncthreads();
-    u16* out = a.out + (int64_t)b * a.d * a.ldo;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int ch = threadIdx.x + 256 * i, cc = ch >> 3, k8 = ch & 7;
       const int64_t j = j0 + cc;
-      if (j < a.d) *(uint4*)(out + j * a.ldo + t0 + 8 * k8) = *(const uint4*)&tile[cc][8 * k8];
+      const int64_t o = (int64_t)b * a.d * a.ldo + j * a.ldo + t0 + 8 * k8;
+      if (j < a.d && a.out) *(uint4*)(a.out + o) = *(const uint4*)&tile[cc][8 * k8];
+      if (j < a.d && a.outW) *(uint4*)(a.outW + o) = *(const uint4*)&tileW[cc][8 * k8];
     }
     __syncthreads();
   }
@@ -630,7 +641,8 @@ bs_status launch_norm_planes(int mode, const NormPlaneArgs& a, hipStream_t st) {
 bs_status launch_trial_planes(const TrialPlaneArgs& a, hipStream_t st) {
   if (a.nb <= 0 || a.d <= 0) return BS_OK;
   // whole 16-byte pieces of padded rows out, four columns per load in
-  if (a.ldo % 64 || ((uintptr_t)a.out & 15) || (a.d & 3) || ((uintptr_t)a.u & 15) || ((uintptr_t)a.codes & 3))
+  if (a.ldo % 64 || ((uintptr_t)a.out & 15) || ((uintptr_t)a.outW & 15) || (a.d & 3) || ((uintptr_t)a.u & 15) ||
+      ((uintptr_t)a.codes & 3))
     return BS_EINVAL;
   dim3 grid((unsigned)((a.d + 63) / 64), (unsigned)((a.ldo + 63) / 64));
   ProfScope prof("trial_planes", st);

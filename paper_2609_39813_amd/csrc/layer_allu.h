@@ -33,7 +33,7 @@ struct AlluIO {
   double* table;           // [8][3][3] (nullable)
 };
 
-size_t allu_ws_size(int B, int S, int d, int H, int F);
+size_t allu_ws_size(int B, int S, int d, int H, int F, int K);
 bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st);
 
 }  // namespace bsp

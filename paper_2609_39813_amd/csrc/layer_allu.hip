@@ -37,17 +37,21 @@ constexpr float kAttnScale = 0.125f;  // 1 / sqrt(64)
 enum { G_DX = 0, G_DGAIN1, G_DWQKV, G_DWO, G_DGAIN2, G_DWG, G_DWU, G_DWD, NGRAD };
 constexpr int NCOMP = 4;  // gradients formed here per trial: dx, dgain1, dWqkv, dWo
 constexpr int NB = 4;     // N trials per update of the shifted sums (one read-modify-write per NB)
+constexpr int KCH = 16;   // N trials per chunk of the batched weight-use contractions (a multiple of NB)
 // maxima (slot arrays) of the scaled fp16 operands: per call dh, dQKV, Wo, Wqkv, V, Q, K; per pass
 // the moves dh_d, dQKV_d, dO_d, D_d
 enum { AM_DH, AM_DQKV, AM_WO, AM_WQKV, AM_V, AM_Q, AM_K, AM_DHD, AM_DQKVD, AM_DOD, AM_DDD, AM_N };
-// their 2^-e: the splits of dh_d (with dh + dh_d), dQKV_d (with dQKV + dQKV_d), Wo, Wqkv; then the
-// attention backward's seven in its order (dO_d, V, Q, K, dS's 2^s, 2^-s-q, 2^-s-k)
-enum { IV_DHD, IV_DQKVD, IV_WO, IV_WQKV, IV_DOD, IV_V, IV_Q, IV_K, IV_DS, IV_DKM, IV_DQM, IV_N };
+// their 2^-e: the splits of dh_d, dQKV_d, Wo, Wqkv, dh, dQKV; then the attention backward's seven
+// in its order (dO_d, V, Q, K, dS's 2^s, 2^-s-q, 2^-s-k)
+enum { IV_DHD, IV_DQKVD, IV_WO, IV_WQKV, IV_DH, IV_DQKV, IV_DOD, IV_V, IV_Q, IV_K, IV_DS, IV_DKM, IV_DQM, IV_N };
 
 struct AlluWs {
   float *u1, *u2, *r1, *r2, *du1, *du2, *m, *l;
   u16 *Vt, *Qt, *Kt, *valT_u1, *valT_O, *dqkvT[3], *dhT[3];
-  u16 *pA[3], *rows3[3], *tA[3], *tB[3], *dOp[3], *dOt[3];
+  u16 *pA[3], *rows3[3], *tB[3], *dOp[3], *dOt[3];
+  u16 *tH[2], *tQ[2];    // dh, dQKV as scaled two-term fp16 splits, transposed
+  u16 *pAn[2], *pWn[2];  // a chunk of N trials' difference and value planes at O's and u1's weight uses
+  float *dWo_n, *dWqkv_n;  // the chunk's weight-use moves [KCH][d][d], [KCH][d][3d]
   float *dh_d, *dO_dt, *dO_dh, *dD, *dQ_d, *dK_d, *dV_d, *du1_d;
   u16 *Wo16, *Wqkv16, *V16;  // the weights and V as scaled fp16 (the moves' contractions)
   u16 *Q16, *K16, *Qt16, *Kt16;  // Q, K as scaled fp16 and their transposed copies
@@ -66,8 +70,9 @@ struct AlluWs {
   float* inv;            // [IV_N]
 };
 
-AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
+AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F, int K) {
   AlluWs w{};
+  const int64_t kc = std::max(1, std::min(K, KCH));
   const int64_t T = (int64_t)B * S, Td = T * d, Tp = round_up(T > 0 ? T : 1, 64), bh = (int64_t)B * H;
   const int64_t Sp = round_up(S, 64), d3 = 3 * (int64_t)d, F2 = 2 * (int64_t)F;
   const int64_t nc[NCOMP] = {Td, d, (int64_t)d * d3, (int64_t)d * d};
@@ -83,7 +88,6 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
     w.dhT[i] = c.take<u16>(d * Tp);
     w.pA[i] = c.take<u16>(d * Tp);
     w.rows3[i] = c.take<u16>(T * std::max(F2, d3));
-    w.tA[i] = c.take<u16>(d3 * Tp);
     w.tB[i] = c.take<u16>(d3 * Tp);
     w.dOp[i] = c.take<u16>(Td);
     w.dOt[i] = c.take<u16>(bh * DH * Sp);
@@ -100,6 +104,14 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F) {
   w.K16 = c.take<u16>(bh * S * DH);
   w.Qt16 = c.take<u16>(bh * DH * Sp);
   w.Kt16 = c.take<u16>(bh * DH * Sp);
+  for (int i = 0; i < 2; ++i) {
+    w.tH[i] = c.take<u16>(d * Tp);
+    w.tQ[i] = c.take<u16>(d3 * Tp);
+    w.pAn[i] = c.take<u16>(kc * d * Tp);
+    w.pWn[i] = c.take<u16>(kc * d * Tp);
+  }
+  w.dWo_n = c.take<float>(kc * d * d);
+  w.dWqkv_n = c.take<float>(kc * d * d3);
   w.gpart = c.take<double>(3 * ((T + 15) / 16) * (int64_t)d);
   for (int i = 0; i < NCOMP; ++i) {
     w.delta[i] = c.take<float>(NB * nc[i]);
@@ -162,9 +174,9 @@ bs_status copy_f32(float* dst, const float* src, int64_t n, hipStream_t st) {
 
 }  // namespace
 
-size_t allu_ws_size(int B, int S, int d, int H, int F) {
+size_t allu_ws_size(int B, int S, int d, int H, int F, int K) {
   Carver c;
-  carve_allu(c, B, S, d, H, F);
+  carve_allu(c, B, S, d, H, F, K);
   return c.used();
 }
 
@@ -174,10 +186,10 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   const int64_t Sp = round_up(S, 64), rows_h = bh * S, d3 = 3 * (int64_t)d, F2 = 2 * (int64_t)F;
   const int64_t nc[NCOMP] = {Td, d, (int64_t)d * d3, (int64_t)d * d};
   Carver probe;
-  carve_allu(probe, B, S, d, H, F);
+  carve_allu(probe, B, S, d, H, F, K);
   if (ws_bytes < probe.used()) return BS_EWORKSPACE;
   Carver c(ws, ws_bytes);
-  const AlluWs w = carve_allu(c, B, S, d, H, F);
+  const AlluWs w = carve_allu(c, B, S, d, H, F, K);
   const F8 f = f8_format(io.fmt);
   const float *s_u1 = io.scales + 0, *s_O = io.scales + 1, *s_u2 = io.scales + 2;
 
@@ -238,6 +250,22 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   }
   BS_TRY(launch_planes(io.dqkv, BS_F32, T, d3, d3, true, w.dqkvT, 3, Tp, 1.0f, st));
   BS_TRY(launch_planes(io.dh, BS_F32, T, d, d, true, w.dhT, 3, Tp, 1.0f, st));
+  // dh and dQKV as scaled two-term fp16 splits: under N a weight use's move is
+  // W_k^T g_d + (W_k - W_q)^T g (g the reference incoming gradient, g_d its move, W_k the trial's
+  // new rounding, W_q the forward's), and the second products of a chunk of trials are one
+  // contraction against these
+  {
+    MoveSrc mh{};
+    mh.rows = io.dh;
+    mh.ldi = d;
+    BS_TRY(launch_split_move(mh, nullptr, 0, T, d, F16Scale{w.amax[AM_DH], nullptr, w.inv + IV_DH}, w.tH, nullptr, Tp,
+                             nullptr, 0, st));
+    MoveSrc mg{};
+    mg.rows = io.dqkv;
+    mg.ldi = d3;
+    BS_TRY(launch_split_move(mg, nullptr, 0, T, d3, F16Scale{w.amax[AM_DQKV], nullptr, w.inv + IV_DQKV}, w.tQ, nullptr,
+                             Tp, nullptr, 0, st));
+  }
 
   // ---- one pass per letter (K per-trial passes for N) ----
   for (int l = 0; l < 3; ++l) {
@@ -247,10 +275,40 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         return StoreRead{x, codes, scale, f, l, io.seed, (uint32_t)k, use};
       };
       const int slot = l == LETTER_N ? (k - 1) % NB : 0;
+      const int kk = (k - 1) % KCH;  // N: the trial's index in its chunk
+      if (l == LETTER_N && kk == 0) {
+        // the chunk's new roundings at O's and u1's weight uses (difference and value planes), and
+        // their differences' products with the reference incoming gradients, the chunk in one
+        // contraction each
+        const int nbk = std::min(KCH, K - k + 1);
+        TrialPlaneArgs to{io.Otok, io.c_Otok, s_O, f, T, d, Tp, io.seed, 1 * 256 + 2, k, nbk, w.pAn[0]};
+        to.f16 = 1;
+        to.outW = w.pWn[0];
+        BS_TRY(launch_trial_planes(to, st));
+        TrialPlaneArgs tu{w.u1, io.c_u1, s_u1, f, T, d, Tp, io.seed, 0 * 256 + 2, k, nbk, w.pAn[1]};
+        tu.f16 = 1;
+        tu.outW = w.pWn[1];
+        BS_TRY(launch_trial_planes(tu, st));
+        Gemm go(nbk * d, d, (int)Tp, Tp, Tp, w.dWo_n, d, s_O);
+        go.g.f16 = 1;
+        go.g.alpha_dev2 = w.inv + IV_DH;
+        BS_TRY(go.add(&w.pAn[0], 1, w.tH, 2).run(w.part, w.part_cap, st));
+        Gemm gg(nbk * d, (int)d3, (int)Tp, Tp, Tp, w.dWqkv_n, d3, s_u1);
+        gg.g.f16 = 1;
+        gg.g.alpha_dev2 = w.inv + IV_DQKV;
+        BS_TRY(gg.add(&w.pAn[1], 1, w.tQ, 2).run(w.part, w.part_cap, st));
+      }
       float* dl[NCOMP];
       for (int i = 0; i < NCOMP; ++i) dl[i] = w.delta[i] + slot * nc[i];
+      if (l == LETTER_N) {
+        dl[2] = w.dWqkv_n + kk * nc[2];
+        dl[3] = w.dWo_n + kk * nc[3];
+      }
       float* dWo = dl[3];
       float* dWqkv = dl[2];
+      // the value planes the weight uses read with the moves: the forward's (R) or trial k's (N)
+      const u16* valO = l == LETTER_N ? w.pWn[0] + (int64_t)kk * d * Tp : w.valT_O;
+      const u16* valU = l == LETTER_N ? w.pWn[1] + (int64_t)kk * d * Tp : w.valT_u1;
       // u2's normalization-input use: the move of dh (and its max |.|)
       if (l != LETTER_U) {
         BS_TRY(launch_fill2d((float*)w.amax[AM_DHD], (AM_N - AM_DHD) * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
@@ -259,31 +317,24 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         ax.amax = w.amax[AM_DHD];
         BS_TRY(launch_allu_dx(ax, st));
       }
-      // one scale for dh_d and dh + dh_d (the contraction has one multiplier)
-      const F16Scale sc_o{w.amax[AM_DHD], w.amax[AM_DH], w.inv + IV_DHD};
-      const F16Scale sc_q{w.amax[AM_DQKVD], w.amax[AM_DQKV], w.inv + IV_DQKVD};
+      const F16Scale sc_o{w.amax[AM_DHD], nullptr, w.inv + IV_DHD};
+      const F16Scale sc_q{w.amax[AM_DQKVD], nullptr, w.inv + IV_DQKVD};
       // O's weight use (Wo)
       if (l == LETTER_U) {
         BS_TRY(planes_of(NP_RESU, io.Otok, io.c_Otok, s_O, w.pA, 3));
         BS_TRY(Gemm(d, d, (int)Tp, Tp, Tp, dWo, d, nullptr).add(w.pA, 3, w.dhT, 3).run(w.part, w.part_cap, st));
       } else {
-        // dh_d's transposed planes (the weight use), under N those of dh_L = dh + dh_d, and its
-        // row planes (the move of dO), one read
+        // dh_d's transposed planes (the weight use) and row planes (the move of dO), one read; the
+        // weight use's move: val^T dh_d (N: added to the chunk's difference product)
         MoveSrc mo{};
         mo.rows = w.dh_d;
         mo.ldi = d;
-        BS_TRY(launch_split_move(mo, l == LETTER_N ? io.dh : nullptr, d, T, d, sc_o, w.tB, w.tA, Tp, w.rows3, d, st));
+        BS_TRY(launch_split_move(mo, nullptr, 0, T, d, sc_o, w.tB, nullptr, Tp, w.rows3, d, st));
         Gemm gw(d, d, (int)Tp, Tp, Tp, dWo, d, s_O);
         gw.g.f16 = 1;
         gw.g.alpha_dev2 = w.inv + IV_DHD;
-        gw.add(&w.valT_O, 1, w.tB, 2);
-        if (l == LETTER_N) {
-          TrialPlaneArgs ta{io.Otok, io.c_Otok, s_O, f, T, d, Tp, io.seed, 1 * 256 + 2, k, 1, w.pA[0]};
-          ta.f16 = 1;
-          BS_TRY(launch_trial_planes(ta, st));
-          gw.add(&w.pA[0], 1, w.tA, 2);
-        }
-        BS_TRY(gw.run(w.part, w.part_cap, st));
+        gw.g.accumulate = l == LETTER_N;
+        BS_TRY(gw.add(&valO, 1, w.tB, 2).run(w.part, w.part_cap, st));
         // the move of dO (token-major, then head-major)
         Gemm gm((int)T, d, d, d, d, w.dO_dt, d, w.inv + IV_WO);
         gm.g.f16 = 1;
@@ -335,8 +386,8 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         ba.dV = w.dV_d;
         ba.n_pol = 0;
         BS_TRY(launch_attn_bwd(ba, B, H, st));
-        // u1's weight use (Wqkv): the move of dQKV read head-major ([T][3d] token-major view),
-        // under N with dQKV + dQKV_d, and its row planes (the move of du1)
+        // u1's weight use (Wqkv): the move of dQKV read head-major ([T][3d] token-major view), and
+        // its row planes (the move of du1)
         MoveSrc mq{};
         mq.heads[0] = w.dQ_d;
         mq.heads[1] = w.dK_d;
@@ -344,19 +395,12 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         mq.S = S;
         mq.H = H;
         mq.d = d;
-        BS_TRY(launch_split_move(mq, l == LETTER_N ? io.dqkv : nullptr, d3, T, d3, sc_q, w.tB, w.tA, Tp, w.rows3, d3,
-                                 st));
+        BS_TRY(launch_split_move(mq, nullptr, 0, T, d3, sc_q, w.tB, nullptr, Tp, w.rows3, d3, st));
         Gemm gq(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, s_u1);
         gq.g.f16 = 1;
         gq.g.alpha_dev2 = w.inv + IV_DQKVD;
-        gq.add(&w.valT_u1, 1, w.tB, 2);
-        if (l == LETTER_N) {
-          TrialPlaneArgs ta{w.u1, io.c_u1, s_u1, f, T, d, Tp, io.seed, 0 * 256 + 2, k, 1, w.pA[0]};
-          ta.f16 = 1;
-          BS_TRY(launch_trial_planes(ta, st));
-          gq.add(&w.pA[0], 1, w.tA, 2);
-        }
-        BS_TRY(gq.run(w.part, w.part_cap, st));
+        gq.g.accumulate = l == LETTER_N;
+        BS_TRY(gq.add(&valU, 1, w.tB, 2).run(w.part, w.part_cap, st));
         // the move of du1, then u1's gain and normalization-input uses
         Gemm gu((int)T, d, (int)d3, d3, d3, w.du1_d, d, w.inv + IV_WQKV);
         gu.g.f16 = 1;
@@ -375,7 +419,8 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       for (int i = 0; i < NCOMP; ++i) {
         if (l == LETTER_N) {
           if (slot == NB - 1 || k == ntr)
-            BS_TRY(launch_trial_accum(w.delta[i], slot + 1, k - slot, nc[i], w.d1[i], w.S1[i], w.S2[i], st));
+            BS_TRY(launch_trial_accum(dl[i] - (int64_t)slot * nc[i], slot + 1, k - slot, nc[i], w.d1[i], w.S1[i],
+                                      w.S2[i], st));
         } else {
           BS_TRY(copy_f32(w.bias[l][i], dl[i], nc[i], st));
         }
