@@ -39,6 +39,7 @@ struct WeightUseIO {
   float* dW_ref;         // [k][n]
   float* bias;           // [3][k][n] for U, R, N
   float* se_n = nullptr; // [k][n] nullable: N's se (the per-trial path)
+  const float* amax_x = nullptr;  // device max |X| (the store's amax; bounds the U residual)
 };
 
 // trials per per-trial contraction (stacked along the output rows)
@@ -51,7 +52,13 @@ struct WeightUseWs {
   u16* tplanes;  // per-trial residual planes [BT][k][Tp]
   float *tdelta, *td1;
   double *tS1, *tS2;
+  uint32_t* am;  // dY's max (slot array) for its fp16 split
+  float* inv;    // 2^-e of dY's split and of the U residual's
 };
+
+// an fp32 incoming gradient enters as a scaled two-term fp16 split against exact fp16 operands
+// (FP8 values, the U residual's split, the N residual) when K <= 256
+inline bool wu_f16(bs_dtype gt, int K) { return gt == BS_F32 && K <= 256; }
 
 WeightUseWs carve_wu(Carver& c, int64_t T, int64_t k, int64_t n, int K = 1, bool se = false) {
   WeightUseWs w{};
@@ -72,6 +79,8 @@ WeightUseWs carve_wu(Carver& c, int64_t T, int64_t k, int64_t n, int K = 1, bool
     w.tS1 = c.take<double>(k * n);
     w.tS2 = c.take<double>(k * n);
   }
+  w.am = c.take<uint32_t>(AMAX_SLOTS * AMAX_STRIDE);
+  w.inv = c.take<float>(2);
   return w;
 }
 
@@ -83,8 +92,19 @@ bs_status weight_use_run(const WeightUseIO& io, void* ws, size_t ws_bytes, hipSt
   Carver c(ws, ws_bytes);
   const WeightUseWs w = carve_wu(c, io.T, io.k, io.n, io.K, se);
   const int64_t Tp = round_up(io.T > 0 ? io.T : 1, 64);
-  const int nt = io.gt == BS_F32 ? 3 : 1;
-  BS_TRY(launch_planes(io.dY, io.gt, io.T, io.n, io.n, true, w.dyT, nt, Tp, 1.0f, st));
+  const bool h16 = wu_f16(io.gt, io.K);
+  const int nt = h16 ? 2 : (io.gt == BS_F32 ? 3 : 1);
+  if (h16) {
+    BS_TRY(launch_fill2d((float*)w.am, AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
+    BS_TRY(launch_amax_f32((const float*)io.dY, io.T * io.n, w.am, st));
+    MoveSrc ms{};
+    ms.rows = (const float*)io.dY;
+    ms.ldi = io.n;
+    BS_TRY(launch_split_move(ms, nullptr, 0, io.T, io.n, F16Scale{w.am, nullptr, w.inv + 0}, w.dyT, nullptr, Tp,
+                             nullptr, 0, st));
+  } else {
+    BS_TRY(launch_planes(io.dY, io.gt, io.T, io.n, io.n, true, w.dyT, nt, Tp, 1.0f, st));
+  }
   NormPlaneArgs pa{};
   pa.u = io.Xs;
   pa.codes = io.codes;
@@ -94,6 +114,11 @@ bs_status weight_use_run(const WeightUseIO& io, void* ws, size_t ws_bytes, hipSt
   pa.T = io.T;
   pa.d = io.k;
   pa.ldo = Tp;
+  pa.f16 = h16;
+  pa.amax_u = io.amax_x;
+  pa.inv_out = h16 ? w.inv + 1 : nullptr;
+  // the N residual (up-count difference times a step) exact in fp16; E5M2's steps scaled by 2^-8
+  pa.resn_scale = io.fmt == BS_E5M2 ? 0x1p-8f : 1.0f;
   auto gemm = [&](u16* const* A, int nA, float* C, float alpha, const float* alpha_dev) -> bs_status {
     GemmArgs g{};
     g.M = (int)io.k;
@@ -107,7 +132,11 @@ bs_status weight_use_run(const WeightUseIO& io, void* ws, size_t ws_bytes, hipSt
     g.C = C;
     g.part = w.gpart;
     g.part_cap = w.gpart_cap;
-    if (!gemm_add_products(g, A, nA, w.dyT, nt)) return BS_EINVAL;
+    if (h16) {
+      g.f16 = 1;
+      g.alpha_dev2 = w.inv + 0;
+    }
+    if (!gemm_add_products(g, A, nA, w.dyT, nt, h16 && nA == 2 ? 1 : 2)) return BS_EINVAL;
     return launch_gemm(g, st);
   };
   // reference: s val(C)^T dY
@@ -115,11 +144,11 @@ bs_status weight_use_run(const WeightUseIO& io, void* ws, size_t ws_bytes, hipSt
   pa.nterms = 1;
   BS_TRY(launch_norm_planes(NP_VAL, pa, st));
   BS_TRY(gemm(&w.valT, 1, io.dW_ref, 1.0f, io.scale));
-  // U: residual X - s val(C) in three exact bf16 terms
+  // U: residual X - s val(C) in three exact bf16 terms (or its scaled two-term fp16 split)
   for (int i = 0; i < 3; ++i) pa.out[i] = w.res[i];
-  pa.nterms = 3;
+  pa.nterms = h16 ? 2 : 3;
   BS_TRY(launch_norm_planes(NP_RESU, pa, st));
-  BS_TRY(gemm(w.res, 3, w.bias_u, 1.0f, nullptr));
+  BS_TRY(gemm(w.res, pa.nterms, w.bias_u, 1.0f, h16 ? w.inv + 1 : nullptr));
   // N: up counts over the K new roundings, residual (n_up - K h) step
   const FreshArgs<float> fa{io.Xs, io.T, io.k, pa.f, io.scale, io.seed, io.use, io.K, w.counts, nullptr, nullptr,
                             nullptr};
@@ -128,7 +157,7 @@ bs_status weight_use_run(const WeightUseIO& io, void* ws, size_t ws_bytes, hipSt
   pa.out[2] = nullptr;
   pa.nterms = io.K > 256 ? 2 : 1;
   BS_TRY(launch_norm_planes(NP_RESN, pa, st));
-  BS_TRY(gemm(w.res, pa.nterms, w.bias_n, 1.0f / (float)io.K, io.scale));
+  BS_TRY(gemm(w.res, pa.nterms, w.bias_n, 1.0f / (float)io.K / (h16 ? pa.resn_scale : 1.0f), io.scale));
   const int64_t kn = io.k * io.n;
   const float* b[3] = {w.bias_u, nullptr, w.bias_n};
   for (int l = 0; l < 3; ++l)
@@ -137,7 +166,8 @@ bs_status weight_use_run(const WeightUseIO& io, void* ws, size_t ws_bytes, hipSt
     const int bt = wu_trial_batch(io.K);
     for (int k0 = 1; k0 <= io.K; k0 += bt) {
       const int nb = io.K - k0 + 1 < bt ? io.K - k0 + 1 : bt;
-      const TrialPlaneArgs ta{io.Xs, io.codes, io.scale, pa.f, io.T, io.k, Tp, io.seed, io.use, k0, nb, w.tplanes};
+      TrialPlaneArgs ta{io.Xs, io.codes, io.scale, pa.f, io.T, io.k, Tp, io.seed, io.use, k0, nb, w.tplanes};
+      ta.f16 = h16;
       BS_TRY(launch_trial_planes(ta, st));
       GemmArgs g{};
       g.M = (int)(nb * io.k);
@@ -151,6 +181,10 @@ bs_status weight_use_run(const WeightUseIO& io, void* ws, size_t ws_bytes, hipSt
       g.C = w.tdelta;
       g.part = w.gpart;
       g.part_cap = w.gpart_cap;
+      if (h16) {
+        g.f16 = 1;
+        g.alpha_dev2 = w.inv + 0;
+      }
       const u16* A0 = w.tplanes;
       if (!gemm_add_products(g, &A0, 1, w.dyT, nt)) return BS_EINVAL;
       BS_TRY(launch_gemm(g, st));
@@ -415,8 +449,9 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
   BS_TRY(norm_run(b2, w.sub, w.sub_bytes, st));
   BS_TRY(launch_add(dOut, BS_BF16, w.dxn2, w.dh, Td, st));
   // store O, weight use of Wo (incoming gradient dh)
-  const WeightUseIO wo{w.Otok, w.c_Otok, scales + 1, fmt, w.dh, BS_F32, T, d, d, K, seed, 1 * 256 + 2, dWo,
-                       w.wo_bias, w.wo_se};
+  WeightUseIO wo{w.Otok, w.c_Otok, scales + 1, fmt, w.dh, BS_F32, T, d, d, K, seed, 1 * 256 + 2, dWo,
+                 w.wo_bias, w.wo_se};
+  wo.amax_x = &dg[1].amax;  // the store of O's max |O|
   BS_TRY(weight_use_run(wo, w.sub, w.sub_bytes, st));
   {  // dO (token-major) = dh Wo^T with dh in three exact bf16 terms
     Carver cs(w.sub, w.sub_bytes);

@@ -40,12 +40,14 @@ inline double gemm_flops(const GemmArgs& g) {
 // flop the matrix cores execute: 2 M N K per segment (every bf16 term of a split operand)
 inline double gemm_exec_flops(const GemmArgs& g) { return 2.0 * g.M * g.N * (double)g.K * g.nseg; }
 
-// Append the products A_i B_j (i + j <= 2) of nA and nB bf16 terms to g's segments (with fp16
-// operands: A of one exact term, B of the two terms of a scaled fp16 split: both products).
-inline bool gemm_add_products(GemmArgs& g, const u16* const* A, int nA, const u16* const* B, int nB) {
+// Append the products A_i B_j (i + j <= maxsum) of nA and nB bf16 terms to g's segments: with
+// three-term splits the products of order 2^-24 and above (maxsum 2); with two-term fp16 splits
+// (one exact term against two, or two against two with maxsum 1) those of order 2^-22 and above.
+inline bool gemm_add_products(GemmArgs& g, const u16* const* A, int nA, const u16* const* B, int nB,
+                              int maxsum = 2) {
   if (g.nprod == 0 && g.nseg > 0) g.nprod = g.nseg;  // segments set before: one product each
   ++g.nprod;
-  for (int s = 0; s <= 2; ++s)
+  for (int s = 0; s <= maxsum; ++s)
     for (int i = 0; i < nA; ++i) {
       const int j = s - i;
       if (j < 0 || j >= nB) continue;

@@ -18,7 +18,13 @@ struct NormPlaneArgs {
   u16* out[3];             // planes [d][ldo]
   int nterms;
   int64_t ldo;
-  int f16 = 0;             // NP_VAL: fp16 values (exact for FP8 codes) instead of bf16
+  int f16 = 0;             // fp16 planes: NP_VAL the values (exact for FP8 codes); NP_RESU the
+                           // two-term split of the residual 2^e (e = f16_scale_exp of max(*amax_u,
+                           // s FMAX), less one: |u - s val| <= |u| + s FMAX), 2^-e to *inv_out;
+                           // NP_RESN one exact term of the residual times resn_scale (K <= 256)
+  const float* amax_u = nullptr;  // device max |u| (nullable)
+  float* inv_out = nullptr;
+  float resn_scale = 1.0f;        // a power of two that keeps K max-step within fp16
 };
 
 // rows per block of the gain use's column partial sums (the partial array holds one row of

@@ -149,6 +149,23 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd8_kernel(const T* __restrict__
 //   NP_VAL : val(C_u)                                      (1 term, exact)
 //   NP_RESU: u - s * val(C_u)  (= minus the forward's rounding error; 3 terms)
 //   NP_RESN: sign * (n_up - K * [C_u rounded up]) * step   (1 term if K <= 256, else 2)
+// split2_f16 of x as one word (hi | lo << 16); kept out of line: inlined into the vector plane
+// kernel's packing it trips the compiler's instruction selection
+__device__ __attribute__((noinline)) uint32_t split2_f16_word(float x) {
+  u16 h, l;
+  split2_f16(x, h, l);
+  return (uint32_t)h | ((uint32_t)l << 16);
+}
+
+// 2^e of the fp16 split of the U residual u - s val(C) (its bound max(max|u|, s FMAX) doubled),
+// with 2^-e stored by the first thread of the grid
+__device__ __forceinline__ float resu_f16_scale(const NormPlaneArgs& a, float s) {
+  const float bound = fmaxf(a.amax_u ? *a.amax_u : 0.0f, s * a.f.fmax);
+  const int e = f16_scale_exp(bound) - 1;
+  if (a.inv_out && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *a.inv_out = ldexpf(1.0f, -e);
+  return ldexpf(1.0f, e);
+}
+
 template <int MODE>
 __global__ __launch_bounds__(256) void norm_planes_t_kernel(NormPlaneArgs a) {
   __shared__ u16 tile[3][64][66];
@@ -156,6 +173,7 @@ __global__ __launch_bounds__(256) void norm_planes_t_kernel(NormPlaneArgs a) {
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
   const float s = *a.scale;
   const double rs = 1.0 / (double)s;
+  const float rsc = MODE == NP_RESU && a.f16 ? resu_f16_scale(a, s) : 1.0f;
 #pragma unroll 2
   for (int i = 0; i < 16; ++i) {
     const int rr = ty + 4 * i;
@@ -170,13 +188,20 @@ __global__ __launch_bounds__(256) void norm_planes_t_kernel(NormPlaneArgs a) {
           o[0] = a.f16 ? f16_bits(v) : bf16_bits(v);
         }
       } else if (MODE == NP_RESU) {
-        split3(fmaf(-s, f8_value(code, a.f), a.u[e]), o[0], o[1], o[2]);
+        const float r = fmaf(-s, f8_value(code, a.f), a.u[e]);
+        if (a.f16)
+          split2_f16(r * rsc, o[0], o[1]);
+        else
+          split3(r, o[0], o[1], o[2]);
       } else {
         const float y = div_scale(a.u[e], rs);
         const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
         const int h = (code & 0x7Fu) != b.base + b.mi;
         const float v = (float)((int)a.counts[e] - a.K * h) * f8_step(b);
-        split3(signbit(y) ? -v : v, o[0], o[1], o[2]);
+        if (a.f16)
+          o[0] = f16_bits((signbit(y) ? -v : v) * a.resn_scale);
+        else
+          split3(signbit(y) ? -v : v, o[0], o[1], o[2]);
       }
     }
     for (int p = 0; p < a.nterms; ++p) tile[p][rr][tx] = o[p];
@@ -201,6 +226,7 @@ __global__ __launch_bounds__(256) void norm_planes_t4_kernel(NormPlaneArgs a) {
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
   const float s = *a.scale;
   const double rs = 1.0 / (double)s;
+  const float rsc = MODE == NP_RESU && a.f16 ? resu_f16_scale(a, s) : 1.0f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int rr = rg + 16 * i;
@@ -232,13 +258,23 @@ __global__ __launch_bounds__(256) void norm_planes_t4_kernel(NormPlaneArgs a) {
           const float v = f8_value(code, a.f);
           o[0][c] = a.f16 ? f16_bits(v) : bf16_bits(v);
         } else if (MODE == NP_RESU) {
-          split3(fmaf(-s, f8_value(code, a.f), uv[c]), o[0][c], o[1][c], o[2][c]);
+          const float r = fmaf(-s, f8_value(code, a.f), uv[c]);
+          if (a.f16) {
+            const uint32_t hl = split2_f16_word(r * rsc);
+            o[0][c] = (u16)(hl & 0xFFFFu);
+            o[1][c] = (u16)(hl >> 16);
+          } else {
+            split3(r, o[0][c], o[1][c], o[2][c]);
+          }
         } else {
           const float y = div_scale(uv[c], rs);
           const Bracket b = f8_bracket(fminf(fabsf(y), a.f.fmax), a.f);
           const int h = (code & 0x7Fu) != b.base + b.mi;
           const float v = (float)((int)cn[c] - a.K * h) * f8_step(b);
-          split3(signbit(y) ? -v : v, o[0][c], o[1][c], o[2][c]);
+          if (a.f16)
+            o[0][c] = f16_bits((signbit(y) ? -v : v) * a.resn_scale);
+          else
+            split3(signbit(y) ? -v : v, o[0][c], o[1][c], o[2][c]);
         }
       }
     }
@@ -616,6 +652,8 @@ bs_status launch_rmsnorm_fwd(const void* X, bs_dtype dt, const float* gain, int6
 }
 
 bs_status launch_norm_planes(int mode, const NormPlaneArgs& a, hipStream_t st) {
+  if (a.f16 && ((mode == NP_RESU) != (a.nterms == 2) || a.nterms > 2 || (mode == NP_RESN && a.K > 256)))
+    return BS_EINVAL;
   if (a.d <= 0 || a.ldo <= 0) return BS_OK;
   dim3 grid((unsigned)((a.d + 63) / 64), (unsigned)((a.ldo + 63) / 64));
   bool vec = a.d % 4 == 0 && a.ldo % 64 == 0 && ((uintptr_t)a.u & 15) == 0 && ((uintptr_t)a.codes & 3) == 0 &&

@@ -354,7 +354,8 @@ bs_status launch_split_move(const MoveSrc& m, const float* base, int64_t ldb, in
   if (!sc.amax_a || !tM || !tM[0] || !tM[1] || (base && (!tS || !tS[0] || !tS[1])) ||
       (rows && (!rows[0] || !rows[1])))
     return BS_EINVAL;
-  if (R <= 0 || C <= 0) return BS_OK;
+  if (R < 0) return BS_EINVAL;
+  if (C <= 0 || ldo <= 0) return BS_OK;  // R = 0: the transposed planes are zero
   bool ok = C % 4 == 0 && ldo % 64 == 0 && ldo >= R && a16(tM[0]) && a16(tM[1]);
   if (m.rows) {
     ok = ok && m.ldi % 4 == 0 && m.ldi >= C && a16(m.rows);

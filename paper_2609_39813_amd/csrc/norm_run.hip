@@ -36,7 +36,16 @@ struct NormWs {
   u16* tplanes;   // per-trial residual planes [BT][d][Tp]
   float *tdelta, *td1, *se_w[2];
   double *tS1, *tS2;
+  // fp16 operands (an fp32 incoming gradient, bf16 W, K <= 256): W as scaled fp16, the maxima of
+  // dY and W (slot arrays) and the multipliers 2^-e of dY, W and the U residual
+  u16* W16;
+  uint32_t* am[2];
+  float* inv;
 };
+
+// the weight and normalization-input contractions take scaled two-term fp16 splits of an fp32
+// incoming gradient against exact fp16 operands (FP8 values, residuals, the scaled weights)
+inline bool use_f16(bs_dtype wt, bs_dtype gt, int K) { return gt == BS_F32 && wt == BS_BF16 && K <= 256; }
 
 NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype wt, bs_dtype gt, const NormPlan& p,
                   bool want_y) {
@@ -87,6 +96,12 @@ NormWs carve_norm(Carver& c, int64_t T, int64_t d, int64_t n, int K, bs_dtype wt
     for (int i = 0; i < 2; ++i)
       if (p.weight_se[i]) w.se_w[i] = c.take<float>(d * n);
   }
+  if (use_f16(wt, gt, K)) {
+    w.W16 = c.take<u16>(d * n);
+    uint32_t* a = c.take<uint32_t>(2 * AMAX_SLOTS * AMAX_STRIDE);
+    for (int i = 0; i < 2; ++i) w.am[i] = a ? a + i * AMAX_SLOTS * AMAX_STRIDE : nullptr;
+    w.inv = c.take<float>(3);
+  }
   // split-K partials for the contractions with few output tiles (du: T x d; weight use: d x n)
   w.gpart_cap = 4 * d * std::max<int64_t>(std::max<int64_t>(T, n), 64);
   w.gpart = c.take<float>(w.gpart_cap);
@@ -111,14 +126,16 @@ NormPlan plan_norm(const bs_norm_policy* pol, int n_pol, bool want_gain_se, bool
 
 
 size_t norm_ws_size(int64_t T, int64_t d, int64_t n, int K) {
-  // sized for the most demanding policy set and fp32 operands everywhere
+  // sized for the most demanding policy set, over the operand types (fp32 everywhere, or the
+  // fp16 path's bf16 W with an fp32 incoming gradient)
   NormPlan p;
   p.gain_n = p.gain_r = p.weight_u = p.want_dxr = p.gain_se = true;
   p.weight_n[0] = p.weight_n[1] = true;
   p.weight_se[0] = p.weight_se[1] = true;
-  Carver c;
+  Carver c, c16;
   carve_norm(c, T, d, n, K, BS_F32, BS_F32, p, true);
-  return c.used();
+  carve_norm(c16, T, d, n, K, BS_BF16, BS_F32, p, true);
+  return std::max(c.used(), c16.used());
 }
 
 bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) {
@@ -187,8 +204,41 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   }
   if (fwd_only) return BS_OK;
 
+  const bool h16 = use_f16(wt, gt, K);
+  const bool du16 = h16 && n % 64 == 0;  // du's fp16 contraction runs on the pipelined kernel (K % 64)
+  const int ntd = h16 ? 2 : nt;  // terms of the incoming gradient's planes
+  if (h16) {
+    // dY's scaled two-term fp16 split in both layouts from one read, W as scaled fp16
+    BS_TRY(launch_fill2d((float*)w.am[0], 2 * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
+    BS_TRY(launch_amax_f32((const float*)dY, T * n, w.am[0], st));
+    BS_TRY(launch_amax_bf16((const u16*)W, d * n, w.am[1], st));
+    BS_TRY(launch_scale_f16((const u16*)W, d * n, w.am[1], w.W16, w.inv + 1, st));
+    MoveSrc ms{};
+    ms.rows = (const float*)dY;
+    ms.ldi = n;
+    BS_TRY(launch_split_move(ms, nullptr, 0, T, n, F16Scale{w.am[0], nullptr, w.inv + 0}, w.dyT, nullptr, Tp,
+                             du16 ? w.dy_rows : nullptr, n, st));
+  }
   // du = dY W^T  (A = dY [T, n], B = W [d, n], both n-contiguous)
-  {
+  if (du16) {
+    GemmArgs g{};
+    g.M = (int)T;
+    g.N = (int)d;
+    g.K = (int)n;
+    g.lda = n;
+    g.ldb = n;
+    g.ldc = d;
+    g.alpha = 1.0f;
+    g.alpha_dev = w.inv + 1;
+    g.alpha_dev2 = w.inv + 0;
+    g.f16 = 1;
+    g.C = w.du;
+    g.part = w.gpart;
+    g.part_cap = w.gpart_cap;
+    const u16* B0 = w.W16;
+    gemm_add_products(g, w.dy_rows, 2, &B0, 1);
+    BS_TRY(launch_gemm(g, st));
+  } else {
     GemmArgs g{};
     g.M = (int)T;
     g.N = (int)d;
@@ -217,7 +267,7 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   }
 
   // weight-use operands in the contraction layout [*, Tp]
-  BS_TRY(launch_planes(dY, gt, T, n, n, true, w.dyT, nt, Tp, 1.0f, st));
+  if (!h16) BS_TRY(launch_planes(dY, gt, T, n, n, true, w.dyT, nt, Tp, 1.0f, st));
   NormPlaneArgs pa{};
   pa.u = w.u;
   pa.codes = u_codes;
@@ -229,6 +279,12 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   pa.ldo = Tp;
   pa.out[0] = w.uvalT;
   pa.nterms = 1;
+  pa.f16 = h16;
+  pa.amax_u = &diag->amax;
+  pa.inv_out = h16 ? w.inv + 2 : nullptr;
+  // the N residual is an up-count difference (|.| <= K <= 256) times a step: exact in fp16 for
+  // E4M3 (steps 2^-9 .. 2^5); E5M2's steps 2^-16 .. 2^13 take the scale 2^-8 (2^-24 .. 2^13)
+  pa.resn_scale = fmt == BS_E5M2 ? 0x1p-8f : 1.0f;
   BS_TRY(launch_norm_planes(NP_VAL, pa, st));
 
   auto weight_gemm = [&](u16* const* A, int nA, float* C, float alpha, const float* alpha_dev) -> bs_status {
@@ -244,7 +300,11 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     g.C = C;
     g.part = w.gpart;
     g.part_cap = w.gpart_cap;
-    if (!gemm_add_products(g, A, nA, w.dyT, nt)) return BS_EINVAL;
+    if (h16) {
+      g.f16 = 1;
+      g.alpha_dev2 = w.inv + 0;
+    }
+    if (!gemm_add_products(g, A, nA, w.dyT, ntd, h16 && nA == 2 ? 1 : 2)) return BS_EINVAL;
     return launch_gemm(g, st);
   };
   // reference: dW = s val(C_u)^T dY
@@ -273,10 +333,10 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   if (p.weight_u) {
     pa.out[0] = w.resU[0];
     pa.out[1] = w.resU[1];
-    pa.out[2] = w.resU[2];
-    pa.nterms = 3;
+    pa.out[2] = h16 ? nullptr : w.resU[2];
+    pa.nterms = h16 ? 2 : 3;
     BS_TRY(launch_norm_planes(NP_RESU, pa, st));
-    BS_TRY(weight_gemm(w.resU, 3, w.bias_u, 1.0f, nullptr));
+    BS_TRY(weight_gemm(w.resU, pa.nterms, w.bias_u, 1.0f, h16 ? w.inv + 2 : nullptr));
   }
   for (int i = 0; i < 2; ++i) {
     if (!p.weight_n[i]) continue;
@@ -286,7 +346,7 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     pa.out[2] = nullptr;
     pa.nterms = K > 256 ? 2 : 1;
     BS_TRY(launch_norm_planes(NP_RESN, pa, st));
-    BS_TRY(weight_gemm(w.resN, pa.nterms, w.bias_n[i], 1.0f / (float)K, u_scale));
+    BS_TRY(weight_gemm(w.resN, pa.nterms, w.bias_n[i], 1.0f / (float)K / (h16 ? pa.resn_scale : 1.0f), u_scale));
   }
 
   // se of the weight use under N: per-trial contractions (trials stacked along the rows of
@@ -296,7 +356,8 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     const int bt = trial_batch(K);
     for (int k0 = 1; k0 <= K; k0 += bt) {
       const int nb = K - k0 + 1 < bt ? K - k0 + 1 : bt;
-      const TrialPlaneArgs ta{w.u, u_codes, u_scale, f, T, d, Tp, seed, use_w[i], k0, nb, w.tplanes};
+      TrialPlaneArgs ta{w.u, u_codes, u_scale, f, T, d, Tp, seed, use_w[i], k0, nb, w.tplanes};
+      ta.f16 = h16;
       BS_TRY(launch_trial_planes(ta, st));
       GemmArgs g{};
       g.M = (int)(nb * d);
@@ -308,8 +369,12 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       g.alpha = 1.0f;
       g.alpha_dev = u_scale;
       g.C = w.tdelta;
+      if (h16) {
+        g.f16 = 1;
+        g.alpha_dev2 = w.inv + 0;
+      }
       const u16* A0 = w.tplanes;
-      if (!gemm_add_products(g, &A0, 1, w.dyT, nt)) return BS_EINVAL;
+      if (!gemm_add_products(g, &A0, 1, w.dyT, ntd)) return BS_EINVAL;
       BS_TRY(launch_gemm(g, st));
       BS_TRY(launch_trial_accum(w.tdelta, nb, k0, d * n, w.td1, w.tS1, w.tS2, st));
     }
