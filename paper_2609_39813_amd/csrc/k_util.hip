@@ -273,16 +273,19 @@ bs_status launch_planes(const void* in, bs_dtype dt, int64_t R, int64_t C, int64
 // ------------------------------------------------------------------------------------
 __device__ __forceinline__ const float* move_at(const MoveSrc& m, int64_t t, int64_t c) {
   if (m.rows) return m.rows + t * m.ldi + c;
-  const int64_t which = c / m.d, cc = c - which * m.d;  // which of Q, K, V; the column in it
-  const int64_t b = t / m.S, s = t - b * m.S;
-  return m.heads[which] + (((b * m.H + (cc >> 6)) * m.S + s) << 6) + (cc & 63);
+  // 32-bit division (the launcher bounds rows and columns below 2^31)
+  const uint32_t which = (uint32_t)c / (uint32_t)m.d, cc = (uint32_t)c - which * (uint32_t)m.d;  // Q, K or V; column
+  const uint32_t b = (uint32_t)t / (uint32_t)m.S, s = (uint32_t)t - b * (uint32_t)m.S;
+  return m.heads[which] + ((((int64_t)b * m.H + (cc >> 6)) * m.S + s) << 6) + (cc & 63);
 }
 
+// BASE: the planes of base + move too (a second LDS tile)
+template <bool BASE>
 __global__ __launch_bounds__(256) void split_move_f16_kernel(MoveSrc src, const float* __restrict__ base, int64_t ldb,
                                                              int64_t R, int64_t C, F16Scale sc, PlaneOut tM,
                                                              PlaneOut tS, int64_t ldo, PlaneOut rows, int64_t ldr) {
   __shared__ float tile[64][65];
-  __shared__ float tileS[64][65];
+  __shared__ float tileS[BASE ? 64 : 1][65];
   const float a = amax_of_slots(sc.amax_a), b = sc.amax_b ? amax_of_slots(sc.amax_b) : 0.0f;
   const int e = f16_scale_exp(fmaxf(a, b)) - (sc.amax_b ? 1 : 0);
   const float scl = ldexpf(1.0f, e);
@@ -297,7 +300,7 @@ __global__ __launch_bounds__(256) void split_move_f16_kernel(MoveSrc src, const 
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f), w = v;
     if (in) {
       v = *(const float4*)move_at(src, r, c);
-      if (base) {
+      if (BASE) {
         const float4 g = *(const float4*)(base + r * ldb + c);
         w = make_float4(g.x + v.x, g.y + v.y, g.z + v.z, g.w + v.w);
       }
@@ -305,7 +308,7 @@ __global__ __launch_bounds__(256) void split_move_f16_kernel(MoveSrc src, const 
     const float x[4] = {v.x * scl, v.y * scl, v.z * scl, v.w * scl};
 #pragma unroll
     for (int q = 0; q < 4; ++q) tile[rr][4 * c4 + q] = x[q];
-    if (base) {
+    if (BASE) {
       tileS[rr][4 * c4 + 0] = w.x * scl;
       tileS[rr][4 * c4 + 1] = w.y * scl;
       tileS[rr][4 * c4 + 2] = w.z * scl;
@@ -343,7 +346,7 @@ __global__ __launch_bounds__(256) void split_move_f16_kernel(MoveSrc src, const 
     const int64_t c = c0 + cc;
     if (c >= C) continue;
     put(tile, tM, cc, c);
-    if (base) put(tileS, tS, cc, c);
+    if (BASE) put(tileS, tS, cc, c);
   }
 }
 
@@ -362,7 +365,7 @@ bs_status launch_split_move(const MoveSrc& m, const float* base, int64_t ldb, in
   } else {
     // head-major: 64-wide heads, C / d of Q, K, V, R = B S rows
     ok = ok && m.d > 0 && m.d % 64 == 0 && m.H * 64 == m.d && m.S > 0 && R % m.S == 0 && C % m.d == 0 &&
-         C / m.d <= 3;
+         C / m.d <= 3 && R < ((int64_t)1 << 31) && C < ((int64_t)1 << 31);
     for (int64_t i = 0; ok && i < C / m.d; ++i) ok = m.heads[i] && a16(m.heads[i]);
   }
   if (base) ok = ok && ldb % 4 == 0 && ldb >= C && a16(base) && a16(tS[0]) && a16(tS[1]);
@@ -372,7 +375,10 @@ bs_status launch_split_move(const MoveSrc& m, const float* base, int64_t ldb, in
   const PlaneOut ps{{base ? tS[0] : nullptr, base ? tS[1] : nullptr, nullptr}};
   const PlaneOut pr{{rows ? rows[0] : nullptr, rows ? rows[1] : nullptr, nullptr}};
   const dim3 grid((unsigned)((C + 63) / 64), (unsigned)(ldo / 64));
-  split_move_f16_kernel<<<grid, 256, 0, st>>>(m, base, ldb, R, C, sc, pm, ps, ldo, pr, ldr);
+  if (base)
+    split_move_f16_kernel<true><<<grid, 256, 0, st>>>(m, base, ldb, R, C, sc, pm, ps, ldo, pr, ldr);
+  else
+    split_move_f16_kernel<false><<<grid, 256, 0, st>>>(m, base, ldb, R, C, sc, pm, ps, ldo, pr, ldr);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

@@ -36,19 +36,22 @@ constexpr int DH = 64;
 constexpr float kAttnScale = 0.125f;  // 1 / sqrt(64)
 enum { G_DX = 0, G_DGAIN1, G_DWQKV, G_DWO, G_DGAIN2, G_DWG, G_DWU, G_DWD, NGRAD };
 constexpr int NCOMP = 4;  // gradients formed here per trial: dx, dgain1, dWqkv, dWo
-constexpr int NB = 4;     // N trials per update of the shifted sums (one read-modify-write per NB)
+constexpr int NB = 16;    // N trials per update of the shifted sums (one read-modify-write per NB)
 constexpr int KCH = 16;   // N trials per chunk of the batched weight-use contractions (a multiple of NB)
 // maxima (slot arrays) of the scaled fp16 operands: per call dh, dQKV, Wo, Wqkv, V, Q, K; per pass
 // the moves dh_d, dQKV_d, dO_d, D_d
 enum { AM_DH, AM_DQKV, AM_WO, AM_WQKV, AM_V, AM_Q, AM_K, AM_DHD, AM_DQKVD, AM_DOD, AM_DDD, AM_N };
-// their 2^-e: the splits of dh_d, dQKV_d, Wo, Wqkv, dh, dQKV; then the attention backward's seven
-// in its order (dO_d, V, Q, K, dS's 2^s, 2^-s-q, 2^-s-k)
-enum { IV_DHD, IV_DQKVD, IV_WO, IV_WQKV, IV_DH, IV_DQKV, IV_DOD, IV_V, IV_Q, IV_K, IV_DS, IV_DKM, IV_DQM, IV_N };
+// their 2^-e: the splits of dh_d, dQKV_d, Wo, Wqkv, dh, dQKV, the U residuals of O and u1; then
+// the attention backward's seven in its order (dO_d, V, Q, K, dS's 2^s, 2^-s-q, 2^-s-k)
+enum {
+  IV_DHD, IV_DQKVD, IV_WO, IV_WQKV, IV_DH, IV_DQKV, IV_RO, IV_RU,
+  IV_DOD, IV_V, IV_Q, IV_K, IV_DS, IV_DKM, IV_DQM, IV_N
+};
 
 struct AlluWs {
   float *u1, *u2, *r1, *r2, *du1, *du2, *m, *l;
-  u16 *Vt, *Qt, *Kt, *valT_u1, *valT_O, *dqkvT[3], *dhT[3];
-  u16 *pA[3], *rows3[3], *tB[3], *dOp[3], *dOt[3];
+  u16 *Vt, *Qt, *Kt, *valT_u1, *valT_O;
+  u16 *pA[2], *rows3[3], *tB[3], *dOp[3], *dOt[3];
   u16 *tH[2], *tQ[2];    // dh, dQKV as scaled two-term fp16 splits, transposed
   u16 *pAn[2], *pWn[2];  // a chunk of N trials' difference and value planes at O's and u1's weight uses
   float *dWo_n, *dWqkv_n;  // the chunk's weight-use moves [KCH][d][d], [KCH][d][3d]
@@ -56,7 +59,8 @@ struct AlluWs {
   u16 *Wo16, *Wqkv16, *V16;  // the weights and V as scaled fp16 (the moves' contractions)
   u16 *Q16, *K16, *Qt16, *Kt16;  // Q, K as scaled fp16 and their transposed copies
   double* gpart;
-  float* delta[NCOMP];      // the passes' moves, [NB][n] (N's trial k in row (k - 1) % NB)
+  float* delta[NCOMP];      // the passes' moves: dx, dgain1 [min(K, NB)][n] (N's trial k in row
+                            // (k - 1) % NB); dWqkv, dWo [1][n] (U, R; N's are in the chunk buffers)
   float* bias[3][NCOMP];    // per letter
   float* se_n[NCOMP];       // N's se
   float *d1[NCOMP];
@@ -84,9 +88,7 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F, int K) {
   w.valT_u1 = c.take<u16>(d * Tp);
   w.valT_O = c.take<u16>(d * Tp);
   for (int i = 0; i < 3; ++i) {
-    w.dqkvT[i] = c.take<u16>(d3 * Tp);
-    w.dhT[i] = c.take<u16>(d * Tp);
-    w.pA[i] = c.take<u16>(d * Tp);
+    if (i < 2) w.pA[i] = c.take<u16>(d * Tp);
     w.rows3[i] = c.take<u16>(T * std::max(F2, d3));
     w.tB[i] = c.take<u16>(d3 * Tp);
     w.dOp[i] = c.take<u16>(Td);
@@ -114,7 +116,7 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F, int K) {
   w.dWqkv_n = c.take<float>(kc * d * d3);
   w.gpart = c.take<double>(3 * ((T + 15) / 16) * (int64_t)d);
   for (int i = 0; i < NCOMP; ++i) {
-    w.delta[i] = c.take<float>(NB * nc[i]);
+    w.delta[i] = c.take<float>((i < 2 ? std::max(1, std::min(K, NB)) : 1) * nc[i]);
     for (int l = 0; l < 3; ++l) w.bias[l][i] = c.take<float>(nc[i]);
     w.se_n[i] = c.take<float>(nc[i]);
     w.d1[i] = c.take<float>(nc[i]);
@@ -154,8 +156,8 @@ struct Gemm {
     g.alpha_dev = alpha_dev;
     g.C = C;
   }
-  Gemm& add(const u16* const* A, int nA, const u16* const* B, int nB) {
-    ok = ok && gemm_add_products(g, A, nA, B, nB);
+  Gemm& add(const u16* const* A, int nA, const u16* const* B, int nB, int maxsum = 2) {
+    ok = ok && gemm_add_products(g, A, nA, B, nB, maxsum);
     return *this;
   }
   bs_status run(float* part, int64_t cap, hipStream_t st) {
@@ -248,8 +250,6 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
     u16* dst[2] = {w.Qt16, w.Kt16};
     BS_TRY(launch_attn_transpose(src, dst, 2, (int)bh, S, (int)Sp, st));
   }
-  BS_TRY(launch_planes(io.dqkv, BS_F32, T, d3, d3, true, w.dqkvT, 3, Tp, 1.0f, st));
-  BS_TRY(launch_planes(io.dh, BS_F32, T, d, d, true, w.dhT, 3, Tp, 1.0f, st));
   // dh and dQKV as scaled two-term fp16 splits: under N a weight use's move is
   // W_k^T g_d + (W_k - W_q)^T g (g the reference incoming gradient, g_d its move, W_k the trial's
   // new rounding, W_q the forward's), and the second products of a chunk of trials are one
@@ -321,8 +321,14 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       const F16Scale sc_q{w.amax[AM_DQKVD], nullptr, w.inv + IV_DQKVD};
       // O's weight use (Wo)
       if (l == LETTER_U) {
-        BS_TRY(planes_of(NP_RESU, io.Otok, io.c_Otok, s_O, w.pA, 3));
-        BS_TRY(Gemm(d, d, (int)Tp, Tp, Tp, dWo, d, nullptr).add(w.pA, 3, w.dhT, 3).run(w.part, w.part_cap, st));
+        // (u - s val)^T dh: the residual's scaled fp16 split against dh's
+        pa.f16 = 1;
+        pa.inv_out = w.inv + IV_RO;
+        BS_TRY(planes_of(NP_RESU, io.Otok, io.c_Otok, s_O, w.pA, 2));
+        Gemm gr(d, d, (int)Tp, Tp, Tp, dWo, d, w.inv + IV_RO);
+        gr.g.f16 = 1;
+        gr.g.alpha_dev2 = w.inv + IV_DH;
+        BS_TRY(gr.add(w.pA, 2, w.tH, 2, 1).run(w.part, w.part_cap, st));
       } else {
         // dh_d's transposed planes (the weight use) and row planes (the move of dO), one read; the
         // weight use's move: val^T dh_d (N: added to the chunk's difference product)
@@ -345,9 +351,14 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       }
       // the D use: U reads the original and dO does not move: no move downstream of it
       if (l == LETTER_U) {
-        BS_TRY(planes_of(NP_RESU, w.u1, io.c_u1, s_u1, w.pA, 3));
-        BS_TRY(Gemm(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, nullptr).add(w.pA, 3, w.dqkvT, 3)
-                   .run(w.part, w.part_cap, st));
+        pa.inv_out = w.inv + IV_RU;
+        BS_TRY(planes_of(NP_RESU, w.u1, io.c_u1, s_u1, w.pA, 2));
+        pa.f16 = 0;
+        pa.inv_out = nullptr;
+        Gemm gr(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, w.inv + IV_RU);
+        gr.g.f16 = 1;
+        gr.g.alpha_dev2 = w.inv + IV_DQKV;
+        BS_TRY(gr.add(w.pA, 2, w.tQ, 2, 1).run(w.part, w.part_cap, st));
         BS_TRY(launch_fill(dl[0], Td, 0.0f, st));
         BS_TRY(launch_fill(dl[1], d, 0.0f, st));
       } else {
