@@ -220,6 +220,7 @@ struct LayerWs {
   size_t sub_bytes;
   void* allu;  // the every-use-at-once check (nullptr when not asked for)
   size_t allu_bytes;
+  float *n_u1, *n_u2, *n_du1, *n_du2, *n_r1, *n_r2;  // every use at once: u, du, rstd of u1 and u2
 };
 
 size_t sub_ws_size(int B, int S, int d, int H, int F, int K, bool se) {
@@ -303,6 +304,9 @@ LayerWs carve_layer(Carver& c, int B, int S, int d, int H, int F, int K, bool al
   if (all_uses) {
     w.allu_bytes = allu_ws_size(B, S, d, H, F, K);
     w.allu = c.take<char>(w.allu_bytes);
+    // the normalization operands the per-use runs hand to the every-use check
+    for (float** q : {&w.n_u1, &w.n_u2, &w.n_du1, &w.n_du2}) *q = c.take<float>(Td);
+    for (float** q : {&w.n_r1, &w.n_r2}) *q = c.take<float>(T);
   }
   return w;
 }
@@ -442,10 +446,15 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
   }
   BS_TRY(launch_swiglu_bwd(w.da, gh, w.dgh, T, F, st));
   // store u2: gain, weight ([Wg | Wu]) and normalization-input uses (incoming gradient [dg | dhh])
-  const NormIO b2{h, BS_F32, wt->gain2, w.Wgu, BS_BF16, w.dgh, BS_F32, T, d, 2 * (int64_t)F, eps, fmt, fwd_mode,
-                  npol, NPOL, K, seed, 2, nullptr, c_u2, scales + 2, dgain2, w.dWgu, w.dxn2,
-                  bs_est{nullptr, w.e2.g_bias, w.e2.g_se}, bs_est{nullptr, w.e2.w_bias, w.e2.w_se},
-                  bs_est{nullptr, w.e2.x_bias, nullptr}, dg + 2};
+  NormIO b2{h, BS_F32, wt->gain2, w.Wgu, BS_BF16, w.dgh, BS_F32, T, d, 2 * (int64_t)F, eps, fmt, fwd_mode,
+            npol, NPOL, K, seed, 2, nullptr, c_u2, scales + 2, dgain2, w.dWgu, w.dxn2,
+            bs_est{nullptr, w.e2.g_bias, w.e2.g_se}, bs_est{nullptr, w.e2.w_bias, w.e2.w_se},
+            bs_est{nullptr, w.e2.x_bias, nullptr}, dg + 2};
+  if (all) {
+    b2.u_out = w.n_u2;
+    b2.rstd_out = w.n_r2;
+    b2.du_out = w.n_du2;
+  }
   BS_TRY(norm_run(b2, w.sub, w.sub_bytes, st));
   BS_TRY(launch_add(dOut, BS_BF16, w.dxn2, w.dh, Td, st));
   // store O, weight use of Wo (incoming gradient dh)
@@ -478,10 +487,15 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
   BS_TRY(attn_run(ba, w.sub, w.sub_bytes, st));
   BS_TRY(launch_dqkv_tokens(w.dQ, w.dK, w.dV, w.dqkv, B, S, H, DH, st));
   // store u1: gain, weight (Wqkv) and normalization-input uses (incoming gradient dQKV)
-  const NormIO b1{x, BS_BF16, wt->gain1, wt->Wqkv, BS_BF16, w.dqkv, BS_F32, T, d, 3 * (int64_t)d, eps, fmt, fwd_mode,
-                  npol, NPOL, K, seed, 0, nullptr, c_u1, scales + 0, dgain1, dWqkv, w.dxn1,
-                  bs_est{nullptr, w.e1.g_bias, w.e1.g_se}, bs_est{nullptr, w.e1.w_bias, w.e1.w_se},
-                  bs_est{nullptr, w.e1.x_bias, nullptr}, dg + 0};
+  NormIO b1{x, BS_BF16, wt->gain1, wt->Wqkv, BS_BF16, w.dqkv, BS_F32, T, d, 3 * (int64_t)d, eps, fmt, fwd_mode,
+            npol, NPOL, K, seed, 0, nullptr, c_u1, scales + 0, dgain1, dWqkv, w.dxn1,
+            bs_est{nullptr, w.e1.g_bias, w.e1.g_se}, bs_est{nullptr, w.e1.w_bias, w.e1.w_se},
+            bs_est{nullptr, w.e1.x_bias, nullptr}, dg + 0};
+  if (all) {
+    b1.u_out = w.n_u1;
+    b1.rstd_out = w.n_r1;
+    b1.du_out = w.n_du1;
+  }
   BS_TRY(norm_run(b1, w.sub, w.sub_bytes, st));
   float* dx = grads.dx ? grads.dx : w.dx;
   if (grads.dx || all) BS_TRY(launch_add(w.dh, BS_F32, w.dxn1, dx, Td, st));
@@ -559,6 +573,12 @@ bs_status bs_decoder_layer_policy(const void* x, const bs_layer_weights* wt, con
     ai.dh = w.dh;
     ai.dOh = w.dOh;
     ai.dqkv = w.dqkv;
+    ai.u1 = w.n_u1;
+    ai.u2 = w.n_u2;
+    ai.r1 = w.n_r1;
+    ai.r2 = w.n_r2;
+    ai.du1 = w.n_du1;
+    ai.du2 = w.n_du2;
     const float* refs[8] = {dx, dgain1, dWqkv, dWo, dgain2, w.dWgu, nullptr, dWd};
     for (int i = 0; i < 8; ++i) ai.ref[i] = refs[i];
     ai.wd_bias = w.wd_bias;

@@ -63,10 +63,11 @@ bs_status launch_allu_dx(const AlluDxArgs<XT>& a, hipStream_t st);
 struct AlluDArgs {
   StoreRead rd;
   const float* dO;   // [rows][64] the reference incoming gradient at the D use
-  const float* ddO;  // nullable [rows][64]
+  const float* ddO;  // nullable [rows][64], or with ddo_heads > 0 token-major [B][S][ddo_heads 64]
   int64_t rows;
   float* out;        // [rows]
   uint32_t* amax = nullptr;  // nullable: slots (AMAX_SLOTS) raised to max |out|
+  int ddo_heads = 0, ddo_S = 0;  // ddO token-major: heads and sequence length (row = (b H + h) S + s)
 };
 bs_status launch_allu_d(const AlluDArgs& a, hipStream_t st);
 

@@ -185,10 +185,15 @@ __global__ __launch_bounds__(256) void allu_d_kernel(AlluDArgs a) {
     const float s = *a.rd.scale;
     const double rs = 1.0 / (double)s;
     const int64_t e = row * 64 + 4 * sub;
+    int64_t ed = e;  // ddO's element
+    if (a.ddo_heads > 0) {
+      const int64_t bh = row / a.ddo_S, s = row - bh * a.ddo_S;
+      ed = (((bh / a.ddo_heads) * a.ddo_S + s) * a.ddo_heads + bh % a.ddo_heads) * 64 + 4 * sub;
+    }
     float o[4], dO[4], ddO[4] = {0.f, 0.f, 0.f, 0.f};
     load4(a.rd.x, e, o);
     load4(a.dO, e, dO);
-    if (a.ddO) load4(a.ddO, e, ddO);
+    if (a.ddO) load4(a.ddO, ed, ddO);
     double v[4];
     read4(a.rd, e, o, rs, s, v);
 #pragma unroll
@@ -250,6 +255,7 @@ template bs_status launch_allu_dx<float>(const AlluDxArgs<float>&, hipStream_t);
 template bs_status launch_allu_dx<u16>(const AlluDxArgs<u16>&, hipStream_t);
 
 bs_status launch_allu_d(const AlluDArgs& a, hipStream_t st) {
+  if (a.ddo_heads < 0 || (a.ddo_heads > 0 && (a.ddo_S <= 0 || a.rows % a.ddo_S))) return BS_EINVAL;
   if (a.rows <= 0) return BS_OK;
   allu_d_kernel<<<(unsigned)((a.rows + 15) / 16), 256, 0, st>>>(a);
   BS_CHECK_LAUNCH();

@@ -95,9 +95,10 @@ bs_status launch_attn_transpose(const u16* const* X, u16* const* Xt, int n, int 
 bs_status launch_attn_split(const float* dO32, int BH, int S, int Sp, u16* const* dOp, u16* const* dOt,
                             hipStream_t st);
 // the two fp16 planes (split2_f16) of dO32 2^e, e from the max in slots (an AMAX_SLOTS array,
-// f16_scale_exp), and their transposes; 2^-e to inv_out
-bs_status launch_attn_split_f16(const float* dO32, int BH, int S, int Sp, const uint32_t* slots, float* inv_out,
-                                u16* const* dOp, u16* const* dOt, hipStream_t st);
+// f16_scale_exp), and their transposes (head-major [BH][S][64] planes); 2^-e to inv_out. dO32 is
+// head-major, or with htok > 0 token-major [BH / htok][S][htok 64] (htok heads)
+bs_status launch_attn_split_f16(const float* dO32, int BH, int S, int Sp, int htok, const uint32_t* slots,
+                                float* inv_out, u16* const* dOp, u16* const* dOt, hipStream_t st);
 // dS's scale of the fp16 backward (f16_inv above, entries 4..6 from entries 2, 3): 2^s from the
 // bound 64 max|dO| max|V| + max|D| of |dS| = P |dP - D| (P <= 1, 64 terms per dP), the maxima
 // held in the slot arrays (AMAX_SLOTS) sdO, sV, sD

@@ -714,9 +714,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
 // tperm) of bf16 X [BH][S][64]; for an fp32 X, its three bf16 planes (row-major) and their
 // transposes
 // ------------------------------------------------------------------------------------
-// H (fp32 x): the two fp16 terms (split2_f16) of x 2^e, e from the max in slots, 2^-e to inv_out
+// H (fp32 x): the two fp16 terms (split2_f16) of x 2^e, e from the max in slots, 2^-e to inv_out;
+// htok > 0: x is token-major [B][S][htok 64] (row s of head bh at ((b S + s) htok + h) 64)
 template <typename X, bool H>
-__global__ __launch_bounds__(256) void attn_prep_kernel(const X* __restrict__ x, int S, int Sp,
+__global__ __launch_bounds__(256) void attn_prep_kernel(const X* __restrict__ x, int S, int Sp, int htok,
                                                         const uint32_t* __restrict__ slots, float* __restrict__ inv_out,
                                                         u16* __restrict__ xt0,
                                                         u16* __restrict__ xt1, u16* __restrict__ xt2,
@@ -732,15 +733,18 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(const X* __restrict__ x,
   }
   const int r0 = blockIdx.x * AT, bh = blockIdx.y;
   const int64_t hb = (int64_t)bh * S * AT, tb = (int64_t)bh * AT * Sp;
+  // source row stride and origin of this head's rows
+  const int64_t xs = htok > 0 ? (int64_t)htok * AT : AT;
+  const int64_t xb = htok > 0 ? ((int64_t)(bh / htok) * S * htok + bh % htok) * AT : hb;
   u16* const xp[3] = {xp0, xp1, xp2};
   u16* const xt[3] = {xt0, xt1, xt2};
   for (int e = threadIdx.x; e < AT * AT; e += 256) {
     const int r = e >> 6, c = e & 63;
     const bool ok = r0 + r < S;
     if constexpr (NP == 1) {
-      t[0][r][c] = ok ? (u16)x[hb + (int64_t)(r0 + r) * AT + c] : (u16)0;
+      t[0][r][c] = ok ? (u16)x[xb + (int64_t)(r0 + r) * xs + c] : (u16)0;
     } else {
-      const float v = ok ? load_f32(x, hb + (int64_t)(r0 + r) * AT + c) : 0.0f;
+      const float v = ok ? load_f32(x, xb + (int64_t)(r0 + r) * xs + c) : 0.0f;
       u16 h[3];
       if constexpr (H)
         split2_f16(v * scl, h[0], h[1]);
@@ -1019,8 +1023,8 @@ bs_status launch_attn_split(const float* dO32, int BH, int S, int Sp, u16* const
                             hipStream_t st) {
   dim3 grid((unsigned)(Sp / AT), (unsigned)BH);
   ProfScope prof("attn_prep", st);
-  attn_prep_kernel<float, false><<<grid, 256, 0, st>>>(dO32, S, Sp, nullptr, nullptr, dOt[0], dOt[1], dOt[2], dOp[0],
-                                                       dOp[1], dOp[2]);
+  attn_prep_kernel<float, false><<<grid, 256, 0, st>>>(dO32, S, Sp, 0, nullptr, nullptr, dOt[0], dOt[1], dOt[2],
+                                                       dOp[0], dOp[1], dOp[2]);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
@@ -1039,13 +1043,13 @@ bs_status launch_attn_f16_scales(const uint32_t* sdO, const uint32_t* sV, const 
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
-bs_status launch_attn_split_f16(const float* dO32, int BH, int S, int Sp, const uint32_t* slots, float* inv_out,
-                                u16* const* dOp, u16* const* dOt, hipStream_t st) {
-  if (!slots || !dO32) return BS_EINVAL;
+bs_status launch_attn_split_f16(const float* dO32, int BH, int S, int Sp, int htok, const uint32_t* slots,
+                                float* inv_out, u16* const* dOp, u16* const* dOt, hipStream_t st) {
+  if (!slots || !dO32 || htok < 0 || (htok > 0 && BH % htok)) return BS_EINVAL;
   dim3 grid((unsigned)(Sp / AT), (unsigned)BH);
   ProfScope prof("attn_prep", st);
-  attn_prep_kernel<float, true><<<grid, 256, 0, st>>>(dO32, S, Sp, slots, inv_out, dOt[0], dOt[1], nullptr, dOp[0],
-                                                      dOp[1], nullptr);
+  attn_prep_kernel<float, true><<<grid, 256, 0, st>>>(dO32, S, Sp, htok, slots, inv_out, dOt[0], dOt[1], nullptr,
+                                                      dOp[0], dOp[1], nullptr);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }

@@ -19,6 +19,9 @@ struct AlluIO {
   const float *O, *Otok, *h, *a;  // O head-major, O token-major, h [T][d], a [T][F]
   const uint8_t *c_u1, *c_O, *c_Otok, *c_u2, *c_a;
   const float* scales;     // [4] u1, O, u2, a
+  // the per-use check's normalization operands: u1, u2 [T][d], their inverse rms [T], and du at
+  // u1 and u2 (dQKV Wqkv^T, [dg | dhh] Wgu^T) [T][d]
+  const float *u1, *u2, *r1, *r2, *du1, *du2;
   const float *dgh, *dh, *dOh, *dqkv;  // reference incoming gradients: [T][2F], [T][d], head-major [T][d], [T][3d]
   // the reference gradients and the per-use biases of the uses whose incoming gradient is the
   // reference's whatever the letter (their means over the same draws are the per-use ones)

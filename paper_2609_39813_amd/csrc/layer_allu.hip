@@ -49,13 +49,13 @@ enum {
 };
 
 struct AlluWs {
-  float *u1, *u2, *r1, *r2, *du1, *du2, *m, *l;
+  float *m, *l;
   u16 *Vt, *Qt, *Kt, *valT_u1, *valT_O;
   u16 *pA[2], *rows3[3], *tB[3], *dOp[3], *dOt[3];
   u16 *tH[2], *tQ[2];    // dh, dQKV as scaled two-term fp16 splits, transposed
   u16 *pAn[2], *pWn[2];  // a chunk of N trials' difference and value planes at O's and u1's weight uses
   float *dWo_n, *dWqkv_n;  // the chunk's weight-use moves [KCH][d][d], [KCH][d][3d]
-  float *dh_d, *dO_dt, *dO_dh, *dD, *dQ_d, *dK_d, *dV_d, *du1_d;
+  float *dh_d, *dO_dt, *dD, *dQ_d, *dK_d, *dV_d, *du1_d;
   u16 *Wo16, *Wqkv16, *V16;  // the weights and V as scaled fp16 (the moves' contractions)
   u16 *Q16, *K16, *Qt16, *Kt16;  // Q, K as scaled fp16 and their transposed copies
   double* gpart;
@@ -69,7 +69,6 @@ struct AlluWs {
   float* part;
   int64_t part_cap;
   double* sumsq_part;
-  bs_diag* diag;
   uint32_t* amax[AM_N];  // slot arrays (AMAX_SLOTS) of max |.|
   float* inv;            // [IV_N]
 };
@@ -80,8 +79,6 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F, int K) {
   const int64_t T = (int64_t)B * S, Td = T * d, Tp = round_up(T > 0 ? T : 1, 64), bh = (int64_t)B * H;
   const int64_t Sp = round_up(S, 64), d3 = 3 * (int64_t)d, F2 = 2 * (int64_t)F;
   const int64_t nc[NCOMP] = {Td, d, (int64_t)d * d3, (int64_t)d * d};
-  for (float** p : {&w.u1, &w.u2, &w.du1, &w.du2}) *p = c.take<float>(Td);
-  for (float** p : {&w.r1, &w.r2}) *p = c.take<float>(T);
   w.m = c.take<float>(bh * S);
   w.l = c.take<float>(bh * S);
   for (u16** p : {&w.Vt, &w.Qt, &w.Kt}) *p = c.take<u16>(bh * DH * Sp);
@@ -94,7 +91,7 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F, int K) {
     w.dOp[i] = c.take<u16>(Td);
     w.dOt[i] = c.take<u16>(bh * DH * Sp);
   }
-  for (float** p : {&w.dh_d, &w.dO_dt, &w.dO_dh, &w.du1_d}) *p = c.take<float>(Td);
+  for (float** p : {&w.dh_d, &w.dO_dt, &w.du1_d}) *p = c.take<float>(Td);
   w.dQ_d = c.take<float>(3 * Td);  // dQ, dK, dV of the move, one block (one max over the three)
   w.dK_d = w.dQ_d ? w.dQ_d + Td : nullptr;
   w.dV_d = w.dQ_d ? w.dQ_d + 2 * Td : nullptr;
@@ -133,7 +130,6 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F, int K) {
   w.part_cap = 8 * (int64_t)d * d3;  // split-K partials of the few-tile weight contractions
   w.part = c.take<float>(w.part_cap);
   w.sumsq_part = c.take<double>(sumsq_part_size());
-  w.diag = c.take<bs_diag>(1);
   {
     uint32_t* a = c.take<uint32_t>(AM_N * AMAX_SLOTS * AMAX_STRIDE);
     for (int i = 0; i < AM_N; ++i) w.amax[i] = a ? a + i * AMAX_SLOTS * AMAX_STRIDE : nullptr;
@@ -196,13 +192,7 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   const float *s_u1 = io.scales + 0, *s_O = io.scales + 1, *s_u2 = io.scales + 2;
 
   // ---- fixed: the stores' inputs and inverse rms, du at u1 and u2, the attention rows ----
-  BS_TRY(launch_init_diag(w.diag, st));
-  BS_TRY(launch_rmsnorm_fwd(io.x, BS_BF16, io.gain1, T, d, io.eps, w.u1, w.r1, w.diag, st));
-  BS_TRY(launch_rmsnorm_fwd(io.h, BS_F32, io.gain2, T, d, io.eps, w.u2, w.r2, w.diag, st));
-  BS_TRY(launch_planes(io.dgh, BS_F32, T, F2, F2, false, w.rows3, 3, F2, 1.0f, st));
-  BS_TRY(Gemm((int)T, d, (int)F2, F2, F2, w.du2, d, nullptr).add(w.rows3, 3, &io.Wgu, 1).run(nullptr, 0, st));
-  BS_TRY(launch_planes(io.dqkv, BS_F32, T, d3, d3, false, w.rows3, 3, d3, 1.0f, st));
-  BS_TRY(Gemm((int)T, d, (int)d3, d3, d3, w.du1, d, nullptr).add(w.rows3, 3, &io.Wqkv, 1).run(nullptr, 0, st));
+  if (!io.u1 || !io.u2 || !io.r1 || !io.r2 || !io.du1 || !io.du2) return BS_EINVAL;
   {
     const u16* src[3] = {io.V, io.Q, io.Kk};
     u16* dst[3] = {w.Vt, w.Qt, w.Kt};
@@ -229,7 +219,7 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   // the R and N weight uses contract fp16 operands: FP8 values (exact in fp16) against the scaled
   // two-term fp16 split of the incoming gradient and its move
   pa.f16 = 1;
-  BS_TRY(planes_of(NP_VAL, w.u1, io.c_u1, s_u1, &w.valT_u1, 1));
+  BS_TRY(planes_of(NP_VAL, io.u1, io.c_u1, s_u1, &w.valT_u1, 1));
   BS_TRY(planes_of(NP_VAL, io.Otok, io.c_Otok, s_O, &w.valT_O, 1));
   pa.f16 = 0;
   BS_TRY(launch_fill2d((float*)w.amax[0], AM_N * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
@@ -285,7 +275,7 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         to.f16 = 1;
         to.outW = w.pWn[0];
         BS_TRY(launch_trial_planes(to, st));
-        TrialPlaneArgs tu{w.u1, io.c_u1, s_u1, f, T, d, Tp, io.seed, 0 * 256 + 2, k, nbk, w.pAn[1]};
+        TrialPlaneArgs tu{io.u1, io.c_u1, s_u1, f, T, d, Tp, io.seed, 0 * 256 + 2, k, nbk, w.pAn[1]};
         tu.f16 = 1;
         tu.outW = w.pWn[1];
         BS_TRY(launch_trial_planes(tu, st));
@@ -312,7 +302,7 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       // u2's normalization-input use: the move of dh (and its max |.|)
       if (l != LETTER_U) {
         BS_TRY(launch_fill2d((float*)w.amax[AM_DHD], (AM_N - AM_DHD) * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
-        AlluDxArgs<float> ax{io.h, w.r2, io.gain2, rd(w.u2, io.c_u2, s_u2, 2 * 256 + 3), w.du2, nullptr,
+        AlluDxArgs<float> ax{io.h, io.r2, io.gain2, rd(io.u2, io.c_u2, s_u2, 2 * 256 + 3), io.du2, nullptr,
                              nullptr, T, d, w.dh_d};
         ax.amax = w.amax[AM_DHD];
         BS_TRY(launch_allu_dx(ax, st));
@@ -341,18 +331,17 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         gw.g.alpha_dev2 = w.inv + IV_DHD;
         gw.g.accumulate = l == LETTER_N;
         BS_TRY(gw.add(&valO, 1, w.tB, 2).run(w.part, w.part_cap, st));
-        // the move of dO (token-major, then head-major)
+        // the move of dO (token-major: the D use and the attention operands read it so)
         Gemm gm((int)T, d, d, d, d, w.dO_dt, d, w.inv + IV_WO);
         gm.g.f16 = 1;
         gm.g.alpha_dev2 = w.inv + IV_DHD;
         gm.g.amax = w.amax[AM_DOD];
         BS_TRY(gm.add(w.rows3, 2, &w.Wo16, 1).run(nullptr, 0, st));
-        BS_TRY(launch_heads_tokens_f32(w.dO_dt, w.dO_dh, B, S, H, DH, false, st));
       }
       // the D use: U reads the original and dO does not move: no move downstream of it
       if (l == LETTER_U) {
         pa.inv_out = w.inv + IV_RU;
-        BS_TRY(planes_of(NP_RESU, w.u1, io.c_u1, s_u1, w.pA, 2));
+        BS_TRY(planes_of(NP_RESU, io.u1, io.c_u1, s_u1, w.pA, 2));
         pa.f16 = 0;
         pa.inv_out = nullptr;
         Gemm gr(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, w.inv + IV_RU);
@@ -362,11 +351,14 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         BS_TRY(launch_fill(dl[0], Td, 0.0f, st));
         BS_TRY(launch_fill(dl[1], d, 0.0f, st));
       } else {
-        AlluDArgs ad{rd(io.O, io.c_O, s_O, 1 * 256 + 1), io.dOh, w.dO_dh, rows_h, w.dD};
+        AlluDArgs ad{rd(io.O, io.c_O, s_O, 1 * 256 + 1), io.dOh, w.dO_dt, rows_h, w.dD};
         ad.amax = w.amax[AM_DDD];
+        ad.ddo_heads = H;
+        ad.ddo_S = S;
         BS_TRY(launch_allu_d(ad, st));
         // dO_d as the scaled two-term fp16 split (V as scaled fp16) for the attention backward
-        BS_TRY(launch_attn_split_f16(w.dO_dh, (int)bh, S, (int)Sp, w.amax[AM_DOD], w.inv + IV_DOD, w.dOp, w.dOt, st));
+        BS_TRY(launch_attn_split_f16(w.dO_dt, (int)bh, S, (int)Sp, H, w.amax[AM_DOD], w.inv + IV_DOD, w.dOp, w.dOt,
+                                     st));
         BS_TRY(launch_attn_f16_scales(w.amax[AM_DOD], w.amax[AM_V], w.amax[AM_DDD], w.inv + IV_DOD, st));
         AttnBwdArgs ba{};
         ba.Qt = w.Qt;
@@ -379,7 +371,7 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         ba.Q = io.Q;
         ba.K = io.Kk;
         ba.V = io.V;
-        ba.dO32 = w.dO_dh;
+        ba.dO32 = nullptr;  // the fp16 planes carry dO_d
         ba.V16 = w.V16;
         ba.Qt16 = w.Qt16;
         ba.Kt16 = w.Kt16;
@@ -417,11 +409,11 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         gu.g.f16 = 1;
         gu.g.alpha_dev2 = w.inv + IV_DQKVD;
         BS_TRY(gu.add(w.rows3, 2, &w.Wqkv16, 1).run(nullptr, 0, st));
-        const AlluGainArgs<u16> ag{io.x, w.r1, io.gain1, rd(w.u1, io.c_u1, s_u1, 0 * 256 + 1), w.du1, w.du1_d, T, d,
+        const AlluGainArgs<u16> ag{io.x, io.r1, io.gain1, rd(io.u1, io.c_u1, s_u1, 0 * 256 + 1), io.du1, w.du1_d, T, d,
                                    w.gpart};
         BS_TRY(launch_allu_gain(ag, st));
         BS_TRY(launch_gain_final(w.gpart, (T + 15) / 16, d, dl[1], nullptr, nullptr, st));
-        const AlluDxArgs<u16> ax{io.x, w.r1, io.gain1, rd(w.u1, io.c_u1, s_u1, 0 * 256 + 3), w.du1, w.du1_d, w.dh_d,
+        const AlluDxArgs<u16> ax{io.x, io.r1, io.gain1, rd(io.u1, io.c_u1, s_u1, 0 * 256 + 3), io.du1, w.du1_d, w.dh_d,
                                  T, d, dl[0]};
         BS_TRY(launch_allu_dx(ax, st));
       }

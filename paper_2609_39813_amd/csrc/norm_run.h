@@ -25,7 +25,9 @@ struct NormIO {
   float *dgain_ref, *dW_ref, *dX_ref;
   bs_est dgain, dW, dX;
   bs_diag* diag;
-  float* u_out = nullptr;  // optional: the fp32 quantizer input u [T][d]
+  float* u_out = nullptr;     // optional: the fp32 quantizer input u [T][d]
+  float* rstd_out = nullptr;  // optional: the inverse rms per row [T]
+  float* du_out = nullptr;    // optional: the incoming gradient at u, du = dY W^T [T][d]
 };
 
 size_t norm_ws_size(int64_t T, int64_t d, int64_t n, int K);

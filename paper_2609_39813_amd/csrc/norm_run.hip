@@ -172,6 +172,8 @@ bs_status norm_run(const NormIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
   if (!ws || ((uintptr_t)ws & 255) || ws_bytes < probe.used()) return BS_EWORKSPACE;
   Carver c(ws, ws_bytes);
   NormWs w = carve_norm(c, T, d, n, K, wt, gt, p, Y != nullptr);
+  if (io.rstd_out) w.rstd = io.rstd_out;
+  if (io.du_out) w.du = io.du_out;
 
   const int64_t Tp = round_up(T > 0 ? T : 1, 64);
   const int nt = gt == BS_F32 ? 3 : 1, ntw = wt == BS_F32 ? 3 : 1;
