@@ -23,22 +23,27 @@ struct GemmArgs {
   const float* alpha_dev2 = nullptr;  // nullable: a second device multiplier of alpha
   uint32_t* amax = nullptr;  // nullable: slots (AMAX_SLOTS) raised to max |C| of the values written
                              // (C's new values, accumulate = 0 only; the pipelined kernel only)
+  // batch > 1: that many independent contractions, z = 0 .. batch - 1, each with every segment's
+  // A and B offset by z sA, z sB elements, C by z sC and alpha_dev2 by z s_alpha2 (no split-K;
+  // the pipelined kernel only)
+  int batch = 1;
+  int64_t sA = 0, sB = 0, sC = 0, s_alpha2 = 0;
 };
 
-// alpha of a launch with its device multipliers
-__device__ __forceinline__ float gemm_alpha(const GemmArgs& g) {
+// alpha of a launch (batch member z) with its device multipliers
+__device__ __forceinline__ float gemm_alpha(const GemmArgs& g, int z = 0) {
   float a = g.alpha;
   if (g.alpha_dev) a *= *g.alpha_dev;
-  if (g.alpha_dev2) a *= *g.alpha_dev2;
+  if (g.alpha_dev2) a *= g.alpha_dev2[(int64_t)z * g.s_alpha2];
   return a;
 }
 
 // algorithmic flop of a contraction launch: 2 M N K per distinct product
 inline double gemm_flops(const GemmArgs& g) {
-  return 2.0 * g.M * g.N * (double)g.K * (g.nprod > 0 ? g.nprod : g.nseg);
+  return 2.0 * g.M * g.N * (double)g.K * (g.nprod > 0 ? g.nprod : g.nseg) * g.batch;
 }
 // flop the matrix cores execute: 2 M N K per segment (every bf16 term of a split operand)
-inline double gemm_exec_flops(const GemmArgs& g) { return 2.0 * g.M * g.N * (double)g.K * g.nseg; }
+inline double gemm_exec_flops(const GemmArgs& g) { return 2.0 * g.M * g.N * (double)g.K * g.nseg * g.batch; }
 
 // Append the products A_i B_j (i + j <= maxsum) of nA and nB bf16 terms to g's segments: with
 // three-term splits the products of order 2^-24 and above (maxsum 2); with two-term fp16 splits

@@ -163,7 +163,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
   const int nblk = gridDim.x;
   int bid = blockIdx.x;
   if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
-  const int split = bid / ntile, tile = bid - split * ntile;
+  const int zs = bid / ntile, tile = bid - zs * ntile;
+  // a batched launch's member z (batched launches do not split K), else the split
+  const int zb = g.batch > 1 ? zs : 0, split = g.batch > 1 ? 0 : zs;
+  const int64_t oA = (int64_t)zb * g.sA, oB = (int64_t)zb * g.sB;
   // groups of GM tile rows: consecutive tiles (one XCD's share) form a GM-row patch, so the
   // A and B panels they read overlap in that XCD's L2
   constexpr int GM = 4;
@@ -192,8 +195,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
   // segment: the loop body is branch-free, and the surplus loads land in a stage that is
   // never read again.
   int iss_seg = c0 / nch, iss_k = (c0 - iss_seg * nch) * LBK;
-  __amdgpu_buffer_rsrc_t ra = rsrc(g.A[iss_seg], bm, rows_a, g.lda);
-  __amdgpu_buffer_rsrc_t rb = rsrc(g.B[iss_seg], bn, rows_b, g.ldb);
+  __amdgpu_buffer_rsrc_t ra = rsrc(g.A[iss_seg] + oA, bm, rows_a, g.lda);
+  __amdgpu_buffer_rsrc_t rb = rsrc(g.B[iss_seg] + oB, bn, rows_b, g.ldb);
   auto issue_one = [&](int st, int i) {
     char* base = smem + st * STAGE;
     if (i < AI)
@@ -210,8 +213,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
     if (iss_k == g.K) {
       iss_k = 0;
       if (++iss_seg < g.nseg) {
-        ra = rsrc(g.A[iss_seg], bm, rows_a, g.lda);
-        rb = rsrc(g.B[iss_seg], bn, rows_b, g.ldb);
+        ra = rsrc(g.A[iss_seg] + oA, bm, rows_a, g.lda);
+        rb = rsrc(g.B[iss_seg] + oB, bn, rows_b, g.ldb);
       }
     }
   };
@@ -315,9 +318,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
 
   // D[i][j] of a 16x16 tile sits in lane (j + 16 * (i / 4)), register i % 4.
   const int oc = lane & 15, orow = (lane >> 4) * 4;
-  float* out = g.part ? g.part + (int64_t)split * g.M * g.N : g.C;
+  float* out = g.part ? g.part + (int64_t)split * g.M * g.N : g.C + (int64_t)zb * g.sC;
   const int64_t ldo = g.part ? g.N : g.ldc;
-  const float alpha = g.part ? 1.0f : gemm_alpha(g);
+  const float alpha = g.part ? 1.0f : gemm_alpha(g, zb);
   const bool acc_in = !g.part && g.accumulate;
   float mx = 0.0f;
 #pragma unroll
@@ -367,6 +370,7 @@ static bs_status launch_gemm_lds(const GemmArgs& g0, hipStream_t st) {
   // minimizes the makespan ceil(tiles * splits / 256) / splits (e.g. 48 tiles: 5 splits in one round
   // of 240 blocks, not 6 in two rounds of 288)
   int splits = 1;
+  if (g.batch > 1) g.part = nullptr;  // batch members fill the CUs
   if (g.part && tiles < 256) {
     const int64_t by_k = total / 16;
     const int64_t by_ws = g.part_cap / ((int64_t)g.M * g.N);
@@ -383,10 +387,11 @@ static bs_status launch_gemm_lds(const GemmArgs& g0, hipStream_t st) {
   const int cps = (total + splits - 1) / splits;
   splits = (total + cps - 1) / cps;
   if (splits == 1) g.part = nullptr;
-  if (tiles * splits > 0x7FFFFFFF) return BS_ESHAPE;
+  const int64_t nblocks = tiles * (g.batch > 1 ? g.batch : splits);
+  if (nblocks > 0x7FFFFFFF) return BS_ESHAPE;
   {
     ProfScope prof("gemm", st, gemm_flops(g), gemm_exec_flops(g));
-    gemm_lds_kernel<BM, BN, WGM, WGN, F16><<<(unsigned)(tiles * splits), 64 * WGM * WGN, 0, st>>>(g, cps);
+    gemm_lds_kernel<BM, BN, WGM, WGN, F16><<<(unsigned)nblocks, 64 * WGM * WGN, 0, st>>>(g, cps);
     BS_CHECK_LAUNCH();
   }
   if (splits > 1) {
@@ -414,6 +419,7 @@ bs_status launch_gemm(const GemmArgs& g, hipStream_t st) {
   if (g.nseg < 1 || g.nseg > GEMM_MAX_SEG) return BS_EINVAL;
   if ((g.K & 7) || (g.lda & 7) || (g.ldb & 7) || g.lda < g.K || g.ldb < g.K) return BS_ESHAPE;
   if (g.amax && g.accumulate) return BS_EINVAL;
+  if (g.batch < 1 || (g.batch > 1 && (g.sA < 0 || g.sB < 0 || g.sC < 0 || g.s_alpha2 < 0))) return BS_EINVAL;
   if (g.K == 0) return g.accumulate ? BS_OK : launch_fill2d(g.C, g.M, g.N, g.ldc, 0.0f, st);
   // pipelined kernel for 64-aligned K and 16-byte aligned operands
   // (buffer offsets of one 256-row tile fit in 31 bits)
@@ -422,7 +428,7 @@ bs_status launch_gemm(const GemmArgs& g, hipStream_t st) {
   const bool big_tiles = (int64_t)g.M * g.N >= (int64_t)256 * 256 * 16;
   if (lds_ok && g.f16)
     return big_tiles ? launch_gemm_lds<256, 256, 2, 4, true>(g, st) : launch_gemm_lds<128, 128, 2, 2, true>(g, st);
-  if (g.f16 || g.amax) return BS_EINVAL;  // fp16 operands, maxima: the pipelined kernel only
+  if (g.f16 || g.amax || g.batch > 1) return BS_EINVAL;  // fp16 operands, maxima, batches: the pipelined kernel only
   if (lds_ok)
     return big_tiles ? launch_gemm_lds<256, 256, 2, 4, false>(g, st) : launch_gemm_lds<128, 128, 2, 2, false>(g, st);
   // 256 x 256 tiles once they still give every CU a tile; 128 x 128 below that

@@ -55,6 +55,10 @@ struct AlluWs {
   u16 *tH[2], *tQ[2];    // dh, dQKV as scaled two-term fp16 splits, transposed
   u16 *pAn[2], *pWn[2];  // a chunk of N trials' difference and value planes at O's and u1's weight uses
   float *dWo_n, *dWqkv_n;  // the chunk's weight-use moves [KCH][d][d], [KCH][d][3d]
+  // the chunk's moves dh_d and dQKV_d as transposed two-term fp16 planes [KCH][2][d or 3d][Tp]
+  // and their 2^-e: the weight uses' products with them run once per chunk, batched
+  u16 *tBo, *tBq;
+  float *invo, *invq;
   float *dh_d, *dO_dt, *dD, *dQ_d, *dK_d, *dV_d, *du1_d;
   u16 *Wo16, *Wqkv16, *V16;  // the weights and V as scaled fp16 (the moves' contractions)
   u16 *Q16, *K16, *Qt16, *Kt16;  // Q, K as scaled fp16 and their transposed copies
@@ -111,6 +115,10 @@ AlluWs carve_allu(Carver& c, int B, int S, int d, int H, int F, int K) {
   }
   w.dWo_n = c.take<float>(kc * d * d);
   w.dWqkv_n = c.take<float>(kc * d * d3);
+  w.tBo = c.take<u16>(kc * 2 * d * Tp);
+  w.tBq = c.take<u16>(kc * 2 * d3 * Tp);
+  w.invo = c.take<float>(kc);
+  w.invq = c.take<float>(kc);
   w.gpart = c.take<double>(3 * ((T + 15) / 16) * (int64_t)d);
   for (int i = 0; i < NCOMP; ++i) {
     w.delta[i] = c.take<float>((i < 2 ? std::max(1, std::min(K, NB)) : 1) * nc[i]);
@@ -296,9 +304,9 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       }
       float* dWo = dl[3];
       float* dWqkv = dl[2];
-      // the value planes the weight uses read with the moves: the forward's (R) or trial k's (N)
-      const u16* valO = l == LETTER_N ? w.pWn[0] + (int64_t)kk * d * Tp : w.valT_O;
-      const u16* valU = l == LETTER_N ? w.pWn[1] + (int64_t)kk * d * Tp : w.valT_u1;
+      // R: the value planes the weight uses read with the moves (the forward's roundings)
+      const u16* valO = w.valT_O;
+      const u16* valU = w.valT_u1;
       // u2's normalization-input use: the move of dh (and its max |.|)
       if (l != LETTER_U) {
         BS_TRY(launch_fill2d((float*)w.amax[AM_DHD], (AM_N - AM_DHD) * AMAX_SLOTS, 1, AMAX_STRIDE, 0.0f, st));
@@ -322,19 +330,28 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
       } else {
         // dh_d's transposed planes (the weight use) and row planes (the move of dO), one read; the
         // weight use's move: val^T dh_d (N: added to the chunk's difference product)
+        // (N: into the chunk's planes, the weight use's product batched at the chunk's end)
         MoveSrc mo{};
         mo.rows = w.dh_d;
         mo.ldi = d;
-        BS_TRY(launch_split_move(mo, nullptr, 0, T, d, sc_o, w.tB, nullptr, Tp, w.rows3, d, st));
-        Gemm gw(d, d, (int)Tp, Tp, Tp, dWo, d, s_O);
-        gw.g.f16 = 1;
-        gw.g.alpha_dev2 = w.inv + IV_DHD;
-        gw.g.accumulate = l == LETTER_N;
-        BS_TRY(gw.add(&valO, 1, w.tB, 2).run(w.part, w.part_cap, st));
+        F16Scale so = sc_o;
+        u16* to[2] = {w.tB[0], w.tB[1]};
+        if (l == LETTER_N) {
+          to[0] = w.tBo + (int64_t)kk * 2 * d * Tp;
+          to[1] = to[0] + d * Tp;
+          so.inv_out = w.invo + kk;
+        }
+        BS_TRY(launch_split_move(mo, nullptr, 0, T, d, so, to, nullptr, Tp, w.rows3, d, st));
+        if (l != LETTER_N) {
+          Gemm gw(d, d, (int)Tp, Tp, Tp, dWo, d, s_O);
+          gw.g.f16 = 1;
+          gw.g.alpha_dev2 = so.inv_out;
+          BS_TRY(gw.add(&valO, 1, to, 2).run(w.part, w.part_cap, st));
+        }
         // the move of dO (token-major: the D use and the attention operands read it so)
         Gemm gm((int)T, d, d, d, d, w.dO_dt, d, w.inv + IV_WO);
         gm.g.f16 = 1;
-        gm.g.alpha_dev2 = w.inv + IV_DHD;
+        gm.g.alpha_dev2 = so.inv_out;
         gm.g.amax = w.amax[AM_DOD];
         BS_TRY(gm.add(w.rows3, 2, &w.Wo16, 1).run(nullptr, 0, st));
       }
@@ -398,16 +415,24 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         mq.S = S;
         mq.H = H;
         mq.d = d;
-        BS_TRY(launch_split_move(mq, nullptr, 0, T, d3, sc_q, w.tB, nullptr, Tp, w.rows3, d3, st));
-        Gemm gq(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, s_u1);
-        gq.g.f16 = 1;
-        gq.g.alpha_dev2 = w.inv + IV_DQKVD;
-        gq.g.accumulate = l == LETTER_N;
-        BS_TRY(gq.add(&valU, 1, w.tB, 2).run(w.part, w.part_cap, st));
+        F16Scale sq = sc_q;
+        u16* tq[2] = {w.tB[0], w.tB[1]};
+        if (l == LETTER_N) {
+          tq[0] = w.tBq + (int64_t)kk * 2 * d3 * Tp;
+          tq[1] = tq[0] + d3 * Tp;
+          sq.inv_out = w.invq + kk;
+        }
+        BS_TRY(launch_split_move(mq, nullptr, 0, T, d3, sq, tq, nullptr, Tp, w.rows3, d3, st));
+        if (l != LETTER_N) {
+          Gemm gq(d, (int)d3, (int)Tp, Tp, Tp, dWqkv, d3, s_u1);
+          gq.g.f16 = 1;
+          gq.g.alpha_dev2 = sq.inv_out;
+          BS_TRY(gq.add(&valU, 1, tq, 2).run(w.part, w.part_cap, st));
+        }
         // the move of du1, then u1's gain and normalization-input uses
         Gemm gu((int)T, d, (int)d3, d3, d3, w.du1_d, d, w.inv + IV_WQKV);
         gu.g.f16 = 1;
-        gu.g.alpha_dev2 = w.inv + IV_DQKVD;
+        gu.g.alpha_dev2 = sq.inv_out;
         BS_TRY(gu.add(w.rows3, 2, &w.Wqkv16, 1).run(nullptr, 0, st));
         const AlluGainArgs<u16> ag{io.x, io.r1, io.gain1, rd(io.u1, io.c_u1, s_u1, 0 * 256 + 1), io.du1, w.du1_d, T, d,
                                    w.gpart};
@@ -416,6 +441,33 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         const AlluDxArgs<u16> ax{io.x, io.r1, io.gain1, rd(io.u1, io.c_u1, s_u1, 0 * 256 + 3), io.du1, w.du1_d, w.dh_d,
                                  T, d, dl[0]};
         BS_TRY(launch_allu_dx(ax, st));
+      }
+      // the chunk's last trial: its weight uses' products val_k^T g_d,k, one batched contraction
+      // each, added to the chunk's difference products
+      if (l == LETTER_N && (kk == KCH - 1 || k == ntr)) {
+        const int nbk = kk + 1;
+        Gemm gw(d, d, (int)Tp, Tp, Tp, w.dWo_n, d, s_O);
+        gw.g.f16 = 1;
+        gw.g.accumulate = 1;
+        gw.g.batch = nbk;
+        gw.g.sA = d * Tp;
+        gw.g.sB = 2 * d * Tp;
+        gw.g.sC = (int64_t)d * d;
+        gw.g.alpha_dev2 = w.invo;
+        gw.g.s_alpha2 = 1;
+        const u16* tbo[2] = {w.tBo, w.tBo + d * Tp};
+        BS_TRY(gw.add(&w.pWn[0], 1, tbo, 2).run(nullptr, 0, st));
+        Gemm gq(d, (int)d3, (int)Tp, Tp, Tp, w.dWqkv_n, d3, s_u1);
+        gq.g.f16 = 1;
+        gq.g.accumulate = 1;
+        gq.g.batch = nbk;
+        gq.g.sA = d * Tp;
+        gq.g.sB = 2 * d3 * Tp;
+        gq.g.sC = (int64_t)d * d3;
+        gq.g.alpha_dev2 = w.invq;
+        gq.g.s_alpha2 = 1;
+        const u16* tbq[2] = {w.tBq, w.tBq + d3 * Tp};
+        BS_TRY(gq.add(&w.pWn[1], 1, tbq, 2).run(nullptr, 0, st));
       }
       // this pass's moves: the letter's bias (U, R), or N's trials k - slot .. k, in order, once
       // NB of them (or the last) are in
