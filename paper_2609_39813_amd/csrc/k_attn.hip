@@ -295,6 +295,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
   const int key = k0 + 16 * w + c16;
   const float dps = H ? a.f16_inv[0] * a.f16_inv[1] : 1.0f, avs = H ? a.f16_inv[0] * 0x1p-14f : 1.0f;
   const float dsc = H ? a.f16_inv[4] : 1.0f, dkm = H ? a.f16_inv[5] : 1.0f;
+  // H: P comes out at its split's scale 2^14 (1/l scaled), and dS at its split's scale 2^s (dP's
+  // multiplier and D scaled by 2^s 2^-14), so neither split multiplies per element
+  const float lsc = H ? 0x1p14f : 1.0f, dpm = H ? dps * dsc * 0x1p-14f : dps, dmul = H ? dsc * 0x1p-14f : 1.0f;
   // this wave's keys as the second operand of S and dP (fixed over the loop)
   bf16x8 fk[2], fv[2];
   const u16* const Vsrc = H ? a.V16 : a.V;
@@ -381,8 +384,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
     // the rows have landed: 1/l in place (wave 1; 0 past S), read after the next barrier
     if (w == 1) {
       const float l = rows[1][lane];
-      rows[1][lane] = q0 + lane < a.S ? 1.0f / l : 0.0f;
+      rows[1][lane] = q0 + lane < a.S ? lsc / l : 0.0f;
     }
+    if (H && w == 2) rows[2][lane] *= dmul;
     // S, dP: query tiles t (rows), this wave's keys (columns)
     floatx4 sv[4], dp[4];
 #pragma unroll
@@ -427,7 +431,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
       for (int r = 0; r < 4; ++r) {
         const int ql = 16 * t + 4 * g + r;
         p[t][r] = __builtin_amdgcn_exp2f(p[t][r]) * rows[1][ql];
-        ds[t][r] = p[t][r] * (dp[t][r] * dps - rows[2][ql]);
+        ds[t][r] = p[t][r] * (dp[t][r] * dpm - rows[2][ql]);
       }
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
@@ -442,8 +446,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_k_kernel(AttnBwdArgs a) {
         float vs[8], ws[8];
 #pragma unroll
         for (int v = 0; v < 8; ++v) {
-          vs[v] = vp[v] * 0x1p14f;
-          ws[v] = vd[v] * dsc;
+          vs[v] = vp[v];  // P 2^14
+          ws[v] = vd[v];  // dS 2^s
         }
         pack2h(vs, tp);
         pack2h(ws, td);
@@ -570,6 +574,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
   const float dq_ref = qok ? a.D_ref[rb + q] : 0.0f;
   const float dps = H ? a.f16_inv[0] * a.f16_inv[1] : 1.0f;
   const float dsc = H ? a.f16_inv[4] : 1.0f, dqm = H ? a.f16_inv[6] : 1.0f;
+  // H: dS comes out at its split's scale 2^s (dP's multiplier and D scaled)
+  const float dpm = dps * dsc, dq_s = dq_ref * dsc;
 
   // K and V end at row S (rows past it read as zero), K^T spans its Sp columns; lane l of load j
   // (two per wave and tile) fills tile row 8 (2 w + j) + l / 8 at chunk position l % 8, which
@@ -640,7 +646,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         p[t][r] = __builtin_amdgcn_exp2f(p[t][r]) * ilq;
-        ds[t][r] = p[t][r] * (dp[t][r] * dps - dq_ref);
+        ds[t][r] = p[t][r] * (dp[t][r] * dpm - dq_s);
       }
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
@@ -655,7 +661,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_q_kernel(AttnBwdArgs a) {
       if constexpr (H) {
         float ws[8];
 #pragma unroll
-        for (int v = 0; v < 8; ++v) ws[v] = vd[v] * dsc;
+        for (int v = 0; v < 8; ++v) ws[v] = vd[v];  // dS 2^s
         pack2h(ws, td);
       } else {
         pack3t(vd, td);

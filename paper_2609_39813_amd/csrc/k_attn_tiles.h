@@ -90,15 +90,21 @@ __device__ __forceinline__ void pack3t(const float* v, bf16x8* t) {
 }
 
 // The two-term fp16 split (bsp_common.h split2_f16) of eight fp32 values below 2^15 in magnitude.
+// Pairs go through the packed conversion (hi of two values in one instruction, round to nearest
+// even); the remainders are exact in fp32 and rounded as a pair again.
+typedef float floatx2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 halfx2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ void pack2h(const float* v, bf16x8* t) {
   uint32_t w[2][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    u16 ha, la, hb, lb;
-    split2_f16(v[2 * i], ha, la);
-    split2_f16(v[2 * i + 1], hb, lb);
-    w[0][i] = (uint32_t)ha | ((uint32_t)hb << 16);
-    w[1][i] = (uint32_t)la | ((uint32_t)lb << 16);
+    const floatx2_t x = {v[2 * i], v[2 * i + 1]};
+    const halfx2_t h = __builtin_convertvector(x, halfx2_t);
+    halfx2_t l;
+    l.x = (_Float16)(x.x - (float)h.x);
+    l.y = (_Float16)(x.y - (float)h.y);
+    w[0][i] = __builtin_bit_cast(uint32_t, h);
+    w[1][i] = __builtin_bit_cast(uint32_t, l);
   }
 #pragma unroll
   for (int p = 0; p < 2; ++p) t[p] = __builtin_bit_cast(bf16x8, make_uint4(w[p][0], w[p][1], w[p][2], w[p][3]));
