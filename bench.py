@@ -48,22 +48,22 @@ PSTORE_ROWS_PEAK_DPS = VALU_LANE_OPS / (452 / 32)
 # HBM bytes per launch of the counter at the benchmark shape, from two rocprofv3 --pmc passes
 # (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) over this script, each scaled by what the
 # counter reads for the 256 MiB device copy at the end of this script: FETCH_SIZE read
-# 131089 KiB for 262144 KiB copied (x 2.000), WRITE_SIZE 262144 KiB (x 1.000). The counter
+# 131088 KiB for 262144 KiB copied (x 2.000), WRITE_SIZE 262144 KiB (x 1.000). The counter
 # read 16573 KiB fetched and 16384 KiB written. Valid only for the kernel source it was
 # measured on (SHA-256 prefix of csrc/k_store.hip + bsp_common.h + bsp_kernels.h, in that
 # order); otherwise reported as null.
 TRAFFIC_BYTES = (16573 * 2.000 + 16384 * 1.000) * 1024
 TRAFFIC_SOURCES = ("k_store.hip", "bsp_common.h", "bsp_kernels.h")
-TRAFFIC_SHA256 = "39bfd6462a91c581"
+TRAFFIC_SHA256 = "1444509ce3a83ed7"
 
 # HBM bytes per launch of the contraction kernel in the decoder-layer step (the headline), averaged
-# over the 274 launches of three steps, from the same two passes over this script and the same
-# calibration: FETCH_SIZE 283256 KiB (x 1.9998), WRITE_SIZE 75942 KiB (x 1.000) per launch. Valid
+# over the 183 launches of three steps, from the same two passes over this script and the same
+# calibration: FETCH_SIZE 261578 KiB (x 1.9998), WRITE_SIZE 86880 KiB (x 1.000) per launch. Valid
 # for the sources below (the kernel and the code that shapes its launches).
-GEMM_TRAFFIC_BYTES = (283256 * 1.9998 + 75942 * 1.000) * 1024
+GEMM_TRAFFIC_BYTES = (261578 * 1.9998 + 86880 * 1.000) * 1024
 GEMM_TRAFFIC_SOURCES = ("k_gemm.hip", "bsp_kernels.h", "bsp_common.h", "api_layer.hip", "layer_allu.hip",
                         "norm_run.hip")
-GEMM_TRAFFIC_SHA256 = "492ac44b73f11bb9"
+GEMM_TRAFFIC_SHA256 = "04f1c9783db8e6c4"
 
 
 def traffic_if_current(value=None, sources=None, sha=None):
