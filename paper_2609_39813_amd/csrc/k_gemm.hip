@@ -269,18 +269,19 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
   // k-step 0: its MFMAs, with the fragments of k-step 1 (same stage, landed) read in between.
   // k-step 1: the MFMAs of the first PA fragment rows; then chunk c + 1 is awaited and every
   //   wave has finished reading chunk c; the loads of chunk c + 2 go into chunk c's stage and
-  //   the first fragments of chunk c + 1 are read, both between the remaining MFMAs.
-  // The instruction order is fixed in source: a scheduling barrier closes every small group
-  // (loads, reads and the MFMAs between them), so reads are issued well before their use and
-  // the loads are spread over the MFMA stream. The last iteration reads a stage of surplus
-  // data that is never used.
+  //   the first fragments of chunk c + 1 are read, both between the remaining MFMAs: one read
+  //   per MFMA, one load per LSP MFMAs, evenly over all of them (a burst of loads stalls the
+  //   wave at issue and with it its MFMAs).
+  // The instruction order is fixed in source: a scheduling barrier closes every MFMA's group
+  // (its load, its read), so reads are issued well before their use. The last iteration reads
+  // a stage of surplus data that is never used.
   constexpr int NM = FM * FN;                  // MFMAs per k-step
   constexpr int RD = FM + FN;                  // fragment reads per k-step
   constexpr int PA = FM >= 4 ? FM / 4 : 1;     // rows before the barrier
   constexpr int NA = PA * FN, NB = NM - NA;    // MFMAs before / after the barrier
   constexpr int M0 = NM / RD >= 2 ? 2 : 1;     // k-step 0: one read per M0 MFMAs
-  constexpr int GRP = LPC > RD ? LPC : RD;     // k-step 1: groups of (load, read, MFMAs)
-  constexpr int M1 = (2 * NB) / (3 * GRP) > 0 ? (2 * NB) / (3 * GRP) : 1;  // groups span 2/3 of NB
+  constexpr int LSP = NB / LPC > 0 ? NB / LPC : 1;  // k-step 1: one load per LSP MFMAs
+  static_assert(RD <= NB && LPC <= NB, "k-step 1 holds the reads and loads");
   for (int c = 0; c < n; ++c) {
     const int st = c & 1;
 #pragma unroll
@@ -300,16 +301,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds_kernel(GemmArgs g, in
     BS_LAND(0);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int q = 0; q < GRP; ++q) {
-      if (q < LPC) issue_one(st, q);
-      if (q < RD) read_q(st ^ 1, 0, q, fa[0], fb[0]);
-#pragma unroll
-      for (int t = NA + q * M1; t < NA + (q + 1) * M1 && t < NM; ++t) mfma_t(1, t);
+    for (int p = 0; p < NB; ++p) {
+      if (p % LSP == 0 && p / LSP < LPC) issue_one(st, p / LSP);
+      if (p < RD) read_q(st ^ 1, 0, p, fa[0], fb[0]);
+      mfma_t(1, NA + p);
       __builtin_amdgcn_sched_barrier(0);
     }
-#pragma unroll
-    for (int t = NA + GRP * M1; t < NM; ++t) mfma_t(1, t);
-    __builtin_amdgcn_sched_barrier(0);
     advance();
   }
   // no load into LDS may outlive the block (the CU hands its LDS to the next block)
