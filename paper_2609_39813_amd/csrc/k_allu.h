@@ -58,6 +58,19 @@ struct AlluDxArgs {
 template <typename XT>
 bs_status launch_allu_dx(const AlluDxArgs<XT>& a, hipStream_t st);
 
+// The gain and normalization-input uses of one store together: one read of X, u, du and ddu
+// serves both. The gain use's partial sums per 16-row tile have allu_gain's layout. Within a
+// tile, each group of 4 rows is summed in row order, then the 4 groups in order. d > 1024
+// falls back to the two separate kernels.
+template <typename XT>
+struct AlluGainDxArgs {
+  AlluDxArgs<XT> dx;  // the normalization-input use (dx.rd its read of the store)
+  StoreRead rd_g;     // the gain use's read of the same store (rd_g.x == dx.rd.x)
+  double* part;       // [ceil(T / 16)][d]
+};
+template <typename XT>
+bs_status launch_allu_gain_dx(const AlluGainDxArgs<XT>& a, hipStream_t st);
+
 // D use (Eq. dterm): per head-major row, rowsum(ddO * O_D) + rowsum(dO * (O_D - O)), O_D what the
 // letter reads of the attention output (rd.x = O head-major), ddO nullable.
 struct AlluDArgs {

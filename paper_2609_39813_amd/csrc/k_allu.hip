@@ -87,15 +87,19 @@ __global__ __launch_bounds__(256) void allu_gain_kernel(AlluGainArgs<XT> a) {
 // gain ddu of the first pass in registers for the second (the letter's read, a Philox draw and
 // an fp64 division per element, is taken once); NI == 0: any d, the second pass reads and
 // computes again.
-template <typename XT, int NI>
-__device__ __forceinline__ float allu_dx_row(const AlluDxArgs<XT>& a, int64_t t, int lane) {
+// GAIN: also the gain use's terms (z_g - z)(du + ddu) + z ddu of this row, z_g from the gain use's
+// read rd_g, added to accg[4 lane + 256 it + c] (LDS) for the lane's columns (NI > 0 only).
+template <typename XT, int NI, bool GAIN = false>
+__device__ __forceinline__ float allu_dx_row(const AlluDxArgs<XT>& a, int64_t t, int lane,
+                                             const StoreRead* rd_g = nullptr, double* accg = nullptr) {
+  static_assert(!GAIN || NI > 0, "the gain terms need the kept columns");
   const float s = a.rd.scale ? *a.rd.scale : 1.0f;
   const double rs = 1.0 / (double)s;
   const float r = a.rstd[t];
   const int64_t rowe = t * a.d;
   constexpr int NK = NI > 0 ? NI : 1;
-  float xk[NK][4];
-  double zk[NK][4], gk[NK][4];
+  float xk[NK][4], dk[NK][4];  // x and ddu, kept for the second pass (NI > 0)
+  double zk[NK][4];
   double dref = 0.0, dl = 0.0;
   // first pass: the two row sums (and, NI > 0, the kept values)
   auto first = [&](int64_t j0, int it) {
@@ -107,16 +111,32 @@ __device__ __forceinline__ float allu_dx_row(const AlluDxArgs<XT>& a, int64_t t,
     if (a.ddu) load4(a.ddu, rowe + j0, ddu);
     double v[4];
     read4(a.rd, rowe + j0, u, rs, s, v);
+    double vg[4];
+    if constexpr (GAIN) {
+      if (rd_g->letter == LETTER_N) {
+        read4(*rd_g, rowe + j0, u, rs, s, vg);
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) vg[c] = v[c];  // U and R read the same at both uses
+      }
+    }
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const double z = (double)(x[c] * r);
-      const double zx = a.rd.letter == LETTER_U ? z : v[c] / (double)g[c];
+      // GAIN: the two uses' reads over one reciprocal of the gain (v / g as v (1 / g), within an
+      // fp64 ulp); else the division
+      const double ig = GAIN ? 1.0 / (double)g[c] : 0.0;
+      const double zx = a.rd.letter == LETTER_U ? z : GAIN ? v[c] * ig : v[c] / (double)g[c];
       dref += (double)g[c] * (double)du[c] * z;
       dl += (double)g[c] * ((double)du[c] + (double)ddu[c]) * zx;
       if constexpr (NI > 0) {
         xk[it][c] = x[c];
         zk[it][c] = zx;
-        gk[it][c] = (double)g[c] * (double)ddu[c];
+        dk[it][c] = ddu[c];
+      }
+      if constexpr (GAIN) {
+        const double zg = rd_g->letter == LETTER_U ? z : vg[c] * ig;
+        accg[4 * lane + 256 * it + c] += (zg - z) * ((double)du[c] + (double)ddu[c]) + z * (double)ddu[c];
       }
     }
   };
@@ -132,14 +152,16 @@ __device__ __forceinline__ float allu_dx_row(const AlluDxArgs<XT>& a, int64_t t,
   const double inv_d = 1.0 / (double)a.d;
   float mx = 0.0f;
   // second pass: out = r (gain ddu - (z_x dl - z dref) / d) + add
-  auto second = [&](int64_t j0, const float (&x)[4], const double (&zx)[4], const double (&gd)[4]) {
-    float ad[4] = {0.f, 0.f, 0.f, 0.f};
+  auto second = [&](int64_t j0, const float (&x)[4], const double (&zx)[4], const float (&ddu)[4]) {
+    float ad[4] = {0.f, 0.f, 0.f, 0.f}, g[4];
     if (a.add) load4(a.add, rowe + j0, ad);
+    load4(a.gain, j0, g);
     float o[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const double z = (double)(x[c] * r);
-      o[c] = (float)((double)r * (gd[c] - (zx[c] * dl - z * dref) * inv_d) + (double)ad[c]);
+      const double gd = (double)g[c] * (double)ddu[c];
+      o[c] = (float)((double)r * (gd - (zx[c] * dl - z * dref) * inv_d) + (double)ad[c]);
       mx = fmaxf(mx, fabsf(o[c]));
     }
     *(float4*)(a.out + rowe + j0) = make_float4(o[0], o[1], o[2], o[3]);
@@ -147,7 +169,7 @@ __device__ __forceinline__ float allu_dx_row(const AlluDxArgs<XT>& a, int64_t t,
   if constexpr (NI > 0) {
 #pragma unroll
     for (int it = 0; it < NI; ++it)
-      if (4 * (int64_t)lane + 256 * it < a.d) second(4 * (int64_t)lane + 256 * it, xk[it], zk[it], gk[it]);
+      if (4 * (int64_t)lane + 256 * it < a.d) second(4 * (int64_t)lane + 256 * it, xk[it], zk[it], dk[it]);
   } else {
     for (int64_t j0 = 4 * (int64_t)lane; j0 < a.d; j0 += 256) {
       float x[4], u[4], ddu[4] = {0.f, 0.f, 0.f, 0.f}, g[4];
@@ -155,14 +177,11 @@ __device__ __forceinline__ float allu_dx_row(const AlluDxArgs<XT>& a, int64_t t,
       load4(a.rd.x, rowe + j0, u);
       load4(a.gain, j0, g);
       if (a.ddu) load4(a.ddu, rowe + j0, ddu);
-      double v[4], zx[4], gd[4];
+      double v[4], zx[4];
       read4(a.rd, rowe + j0, u, rs, s, v);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        zx[c] = a.rd.letter == LETTER_U ? (double)(x[c] * r) : v[c] / (double)g[c];
-        gd[c] = (double)g[c] * (double)ddu[c];
-      }
-      second(j0, x, zx, gd);
+      for (int c = 0; c < 4; ++c) zx[c] = a.rd.letter == LETTER_U ? (double)(x[c] * r) : v[c] / (double)g[c];
+      second(j0, x, zx, ddu);
     }
   }
   return mx;
@@ -173,6 +192,24 @@ __global__ __launch_bounds__(256) void allu_dx_kernel(AlluDxArgs<XT> a) {
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const float mx = t < a.T ? allu_dx_row<XT, NI>(a, t, lane) : 0.0f;  // uniform per wave
   if (a.amax) block_amax_to_slot(mx, a.amax);
+}
+
+// 16 rows per block (the gain use's tile), 4 consecutive rows per wave; the gain terms of a column
+// summed over the wave's rows in order, then over the 4 waves in order through LDS
+template <typename XT, int NI>
+__global__ __launch_bounds__(256, 3) void allu_gain_dx_kernel(AlluGainDxArgs<XT> a) {
+  __shared__ double red[4][256 * NI];  // per wave, the gain terms of its rows by column
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int j = lane; j < 256 * NI; j += 64) red[w][j] = 0.0;  // each lane's own columns below
+  float mx = 0.0f;
+  for (int i = 0; i < 4; ++i) {
+    const int64_t t = (int64_t)blockIdx.x * ALLU_RT + 4 * w + i;
+    if (t < a.dx.T) mx = fmaxf(mx, allu_dx_row<XT, NI, true>(a.dx, t, lane, &a.rd_g, red[w]));  // uniform per wave
+  }
+  __syncthreads();
+  for (int j = threadIdx.x; j < a.dx.d; j += 256)
+    a.part[(int64_t)blockIdx.x * a.dx.d + j] = ((red[0][j] + red[1][j]) + red[2][j]) + red[3][j];
+  if (a.dx.amax) block_amax_to_slot(mx, a.dx.amax);
 }
 
 // 16 lanes per row of 64, 4 elements each; 16 rows per block
@@ -253,6 +290,31 @@ bs_status launch_allu_dx(const AlluDxArgs<XT>& a, hipStream_t st) {
 }
 template bs_status launch_allu_dx<float>(const AlluDxArgs<float>&, hipStream_t);
 template bs_status launch_allu_dx<u16>(const AlluDxArgs<u16>&, hipStream_t);
+
+template <typename XT>
+bs_status launch_allu_gain_dx(const AlluGainDxArgs<XT>& a, hipStream_t st) {
+  const AlluDxArgs<XT>& x = a.dx;
+  if (x.T <= 0 || x.d <= 0) return BS_OK;
+  if (x.d & 3) return BS_ESHAPE;
+  if (a.rd_g.x != x.rd.x || a.rd_g.codes != x.rd.codes || a.rd_g.scale != x.rd.scale || a.rd_g.letter != x.rd.letter)
+    return BS_EINVAL;
+  if (x.d > 1024) {
+    const AlluGainArgs<XT> g{x.X, x.rstd, x.gain, a.rd_g, x.du, x.ddu, x.T, x.d, a.part};
+    const bs_status e = launch_allu_gain(g, st);
+    return e != BS_OK ? e : launch_allu_dx(x, st);
+  }
+  const unsigned grid = (unsigned)((x.T + ALLU_RT - 1) / ALLU_RT);
+  if (x.d <= 256)
+    allu_gain_dx_kernel<XT, 1><<<grid, 256, 0, st>>>(a);
+  else if (x.d <= 512)
+    allu_gain_dx_kernel<XT, 2><<<grid, 256, 0, st>>>(a);
+  else
+    allu_gain_dx_kernel<XT, 4><<<grid, 256, 0, st>>>(a);
+  BS_CHECK_LAUNCH();
+  return BS_OK;
+}
+template bs_status launch_allu_gain_dx<float>(const AlluGainDxArgs<float>&, hipStream_t);
+template bs_status launch_allu_gain_dx<u16>(const AlluGainDxArgs<u16>&, hipStream_t);
 
 bs_status launch_allu_d(const AlluDArgs& a, hipStream_t st) {
   if (a.ddo_heads < 0 || (a.ddo_heads > 0 && (a.ddo_S <= 0 || a.rows % a.ddo_S))) return BS_EINVAL;

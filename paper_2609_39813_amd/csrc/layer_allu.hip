@@ -434,13 +434,12 @@ bs_status allu_run(const AlluIO& io, void* ws, size_t ws_bytes, hipStream_t st) 
         gu.g.f16 = 1;
         gu.g.alpha_dev2 = sq.inv_out;
         BS_TRY(gu.add(w.rows3, 2, &w.Wqkv16, 1).run(nullptr, 0, st));
-        const AlluGainArgs<u16> ag{io.x, io.r1, io.gain1, rd(io.u1, io.c_u1, s_u1, 0 * 256 + 1), io.du1, w.du1_d, T, d,
-                                   w.gpart};
-        BS_TRY(launch_allu_gain(ag, st));
+        // (one pass over u1's operands for both uses)
+        AlluDxArgs<u16> ax{io.x, io.r1, io.gain1, rd(io.u1, io.c_u1, s_u1, 0 * 256 + 3), io.du1, w.du1_d, w.dh_d,
+                           T, d, dl[0]};
+        const AlluGainDxArgs<u16> agx{ax, rd(io.u1, io.c_u1, s_u1, 0 * 256 + 1), w.gpart};
+        BS_TRY(launch_allu_gain_dx(agx, st));
         BS_TRY(launch_gain_final(w.gpart, (T + 15) / 16, d, dl[1], nullptr, nullptr, st));
-        const AlluDxArgs<u16> ax{io.x, io.r1, io.gain1, rd(io.u1, io.c_u1, s_u1, 0 * 256 + 3), io.du1, w.du1_d, w.dh_d,
-                                 T, d, dl[0]};
-        BS_TRY(launch_allu_dx(ax, st));
       }
       // the chunk's last trial: its weight uses' products val_k^T g_d,k, one batched contraction
       // each, added to the chunk's difference products
