@@ -163,18 +163,20 @@ __device__ __forceinline__ uint32_t codes4(const float* y, const uint32_t* R) {
   return cvt_rne2<FMT, true>(y[2], y[3], cvt_rne2<FMT, false>(y[0], y[1], 0u));
 }
 
-// Eight consecutive elements per thread (two Philox groups): one 16- or 32-byte load, an 8-byte
-// store of the codes. The last thread of a ragged tensor takes the element-wise path.
+// Groups of eight consecutive elements (two Philox groups), grid-stride: one 16- or 32-byte load
+// and an 8-byte store of the codes per group. The last group of a ragged tensor takes the
+// element-wise path. A thread takes several groups, so that the per-wave set-up is paid once
+// per several groups.
 template <typename T, int FMT, int MODE>
 __global__ __launch_bounds__(256) void quantize_kernel(const T* __restrict__ x, int64_t n, float fmax,
                                                        bs_diag* __restrict__ diag, uint8_t* __restrict__ codes,
                                                        uint64_t seed, uint32_t trial, uint32_t use) {
   if (diag->nonfinite) return;
   const double rs = 1.0 / (double)diag->scale;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t e0 = t * 8;
+  const int64_t ngroups = (n + 7) / 8, stride = (int64_t)gridDim.x * blockDim.x;
   uint32_t nsat = 0;
-  if (e0 < n) {
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < ngroups; t += stride) {
+    const int64_t e0 = t * 8;
     float xv[8];
     const int cnt = (int)((n - e0) < 8 ? (n - e0) : 8);
     const bool vec = cnt == 8 && (((uintptr_t)(x + e0)) & 15) == 0 && (((uintptr_t)(codes + e0)) & 7) == 0;
@@ -213,7 +215,8 @@ __global__ __launch_bounds__(256) void quantize_kernel(const T* __restrict__ x, 
       for (int q = 0; q < cnt; ++q) codes[e0 + q] = (uint8_t)((q < 4 ? lo >> (8 * q) : hi >> (8 * (q - 4))));
     }
   }
-  // nsat is the wave's count here (threads past n contribute zeros to the ballots)
+  // nsat is the wave's count here: lane 0 has the smallest group index of its wave, so it takes
+  // part in every ballot of the wave
   if ((threadIdx.x & 63) == 0 && nsat) atomicAdd(&diag->n_saturated, nsat);
 }
 
@@ -393,8 +396,9 @@ bs_status launch_store(const void* x, bs_dtype xt, int64_t n, int fmt, int mode,
   }
   finalize_scale_kernel<<<1, 64, 0, st>>>(diag, scale_in, scale_out, f.fmax);
   if (n > 0 && codes) {  // codes == nullptr: the scale only
+    // up to 8192 blocks (32 waves per CU), each thread then taking several groups of eight
     const int64_t threads = (n + 7) / 8;
-    const unsigned blocks = (unsigned)((threads + 255) / 256);
+    const unsigned blocks = (unsigned)std::min<int64_t>((threads + 255) / 256, 8192);
     ProfScope prof("quantize", st);
 #define QK(T, FM, M) \
   quantize_kernel<T, FM, M><<<blocks, 256, 0, st>>>((const T*)x, n, f.fmax, diag, codes, seed, trial, use)
