@@ -303,22 +303,28 @@ __global__ __launch_bounds__(256) void norm_planes_t4_kernel(NormPlaneArgs a) {
 }
 
 // Per-trial residual planes of the weight use (the per-trial contraction path): a block covers
-// 64 rows t x 64 columns j; a thread holds 4 rows x 4 consecutive columns (one Philox call per
-// row and trial), the trial's values go through an LDS tile (rows of 144 bytes) to rows of the
-// plane [j][t], leaving it as 16-byte pieces (eight consecutive t per thread and piece).
+// 64 rows t x 64 columns j; a thread holds 4 consecutive rows x 4 consecutive columns (one Philox
+// call per row and trial). A trial's values go through an LDS tile [j][t] to rows of the plane
+// [j][t] and leave as 16-byte pieces. A thread's four rows of a column enter the tile as one
+// 8-byte store. Tile rows are 34 words apart, and the words of row r are rotated by
+// 2 ((r >> 4) & 3) (tp_word), so that the 16 lanes of a store pass and of a read pass fall on
+// distinct banks.
+__device__ __forceinline__ int tp_word(int r, int w) { return r * 34 + ((w + 2 * ((r >> 4) & 3)) & 31); }
+
 __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 tile[64][72];
-  __shared__ __attribute__((aligned(16))) u16 tileW[64][72];
+  __shared__ __attribute__((aligned(16))) uint32_t tile[64 * 34];
+  __shared__ __attribute__((aligned(16))) uint32_t tileW[64 * 34];
   const int64_t t0 = (int64_t)blockIdx.y * 64, j0 = (int64_t)blockIdx.x * 64;
   const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;  // column group, row group
+  const int64_t jg = j0 + 4 * cg, tb = t0 + 4 * rg;          // first column, first row
   const double rs = 1.0 / (double)*a.scale;
   uint32_t F[4][4];
   u16 sv[4][4];    // bf16 of sign * step
   float ov[4][4], stp[4][4];  // the forward's value and sign * step (outW)
-  uint32_t h[4];   // bit q: the forward's code was rounded up
+  uint32_t h[4];   // bit c: the forward's code was rounded up
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int64_t t = t0 + rg + 16 * q, jg = j0 + 4 * cg;
+    const int64_t t = tb + q;
     h[q] = 0;
     // the row's four columns in one 16-byte and one 4-byte load (d % 4 == 0)
     const bool ok = t < a.T && jg < a.d;
@@ -344,22 +350,29 @@ __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
   }
   for (int b = 0; b < a.nb; ++b) {
     const uint32_t k = (uint32_t)(a.k0 + b);
+    u16 dv[4][4], wv[4][4];  // [c][q]: the difference and the new rounding's value
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int64_t t = t0 + rg + 16 * q;
-      const int64_t jg = j0 + 4 * cg;
+      const int64_t t = tb + q;
       const Philox4 p = philox_group(a.seed, (uint64_t)((t * a.d + jg) >> 2), k, a.use);
       const uint32_t R[4] = {p.w0, p.w1, p.w2, p.w3};
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const uint32_t up = sr_up(F[q][c], R[c]), hb = (h[q] >> c) & 1u;
-        tile[4 * cg + c][rg + 16 * q] = up == hb ? (u16)0 : (up ? sv[q][c] : (u16)(sv[q][c] ^ 0x8000u));
-        if (a.outW) {
-          // the new rounding's value: exact (an FP8 value)
-          const float nv = up == hb ? ov[q][c] : (up ? ov[q][c] + stp[q][c] : ov[q][c] - stp[q][c]);
-          tileW[4 * cg + c][rg + 16 * q] = a.f16 ? f16_bits(nv) : bf16_bits(nv);
-        }
+        dv[c][q] = up == hb ? (u16)0 : (up ? sv[q][c] : (u16)(sv[q][c] ^ 0x8000u));
+        // the new rounding's value: exact (an FP8 value)
+        const float nv = up == hb ? ov[q][c] : (up ? ov[q][c] + stp[q][c] : ov[q][c] - stp[q][c]);
+        wv[c][q] = a.f16 ? f16_bits(nv) : bf16_bits(nv);
       }
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int wd = tp_word(4 * cg + c, 2 * rg);  // words 2 rg, 2 rg + 1 of row 4 cg + c
+      *(uint2*)&tile[wd] = make_uint2((uint32_t)dv[c][0] | ((uint32_t)dv[c][1] << 16),
+                                      (uint32_t)dv[c][2] | ((uint32_t)dv[c][3] << 16));
+      if (a.outW)
+        *(uint2*)&tileW[wd] = make_uint2((uint32_t)wv[c][0] | ((uint32_t)wv[c][1] << 16),
+                                         (uint32_t)wv[c][2] | ((uint32_t)wv[c][3] << 16));
     }
     __syncthreads();
 #pragma unroll
@@ -367,8 +380,15 @@ __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
       const int ch = threadIdx.x + 256 * i, cc = ch >> 3, k8 = ch & 7;
       const int64_t j = j0 + cc;
       const int64_t o = (int64_t)b * a.d * a.ldo + j * a.ldo + t0 + 8 * k8;
-      if (j < a.d && a.out) *(uint4*)(a.out + o) = *(const uint4*)&tile[cc][8 * k8];
-      if (j < a.d && a.outW) *(uint4*)(a.outW + o) = *(const uint4*)&tileW[cc][8 * k8];
+      const int w0 = tp_word(cc, 4 * k8), w1 = tp_word(cc, 4 * k8 + 2);
+      if (j < a.d && a.out) {
+        const uint2 x0 = *(const uint2*)&tile[w0], x1 = *(const uint2*)&tile[w1];
+        *(uint4*)(a.out + o) = make_uint4(x0.x, x0.y, x1.x, x1.y);
+      }
+      if (j < a.d && a.outW) {
+        const uint2 x0 = *(const uint2*)&tileW[w0], x1 = *(const uint2*)&tileW[w1];
+        *(uint4*)(a.outW + o) = make_uint4(x0.x, x0.y, x1.x, x1.y);
+      }
     }
     __syncthreads();
   }
