@@ -29,6 +29,7 @@ def run_all(lib, B, S, d, H, F, K, seed, fmt, mode):
 @pytest.mark.parametrize("B,S,d,H,F,K,seed,fmt,mode", [
     (2, 40, 128, 2, 256, 5, 31, "e4m3", "rne"),   # T = 80: a full and a ragged 64-row tile
     (1, 72, 64, 1, 136, 4, 32, "e5m2", "sr"),     # F = 136: ragged contraction columns
+    (1, 16, 1088, 17, 128, 2, 34, "e4m3", "sr"),  # d > 1024: u1's gain and norm-input uses in two kernels
 ])
 def test_every_use_at_once_matches_oracle(lib, B, S, d, H, F, K, seed, fmt, mode):
     out, ref, r = run_all(lib, B, S, d, H, F, K, seed, fmt, mode)
