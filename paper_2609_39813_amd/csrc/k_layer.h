@@ -28,6 +28,8 @@ struct SumsqJob {
 struct SumsqBatch {
   SumsqJob job[SUMSQ_MAX];
   int count;
+  int row[SUMSQ_MAX];  // set by launch_sumsq_batch: the partial-sum row of each job (jobs on the
+                       // same array and length share one)
 };
 inline size_t sumsq_part_size() { return (size_t)SUMSQ_MAX * SUMSQ_BLOCKS; }  // doubles
 bs_status launch_sumsq_batch(const SumsqBatch& b, double* part, hipStream_t st);

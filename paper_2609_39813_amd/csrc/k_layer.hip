@@ -190,7 +190,7 @@ __global__ __launch_bounds__(256) void sumsq_batch_kernel(SumsqBatch b, double* 
 __global__ __launch_bounds__(256) void sumsq_batch_final(SumsqBatch b, const double* __restrict__ part) {
   const SumsqJob j = b.job[blockIdx.x];
   __shared__ double t[SUMSQ_BLOCKS];
-  t[threadIdx.x] = part[(int64_t)blockIdx.x * SUMSQ_BLOCKS + threadIdx.x];
+  t[threadIdx.x] = j.x ? part[(int64_t)b.row[blockIdx.x] * SUMSQ_BLOCKS + threadIdx.x] : 0.0;
   __syncthreads();
   for (int o = SUMSQ_BLOCKS / 2; o > 0; o >>= 1) {
     if ((int)threadIdx.x < o) t[threadIdx.x] += t[threadIdx.x + o];
@@ -282,8 +282,21 @@ bs_status launch_add(const void* a, bs_dtype at, const float* b, float* out, int
 bs_status launch_sumsq_batch(const SumsqBatch& b, double* part, hipStream_t st) {
   if (b.count <= 0) return BS_OK;
   if (b.count > SUMSQ_MAX) return BS_EINVAL;
-  sumsq_batch_kernel<<<dim3(SUMSQ_BLOCKS, (unsigned)b.count), 256, 0, st>>>(b, part);
-  sumsq_batch_final<<<(unsigned)b.count, SUMSQ_BLOCKS, 0, st>>>(b, part);
+  // one partial-sum row per distinct (array, length): a reference read by several letters' rows
+  // is summed once (same sum, same order)
+  SumsqBatch u{}, f = b;
+  for (int i = 0; i < b.count; ++i) {
+    f.row[i] = -1;
+    if (!b.job[i].x) continue;
+    for (int k = 0; k < u.count && f.row[i] < 0; ++k)
+      if (u.job[k].x == b.job[i].x && u.job[k].n == b.job[i].n) f.row[i] = k;
+    if (f.row[i] < 0) {
+      f.row[i] = u.count;
+      u.job[u.count++] = b.job[i];
+    }
+  }
+  if (u.count > 0) sumsq_batch_kernel<<<dim3(SUMSQ_BLOCKS, (unsigned)u.count), 256, 0, st>>>(u, part);
+  sumsq_batch_final<<<(unsigned)f.count, SUMSQ_BLOCKS, 0, st>>>(f, part);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
