@@ -411,6 +411,40 @@ __global__ __launch_bounds__(256) void trial_accum_kernel(const float* __restric
   }
 }
 
+// The same over four consecutive elements per thread (m % 4 == 0, 16-byte aligned arrays): 16-byte
+// loads, and the trial loop unrolled so that several trials' loads are in flight; each element's
+// trials are still added in order.
+__global__ __launch_bounds__(256) void trial_accum4_kernel(const float4* __restrict__ delta, int nb, int k0, int64_t m4,
+                                                           float4* __restrict__ d1, double2* __restrict__ S1,
+                                                           double2* __restrict__ S2) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m4; i += (int64_t)gridDim.x * blockDim.x) {
+    const float4 sh = k0 == 1 ? delta[i] : d1[i];
+    const float shift[4] = {sh.x, sh.y, sh.z, sh.w};
+    double a1[4] = {0.0, 0.0, 0.0, 0.0}, a2[4] = {0.0, 0.0, 0.0, 0.0};
+    if (k0 != 1) {
+      const double2 p0 = S1[2 * i], p1 = S1[2 * i + 1], q0 = S2[2 * i], q1 = S2[2 * i + 1];
+      a1[0] = p0.x; a1[1] = p0.y; a1[2] = p1.x; a1[3] = p1.y;
+      a2[0] = q0.x; a2[1] = q0.y; a2[2] = q1.x; a2[3] = q1.y;
+    }
+#pragma unroll 4
+    for (int b = (k0 == 1 ? 1 : 0); b < nb; ++b) {
+      const float4 v = delta[(int64_t)b * m4 + i];
+      const float xv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const double x = (double)xv[c] - (double)shift[c];
+        a1[c] += x;
+        a2[c] += x * x;
+      }
+    }
+    if (k0 == 1) d1[i] = sh;
+    S1[2 * i] = make_double2(a1[0], a1[1]);
+    S1[2 * i + 1] = make_double2(a1[2], a1[3]);
+    S2[2 * i] = make_double2(a2[0], a2[1]);
+    S2[2 * i + 1] = make_double2(a2[2], a2[3]);
+  }
+}
+
 __global__ __launch_bounds__(256) void trial_se_kernel(const double* __restrict__ S1, const double* __restrict__ S2,
                                                        int K, int64_t m, float* __restrict__ se) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += (int64_t)gridDim.x * blockDim.x) {
@@ -711,7 +745,13 @@ bs_status launch_trial_planes(const TrialPlaneArgs& a, hipStream_t st) {
 bs_status launch_trial_accum(const float* delta, int nb, int k0, int64_t m, float* d1, double* S1, double* S2,
                              hipStream_t st) {
   if (m <= 0 || nb <= 0) return BS_OK;
-  trial_accum_kernel<<<grid1d(m), 256, 0, st>>>(delta, nb, k0, m, d1, S1, S2);
+  const bool vec = m % 4 == 0 && ((uintptr_t)delta & 15) == 0 && ((uintptr_t)d1 & 15) == 0 && ((uintptr_t)S1 & 15) == 0 &&
+                   ((uintptr_t)S2 & 15) == 0;
+  if (vec)
+    trial_accum4_kernel<<<grid1d(m / 4), 256, 0, st>>>((const float4*)delta, nb, k0, m / 4, (float4*)d1, (double2*)S1,
+                                                       (double2*)S2);
+  else
+    trial_accum_kernel<<<grid1d(m), 256, 0, st>>>(delta, nb, k0, m, d1, S1, S2);
   BS_CHECK_LAUNCH();
   return BS_OK;
 }
