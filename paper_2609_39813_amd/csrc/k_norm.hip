@@ -216,22 +216,30 @@ __global__ __launch_bounds__(256) void norm_planes_t_kernel(NormPlaneArgs a) {
   }
 }
 
+// LDS tile [j][t] of 64 x 64 16-bit values: rows 34 words apart, the words of row r rotated by
+// 2 ((r >> 4) & 3), so that 8-byte stores of a thread's four consecutive t of one column and
+// 8-byte reads along a row leave every 16-lane pass on distinct banks.
+__device__ __forceinline__ int tp_word(int r, int w) { return r * 34 + ((w + 2 * ((r >> 4) & 3)) & 31); }
+
 // The same planes with vector accesses (d a multiple of 4, ldo of 64, 16-byte aligned u, 4-byte
 // aligned codes, 8-byte aligned counts): a thread forms 4 consecutive columns of a row, and each
 // output row (one column j) leaves the LDS tile as 16-byte stores of 8 consecutive t.
 template <int MODE>
 __global__ __launch_bounds__(256) void norm_planes_t4_kernel(NormPlaneArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 tile[3][64][72];
-  const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  __shared__ __attribute__((aligned(16))) uint32_t tile[3][64 * 34];
+  const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;  // 4 columns, 4 consecutive rows
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
   const float s = *a.scale;
   const double rs = 1.0 / (double)s;
   const float rsc = MODE == NP_RESU && a.f16 ? resu_f16_scale(a, s) : 1.0f;
+  u16 o[3][4][4];  // [plane][column c][row i]
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int rr = rg + 16 * i;
-    const int64_t t = r0 + rr, j = c0 + 4 * cg;
-    u16 o[3][4] = {{0, 0, 0, 0}, {0, 0, 0, 0}, {0, 0, 0, 0}};
+    const int64_t t = r0 + 4 * rg + i, j = c0 + 4 * cg;
+#pragma unroll
+    for (int p = 0; p < 3; ++p)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) o[p][c][i] = 0;
     if (t < a.T && j < a.d) {
       const int64_t e = t * a.d + j;
       const uint32_t cw = *(const uint32_t*)(a.codes + e);
@@ -256,15 +264,15 @@ __global__ __launch_bounds__(256) void norm_planes_t4_kernel(NormPlaneArgs a) {
         const uint32_t code = (cw >> (8 * c)) & 0xFFu;
         if (MODE == NP_VAL) {
           const float v = f8_value(code, a.f);
-          o[0][c] = a.f16 ? f16_bits(v) : bf16_bits(v);
+          o[0][c][i] = a.f16 ? f16_bits(v) : bf16_bits(v);
         } else if (MODE == NP_RESU) {
           const float r = fmaf(-s, f8_value(code, a.f), uv[c]);
           if (a.f16) {
             const uint32_t hl = split2_f16_word(r * rsc);
-            o[0][c] = (u16)(hl & 0xFFFFu);
-            o[1][c] = (u16)(hl >> 16);
+            o[0][c][i] = (u16)(hl & 0xFFFFu);
+            o[1][c][i] = (u16)(hl >> 16);
           } else {
-            split3(r, o[0][c], o[1][c], o[2][c]);
+            split3(r, o[0][c][i], o[1][c][i], o[2][c][i]);
           }
         } else {
           const float y = div_scale(uv[c], rs);
@@ -272,32 +280,32 @@ __global__ __launch_bounds__(256) void norm_planes_t4_kernel(NormPlaneArgs a) {
           const int h = (code & 0x7Fu) != b.base + b.mi;
           const float v = (float)((int)cn[c] - a.K * h) * f8_step(b);
           if (a.f16)
-            o[0][c] = f16_bits((signbit(y) ? -v : v) * a.resn_scale);
+            o[0][c][i] = f16_bits((signbit(y) ? -v : v) * a.resn_scale);
           else
-            split3(signbit(y) ? -v : v, o[0][c], o[1][c], o[2][c]);
+            split3(signbit(y) ? -v : v, o[0][c][i], o[1][c][i], o[2][c][i]);
         }
       }
     }
-#pragma unroll
-    for (int p = 0; p < 3; ++p)
-      if (p < a.nterms)
-        *(uint2*)&tile[p][rr][4 * cg] = make_uint2((uint32_t)o[p][0] | ((uint32_t)o[p][1] << 16),
-                                                   (uint32_t)o[p][2] | ((uint32_t)o[p][3] << 16));
   }
+#pragma unroll
+  for (int p = 0; p < 3; ++p)
+    if (p < a.nterms)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        *(uint2*)&tile[p][tp_word(4 * cg + c, 2 * rg)] =
+            make_uint2((uint32_t)o[p][c][0] | ((uint32_t)o[p][c][1] << 16), (uint32_t)o[p][c][2] | ((uint32_t)o[p][c][3] << 16));
   __syncthreads();
-  const int q = (threadIdx.x & 7) * 8;
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
-    const int cc = (threadIdx.x >> 3) + 32 * pass;
+    const int ch = threadIdx.x + 256 * pass, cc = ch >> 3, k8 = ch & 7;
     const int64_t j = c0 + cc;
     if (j >= a.d) continue;
+    const int w0 = tp_word(cc, 4 * k8), w1 = tp_word(cc, 4 * k8 + 2);
 #pragma unroll
     for (int p = 0; p < 3; ++p) {
       if (p >= a.nterms) break;
-      uint32_t w[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)tile[p][q + 2 * i][cc] | ((uint32_t)tile[p][q + 2 * i + 1][cc] << 16);
-      *(uint4*)(a.out[p] + j * a.ldo + r0 + q) = make_uint4(w[0], w[1], w[2], w[3]);
+      const uint2 x0 = *(const uint2*)&tile[p][w0], x1 = *(const uint2*)&tile[p][w1];
+      *(uint4*)(a.out[p] + j * a.ldo + r0 + 8 * k8) = make_uint4(x0.x, x0.y, x1.x, x1.y);
     }
   }
 }
@@ -309,8 +317,6 @@ __global__ __launch_bounds__(256) void norm_planes_t4_kernel(NormPlaneArgs a) {
 // 8-byte store. Tile rows are 34 words apart, and the words of row r are rotated by
 // 2 ((r >> 4) & 3) (tp_word), so that the 16 lanes of a store pass and of a read pass fall on
 // distinct banks.
-__device__ __forceinline__ int tp_word(int r, int w) { return r * 34 + ((w + 2 * ((r >> 4) & 3)) & 31); }
-
 __global__ __launch_bounds__(256) void trial_planes_kernel(TrialPlaneArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t tile[64 * 34];
   __shared__ __attribute__((aligned(16))) uint32_t tileW[64 * 34];
