@@ -102,6 +102,24 @@ def test_large_tensor_sampled_sr(lib):
     assert np.array_equal(codes[idx], ref)
 
 
+def test_ragged_tensor_past_one_grid_sweep_sr(lib):
+    # more groups of eight than one sweep of the grid (8192 blocks x 256 threads), the ragged last
+    # group (five elements) in a later sweep, fp32 input
+    n = 8192 * 256 * 8 + 8 * 1000 + 5
+    g = torch.Generator().manual_seed(12)
+    x = torch.randn(n, generator=g) * 3.0
+    codes, s, dg = run(lib, x, "e4m3", "sr", seed=0xB5F7, trial=4, use=6)
+    xf = x.numpy()
+    amax = np.float32(np.abs(xf).max())
+    assert dg["amax"] == float(amax) and dg["nonfinite"] == 0
+    sc = oq.scale_of(amax, fp8.E4M3)
+    assert s == float(sc)
+    idx = np.unique(np.concatenate([np.arange(2048), np.random.default_rng(1).integers(0, n, 100000),
+                                    np.arange(n - 4096, n)]))
+    ref, _ = oq.round_scaled(oq.scaled(xf[idx], sc), fp8.E4M3, oq.SR, 0xB5F7, 4, 6, elements=idx.astype(np.uint64))
+    assert np.array_equal(codes[idx], ref)
+
+
 @pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
 def test_sr_decision_at_the_full_word_boundary(lib, fmt):
     """Magnitudes just above zero whose rounding threshold F uses all 32 bits (the fraction of
